@@ -1,0 +1,245 @@
+"""Pins for the oracle's composed training step: the hand-written backward of
+the residual unit, attention module, full network and partition is checked
+against an independent torch-autograd build of the same graph and against
+central finite differences (float64); plus the micro-batch accumulation
+identity, the parameter counts and the conv FLOP totals."""
+import numpy as np
+import pytest
+
+from oracle import net, ops
+from paper_2104_05035_amd import synth
+
+
+def _params(kind, c_in, c, seed, **kw):
+    rng = np.random.default_rng(seed)
+    layout = net.param_layout(kind, c_in, c, **kw)
+    return synth.init_params(rng, layout, bias_std=0.1, perturb_bn=0.2), layout
+
+
+# ------------------------------------------------------- torch re-build
+def _torch_graph():
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
+
+    def bn(P, name, x):
+        return F.batch_norm(x, None, None, P[name + ".g"], P[name + ".b"], training=True,
+                            eps=1e-5)
+
+    def ru(P, pre, x, s):
+        a1 = torch.relu(bn(P, pre + "bn1", F.conv3d(x, P[pre + "conv1.w"], None, s, 1)))
+        h2 = bn(P, pre + "bn2", F.conv3d(a1, P[pre + "conv2.w"], None, 1, 1))
+        if pre + "proj.w" in P:
+            skip = bn(P, pre + "projbn", F.conv3d(x, P[pre + "proj.w"], None, s, 0))
+        else:
+            skip = x
+        return torch.relu(h2 + skip)
+
+    def am(P, pre, x):
+        T = ru(P, pre + "t2.", ru(P, pre + "t1.", x, 1), 1)
+        r1 = ru(P, pre + "m1.", F.max_pool3d(x, 3, 2, 1), 1)
+        r2 = ru(P, pre + "m3.", ru(P, pre + "m2.", F.max_pool3d(r1, 3, 2, 1), 1), 1)
+        u1 = F.interpolate(r2, size=r1.shape[2:], mode="trilinear", align_corners=False)
+        r3 = ru(P, pre + "m4.", u1, 1)
+        u2 = F.interpolate(r3, size=x.shape[2:], mode="trilinear", align_corners=False)
+        a = torch.relu(bn(P, pre + "bn", F.conv3d(u2, P[pre + "c1.w"])))
+        z = F.conv3d(a, P[pre + "c2.w"], P[pre + "c2.bias"])
+        return (1.0 + torch.sigmoid(z)) * T
+
+    def stem(P, x, pool):
+        a0 = torch.relu(bn(P, "stem.bn", F.conv3d(x, P["stem.w"], None, 2, 3)))
+        return F.max_pool3d(a0, 3, 2, 1) if pool else a0
+
+    def resattnet(P, x, labels, nst):
+        h = stem(P, x, True)
+        for i in range(nst):
+            h = ru(P, "s%d.ru." % (i + 1), h, 1 if i == 0 else 2)
+            h = am(P, "s%d.am." % (i + 1), h)
+        logits = F.linear(h.mean(dim=(2, 3, 4)), P["fc.w"], P["fc.b"])
+        return F.cross_entropy(logits, labels), logits
+
+    def partition1(P, x):
+        return am(P, "am.", ru(P, "ru.", stem(P, x, False), 1))
+
+    return torch, dict(ru=ru, am=am, resattnet=resattnet, partition1=partition1)
+
+
+def _tp(torch, params):
+    return {k: torch.tensor(v, requires_grad=True) for k, v in params.items()}
+
+
+def _cmp_grads(G, TP, rtol=1e-9):
+    for k, t in TP.items():
+        ref = t.grad.numpy()
+        err = np.linalg.norm(G[k] - ref) / max(np.linalg.norm(ref), 1e-300)
+        assert err < rtol, (k, err)
+
+
+def test_resunit_against_autograd():
+    torch, g = _torch_graph()
+    for c_in, c, proj in [(3, 3, False)]:
+        P, _ = _params("resunit", c_in, c, 1)
+        rng = np.random.default_rng(2)
+        x = rng.standard_normal((2, c_in, 5, 6, 4))
+        dy = rng.standard_normal((2, c, 5, 6, 4))
+        y, dx, G, _ = net.block_fwd_bwd("resunit", P, x, dy, bf16=False)
+        TP = _tp(torch, P)
+        xt = torch.tensor(x, requires_grad=True)
+        yt = g["ru"](TP, "", xt, 1)
+        np.testing.assert_allclose(y, yt.detach().numpy(), rtol=1e-11, atol=1e-11)
+        yt.backward(torch.tensor(dy))
+        np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-9, atol=1e-10)
+        _cmp_grads(G, TP)
+
+
+def test_attn_against_autograd():
+    torch, g = _torch_graph()
+    P, _ = _params("attn", 4, 4, 3)
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((2, 4, 8, 10, 7))
+    dy = rng.standard_normal((2, 4, 8, 10, 7))
+    y, dx, G, _ = net.block_fwd_bwd("attn", P, x, dy, bf16=False)
+    TP = _tp(torch, P)
+    xt = torch.tensor(x, requires_grad=True)
+    yt = g["am"](TP, "", xt)
+    np.testing.assert_allclose(y, yt.detach().numpy(), rtol=1e-10, atol=1e-10)
+    yt.backward(torch.tensor(dy))
+    np.testing.assert_allclose(dx, xt.grad.numpy(), rtol=1e-8, atol=1e-9)
+    _cmp_grads(G, TP, 1e-8)
+
+
+def test_resattnet_against_autograd():
+    torch, g = _torch_graph()
+    P, _ = _params("resattnet", 1, 4, 5, stages=(8, 8, 8), stem_c=4)
+    rng = np.random.default_rng(6)
+    x = rng.standard_normal((2, 1, 24, 28, 24))
+    labels = np.array([0, 1])
+    loss, logits, G, _ = net.resattnet_fwd_bwd(P, x, labels, bf16=False)
+    TP = _tp(torch, P)
+    Lt, lt = g["resattnet"](TP, torch.tensor(x), torch.tensor(labels), 3)
+    assert abs(loss - Lt.item()) < 1e-10
+    np.testing.assert_allclose(logits, lt.detach().numpy(), rtol=1e-10, atol=1e-10)
+    Lt.backward()
+    _cmp_grads(G, TP, 1e-7)
+
+
+def test_partition1_against_autograd_and_accumulation():
+    torch, g = _torch_graph()
+    P, _ = _params("partition1", 1, 8, 7, stem_c=4)
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal((2, 1, 12, 14, 12))
+    dy = rng.standard_normal((2, 8, 6, 7, 6))
+    y, G, _ = net.partition1_fwd_bwd(P, x, dy, bf16=False)
+    TP = _tp(torch, P)
+    yt = g["partition1"](TP, torch.tensor(x))
+    np.testing.assert_allclose(y, yt.detach().numpy(), rtol=1e-10, atol=1e-10)
+    yt.backward(torch.tensor(dy))
+    _cmp_grads(G, TP, 1e-8)
+    # four identical micro-batches accumulate to four times one micro-batch
+    xs, dys = np.concatenate([x] * 4), np.concatenate([dy] * 4)
+    new, G4, info = net.train_step("partition1", P, 1e-4, False, x=xs, dy=dys,
+                                   micro_batches=4)
+    for k in P:
+        np.testing.assert_allclose(G4[k], 4 * G[k], rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(new[k], P[k] - 1e-4 * G4[k], rtol=1e-15, atol=0)
+
+
+def test_resattnet_finite_differences():
+    P, layout = _params("resattnet", 1, 4, 9, stages=(6, 6, 6), stem_c=4)
+    rng = np.random.default_rng(10)
+    x = rng.standard_normal((2, 1, 20, 24, 20))
+    labels = np.array([1, 0])
+    loss, _, G, _ = net.resattnet_fwd_bwd(P, x, labels, bf16=False)
+    h = 1e-6
+    names = ["stem.w", "s1.ru.conv1.w", "s1.ru.projbn.g", "s2.am.m3.conv2.w",
+             "s2.am.c2.bias", "s3.am.t1.bn2.b", "s3.am.c1.w", "fc.w"]
+    for name in names:
+        idx = tuple(rng.integers(0, m) for m in P[name].shape)
+        Pp = {k: v.copy() for k, v in P.items()}
+        Pm = {k: v.copy() for k, v in P.items()}
+        Pp[name][idx] += h
+        Pm[name][idx] -= h
+        lp = net.resattnet_fwd_bwd(Pp, x, labels, bf16=False)[0]
+        lm = net.resattnet_fwd_bwd(Pm, x, labels, bf16=False)[0]
+        fd = (lp - lm) / (2 * h)
+        assert abs(fd - G[name][idx]) <= 1e-6 * max(1.0, abs(fd)) + 1e-8, (name, fd,
+                                                                          G[name][idx])
+
+
+def test_bf16_mode_stays_close_to_exact():
+    P, _ = _params("attn", 4, 4, 12)
+    rng = np.random.default_rng(13)
+    x = rng.standard_normal((2, 4, 8, 8, 8))
+    dy = rng.standard_normal((2, 4, 8, 8, 8))
+    y32, dx32, G32, _ = net.block_fwd_bwd("attn", P, x, dy, bf16=False)
+    xb, dyb = ops.round_bf16(x), ops.round_bf16(dy)
+    y16, dx16, G16, _ = net.block_fwd_bwd("attn", P, xb, dyb, bf16=True)
+    assert np.array_equal(y16, ops.round_bf16(y16))
+    rel = lambda a, b: np.linalg.norm(a - b) / np.linalg.norm(b)
+    # the forward stays within bfloat16 error; the input gradient of this tiny
+    # module (BN over 16 values in the deepest mask level, near-tie argmax
+    # flips) is far more sensitive, so only a loose sanity bound applies there
+    assert rel(y16, y32) < 2e-2 and rel(dx16, dx32) < 0.3
+
+
+def test_parameter_counts():
+    count = lambda L: sum(int(np.prod(s)) for _, s in L)
+    L4 = net.param_layout("resattnet", 1, 32)
+    L5 = net.param_layout("partition1", 1, 64)
+    assert sum(1 for n, s in L4 if len(s) == 5) == 52
+    assert sum(1 for n, s in L5 if len(s) == 5) == 18
+    assert count(L4) == 31594210 and count(L5) == 1516384
+
+
+def _conv_list(kind, n, c_in, c, d, h, w):
+    """(N, Ci, Co, out_spatial, k, needs_dgrad) of every conv of one pass,
+    derived from the graph layout."""
+    out = []
+
+    def ru(cin, cout, sp, s):
+        o = tuple((x + 2 - 3) // s + 1 for x in sp)
+        out.append((n, cin, cout, o, 3, True))
+        out.append((n, cout, cout, o, 3, True))
+        if cin != cout or s != 1:
+            out.append((n, cin, cout, o, 1, True))
+        return o
+
+    def am(cc, sp):
+        ru(cc, cc, sp, 1); ru(cc, cc, sp, 1)
+        p1 = tuple(ops.out_size(x, 3, 2, 1) for x in sp)
+        ru(cc, cc, p1, 1)
+        p2 = tuple(ops.out_size(x, 3, 2, 1) for x in p1)
+        ru(cc, cc, p2, 1); ru(cc, cc, p2, 1); ru(cc, cc, p1, 1)
+        out.append((n, cc, cc, sp, 1, True)); out.append((n, cc, cc, sp, 1, True))
+
+    if kind == "attn":
+        am(c, (d, h, w))
+    elif kind in ("resattnet", "partition1"):
+        sp = tuple(ops.out_size(x, 7, 2, 3) for x in (d, h, w))
+        out.append((n, 1, 32, sp, 7, False))
+        if kind == "resattnet":
+            sp = tuple(ops.out_size(x, 3, 2, 1) for x in sp)
+            cprev = 32
+            for i, cs in enumerate(net.STAGES):
+                sp = ru(cprev, cs, sp, 1 if i == 0 else 2)
+                am(cs, sp)
+                cprev = cs
+        else:
+            ru(32, c, sp, 1)
+            am(c, sp)
+    return out
+
+
+def test_conv_flop_totals():
+    def tot(kind, *a):
+        L = _conv_list(kind, *a)
+        fwd = sum(ops.conv_flops(nn, ci, co, sp, k) for nn, ci, co, sp, k, _ in L)
+        allp = sum(ops.conv_flops(nn, ci, co, sp, k) * (3 if dg else 2)
+                   for nn, ci, co, sp, k, dg in L)
+        return fwd, allp, len(L)
+    f3, a3, n3 = tot("attn", 4, 64, 64, 48, 48, 48)
+    f4, a4, n4 = tot("resattnet", 8, 1, 32, 96, 112, 96)
+    f5, a5, n5 = tot("partition1", 16, 1, 64, 96, 112, 96)
+    assert (n3, n4, n5) == (14, 52, 18)
+    assert abs(f3 / 1e9 - 453.7) < 0.1 and abs(a3 / 1e12 - 1.361) < 0.001
+    assert abs(f4 / 1e9 - 331.2) < 0.1 and abs(a4 / 1e12 - 0.971) < 0.001
+    assert abs(f5 / 1e12 - 2.856) < 0.001 and abs(a5 / 1e12 - 8.522) < 0.001
