@@ -1,0 +1,431 @@
+// Generic 3D convolution as an implicit GEMM on MFMA, any kernel size,
+// stride and padding, float32 or bfloat16 storage.
+//
+// forward:  rows = output voxels (n, o), cols = C_out, K = C_in * k^3
+//           A[m][(ci,t)] = x[n, ci, o*s - p + t]   (gathered, zero outside)
+//           B[(ci,t)][co] = w[co, ci, t]           (contiguous in K)
+// dgrad:    rows = input voxels (n, i), cols = C_in, K = C_out * k^3
+//           A[m][(co,t)] = dy[n, co, (i + p - t)/s] when divisible and in range
+//           B[(co,t)][ci] = w[co, ci, t]
+// wgrad:    rows = C_out, cols = C_in * k^3, K = output voxels (split over
+//           workgroups; partial tiles reduced in a fixed order afterwards)
+//           A[co][(n,o)] = dy[n, co, o],  B[(n,o)][(ci,t)] = x[n, ci, o*s - p + t]
+//
+// Workgroup tile 64 x 64, four waves of 32 x 32 (2 x 2 MFMA 16x16 tiles).
+// Each K step stages a 64 x BK slab of A and of B in LDS with the K index
+// innermost, so that every lane fetches its MFMA operand with one 16-byte
+// LDS read: bf16 uses v_mfma_f32_16x16x32_bf16 (8 K values per lane),
+// float32 uses four v_mfma_f32_16x16x4_f32 (4 K values per lane).
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace rat3d {
+
+template <typename T> struct MfmaCfg;
+template <> struct MfmaCfg<bf16> { static constexpr int KV = 8, BK = 32; };
+template <> struct MfmaCfg<float> { static constexpr int KV = 4, BK = 16; };
+
+union Frag16 {
+    uint4 u;
+    bf16x8 b;
+    float f[4];
+    bf16 h[8];
+};
+
+template <typename T> __device__ __forceinline__ void mma16(f32x4& acc, const Frag16& a,
+                                                            const Frag16& b);
+template <> __device__ __forceinline__ void mma16<bf16>(f32x4& acc, const Frag16& a,
+                                                        const Frag16& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.b, b.b, acc, 0, 0, 0);
+}
+template <> __device__ __forceinline__ void mma16<float>(f32x4& acc, const Frag16& a,
+                                                         const Frag16& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.f[0], b.f[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.f[1], b.f[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.f[2], b.f[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.f[3], b.f[3], acc, 0, 0, 0);
+}
+
+constexpr int kRow = 80;  // LDS bytes per staged row: 64 bytes of K values + 16 pad
+
+template <typename T>
+__device__ __forceinline__ void store_frag(unsigned char* lds, const T (&v)[16 / sizeof(T)]) {
+    Frag16 f;
+#pragma unroll
+    for (int j = 0; j < (int)(16 / sizeof(T)); ++j) {
+        if constexpr (sizeof(T) == 2) f.h[j] = (bf16)v[j];
+        else f.f[j] = (float)v[j];
+    }
+    *reinterpret_cast<uint4*>(lds) = f.u;
+}
+
+// One K step of the 64x64 tile: each wave multiplies its 32x32 quarter.
+template <typename T>
+__device__ __forceinline__ void tile_mma(const unsigned char* As, const unsigned char* Bs,
+                                         f32x4 (&acc)[2][2], int lane, int wm, int wn) {
+    Frag16 a[2], b[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        a[i].u = *reinterpret_cast<const uint4*>(As + (wm * 32 + i * 16 + (lane & 15)) * kRow +
+                                                 (lane >> 4) * 16);
+        b[i].u = *reinterpret_cast<const uint4*>(Bs + (wn * 32 + i * 16 + (lane & 15)) * kRow +
+                                                 (lane >> 4) * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) mma16<T>(acc[i][j], a[i], b[j]);
+}
+
+// ---------------------------------------------------------------- fwd / dgrad
+template <typename T, bool DGRAD>
+__global__ __launch_bounds__(256) void conv_gather_fd(ConvGeom g, const T* __restrict__ src,
+                                                      const T* __restrict__ wt,
+                                                      const float* __restrict__ bias,
+                                                      T* __restrict__ dst, int accumulate) {
+    constexpr int KV = MfmaCfg<T>::KV, BK = MfmaCfg<T>::BK;
+    __shared__ __align__(16) unsigned char As[64 * kRow];
+    __shared__ __align__(16) unsigned char Bs[64 * kRow];
+    __shared__ int4 ktab[BK];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    // GEMM rows are voxels of the destination tensor.
+    const int RD = DGRAD ? g.D : g.Do, RH = DGRAD ? g.H : g.Ho, RW = DGRAD ? g.W : g.Wo;
+    const int64_t Vrow = (int64_t)RD * RH * RW;
+    const int64_t M = (int64_t)g.N * Vrow;
+    const int Ncol = DGRAD ? g.Ci : g.Co;
+    const int Csrc = DGRAD ? g.Co : g.Ci;
+    const int SD = DGRAD ? g.Do : g.D, SH = DGRAD ? g.Ho : g.H, SW = DGRAD ? g.Wo : g.W;
+    const int64_t Vsrc = (int64_t)SD * SH * SW;
+    const int KT = g.k * g.k * g.k;
+    const int K = Csrc * KT;
+    const int64_t m0 = (int64_t)blockIdx.x * 64;
+    const int c0 = blockIdx.y * 64;
+
+    const int ar = tid >> 2, aq = tid & 3;
+    const int64_t am = m0 + ar;
+    const bool arow_ok = am < M;
+    int a_d = 0, a_h = 0, a_w = 0;
+    int64_t a_base = 0;
+    if (arow_ok) {
+        const int64_t n = am / Vrow;
+        int64_t sp = am - n * Vrow;
+        a_d = (int)(sp / ((int64_t)RH * RW));
+        sp -= (int64_t)a_d * RH * RW;
+        a_h = (int)(sp / RW);
+        a_w = (int)(sp - (int64_t)a_h * RW);
+        a_base = n * Csrc * Vsrc;
+    }
+    const int bcol = c0 + (tid >> 2), bq = tid & 3;
+
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int k0 = 0; k0 < K; k0 += BK) {
+        if (tid < BK) {
+            const int k = k0 + tid;
+            int4 e = make_int4(-1, 0, 0, 0);
+            if (k < K) {
+                const int c = k / KT;
+                const int t = k - c * KT;
+                const int kd = t / (g.k * g.k);
+                const int r = t - kd * g.k * g.k;
+                const int kh = r / g.k;
+                e = make_int4(c, kd, kh, r - kh * g.k);
+            }
+            ktab[tid] = e;
+        }
+        __syncthreads();
+        {
+            T v[KV];
+#pragma unroll
+            for (int j = 0; j < KV; ++j) {
+                const int4 e = ktab[aq * KV + j];
+                T val = Elt<T>::to_bits(0.f);
+                if (arow_ok && e.x >= 0) {
+                    if constexpr (!DGRAD) {
+                        const int id = a_d * g.s - g.p + e.y, ih = a_h * g.s - g.p + e.z,
+                                  iw = a_w * g.s - g.p + e.w;
+                        if ((unsigned)id < (unsigned)g.D && (unsigned)ih < (unsigned)g.H &&
+                            (unsigned)iw < (unsigned)g.W)
+                            val = src[a_base + e.x * Vsrc + ((int64_t)id * g.H + ih) * g.W + iw];
+                    } else {
+                        const int nd = a_d + g.p - e.y, nh = a_h + g.p - e.z,
+                                  nw = a_w + g.p - e.w;
+                        if (nd >= 0 && nh >= 0 && nw >= 0 && nd % g.s == 0 && nh % g.s == 0 &&
+                            nw % g.s == 0) {
+                            const int od = nd / g.s, oh = nh / g.s, ow = nw / g.s;
+                            if (od < g.Do && oh < g.Ho && ow < g.Wo)
+                                val = src[a_base + e.x * Vsrc + ((int64_t)od * g.Ho + oh) * g.Wo +
+                                          ow];
+                        }
+                    }
+                }
+                v[j] = val;
+            }
+            store_frag<T>(As + ar * kRow + aq * 16, v);
+        }
+        {
+            T v[KV];
+#pragma unroll
+            for (int j = 0; j < KV; ++j) {
+                const int k = k0 + bq * KV + j;
+                T val = Elt<T>::to_bits(0.f);
+                if (bcol < Ncol && k < K) {
+                    if constexpr (!DGRAD) {
+                        val = wt[(int64_t)bcol * K + k];
+                    } else {
+                        const int co = ktab[bq * KV + j].x;
+                        val = wt[((int64_t)co * g.Ci + bcol) * KT + (k - co * KT)];
+                    }
+                }
+                v[j] = val;
+            }
+            store_frag<T>(Bs + (tid >> 2) * kRow + bq * 16, v);
+        }
+        __syncthreads();
+        tile_mma<T>(As, Bs, acc, lane, wm, wn);
+    }
+
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int row = wm * 32 + i * 16 + 4 * (lane >> 4) + e;
+                const int col = wn * 32 + j * 16 + (lane & 15);
+                const int64_t m = m0 + row;
+                const int c = c0 + col;
+                if (m < M && c < Ncol) {
+                    const int64_t n = m / Vrow, sp = m - n * Vrow;
+                    const int64_t off = (n * Ncol + c) * Vrow + sp;
+                    float v = acc[i][j][e];
+                    if (bias) v += bias[c];
+                    if (accumulate) v += Elt<T>::ld(dst + off);
+                    Elt<T>::st(dst + off, v);
+                }
+            }
+}
+
+// ---------------------------------------------------------------- wgrad
+template <typename T>
+__global__ __launch_bounds__(256) void conv_gather_wgrad(ConvGeom g, const T* __restrict__ x,
+                                                         const T* __restrict__ dy,
+                                                         float* __restrict__ part,
+                                                         int64_t kchunk) {
+    constexpr int KV = MfmaCfg<T>::KV, BK = MfmaCfg<T>::BK;
+    __shared__ __align__(16) unsigned char As[64 * kRow];
+    __shared__ __align__(16) unsigned char Bs[64 * kRow];
+    __shared__ int4 vtab[BK];    // (n or -1, od*s-p, oh*s-p, ow*s-p)
+    __shared__ int64_t vdy[BK];  // n*Co*Vo + o
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    const int KT = g.k * g.k * g.k;
+    const int Ncols = g.Ci * KT;
+    const int64_t Vo = (int64_t)g.Do * g.Ho * g.Wo, Vi = (int64_t)g.D * g.H * g.W;
+    const int64_t Ktot = (int64_t)g.N * Vo;
+    const int64_t kbeg = (int64_t)blockIdx.z * kchunk;
+    const int64_t kend = kbeg + kchunk < Ktot ? kbeg + kchunk : Ktot;
+    const int co0 = blockIdx.x * 64, col0 = blockIdx.y * 64;
+
+    const int aco = co0 + (tid >> 2), aq = tid & 3;
+    const int bcol = col0 + (tid >> 2), bq = tid & 3;
+    int b_ci = 0, b_kd = 0, b_kh = 0, b_kw = 0;
+    const bool bcol_ok = bcol < Ncols;
+    if (bcol_ok) {
+        b_ci = bcol / KT;
+        const int t = bcol - b_ci * KT;
+        b_kd = t / (g.k * g.k);
+        const int r = t - b_kd * g.k * g.k;
+        b_kh = r / g.k;
+        b_kw = r - b_kh * g.k;
+    }
+
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int64_t v0 = kbeg; v0 < kend; v0 += BK) {
+        if (tid < BK) {
+            const int64_t v = v0 + tid;
+            int4 e = make_int4(-1, 0, 0, 0);
+            int64_t off = 0;
+            if (v < kend) {
+                const int64_t n = v / Vo;
+                int64_t o = v - n * Vo;
+                const int od = (int)(o / ((int64_t)g.Ho * g.Wo));
+                const int64_t r = o - (int64_t)od * g.Ho * g.Wo;
+                const int oh = (int)(r / g.Wo), ow = (int)(r - (int64_t)oh * g.Wo);
+                e = make_int4((int)n, od * g.s - g.p, oh * g.s - g.p, ow * g.s - g.p);
+                off = n * g.Co * Vo + o;
+            }
+            vtab[tid] = e;
+            vdy[tid] = off;
+        }
+        __syncthreads();
+        {
+            T v[KV];
+#pragma unroll
+            for (int j = 0; j < KV; ++j) {
+                T val = Elt<T>::to_bits(0.f);
+                if (aco < g.Co && vtab[aq * KV + j].x >= 0)
+                    val = dy[vdy[aq * KV + j] + (int64_t)aco * Vo];
+                v[j] = val;
+            }
+            store_frag<T>(As + (tid >> 2) * kRow + aq * 16, v);
+        }
+        {
+            T v[KV];
+#pragma unroll
+            for (int j = 0; j < KV; ++j) {
+                T val = Elt<T>::to_bits(0.f);
+                const int4 e = vtab[bq * KV + j];
+                if (bcol_ok && e.x >= 0) {
+                    const int id = e.y + b_kd, ih = e.z + b_kh, iw = e.w + b_kw;
+                    if ((unsigned)id < (unsigned)g.D && (unsigned)ih < (unsigned)g.H &&
+                        (unsigned)iw < (unsigned)g.W)
+                        val = x[((int64_t)e.x * g.Ci + b_ci) * Vi + ((int64_t)id * g.H + ih) * g.W +
+                                iw];
+                }
+                v[j] = val;
+            }
+            store_frag<T>(Bs + (tid >> 2) * kRow + bq * 16, v);
+        }
+        __syncthreads();
+        tile_mma<T>(As, Bs, acc, lane, wm, wn);
+    }
+
+    float* out = part + (int64_t)blockIdx.z * g.Co * Ncols;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int co = co0 + wm * 32 + i * 16 + 4 * (lane >> 4) + e;
+                const int col = col0 + wn * 32 + j * 16 + (lane & 15);
+                if (co < g.Co && col < Ncols) out[(int64_t)co * Ncols + col] = acc[i][j][e];
+            }
+}
+
+// Sums `splits` partial weight-gradient tiles in split order into dw.
+__global__ void wgrad_reduce(const float* __restrict__ part, int splits, int64_t count,
+                             float* __restrict__ dw, int accumulate) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= count) return;
+    float s = accumulate ? dw[i] : 0.f;
+    for (int z = 0; z < splits; ++z) s += part[(int64_t)z * count + i];
+    dw[i] = s;
+}
+
+// dbias[c] (+)= sum over n and voxels of dy[n, c, :].  One block per channel;
+// fixed-shape tree reduction.
+template <typename T>
+__global__ __launch_bounds__(256) void bias_grad(const T* __restrict__ dy, int N, int C,
+                                                 int64_t V, float* __restrict__ db,
+                                                 int accumulate) {
+    __shared__ float red[256];
+    const int c = blockIdx.x;
+    float s = 0.f;
+    for (int n = 0; n < N; ++n) {
+        const T* p = dy + ((int64_t)n * C + c) * V;
+        for (int64_t i = threadIdx.x; i < V; i += 256) s += Elt<T>::ld(p + i);
+    }
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) db[c] = (accumulate ? db[c] : 0.f) + red[0];
+}
+
+// ---------------------------------------------------------------- launchers
+int wgrad_gather_splits(const ConvGeom& g) {
+    const int64_t Ktot = (int64_t)g.N * g.Do * g.Ho * g.Wo;
+    const int64_t tiles = ceil_div(g.Co, 64) * ceil_div((int64_t)g.Ci * g.k * g.k * g.k, 64);
+    int64_t splits = ceil_div(2048, tiles);
+    const int64_t max_splits = ceil_div(Ktot, 256);  // at least 256 voxels per split
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    if (splits > 4096) splits = 4096;
+    return (int)splits;
+}
+
+size_t wgrad_gather_ws(const ConvGeom& g) {
+    return (size_t)wgrad_gather_splits(g) * g.Co * g.Ci * g.k * g.k * g.k * sizeof(float);
+}
+
+template <typename T>
+static rat3d_status gather_fd(const ConvGeom& g, bool dgrad, const void* src, const void* w,
+                              const float* bias, void* dst, int accumulate, hipStream_t st) {
+    const int64_t rows = (int64_t)g.N * (dgrad ? (int64_t)g.D * g.H * g.W
+                                               : (int64_t)g.Do * g.Ho * g.Wo);
+    const int cols = dgrad ? g.Ci : g.Co;
+    dim3 grid((unsigned)ceil_div(rows, 64), (unsigned)ceil_div(cols, 64));
+    if (dgrad)
+        conv_gather_fd<T, true><<<grid, 256, 0, st>>>(g, (const T*)src, (const T*)w, nullptr,
+                                                      (T*)dst, accumulate);
+    else
+        conv_gather_fd<T, false><<<grid, 256, 0, st>>>(g, (const T*)src, (const T*)w, bias,
+                                                       (T*)dst, accumulate);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
+rat3d_status conv_fwd_gather(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* w,
+                             const float* bias, void* y, hipStream_t st) {
+    return dt == RAT3D_BF16 ? gather_fd<bf16>(g, false, x, w, bias, y, 0, st)
+                            : gather_fd<float>(g, false, x, w, bias, y, 0, st);
+}
+
+rat3d_status conv_dgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* dy, const void* w,
+                               void* dx, int accumulate, hipStream_t st) {
+    return dt == RAT3D_BF16 ? gather_fd<bf16>(g, true, dy, w, nullptr, dx, accumulate, st)
+                            : gather_fd<float>(g, true, dy, w, nullptr, dx, accumulate, st);
+}
+
+rat3d_status conv_wgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* dy,
+                               float* dw, int accumulate, void* ws, hipStream_t st) {
+    const int splits = wgrad_gather_splits(g);
+    const int64_t Ktot = (int64_t)g.N * g.Do * g.Ho * g.Wo;
+    const int BK = dt == RAT3D_BF16 ? 32 : 16;
+    const int64_t kchunk = ceil_div(ceil_div(Ktot, splits), BK) * BK;
+    const int real_splits = (int)ceil_div(Ktot, kchunk);
+    const int Ncols = g.Ci * g.k * g.k * g.k;
+    dim3 grid((unsigned)ceil_div(g.Co, 64), (unsigned)ceil_div(Ncols, 64), (unsigned)real_splits);
+    float* part = (float*)ws;
+    if (dt == RAT3D_BF16)
+        conv_gather_wgrad<bf16><<<grid, 256, 0, st>>>(g, (const bf16*)x, (const bf16*)dy, part,
+                                                      kchunk);
+    else
+        conv_gather_wgrad<float><<<grid, 256, 0, st>>>(g, (const float*)x, (const float*)dy,
+                                                       part, kchunk);
+    RAT3D_LAUNCH_CHECK();
+    const int64_t count = (int64_t)g.Co * Ncols;
+    wgrad_reduce<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(part, real_splits, count, dw,
+                                                                 accumulate);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
+rat3d_status conv_bias_grad(const ConvGeom& g, rat3d_dtype dt, const void* dy, float* db,
+                            int accumulate, hipStream_t st) {
+    const int64_t Vo = (int64_t)g.Do * g.Ho * g.Wo;
+    if (dt == RAT3D_BF16)
+        bias_grad<bf16><<<g.Co, 256, 0, st>>>((const bf16*)dy, g.N, g.Co, Vo, db, accumulate);
+    else
+        bias_grad<float><<<g.Co, 256, 0, st>>>((const float*)dy, g.N, g.Co, Vo, db, accumulate);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
+}  // namespace rat3d

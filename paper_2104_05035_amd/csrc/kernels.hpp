@@ -1,0 +1,94 @@
+// Host-side launchers of the librat3d kernels.  Every launcher enqueues on the
+// given stream, checks the launch and returns a rat3d_status; shapes have been
+// validated by the caller.
+#pragma once
+
+#include "common.hpp"
+
+namespace rat3d {
+
+// Geometry of one convolution (input N x Ci x D x H x W, cubic kernel k).
+struct ConvGeom {
+    int N, Ci, Co, D, H, W, k, s, p;
+    int Do, Ho, Wo;
+};
+
+inline ConvGeom make_geom(int N, int Ci, int Co, int D, int H, int W, int k, int s, int p) {
+    ConvGeom g{N, Ci, Co, D, H, W, k, s, p, 0, 0, 0};
+    g.Do = out_dim(D, k, s, p);
+    g.Ho = out_dim(H, k, s, p);
+    g.Wo = out_dim(W, k, s, p);
+    return g;
+}
+
+// ---- convolution: dispatch (conv.cpp) ----------------------------------
+// Workspace bytes of a pass (0 fwd, 1 dgrad, 2 wgrad).
+size_t conv_ws_bytes(const ConvGeom& g, rat3d_dtype dt, int pass);
+// Public-layout entry points: w is [Co][Ci][k^3] in dtype dt.
+rat3d_status conv_fwd(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* w,
+                      const float* bias, void* y, void* ws, size_t ws_bytes, hipStream_t st);
+rat3d_status conv_dgrad(const ConvGeom& g, rat3d_dtype dt, const void* dy, const void* w,
+                        void* dx, int accumulate, void* ws, size_t ws_bytes, hipStream_t st);
+rat3d_status conv_wgrad(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* dy,
+                        float* dw, float* db, int accumulate, void* ws, size_t ws_bytes,
+                        hipStream_t st);
+
+// ---- generic gather implicit GEMM (conv_gather.hip) --------------------
+rat3d_status conv_fwd_gather(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* w,
+                             const float* bias, void* y, hipStream_t st);
+rat3d_status conv_dgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* dy, const void* w,
+                               void* dx, int accumulate, hipStream_t st);
+size_t wgrad_gather_ws(const ConvGeom& g);
+rat3d_status conv_wgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* dy,
+                               float* dw, int accumulate, void* ws, hipStream_t st);
+rat3d_status conv_bias_grad(const ConvGeom& g, rat3d_dtype dt, const void* dy, float* db,
+                            int accumulate, hipStream_t st);
+
+// ---- batch norm (bn.hip) -----------------------------------------------
+struct BnGeom {
+    int N, C;
+    int64_t V;  // voxels per (n, c) plane
+};
+size_t bn_ws_bytes(const BnGeom& g);
+rat3d_status bn_fwd(const BnGeom& g, rat3d_dtype dt, int relu, float eps, float momentum,
+                    const void* x, const void* residual, const float* gamma, const float* beta,
+                    void* y, float* save_mean, float* save_invstd, float* run_mean,
+                    float* run_var, void* ws, hipStream_t st);
+rat3d_status bn_bwd(const BnGeom& g, rat3d_dtype dt, int relu, const void* dy, const void* x,
+                    const void* y, const float* gamma, const float* save_mean,
+                    const float* save_invstd, void* dx, void* dres, float* dgamma,
+                    float* dbeta, int accumulate, void* ws, hipStream_t st);
+
+// ---- soft-mask branch (softmask.hip) -----------------------------------
+rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, rat3d_dtype dt,
+                      const void* x, void* y, uint8_t* argmax, hipStream_t st);
+rat3d_status pool_bwd(int N, int C, int D, int H, int W, int k, int s, int p, rat3d_dtype dt,
+                      const void* dy, const uint8_t* argmax, void* dx, int accumulate,
+                      hipStream_t st);
+rat3d_status up_fwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo,
+                    rat3d_dtype dt, const void* x, void* y, hipStream_t st);
+rat3d_status up_bwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo,
+                    rat3d_dtype dt, const void* dy, void* dx, int accumulate, hipStream_t st);
+rat3d_status softmask_fwd(int64_t count, rat3d_dtype dt, const void* z, const void* t,
+                          void* out, void* m, hipStream_t st);
+rat3d_status softmask_bwd(int64_t count, rat3d_dtype dt, const void* dout, const void* t,
+                          const void* m, void* dt_out, int accumulate_dt, void* dz,
+                          hipStream_t st);
+
+// ---- head, update, casts (head.hip) ------------------------------------
+size_t head_ws_bytes(int N, int C, int classes);
+rat3d_status head_fwd_bwd(int N, int C, int64_t V, int classes, rat3d_dtype dt, const void* x,
+                          const float* fc_w, const float* fc_b, const int32_t* labels,
+                          float* logits, float* loss, void* dx, float* dfc_w, float* dfc_b,
+                          int accumulate, void* ws, hipStream_t st);
+rat3d_status sgd_update(int64_t count, float lr, float* params, const float* grads,
+                        hipStream_t st);
+// dst[i] = bf16(src[i]) for i < count.
+rat3d_status cast_f32_bf16(int64_t count, const float* src, bf16* dst, hipStream_t st);
+// dst[i] = value.
+rat3d_status fill_f32(int64_t count, float value, float* dst, hipStream_t st);
+// dst[i] (+)= a[i] + b[i] in dtype (one rounding).
+rat3d_status add_tensors(int64_t count, rat3d_dtype dt, const void* a, const void* b, void* dst,
+                         hipStream_t st);
+
+}  // namespace rat3d

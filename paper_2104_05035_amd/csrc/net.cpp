@@ -1,0 +1,715 @@
+// Composite blocks and the training step: a host-side plan (parameter arena
+// and workspace layout) plus an executor that enqueues the kernels of the
+// forward pass, the backward pass and the SGD update on one stream.
+//
+// Graph readings (the paper names conv blocks, residual layers and a
+// self-attention layer but leaves their wiring open):
+//   residual unit   conv3(s) -> BN -> ReLU -> conv3 -> BN, + skip, ReLU; the
+//                   skip is a 1^3 conv (stride s) + BN when channels or
+//                   stride change;
+//   attention       trunk = RU -> RU; mask = maxpool -> RU -> maxpool -> RU ->
+//                   RU -> up -> RU -> up -> 1^3 conv -> BN -> ReLU -> 1^3 conv
+//                   (+bias) -> sigmoid; out = (1 + M) * T;
+//   stem            7^3 conv stride 2 pad 3 -> BN -> ReLU (-> maxpool);
+//   full network    stem+pool, stages of 64/128/256 channels (RU with stride
+//                   1/2/2, then attention), global average pool, FC, CE.
+// Store points: every activation and activation gradient is stored in the
+// network dtype.  Where a tensor feeds several consumers its gradient is
+// formed in a fixed order: in a residual unit the skip-branch gradient is
+// stored first (added to any gradient already there), then the conv1 input
+// gradient is accumulated onto it; in an attention module the mask branch's
+// input gradient is stored first and the trunk's is accumulated onto it.
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+
+using namespace rat3d;
+
+namespace {
+
+constexpr int64_t kExtX = -1, kExtY = -2, kExtDx = -3, kExtDy = -4, kNone = -100;
+
+struct Shape {
+    int n, c, d, h, w;
+    int64_t vox() const { return (int64_t)d * h * w; }
+    int64_t count() const { return (int64_t)n * c * d * h * w; }
+};
+
+struct TRef {  // activation and its gradient: ws byte offsets or external slots
+    int64_t off = kNone, goff = kNone;
+    Shape s{};
+};
+
+struct ConvL {
+    ConvGeom g{};
+    size_t w_off = 0, b_off = 0;  // parameter-arena offsets (elements)
+    bool bias = false;
+};
+
+struct BnL {
+    int c = 0;
+    size_t g_off = 0, b_off = 0;  // arena offsets of gamma, beta
+    int64_t stat_off = 0;         // ws bytes: mean [c], invstd [c]
+    size_t run_idx = 0;           // index into the running-statistics regions
+};
+
+struct RUPlan {
+    ConvL c1, c2, cp;
+    BnL b1, b2, bp;
+    bool proj = false;
+    TRef x, h1, a1, h2, hp, sp, y;
+    int64_t dskip = kNone;  // ws offset of the skip-branch gradient
+};
+
+struct AMPlan {
+    RUPlan t1, t2, m1, m2, m3, m4;
+    ConvL c1, c2;
+    BnL bn;
+    TRef x, p1, p2, u1, u2, h1, a, z, out, m;
+    int64_t am1 = 0, am2 = 0;  // argmax byte offsets
+};
+
+struct ParamRec {
+    std::string name;
+    size_t off;
+    int ndim;
+    int shape[5];
+};
+
+struct TensorRec {
+    std::string name;
+    size_t off;
+    rat3d_dtype dt;
+    int shape[5];
+};
+
+}  // namespace
+
+struct rat3d_net {
+    rat3d_net_desc d{};
+    rat3d_dtype dt = RAT3D_BF16;
+    size_t esz = 2;
+    std::vector<ParamRec> params;
+    std::vector<TensorRec> tensors;
+    size_t param_count = 0, ws_bytes = 0;
+    // layout
+    size_t mirror_off = 0, conv_scr_off = 0, conv_scr_bytes = 0, bn_scr_off = 0,
+           bn_scr_bytes = 0, head_scr_off = 0, run_mean_off = 0, run_var_off = 0,
+           logits_off = 0, loss_off = 0;
+    size_t run_count = 0;
+    // plan
+    TRef stem_h, stem_a, stem_p;
+    ConvL stem_conv;
+    BnL stem_bn;
+    int64_t stem_am = 0;
+    std::vector<RUPlan> rus;   // RESATTNET: 3 stage units; PARTITION1: 1; RESUNIT: 1
+    std::vector<AMPlan> ams;   // RESATTNET: 3; PARTITION1 / ATTN: 1
+    ConvL fc;                  // only offsets used (FC weight [2][C], bias [2])
+    int fc_c = 0;
+    // binding
+    float* P = nullptr;
+    float* G = nullptr;
+    char* ws = nullptr;
+    bool reset_running = false;
+    // external pointers of the current call
+    const void* ext_x = nullptr;
+    void* ext_y = nullptr;
+    void* ext_dx = nullptr;
+    const void* ext_dy = nullptr;
+};
+
+namespace {
+
+// ------------------------------------------------------------------ builder
+struct Builder {
+    rat3d_net* net;
+    size_t top = 0;
+
+    size_t alloc(size_t bytes) {
+        top = (top + 255) & ~(size_t)255;
+        const size_t off = top;
+        top += bytes;
+        return off;
+    }
+    void record(const std::string& name, size_t off, rat3d_dtype dt, Shape s) {
+        net->tensors.push_back(TensorRec{name, off, dt, {s.n, s.c, s.d, s.h, s.w}});
+    }
+    size_t param(const std::string& name, std::initializer_list<int> shape) {
+        ParamRec r;
+        r.name = name;
+        r.off = net->param_count;
+        r.ndim = (int)shape.size();
+        size_t cnt = 1;
+        int i = 0;
+        for (int v : shape) {
+            r.shape[i++] = v;
+            cnt *= (size_t)v;
+        }
+        for (; i < 5; ++i) r.shape[i] = 1;
+        net->params.push_back(r);
+        net->param_count += cnt;
+        return r.off;
+    }
+    TRef act(const std::string& name, Shape s, bool grad = true) {
+        TRef t;
+        t.s = s;
+        t.off = (int64_t)alloc((size_t)s.count() * net->esz);
+        record(name, (size_t)t.off, net->dt, s);
+        if (grad) {
+            t.goff = (int64_t)alloc((size_t)s.count() * net->esz);
+            record("d:" + name, (size_t)t.goff, net->dt, s);
+        }
+        return t;
+    }
+    ConvL conv(const std::string& name, int ci, int co, int k, int s, int p, bool bias,
+               Shape in) {
+        ConvL c;
+        c.g = make_geom(in.n, ci, co, in.d, in.h, in.w, k, s, p);
+        c.w_off = param(name + ".w", {co, ci, k, k, k});
+        c.bias = bias;
+        if (bias) c.b_off = param(name + ".bias", {co});
+        size_t need = 0;
+        for (int pass = 0; pass < 3; ++pass) {
+            const size_t b = conv_ws_bytes(c.g, net->dt, pass);
+            if (b > need) need = b;
+        }
+        if (need > net->conv_scr_bytes) net->conv_scr_bytes = need;
+        return c;
+    }
+    BnL bn(const std::string& name, int c, Shape s) {
+        BnL b;
+        b.c = c;
+        b.g_off = param(name + ".g", {c});
+        b.b_off = param(name + ".b", {c});
+        b.stat_off = (int64_t)alloc((size_t)2 * c * sizeof(float));
+        record(name + ".mean", (size_t)b.stat_off, RAT3D_F32, Shape{1, c, 1, 1, 1});
+        record(name + ".invstd", (size_t)b.stat_off + c * sizeof(float), RAT3D_F32,
+               Shape{1, c, 1, 1, 1});
+        b.run_idx = net->run_count;
+        net->run_count += (size_t)c;
+        const size_t need = bn_ws_bytes(BnGeom{s.n, c, s.vox()});
+        if (need > net->bn_scr_bytes) net->bn_scr_bytes = need;
+        return b;
+    }
+
+    RUPlan ru(const std::string& pre, TRef x, int cout, int stride) {
+        RUPlan r;
+        const int cin = x.s.c;
+        r.proj = cin != cout || stride != 1;
+        r.x = x;
+        r.c1 = conv(pre + "conv1", cin, cout, 3, stride, 1, false, x.s);
+        const Shape o{x.s.n, cout, r.c1.g.Do, r.c1.g.Ho, r.c1.g.Wo};
+        r.b1 = bn(pre + "bn1", cout, o);
+        r.c2 = conv(pre + "conv2", cout, cout, 3, 1, 1, false, o);
+        r.b2 = bn(pre + "bn2", cout, o);
+        if (r.proj) {
+            r.cp = conv(pre + "proj", cin, cout, 1, stride, 0, false, x.s);
+            r.bp = bn(pre + "projbn", cout, o);
+        }
+        r.h1 = act(pre + "h1", o);
+        r.a1 = act(pre + "a1", o);
+        r.h2 = act(pre + "h2", o);
+        if (r.proj) {
+            r.hp = act(pre + "hp", o);
+            r.sp = act(pre + "sp", o, false);
+        }
+        r.y = act(pre + "y", o);
+        r.dskip = (int64_t)alloc((size_t)o.count() * net->esz);
+        record("d:" + pre + "skip", (size_t)r.dskip, net->dt, o);
+        return r;
+    }
+
+    AMPlan am(const std::string& pre, TRef x) {
+        AMPlan a;
+        const int c = x.s.c;
+        a.x = x;
+        a.t1 = ru(pre + "t1.", x, c, 1);
+        a.t2 = ru(pre + "t2.", a.t1.y, c, 1);
+        const Shape s1{x.s.n, c, out_dim(x.s.d, 3, 2, 1), out_dim(x.s.h, 3, 2, 1),
+                       out_dim(x.s.w, 3, 2, 1)};
+        a.p1 = act(pre + "p1", s1);
+        a.am1 = (int64_t)alloc((size_t)s1.count());
+        record(pre + "p1.argmax", (size_t)a.am1, RAT3D_U8, s1);
+        a.m1 = ru(pre + "m1.", a.p1, c, 1);
+        const Shape s2{x.s.n, c, out_dim(s1.d, 3, 2, 1), out_dim(s1.h, 3, 2, 1),
+                       out_dim(s1.w, 3, 2, 1)};
+        a.p2 = act(pre + "p2", s2);
+        a.am2 = (int64_t)alloc((size_t)s2.count());
+        record(pre + "p2.argmax", (size_t)a.am2, RAT3D_U8, s2);
+        a.m2 = ru(pre + "m2.", a.p2, c, 1);
+        a.m3 = ru(pre + "m3.", a.m2.y, c, 1);
+        a.u1 = act(pre + "u1", s1);
+        a.m4 = ru(pre + "m4.", a.u1, c, 1);
+        a.u2 = act(pre + "u2", x.s);
+        a.c1 = conv(pre + "c1", c, c, 1, 1, 0, false, x.s);
+        a.bn = bn(pre + "bn", c, x.s);
+        a.c2 = conv(pre + "c2", c, c, 1, 1, 0, true, x.s);
+        a.h1 = act(pre + "c1out", x.s);
+        a.a = act(pre + "a", x.s);
+        a.z = act(pre + "z", x.s);
+        a.m = act(pre + "m", x.s, false);
+        a.out = act(pre + "out", x.s);
+        return a;
+    }
+};
+
+// ------------------------------------------------------------------ executor
+struct Exec {
+    rat3d_net* n;
+    hipStream_t st;
+    int acc;  // accumulate parameter gradients (micro-batches after the first)
+
+    void* p(int64_t off) const {
+        switch (off) {
+            case kExtX: return const_cast<void*>(n->ext_x);
+            case kExtY: return n->ext_y;
+            case kExtDx: return n->ext_dx;
+            case kExtDy: return const_cast<void*>(n->ext_dy);
+            default: return n->ws + off;
+        }
+    }
+    void* a(const TRef& t) const { return p(t.off); }
+    void* g(const TRef& t) const { return p(t.goff); }
+    const void* w(const ConvL& c) const {
+        if (n->dt == RAT3D_BF16) return n->ws + n->mirror_off + c.w_off * 2;
+        return n->P + c.w_off;
+    }
+    float* par(size_t off) const { return n->P + off; }
+    float* grd(size_t off) const { return n->G + off; }
+    void* conv_scr() const { return n->ws + n->conv_scr_off; }
+    void* bn_scr() const { return n->ws + n->bn_scr_off; }
+    float* mean(const BnL& b) const { return (float*)(n->ws + b.stat_off); }
+    float* invstd(const BnL& b) const { return (float*)(n->ws + b.stat_off) + b.c; }
+    float* rmean(const BnL& b) const { return (float*)(n->ws + n->run_mean_off) + b.run_idx; }
+    float* rvar(const BnL& b) const { return (float*)(n->ws + n->run_var_off) + b.run_idx; }
+
+    rat3d_status conv_f(const ConvL& c, const void* x, void* y) const {
+        return conv_fwd(c.g, n->dt, x, w(c), c.bias ? par(c.b_off) : nullptr, y, conv_scr(),
+                        n->conv_scr_bytes, st);
+    }
+    rat3d_status conv_d(const ConvL& c, const void* dy, void* dx, int accumulate) const {
+        return conv_dgrad(c.g, n->dt, dy, w(c), dx, accumulate, conv_scr(), n->conv_scr_bytes,
+                          st);
+    }
+    rat3d_status conv_w(const ConvL& c, const void* x, const void* dy) const {
+        return conv_wgrad(c.g, n->dt, x, dy, grd(c.w_off), c.bias ? grd(c.b_off) : nullptr, acc,
+                          conv_scr(), n->conv_scr_bytes, st);
+    }
+    rat3d_status bn_f(const BnL& b, const TRef& x, const void* res, int relu, void* y) const {
+        return bn_fwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, relu, n->d.bn_eps, n->d.bn_momentum,
+                      a(x), res, par(b.g_off), par(b.b_off), y, mean(b), invstd(b), rmean(b),
+                      rvar(b), bn_scr(), st);
+    }
+    rat3d_status bn_b(const BnL& b, const void* dy, const TRef& x, const void* y, int relu,
+                      void* dx, void* dres) const {
+        return bn_bwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, relu, dy, a(x), y, par(b.g_off),
+                      mean(b), invstd(b), dx, dres, grd(b.g_off), grd(b.b_off), acc, bn_scr(),
+                      st);
+    }
+};
+
+#define RAT3D_TRY(expr)                       \
+    do {                                      \
+        rat3d_status s_ = (expr);             \
+        if (s_ != RAT3D_OK) return s_;        \
+    } while (0)
+
+rat3d_status ru_fwd(const Exec& e, const RUPlan& r) {
+    RAT3D_TRY(e.conv_f(r.c1, e.a(r.x), e.a(r.h1)));
+    RAT3D_TRY(e.bn_f(r.b1, r.h1, nullptr, 1, e.a(r.a1)));
+    RAT3D_TRY(e.conv_f(r.c2, e.a(r.a1), e.a(r.h2)));
+    const void* skip = e.a(r.x);
+    if (r.proj) {
+        RAT3D_TRY(e.conv_f(r.cp, e.a(r.x), e.a(r.hp)));
+        RAT3D_TRY(e.bn_f(r.bp, r.hp, nullptr, 0, e.a(r.sp)));
+        skip = e.a(r.sp);
+    }
+    return e.bn_f(r.b2, r.h2, skip, 1, e.a(r.y));
+}
+
+// Backward of a residual unit from y's gradient to x's gradient.  acc_dx: the
+// input gradient already holds a partial sum to add to.
+rat3d_status ru_bwd(const Exec& e, const RUPlan& r, bool acc_dx, bool need_dx = true) {
+    void* dskip = e.p(r.dskip);
+    void* dx = need_dx ? e.g(r.x) : nullptr;
+    const bool skip_direct = !r.proj && !acc_dx && need_dx;
+    RAT3D_TRY(e.bn_b(r.b2, e.g(r.y), r.h2, e.a(r.y), 1, e.g(r.h2), skip_direct ? dx : dskip));
+    RAT3D_TRY(e.conv_d(r.c2, e.g(r.h2), e.g(r.a1), 0));
+    RAT3D_TRY(e.conv_w(r.c2, e.a(r.a1), e.g(r.h2)));
+    RAT3D_TRY(e.bn_b(r.b1, e.g(r.a1), r.h1, e.a(r.a1), 1, e.g(r.h1), nullptr));
+    if (r.proj) {
+        RAT3D_TRY(e.bn_b(r.bp, dskip, r.hp, nullptr, 0, e.g(r.hp), nullptr));
+        if (need_dx) RAT3D_TRY(e.conv_d(r.cp, e.g(r.hp), dx, acc_dx ? 1 : 0));
+        RAT3D_TRY(e.conv_w(r.cp, e.a(r.x), e.g(r.hp)));
+    } else if (need_dx && acc_dx) {
+        RAT3D_TRY(add_tensors(r.x.s.count(), e.n->dt, dx, dskip, dx, e.st));
+    }
+    if (need_dx) RAT3D_TRY(e.conv_d(r.c1, e.g(r.h1), dx, 1));
+    return e.conv_w(r.c1, e.a(r.x), e.g(r.h1));
+}
+
+rat3d_status am_fwd(const Exec& e, const AMPlan& m) {
+    const Shape& s = m.x.s;
+    const rat3d_dtype dt = e.n->dt;
+    RAT3D_TRY(ru_fwd(e, m.t1));
+    RAT3D_TRY(ru_fwd(e, m.t2));
+    RAT3D_TRY(pool_fwd(s.n, s.c, s.d, s.h, s.w, 3, 2, 1, dt, e.a(m.x), e.a(m.p1),
+                       (uint8_t*)e.p(m.am1), e.st));
+    RAT3D_TRY(ru_fwd(e, m.m1));
+    const Shape& s1 = m.p1.s;
+    RAT3D_TRY(pool_fwd(s.n, s.c, s1.d, s1.h, s1.w, 3, 2, 1, dt, e.a(m.m1.y), e.a(m.p2),
+                       (uint8_t*)e.p(m.am2), e.st));
+    RAT3D_TRY(ru_fwd(e, m.m2));
+    RAT3D_TRY(ru_fwd(e, m.m3));
+    const Shape& s2 = m.p2.s;
+    RAT3D_TRY(up_fwd(s.n, s.c, s2.d, s2.h, s2.w, s1.d, s1.h, s1.w, dt, e.a(m.m3.y), e.a(m.u1),
+                     e.st));
+    RAT3D_TRY(ru_fwd(e, m.m4));
+    RAT3D_TRY(up_fwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.a(m.m4.y), e.a(m.u2),
+                     e.st));
+    RAT3D_TRY(e.conv_f(m.c1, e.a(m.u2), e.a(m.h1)));
+    RAT3D_TRY(e.bn_f(m.bn, m.h1, nullptr, 1, e.a(m.a)));
+    RAT3D_TRY(e.conv_f(m.c2, e.a(m.a), e.a(m.z)));
+    return softmask_fwd(s.count(), dt, e.a(m.z), e.a(m.t2.y), e.a(m.out), e.a(m.m), e.st);
+}
+
+rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
+    const Shape& s = m.x.s;
+    const Shape& s1 = m.p1.s;
+    const Shape& s2 = m.p2.s;
+    const rat3d_dtype dt = e.n->dt;
+    RAT3D_TRY(softmask_bwd(s.count(), dt, e.g(m.out), e.a(m.t2.y), e.a(m.m), e.g(m.t2.y), 0,
+                           e.g(m.z), e.st));
+    RAT3D_TRY(e.conv_d(m.c2, e.g(m.z), e.g(m.a), 0));
+    RAT3D_TRY(e.conv_w(m.c2, e.a(m.a), e.g(m.z)));
+    RAT3D_TRY(e.bn_b(m.bn, e.g(m.a), m.h1, e.a(m.a), 1, e.g(m.h1), nullptr));
+    RAT3D_TRY(e.conv_d(m.c1, e.g(m.h1), e.g(m.u2), 0));
+    RAT3D_TRY(e.conv_w(m.c1, e.a(m.u2), e.g(m.h1)));
+    RAT3D_TRY(up_bwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.g(m.u2), e.g(m.m4.y), 0,
+                     e.st));
+    RAT3D_TRY(ru_bwd(e, m.m4, false));
+    RAT3D_TRY(up_bwd(s.n, s.c, s2.d, s2.h, s2.w, s1.d, s1.h, s1.w, dt, e.g(m.u1), e.g(m.m3.y), 0,
+                     e.st));
+    RAT3D_TRY(ru_bwd(e, m.m3, false));
+    RAT3D_TRY(ru_bwd(e, m.m2, false));
+    RAT3D_TRY(pool_bwd(s.n, s.c, s1.d, s1.h, s1.w, 3, 2, 1, dt, e.g(m.p2),
+                       (const uint8_t*)e.p(m.am2), e.g(m.m1.y), 0, e.st));
+    RAT3D_TRY(ru_bwd(e, m.m1, false));
+    if (need_dx)
+        RAT3D_TRY(pool_bwd(s.n, s.c, s.d, s.h, s.w, 3, 2, 1, dt, e.g(m.p1),
+                           (const uint8_t*)e.p(m.am1), e.g(m.x), 0, e.st));
+    RAT3D_TRY(ru_bwd(e, m.t2, false));
+    return ru_bwd(e, m.t1, true, need_dx);
+}
+
+rat3d_status stem_fwd(const Exec& e, bool pool) {
+    rat3d_net* n = e.n;
+    RAT3D_TRY(e.conv_f(n->stem_conv, n->ext_x, e.a(n->stem_h)));
+    RAT3D_TRY(e.bn_f(n->stem_bn, n->stem_h, nullptr, 1, e.a(n->stem_a)));
+    if (!pool) return RAT3D_OK;
+    const Shape& s = n->stem_a.s;
+    return pool_fwd(s.n, s.c, s.d, s.h, s.w, 3, 2, 1, n->dt, e.a(n->stem_a), e.a(n->stem_p),
+                    (uint8_t*)e.p(n->stem_am), e.st);
+}
+
+rat3d_status stem_bwd(const Exec& e, bool pool) {
+    rat3d_net* n = e.n;
+    if (pool) {
+        const Shape& s = n->stem_a.s;
+        RAT3D_TRY(pool_bwd(s.n, s.c, s.d, s.h, s.w, 3, 2, 1, n->dt, e.g(n->stem_p),
+                           (const uint8_t*)e.p(n->stem_am), e.g(n->stem_a), 0, e.st));
+    }
+    RAT3D_TRY(e.bn_b(n->stem_bn, e.g(n->stem_a), n->stem_h, e.a(n->stem_a), 1, e.g(n->stem_h),
+                     nullptr));
+    return e.conv_w(n->stem_conv, n->ext_x, e.g(n->stem_h));
+}
+
+rat3d_status prepare_call(rat3d_net* n, hipStream_t st) {
+    if (!n->P || !n->G || !n->ws) {
+        set_error("rat3d_net: buffers not bound (call rat3d_net_bind first)");
+        return RAT3D_EINVAL;
+    }
+    if (n->reset_running) {
+        RAT3D_TRY(fill_f32((int64_t)n->run_count, 0.f, (float*)(n->ws + n->run_mean_off), st));
+        RAT3D_TRY(fill_f32((int64_t)n->run_count, 1.f, (float*)(n->ws + n->run_var_off), st));
+        n->reset_running = false;
+    }
+    if (n->dt == RAT3D_BF16)
+        RAT3D_TRY(cast_f32_bf16((int64_t)n->param_count, n->P, (bf16*)(n->ws + n->mirror_off), st));
+    return RAT3D_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+rat3d_status rat3d_net_create(const rat3d_net_desc* desc, rat3d_net** out) {
+    if (!desc || !out) {
+        set_error("rat3d_net_create: NULL argument");
+        return RAT3D_EINVAL;
+    }
+    *out = nullptr;
+    const rat3d_net_desc& d = *desc;
+    if (d.dtype != RAT3D_F32 && d.dtype != RAT3D_BF16) {
+        set_error("rat3d_net_create: unsupported dtype");
+        return RAT3D_EUNSUPPORTED;
+    }
+    if (d.n < 1 || d.d < 1 || d.h < 1 || d.w < 1 || d.bn_eps <= 0.f || d.bn_momentum < 0.f ||
+        d.bn_momentum > 1.f) {
+        set_error("rat3d_net_create: invalid sizes or BN settings");
+        return RAT3D_EINVAL;
+    }
+    const int mb = d.micro_batches < 1 ? 1 : d.micro_batches;
+    if (mb != 1 && d.kind != RAT3D_NET_PARTITION1) {
+        set_error("rat3d_net_create: micro_batches > 1 only for PARTITION1");
+        return RAT3D_EINVAL;
+    }
+    rat3d_net* n = new rat3d_net();
+    n->d = d;
+    n->d.micro_batches = mb;
+    n->dt = d.dtype;
+    n->esz = d.dtype == RAT3D_BF16 ? 2 : 4;
+    Builder b{n};
+    const Shape in{d.n, d.c_in, d.d, d.h, d.w};
+    TRef x;
+    x.off = kExtX;
+    x.goff = kExtDx;
+    x.s = in;
+    switch (d.kind) {
+        case RAT3D_NET_RESUNIT: {
+            if (d.c_in < 1 || d.c < 1) break;
+            RUPlan r = b.ru("", x, d.c, 1);
+            r.y.off = kExtY;
+            r.y.goff = kExtDy;
+            n->rus.push_back(r);
+            break;
+        }
+        case RAT3D_NET_ATTN: {
+            if (d.c < 1 || d.c_in != d.c) break;
+            AMPlan m = b.am("", x);
+            m.out.off = kExtY;
+            m.out.goff = kExtDy;
+            n->ams.push_back(m);
+            break;
+        }
+        case RAT3D_NET_RESATTNET:
+        case RAT3D_NET_PARTITION1: {
+            if (d.c_in != 1) break;
+            const bool full = d.kind == RAT3D_NET_RESATTNET;
+            if (!full && d.c < 1) break;
+            n->stem_conv = b.conv("stem", 1, 32, 7, 2, 3, false, in);
+            const ConvGeom& g = n->stem_conv.g;
+            const Shape so{d.n, 32, g.Do, g.Ho, g.Wo};
+            n->stem_bn = b.bn("stem.bn", 32, so);
+            n->stem_h = b.act("stem.h", so);
+            n->stem_a = b.act("stem.a", so);
+            TRef h = n->stem_a;
+            if (full) {
+                const Shape sp{d.n, 32, out_dim(so.d, 3, 2, 1), out_dim(so.h, 3, 2, 1),
+                               out_dim(so.w, 3, 2, 1)};
+                n->stem_p = b.act("stem.p", sp);
+                n->stem_am = (int64_t)b.alloc((size_t)sp.count());
+                b.record("stem.p.argmax", (size_t)n->stem_am, RAT3D_U8, sp);
+                h = n->stem_p;
+                const int stages[3] = {64, 128, 256};
+                for (int i = 0; i < 3; ++i) {
+                    const std::string pre = "s" + std::to_string(i + 1) + ".";
+                    n->rus.push_back(b.ru(pre + "ru.", h, stages[i], i == 0 ? 1 : 2));
+                    n->ams.push_back(b.am(pre + "am.", n->rus.back().y));
+                    h = n->ams.back().out;
+                }
+                n->fc_c = 256;
+                n->fc.w_off = b.param("fc.w", {2, 256});
+                n->fc.b_off = b.param("fc.b", {2});
+            } else {
+                n->rus.push_back(b.ru("ru.", h, d.c, 1));
+                n->ams.push_back(b.am("am.", n->rus.back().y));
+                // the output gradient is read straight from the caller's buffer
+                n->ams.back().out.goff = kExtDy;
+            }
+            break;
+        }
+        default:
+            break;
+    }
+    if (n->params.empty()) {
+        delete n;
+        set_error("rat3d_net_create: invalid kind or channel counts");
+        return RAT3D_EINVAL;
+    }
+    // fixed regions
+    if (n->dt == RAT3D_BF16) n->mirror_off = b.alloc(n->param_count * 2);
+    n->conv_scr_off = b.alloc(n->conv_scr_bytes);
+    n->bn_scr_off = b.alloc(n->bn_scr_bytes);
+    n->head_scr_off = b.alloc(head_ws_bytes(d.n, 256, 2));
+    n->run_mean_off = b.alloc(n->run_count * sizeof(float));
+    n->run_var_off = b.alloc(n->run_count * sizeof(float));
+    n->logits_off = b.alloc((size_t)d.n * 2 * sizeof(float));
+    n->loss_off = b.alloc(sizeof(float));
+    b.record("logits", n->logits_off, RAT3D_F32, Shape{d.n, 2, 1, 1, 1});
+    b.record("loss", n->loss_off, RAT3D_F32, Shape{1, 1, 1, 1, 1});
+    b.record("running_mean", n->run_mean_off, RAT3D_F32, Shape{1, (int)n->run_count, 1, 1, 1});
+    b.record("running_var", n->run_var_off, RAT3D_F32, Shape{1, (int)n->run_count, 1, 1, 1});
+    n->ws_bytes = (b.top + 255) & ~(size_t)255;
+    *out = n;
+    return RAT3D_OK;
+}
+
+void rat3d_net_destroy(rat3d_net* net) { delete net; }
+
+size_t rat3d_net_param_count(const rat3d_net* net) { return net ? net->param_count : 0; }
+
+size_t rat3d_net_workspace_size(const rat3d_net* net) { return net ? net->ws_bytes : 0; }
+
+int rat3d_net_num_params(const rat3d_net* net) { return net ? (int)net->params.size() : 0; }
+
+rat3d_status rat3d_net_param_info(const rat3d_net* net, int i, const char** name,
+                                  size_t* offset, int* ndim, int shape[5]) {
+    if (!net || i < 0 || i >= (int)net->params.size()) {
+        set_error("rat3d_net_param_info: index out of range");
+        return RAT3D_EINVAL;
+    }
+    const ParamRec& r = net->params[i];
+    if (name) *name = r.name.c_str();
+    if (offset) *offset = r.off;
+    if (ndim) *ndim = r.ndim;
+    if (shape)
+        for (int k = 0; k < 5; ++k) shape[k] = r.shape[k];
+    return RAT3D_OK;
+}
+
+int rat3d_net_num_tensors(const rat3d_net* net) { return net ? (int)net->tensors.size() : 0; }
+
+rat3d_status rat3d_net_tensor_info(const rat3d_net* net, int i, const char** name,
+                                   size_t* byte_offset, rat3d_dtype* dtype, int shape[5]) {
+    if (!net || i < 0 || i >= (int)net->tensors.size()) {
+        set_error("rat3d_net_tensor_info: index out of range");
+        return RAT3D_EINVAL;
+    }
+    const TensorRec& r = net->tensors[i];
+    if (name) *name = r.name.c_str();
+    if (byte_offset) *byte_offset = r.off;
+    if (dtype) *dtype = r.dt;
+    if (shape)
+        for (int k = 0; k < 5; ++k) shape[k] = r.shape[k];
+    return RAT3D_OK;
+}
+
+rat3d_status rat3d_net_bind(rat3d_net* net, float* params, float* grads, void* ws,
+                            size_t ws_bytes) {
+    if (!net || !params || !grads || !ws) {
+        set_error("rat3d_net_bind: NULL argument");
+        return RAT3D_EINVAL;
+    }
+    if (ws_bytes < net->ws_bytes) {
+        set_error("rat3d_net_bind: workspace needs %zu bytes, got %zu", net->ws_bytes, ws_bytes);
+        return RAT3D_EWORKSPACE;
+    }
+    if (!aligned16(params) || !aligned16(grads) || ((uintptr_t)ws & 255u) != 0) {
+        set_error("rat3d_net_bind: arenas must be 16-byte and the workspace 256-byte aligned");
+        return RAT3D_EALIGN;
+    }
+    net->P = params;
+    net->G = grads;
+    net->ws = (char*)ws;
+    net->reset_running = true;
+    return RAT3D_OK;
+}
+
+rat3d_status rat3d_block_fwd_bwd(rat3d_net* net, const void* x, const void* dy, void* y,
+                                 void* dx, void* stream) {
+    if (!net || (net->d.kind != RAT3D_NET_RESUNIT && net->d.kind != RAT3D_NET_ATTN)) {
+        set_error("rat3d_block_fwd_bwd: needs a RESUNIT or ATTN network");
+        return RAT3D_EINVAL;
+    }
+    if (!x || !dy || !y || !dx) {
+        set_error("rat3d_block_fwd_bwd: NULL tensor");
+        return RAT3D_EINVAL;
+    }
+    if (!aligned16(x) || !aligned16(dy) || !aligned16(y) || !aligned16(dx)) {
+        set_error("rat3d_block_fwd_bwd: tensors must be 16-byte aligned");
+        return RAT3D_EALIGN;
+    }
+    hipStream_t st = (hipStream_t)stream;
+    RAT3D_TRY(prepare_call(net, st));
+    net->ext_x = x;
+    net->ext_dy = dy;
+    net->ext_y = y;
+    net->ext_dx = dx;
+    Exec e{net, st, 0};
+    if (net->d.kind == RAT3D_NET_RESUNIT) {
+        RAT3D_TRY(ru_fwd(e, net->rus[0]));
+        return ru_bwd(e, net->rus[0], false);
+    }
+    RAT3D_TRY(am_fwd(e, net->ams[0]));
+    return am_bwd(e, net->ams[0]);
+}
+
+rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labels,
+                              const void* dy_upstream, float* loss_dev, void* stream) {
+    if (!net || (net->d.kind != RAT3D_NET_RESATTNET && net->d.kind != RAT3D_NET_PARTITION1)) {
+        set_error("rat3d_train_step: needs a RESATTNET or PARTITION1 network");
+        return RAT3D_EINVAL;
+    }
+    const bool full = net->d.kind == RAT3D_NET_RESATTNET;
+    if (!x || (full && !labels) || (!full && !dy_upstream)) {
+        set_error("rat3d_train_step: NULL input");
+        return RAT3D_EINVAL;
+    }
+    if (!aligned16(x) || (dy_upstream && !aligned16(dy_upstream))) {
+        set_error("rat3d_train_step: tensors must be 16-byte aligned");
+        return RAT3D_EALIGN;
+    }
+    hipStream_t st = (hipStream_t)stream;
+    RAT3D_TRY(prepare_call(net, st));
+    const rat3d_net_desc& d = net->d;
+    const size_t x_bytes = (size_t)d.n * d.d * d.h * d.w * net->esz;
+    if (full) {
+        net->ext_x = x;
+        Exec e{net, st, 0};
+        RAT3D_TRY(stem_fwd(e, true));
+        for (int i = 0; i < 3; ++i) {
+            RAT3D_TRY(ru_fwd(e, net->rus[i]));
+            RAT3D_TRY(am_fwd(e, net->ams[i]));
+        }
+        const TRef& top = net->ams[2].out;
+        RAT3D_TRY(head_fwd_bwd(d.n, net->fc_c, top.s.vox(), 2, net->dt, e.a(top),
+                               e.par(net->fc.w_off), e.par(net->fc.b_off), labels,
+                               (float*)(net->ws + net->logits_off),
+                               (float*)(net->ws + net->loss_off), e.g(top), e.grd(net->fc.w_off),
+                               e.grd(net->fc.b_off), 0, net->ws + net->head_scr_off, st));
+        for (int i = 2; i >= 0; --i) {
+            RAT3D_TRY(am_bwd(e, net->ams[i]));
+            RAT3D_TRY(ru_bwd(e, net->rus[i], false));
+        }
+        RAT3D_TRY(stem_bwd(e, true));
+        if (loss_dev) {
+            if (hipMemcpyAsync(loss_dev, net->ws + net->loss_off, sizeof(float),
+                               hipMemcpyDeviceToDevice, st) != hipSuccess) {
+                set_error("rat3d_train_step: loss copy failed");
+                return RAT3D_EHIP;
+            }
+        }
+    } else {
+        const AMPlan& am = net->ams[0];
+        const size_t dy_bytes = (size_t)am.out.s.count() * net->esz;
+        for (int mb = 0; mb < d.micro_batches; ++mb) {
+            net->ext_x = (const char*)x + mb * x_bytes;
+            // the partition's output gradient arrives from the next partition
+            net->ext_dy = (const char*)dy_upstream + mb * dy_bytes;
+            Exec e{net, st, mb > 0 ? 1 : 0};
+            RAT3D_TRY(stem_fwd(e, false));
+            RAT3D_TRY(ru_fwd(e, net->rus[0]));
+            RAT3D_TRY(am_fwd(e, am));
+            RAT3D_TRY(am_bwd(e, am));
+            RAT3D_TRY(ru_bwd(e, net->rus[0], false));
+            RAT3D_TRY(stem_bwd(e, false));
+        }
+    }
+    return sgd_update((int64_t)net->param_count, d.lr, net->P, net->G, st);
+}
+
+}  // extern "C"

@@ -1,0 +1,131 @@
+"""GPU parity of the composite blocks and training steps against the oracle,
+element by element: the single conv layer, the residual unit and the
+attention module at their full workload sizes, the full network and the
+first-stage partition at reduced volumes (the full sizes are covered by
+tests/test_gpu_full.py), plus reduced attention modules with ragged
+volumes."""
+import numpy as np
+import pytest
+
+from oracle import net as onet
+from oracle import ops
+from paper_2104_05035_amd import rat3d as R
+from paper_2104_05035_amd import synth
+from tests import gpu_util as U
+from tests.net_util import Bound, check_sgd, compare_grads
+
+pytestmark = pytest.mark.gpu
+
+
+def test_conv_layer_workload():
+    """Single conv3d layer fwd + dgrad + wgrad, float32: N=1, 4 -> 8 channels,
+    16^3, 3^3 kernel, stride 1, pad 1, bias; x U(-1,1), w and b N(0,0.1),
+    upstream gradient N(0,1)."""
+    cfg = synth.WORKLOADS[0]
+    rx, rw, rb, rdy = synth.streams(0, 4)
+    x, xr = U.dev_input(rx.uniform(-1, 1, (1, 4, 16, 16, 16)), "f32")
+    w, wr = U.dev_input(rw.normal(0, 0.1, (8, 4, 3, 3, 3)), "f32")
+    b, br = U.dev_input(rb.normal(0, 0.1, 8), "f32")
+    dy, dyr = U.dev_input(rdy.standard_normal((1, 8, 16, 16, 16)), "f32")
+    desc = R.conv_desc(1, 4, 8, 16, 16, 16, 3, 1, 1, True, R.F32)
+    ws = U.workspace(max(R.rat3d_conv3d_workspace_size(desc, i) for i in range(3)))
+    y, dx = U.empty((1, 8, 16, 16, 16), "f32"), U.empty((1, 4, 16, 16, 16), "f32")
+    dw, db = U.zeros_f32((8, 4, 3, 3, 3)), U.zeros_f32((8,))
+    R.rat3d_conv3d_fwd(desc, x, w, b, y, ws, ws.numel())
+    R.rat3d_conv3d_dgrad(desc, dy, w, dx, 0, ws, ws.numel())
+    R.rat3d_conv3d_wgrad(desc, x, dy, dw, db, 0, ws, ws.numel())
+    U.sync()
+    assert cfg["k"] == 3 and cfg["bias"]
+    U.check(U.f64(y), ops.conv3d_fwd(xr, wr, br, 1, 1), "f32", "y")
+    U.check(U.f64(dx), ops.conv3d_dgrad(dyr, wr, xr.shape, 1, 1), "f32", "dx")
+    dwr, dbr = ops.conv3d_wgrad(xr, dyr, 3, 1, 1, True)
+    U.check(U.f64(dw), dwr, "f32", "dw")
+    U.check(U.f64(db), dbr, "f32", "db")
+
+
+def _block(kind, code, n, c, d, h, w, dt, seed, perturb_bn=0.0):
+    rng, rx, rdy = synth.streams(seed, 3)
+    B = Bound(code, n, c, c, d, h, w, dt, rng, perturb_bn=perturb_bn, bias_std=0.1)
+    x, xr = U.dev_input(rx.standard_normal((n, c, d, h, w)), dt)
+    dy, dyr = U.dev_input(rdy.standard_normal((n, c, d, h, w)), dt)
+    y, dx = U.empty((n, c, d, h, w), dt), U.empty((n, c, d, h, w), dt)
+    B.net.rat3d_block_fwd_bwd(x, dy, y, dx)
+    U.sync()
+    yref, dxref, Gref, _ = onet.block_fwd_bwd(kind, B.params, xr, dyr, bf16=(dt == "bf16"))
+    U.check(U.f64(y), yref, dt, "y")
+    U.check(U.f64(dx), dxref, dt, "dx")
+    compare_grads(B.grads(), Gref, dt)
+
+
+def test_resunit_workload():
+    """Residual unit fwd+bwd, float32: N=2, C=32, 32^3, He weights, BN
+    (batch statistics, eps 1e-5), identity skip."""
+    _block("resunit", R.NET_RESUNIT, 2, 32, 32, 32, 32, "f32", 1)
+
+
+def test_resunit_ragged_perturbed_bn():
+    _block("resunit", R.NET_RESUNIT, 3, 16, 7, 9, 5, "f32", 11, perturb_bn=0.2)
+
+
+def test_attn_reduced_bf16():
+    _block("attn", R.NET_ATTN, 2, 16, 24, 24, 24, "bf16", 12, perturb_bn=0.1)
+
+
+def test_attn_ragged_f32():
+    _block("attn", R.NET_ATTN, 2, 8, 12, 14, 12, "f32", 13, perturb_bn=0.1)
+
+
+@pytest.mark.timeout(900)
+def test_attn_workload():
+    """Attention module fwd+bwd, bf16 storage / fp32 accumulation: N=4, C=64,
+    48^3 (trunk 2 RUs; mask pool-RU-pool-2RU-up-RU-up-1^3-1^3-sigmoid)."""
+    _block("attn", R.NET_ATTN, 4, 64, 48, 48, 48, "bf16", 2)
+
+
+def _resattnet(n, d, h, w, seed):
+    rng, rx, rl = synth.streams(seed, 3)
+    B = Bound(R.NET_RESATTNET, n, 1, 32, d, h, w, "bf16", rng)
+    vol = synth.mri_volumes(rx, n, (d, h, w))
+    x, xr = U.dev_input(vol, "bf16")
+    lab = rl.integers(0, 2, n).astype(np.int32)
+    torch = U.torch_mod()
+    labels = U.to_dev(torch.from_numpy(lab))
+    loss = U.zeros_f32((1,))
+    old = {k: v.copy() for k, v in B.params.items()}
+    B.net.rat3d_train_step(x, labels, None, loss)
+    U.sync()
+    new, Gref, info = onet.train_step("resattnet", B.params, 1e-4, True, x=xr, labels=lab)
+    G = B.grads()
+    assert abs(float(U.f64(loss)[0]) - info["loss"]) <= 2e-2 * abs(info["loss"])
+    U.check(B.tensor("logits"), info["logits"], "bf16", "logits")
+    compare_grads(G, Gref, "bf16")
+    check_sgd(old, B.new_params(), G, 1e-4)
+
+
+def test_resattnet_reduced():
+    """Full network step on 2 volumes of 48x56x48 (same graph, smaller maps)."""
+    _resattnet(2, 48, 56, 48, 23)
+
+
+def _partition(n, mb, d, h, w, c, seed):
+    rng, rx, rdy = synth.streams(seed, 3)
+    B = Bound(R.NET_PARTITION1, n, 1, c, d, h, w, "bf16", rng, micro_batches=mb)
+    vol = synth.mri_volumes(rx, n * mb, (d, h, w))
+    x, xr = U.dev_input(vol, "bf16")
+    so = [ops.out_size(v, 7, 2, 3) for v in (d, h, w)]
+    dy, dyr = U.dev_input(rdy.standard_normal((n * mb, c) + tuple(so)), "bf16")
+    old = {k: v.copy() for k, v in B.params.items()}
+    B.net.rat3d_train_step(x, None, dy, None)
+    U.sync()
+    new, Gref, info = onet.train_step("partition1", B.params, 1e-4, True, x=xr, dy=dyr,
+                                      micro_batches=mb)
+    G = B.grads()
+    U.check(B.tensor("am.out"), info["y"][-1], "bf16", "partition output (last micro-batch)")
+    compare_grads(G, Gref, "bf16")
+    check_sgd(old, B.new_params(), G, 1e-4)
+    return B
+
+
+def test_partition1_reduced():
+    """First-stage partition, 2 micro-batches of 2 volumes of 48x56x48."""
+    _partition(2, 2, 48, 56, 48, 64, 24)

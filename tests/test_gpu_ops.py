@@ -1,0 +1,260 @@
+"""GPU parity of each C-ABI operation against the oracle, element by element,
+at sizes the oracle finishes in seconds: several tiles, ragged tails, odd
+volumes, both storage types, and the degenerate cases (one voxel, one
+channel).  Gates: see tests/gpu_util.py."""
+import zlib
+
+import numpy as np
+import pytest
+
+from oracle import ops
+from tests import gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+CONV_CASES = [
+    # N, Ci, Co, D, H, W, k, s, p, bias, dtype
+    (1, 4, 8, 16, 16, 16, 3, 1, 1, True, "f32"),
+    (2, 3, 5, 7, 9, 11, 3, 1, 1, False, "f32"),
+    (2, 32, 32, 9, 10, 13, 3, 1, 1, False, "f32"),
+    (2, 32, 64, 9, 10, 13, 3, 1, 1, False, "bf16"),
+    (2, 64, 64, 12, 14, 12, 3, 1, 1, False, "bf16"),
+    (1, 64, 64, 5, 16, 48, 3, 1, 1, False, "bf16"),
+    (1, 1, 32, 20, 22, 18, 7, 2, 3, False, "bf16"),
+    (2, 64, 128, 12, 14, 12, 3, 2, 1, False, "bf16"),
+    (2, 32, 64, 10, 9, 8, 1, 1, 0, False, "bf16"),
+    (2, 64, 128, 12, 14, 12, 1, 2, 0, False, "bf16"),
+    (2, 64, 64, 6, 7, 6, 1, 1, 0, True, "bf16"),
+    (1, 1, 1, 1, 1, 1, 1, 1, 0, True, "f32"),
+    (1, 2, 3, 2, 2, 2, 3, 1, 1, False, "bf16"),
+    (3, 5, 70, 5, 3, 4, 3, 1, 1, True, "bf16"),
+    (2, 128, 256, 6, 7, 6, 3, 2, 1, False, "bf16"),
+]
+
+
+def _id(c):
+    return "n%d_%dto%d_%dx%dx%d_k%ds%dp%d_%s%s" % (c[0], c[1], c[2], c[3], c[4], c[5], c[6], c[7],
+                                                   c[8], c[10], "_bias" if c[9] else "")
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=_id)
+def test_conv3d(case):
+    from paper_2104_05035_amd import rat3d as R
+    N, Ci, Co, D, H, W, k, s, p, has_bias, dt = case
+    rng = np.random.default_rng(zlib.crc32(repr(case).encode()))
+    rnd = ops.round_bf16 if dt == "bf16" else ops.identity
+    x, xr = U.dev_input(rng.standard_normal((N, Ci, D, H, W)), dt)
+    w, wr = U.dev_input(rng.normal(0, np.sqrt(2.0 / (Ci * k ** 3)), (Co, Ci, k, k, k)), dt)
+    b32 = rng.normal(0, 0.1, Co).astype(np.float32)
+    bias = U.to_dev(U.torch_mod().from_numpy(b32)) if has_bias else None
+    br = b32.astype(np.float64) if has_bias else None
+    desc = R.conv_desc(N, Ci, Co, D, H, W, k, s, p, has_bias, U.code(dt))
+    Do, Ho, Wo = (ops.out_size(v, k, s, p) for v in (D, H, W))
+    ws = U.workspace(max(R.rat3d_conv3d_workspace_size(desc, i) for i in range(3)))
+    nbytes = ws.numel()
+    # forward
+    y = U.empty((N, Co, Do, Ho, Wo), dt)
+    R.rat3d_conv3d_fwd(desc, x, w, bias, y, ws, nbytes)
+    yref = rnd(ops.conv3d_fwd(xr, wr, br, s, p))
+    # input gradient, plain and accumulated
+    dy, dyr = U.dev_input(rng.standard_normal((N, Co, Do, Ho, Wo)), dt)
+    dx = U.empty((N, Ci, D, H, W), dt)
+    R.rat3d_conv3d_dgrad(desc, dy, w, dx, 0, ws, nbytes)
+    dxref = ops.conv3d_dgrad(dyr, wr, xr.shape, s, p)
+    base, baser = U.dev_input(rng.standard_normal((N, Ci, D, H, W)), dt)
+    R.rat3d_conv3d_dgrad(desc, dy, w, base, 1, ws, nbytes)
+    # weight gradient, plain and accumulated
+    dw = U.zeros_f32((Co, Ci, k, k, k))
+    db = U.zeros_f32((Co,)) if has_bias else None
+    R.rat3d_conv3d_wgrad(desc, x, dy, dw, db, 0, ws, nbytes)
+    dw2 = U.to_dev(U.torch_mod().ones((Co, Ci, k, k, k)))
+    R.rat3d_conv3d_wgrad(desc, x, dy, dw2, None, 1, ws, nbytes)
+    U.sync()
+    dwref, dbref = ops.conv3d_wgrad(xr, dyr, k, s, p, has_bias)
+    U.check(U.f64(y), yref, dt, "y")
+    U.check(U.f64(dx), rnd(dxref), dt, "dx")
+    U.check(U.f64(base), rnd(baser + dxref), dt, "dx accumulate")
+    U.check(U.f64(dw), dwref, dt, "dw")
+    U.check(U.f64(dw2), dwref + 1.0, dt, "dw accumulate")
+    if has_bias:
+        U.check(U.f64(db), dbref, dt, "db")
+
+
+BN_CASES = [
+    (2, 3, 5, 6, 7, "f32"), (4, 16, 12, 14, 12, "bf16"), (2, 8, 6, 7, 6, "bf16"),
+    (1, 2, 1, 1, 3, "f32"), (3, 4, 3, 4, 3, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", BN_CASES, ids=lambda c: "%dx%dx%dx%dx%d_%s" % c)
+@pytest.mark.parametrize("relu,resid", [(1, False), (0, False), (1, True)])
+def test_bn(case, relu, resid):
+    from paper_2104_05035_amd import rat3d as R
+    torch = U.torch_mod()
+    N, C, D, H, W, dt = case
+    rng = np.random.default_rng(N * 1000 + C * 10 + relu + 2 * resid)
+    rnd = ops.round_bf16 if dt == "bf16" else ops.identity
+    shp = (N, C, D, H, W)
+    x, xr = U.dev_input(1.5 + 2.0 * rng.standard_normal(shp), dt)
+    r, rr = U.dev_input(rng.standard_normal(shp), dt) if resid else (None, None)
+    g32 = (1.0 + 0.3 * rng.standard_normal(C)).astype(np.float32)
+    b32 = (0.2 * rng.standard_normal(C)).astype(np.float32)
+    gamma, beta = U.to_dev(torch.from_numpy(g32)), U.to_dev(torch.from_numpy(b32))
+    desc = R.BnDesc(N, C, D, H, W, relu, 1e-5, 0.1, U.code(dt))
+    ws = U.workspace(R.rat3d_bn_workspace_size(desc))
+    y = U.empty(shp, dt)
+    mean, invstd = U.zeros_f32((C,)), U.zeros_f32((C,))
+    rm, rv = U.zeros_f32((C,)), U.to_dev(torch.ones(C))
+    R.rat3d_bn_relu_fwd(desc, x, r, gamma, beta, y, mean, invstd, rm, rv, ws, ws.numel())
+    dy, dyr = U.dev_input(rng.standard_normal(shp), dt)
+    dx = U.empty(shp, dt)
+    dres = U.empty(shp, dt) if resid else None
+    dg, dbt = U.zeros_f32((C,)), U.zeros_f32((C,))
+    R.rat3d_bn_relu_bwd(desc, dy, x, y, gamma, mean, invstd, dx, dres, dg, dbt, 0, ws,
+                        ws.numel())
+    U.sync()
+    yref, mref, vref, isref = ops.bn_fwd(xr, g32.astype(np.float64), b32.astype(np.float64),
+                                         1e-5, relu, rr)
+    yref = rnd(yref)
+    U.check(U.f64(y), yref, dt, "y")
+    U.check(U.f64(mean), mref, "f32", "mean")
+    U.check(U.f64(invstd), isref, "f32", "invstd")
+    cnt = N * D * H * W
+    rmr, rvr = ops.bn_running_update(np.zeros(C), np.ones(C), mref, vref, cnt, 0.1)
+    U.check(U.f64(rm), rmr, "f32", "running mean")
+    U.check(U.f64(rv), rvr, "f32", "running var")
+    dxr, gr, dgr, dbr = ops.bn_bwd(dyr, xr, yref, g32.astype(np.float64), mref, isref, relu)
+    U.check(U.f64(dx), rnd(dxr), dt, "dx")
+    U.check(U.f64(dg), dgr, dt, "dgamma")
+    U.check(U.f64(dbt), dbr, dt, "dbeta")
+    if resid:
+        U.check(U.f64(dres), gr, dt, "dresidual")
+
+
+POOL_CASES = [(2, 3, 9, 8, 7, "bf16"), (2, 16, 24, 28, 24, "bf16"), (1, 2, 3, 4, 3, "f32"),
+              (1, 1, 2, 2, 2, "bf16"), (2, 4, 6, 7, 6, "bf16"), (1, 1, 1, 1, 1, "f32")]
+
+
+@pytest.mark.parametrize("case", POOL_CASES, ids=lambda c: "%dx%dx%dx%dx%d_%s" % c)
+def test_maxpool(case):
+    from paper_2104_05035_amd import rat3d as R
+    torch = U.torch_mod()
+    N, C, D, H, W, dt = case
+    rng = np.random.default_rng(D * 100 + H * 10 + W)
+    rnd = ops.round_bf16 if dt == "bf16" else ops.identity
+    x, xr = U.dev_input(rng.standard_normal((N, C, D, H, W)), dt)
+    yref, amref = ops.maxpool3d_fwd(xr)
+    desc = R.PoolDesc(N, C, D, H, W, 3, 2, 1, U.code(dt))
+    y = U.empty(yref.shape, dt)
+    am = torch.empty(yref.shape, dtype=torch.uint8, device="cuda:0")
+    R.rat3d_softmask_down_fwd(desc, x, y, am)
+    dy, dyr = U.dev_input(rng.standard_normal(yref.shape), dt)
+    dx = U.empty((N, C, D, H, W), dt)
+    R.rat3d_softmask_down_bwd(desc, dy, am, dx, 0)
+    base, baser = U.dev_input(rng.standard_normal((N, C, D, H, W)), dt)
+    R.rat3d_softmask_down_bwd(desc, dy, am, base, 1)
+    U.sync()
+    np.testing.assert_array_equal(U.f64(y), yref)                      # bit-exact
+    np.testing.assert_array_equal(am.cpu().numpy().astype(np.int32), amref)
+    dxr = ops.maxpool3d_bwd(dyr, amref, xr.shape)
+    U.check(U.f64(dx), rnd(dxr), dt, "dx")
+    U.check(U.f64(base), rnd(baser + dxr), dt, "dx accumulate")
+
+
+UP_CASES = [((6, 7, 6), (12, 14, 12)), ((3, 4, 3), (6, 7, 6)), ((2, 2, 2), (3, 4, 3)),
+            ((12, 12, 12), (24, 24, 24)), ((5, 3, 4), (5, 9, 7)), ((1, 1, 1), (2, 3, 1))]
+
+
+@pytest.mark.parametrize("sizes", UP_CASES, ids=lambda s: "%s_to_%s" % s)
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_trilinear(sizes, dt):
+    from paper_2104_05035_amd import rat3d as R
+    (Di, Hi, Wi), (Do, Ho, Wo) = sizes
+    rng = np.random.default_rng(Di * 7 + Do)
+    rnd = ops.round_bf16 if dt == "bf16" else ops.identity
+    N, C = 2, 3
+    x, xr = U.dev_input(rng.standard_normal((N, C, Di, Hi, Wi)), dt)
+    desc = R.UpDesc(N, C, Di, Hi, Wi, Do, Ho, Wo, U.code(dt))
+    y = U.empty((N, C, Do, Ho, Wo), dt)
+    R.rat3d_softmask_up_fwd(desc, x, y)
+    dy, dyr = U.dev_input(rng.standard_normal((N, C, Do, Ho, Wo)), dt)
+    dx = U.empty((N, C, Di, Hi, Wi), dt)
+    R.rat3d_softmask_up_bwd(desc, dy, dx, 0)
+    U.sync()
+    U.check(U.f64(y), rnd(ops.trilinear_fwd(xr, (Do, Ho, Wo))), dt, "y")
+    U.check(U.f64(dx), rnd(ops.trilinear_bwd(dyr, (Di, Hi, Wi))), dt, "dx")
+
+
+@pytest.mark.parametrize("count", [1, 1001, 4096, 131072 + 5])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_softmask_fuse(count, dt):
+    from paper_2104_05035_amd import rat3d as R
+    rng = np.random.default_rng(count)
+    rnd = ops.round_bf16 if dt == "bf16" else ops.identity
+    z, zr = U.dev_input(3 * rng.standard_normal(count), dt)
+    t, tr = U.dev_input(rng.standard_normal(count), dt)
+    out, m = U.empty((count,), dt), U.empty((count,), dt)
+    R.rat3d_softmask_fwd(count, U.code(dt), z, t, out, m)
+    dout, doutr = U.dev_input(rng.standard_normal(count), dt)
+    dtt, dz = U.empty((count,), dt), U.empty((count,), dt)
+    R.rat3d_softmask_bwd(count, U.code(dt), dout, t, m, dtt, 0, dz)
+    acc, accr = U.dev_input(rng.standard_normal(count), dt)
+    dz2 = U.empty((count,), dt)
+    R.rat3d_softmask_bwd(count, U.code(dt), dout, t, m, acc, 1, dz2)
+    U.sync()
+    outr, mr = ops.softmask_fwd(zr, tr, rnd)
+    U.check(U.f64(out), outr, dt, "out")
+    U.check(U.f64(m), mr, dt, "m")
+    dtr, dzr = ops.softmask_bwd(doutr, tr, mr, rnd)
+    U.check(U.f64(dtt), dtr, dt, "dt")
+    U.check(U.f64(dz), dzr, dt, "dz")
+    U.check(U.f64(acc), rnd(accr + (1.0 + mr) * doutr), dt, "dt accumulate")
+
+
+@pytest.mark.parametrize("N,C,V,dt", [(8, 256, 252, "bf16"), (3, 5, 7, "f32"), (1, 1, 1, "f32")])
+def test_head(N, C, V, dt):
+    from paper_2104_05035_amd import rat3d as R
+    torch = U.torch_mod()
+    rng = np.random.default_rng(N + C + V)
+    rnd = ops.round_bf16 if dt == "bf16" else ops.identity
+    x, xr = U.dev_input(rng.standard_normal((N, C, V)) + 0.3, dt)
+    w32 = rng.normal(0, np.sqrt(1.0 / C), (2, C)).astype(np.float32)
+    b32 = rng.normal(0, 0.1, 2).astype(np.float32)
+    lab = rng.integers(0, 2, N).astype(np.int32)
+    fw, fb = U.to_dev(torch.from_numpy(w32)), U.to_dev(torch.from_numpy(b32))
+    labels = U.to_dev(torch.from_numpy(lab))
+    logits, loss = U.zeros_f32((N, 2)), U.zeros_f32((1,))
+    dx = U.empty((N, C, V), dt)
+    dfw, dfb = U.zeros_f32((2, C)), U.zeros_f32((2,))
+    ws = U.workspace(R.rat3d_head_workspace_size(N, C, 2))
+    R.rat3d_head_fwd_bwd(N, C, V, 2, U.code(dt), x, fw, fb, labels, logits, loss, dx, dfw, dfb, 0,
+                         ws, ws.numel())
+    U.sync()
+    g = xr.mean(axis=2)
+    lref = ops.fc_fwd(g, w32.astype(np.float64), b32.astype(np.float64))
+    lossr, dl = ops.ce_fwd_bwd(lref, lab)
+    dg, dwr, dbr = ops.fc_bwd(dl, g, w32.astype(np.float64))
+    U.check(U.f64(logits), lref, "f32", "logits")
+    assert abs(float(U.f64(loss)[0]) - lossr) <= 1e-4 * max(1.0, abs(lossr))
+    U.check(U.f64(dfw), dwr, "f32", "dfc_w")
+    U.check(U.f64(dfb), dbr, "f32", "dfc_b")
+    U.check(U.f64(dx), rnd(np.repeat(dg[:, :, None] / V, V, axis=2)), dt, "dx")
+
+
+def test_sgd_update_is_one_rounding():
+    from paper_2104_05035_amd import rat3d as R
+    torch = U.torch_mod()
+    rng = np.random.default_rng(5)
+    n = 1000003
+    w32 = rng.standard_normal(n).astype(np.float32)
+    g32 = rng.standard_normal(n).astype(np.float32)
+    w = U.to_dev(torch.from_numpy(w32.copy()))
+    g = U.to_dev(torch.from_numpy(g32))
+    R.rat3d_sgd(n, 1e-4, w, g)
+    U.sync()
+    lr = np.float64(np.float32(1e-4))
+    exact = w32.astype(np.float64) - lr * g32.astype(np.float64)
+    got = w.cpu().numpy()
+    # within one float32 rounding of the exact update
+    ulp = np.spacing(np.abs(exact).astype(np.float32)).astype(np.float64)
+    assert np.all(np.abs(got.astype(np.float64) - exact) <= ulp)
