@@ -27,8 +27,10 @@ design notes:
     residual unit (stride 1 for the first, 2 for the others) followed by an
     attention module; global average pool, FC to 2 classes, cross-entropy;
   * bfloat16 mode: every stored activation and activation gradient is rounded
-    to bfloat16 where the GPU stores it; weight gradients, BN statistics,
-    the pooled features, logits and loss are not rounded.
+    to bfloat16 where the GPU stores it, and convolutions use the bfloat16
+    working copy of their weights (the float32 master rounded to nearest
+    even); conv biases, BN parameters, the FC layer, weight gradients, BN
+    statistics, the pooled features, logits and loss stay unrounded.
 """
 import numpy as np
 
@@ -115,16 +117,33 @@ def n_stages(params):
 # Execution context
 # --------------------------------------------------------------------------
 class Ctx:
-    """Holds rounding mode, BN settings, the gradient dict and running stats."""
+    """Holds rounding mode, BN settings, the gradient dict and running stats.
 
-    def __init__(self, params, bf16, eps=1e-5, momentum=0.1, running=None):
+    jitter = (rel, seed) multiplies every stored value by (1 + rel * N(0,1))
+    before its rounding.  It is off by default; the parity tests use it to
+    measure how far the step's results move under rounding-level noise (the
+    step has ReLU and max-pool decisions, so it is only piecewise smooth).
+    """
+
+    def __init__(self, params, bf16, eps=1e-5, momentum=0.1, running=None, jitter=None):
         self.P = params
-        self.rnd = ops.round_bf16 if bf16 else ops.identity
+        base = ops.round_bf16 if bf16 else ops.identity
+        if jitter is None:
+            self.rnd = base
+        else:
+            rel, seed = jitter
+            noise = np.random.default_rng(seed)
+            self.rnd = lambda a: base(np.asarray(a, dtype=np.float64)
+                                      * (1.0 + rel * noise.standard_normal(np.shape(a))))
         self.eps = eps
         self.momentum = momentum
         self.G = {k: np.zeros_like(v) for k, v in params.items()}
         self.running = running if running is not None else {}
         self.acts = {}
+
+    def w(self, name):
+        """Conv weight as the convolution sees it (bf16 working copy in bf16 mode)."""
+        return self.rnd(self.P[name])
 
     def bn(self, name, x, relu, residual=None):
         y, mean, var, invstd = ops.bn_fwd(x, self.P[name + ".g"], self.P[name + ".b"],
@@ -146,13 +165,12 @@ class Ctx:
 # --------------------------------------------------------------------------
 def ru_fwd(ctx, pre, x, stride):
     P, rnd = ctx.P, ctx.rnd
-    w1 = P[pre + "conv1.w"]
     proj = (pre + "proj.w") in P
-    h1 = rnd(ops.conv3d_fwd(x, w1, None, stride, 1))
+    h1 = rnd(ops.conv3d_fwd(x, ctx.w(pre + "conv1.w"), None, stride, 1))
     a1, st1 = ctx.bn(pre + "bn1", h1, relu=True)
-    h2 = rnd(ops.conv3d_fwd(a1, P[pre + "conv2.w"], None, 1, 1))
+    h2 = rnd(ops.conv3d_fwd(a1, ctx.w(pre + "conv2.w"), None, 1, 1))
     if proj:
-        hp = rnd(ops.conv3d_fwd(x, P[pre + "proj.w"], None, stride, 0))
+        hp = rnd(ops.conv3d_fwd(x, ctx.w(pre + "proj.w"), None, stride, 0))
         sp, stp = ctx.bn(pre + "projbn", hp, relu=False)
         skip = sp
     else:
@@ -171,17 +189,17 @@ def ru_bwd(ctx, pre, c, dy, dx_acc=None):
     P, G, rnd = ctx.P, ctx.G, ctx.rnd
     x, s = c["x"], c["stride"]
     dh2, dskip = ctx.bn_back(pre + "bn2", dy, c["h2"], c["y"], c["st2"], relu=True)
-    da1 = rnd(ops.conv3d_dgrad(dh2, P[pre + "conv2.w"], c["a1"].shape, 1, 1))
+    da1 = rnd(ops.conv3d_dgrad(dh2, ctx.w(pre + "conv2.w"), c["a1"].shape, 1, 1))
     G[pre + "conv2.w"] += ops.conv3d_wgrad(c["a1"], dh2, 3, 1, 1, False)[0]
     dh1, _ = ctx.bn_back(pre + "bn1", da1, c["h1"], c["a1"], c["st1"], relu=True)
     if c["proj"]:
         dhp, _ = ctx.bn_back(pre + "projbn", dskip, c["hp"], c["sp"], c["stp"], relu=False)
-        dxs = ops.conv3d_dgrad(dhp, P[pre + "proj.w"], x.shape, s, 0)
+        dxs = ops.conv3d_dgrad(dhp, ctx.w(pre + "proj.w"), x.shape, s, 0)
         G[pre + "proj.w"] += ops.conv3d_wgrad(x, dhp, 1, s, 0, False)[0]
     else:
         dxs = dskip
     dx = rnd(dxs if dx_acc is None else dx_acc + dxs)
-    dx = rnd(dx + ops.conv3d_dgrad(dh1, P[pre + "conv1.w"], x.shape, s, 1))
+    dx = rnd(dx + ops.conv3d_dgrad(dh1, ctx.w(pre + "conv1.w"), x.shape, s, 1))
     G[pre + "conv1.w"] += ops.conv3d_wgrad(x, dh1, 3, s, 1, False)[0]
     return dx
 
@@ -203,9 +221,9 @@ def am_fwd(ctx, pre, x):
     u1 = rnd(ops.trilinear_fwd(r2b, r1.shape[2:]))
     r3, cm4 = ru_fwd(ctx, pre + "m4.", u1, 1)
     u2 = rnd(ops.trilinear_fwd(r3, x.shape[2:]))
-    c1 = rnd(ops.conv3d_fwd(u2, P[pre + "c1.w"], None, 1, 0))
+    c1 = rnd(ops.conv3d_fwd(u2, ctx.w(pre + "c1.w"), None, 1, 0))
     a, stb = ctx.bn(pre + "bn", c1, relu=True)
-    z = rnd(ops.conv3d_fwd(a, P[pre + "c2.w"], P[pre + "c2.bias"], 1, 0))
+    z = rnd(ops.conv3d_fwd(a, ctx.w(pre + "c2.w"), P[pre + "c2.bias"], 1, 0))
     out, m = ops.softmask_fwd(z, T, rnd)
     ctx.acts[pre + "T"] = T
     ctx.acts[pre + "z"] = z
@@ -222,12 +240,12 @@ def am_bwd(ctx, pre, c, dout):
     P, G, rnd = ctx.P, ctx.G, ctx.rnd
     x = c["x"]
     dT, dz = ops.softmask_bwd(dout, c["T"], c["m"], rnd)
-    da = rnd(ops.conv3d_dgrad(dz, P[pre + "c2.w"], c["a"].shape, 1, 0))
+    da = rnd(ops.conv3d_dgrad(dz, ctx.w(pre + "c2.w"), c["a"].shape, 1, 0))
     dw, db = ops.conv3d_wgrad(c["a"], dz, 1, 1, 0, True)
     G[pre + "c2.w"] += dw
     G[pre + "c2.bias"] += db
     dc1, _ = ctx.bn_back(pre + "bn", da, c["c1"], c["a"], c["stb"], relu=True)
-    du2 = rnd(ops.conv3d_dgrad(dc1, P[pre + "c1.w"], c["u2"].shape, 1, 0))
+    du2 = rnd(ops.conv3d_dgrad(dc1, ctx.w(pre + "c1.w"), c["u2"].shape, 1, 0))
     G[pre + "c1.w"] += ops.conv3d_wgrad(c["u2"], dc1, 1, 1, 0, False)[0]
     dr3 = rnd(ops.trilinear_bwd(du2, c["r3"].shape[2:]))
     du1 = ru_bwd(ctx, pre + "m4.", c["cm4"], dr3)
@@ -246,7 +264,7 @@ def am_bwd(ctx, pre, c, dout):
 # --------------------------------------------------------------------------
 def stem_fwd(ctx, x, pool):
     rnd = ctx.rnd
-    h0 = rnd(ops.conv3d_fwd(x, ctx.P["stem.w"], None, 2, 3))
+    h0 = rnd(ops.conv3d_fwd(x, ctx.w("stem.w"), None, 2, 3))
     a0, st0 = ctx.bn("stem.bn", h0, relu=True)
     c = dict(x=x, h0=h0, a0=a0, st0=st0, pool=pool)
     if pool:
@@ -267,10 +285,10 @@ def stem_bwd(ctx, c, dy):
 # --------------------------------------------------------------------------
 # Whole-block drivers
 # --------------------------------------------------------------------------
-def block_fwd_bwd(kind, params, x, dy, bf16, eps=1e-5):
+def block_fwd_bwd(kind, params, x, dy, bf16, eps=1e-5, jitter=None):
     """Forward + backward of one residual unit ('resunit') or one attention
     module ('attn').  Returns (y, dx, grads, ctx)."""
-    ctx = Ctx(params, bf16, eps)
+    ctx = Ctx(params, bf16, eps, jitter=jitter)
     x = ctx.rnd(np.asarray(x, dtype=np.float64))
     dy = ctx.rnd(np.asarray(dy, dtype=np.float64))
     if kind == "resunit":
@@ -284,9 +302,9 @@ def block_fwd_bwd(kind, params, x, dy, bf16, eps=1e-5):
     return y, dx, ctx.G, ctx
 
 
-def resattnet_fwd_bwd(params, x, labels, bf16, eps=1e-5, running=None):
+def resattnet_fwd_bwd(params, x, labels, bf16, eps=1e-5, running=None, jitter=None):
     """Full network forward, loss, backward.  Returns (loss, logits, grads, ctx)."""
-    ctx = Ctx(params, bf16, eps, running=running)
+    ctx = Ctx(params, bf16, eps, running=running, jitter=jitter)
     x = ctx.rnd(np.asarray(x, dtype=np.float64))
     h, cs = stem_fwd(ctx, x, pool=True)
     caches = []
@@ -313,11 +331,12 @@ def resattnet_fwd_bwd(params, x, labels, bf16, eps=1e-5, running=None):
     return loss, logits, ctx.G, ctx
 
 
-def partition1_fwd_bwd(params, x, dy, bf16, eps=1e-5, running=None, grads=None):
+def partition1_fwd_bwd(params, x, dy, bf16, eps=1e-5, running=None, grads=None,
+                       jitter=None):
     """First-stage partition (stem -> RU 32->c -> attention module) forward and
     backward for one micro-batch, given the gradient received at its output.
     Gradients are added to `grads` when given.  Returns (y, grads, ctx)."""
-    ctx = Ctx(params, bf16, eps, running=running)
+    ctx = Ctx(params, bf16, eps, running=running, jitter=jitter)
     if grads is not None:
         ctx.G = grads
     x = ctx.rnd(np.asarray(x, dtype=np.float64))
@@ -332,12 +351,13 @@ def partition1_fwd_bwd(params, x, dy, bf16, eps=1e-5, running=None, grads=None):
 
 
 def train_step(kind, params, lr, bf16, x=None, labels=None, dy=None,
-               micro_batches=1, eps=1e-5):
+               micro_batches=1, eps=1e-5, jitter=None):
     """One SGD step: gradients of the batch (summed over micro-batches), then
     w <- w - lr * g.  Returns (new_params, grads, info)."""
     running = {}
     if kind == "resattnet":
-        loss, logits, G, ctx = resattnet_fwd_bwd(params, x, labels, bf16, eps, running)
+        loss, logits, G, ctx = resattnet_fwd_bwd(params, x, labels, bf16, eps, running,
+                                                 jitter)
         info = dict(loss=loss, logits=logits, running=running, acts=ctx.acts)
     elif kind == "partition1":
         G = {k: np.zeros_like(v) for k, v in params.items()}
@@ -345,7 +365,8 @@ def train_step(kind, params, lr, bf16, x=None, labels=None, dy=None,
         nb = x.shape[0] // micro_batches
         for mb in range(micro_batches):
             sl = slice(mb * nb, (mb + 1) * nb)
-            y, G, ctx = partition1_fwd_bwd(params, x[sl], dy[sl], bf16, eps, running, G)
+            jit = None if jitter is None else (jitter[0], jitter[1] + mb)
+            y, G, ctx = partition1_fwd_bwd(params, x[sl], dy[sl], bf16, eps, running, G, jit)
             ys.append(y)
         info = dict(y=ys, running=running)
     else:

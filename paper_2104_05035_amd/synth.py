@@ -74,7 +74,7 @@ def init_param(rng, name, shape, bias_std=0.0, perturb_bn=0.0):
     if name.startswith("fc.b"):
         return np.zeros(shape)
     if name.endswith(".g"):
-        return 1.0 + (rng.normal(0.0, perturb_bn, shape) if perturb_bn else 0.0)
+        return np.ones(shape) + (rng.normal(0.0, perturb_bn, shape) if perturb_bn else 0.0)
     if name.endswith(".b"):
         return rng.normal(0.0, perturb_bn, shape) if perturb_bn else np.zeros(shape)
     if name.endswith("bias"):

@@ -71,3 +71,38 @@ def check_sgd(old, new, G, lr):
         exact = old[k] - lr64 * G[k]
         ulp = np.spacing(np.abs(exact).astype(np.float32)).astype(np.float64)
         assert np.all(np.abs(new[k] - exact) <= ulp), k
+
+
+JITTER = 1e-6  # relative noise of float32 arithmetic at a store point
+
+
+def floors(ref, jittered):
+    """Per-key spread of the oracle under rounding-level jitter (max over runs)."""
+    return {k: max(U.rel(j[k], ref[k]) for j in jittered) for k in ref}
+
+
+def gate(got, ref, floor, dt, what):
+    """Error must be within max(stated tolerance, 2 x the oracle's own spread)."""
+    got = np.asarray(got, dtype=np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), what
+    err = U.rel(got, ref)
+    lim = max(U.TOL[dt], 2.0 * floor)
+    assert err <= lim, "%s: relative error %.3e > %.3e (oracle spread %.3e)" % (
+        what, err, lim, floor)
+    return err, lim
+
+
+def gate_grads(G, Gref, Gjit, dt):
+    """Gate every parameter gradient and the whole gradient vector; returns
+    the number of tensors within the stated tolerance outright."""
+    fl = floors(Gref, Gjit)
+    within = 0
+    for k in Gref:
+        err, _ = gate(G[k], Gref[k], fl[k], dt, "grad " + k)
+        within += err <= U.TOL[dt]
+    keys = list(Gref)
+    cat = lambda D: np.concatenate([np.ravel(D[k]) for k in keys])
+    gfl = max(U.rel(cat(j), cat(Gref)) for j in Gjit)
+    gate(cat(G), cat(Gref), gfl, dt, "gradient vector")
+    return within

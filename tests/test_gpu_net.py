@@ -1,9 +1,18 @@
 """GPU parity of the composite blocks and training steps against the oracle,
-element by element: the single conv layer, the residual unit and the
-attention module at their full workload sizes, the full network and the
-first-stage partition at reduced volumes (the full sizes are covered by
-tests/test_gpu_full.py), plus reduced attention modules with ragged
-volumes."""
+element by element: the single conv layer, the residual unit, the attention
+module and the full network at their full workload sizes, the first-stage
+partition at a reduced volume (its full size is covered by
+tests/test_gpu_full.py), plus reduced and ragged blocks.
+
+Gates.  Forward outputs (block output, logits, loss, partition output) must
+be within the stated tolerance (1e-4 float32, 2e-2 bfloat16) outright.  The
+step is only piecewise smooth (ReLU masks, first-maximum pooling), so some
+gradients -- BN parameters and convolutions deep in the mask branch, whose
+incoming gradient has been made zero-mean by a BN backward -- move by more
+than that under rounding-level noise in ANY implementation.  Each gradient,
+and the gradient vector as a whole, must therefore be within the larger of
+the stated tolerance and twice the oracle's own spread when its stored values
+are jittered by 1e-6 relative (two seeds)."""
 import numpy as np
 import pytest
 
@@ -12,7 +21,7 @@ from oracle import ops
 from paper_2104_05035_amd import rat3d as R
 from paper_2104_05035_amd import synth
 from tests import gpu_util as U
-from tests.net_util import Bound, check_sgd, compare_grads
+from tests.net_util import JITTER, Bound, check_sgd, gate, gate_grads
 
 pytestmark = pytest.mark.gpu
 
@@ -51,10 +60,13 @@ def _block(kind, code, n, c, d, h, w, dt, seed, perturb_bn=0.0):
     y, dx = U.empty((n, c, d, h, w), dt), U.empty((n, c, d, h, w), dt)
     B.net.rat3d_block_fwd_bwd(x, dy, y, dx)
     U.sync()
-    yref, dxref, Gref, _ = onet.block_fwd_bwd(kind, B.params, xr, dyr, bf16=(dt == "bf16"))
+    bf = dt == "bf16"
+    yref, dxref, Gref, _ = onet.block_fwd_bwd(kind, B.params, xr, dyr, bf16=bf)
+    jit = [onet.block_fwd_bwd(kind, B.params, xr, dyr, bf16=bf, jitter=(JITTER, s))
+           for s in (1, 2)]
     U.check(U.f64(y), yref, dt, "y")
-    U.check(U.f64(dx), dxref, dt, "dx")
-    compare_grads(B.grads(), Gref, dt)
+    gate(U.f64(dx), dxref, max(U.rel(j[1], dxref) for j in jit), dt, "dx")
+    gate_grads(B.grads(), Gref, [j[2] for j in jit], dt)
 
 
 def test_resunit_workload():
@@ -95,16 +107,26 @@ def _resattnet(n, d, h, w, seed):
     B.net.rat3d_train_step(x, labels, None, loss)
     U.sync()
     new, Gref, info = onet.train_step("resattnet", B.params, 1e-4, True, x=xr, labels=lab)
+    jit = [onet.train_step("resattnet", B.params, 1e-4, True, x=xr, labels=lab,
+                           jitter=(JITTER, s))[1] for s in (1, 2)]
     G = B.grads()
     assert abs(float(U.f64(loss)[0]) - info["loss"]) <= 2e-2 * abs(info["loss"])
-    U.check(B.tensor("logits"), info["logits"], "bf16", "logits")
-    compare_grads(G, Gref, "bf16")
+    U.check(B.tensor("logits").reshape(n, 2), info["logits"], "bf16", "logits")
+    gate_grads(G, Gref, jit, "bf16")
     check_sgd(old, B.new_params(), G, 1e-4)
 
 
 def test_resattnet_reduced():
     """Full network step on 2 volumes of 48x56x48 (same graph, smaller maps)."""
     _resattnet(2, 48, 56, 48, 23)
+
+
+@pytest.mark.timeout(900)
+def test_resattnet_workload():
+    """Full network train step: 8 MRI-shaped volumes 96x112x96, bf16 storage,
+    stem 7^3 s2 -> 32 ch, maxpool, stages 64/128/256 (RU + attention), GAP,
+    FC to 2 classes, cross-entropy with random labels, SGD."""
+    _resattnet(8, 96, 112, 96, 3)
 
 
 def _partition(n, mb, d, h, w, c, seed):
@@ -119,9 +141,11 @@ def _partition(n, mb, d, h, w, c, seed):
     U.sync()
     new, Gref, info = onet.train_step("partition1", B.params, 1e-4, True, x=xr, dy=dyr,
                                       micro_batches=mb)
+    jit = [onet.train_step("partition1", B.params, 1e-4, True, x=xr, dy=dyr,
+                           micro_batches=mb, jitter=(JITTER, 10 * s))[1] for s in (1, 2)]
     G = B.grads()
     U.check(B.tensor("am.out"), info["y"][-1], "bf16", "partition output (last micro-batch)")
-    compare_grads(G, Gref, "bf16")
+    gate_grads(G, Gref, jit, "bf16")
     check_sgd(old, B.new_params(), G, 1e-4)
     return B
 
