@@ -1,0 +1,156 @@
+"""Benchmark: one training step of the first-stage partition of 3D-ResAttNet
+on one MI355X, through the librat3d C ABI.
+
+Workload (the largest single-GPU configuration): stem (7^3 stride-2 conv to
+32 channels, BN, ReLU) -> residual unit 32 -> 64 -> residual attention module
+on 64 channels, on 48x56x48 maps; 4 micro-batches of 16 single-channel
+volumes 96x112x96 (bf16 storage, fp32 accumulation); weight gradients summed
+over the micro-batches in fp32, then one SGD step.  The gradient arriving at
+the partition's output is a seeded N(0,1) tensor.  Volumes are synthetic
+MRI-shaped fields (see paper_2104_05035_amd/synth.py).
+
+Prints one JSON line.  value = algorithmic conv3d fwd+dgrad+wgrad TFLOP/s of
+the whole step (conv flops per step / step time); volumes_per_s is the same
+step counted in volumes.  The roofline object is for the kernel with the most
+time, timed with hipEvents recorded on its own launch stream by the library
+during the timed region.  cpu_baseline times the oracle on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "conv3d fwd+bwd TFLOP/s (% bf16 MFMA peak) and train volumes/sec, 1 MI355X"
+
+
+def build_inputs(torch, R, synth, n, mb, vol, c):
+    """Seeded parameters, volumes and upstream gradients, resident on the GPU."""
+    rng_p, rng_x, rng_dy = synth.streams(4, 3)
+    net = R.Net(R.NET_PARTITION1, n, 1, c, *vol, R.BF16, micro_batches=mb, lr=1e-4)
+    layout = net.params()
+    P0 = synth.init_params(rng_p, [(nm, shp) for nm, _, shp in layout])
+    import numpy as np
+    arena = np.concatenate([P0[nm].astype(np.float32).ravel() for nm, _, _ in layout])
+    P = torch.from_numpy(arena).to("cuda:0")
+    G = torch.zeros_like(P)
+    ws = torch.empty(net.workspace_size, dtype=torch.uint8, device="cuda:0")
+    net.rat3d_net_bind(P, G, ws, ws.numel())
+    xs = synth.mri_volumes(rng_x, n * mb, vol)
+    x = torch.from_numpy(xs).to(torch.bfloat16).to("cuda:0")
+    so = tuple((v + 6 - 7) // 2 + 1 for v in vol)
+    dys = []
+    for _ in range(mb):  # one micro-batch at a time keeps host memory small
+        a = rng_dy.standard_normal((n, c) + so, dtype=np.float32)
+        dys.append(torch.from_numpy(a).to(torch.bfloat16).to("cuda:0"))
+    dy = torch.cat(dys)
+    return net, P, G, ws, x, dy
+
+
+def cpu_baseline(budget_s=30.0):
+    """The oracle as it stands, on a bounded sample of the same workload: the
+    partition's forward and backward for ONE volume (same graph and shapes,
+    BN statistics over that volume), bf16 store points, float64 arithmetic."""
+    import numpy as np
+    from oracle import net as onet, ops
+    from paper_2104_05035_amd import synth
+    rng_p, rng_x, rng_dy = synth.streams(4, 3)
+    L = onet.param_layout("partition1", 1, 64)
+    P = {k: v.astype(np.float32).astype(np.float64) for k, v in synth.init_params(rng_p, L).items()}
+    x = ops.round_bf16(synth.mri_volumes(rng_x, 1, (96, 112, 96)))
+    dy = ops.round_bf16(rng_dy.standard_normal((1, 64, 48, 56, 48), dtype=np.float32))
+    t0 = time.perf_counter()
+    onet.partition1_fwd_bwd(P, x, dy, bf16=True)
+    dt = time.perf_counter() - t0
+    flops = 8.522e12 / 16.0  # conv flops of one volume through the partition
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": ops.num_threads(),
+            "kind": "oracle", "volumes_per_s": round(1.0 / dt, 6), "seconds": round(dt, 2),
+            "sample": "oracle forward+backward of the partition for 1 volume 96x112x96 "
+                      "(0.533 TFLOP of conv work), float64 loops, bf16 store points"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build runs the per-device training step "
+              "on a single MI355X and uses no collectives; run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2104_05035_amd import rat3d as R, synth
+    R.lib()
+    n, mb, vol, c = 16, 4, (96, 112, 96), 64
+    net, P, G, ws, x, dy = build_inputs(torch, R, synth, n, mb, vol, c)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        net.rat3d_train_step(x, None, dy, None)
+    torch.cuda.synchronize()
+
+    R.rat3d_profile_reset()
+    R.rat3d_profile_enable(1)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        net.rat3d_train_step(x, None, dy, None)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    R.rat3d_profile_enable(0)
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+
+    tags = [R.rat3d_profile_read(i) for i in range(R.rat3d_profile_count())]
+    conv_flops = sum(t[3] for t in tags if t[0].startswith("conv")) / args.steps
+    dom = max(tags, key=lambda t: t[2])
+    per_launch_ms = dom[2] / dom[1]
+    if dom[3] > 0:
+        achieved = dom[3] / dom[1] / (per_launch_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 5),
+                "traffic": None}
+    else:
+        achieved = dom[4] / dom[1] / (per_launch_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 3), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 5), "traffic": None}
+    roof["kernel"] = dom[0]
+    roof["avg_launch_us"] = round(per_launch_ms * 1e3, 3)
+    roof["launches_per_step"] = dom[1] // args.steps
+
+    tflops = conv_flops / (ms_step * 1e-3) / 1e12
+    vols = n * mb / (ms_step * 1e-3)
+    kernels = sorted(tags, key=lambda t: -t[2])[:8]
+    out = {
+        "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "partition1: stem 7^3 s2 1->32, RU 32->64, attention module 64 "
+                               "on 48x56x48; 4 micro-batches x 16 volumes 96x112x96",
+                   "micro_batches": mb, "volumes_per_micro_batch": n, "volume": list(vol),
+                   "channels": c, "parallelism": "none (1 GPU)"},
+        "volumes_per_s": round(vols, 3),
+        "pct_bf16_mfma_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 3),
+        "conv_tflop_per_step": round(conv_flops / 1e12, 4),
+        "wall_s_timed": round(wall, 3),
+        "kernels_ms_per_step": {t[0]: round(t[2] / args.steps, 3) for t in kernels},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

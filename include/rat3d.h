@@ -312,6 +312,21 @@ rat3d_status rat3d_block_fwd_bwd(rat3d_net* net, const void* x, const void* dy, 
 rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labels,
                               const void* dy_upstream, float* loss_dev, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Measurement (off by default).  While enabled, every launch of a hot kernel
+ * is bracketed by two hipEvents recorded on the stream it is launched on, and
+ * the operation's algorithmic work is added to its tag: convolutions count
+ * 2 * N * C_out * C_in * k^3 * (output voxels) flops per pass (the cost
+ * formula of the use-case section, two flops per multiply-add), elementwise
+ * kernels the bytes they must read and write once.  Reading a tag waits for
+ * its pending events.  Not for use while another thread launches work.
+ * ------------------------------------------------------------------------ */
+rat3d_status rat3d_profile_enable(int enable);
+rat3d_status rat3d_profile_reset(void);
+int rat3d_profile_count(void);
+rat3d_status rat3d_profile_read(int i, const char** name, int64_t* launches, double* total_ms,
+                                double* alg_flops, double* alg_bytes);
+
 #ifdef __cplusplus
 }
 #endif

@@ -45,6 +45,8 @@ def _lib():
         lib.orc_maxpool3d_bwd.argtypes = [i] * 8 + [dp, ip, dp, i]
         lib.orc_trilinear_fwd.argtypes = [i] * 8 + [dp, dp]
         lib.orc_trilinear_bwd.argtypes = [i] * 8 + [dp, dp, i]
+        lib.orc_num_threads.argtypes = []
+        lib.orc_num_threads.restype = ctypes.c_int
         lib.orc_conv3d_fwd_points.argtypes = [i] * 9 + [dp, dp, dp, i, ip, dp]
         lib.orc_conv3d_dgrad_points.argtypes = [i] * 9 + [dp, dp, i, ip, dp]
         lib.orc_conv3d_wgrad_points.argtypes = [i] * 9 + [dp, dp, i, ip, dp]
@@ -72,6 +74,11 @@ def _iptr(a):
 
 def _f64(a):
     return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def num_threads():
+    """Threads used by the oracle's parallel loops."""
+    return _lib().orc_num_threads()
 
 
 def out_size(i, k, s, p):

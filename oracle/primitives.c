@@ -432,3 +432,7 @@ void orc_conv3d_wgrad_points(int N, int Ci, int Co, int D, int H, int W, int k, 
         out[q] = acc;
     }
 }
+
+/* Threads the oracle's parallel loops use. */
+#include <omp.h>
+int orc_num_threads(void) { return omp_get_max_threads(); }

@@ -16,6 +16,7 @@
 #include "common.hpp"
 #include "kernels.hpp"
 #include "vec.hpp"
+#include "prof.hpp"
 
 namespace rat3d {
 
@@ -248,15 +249,20 @@ static rat3d_status bn_fwd_t(const BnGeom& g, int relu, float eps, float momentu
     const BnSlices sl = bn_slices(g);
     float* part = (float*)ws;
     float* coef = part + (size_t)g.C * sl.per_channel * 2;
+    const double tb = (double)g.N * g.C * g.V * sizeof(T);
+    {
+    ProfScope ps("bn_fwd_stats", st, 0.0, tb);
     bn_fwd_stats<T, VEC><<<dim3(g.C, sl.per_channel), kBnThreads, 0, st>>>(x, g.N, g.C, g.V,
                                                                           sl.len, part);
     RAT3D_LAUNCH_CHECK();
+    }
     bn_fwd_finalize<T><<<(unsigned)ceil_div(g.C, 64), 64, 0, st>>>(
         x, g.N, g.C, g.V, sl.per_channel, part, gamma, beta, eps, momentum, save_mean,
         save_invstd, run_mean, run_var, coef);
     RAT3D_LAUNCH_CHECK();
     const int64_t total = (int64_t)g.N * g.C * g.V;
     const unsigned blocks = (unsigned)ceil_div(total / VEC, kBnThreads);
+    ProfScope ps("bn_fwd_apply", st, 0.0, tb * (r ? 3 : 2));
     if (relu && r)
         bn_fwd_apply<T, VEC, true, true><<<blocks, kBnThreads, 0, st>>>(x, r, g.C, g.V, total, coef, y);
     else if (relu)
@@ -278,6 +284,9 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
     float* part = (float*)ws;
     float* coef = part + (size_t)g.C * sl.per_channel * 2;
     const dim3 sg(g.C, sl.per_channel);
+    const double tb = (double)g.N * g.C * g.V * sizeof(T);
+    {
+    ProfScope ps("bn_bwd_stats", st, 0.0, tb * (relu ? 3 : 2));
     if (relu)
         bn_bwd_stats<T, VEC, true><<<sg, kBnThreads, 0, st>>>(dy, x, y, g.N, g.C, g.V, sl.len,
                                                               save_mean, part);
@@ -285,11 +294,13 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
         bn_bwd_stats<T, VEC, false><<<sg, kBnThreads, 0, st>>>(dy, x, y, g.N, g.C, g.V, sl.len,
                                                                save_mean, part);
     RAT3D_LAUNCH_CHECK();
+    }
     bn_bwd_finalize<<<(unsigned)ceil_div(g.C, 64), 64, 0, st>>>(
         g.N, g.C, g.V, sl.per_channel, part, gamma, save_invstd, dgamma, dbeta, accumulate, coef);
     RAT3D_LAUNCH_CHECK();
     const int64_t total = (int64_t)g.N * g.C * g.V;
     const unsigned blocks = (unsigned)ceil_div(total / VEC, kBnThreads);
+    ProfScope ps("bn_bwd_apply", st, 0.0, tb * ((relu ? 4 : 3) + (dres ? 1 : 0)));
 #define RAT3D_BN_BWD(R, D)                                                                   \
     bn_bwd_apply<T, VEC, R, D><<<blocks, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, total,     \
                                                               save_mean, coef, dx, dres)

@@ -18,6 +18,7 @@
 // float32 uses four v_mfma_f32_16x16x4_f32 (4 K values per lane).
 #include "common.hpp"
 #include "kernels.hpp"
+#include "prof.hpp"
 
 namespace rat3d {
 
@@ -364,9 +365,21 @@ size_t wgrad_gather_ws(const ConvGeom& g) {
     return (size_t)wgrad_gather_splits(g) * g.Co * g.Ci * g.k * g.k * g.k * sizeof(float);
 }
 
+double conv_flops(const ConvGeom& g) {
+    return 2.0 * g.N * g.Co * g.Ci * (double)(g.k * g.k * g.k) * g.Do * g.Ho * g.Wo;
+}
+
+double conv_bytes(const ConvGeom& g, size_t esz) {
+    return (double)esz * ((double)g.N * g.Ci * g.D * g.H * g.W +
+                          (double)g.Co * g.Ci * g.k * g.k * g.k +
+                          (double)g.N * g.Co * g.Do * g.Ho * g.Wo);
+}
+
 template <typename T>
 static rat3d_status gather_fd(const ConvGeom& g, bool dgrad, const void* src, const void* w,
                               const float* bias, void* dst, int accumulate, hipStream_t st) {
+    ProfScope ps(dgrad ? "conv_gather_dgrad" : "conv_gather_fwd", st, conv_flops(g),
+                 conv_bytes(g, sizeof(T)));
     const int64_t rows = (int64_t)g.N * (dgrad ? (int64_t)g.D * g.H * g.W
                                                : (int64_t)g.Do * g.Ho * g.Wo);
     const int cols = dgrad ? g.Ci : g.Co;
@@ -403,6 +416,9 @@ rat3d_status conv_wgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* x,
     const int Ncols = g.Ci * g.k * g.k * g.k;
     dim3 grid((unsigned)ceil_div(g.Co, 64), (unsigned)ceil_div(Ncols, 64), (unsigned)real_splits);
     float* part = (float*)ws;
+    {
+    ProfScope ps("conv_gather_wgrad", st, conv_flops(g),
+                 conv_bytes(g, dt == RAT3D_BF16 ? 2 : 4));
     if (dt == RAT3D_BF16)
         conv_gather_wgrad<bf16><<<grid, 256, 0, st>>>(g, (const bf16*)x, (const bf16*)dy, part,
                                                       kchunk);
@@ -410,7 +426,9 @@ rat3d_status conv_wgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* x,
         conv_gather_wgrad<float><<<grid, 256, 0, st>>>(g, (const float*)x, (const float*)dy,
                                                        part, kchunk);
     RAT3D_LAUNCH_CHECK();
+    }
     const int64_t count = (int64_t)g.Co * Ncols;
+    ProfScope ps("wgrad_reduce", st, 0.0, 4.0 * count * (real_splits + 1 + accumulate));
     wgrad_reduce<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(part, real_splits, count, dw,
                                                                  accumulate);
     RAT3D_LAUNCH_CHECK();
@@ -420,6 +438,7 @@ rat3d_status conv_wgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* x,
 rat3d_status conv_bias_grad(const ConvGeom& g, rat3d_dtype dt, const void* dy, float* db,
                             int accumulate, hipStream_t st) {
     const int64_t Vo = (int64_t)g.Do * g.Ho * g.Wo;
+    ProfScope ps("bias_grad", st, 0.0, (dt == RAT3D_BF16 ? 2.0 : 4.0) * g.N * g.Co * Vo);
     if (dt == RAT3D_BF16)
         bias_grad<bf16><<<g.Co, 256, 0, st>>>((const bf16*)dy, g.N, g.Co, Vo, db, accumulate);
     else

@@ -2,6 +2,7 @@
 // its backward), the SGD update, and small fill/cast kernels.
 #include "common.hpp"
 #include "kernels.hpp"
+#include "prof.hpp"
 
 namespace rat3d {
 
@@ -138,6 +139,7 @@ rat3d_status head_fwd_bwd(int N, int C, int64_t V, int classes, rat3d_dtype dt, 
 rat3d_status sgd_update(int64_t count, float lr, float* params, const float* grads,
                         hipStream_t st) {
     if (count == 0) return RAT3D_OK;
+    ProfScope ps("sgd", st, 0.0, 12.0 * count);
     sgd_k<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(count, lr, params, grads);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
@@ -145,6 +147,7 @@ rat3d_status sgd_update(int64_t count, float lr, float* params, const float* gra
 
 rat3d_status cast_f32_bf16(int64_t count, const float* src, bf16* dst, hipStream_t st) {
     if (count == 0) return RAT3D_OK;
+    ProfScope ps("cast", st, 0.0, 6.0 * count);
     cast_k<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(count, src, dst);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;

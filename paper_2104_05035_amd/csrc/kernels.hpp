@@ -33,6 +33,11 @@ rat3d_status conv_wgrad(const ConvGeom& g, rat3d_dtype dt, const void* x, const 
                         float* dw, float* db, int accumulate, void* ws, size_t ws_bytes,
                         hipStream_t st);
 
+// Algorithmic work of one conv pass: 2 * N * Co * Ci * k^3 * Vout flops, and
+// one read of the input and weights plus one write of the output.
+double conv_flops(const ConvGeom& g);
+double conv_bytes(const ConvGeom& g, size_t esz);
+
 // ---- generic gather implicit GEMM (conv_gather.hip) --------------------
 rat3d_status conv_fwd_gather(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* w,
                              const float* bias, void* y, hipStream_t st);

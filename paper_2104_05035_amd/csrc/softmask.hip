@@ -6,6 +6,7 @@
 #include "common.hpp"
 #include "kernels.hpp"
 #include "vec.hpp"
+#include "prof.hpp"
 
 namespace rat3d {
 
@@ -246,6 +247,8 @@ rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, ra
     const int Do = out_dim(D, k, s, p), Ho = out_dim(H, k, s, p), Wo = out_dim(W, k, s, p);
     const int64_t total = (int64_t)N * C * Do * Ho * Wo;
     const unsigned blocks = (unsigned)ceil_div(total, kEwThreads);
+    const double es = dt == RAT3D_BF16 ? 2.0 : 4.0;
+    ProfScope ps("pool_fwd", st, 0.0, es * ((double)N * C * D * H * W + total) + total);
     if (dt == RAT3D_BF16)
         pool_fwd_k<bf16><<<blocks, kEwThreads, 0, st>>>((const bf16*)x, N * C, D, H, W, k, s, p,
                                                         Do, Ho, Wo, (bf16*)y, argmax);
@@ -262,6 +265,9 @@ rat3d_status pool_bwd(int N, int C, int D, int H, int W, int k, int s, int p, ra
     const int Do = out_dim(D, k, s, p), Ho = out_dim(H, k, s, p), Wo = out_dim(W, k, s, p);
     const int64_t total = (int64_t)N * C * D * H * W;
     const unsigned blocks = (unsigned)ceil_div(total, kEwThreads);
+    const double es = dt == RAT3D_BF16 ? 2.0 : 4.0;
+    const double small = (double)N * C * Do * Ho * Wo;
+    ProfScope ps("pool_bwd", st, 0.0, es * (small + total * (1 + accumulate)) + small);
     if (dt == RAT3D_BF16)
         pool_bwd_k<bf16><<<blocks, kEwThreads, 0, st>>>((const bf16*)dy, argmax, N * C, D, H, W,
                                                         k, s, p, Do, Ho, Wo, (bf16*)dx,
@@ -281,6 +287,8 @@ rat3d_status up_fwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
     const int64_t total = (int64_t)N * C * Do * Ho * Wo;
     const unsigned blocks = (unsigned)ceil_div(total, kEwThreads);
     const float sd = up_scale(Di, Do), sh = up_scale(Hi, Ho), sw = up_scale(Wi, Wo);
+    ProfScope ps("up_fwd", st, 0.0,
+                 (dt == RAT3D_BF16 ? 2.0 : 4.0) * ((double)N * C * Di * Hi * Wi + total));
     if (dt == RAT3D_BF16)
         up_fwd_k<bf16><<<blocks, kEwThreads, 0, st>>>((const bf16*)x, N * C, Di, Hi, Wi, Do, Ho,
                                                       Wo, sd, sh, sw, (bf16*)y);
@@ -296,6 +304,9 @@ rat3d_status up_bwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
     const int64_t total = (int64_t)N * C * Di * Hi * Wi;
     const unsigned blocks = (unsigned)ceil_div(total, kEwThreads);
     const float sd = up_scale(Di, Do), sh = up_scale(Hi, Ho), sw = up_scale(Wi, Wo);
+    ProfScope ps("up_bwd", st, 0.0,
+                 (dt == RAT3D_BF16 ? 2.0 : 4.0) *
+                     ((double)N * C * Do * Ho * Wo + total * (1 + accumulate)));
     if (dt == RAT3D_BF16)
         up_bwd_k<bf16><<<blocks, kEwThreads, 0, st>>>((const bf16*)dy, N * C, Di, Hi, Wi, Do, Ho,
                                                       Wo, sd, sh, sw, (bf16*)dx, accumulate);
@@ -309,6 +320,7 @@ rat3d_status up_bwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
 
 rat3d_status softmask_fwd(int64_t count, rat3d_dtype dt, const void* z, const void* t,
                           void* out, void* m, hipStream_t st) {
+    ProfScope ps("softmask_fwd", st, 0.0, (dt == RAT3D_BF16 ? 2.0 : 4.0) * count * (m ? 4 : 3));
     if (dt == RAT3D_BF16) {
         if (count % 8 == 0)
             softmask_fwd_k<bf16, 8><<<(unsigned)ceil_div(count / 8, kEwThreads), kEwThreads, 0,
@@ -335,6 +347,8 @@ rat3d_status softmask_fwd(int64_t count, rat3d_dtype dt, const void* z, const vo
 rat3d_status softmask_bwd(int64_t count, rat3d_dtype dt, const void* dout, const void* t,
                           const void* m, void* dt_out, int accumulate_dt, void* dz,
                           hipStream_t st) {
+    ProfScope ps("softmask_bwd", st, 0.0,
+                 (dt == RAT3D_BF16 ? 2.0 : 4.0) * count * (5 + accumulate_dt));
     if (dt == RAT3D_BF16) {
         if (count % 8 == 0)
             softmask_bwd_k<bf16, 8><<<(unsigned)ceil_div(count / 8, kEwThreads), kEwThreads, 0,
@@ -362,6 +376,7 @@ rat3d_status softmask_bwd(int64_t count, rat3d_dtype dt, const void* dout, const
 
 rat3d_status add_tensors(int64_t count, rat3d_dtype dt, const void* a, const void* b, void* dst,
                          hipStream_t st) {
+    ProfScope ps("add", st, 0.0, (dt == RAT3D_BF16 ? 2.0 : 4.0) * count * 3);
     if (dt == RAT3D_BF16) {
         if (count % 8 == 0)
             add_k<bf16, 8><<<(unsigned)ceil_div(count / 8, kEwThreads), kEwThreads, 0, st>>>(

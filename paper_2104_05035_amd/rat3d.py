@@ -96,6 +96,12 @@ _SIGS = {
     "rat3d_net_bind": (_I, [_VP, _VP, _VP, _VP, _SZ]),
     "rat3d_block_fwd_bwd": (_I, [_VP] * 6),
     "rat3d_train_step": (_I, [_VP] * 6),
+    "rat3d_profile_enable": (_I, [_I]),
+    "rat3d_profile_reset": (_I, []),
+    "rat3d_profile_count": (_I, []),
+    "rat3d_profile_read": (_I, [_I, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(_I64),
+                                ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                ctypes.POINTER(ctypes.c_double)]),
 }
 
 
@@ -245,6 +251,28 @@ def rat3d_head_fwd_bwd(n, c, v, classes, dtype, x, fc_w, fc_b, labels, logits, l
 
 def rat3d_sgd(count, lr, params, grads, stream=None):
     _check(lib().rat3d_sgd(count, lr, _p(params), _p(grads), _stream(stream)))
+
+
+# ---------------------------------------------------------------- measurement
+def rat3d_profile_enable(enable):
+    _check(lib().rat3d_profile_enable(int(enable)))
+
+
+def rat3d_profile_reset():
+    _check(lib().rat3d_profile_reset())
+
+
+def rat3d_profile_count():
+    return lib().rat3d_profile_count()
+
+
+def rat3d_profile_read(i):
+    """(tag, launches, total_ms, alg_flops, alg_bytes) of tag i (waits for its events)."""
+    name, n = ctypes.c_char_p(), _I64()
+    ms, fl, by = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(lib().rat3d_profile_read(i, ctypes.byref(name), ctypes.byref(n), ctypes.byref(ms),
+                                    ctypes.byref(fl), ctypes.byref(by)))
+    return name.value.decode(), n.value, ms.value, fl.value, by.value
 
 
 # ---------------------------------------------------------------- network
