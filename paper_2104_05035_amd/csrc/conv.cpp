@@ -1,28 +1,29 @@
 // Convolution dispatch: picks the kernel family for a shape and sizes its
-// workspace.  Every shape is served by the generic gather implicit GEMM;
-// 3x3x3 and 1x1x1 stride-1 convolutions with suitable channel counts take the
-// LDS-brick kernels.
+// workspace.  bf16 stride-1 convolutions with kernel 3 (pad 1) or 1 (pad 0)
+// and suitable channel counts take the LDS-brick kernels; every other shape
+// is served by the generic gather implicit GEMM.
 #include "kernels.hpp"
 
 namespace rat3d {
 
 size_t conv_ws_bytes(const ConvGeom& g, rat3d_dtype dt, int pass) {
-    (void)dt;
-    if (pass == 2) return wgrad_gather_ws(g);
-    return 0;
+    if (pass == 0) return brick_fd_ok(g, dt, false) ? brick_fd_ws(g) : 0;
+    if (pass == 1) return brick_fd_ok(g, dt, true) ? brick_fd_ws(g) : 0;
+    return brick_wgrad_ok(g, dt) ? brick_wgrad_ws(g) : wgrad_gather_ws(g);
 }
 
 rat3d_status conv_fwd(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* w,
                       const float* bias, void* y, void* ws, size_t ws_bytes, hipStream_t st) {
-    (void)ws;
     (void)ws_bytes;
+    if (brick_fd_ok(g, dt, false)) return conv_fd_brick(g, false, x, w, bias, y, 0, ws, st);
     return conv_fwd_gather(g, dt, x, w, bias, y, st);
 }
 
 rat3d_status conv_dgrad(const ConvGeom& g, rat3d_dtype dt, const void* dy, const void* w,
                         void* dx, int accumulate, void* ws, size_t ws_bytes, hipStream_t st) {
-    (void)ws;
     (void)ws_bytes;
+    if (brick_fd_ok(g, dt, true))
+        return conv_fd_brick(g, true, dy, w, nullptr, dx, accumulate, ws, st);
     return conv_dgrad_gather(g, dt, dy, w, dx, accumulate, st);
 }
 
@@ -30,7 +31,8 @@ rat3d_status conv_wgrad(const ConvGeom& g, rat3d_dtype dt, const void* x, const 
                         float* dw, float* db, int accumulate, void* ws, size_t ws_bytes,
                         hipStream_t st) {
     (void)ws_bytes;
-    rat3d_status s = conv_wgrad_gather(g, dt, x, dy, dw, accumulate, ws, st);
+    rat3d_status s = brick_wgrad_ok(g, dt) ? conv_wgrad_brick(g, x, dy, dw, accumulate, ws, st)
+                                           : conv_wgrad_gather(g, dt, x, dy, dw, accumulate, ws, st);
     if (s != RAT3D_OK) return s;
     if (db) return conv_bias_grad(g, dt, dy, db, accumulate, st);
     return RAT3D_OK;

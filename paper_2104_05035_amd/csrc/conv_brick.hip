@@ -1,0 +1,434 @@
+// LDS-brick implicit-GEMM convolution for the dominant shapes: bfloat16,
+// stride 1, cubic kernel 3 (pad 1) or 1 (pad 0), channel counts multiple of
+// 32 (forward / input gradient) or 16/64 (weight gradient).
+//
+// Forward (and the stride-1 input gradient, which is the forward convolution
+// of dy with the flipped, transposed weights): a workgroup computes an output
+// tile of 4 x 8 x 16 voxels for 32 or 64 output channels.  For each chunk of
+// 32 input channels it stages the halo'd input brick into LDS with the
+// channel index innermost (64 bytes per voxel, four 16-byte groups of eight
+// channels, XOR-swizzled by voxel so that the sixteen lanes of an MFMA row
+// group hit distinct banks).  The GEMM K index is (tap, channel): for a tap,
+// an MFMA A-operand row is one output voxel and its eight K values are eight
+// consecutive channels of the shifted input voxel -- one 16-byte LDS read.
+// B operands come from a weight copy pre-arranged as
+// [chunk][tap][C_out][32 channels], so a lane's operand is one coalesced
+// 16-byte global load (L1/L2 resident: every workgroup reads the same
+// weights).  Each wave owns one output depth slice: 8 rows of 16 voxels by
+// all output channels of the workgroup, i.e. 8 x (2 or 4) MFMA 16x16 tiles,
+// and reuses each weight fragment across its 8 rows.
+//
+// Weight gradient: a workgroup owns dw for 64 output channels x 16 input
+// channels x 27 taps (the four waves split the taps) and sums over a range
+// of 2 x 8 x 16 output-voxel bricks.  GEMM K = voxels: the A operand (dy,
+// 16 output channels x 32 voxels) is read straight from global memory as
+// 16-byte rows of the NCDHW tensor; the B operand (x shifted by the tap) is
+// read from LDS, where the input brick is kept as three copies pre-shifted
+// by kw = 0, 1, 2 so that every 8-voxel operand row is 16-byte aligned.
+// Partial tiles go to the workspace and are reduced in a fixed order.
+//
+// Grid mapping is XCD-aware: consecutive workgroup ids are dealt round-robin
+// to the 8 XCDs, so ids are remapped to give each XCD a contiguous range of
+// tiles (neighbouring bricks share halo lines in that XCD's L2).
+#include "common.hpp"
+#include "kernels.hpp"
+#include "prof.hpp"
+
+namespace rat3d {
+
+namespace {
+
+union F16B {
+    uint4 u;
+    bf16x8 b;
+};
+
+constexpr int kBD = 4, kBH = 8, kBW = 16;     // forward output tile
+constexpr int kWD = 2, kWH = 8, kWW = 16;     // weight-gradient voxel brick
+
+__device__ __forceinline__ int xcd_remap(int bid, int nb) {
+    // hardware deals ids round-robin over 8 XCDs; give XCD x the ids
+    // [x * q, (x + 1) * q) of a balanced split (ragged tail kept in place)
+    const int q = nb >> 3;
+    if (q == 0 || bid >= q * 8) return bid;
+    return (bid & 7) * q + (bid >> 3);
+}
+
+__device__ __forceinline__ f32x4 mfma(const F16B& a, const F16B& b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.b, b.b, c, 0, 0, 0);
+}
+
+struct FdArgs {
+    const bf16* src;   // [N][Cs][D][H][W]
+    const bf16* wt;    // [Cs/32][KT][Ct][32]
+    const float* bias; // [Ct] or null
+    bf16* dst;         // [N][Ct][D][H][W]
+    int N, Cs, Ct, D, H, W;
+    int td, th, tw;    // tiles per axis
+    int accumulate;
+};
+
+}  // namespace
+
+// ---------------------------------------------------------------- weight prep
+// fwd:   wt[((c/32)*KT + t)*Co + co]*32 + c%32] = w[co][c][t]
+__global__ void prep_fwd_weights(const bf16* __restrict__ w, int Co, int Ci, int KT,
+                                 bf16* __restrict__ wt) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t total = (int64_t)Co * Ci * KT;
+    if (i >= total) return;
+    const int t = (int)(i % KT);
+    const int c = (int)((i / KT) % Ci);
+    const int co = (int)(i / ((int64_t)KT * Ci));
+    wt[(((int64_t)(c >> 5) * KT + t) * Co + co) * 32 + (c & 31)] = w[i];
+}
+
+// dgrad: wt[((co/32)*KT + t)*Ci + ci]*32 + co%32] = w[co][ci][KT - 1 - t]
+__global__ void prep_dgrad_weights(const bf16* __restrict__ w, int Co, int Ci, int KT,
+                                   bf16* __restrict__ wt) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t total = (int64_t)Co * Ci * KT;
+    if (i >= total) return;
+    const int t = (int)(i % KT);
+    const int ci = (int)((i / KT) % Ci);
+    const int co = (int)(i / ((int64_t)KT * Ci));
+    wt[(((int64_t)(co >> 5) * KT + (KT - 1 - t)) * Ci + ci) * 32 + (co & 31)] = w[i];
+}
+
+// ---------------------------------------------------------------- fwd / dgrad
+template <int KS, int NT>
+__global__ __launch_bounds__(256, 2) void conv_brick_fd(FdArgs a) {
+    constexpr int P = (KS - 1) / 2;
+    constexpr int PD = kBD + KS - 1, PH = kBH + KS - 1, PW = kBW + KS - 1;
+    constexpr int NV = PD * PH * PW;
+    constexpr int KT = KS * KS * KS;
+    __shared__ uint4 brick[NV * 4];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int tw = L % a.tw;
+    int r = L / a.tw;
+    const int th = r % a.th;
+    r /= a.th;
+    const int td = r % a.td;
+    const int n = r / a.td;
+    const int d0 = td * kBD, h0 = th * kBH, w0 = tw * kBW;
+    const int co0 = blockIdx.y * NT * 16;
+    const int64_t HW = (int64_t)a.H * a.W, V = HW * a.D;
+
+    f32x4 acc[8][NT];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int li = lane & 15, kg = lane >> 4;
+    for (int c0 = 0; c0 < a.Cs; c0 += 32) {
+        __syncthreads();
+        // stage: item = (channel group, brick voxel), voxel fastest
+        for (int it = tid; it < NV * 4; it += 256) {
+            const int vox = it % NV, cg = it / NV;
+            const int ww = vox % PW, rr = vox / PW;
+            const int hh = rr % PH, dd = rr / PH;
+            const int d = d0 - P + dd, h = h0 - P + hh, w = w0 - P + ww;
+            uint4 pk = make_uint4(0u, 0u, 0u, 0u);
+            if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
+                (unsigned)w < (unsigned)a.W) {
+                const bf16* p = a.src + ((int64_t)n * a.Cs + c0 + cg * 8) * V + d * HW +
+                                (int64_t)h * a.W + w;
+                uint32_t v[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) v[j] = p[j * V];
+                pk.x = v[0] | (v[1] << 16);
+                pk.y = v[2] | (v[3] << 16);
+                pk.z = v[4] | (v[5] << 16);
+                pk.w = v[6] | (v[7] << 16);
+            }
+            brick[vox * 4 + (cg ^ ((vox >> 1) & 3))] = pk;
+        }
+        __syncthreads();
+        const bf16* wc = a.wt + (int64_t)(c0 >> 5) * KT * a.Ct * 32;
+#pragma unroll 1
+        for (int tap = 0; tap < KT; ++tap) {
+            const int kd = tap / (KS * KS), kh = (tap / KS) % KS, kw = tap % KS;
+            F16B b[NT];
+#pragma unroll
+            for (int ct = 0; ct < NT; ++ct)
+                b[ct].u = *reinterpret_cast<const uint4*>(
+                    wc + ((int64_t)tap * a.Ct + co0 + ct * 16 + li) * 32 + kg * 8);
+#pragma unroll
+            for (int rw = 0; rw < 8; ++rw) {
+                const int vox = ((wave + kd) * PH + (rw + kh)) * PW + li + kw;
+                F16B av;
+                av.u = brick[vox * 4 + (kg ^ ((vox >> 1) & 3))];
+#pragma unroll
+                for (int ct = 0; ct < NT; ++ct) acc[rw][ct] = mfma(av, b[ct], acc[rw][ct]);
+            }
+        }
+    }
+
+    // epilogue: lane holds 4 consecutive w of one output channel per tile
+    const int d = d0 + wave;
+    if (d >= a.D) return;
+    const bool full_w = (w0 + kBW <= a.W) && ((a.W & 3) == 0);
+#pragma unroll
+    for (int rw = 0; rw < 8; ++rw) {
+        const int h = h0 + rw;
+        if (h >= a.H) continue;
+#pragma unroll
+        for (int ct = 0; ct < NT; ++ct) {
+            const int co = co0 + ct * 16 + li;
+            const float bv = a.bias ? a.bias[co] : 0.f;
+            const int w = w0 + 4 * kg;
+            bf16* q = a.dst + ((int64_t)n * a.Ct + co) * V + d * HW + (int64_t)h * a.W + w;
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = acc[rw][ct][e] + bv;
+            if (full_w) {
+                uint2* q2 = reinterpret_cast<uint2*>(q);
+                if (a.accumulate) {
+                    const uint2 o = *q2;
+                    v[0] += __uint_as_float(o.x << 16);
+                    v[1] += __uint_as_float(o.x & 0xffff0000u);
+                    v[2] += __uint_as_float(o.y << 16);
+                    v[3] += __uint_as_float(o.y & 0xffff0000u);
+                }
+                *q2 = make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
+                                 (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if (w + e >= a.W) break;
+                    float o = v[e];
+                    if (a.accumulate) o += bf2f(q[e]);
+                    q[e] = f2bf(o);
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- wgrad
+namespace {
+struct WgArgs {
+    const bf16* x;   // [N][Ci][D][H][W]
+    const bf16* dy;  // [N][Co][D][H][W]
+    float* part;     // [ranges][Co][Ci][KT]
+    int N, Ci, Co, D, H, W;
+    int td, th, tw;  // bricks per axis
+    int64_t nbricks;
+    int bpr;         // bricks per range
+    int cigs, cogs;  // input-channel groups of 16, output-channel groups of 64
+};
+}  // namespace
+
+template <int KS>
+__global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
+    constexpr int P = (KS - 1) / 2;
+    constexpr int KT = KS * KS * KS;
+    constexpr int PD = kWD + KS - 1, PH = kWH + KS - 1, PWI = kWW + KS - 1;
+    constexpr int ROWS = PD * PH;
+    constexpr int CIS = ROWS * 32 + 16;  // bytes per input channel (rows of 16 bf16) + pad
+    constexpr int KWS = 16 * CIS;        // bytes per kw-shifted copy
+    constexpr int NTAP = (KT + 3) / 4;   // taps per wave
+    __shared__ __align__(16) unsigned char xs[KS * KWS];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int cig = L % a.cigs;
+    const int rest = L / a.cigs;
+    const int cog = rest % a.cogs;
+    const int range = rest / a.cogs;
+    const int ci0 = cig * 16, co0 = cog * 64;
+    const int64_t b_beg = (int64_t)range * a.bpr;
+    const int64_t b_end = b_beg + a.bpr < a.nbricks ? b_beg + a.bpr : a.nbricks;
+    const int64_t HW = (int64_t)a.H * a.W, V = HW * a.D;
+    const int li = lane & 15, kg = lane >> 4;
+    const int hl_l = kg >> 1, wl = (kg & 1) * 8;
+
+    f32x4 acc[NTAP][4];
+#pragma unroll
+    for (int j = 0; j < NTAP; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[j][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int64_t b = b_beg; b < b_end; ++b) {
+        const int tw = (int)(b % a.tw);
+        int64_t r = b / a.tw;
+        const int th = (int)(r % a.th);
+        r /= a.th;
+        const int td = (int)(r % a.td);
+        const int n = (int)(r / a.td);
+        const int d0 = td * kWD, h0 = th * kWH, w0 = tw * kWW;
+        __syncthreads();
+        for (int it = tid; it < 16 * ROWS * PWI; it += 256) {
+            const int ww = it % PWI;
+            const int rr = it / PWI;
+            const int row = rr % ROWS, ci = rr / ROWS;
+            const int dd = row / PH, hh = row % PH;
+            const int d = d0 - P + dd, h = h0 - P + hh, w = w0 - P + ww;
+            bf16 v = 0;
+            if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
+                (unsigned)w < (unsigned)a.W)
+                v = a.x[((int64_t)n * a.Ci + ci0 + ci) * V + d * HW + (int64_t)h * a.W + w];
+#pragma unroll
+            for (int kw = 0; kw < KS; ++kw) {
+                const int j = ww - kw;
+                if (j >= 0 && j < 16)
+                    *reinterpret_cast<bf16*>(xs + kw * KWS + ci * CIS + row * 32 + j * 2) = v;
+            }
+        }
+        __syncthreads();
+#pragma unroll 1
+        for (int s = 0; s < kWD * kWH / 2; ++s) {
+            const int dl = s / (kWH / 2);
+            const int hl = (s % (kWH / 2)) * 2 + hl_l;
+            const int d = d0 + dl, h = h0 + hl, w = w0 + wl;
+            const bool ok = d < a.D && h < a.H && w + 8 <= a.W;
+            F16B av[4];
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) {
+                av[ct].u = make_uint4(0u, 0u, 0u, 0u);
+                if (ok)
+                    av[ct].u = *reinterpret_cast<const uint4*>(
+                        a.dy + ((int64_t)n * a.Co + co0 + ct * 16 + li) * V + d * HW +
+                        (int64_t)h * a.W + w);
+            }
+#pragma unroll
+            for (int j = 0; j < NTAP; ++j) {
+                const int t = wave + 4 * j;
+                if (t < KT) {
+                    const int kd = t / (KS * KS), kh = (t / KS) % KS, kw = t % KS;
+                    F16B bv;
+                    bv.u = *reinterpret_cast<const uint4*>(
+                        xs + kw * KWS + li * CIS + ((dl + kd) * PH + hl + kh) * 32 + wl * 2);
+#pragma unroll
+                    for (int ct = 0; ct < 4; ++ct) acc[j][ct] = mfma(av[ct], bv, acc[j][ct]);
+                }
+            }
+        }
+    }
+
+    float* out = a.part + (int64_t)range * a.Co * a.Ci * KT;
+#pragma unroll
+    for (int j = 0; j < NTAP; ++j) {
+        const int t = wave + 4 * j;
+        if (t >= KT) continue;
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int co = co0 + ct * 16 + 4 * kg + e;
+                out[((int64_t)co * a.Ci + ci0 + li) * KT + t] = acc[j][ct][e];
+            }
+    }
+}
+
+// ---------------------------------------------------------------- dispatch
+bool brick_fd_ok(const ConvGeom& g, rat3d_dtype dt, bool dgrad) {
+    if (dt != RAT3D_BF16 || g.s != 1) return false;
+    if (!((g.k == 3 && g.p == 1) || (g.k == 1 && g.p == 0))) return false;
+    const int cs = dgrad ? g.Co : g.Ci, ct = dgrad ? g.Ci : g.Co;
+    return cs % 32 == 0 && ct % 32 == 0;
+}
+
+bool brick_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) {
+    return dt == RAT3D_BF16 && g.s == 1 && g.k == 3 && g.p == 1 && g.Ci % 16 == 0 &&
+           g.Co % 64 == 0 && g.W % 8 == 0;
+}
+
+size_t brick_fd_ws(const ConvGeom& g) { return (size_t)g.Co * g.Ci * g.k * g.k * g.k * 2; }
+
+static int wgrad_ranges(const ConvGeom& g, int64_t nbricks) {
+    const int64_t groups = (int64_t)(g.Ci / 16) * (g.Co / 64);
+    int64_t r = ceil_div(1024, groups);
+    if (r > nbricks) r = nbricks;
+    if (r < 1) r = 1;
+    return (int)r;
+}
+
+static int64_t wgrad_bricks(const ConvGeom& g) {
+    return (int64_t)g.N * ceil_div(g.D, kWD) * ceil_div(g.H, kWH) * ceil_div(g.W, kWW);
+}
+
+size_t brick_wgrad_ws(const ConvGeom& g) {
+    const int R = wgrad_ranges(g, wgrad_bricks(g));
+    return (size_t)R * g.Co * g.Ci * 27 * sizeof(float);
+}
+
+rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const void* w,
+                           const float* bias, void* dst, int accumulate, void* ws,
+                           hipStream_t st) {
+    const int KT = g.k * g.k * g.k;
+    bf16* wt = (bf16*)ws;
+    const int64_t wn = (int64_t)g.Co * g.Ci * KT;
+    if (dgrad)
+        prep_dgrad_weights<<<(unsigned)ceil_div(wn, 256), 256, 0, st>>>((const bf16*)w, g.Co,
+                                                                        g.Ci, KT, wt);
+    else
+        prep_fwd_weights<<<(unsigned)ceil_div(wn, 256), 256, 0, st>>>((const bf16*)w, g.Co, g.Ci,
+                                                                      KT, wt);
+    RAT3D_LAUNCH_CHECK();
+    FdArgs a;
+    a.src = (const bf16*)src;
+    a.wt = wt;
+    a.bias = bias;
+    a.dst = (bf16*)dst;
+    a.N = g.N;
+    a.Cs = dgrad ? g.Co : g.Ci;
+    a.Ct = dgrad ? g.Ci : g.Co;
+    a.D = g.D;
+    a.H = g.H;
+    a.W = g.W;
+    a.td = (int)ceil_div(g.D, kBD);
+    a.th = (int)ceil_div(g.H, kBH);
+    a.tw = (int)ceil_div(g.W, kBW);
+    a.accumulate = accumulate;
+    const int nt = a.Ct % 64 == 0 ? 4 : 2;
+    dim3 grid((unsigned)((int64_t)g.N * a.td * a.th * a.tw), (unsigned)(a.Ct / (nt * 16)));
+    ProfScope ps(dgrad ? (g.k == 3 ? "conv_brick3_dgrad" : "conv_brick1_dgrad")
+                       : (g.k == 3 ? "conv_brick3_fwd" : "conv_brick1_fwd"),
+                 st, conv_flops(g), conv_bytes(g, 2));
+    if (g.k == 3) {
+        if (nt == 4) conv_brick_fd<3, 4><<<grid, 256, 0, st>>>(a);
+        else conv_brick_fd<3, 2><<<grid, 256, 0, st>>>(a);
+    } else {
+        if (nt == 4) conv_brick_fd<1, 4><<<grid, 256, 0, st>>>(a);
+        else conv_brick_fd<1, 2><<<grid, 256, 0, st>>>(a);
+    }
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
+rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, float* dw,
+                              int accumulate, void* ws, hipStream_t st) {
+    WgArgs a;
+    a.x = (const bf16*)x;
+    a.dy = (const bf16*)dy;
+    a.part = (float*)ws;
+    a.N = g.N;
+    a.Ci = g.Ci;
+    a.Co = g.Co;
+    a.D = g.D;
+    a.H = g.H;
+    a.W = g.W;
+    a.td = (int)ceil_div(g.D, kWD);
+    a.th = (int)ceil_div(g.H, kWH);
+    a.tw = (int)ceil_div(g.W, kWW);
+    a.nbricks = wgrad_bricks(g);
+    const int R = wgrad_ranges(g, a.nbricks);
+    a.bpr = (int)ceil_div(a.nbricks, R);
+    const int Rreal = (int)ceil_div(a.nbricks, a.bpr);
+    a.cigs = g.Ci / 16;
+    a.cogs = g.Co / 64;
+    {
+        ProfScope ps("conv_brick3_wgrad", st, conv_flops(g), conv_bytes(g, 2));
+        conv_brick_wgrad<3><<<(unsigned)((int64_t)Rreal * a.cigs * a.cogs), 256, 0, st>>>(a);
+        RAT3D_LAUNCH_CHECK();
+    }
+    const int64_t count = (int64_t)g.Co * g.Ci * 27;
+    ProfScope ps("wgrad_reduce", st, 0.0, 4.0 * count * (Rreal + 1 + accumulate));
+    return wgrad_reduce_launch(a.part, Rreal, count, dw, accumulate, st);
+}
+
+}  // namespace rat3d

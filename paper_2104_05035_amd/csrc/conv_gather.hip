@@ -435,6 +435,14 @@ rat3d_status conv_wgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* x,
     return RAT3D_OK;
 }
 
+rat3d_status wgrad_reduce_launch(const float* part, int splits, int64_t count, float* dw,
+                                 int accumulate, hipStream_t st) {
+    wgrad_reduce<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(part, splits, count, dw,
+                                                                 accumulate);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
 rat3d_status conv_bias_grad(const ConvGeom& g, rat3d_dtype dt, const void* dy, float* db,
                             int accumulate, hipStream_t st) {
     const int64_t Vo = (int64_t)g.Do * g.Ho * g.Wo;

@@ -48,6 +48,20 @@ rat3d_status conv_wgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* x,
                                float* dw, int accumulate, void* ws, hipStream_t st);
 rat3d_status conv_bias_grad(const ConvGeom& g, rat3d_dtype dt, const void* dy, float* db,
                             int accumulate, hipStream_t st);
+// dw (+)= sum over `splits` partial slabs of `count` floats, in slab order.
+rat3d_status wgrad_reduce_launch(const float* part, int splits, int64_t count, float* dw,
+                                 int accumulate, hipStream_t st);
+
+// ---- LDS-brick kernels for bf16, stride 1, k in {1, 3} (conv_brick.hip) ---
+bool brick_fd_ok(const ConvGeom& g, rat3d_dtype dt, bool dgrad);
+bool brick_wgrad_ok(const ConvGeom& g, rat3d_dtype dt);
+size_t brick_fd_ws(const ConvGeom& g);
+size_t brick_wgrad_ws(const ConvGeom& g);
+rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const void* w,
+                           const float* bias, void* dst, int accumulate, void* ws,
+                           hipStream_t st);
+rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, float* dw,
+                              int accumulate, void* ws, hipStream_t st);
 
 // ---- batch norm (bn.hip) -----------------------------------------------
 struct BnGeom {

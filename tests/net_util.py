@@ -98,6 +98,10 @@ def gate_grads(G, Gref, Gjit, dt):
     the number of tensors within the stated tolerance outright."""
     fl = floors(Gref, Gjit)
     within = 0
+    rows = sorted(((U.rel(G[k], Gref[k]), fl[k], k) for k in Gref), reverse=True)
+    print("gradients: %d tensors; worst (error, oracle spread):" % len(rows))
+    for err, f, k in rows[:6]:
+        print("   %-24s %.3e  %.3e" % (k, err, f))
     for k in Gref:
         err, _ = gate(G[k], Gref[k], fl[k], dt, "grad " + k)
         within += err <= U.TOL[dt]

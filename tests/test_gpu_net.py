@@ -4,8 +4,10 @@ module and the full network at their full workload sizes, the first-stage
 partition at a reduced volume (its full size is covered by
 tests/test_gpu_full.py), plus reduced and ragged blocks.
 
-Gates.  Forward outputs (block output, logits, loss, partition output) must
-be within the stated tolerance (1e-4 float32, 2e-2 bfloat16) outright.  The
+Gates.  Block and partition outputs must be within the stated tolerance
+(1e-4 float32, 2e-2 bfloat16) outright; the full network's logits and loss,
+like the gradients below, are gated against the oracle's noise floor (its
+deepest mask branch normalises over 2-64 values).  The
 step is only piecewise smooth (ReLU masks, first-maximum pooling), so some
 gradients -- BN parameters and convolutions deep in the mask branch, whose
 incoming gradient has been made zero-mean by a BN backward -- move by more
@@ -94,11 +96,11 @@ def test_attn_workload():
     _block("attn", R.NET_ATTN, 4, 64, 48, 48, 48, "bf16", 2)
 
 
-def _resattnet(n, d, h, w, seed):
+def _resattnet(n, d, h, w, seed, dt="bf16"):
     rng, rx, rl = synth.streams(seed, 3)
-    B = Bound(R.NET_RESATTNET, n, 1, 32, d, h, w, "bf16", rng)
+    B = Bound(R.NET_RESATTNET, n, 1, 32, d, h, w, dt, rng)
     vol = synth.mri_volumes(rx, n, (d, h, w))
-    x, xr = U.dev_input(vol, "bf16")
+    x, xr = U.dev_input(vol, dt)
     lab = rl.integers(0, 2, n).astype(np.int32)
     torch = U.torch_mod()
     labels = U.to_dev(torch.from_numpy(lab))
@@ -106,19 +108,28 @@ def _resattnet(n, d, h, w, seed):
     old = {k: v.copy() for k, v in B.params.items()}
     B.net.rat3d_train_step(x, labels, None, loss)
     U.sync()
-    new, Gref, info = onet.train_step("resattnet", B.params, 1e-4, True, x=xr, labels=lab)
-    jit = [onet.train_step("resattnet", B.params, 1e-4, True, x=xr, labels=lab,
-                           jitter=(JITTER, s))[1] for s in (1, 2)]
+    bf = dt == "bf16"
+    new, Gref, info = onet.train_step("resattnet", B.params, 1e-4, bf, x=xr, labels=lab)
+    jruns = [onet.train_step("resattnet", B.params, 1e-4, bf, x=xr, labels=lab,
+                             jitter=(JITTER, s)) for s in (1, 2)]
     G = B.grads()
-    assert abs(float(U.f64(loss)[0]) - info["loss"]) <= 2e-2 * abs(info["loss"])
-    U.check(B.tensor("logits").reshape(n, 2), info["logits"], "bf16", "logits")
-    gate_grads(G, Gref, jit, "bf16")
+    # the third stage's mask branch normalises over as few as 2-64 values, so
+    # even the logits move by percents under rounding-level noise
+    lspread = max(U.rel(j[2]["logits"], info["logits"]) for j in jruns)
+    gate(B.tensor("logits").reshape(n, 2), info["logits"], lspread, dt, "logits")
+    # the loss of confident logits (loss ~ exp(-margin)) amplifies their noise
+    spread = max(abs(j[2]["loss"] - info["loss"]) / abs(info["loss"]) for j in jruns)
+    gate(np.array([float(U.f64(loss)[0])]), np.array([info["loss"]]), spread, dt, "loss")
+    gate_grads(G, Gref, [j[1] for j in jruns], dt)
     check_sgd(old, B.new_params(), G, 1e-4)
 
 
-def test_resattnet_reduced():
-    """Full network step on 2 volumes of 48x56x48 (same graph, smaller maps)."""
-    _resattnet(2, 48, 56, 48, 23)
+def test_resattnet_reduced_f32():
+    """Full network step on 2 volumes of 48x56x48 in float32 (same graph,
+    smaller maps).  At this size the third stage's mask branch reaches 1x1x1
+    and normalises over 2 values, so its bf16 rounding differences are
+    amplified up to 1/sqrt(eps); float32 keeps the check meaningful."""
+    _resattnet(2, 48, 56, 48, 23, "f32")
 
 
 @pytest.mark.timeout(900)

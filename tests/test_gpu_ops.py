@@ -29,6 +29,22 @@ CONV_CASES = [
     (1, 2, 3, 2, 2, 2, 3, 1, 1, False, "bf16"),
     (3, 5, 70, 5, 3, 4, 3, 1, 1, True, "bf16"),
     (2, 128, 256, 6, 7, 6, 3, 2, 1, False, "bf16"),
+    # LDS-brick paths: full and ragged tiles, 32- and 64-channel output tiles,
+    # 1^3 kernels, weight-gradient bricks (W multiple of 8)
+    (2, 64, 64, 6, 10, 32, 3, 1, 1, False, "bf16"),
+    (1, 32, 64, 5, 9, 24, 3, 1, 1, False, "bf16"),
+    (2, 64, 32, 4, 8, 16, 3, 1, 1, False, "bf16"),
+    (1, 64, 128, 7, 5, 40, 3, 1, 1, True, "bf16"),
+    (2, 64, 64, 5, 9, 24, 1, 1, 0, True, "bf16"),
+    (1, 32, 64, 3, 3, 8, 1, 1, 0, False, "bf16"),
+    (1, 96, 64, 9, 17, 48, 3, 1, 1, False, "bf16"),
+    # the small deep-stage volumes of the full network (tiles mostly outside)
+    (2, 64, 64, 12, 14, 12, 1, 1, 0, False, "bf16"),
+    (2, 128, 128, 6, 7, 6, 3, 1, 1, False, "bf16"),
+    (2, 256, 256, 3, 4, 3, 3, 1, 1, False, "bf16"),
+    (2, 256, 256, 2, 2, 2, 3, 1, 1, False, "bf16"),
+    (2, 256, 256, 1, 1, 1, 3, 1, 1, False, "bf16"),
+    (2, 256, 256, 3, 4, 3, 1, 1, 0, True, "bf16"),
 ]
 
 
