@@ -9,7 +9,9 @@ namespace rat3d {
 size_t conv_ws_bytes(const ConvGeom& g, rat3d_dtype dt, int pass) {
     if (pass == 0) return brick_fd_ok(g, dt, false) ? brick_fd_ws(g) : 0;
     if (pass == 1) return brick_fd_ok(g, dt, true) ? brick_fd_ws(g) : 0;
-    return brick_wgrad_ok(g, dt) ? brick_wgrad_ws(g) : wgrad_gather_ws(g);
+    // weight-gradient partials, then the bias-gradient slice sums
+    const size_t wb = brick_wgrad_ok(g, dt) ? brick_wgrad_ws(g) : wgrad_gather_ws(g);
+    return ((wb + 255) & ~(size_t)255) + bias_grad_ws(g);
 }
 
 rat3d_status conv_fwd(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* w,
@@ -34,7 +36,11 @@ rat3d_status conv_wgrad(const ConvGeom& g, rat3d_dtype dt, const void* x, const 
     rat3d_status s = brick_wgrad_ok(g, dt) ? conv_wgrad_brick(g, x, dy, dw, accumulate, ws, st)
                                            : conv_wgrad_gather(g, dt, x, dy, dw, accumulate, ws, st);
     if (s != RAT3D_OK) return s;
-    if (db) return conv_bias_grad(g, dt, dy, db, accumulate, st);
+    if (db) {
+        const size_t wb = brick_wgrad_ok(g, dt) ? brick_wgrad_ws(g) : wgrad_gather_ws(g);
+        return conv_bias_grad(g, dt, dy, db, accumulate,
+                              (char*)ws + ((wb + 255) & ~(size_t)255), st);
+    }
     return RAT3D_OK;
 }
 

@@ -125,45 +125,94 @@ __global__ __launch_bounds__(256, 2) void conv_brick_fd(FdArgs a) {
     const int li = lane & 15, kg = lane >> 4;
     for (int c0 = 0; c0 < a.Cs; c0 += 32) {
         __syncthreads();
-        // stage: item = (channel group, brick voxel), voxel fastest
-        for (int it = tid; it < NV * 4; it += 256) {
-            const int vox = it % NV, cg = it / NV;
-            const int ww = vox % PW, rr = vox / PW;
-            const int hh = rr % PH, dd = rr / PH;
-            const int d = d0 - P + dd, h = h0 - P + hh, w = w0 - P + ww;
-            uint4 pk = make_uint4(0u, 0u, 0u, 0u);
-            if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
-                (unsigned)w < (unsigned)a.W) {
-                const bf16* p = a.src + ((int64_t)n * a.Cs + c0 + cg * 8) * V + d * HW +
-                                (int64_t)h * a.W + w;
-                uint32_t v[8];
+        if (a.W % 4 == 0) {
+            // item = (channel group, brick row, aligned 4-wide column group):
+            // eight 8-byte loads (one per channel) give 4 voxels x 8 channels
+            constexpr int GS0 = -4 * ((P + 3) / 4);          // first group, relative to w0
+            constexpr int NG = (PW - P - GS0 + 3) / 4;       // groups covering the brick row
+            for (int it = tid; it < 4 * PD * PH * NG; it += 256) {
+                const int q = it % NG;
+                const int rr = it / NG;
+                const int row = rr % (PD * PH), cg = rr / (PD * PH);
+                const int hh = row % PH, dd = row / PH;
+                const int d = d0 - P + dd, h = h0 - P + hh, wg = w0 + GS0 + 4 * q;
+                uint2 v[8];
+                if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
+                    (unsigned)wg < (unsigned)a.W) {
+                    const bf16* p = a.src + ((int64_t)n * a.Cs + c0 + cg * 8) * V + d * HW +
+                                    (int64_t)h * a.W + wg;
 #pragma unroll
-                for (int j = 0; j < 8; ++j) v[j] = p[j * V];
-                pk.x = v[0] | (v[1] << 16);
-                pk.y = v[2] | (v[3] << 16);
-                pk.z = v[4] | (v[5] << 16);
-                pk.w = v[6] | (v[7] << 16);
+                    for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const uint2*>(p + j * V);
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) v[j] = make_uint2(0u, 0u);
+                }
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int ww = wg + e - (w0 - P);
+                    if (ww < 0 || ww >= PW) continue;
+                    const int vox = (dd * PH + hh) * PW + ww;
+                    uint32_t c[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const uint32_t word = (e < 2) ? v[j].x : v[j].y;
+                        c[j] = (e & 1) ? (word >> 16) : (word & 0xffffu);
+                    }
+                    brick[vox * 4 + (cg ^ ((vox >> 1) & 3))] =
+                        make_uint4(c[0] | (c[1] << 16), c[2] | (c[3] << 16), c[4] | (c[5] << 16),
+                                   c[6] | (c[7] << 16));
+                }
             }
-            brick[vox * 4 + (cg ^ ((vox >> 1) & 3))] = pk;
+        } else {
+            // item = (channel group, brick voxel), voxel fastest
+            for (int it = tid; it < NV * 4; it += 256) {
+                const int vox = it % NV, cg = it / NV;
+                const int ww = vox % PW, rr = vox / PW;
+                const int hh = rr % PH, dd = rr / PH;
+                const int d = d0 - P + dd, h = h0 - P + hh, w = w0 - P + ww;
+                uint4 pk = make_uint4(0u, 0u, 0u, 0u);
+                if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
+                    (unsigned)w < (unsigned)a.W) {
+                    const bf16* p = a.src + ((int64_t)n * a.Cs + c0 + cg * 8) * V + d * HW +
+                                    (int64_t)h * a.W + w;
+                    uint32_t v[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) v[j] = p[j * V];
+                    pk.x = v[0] | (v[1] << 16);
+                    pk.y = v[2] | (v[3] << 16);
+                    pk.z = v[4] | (v[5] << 16);
+                    pk.w = v[6] | (v[7] << 16);
+                }
+                brick[vox * 4 + (cg ^ ((vox >> 1) & 3))] = pk;
+            }
         }
         __syncthreads();
         const bf16* wc = a.wt + (int64_t)(c0 >> 5) * KT * a.Ct * 32;
+        // weight fragments are double-buffered: tap t+1 loads while tap t multiplies
+        F16B bc[NT];
+#pragma unroll
+        for (int ct = 0; ct < NT; ++ct)
+            bc[ct].u = *reinterpret_cast<const uint4*>(wc + ((int64_t)(co0 + ct * 16 + li)) * 32 +
+                                                        kg * 8);
 #pragma unroll 1
         for (int tap = 0; tap < KT; ++tap) {
             const int kd = tap / (KS * KS), kh = (tap / KS) % KS, kw = tap % KS;
-            F16B b[NT];
+            F16B bn[NT];
+            const int tn = tap + 1 < KT ? tap + 1 : tap;
 #pragma unroll
             for (int ct = 0; ct < NT; ++ct)
-                b[ct].u = *reinterpret_cast<const uint4*>(
-                    wc + ((int64_t)tap * a.Ct + co0 + ct * 16 + li) * 32 + kg * 8);
+                bn[ct].u = *reinterpret_cast<const uint4*>(
+                    wc + ((int64_t)tn * a.Ct + co0 + ct * 16 + li) * 32 + kg * 8);
 #pragma unroll
             for (int rw = 0; rw < 8; ++rw) {
                 const int vox = ((wave + kd) * PH + (rw + kh)) * PW + li + kw;
                 F16B av;
                 av.u = brick[vox * 4 + (kg ^ ((vox >> 1) & 3))];
 #pragma unroll
-                for (int ct = 0; ct < NT; ++ct) acc[rw][ct] = mfma(av, b[ct], acc[rw][ct]);
+                for (int ct = 0; ct < NT; ++ct) acc[rw][ct] = mfma(av, bc[ct], acc[rw][ct]);
             }
+#pragma unroll
+            for (int ct = 0; ct < NT; ++ct) bc[ct] = bn[ct];
         }
     }
 
@@ -226,7 +275,8 @@ template <int KS>
 __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
     constexpr int P = (KS - 1) / 2;
     constexpr int KT = KS * KS * KS;
-    constexpr int PD = kWD + KS - 1, PH = kWH + KS - 1, PWI = kWW + KS - 1;
+    static_assert(KS == 3, "the weight-gradient brick assembles kw = 0, 1, 2 copies");
+    constexpr int PD = kWD + KS - 1, PH = kWH + KS - 1;
     constexpr int ROWS = PD * PH;
     constexpr int CIS = ROWS * 32 + 16;  // bytes per input channel (rows of 16 bf16) + pad
     constexpr int KWS = 16 * CIS;        // bytes per kw-shifted copy
@@ -261,31 +311,56 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
         const int n = (int)(r / a.td);
         const int d0 = td * kWD, h0 = th * kWH, w0 = tw * kWW;
         __syncthreads();
-        for (int it = tid; it < 16 * ROWS * PWI; it += 256) {
-            const int ww = it % PWI;
-            const int rr = it / PWI;
-            const int row = rr % ROWS, ci = rr / ROWS;
+        // item = (input channel, brick row): the row's 16 aligned voxels come in
+        // as two 16-byte loads plus one halo voxel on each side; the three
+        // kw-shifted copies are assembled in registers and stored as aligned
+        // 16-byte LDS rows (copy kw holds input columns w0 - 1 + kw ...).
+        for (int it = tid; it < 16 * ROWS; it += 256) {
+            const int row = it % ROWS, ci = it / ROWS;
             const int dd = row / PH, hh = row % PH;
-            const int d = d0 - P + dd, h = h0 - P + hh, w = w0 - P + ww;
-            bf16 v = 0;
-            if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
-                (unsigned)w < (unsigned)a.W)
-                v = a.x[((int64_t)n * a.Ci + ci0 + ci) * V + d * HW + (int64_t)h * a.W + w];
+            const int d = d0 - P + dd, h = h0 - P + hh;
+            uint32_t m[10];  // m[0] = (?, x[w0-1]), m[1..8] = x[w0..w0+15], m[9] = (x[w0+16], ?)
 #pragma unroll
-            for (int kw = 0; kw < KS; ++kw) {
-                const int j = ww - kw;
-                if (j >= 0 && j < 16)
-                    *reinterpret_cast<bf16*>(xs + kw * KWS + ci * CIS + row * 32 + j * 2) = v;
+            for (int j = 0; j < 10; ++j) m[j] = 0u;
+            if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H) {
+                const bf16* p = a.x + ((int64_t)n * a.Ci + ci0 + ci) * V + d * HW +
+                                (int64_t)h * a.W + w0;
+                if (w0 + 8 <= a.W) {
+                    const uint4 u = *reinterpret_cast<const uint4*>(p);
+                    m[1] = u.x; m[2] = u.y; m[3] = u.z; m[4] = u.w;
+                }
+                if (w0 + 16 <= a.W) {
+                    const uint4 u = *reinterpret_cast<const uint4*>(p + 8);
+                    m[5] = u.x; m[6] = u.y; m[7] = u.z; m[8] = u.w;
+                }
+                if (w0 >= 1) m[0] = (uint32_t)p[-1] << 16;
+                if (w0 + 16 < a.W) m[9] = (uint32_t)p[16];
             }
+            unsigned char* base = xs + ci * CIS + row * 32;
+            // kw = 1: columns w0 .. w0+15 (aligned)
+            *reinterpret_cast<uint4*>(base + KWS) = make_uint4(m[1], m[2], m[3], m[4]);
+            *reinterpret_cast<uint4*>(base + KWS + 16) = make_uint4(m[5], m[6], m[7], m[8]);
+            // kw = 0: columns w0-1 .. w0+14: dword i = (hi of m[i], lo of m[i+1])
+            uint32_t s0[8], s2[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                s0[i] = (m[i] >> 16) | (m[i + 1] << 16);
+                s2[i] = (m[i + 1] >> 16) | (m[i + 2] << 16);
+            }
+            *reinterpret_cast<uint4*>(base) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
+            *reinterpret_cast<uint4*>(base + 16) = make_uint4(s0[4], s0[5], s0[6], s0[7]);
+            // kw = 2: columns w0+1 .. w0+16
+            *reinterpret_cast<uint4*>(base + 2 * KWS) = make_uint4(s2[0], s2[1], s2[2], s2[3]);
+            *reinterpret_cast<uint4*>(base + 2 * KWS + 16) = make_uint4(s2[4], s2[5], s2[6], s2[7]);
         }
         __syncthreads();
-#pragma unroll 1
-        for (int s = 0; s < kWD * kWH / 2; ++s) {
+        // K step s covers rows (h0 + 2*(s%4) + {0,1}) of depth d0 + s/4; dy
+        // rows for step s+1 are fetched while step s multiplies
+        auto load_a = [&](int s, F16B (&av)[4]) {
             const int dl = s / (kWH / 2);
             const int hl = (s % (kWH / 2)) * 2 + hl_l;
             const int d = d0 + dl, h = h0 + hl, w = w0 + wl;
             const bool ok = d < a.D && h < a.H && w + 8 <= a.W;
-            F16B av[4];
 #pragma unroll
             for (int ct = 0; ct < 4; ++ct) {
                 av[ct].u = make_uint4(0u, 0u, 0u, 0u);
@@ -294,6 +369,15 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
                         a.dy + ((int64_t)n * a.Co + co0 + ct * 16 + li) * V + d * HW +
                         (int64_t)h * a.W + w);
             }
+        };
+        F16B ac[4];
+        load_a(0, ac);
+#pragma unroll 1
+        for (int s = 0; s < kWD * kWH / 2; ++s) {
+            F16B an[4];
+            load_a(s + 1 < kWD * kWH / 2 ? s + 1 : s, an);
+            const int dl = s / (kWH / 2);
+            const int hl = (s % (kWH / 2)) * 2 + hl_l;
 #pragma unroll
             for (int j = 0; j < NTAP; ++j) {
                 const int t = wave + 4 * j;
@@ -303,9 +387,11 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
                     bv.u = *reinterpret_cast<const uint4*>(
                         xs + kw * KWS + li * CIS + ((dl + kd) * PH + hl + kh) * 32 + wl * 2);
 #pragma unroll
-                    for (int ct = 0; ct < 4; ++ct) acc[j][ct] = mfma(av[ct], bv, acc[j][ct]);
+                    for (int ct = 0; ct < 4; ++ct) acc[j][ct] = mfma(ac[ct], bv, acc[j][ct]);
                 }
             }
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) ac[ct] = an[ct];
         }
     }
 
@@ -340,8 +426,9 @@ bool brick_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) {
 size_t brick_fd_ws(const ConvGeom& g) { return (size_t)g.Co * g.Ci * g.k * g.k * g.k * 2; }
 
 static int wgrad_ranges(const ConvGeom& g, int64_t nbricks) {
+    // about two workgroups per CU in one wave (256 CUs, 2 resident each)
     const int64_t groups = (int64_t)(g.Ci / 16) * (g.Co / 64);
-    int64_t r = ceil_div(1024, groups);
+    int64_t r = ceil_div(512, groups);
     if (r > nbricks) r = nbricks;
     if (r < 1) r = 1;
     return (int)r;

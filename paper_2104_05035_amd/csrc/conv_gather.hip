@@ -317,36 +317,73 @@ __global__ __launch_bounds__(256) void conv_gather_wgrad(ConvGeom g, const T* __
             }
 }
 
-// Sums `splits` partial weight-gradient tiles in split order into dw.
+// Sums `splits` partial weight-gradient slabs in split order into dw; four
+// consecutive elements per thread (count is a multiple of 4 on that path).
+__global__ void wgrad_reduce4(const float4* __restrict__ part, int splits, int64_t count4,
+                              float4* __restrict__ dw, int accumulate) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= count4) return;
+    float4 s = accumulate ? dw[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+    for (int z = 0; z < splits; ++z) {
+        const float4 v = part[(int64_t)z * count4 + i];
+        s.x += v.x;
+        s.y += v.y;
+        s.z += v.z;
+        s.w += v.w;
+    }
+    dw[i] = s;
+}
+
 __global__ void wgrad_reduce(const float* __restrict__ part, int splits, int64_t count,
                              float* __restrict__ dw, int accumulate) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= count) return;
     float s = accumulate ? dw[i] : 0.f;
+#pragma unroll 8
     for (int z = 0; z < splits; ++z) s += part[(int64_t)z * count + i];
     dw[i] = s;
 }
 
-// dbias[c] (+)= sum over n and voxels of dy[n, c, :].  One block per channel;
-// fixed-shape tree reduction.
+// dbias: stage 1 sums one segment of one (n, c) plane per block (each plane
+// split into SP segments), stage 2 adds each channel's N*SP segment sums in
+// order.
+static int bias_segments(const ConvGeom& g) {
+    const int sp = (int)ceil_div(64, g.N);
+    return sp < 1 ? 1 : sp;
+}
+
 template <typename T>
-__global__ __launch_bounds__(256) void bias_grad(const T* __restrict__ dy, int N, int C,
-                                                 int64_t V, float* __restrict__ db,
-                                                 int accumulate) {
+__global__ __launch_bounds__(256) void bias_grad_part(const T* __restrict__ dy, int C, int64_t V,
+                                                      int SP, float* __restrict__ part) {
     __shared__ float red[256];
-    const int c = blockIdx.x;
+    const int c = blockIdx.x, sl = blockIdx.y;  // sl = n * SP + segment
+    const int n = sl / SP, seg = sl - n * SP;
+    const int64_t len = (V + SP - 1) / SP;
+    const int64_t beg = seg * len, end = beg + len < V ? beg + len : V;
+    const T* p = dy + ((int64_t)n * C + c) * V;
     float s = 0.f;
-    for (int n = 0; n < N; ++n) {
-        const T* p = dy + ((int64_t)n * C + c) * V;
-        for (int64_t i = threadIdx.x; i < V; i += 256) s += Elt<T>::ld(p + i);
-    }
+    for (int64_t e = beg + threadIdx.x; e < end; e += 256) s += Elt<T>::ld(p + e);
     red[threadIdx.x] = s;
     __syncthreads();
     for (int w = 128; w > 0; w >>= 1) {
         if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
         __syncthreads();
     }
-    if (threadIdx.x == 0) db[c] = (accumulate ? db[c] : 0.f) + red[0];
+    if (threadIdx.x == 0) part[(int64_t)c * gridDim.y + sl] = red[0];
+}
+
+__global__ void bias_grad_final(const float* __restrict__ part, int C, int S,
+                                float* __restrict__ db, int accumulate) {
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= C) return;
+    float s = accumulate ? db[c] : 0.f;
+    for (int i = 0; i < S; ++i) s += part[(int64_t)c * S + i];
+    db[c] = s;
+}
+
+size_t bias_grad_ws(const ConvGeom& g) {
+    return (size_t)g.Co * g.N * bias_segments(g) * sizeof(float);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -429,28 +466,35 @@ rat3d_status conv_wgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* x,
     }
     const int64_t count = (int64_t)g.Co * Ncols;
     ProfScope ps("wgrad_reduce", st, 0.0, 4.0 * count * (real_splits + 1 + accumulate));
-    wgrad_reduce<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(part, real_splits, count, dw,
-                                                                 accumulate);
-    RAT3D_LAUNCH_CHECK();
-    return RAT3D_OK;
+    return wgrad_reduce_launch(part, real_splits, count, dw, accumulate, st);
 }
 
 rat3d_status wgrad_reduce_launch(const float* part, int splits, int64_t count, float* dw,
                                  int accumulate, hipStream_t st) {
-    wgrad_reduce<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(part, splits, count, dw,
-                                                                 accumulate);
+    if (count % 4 == 0 && ((uintptr_t)dw & 15u) == 0 && ((uintptr_t)part & 15u) == 0)
+        wgrad_reduce4<<<(unsigned)ceil_div(count / 4, 256), 256, 0, st>>>(
+            (const float4*)part, splits, count / 4, (float4*)dw, accumulate);
+    else
+        wgrad_reduce<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(part, splits, count, dw,
+                                                                     accumulate);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }
 
 rat3d_status conv_bias_grad(const ConvGeom& g, rat3d_dtype dt, const void* dy, float* db,
-                            int accumulate, hipStream_t st) {
+                            int accumulate, void* ws, hipStream_t st) {
     const int64_t Vo = (int64_t)g.Do * g.Ho * g.Wo;
+    float* part = (float*)ws;
     ProfScope ps("bias_grad", st, 0.0, (dt == RAT3D_BF16 ? 2.0 : 4.0) * g.N * g.Co * Vo);
+    const int SP = bias_segments(g);
+    const dim3 grid(g.Co, g.N * SP);
     if (dt == RAT3D_BF16)
-        bias_grad<bf16><<<g.Co, 256, 0, st>>>((const bf16*)dy, g.N, g.Co, Vo, db, accumulate);
+        bias_grad_part<bf16><<<grid, 256, 0, st>>>((const bf16*)dy, g.Co, Vo, SP, part);
     else
-        bias_grad<float><<<g.Co, 256, 0, st>>>((const float*)dy, g.N, g.Co, Vo, db, accumulate);
+        bias_grad_part<float><<<grid, 256, 0, st>>>((const float*)dy, g.Co, Vo, SP, part);
+    RAT3D_LAUNCH_CHECK();
+    bias_grad_final<<<(unsigned)ceil_div(g.Co, 64), 64, 0, st>>>(part, g.Co, g.N * SP, db,
+                                                                 accumulate);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }

@@ -46,8 +46,9 @@ rat3d_status conv_dgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* dy
 size_t wgrad_gather_ws(const ConvGeom& g);
 rat3d_status conv_wgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* dy,
                                float* dw, int accumulate, void* ws, hipStream_t st);
+size_t bias_grad_ws(const ConvGeom& g);
 rat3d_status conv_bias_grad(const ConvGeom& g, rat3d_dtype dt, const void* dy, float* db,
-                            int accumulate, hipStream_t st);
+                            int accumulate, void* ws, hipStream_t st);
 // dw (+)= sum over `splits` partial slabs of `count` floats, in slab order.
 rat3d_status wgrad_reduce_launch(const float* part, int splits, int64_t count, float* dw,
                                  int accumulate, hipStream_t st);
