@@ -1,22 +1,34 @@
 // Convolution dispatch: picks the kernel family for a shape and sizes its
 // workspace.  bf16 stride-1 convolutions with kernel 3 (pad 1) or 1 (pad 0)
-// and suitable channel counts take the LDS-brick kernels; every other shape
-// is served by the generic gather implicit GEMM.
+// and suitable channel counts take the LDS-brick kernels (1^3 weight
+// gradients a direct GEMM); the single-channel 7^3 stride-2 stem has its own
+// kernels; every other shape is served by the generic gather implicit GEMM.
 #include "kernels.hpp"
 
 namespace rat3d {
 
+static size_t wgrad_ws(const ConvGeom& g, rat3d_dtype dt) {
+    if (stem_wgrad_ok(g, dt)) return stem_wgrad_ws(g);
+    if (brick_wgrad_ok(g, dt)) return brick_wgrad_ws(g);
+    if (pw_wgrad_ok(g, dt)) return pw_wgrad_ws(g);
+    return wgrad_gather_ws(g);
+}
+
 size_t conv_ws_bytes(const ConvGeom& g, rat3d_dtype dt, int pass) {
-    if (pass == 0) return brick_fd_ok(g, dt, false) ? brick_fd_ws(g) : 0;
+    if (pass == 0) {
+        if (stem_ok(g, dt)) return stem_fwd_ws();
+        return brick_fd_ok(g, dt, false) ? brick_fd_ws(g) : 0;
+    }
     if (pass == 1) return brick_fd_ok(g, dt, true) ? brick_fd_ws(g) : 0;
     // weight-gradient partials, then the bias-gradient slice sums
-    const size_t wb = brick_wgrad_ok(g, dt) ? brick_wgrad_ws(g) : wgrad_gather_ws(g);
+    const size_t wb = wgrad_ws(g, dt);
     return ((wb + 255) & ~(size_t)255) + bias_grad_ws(g);
 }
 
 rat3d_status conv_fwd(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* w,
                       const float* bias, void* y, void* ws, size_t ws_bytes, hipStream_t st) {
     (void)ws_bytes;
+    if (stem_ok(g, dt) && !bias) return conv_fwd_stem(g, x, w, y, ws, st);
     if (brick_fd_ok(g, dt, false)) return conv_fd_brick(g, false, x, w, bias, y, 0, ws, st);
     return conv_fwd_gather(g, dt, x, w, bias, y, st);
 }
@@ -33,11 +45,14 @@ rat3d_status conv_wgrad(const ConvGeom& g, rat3d_dtype dt, const void* x, const 
                         float* dw, float* db, int accumulate, void* ws, size_t ws_bytes,
                         hipStream_t st) {
     (void)ws_bytes;
-    rat3d_status s = brick_wgrad_ok(g, dt) ? conv_wgrad_brick(g, x, dy, dw, accumulate, ws, st)
-                                           : conv_wgrad_gather(g, dt, x, dy, dw, accumulate, ws, st);
+    rat3d_status s;
+    if (stem_wgrad_ok(g, dt)) s = conv_wgrad_stem(g, x, dy, dw, accumulate, ws, st);
+    else if (brick_wgrad_ok(g, dt)) s = conv_wgrad_brick(g, x, dy, dw, accumulate, ws, st);
+    else if (pw_wgrad_ok(g, dt)) s = conv_wgrad_pw(g, x, dy, dw, accumulate, ws, st);
+    else s = conv_wgrad_gather(g, dt, x, dy, dw, accumulate, ws, st);
     if (s != RAT3D_OK) return s;
     if (db) {
-        const size_t wb = brick_wgrad_ok(g, dt) ? brick_wgrad_ws(g) : wgrad_gather_ws(g);
+        const size_t wb = wgrad_ws(g, dt);
         return conv_bias_grad(g, dt, dy, db, accumulate,
                               (char*)ws + ((wb + 255) & ~(size_t)255), st);
     }

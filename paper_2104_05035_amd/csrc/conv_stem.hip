@@ -1,0 +1,351 @@
+// The stem convolution: one input channel, cubic kernel 7, stride 2, pad 3
+// (bf16).  With a single input channel the GEMM K index is the tap alone, so
+// the channel-chunked brick kernels do not apply.
+//
+// Forward: a workgroup computes 4 x 8 x 16 output voxels for 32 output
+// channels.  K is ordered (kd, kh, kw) with kw padded from 7 to 8, so the
+// eight K values of one MFMA operand row are eight consecutive input columns
+// of one (kd, kh) row: columns 2i .. 2i+7 of the input brick for output
+// column i.  The brick is stored twice, the second copy shifted by two
+// columns, so that the row starts on an 8-byte boundary in one of the copies
+// and the operand is two aligned 8-byte LDS reads.  Padding taps (kw = 7,
+// and (kd, kh) rows 49..51 of the last K step) have zero weights.
+//
+// Weight gradient: rows = output channels, columns = padded taps, K = output
+// voxels.  The A operand is dy (8 consecutive output voxels of one channel:
+// one 16-byte global load); the B operand needs input columns 2w - 3 + kw at
+// stride 2, so the input brick is stored split by column parity, each parity
+// plane twice (shifted by one element) so that the 8 values start on a
+// 4-byte boundary and load as four aligned 4-byte LDS reads.
+#include "common.hpp"
+#include "kernels.hpp"
+#include "prof.hpp"
+
+namespace rat3d {
+
+namespace {
+union F16B {
+    uint4 u;
+    uint2 h[2];
+    uint32_t w[4];
+    bf16x8 b;
+};
+
+constexpr int kSK = 7, kSS = 2, kSP = 3;          // kernel, stride, pad
+constexpr int kSRows = kSK * kSK;                 // (kd, kh) rows
+constexpr int kSRowsPad = 52;                     // 13 K steps x 4 rows
+constexpr int kSCo = 32;                          // output channels handled
+
+// forward tile and brick
+constexpr int kFD = 4, kFH = 8, kFW = 16;
+constexpr int kFBD = (kFD - 1) * kSS + kSK;       // 13
+constexpr int kFBH = (kFH - 1) * kSS + kSK;       // 21
+constexpr int kFBW = 40;                          // >= (16-1)*2 + 8 = 38 columns, 80-byte rows
+}  // namespace
+
+// wp[co][r][8] = w[co][0][kd][kh][kw] (r = kd*7 + kh, kw < 7), zero elsewhere
+__global__ void stem_prep_weights(const bf16* __restrict__ w, bf16* __restrict__ wp) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= kSCo * kSRowsPad * 8) return;
+    const int kw = i & 7, r = (i >> 3) % kSRowsPad, co = i / (8 * kSRowsPad);
+    bf16 v = 0;
+    if (kw < kSK && r < kSRows) v = w[(co * kSRows + r) * kSK + kw];
+    wp[i] = v;
+}
+
+__global__ __launch_bounds__(256, 2) void stem_fwd_k(const bf16* __restrict__ x,
+                                                     const bf16* __restrict__ wp,
+                                                     bf16* __restrict__ y, int N, int D, int H,
+                                                     int W, int Do, int Ho, int Wo, int td,
+                                                     int th, int tw) {
+    __shared__ __align__(16) bf16 brick[2][kFBD * kFBH * kFBW];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, kg = lane >> 4;
+    int L = blockIdx.x;
+    const int twi = L % tw;
+    L /= tw;
+    const int thi = L % th;
+    L /= th;
+    const int tdi = L % td;
+    const int n = L / td;
+    const int d0 = tdi * kFD, h0 = thi * kFH, w0 = twi * kFW;
+    const int bd = d0 * kSS - kSP, bh = h0 * kSS - kSP, bw = w0 * kSS - kSP;
+    const int64_t HW = (int64_t)H * W;
+    const bf16* xp = x + (int64_t)n * D * HW;
+
+    for (int it = tid; it < kFBD * kFBH * kFBW; it += 256) {
+        const int c = it % kFBW, r = it / kFBW;
+        const int hh = r % kFBH, dd = r / kFBH;
+        const int d = bd + dd, h = bh + hh, w = bw + c;
+        bf16 v = 0;
+        if ((unsigned)d < (unsigned)D && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W)
+            v = xp[d * HW + (int64_t)h * W + w];
+        brick[0][it] = v;
+        if (c >= 2) brick[1][it - 2] = v;  // copy 1 column c' holds column c' + 2
+        if (c >= kFBW - 2) brick[1][it] = 0;
+    }
+    __syncthreads();
+
+    f32x4 acc[8][2];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        acc[i][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc[i][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    // operand column start 2*li: copy 0 when li is even (8-byte aligned),
+    // else copy 1 at column 2*li - 2
+    const int copy = li & 1;
+    const int col = 2 * li - 2 * copy;
+#pragma unroll 1
+    for (int ks = 0; ks < kSRowsPad / 4; ++ks) {
+        const int r = ks * 4 + kg;
+        F16B b[2];
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct)
+            b[ct].u = *reinterpret_cast<const uint4*>(wp + ((ct * 16 + li) * kSRowsPad + r) * 8);
+        const int rr = r < kSRows ? r : kSRows - 1;  // padding rows: any valid row, zero weights
+        const int kd = rr / kSK, kh = rr - kd * kSK;
+#pragma unroll
+        for (int rw = 0; rw < 8; ++rw) {
+            const int dd = wave * kSS + kd, hh = rw * kSS + kh;
+            const bf16* src = &brick[copy][(dd * kFBH + hh) * kFBW + col];
+            F16B a;
+            a.h[0] = *reinterpret_cast<const uint2*>(src);
+            a.h[1] = *reinterpret_cast<const uint2*>(src + 4);
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct)
+                acc[rw][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.b, b[ct].b, acc[rw][ct],
+                                                                     0, 0, 0);
+        }
+    }
+
+    const int d = d0 + wave;
+    if (d >= Do) return;
+    const int64_t V = (int64_t)Do * Ho * Wo;
+    const bool full = (w0 + kFW <= Wo) && (Wo % 4 == 0);
+#pragma unroll
+    for (int rw = 0; rw < 8; ++rw) {
+        const int h = h0 + rw;
+        if (h >= Ho) continue;
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct) {
+            const int co = ct * 16 + li;
+            const int w = w0 + 4 * kg;
+            bf16* q = y + ((int64_t)n * kSCo + co) * V + ((int64_t)d * Ho + h) * Wo + w;
+            if (full) {
+                *reinterpret_cast<uint2*>(q) =
+                    make_uint2((uint32_t)f2bf(acc[rw][ct][0]) | ((uint32_t)f2bf(acc[rw][ct][1]) << 16),
+                               (uint32_t)f2bf(acc[rw][ct][2]) | ((uint32_t)f2bf(acc[rw][ct][3]) << 16));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (w + e < Wo) q[e] = f2bf(acc[rw][ct][e]);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- weight gradient
+namespace {
+constexpr int kGD = 2, kGH = 8, kGW = 16;          // output voxels per brick (256)
+constexpr int kGBD = (kGD - 1) * kSS + kSK;        // 9
+constexpr int kGBH = (kGH - 1) * kSS + kSK;        // 21
+constexpr int kGHalf = 24;                         // parity-plane columns (>= 19 + 3 + pad)
+constexpr int kTapTiles = (kSRows * 8 + 15) / 16;  // 25 tiles of 16 padded taps
+constexpr int kTilesPerWave = (kTapTiles + 3) / 4; // 7
+
+struct StemWg {
+    const bf16* x;
+    const bf16* dy;
+    float* part;  // [ranges][32][kSRows * 8]
+    int N, D, H, W, Do, Ho, Wo;
+    int td, th, tw;
+    int64_t nbricks;
+    int bpr;
+};
+}  // namespace
+
+__global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
+    // xs[parity][shift][row][col]: parity plane p holds brick columns 2c + p;
+    // shift 1 is the same plane moved left by one column
+    __shared__ __align__(16) bf16 xs[2][2][kGBD * kGBH][kGHalf];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, kg = lane >> 4;
+    const int hl_l = kg >> 1, wl = (kg & 1) * 8;
+    const int64_t b_beg = (int64_t)blockIdx.x * a.bpr;
+    const int64_t b_end = b_beg + a.bpr < a.nbricks ? b_beg + a.bpr : a.nbricks;
+    const int64_t HW = (int64_t)a.H * a.W, Vo = (int64_t)a.Do * a.Ho * a.Wo;
+
+    f32x4 acc[kTilesPerWave][2];
+#pragma unroll
+    for (int j = 0; j < kTilesPerWave; ++j) {
+        acc[j][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc[j][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    for (int64_t b = b_beg; b < b_end; ++b) {
+        const int twi = (int)(b % a.tw);
+        int64_t r = b / a.tw;
+        const int thi = (int)(r % a.th);
+        r /= a.th;
+        const int tdi = (int)(r % a.td);
+        const int n = (int)(r / a.td);
+        const int d0 = tdi * kGD, h0 = thi * kGH, w0 = twi * kGW;
+        const int bd = d0 * kSS - kSP, bh = h0 * kSS - kSP, bw = w0 * kSS - kSP;
+        const bf16* xp = a.x + (int64_t)n * a.D * HW;
+        __syncthreads();
+        for (int it = tid; it < kGBD * kGBH * 2 * kGHalf; it += 256) {
+            const int c = it % (2 * kGHalf), row = it / (2 * kGHalf);
+            const int hh = row % kGBH, dd = row / kGBH;
+            const int d = bd + dd, h = bh + hh, w = bw + c;
+            bf16 v = 0;
+            if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
+                (unsigned)w < (unsigned)a.W)
+                v = xp[d * HW + (int64_t)h * a.W + w];
+            const int p = c & 1, cc = c >> 1;
+            xs[p][0][row][cc] = v;
+            if (cc >= 1) xs[p][1][row][cc - 1] = v;
+            if (cc == kGHalf - 1) xs[p][1][row][cc] = 0;
+        }
+        __syncthreads();
+#pragma unroll 1
+        for (int s = 0; s < kGD * kGH / 2; ++s) {
+            const int dl = s / (kGH / 2);
+            const int hl = (s % (kGH / 2)) * 2 + hl_l;
+            const int d = d0 + dl, h = h0 + hl, w = w0 + wl;
+            const bool ok = d < a.Do && h < a.Ho && w + 8 <= a.Wo;
+            F16B av[2];
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                av[ct].u = make_uint4(0u, 0u, 0u, 0u);
+                if (ok)
+                    av[ct].u = *reinterpret_cast<const uint4*>(
+                        a.dy + ((int64_t)n * kSCo + ct * 16 + li) * Vo +
+                        ((int64_t)d * a.Ho + h) * a.Wo + w);
+            }
+#pragma unroll
+            for (int j = 0; j < kTilesPerWave; ++j) {
+                const int tile = wave + 4 * j;
+                if (tile >= kTapTiles) continue;
+                // this lane's B column: padded tap t = tile*16 + li
+                const int t = tile * 16 + li;
+                const int rrow = t >> 3, kw = t & 7;
+                F16B bv;
+                bv.u = make_uint4(0u, 0u, 0u, 0u);
+                if (rrow < kSRows && kw < kSK) {
+                    const int kd = rrow / kSK, kh = rrow - kd * kSK;
+                    // input column (brick) for output column wl + i: 2*(wl + i) + kw
+                    // = parity kw & 1, plane column wl + i + (kw >> 1)
+                    const int start = wl + (kw >> 1);
+                    const int sh = start & 1;
+                    const bf16* src =
+                        &xs[kw & 1][sh][(dl * kSS + kd) * kGBH + hl * kSS + kh][start - sh];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) bv.w[q] = reinterpret_cast<const uint32_t*>(src)[q];
+                }
+#pragma unroll
+                for (int ct = 0; ct < 2; ++ct)
+                    acc[j][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[ct].b, bv.b,
+                                                                        acc[j][ct], 0, 0, 0);
+            }
+        }
+    }
+
+    float* out = a.part + (int64_t)blockIdx.x * kSCo * kSRows * 8;
+#pragma unroll
+    for (int j = 0; j < kTilesPerWave; ++j) {
+        const int tile = wave + 4 * j;
+        if (tile >= kTapTiles) continue;
+        const int t = tile * 16 + li;
+        if ((t >> 3) >= kSRows) continue;
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                out[(ct * 16 + 4 * kg + e) * kSRows * 8 + t] = acc[j][ct][e];
+    }
+}
+
+// part is [ranges][32][49*8]; dw is [32][1][7][7][7] (padding column kw = 7 dropped)
+__global__ void stem_wgrad_reduce(const float* __restrict__ part, int ranges,
+                                  float* __restrict__ dw, int accumulate) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= kSCo * kSRows * kSK) return;
+    const int kw = i % kSK, r = (i / kSK) % kSRows, co = i / (kSK * kSRows);
+    const int64_t src = (int64_t)co * kSRows * 8 + r * 8 + kw;
+    float s = accumulate ? dw[i] : 0.f;
+    for (int z = 0; z < ranges; ++z) s += part[(int64_t)z * kSCo * kSRows * 8 + src];
+    dw[i] = s;
+}
+
+bool stem_ok(const ConvGeom& g, rat3d_dtype dt) {
+    return dt == RAT3D_BF16 && g.Ci == 1 && g.Co == kSCo && g.k == kSK && g.s == kSS &&
+           g.p == kSP;
+}
+
+size_t stem_fwd_ws() { return (size_t)kSCo * kSRowsPad * 8 * 2; }
+
+static int stem_ranges(int64_t nbricks) {
+    int64_t r = 512;
+    if (r > nbricks) r = nbricks;
+    return (int)(r < 1 ? 1 : r);
+}
+
+static int64_t stem_bricks(const ConvGeom& g) {
+    return (int64_t)g.N * ceil_div(g.Do, kGD) * ceil_div(g.Ho, kGH) * ceil_div(g.Wo, kGW);
+}
+
+bool stem_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) { return stem_ok(g, dt) && g.Wo % 8 == 0; }
+
+size_t stem_wgrad_ws(const ConvGeom& g) {
+    return (size_t)stem_ranges(stem_bricks(g)) * kSCo * kSRows * 8 * sizeof(float);
+}
+
+rat3d_status conv_fwd_stem(const ConvGeom& g, const void* x, const void* w, void* y, void* ws,
+                           hipStream_t st) {
+    bf16* wp = (bf16*)ws;
+    stem_prep_weights<<<(unsigned)ceil_div(kSCo * kSRowsPad * 8, 256), 256, 0, st>>>(
+        (const bf16*)w, wp);
+    RAT3D_LAUNCH_CHECK();
+    const int td = (int)ceil_div(g.Do, kFD), th = (int)ceil_div(g.Ho, kFH),
+              tw = (int)ceil_div(g.Wo, kFW);
+    ProfScope ps("conv_stem_fwd", st, conv_flops(g), conv_bytes(g, 2));
+    stem_fwd_k<<<(unsigned)((int64_t)g.N * td * th * tw), 256, 0, st>>>(
+        (const bf16*)x, wp, (bf16*)y, g.N, g.D, g.H, g.W, g.Do, g.Ho, g.Wo, td, th, tw);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
+rat3d_status conv_wgrad_stem(const ConvGeom& g, const void* x, const void* dy, float* dw,
+                             int accumulate, void* ws, hipStream_t st) {
+    StemWg a;
+    a.x = (const bf16*)x;
+    a.dy = (const bf16*)dy;
+    a.part = (float*)ws;
+    a.N = g.N;
+    a.D = g.D;
+    a.H = g.H;
+    a.W = g.W;
+    a.Do = g.Do;
+    a.Ho = g.Ho;
+    a.Wo = g.Wo;
+    a.td = (int)ceil_div(g.Do, kGD);
+    a.th = (int)ceil_div(g.Ho, kGH);
+    a.tw = (int)ceil_div(g.Wo, kGW);
+    a.nbricks = stem_bricks(g);
+    const int R = stem_ranges(a.nbricks);
+    a.bpr = (int)ceil_div(a.nbricks, R);
+    const int Rreal = (int)ceil_div(a.nbricks, a.bpr);
+    {
+        ProfScope ps("conv_stem_wgrad", st, conv_flops(g), conv_bytes(g, 2));
+        stem_wgrad_k<<<(unsigned)Rreal, 256, 0, st>>>(a);
+        RAT3D_LAUNCH_CHECK();
+    }
+    ProfScope ps("wgrad_reduce", st, 0.0, 4.0 * kSCo * kSRows * 8 * (Rreal + 1 + accumulate));
+    stem_wgrad_reduce<<<(unsigned)ceil_div(kSCo * kSRows * kSK, 256), 256, 0, st>>>(a.part, Rreal,
+                                                                                   dw, accumulate);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
+}  // namespace rat3d

@@ -64,6 +64,22 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
 rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, float* dw,
                               int accumulate, void* ws, hipStream_t st);
 
+// ---- stem: one input channel, 7^3, stride 2, pad 3 (conv_stem.hip) -------
+bool stem_ok(const ConvGeom& g, rat3d_dtype dt);
+bool stem_wgrad_ok(const ConvGeom& g, rat3d_dtype dt);
+size_t stem_fwd_ws();
+size_t stem_wgrad_ws(const ConvGeom& g);
+rat3d_status conv_fwd_stem(const ConvGeom& g, const void* x, const void* w, void* y, void* ws,
+                           hipStream_t st);
+rat3d_status conv_wgrad_stem(const ConvGeom& g, const void* x, const void* dy, float* dw,
+                             int accumulate, void* ws, hipStream_t st);
+
+// ---- 1x1x1 weight gradient as a direct GEMM (conv_pw.hip) ---------------
+bool pw_wgrad_ok(const ConvGeom& g, rat3d_dtype dt);
+size_t pw_wgrad_ws(const ConvGeom& g);
+rat3d_status conv_wgrad_pw(const ConvGeom& g, const void* x, const void* dy, float* dw,
+                           int accumulate, void* ws, hipStream_t st);
+
 // ---- batch norm (bn.hip) -----------------------------------------------
 struct BnGeom {
     int N, C;

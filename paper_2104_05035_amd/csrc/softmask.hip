@@ -241,6 +241,353 @@ __global__ __launch_bounds__(kEwThreads) void add_k(const T* __restrict__ a,
     vstore<T, VEC>(dst + i, x);
 }
 
+// ---------------------------------------------------------------- fast paths
+// Grids are (plane chunk, n*c*depth): one block row per output (or input)
+// depth plane, so in-plane indices need only 32-bit arithmetic.
+
+// Max pool 3^3, stride 2, pad 1: the common case, same scan order and
+// first-maximum rule as pool_fwd_k.
+template <typename T>
+__global__ __launch_bounds__(kEwThreads) void pool332_fwd_k(const T* __restrict__ x, int D,
+                                                            int H, int W, int Do, int Ho, int Wo,
+                                                            T* __restrict__ y,
+                                                            uint8_t* __restrict__ am) {
+    const int t = blockIdx.x * kEwThreads + threadIdx.x;
+    if (t >= Ho * Wo) return;
+    const int oh = t / Wo, ow = t - oh * Wo;
+    const int plane = blockIdx.y;  // nc * Do + od
+    const int nc = plane / Do, od = plane - nc * Do;
+    const T* xp = x + (int64_t)nc * D * H * W;
+    float best = 0.f;
+    int arg = -1;
+#pragma unroll
+    for (int kd = 0; kd < 3; ++kd) {
+        const int id = 2 * od - 1 + kd;
+        if ((unsigned)id >= (unsigned)D) continue;
+#pragma unroll
+        for (int kh = 0; kh < 3; ++kh) {
+            const int ih = 2 * oh - 1 + kh;
+            if ((unsigned)ih >= (unsigned)H) continue;
+            const T* row = xp + ((int64_t)id * H + ih) * W;
+#pragma unroll
+            for (int kw = 0; kw < 3; ++kw) {
+                const int iw = 2 * ow - 1 + kw;
+                if ((unsigned)iw >= (unsigned)W) continue;
+                const float v = Elt<T>::ld(row + iw);
+                if (arg < 0 || v > best) {
+                    best = v;
+                    arg = (kd * 3 + kh) * 3 + kw;
+                }
+            }
+        }
+    }
+    const int64_t o = (int64_t)plane * Ho * Wo + t;
+    Elt<T>::st(y + o, best);
+    am[o] = (uint8_t)arg;
+}
+
+// Windows (3^3, stride 2, pad 1) containing input index i along one axis:
+// even i -> window i/2 (tap 1); odd i -> windows (i-1)/2 (tap 2) and
+// (i+1)/2 (tap 0), each only if inside [0, O).
+__device__ __forceinline__ int pool332_windows(int i, int O, int (&o)[2], int (&tap)[2]) {
+    if ((i & 1) == 0) {
+        o[0] = i >> 1;
+        tap[0] = 1;
+        return o[0] < O ? 1 : 0;
+    }
+    int n = 0;
+    if (((i - 1) >> 1) < O) { o[n] = (i - 1) >> 1; tap[n] = 2; ++n; }
+    if (((i + 1) >> 1) < O) { o[n] = (i + 1) >> 1; tap[n] = 0; ++n; }
+    return n;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kEwThreads) void pool332_bwd_k(const T* __restrict__ dy,
+                                                            const uint8_t* __restrict__ am,
+                                                            int D, int H, int W, int Do, int Ho,
+                                                            int Wo, T* __restrict__ dx,
+                                                            int accumulate) {
+    const int t = blockIdx.x * kEwThreads + threadIdx.x;
+    if (t >= H * W) return;
+    const int ih = t / W, iw = t - ih * W;
+    const int plane = blockIdx.y;  // nc * D + id
+    const int nc = plane / D, id = plane - nc * D;
+    int od[2], td[2], oh[2], th[2], ow[2], tw[2];
+    const int nd = pool332_windows(id, Do, od, td);
+    const int nh = pool332_windows(ih, Ho, oh, th);
+    const int nw = pool332_windows(iw, Wo, ow, tw);
+    const int64_t ob = (int64_t)nc * Do * Ho * Wo;
+    float sum = 0.f;
+    for (int a = 0; a < nd; ++a)
+        for (int b = 0; b < nh; ++b) {
+            const int64_t rb = ob + ((int64_t)od[a] * Ho + oh[b]) * Wo;
+            for (int c = 0; c < nw; ++c) {
+                const int off = (td[a] * 3 + th[b]) * 3 + tw[c];
+                if ((int)am[rb + ow[c]] == off) sum += Elt<T>::ld(dy + rb + ow[c]);
+            }
+        }
+    const int64_t i = (int64_t)plane * H * W + t;
+    const float base = accumulate ? Elt<T>::ld(dx + i) : 0.f;
+    Elt<T>::st(dx + i, base + sum);
+}
+
+// Trilinear with per-axis tables built once per block in LDS.  Axes longer
+// than kAxisMax use the generic kernels.
+constexpr int kAxisMax = 256;
+
+template <typename T>
+__global__ __launch_bounds__(kEwThreads) void up_fwd_tab_k(const T* __restrict__ x, int Di,
+                                                           int Hi, int Wi, int Do, int Ho, int Wo,
+                                                           float sd, float sh, float sw,
+                                                           T* __restrict__ y) {
+    __shared__ int h0s[kAxisMax], h1s[kAxisMax], w0s[kAxisMax], w1s[kAxisMax];
+    __shared__ float lhs[kAxisMax], lws[kAxisMax];
+    for (int i = threadIdx.x; i < Ho; i += kEwThreads) lin_src(i, Hi, sh, h0s[i], h1s[i], lhs[i]);
+    for (int i = threadIdx.x; i < Wo; i += kEwThreads) lin_src(i, Wi, sw, w0s[i], w1s[i], lws[i]);
+    __syncthreads();
+    const int t = blockIdx.x * kEwThreads + threadIdx.x;
+    if (t >= Ho * Wo) return;
+    const int oh = t / Wo, ow = t - oh * Wo;
+    const int plane = blockIdx.y;  // nc * Do + od
+    const int nc = plane / Do, od = plane - nc * Do;
+    int d0, d1;
+    float ld;
+    lin_src(od, Di, sd, d0, d1, ld);
+    const int h0 = h0s[oh], h1 = h1s[oh], w0 = w0s[ow], w1 = w1s[ow];
+    const float lh = lhs[oh], lw = lws[ow];
+    const T* xp = x + (int64_t)nc * Di * Hi * Wi;
+    auto at = [&](int d, int h, int w) { return Elt<T>::ld(xp + ((int64_t)d * Hi + h) * Wi + w); };
+    const float c00 = at(d0, h0, w0) * (1.f - lw) + at(d0, h0, w1) * lw;
+    const float c01 = at(d0, h1, w0) * (1.f - lw) + at(d0, h1, w1) * lw;
+    const float c10 = at(d1, h0, w0) * (1.f - lw) + at(d1, h0, w1) * lw;
+    const float c11 = at(d1, h1, w0) * (1.f - lw) + at(d1, h1, w1) * lw;
+    const float c0 = c00 * (1.f - lh) + c01 * lh;
+    const float c1 = c10 * (1.f - lh) + c11 * lh;
+    Elt<T>::st(y + (int64_t)plane * Ho * Wo + t, c0 * (1.f - ld) + c1 * ld);
+}
+
+template <typename T>
+__global__ __launch_bounds__(kEwThreads) void up_bwd_tab_k(const T* __restrict__ dy, int Di,
+                                                           int Hi, int Wi, int Do, int Ho, int Wo,
+                                                           float sd, float sh, float sw,
+                                                           T* __restrict__ dx, int accumulate) {
+    __shared__ AxisTaps hts[kAxisMax], wts[kAxisMax];
+    for (int i = threadIdx.x; i < Hi; i += kEwThreads) axis_taps(i, Hi, Ho, sh, hts[i]);
+    for (int i = threadIdx.x; i < Wi; i += kEwThreads) axis_taps(i, Wi, Wo, sw, wts[i]);
+    __syncthreads();
+    const int t = blockIdx.x * kEwThreads + threadIdx.x;
+    if (t >= Hi * Wi) return;
+    const int ih = t / Wi, iw = t - ih * Wi;
+    const int plane = blockIdx.y;  // nc * Di + id
+    const int nc = plane / Di, id = plane - nc * Di;
+    AxisTaps td;
+    axis_taps(id, Di, Do, sd, td);
+    const AxisTaps& th = hts[ih];
+    const AxisTaps& tw = wts[iw];
+    const T* g = dy + (int64_t)nc * Do * Ho * Wo;
+    float sum = 0.f;
+    for (int a = 0; a < td.n; ++a)
+        for (int b = 0; b < th.n; ++b) {
+            const T* row = g + ((int64_t)td.o[a] * Ho + th.o[b]) * Wo;
+            float r = 0.f;
+            for (int c = 0; c < tw.n; ++c) r += tw.w[c] * Elt<T>::ld(row + tw.o[c]);
+            sum += td.w[a] * th.w[b] * r;
+        }
+    const int64_t i = (int64_t)plane * Hi * Wi + t;
+    const float base = accumulate ? Elt<T>::ld(dx + i) : 0.f;
+    Elt<T>::st(dx + i, base + sum);
+}
+
+// ---------------------------------------------------------------- exact x2, bf16
+// When every axis doubles (out = 2 * in), the half-pixel weights are 1/4 and
+// 3/4 exactly: fine o = 2m takes 1/4 c[m-1] + 3/4 c[m] (c[0] alone at m = 0),
+// o = 2m + 1 takes 3/4 c[m] + 1/4 c[m+1] (c[m] alone at the last m).  The
+// transpose gives coarse i 1/4 f[2i-1] + 3/4 f[2i] + 3/4 f[2i+1] + 1/4 f[2i+2]
+// with the border terms folded the same way.  These are the same weights the
+// general kernels compute, applied separably.
+
+// Weight of coarse index m for fine index o along one doubled axis of coarse
+// length n (0 if o does not read m).
+__device__ __forceinline__ float x2_w(int o, int m, int n) {
+    const int half = o >> 1;
+    if ((o & 1) == 0) {  // 1/4 c[half-1] + 3/4 c[half]
+        if (half == 0) return m == 0 ? 1.f : 0.f;
+        return m == half ? 0.75f : (m == half - 1 ? 0.25f : 0.f);
+    }
+    if (half == n - 1) return m == half ? 1.f : 0.f;  // 3/4 c[half] + 1/4 c[half+1]
+    return m == half ? 0.75f : (m == half + 1 ? 0.25f : 0.f);
+}
+
+// Forward: one thread writes 8 consecutive fine voxels of one row.
+__global__ __launch_bounds__(kEwThreads) void up2_fwd_k(const bf16* __restrict__ x, int Di,
+                                                        int Hi, int Wi, bf16* __restrict__ y) {
+    const int Do = 2 * Di, Ho = 2 * Hi, Wo = 2 * Wi, G = Wo / 8;
+    const int t = blockIdx.x * kEwThreads + threadIdx.x;
+    if (t >= Ho * G) return;
+    const int oh = t / G, g = t - oh * G;
+    const int plane = blockIdx.y;  // nc * Do + od
+    const int nc = plane / Do, od = plane - nc * Do;
+    const int m0 = 4 * g;  // coarse w of the group: fine 8g .. 8g+7 read coarse m0-1 .. m0+4
+    const bf16* xp = x + (int64_t)nc * Di * Hi * Wi;
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    const int dlo = (od >> 1) - 1, hlo = (oh >> 1) - 1;
+    for (int dd = 0; dd < 3; ++dd) {
+        const int md = dlo + dd;
+        if (md < 0 || md >= Di) continue;
+        const float wd = x2_w(od, md, Di);
+        if (wd == 0.f) continue;
+        for (int hh = 0; hh < 3; ++hh) {
+            const int mh = hlo + hh;
+            if (mh < 0 || mh >= Hi) continue;
+            const float wdh = wd * x2_w(oh, mh, Hi);
+            if (wdh == 0.f) continue;
+            const bf16* row = xp + ((int64_t)md * Hi + mh) * Wi;
+            float c[6];  // coarse m0-1 .. m0+4 (clamped reads; weights decide)
+#pragma unroll
+            for (int j = 0; j < 6; ++j) {
+                const int m = min(max(m0 - 1 + j, 0), Wi - 1);
+                c[j] = bf2f(row[m]);
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int o = 8 * g + j;
+                float v = 0.f;
+#pragma unroll
+                for (int q = 0; q < 6; ++q) {
+                    const int m = m0 - 1 + q;
+                    if (m >= 0 && m < Wi) v += x2_w(o, m, Wi) * c[q];
+                }
+                acc[j] += wdh * v;
+            }
+        }
+    }
+    uint32_t w4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        w4[j] = (uint32_t)f2bf(acc[2 * j]) | ((uint32_t)f2bf(acc[2 * j + 1]) << 16);
+    *reinterpret_cast<uint4*>(y + (int64_t)plane * Ho * Wo + (int64_t)oh * Wo + 8 * g) =
+        make_uint4(w4[0], w4[1], w4[2], w4[3]);
+}
+
+// Backward: one thread writes 4 consecutive coarse voxels of one row, reading
+// fine columns 8g-1 .. 8g+8 of the 4 x 4 fine rows that touch them.
+__global__ __launch_bounds__(kEwThreads) void up2_bwd_k(const bf16* __restrict__ dy, int Di,
+                                                        int Hi, int Wi, bf16* __restrict__ dx,
+                                                        int accumulate) {
+    const int Do = 2 * Di, Ho = 2 * Hi, Wo = 2 * Wi, G = Wi / 4;
+    const int t = blockIdx.x * kEwThreads + threadIdx.x;
+    if (t >= Hi * G) return;
+    const int ih = t / G, g = t - ih * G;
+    const int plane = blockIdx.y;  // nc * Di + id
+    const int nc = plane / Di, id = plane - nc * Di;
+    const int m0 = 4 * g;
+    const bf16* gp = dy + (int64_t)nc * Do * Ho * Wo;
+    float rowacc[10];  // fine columns 8g-1 .. 8g+8, weighted over the (d, h) rows
+#pragma unroll
+    for (int j = 0; j < 10; ++j) rowacc[j] = 0.f;
+    for (int dd = 0; dd < 4; ++dd) {
+        const int od = 2 * id - 1 + dd;
+        if (od < 0 || od >= Do) continue;
+        const float wd = x2_w(od, id, Di);
+        if (wd == 0.f) continue;
+        for (int hh = 0; hh < 4; ++hh) {
+            const int oh = 2 * ih - 1 + hh;
+            if (oh < 0 || oh >= Ho) continue;
+            const float wdh = wd * x2_w(oh, ih, Hi);
+            if (wdh == 0.f) continue;
+            const bf16* row = gp + ((int64_t)od * Ho + oh) * Wo;
+            const uint4 u = *reinterpret_cast<const uint4*>(row + 8 * g);  // 8g .. 8g+7
+            const uint32_t ws[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                rowacc[1 + 2 * j] += wdh * __uint_as_float(ws[j] << 16);
+                rowacc[2 + 2 * j] += wdh * __uint_as_float(ws[j] & 0xffff0000u);
+            }
+            if (8 * g - 1 >= 0) rowacc[0] += wdh * bf2f(row[8 * g - 1]);
+            if (8 * g + 8 < Wo) rowacc[9] += wdh * bf2f(row[8 * g + 8]);
+        }
+    }
+    float out[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int m = m0 + k;
+        float v = 0.f;
+#pragma unroll
+        for (int j = 0; j < 10; ++j) {
+            const int o = 8 * g - 1 + j;
+            if (o >= 0 && o < Wo) v += x2_w(o, m, Wi) * rowacc[j];
+        }
+        out[k] = v;
+    }
+    bf16* q = dx + (int64_t)plane * Hi * Wi + (int64_t)ih * Wi + m0;
+    uint2* q2 = reinterpret_cast<uint2*>(q);
+    if (accumulate) {
+        const uint2 o = *q2;
+        out[0] += __uint_as_float(o.x << 16);
+        out[1] += __uint_as_float(o.x & 0xffff0000u);
+        out[2] += __uint_as_float(o.y << 16);
+        out[3] += __uint_as_float(o.y & 0xffff0000u);
+    }
+    *q2 = make_uint2((uint32_t)f2bf(out[0]) | ((uint32_t)f2bf(out[1]) << 16),
+                     (uint32_t)f2bf(out[2]) | ((uint32_t)f2bf(out[3]) << 16));
+}
+
+// Max-pool gradient (3^3, stride 2, pad 1), bf16: one thread writes 8
+// consecutive input voxels of a row; the windows along w are 4g-1 .. 4g+4.
+__global__ __launch_bounds__(kEwThreads) void pool332_bwd8_k(const bf16* __restrict__ dy,
+                                                             const uint8_t* __restrict__ am,
+                                                             int D, int H, int W, int Do, int Ho,
+                                                             int Wo, bf16* __restrict__ dx,
+                                                             int accumulate) {
+    const int G = W / 8;
+    const int t = blockIdx.x * kEwThreads + threadIdx.x;
+    if (t >= H * G) return;
+    const int ih = t / G, g = t - ih * G;
+    const int plane = blockIdx.y;  // nc * D + id
+    const int nc = plane / D, id = plane - nc * D;
+    int od[2], td[2], oh[2], th[2];
+    const int nd = pool332_windows(id, Do, od, td);
+    const int nh = pool332_windows(ih, Ho, oh, th);
+    const int64_t ob = (int64_t)nc * Do * Ho * Wo;
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    for (int a = 0; a < nd; ++a)
+        for (int b = 0; b < nh; ++b) {
+            const int64_t rb = ob + ((int64_t)od[a] * Ho + oh[b]) * Wo;
+            const int base = (td[a] * 3 + th[b]) * 3;
+#pragma unroll
+            for (int q = 0; q < 6; ++q) {
+                const int ow = 4 * g - 1 + q;
+                if (ow < 0 || ow >= Wo) continue;
+                const int arg = (int)am[rb + ow];
+                if (arg / 3 != base / 3) continue;  // argmax in another (kd, kh) plane
+                // the window's argmax column iw = 2*ow - 1 + kw, kw = arg % 3
+                const int iw = 2 * ow - 1 + (arg - base);
+                const int j = iw - 8 * g;
+                if (j >= 0 && j < 8) acc[j] += bf2f(dy[rb + ow]);
+            }
+        }
+    bf16* q = dx + (int64_t)plane * H * W + (int64_t)ih * W + 8 * g;
+    uint4* q4 = reinterpret_cast<uint4*>(q);
+    if (accumulate) {
+        const uint4 o = *q4;
+        const uint32_t ws[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            acc[2 * j] += __uint_as_float(ws[j] << 16);
+            acc[2 * j + 1] += __uint_as_float(ws[j] & 0xffff0000u);
+        }
+    }
+    uint32_t w4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        w4[j] = (uint32_t)f2bf(acc[2 * j]) | ((uint32_t)f2bf(acc[2 * j + 1]) << 16);
+    *q4 = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+}
+
 // ---------------------------------------------------------------- launchers
 rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, rat3d_dtype dt,
                       const void* x, void* y, uint8_t* argmax, hipStream_t st) {
@@ -249,6 +596,17 @@ rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, ra
     const unsigned blocks = (unsigned)ceil_div(total, kEwThreads);
     const double es = dt == RAT3D_BF16 ? 2.0 : 4.0;
     ProfScope ps("pool_fwd", st, 0.0, es * ((double)N * C * D * H * W + total) + total);
+    if (k == 3 && s == 2 && p == 1 && (int64_t)N * C * Do < 65536) {
+        const dim3 grid((unsigned)ceil_div((int64_t)Ho * Wo, kEwThreads), N * C * Do);
+        if (dt == RAT3D_BF16)
+            pool332_fwd_k<bf16><<<grid, kEwThreads, 0, st>>>((const bf16*)x, D, H, W, Do, Ho, Wo,
+                                                             (bf16*)y, argmax);
+        else
+            pool332_fwd_k<float><<<grid, kEwThreads, 0, st>>>((const float*)x, D, H, W, Do, Ho,
+                                                              Wo, (float*)y, argmax);
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
     if (dt == RAT3D_BF16)
         pool_fwd_k<bf16><<<blocks, kEwThreads, 0, st>>>((const bf16*)x, N * C, D, H, W, k, s, p,
                                                         Do, Ho, Wo, (bf16*)y, argmax);
@@ -268,6 +626,25 @@ rat3d_status pool_bwd(int N, int C, int D, int H, int W, int k, int s, int p, ra
     const double es = dt == RAT3D_BF16 ? 2.0 : 4.0;
     const double small = (double)N * C * Do * Ho * Wo;
     ProfScope ps("pool_bwd", st, 0.0, es * (small + total * (1 + accumulate)) + small);
+    if (k == 3 && s == 2 && p == 1 && dt == RAT3D_BF16 && W % 8 == 0 &&
+        (int64_t)N * C * D < 65536) {
+        const dim3 grid((unsigned)ceil_div((int64_t)H * (W / 8), kEwThreads), N * C * D);
+        pool332_bwd8_k<<<grid, kEwThreads, 0, st>>>((const bf16*)dy, argmax, D, H, W, Do, Ho, Wo,
+                                                    (bf16*)dx, accumulate);
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
+    if (k == 3 && s == 2 && p == 1 && (int64_t)N * C * D < 65536) {
+        const dim3 grid((unsigned)ceil_div((int64_t)H * W, kEwThreads), N * C * D);
+        if (dt == RAT3D_BF16)
+            pool332_bwd_k<bf16><<<grid, kEwThreads, 0, st>>>((const bf16*)dy, argmax, D, H, W, Do,
+                                                             Ho, Wo, (bf16*)dx, accumulate);
+        else
+            pool332_bwd_k<float><<<grid, kEwThreads, 0, st>>>((const float*)dy, argmax, D, H, W,
+                                                              Do, Ho, Wo, (float*)dx, accumulate);
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
     if (dt == RAT3D_BF16)
         pool_bwd_k<bf16><<<blocks, kEwThreads, 0, st>>>((const bf16*)dy, argmax, N * C, D, H, W,
                                                         k, s, p, Do, Ho, Wo, (bf16*)dx,
@@ -289,6 +666,24 @@ rat3d_status up_fwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
     const float sd = up_scale(Di, Do), sh = up_scale(Hi, Ho), sw = up_scale(Wi, Wo);
     ProfScope ps("up_fwd", st, 0.0,
                  (dt == RAT3D_BF16 ? 2.0 : 4.0) * ((double)N * C * Di * Hi * Wi + total));
+    const bool x2 = Do == 2 * Di && Ho == 2 * Hi && Wo == 2 * Wi;
+    if (x2 && dt == RAT3D_BF16 && Wo % 8 == 0 && (int64_t)N * C * Do < 65536) {
+        const dim3 grid((unsigned)ceil_div((int64_t)Ho * (Wo / 8), kEwThreads), N * C * Do);
+        up2_fwd_k<<<grid, kEwThreads, 0, st>>>((const bf16*)x, Di, Hi, Wi, (bf16*)y);
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
+    if (Ho <= kAxisMax && Wo <= kAxisMax && (int64_t)N * C * Do < 65536) {
+        const dim3 grid((unsigned)ceil_div((int64_t)Ho * Wo, kEwThreads), N * C * Do);
+        if (dt == RAT3D_BF16)
+            up_fwd_tab_k<bf16><<<grid, kEwThreads, 0, st>>>((const bf16*)x, Di, Hi, Wi, Do, Ho, Wo,
+                                                            sd, sh, sw, (bf16*)y);
+        else
+            up_fwd_tab_k<float><<<grid, kEwThreads, 0, st>>>((const float*)x, Di, Hi, Wi, Do, Ho,
+                                                             Wo, sd, sh, sw, (float*)y);
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
     if (dt == RAT3D_BF16)
         up_fwd_k<bf16><<<blocks, kEwThreads, 0, st>>>((const bf16*)x, N * C, Di, Hi, Wi, Do, Ho,
                                                       Wo, sd, sh, sw, (bf16*)y);
@@ -307,6 +702,26 @@ rat3d_status up_bwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
     ProfScope ps("up_bwd", st, 0.0,
                  (dt == RAT3D_BF16 ? 2.0 : 4.0) *
                      ((double)N * C * Do * Ho * Wo + total * (1 + accumulate)));
+    const bool x2 = Do == 2 * Di && Ho == 2 * Hi && Wo == 2 * Wi;
+    if (x2 && dt == RAT3D_BF16 && Wi % 4 == 0 && (int64_t)N * C * Di < 65536) {
+        const dim3 grid((unsigned)ceil_div((int64_t)Hi * (Wi / 4), kEwThreads), N * C * Di);
+        up2_bwd_k<<<grid, kEwThreads, 0, st>>>((const bf16*)dy, Di, Hi, Wi, (bf16*)dx,
+                                               accumulate);
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
+    if (Hi <= kAxisMax && Wi <= kAxisMax && (int64_t)N * C * Di < 65536) {
+        const dim3 grid((unsigned)ceil_div((int64_t)Hi * Wi, kEwThreads), N * C * Di);
+        if (dt == RAT3D_BF16)
+            up_bwd_tab_k<bf16><<<grid, kEwThreads, 0, st>>>((const bf16*)dy, Di, Hi, Wi, Do, Ho, Wo,
+                                                            sd, sh, sw, (bf16*)dx, accumulate);
+        else
+            up_bwd_tab_k<float><<<grid, kEwThreads, 0, st>>>((const float*)dy, Di, Hi, Wi, Do, Ho,
+                                                             Wo, sd, sh, sw, (float*)dx,
+                                                             accumulate);
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
     if (dt == RAT3D_BF16)
         up_bwd_k<bf16><<<blocks, kEwThreads, 0, st>>>((const bf16*)dy, N * C, Di, Hi, Wi, Do, Ho,
                                                       Wo, sd, sh, sw, (bf16*)dx, accumulate);

@@ -45,6 +45,14 @@ CONV_CASES = [
     (2, 256, 256, 2, 2, 2, 3, 1, 1, False, "bf16"),
     (2, 256, 256, 1, 1, 1, 3, 1, 1, False, "bf16"),
     (2, 256, 256, 3, 4, 3, 1, 1, 0, True, "bf16"),
+    # 1^3 weight gradient as a direct GEMM (voxels per volume a multiple of 32)
+    (2, 64, 64, 4, 8, 16, 1, 1, 0, True, "bf16"),
+    (1, 32, 64, 8, 8, 8, 1, 1, 0, False, "bf16"),
+    (3, 80, 48, 4, 4, 8, 1, 1, 0, False, "bf16"),
+    # stem kernels (1 -> 32, 7^3, stride 2, pad 3): full and ragged tiles
+    (2, 1, 32, 24, 30, 32, 7, 2, 3, False, "bf16"),
+    (1, 1, 32, 13, 9, 21, 7, 2, 3, False, "bf16"),
+    (2, 1, 32, 20, 34, 48, 7, 2, 3, False, "bf16"),
 ]
 
 
@@ -148,7 +156,8 @@ def test_bn(case, relu, resid):
 
 
 POOL_CASES = [(2, 3, 9, 8, 7, "bf16"), (2, 16, 24, 28, 24, "bf16"), (1, 2, 3, 4, 3, "f32"),
-              (1, 1, 2, 2, 2, "bf16"), (2, 4, 6, 7, 6, "bf16"), (1, 1, 1, 1, 1, "f32")]
+              (1, 1, 2, 2, 2, "bf16"), (2, 4, 6, 7, 6, "bf16"), (1, 1, 1, 1, 1, "f32"),
+              (1, 2, 48, 56, 48, "bf16"), (1, 1, 5, 300, 7, "f32")]
 
 
 @pytest.mark.parametrize("case", POOL_CASES, ids=lambda c: "%dx%dx%dx%dx%d_%s" % c)
@@ -178,7 +187,8 @@ def test_maxpool(case):
 
 
 UP_CASES = [((6, 7, 6), (12, 14, 12)), ((3, 4, 3), (6, 7, 6)), ((2, 2, 2), (3, 4, 3)),
-            ((12, 12, 12), (24, 24, 24)), ((5, 3, 4), (5, 9, 7)), ((1, 1, 1), (2, 3, 1))]
+            ((12, 12, 12), (24, 24, 24)), ((5, 3, 4), (5, 9, 7)), ((1, 1, 1), (2, 3, 1)),
+            ((24, 28, 24), (48, 56, 48)), ((2, 130, 3), (4, 260, 5))]
 
 
 @pytest.mark.parametrize("sizes", UP_CASES, ids=lambda s: "%s_to_%s" % s)
