@@ -74,12 +74,31 @@ def cpu_baseline(budget_s=30.0):
                       "(0.533 TFLOP of conv work), float64 loops, bf16 store points"}
 
 
+def elementwise_hbm(tags):
+    """Achieved HBM bandwidth of the bandwidth-bound kernels: algorithmic bytes
+    (each tensor a kernel must read or write, once) over their hipEvent time,
+    overall and per kernel tag, as a fraction of the 8 TB/s peak."""
+    ew = [t for t in tags if t[3] == 0 and t[4] > 0]
+    tot_b = sum(t[4] for t in ew)
+    tot_ms = sum(t[2] for t in ew)
+    if tot_ms <= 0:
+        return None
+    per = sorted(ew, key=lambda t: -t[2])[:10]
+    return {"achieved": round(tot_b / (tot_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(tot_b / (tot_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "by_kernel": {t[0]: round(t[4] / (t[2] * 1e-3) / 1e9 / PEAK_HBM_GBS, 3)
+                          for t in per}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="after the timed steps, copy 256 MiB device-to-device once (the "
+                         "reference dispatch that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build runs the per-device training step "
@@ -124,9 +143,18 @@ def main():
         achieved = dom[4] / dom[1] / (per_launch_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 3), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 5), "traffic": None}
+    from paper_2104_05035_amd import profsum
+    roof["traffic"] = profsum.lookup(dom[0])
     roof["kernel"] = dom[0]
     roof["avg_launch_us"] = round(per_launch_ms * 1e3, 3)
     roof["launches_per_step"] = dom[1] // args.steps
+
+    if args.calib_copy:
+        src = torch.empty(256 * 1024 * 1024, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     tflops = conv_flops / (ms_step * 1e-3) / 1e12
     vols = n * mb / (ms_step * 1e-3)
@@ -146,6 +174,7 @@ def main():
         "wall_s_timed": round(wall, 3),
         "kernels_ms_per_step": {t[0]: round(t[2] / args.steps, 3) for t in kernels},
         "roofline": roof,
+        "elementwise_hbm": elementwise_hbm(tags),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()

@@ -45,6 +45,15 @@ template <> struct Elt<bf16> {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 
+// Workgroup ids are dealt round-robin over the 8 XCDs; remap them so that
+// XCD x runs the contiguous ids [x * q, (x + 1) * q) of a balanced split
+// (a ragged tail keeps its place).  Neighbouring tiles then share an L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nb) {
+    const int q = nb >> 3;
+    if (q == 0 || bid >= q * 8) return bid;
+    return (bid & 7) * q + (bid >> 3);
+}
+
 __host__ __device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) {
     return (a + b - 1) / b;
 }

@@ -46,14 +46,6 @@ union F16B {
 constexpr int kBD = 4, kBH = 8, kBW = 16;     // forward output tile
 constexpr int kWD = 2, kWH = 8, kWW = 16;     // weight-gradient voxel brick
 
-__device__ __forceinline__ int xcd_remap(int bid, int nb) {
-    // hardware deals ids round-robin over 8 XCDs; give XCD x the ids
-    // [x * q, (x + 1) * q) of a balanced split (ragged tail kept in place)
-    const int q = nb >> 3;
-    if (q == 0 || bid >= q * 8) return bid;
-    return (bid & 7) * q + (bid >> 3);
-}
-
 __device__ __forceinline__ f32x4 mfma(const F16B& a, const F16B& b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.b, b.b, c, 0, 0, 0);
 }
@@ -271,6 +263,13 @@ struct WgArgs {
 };
 }  // namespace
 
+// Partials are stored in the accumulators' register order: per workgroup a
+// block of kWgPart floats, element ((j * 4 + ct) * 4 + e) * 256 + tid, so every
+// store instruction writes 256 contiguous bytes.  wgrad_brick_reduce sums the
+// ranges in order and scatters each sum to its (co, ci, tap).
+constexpr int kWgNtap = 7;                       // taps per wave: wave + 4 j < 27
+constexpr int kWgPart = kWgNtap * 4 * 4 * 256;   // floats per workgroup partial
+
 template <int KS>
 __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
     constexpr int P = (KS - 1) / 2;
@@ -281,6 +280,8 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
     constexpr int CIS = ROWS * 32 + 16;  // bytes per input channel (rows of 16 bf16) + pad
     constexpr int KWS = 16 * CIS;        // bytes per kw-shifted copy
     constexpr int NTAP = (KT + 3) / 4;   // taps per wave
+    static_assert(NTAP == kWgNtap, "partial layout");
+    constexpr int NIT = (16 * ROWS + 255) / 256;  // staging items per thread
     __shared__ __align__(16) unsigned char xs[KS * KWS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -302,71 +303,95 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[j][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int64_t b = b_beg; b < b_end; ++b) {
-        const int tw = (int)(b % a.tw);
+    struct Brick {
+        int n, d0, h0, w0;
+    };
+    auto brick_at = [&](int64_t b) {
+        Brick k;
+        k.w0 = (int)(b % a.tw) * kWW;
         int64_t r = b / a.tw;
-        const int th = (int)(r % a.th);
+        k.h0 = (int)(r % a.th) * kWH;
         r /= a.th;
-        const int td = (int)(r % a.td);
-        const int n = (int)(r / a.td);
-        const int d0 = td * kWD, h0 = th * kWH, w0 = tw * kWW;
-        __syncthreads();
-        // item = (input channel, brick row): the row's 16 aligned voxels come in
-        // as two 16-byte loads plus one halo voxel on each side; the three
-        // kw-shifted copies are assembled in registers and stored as aligned
-        // 16-byte LDS rows (copy kw holds input columns w0 - 1 + kw ...).
-        for (int it = tid; it < 16 * ROWS; it += 256) {
-            const int row = it % ROWS, ci = it / ROWS;
-            const int dd = row / PH, hh = row % PH;
-            const int d = d0 - P + dd, h = h0 - P + hh;
-            uint32_t m[10];  // m[0] = (?, x[w0-1]), m[1..8] = x[w0..w0+15], m[9] = (x[w0+16], ?)
+        k.d0 = (int)(r % a.td) * kWD;
+        k.n = (int)(r / a.td);
+        return k;
+    };
+
+    // Staging item = (input channel, brick row): the row's 16 aligned voxels
+    // (two 16-byte loads) plus one halo voxel on each side, held in registers
+    // m[0] = (?, x[w0-1]), m[1..8] = x[w0 .. w0+15], m[9] = (x[w0+16], ?).
+    // The next brick's rows are fetched before the current brick's K loop so
+    // that the loads are in flight while the MFMAs run.
+    uint32_t m[NIT][10];
+    auto fetch = [&](const Brick& k) {
 #pragma unroll
-            for (int j = 0; j < 10; ++j) m[j] = 0u;
-            if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H) {
-                const bf16* p = a.x + ((int64_t)n * a.Ci + ci0 + ci) * V + d * HW +
-                                (int64_t)h * a.W + w0;
-                if (w0 + 8 <= a.W) {
-                    const uint4 u = *reinterpret_cast<const uint4*>(p);
-                    m[1] = u.x; m[2] = u.y; m[3] = u.z; m[4] = u.w;
-                }
-                if (w0 + 16 <= a.W) {
-                    const uint4 u = *reinterpret_cast<const uint4*>(p + 8);
-                    m[5] = u.x; m[6] = u.y; m[7] = u.z; m[8] = u.w;
-                }
-                if (w0 >= 1) m[0] = (uint32_t)p[-1] << 16;
-                if (w0 + 16 < a.W) m[9] = (uint32_t)p[16];
+        for (int q = 0; q < NIT; ++q) {
+#pragma unroll
+            for (int j = 0; j < 10; ++j) m[q][j] = 0u;
+            const int it = tid + 256 * q;
+            if (it >= 16 * ROWS) continue;
+            const int row = it % ROWS, ci = it / ROWS;
+            const int d = k.d0 - P + row / PH, h = k.h0 - P + row % PH;
+            if ((unsigned)d >= (unsigned)a.D || (unsigned)h >= (unsigned)a.H) continue;
+            const bf16* p = a.x + ((int64_t)k.n * a.Ci + ci0 + ci) * V + d * HW +
+                            (int64_t)h * a.W + k.w0;
+            if (k.w0 + 8 <= a.W) {
+                const uint4 u = *reinterpret_cast<const uint4*>(p);
+                m[q][1] = u.x; m[q][2] = u.y; m[q][3] = u.z; m[q][4] = u.w;
             }
+            if (k.w0 + 16 <= a.W) {
+                const uint4 u = *reinterpret_cast<const uint4*>(p + 8);
+                m[q][5] = u.x; m[q][6] = u.y; m[q][7] = u.z; m[q][8] = u.w;
+            }
+            if (k.w0 >= 1) m[q][0] = (uint32_t)p[-1] << 16;
+            if (k.w0 + 16 < a.W) m[q][9] = (uint32_t)p[16];
+        }
+    };
+    // copy kw holds input columns w0 - 1 + kw ... as aligned 16-byte LDS rows
+    auto commit = [&]() {
+#pragma unroll
+        for (int q = 0; q < NIT; ++q) {
+            const int it = tid + 256 * q;
+            if (it >= 16 * ROWS) continue;
+            const int row = it % ROWS, ci = it / ROWS;
             unsigned char* base = xs + ci * CIS + row * 32;
-            // kw = 1: columns w0 .. w0+15 (aligned)
-            *reinterpret_cast<uint4*>(base + KWS) = make_uint4(m[1], m[2], m[3], m[4]);
-            *reinterpret_cast<uint4*>(base + KWS + 16) = make_uint4(m[5], m[6], m[7], m[8]);
-            // kw = 0: columns w0-1 .. w0+14: dword i = (hi of m[i], lo of m[i+1])
+            *reinterpret_cast<uint4*>(base + KWS) = make_uint4(m[q][1], m[q][2], m[q][3], m[q][4]);
+            *reinterpret_cast<uint4*>(base + KWS + 16) =
+                make_uint4(m[q][5], m[q][6], m[q][7], m[q][8]);
             uint32_t s0[8], s2[8];
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                s0[i] = (m[i] >> 16) | (m[i + 1] << 16);
-                s2[i] = (m[i + 1] >> 16) | (m[i + 2] << 16);
+                s0[i] = (m[q][i] >> 16) | (m[q][i + 1] << 16);
+                s2[i] = (m[q][i + 1] >> 16) | (m[q][i + 2] << 16);
             }
             *reinterpret_cast<uint4*>(base) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
             *reinterpret_cast<uint4*>(base + 16) = make_uint4(s0[4], s0[5], s0[6], s0[7]);
-            // kw = 2: columns w0+1 .. w0+16
             *reinterpret_cast<uint4*>(base + 2 * KWS) = make_uint4(s2[0], s2[1], s2[2], s2[3]);
-            *reinterpret_cast<uint4*>(base + 2 * KWS + 16) = make_uint4(s2[4], s2[5], s2[6], s2[7]);
+            *reinterpret_cast<uint4*>(base + 2 * KWS + 16) =
+                make_uint4(s2[4], s2[5], s2[6], s2[7]);
         }
+    };
+
+    if (b_beg < b_end) fetch(brick_at(b_beg));
+    for (int64_t b = b_beg; b < b_end; ++b) {
+        const Brick k = brick_at(b);
+        __syncthreads();  // every wave is done reading the previous brick
+        commit();
         __syncthreads();
+        if (b + 1 < b_end) fetch(brick_at(b + 1));
         // K step s covers rows (h0 + 2*(s%4) + {0,1}) of depth d0 + s/4; dy
         // rows for step s+1 are fetched while step s multiplies
         auto load_a = [&](int s, F16B (&av)[4]) {
             const int dl = s / (kWH / 2);
             const int hl = (s % (kWH / 2)) * 2 + hl_l;
-            const int d = d0 + dl, h = h0 + hl, w = w0 + wl;
+            const int d = k.d0 + dl, h = k.h0 + hl, w = k.w0 + wl;
             const bool ok = d < a.D && h < a.H && w + 8 <= a.W;
 #pragma unroll
             for (int ct = 0; ct < 4; ++ct) {
                 av[ct].u = make_uint4(0u, 0u, 0u, 0u);
                 if (ok)
                     av[ct].u = *reinterpret_cast<const uint4*>(
-                        a.dy + ((int64_t)n * a.Co + co0 + ct * 16 + li) * V + d * HW +
+                        a.dy + ((int64_t)k.n * a.Co + co0 + ct * 16 + li) * V + d * HW +
                         (int64_t)h * a.W + w);
             }
         };
@@ -395,19 +420,39 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
         }
     }
 
-    float* out = a.part + (int64_t)range * a.Co * a.Ci * KT;
+    float* out = a.part + (int64_t)L * kWgPart + tid;
 #pragma unroll
-    for (int j = 0; j < NTAP; ++j) {
-        const int t = wave + 4 * j;
-        if (t >= KT) continue;
+    for (int j = 0; j < NTAP; ++j)
 #pragma unroll
         for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int co = co0 + ct * 16 + 4 * kg + e;
-                out[((int64_t)co * a.Ci + ci0 + li) * KT + t] = acc[j][ct][e];
-            }
-    }
+            for (int e = 0; e < 4; ++e) out[((j * 4 + ct) * 4 + e) * 256] = acc[j][ct][e];
+}
+
+// dw[co][ci][t] (+)= sum over ranges, in range order, of the partial element
+// that holds (co, ci, t).  One thread per partial element of a workgroup
+// tile (group = cig + cigs * cog), reading the ranges with coalesced loads.
+__global__ __launch_bounds__(256) void wgrad_brick_reduce(const float* __restrict__ part,
+                                                          int ranges, int groups, int cigs,
+                                                          int Ci, float* __restrict__ dw,
+                                                          int accumulate) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)groups * kWgPart) return;
+    const int group = (int)(i / kWgPart), r = (int)(i - (int64_t)group * kWgPart);
+    const int tid = r & 255, jce = r >> 8;
+    const int e = jce & 3, ct = (jce >> 2) & 3, j = jce >> 4;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int t = wave + 4 * j;
+    if (t >= 27) return;
+    const int cig = group % cigs, cog = group / cigs;
+    const int co = cog * 64 + ct * 16 + 4 * (lane >> 4) + e;
+    const int ci = cig * 16 + (lane & 15);
+    const int64_t stride = (int64_t)groups * kWgPart;
+    float s = 0.f;
+#pragma unroll 8
+    for (int z = 0; z < ranges; ++z) s += part[(int64_t)z * stride + i];
+    float* o = dw + ((int64_t)co * Ci + ci) * 27 + t;
+    *o = accumulate ? *o + s : s;
 }
 
 // ---------------------------------------------------------------- dispatch
@@ -440,7 +485,7 @@ static int64_t wgrad_bricks(const ConvGeom& g) {
 
 size_t brick_wgrad_ws(const ConvGeom& g) {
     const int R = wgrad_ranges(g, wgrad_bricks(g));
-    return (size_t)R * g.Co * g.Ci * 27 * sizeof(float);
+    return (size_t)R * (g.Ci / 16) * (g.Co / 64) * kWgPart * sizeof(float);
 }
 
 rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const void* w,
@@ -513,9 +558,14 @@ rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, 
         conv_brick_wgrad<3><<<(unsigned)((int64_t)Rreal * a.cigs * a.cogs), 256, 0, st>>>(a);
         RAT3D_LAUNCH_CHECK();
     }
-    const int64_t count = (int64_t)g.Co * g.Ci * 27;
-    ProfScope ps("wgrad_reduce", st, 0.0, 4.0 * count * (Rreal + 1 + accumulate));
-    return wgrad_reduce_launch(a.part, Rreal, count, dw, accumulate, st);
+    const int groups = a.cigs * a.cogs;
+    const int64_t count = (int64_t)groups * kWgPart;
+    ProfScope ps("wgrad_reduce", st, 0.0,
+                 4.0 * (count * Rreal + (double)g.Co * g.Ci * 27 * (1 + accumulate)));
+    wgrad_brick_reduce<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(
+        a.part, Rreal, groups, a.cigs, g.Ci, dw, accumulate);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
 }
 
 }  // namespace rat3d

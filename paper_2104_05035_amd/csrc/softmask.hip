@@ -418,174 +418,374 @@ __device__ __forceinline__ float x2_w(int o, int m, int n) {
     return m == half ? 0.75f : (m == half + 1 ? 0.25f : 0.f);
 }
 
-// Forward: one thread writes 8 consecutive fine voxels of one row.
-__global__ __launch_bounds__(kEwThreads) void up2_fwd_k(const bf16* __restrict__ x, int Di,
-                                                        int Hi, int Wi, bf16* __restrict__ y) {
-    const int Do = 2 * Di, Ho = 2 * Hi, Wo = 2 * Wi, G = Wo / 8;
-    const int t = blockIdx.x * kEwThreads + threadIdx.x;
-    if (t >= Ho * G) return;
-    const int oh = t / G, g = t - oh * G;
-    const int plane = blockIdx.y;  // nc * Do + od
-    const int nc = plane / Do, od = plane - nc * Do;
-    const int m0 = 4 * g;  // coarse w of the group: fine 8g .. 8g+7 read coarse m0-1 .. m0+4
-    const bf16* xp = x + (int64_t)nc * Di * Hi * Wi;
-    float acc[8];
+// ---------------------------------------------------------------- plane-staged fast paths
+// bfloat16 pooling and exact x2 upsampling.  A block owns a few consecutive
+// depth planes of one (n, c) volume.  Phase A streams the source planes it
+// needs with 16-byte loads (each source element read once per block) and
+// reduces them along depth into LDS; phase B finishes the in-plane stencil
+// from LDS and writes whole 8- or 4-element groups.  Neighbouring blocks
+// share at most one or two halo planes; the XCD-aware block order keeps
+// them in the same L2.
+
+constexpr int kPlanes = 2;           // destination depth planes per block
+constexpr size_t kPlaneLds = 65536;  // dynamic LDS limit of the staged kernels
+
+// 8 consecutive elements p .. p+7 of a plane of n elements (p % 8 == 0);
+// elements at or past n read as 0.  vec: n % 8 == 0 (16-byte aligned rows).
+__device__ __forceinline__ void ld8(const bf16* __restrict__ plane, int p, int n, bool vec,
+                                    float (&v)[8]) {
+    if (vec) {
+        const uint4 u = *reinterpret_cast<const uint4*>(plane + p);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-    const int dlo = (od >> 1) - 1, hlo = (oh >> 1) - 1;
-    for (int dd = 0; dd < 3; ++dd) {
-        const int md = dlo + dd;
-        if (md < 0 || md >= Di) continue;
-        const float wd = x2_w(od, md, Di);
-        if (wd == 0.f) continue;
+        for (int i = 0; i < 4; ++i) {
+            v[2 * i] = __uint_as_float(w[i] << 16);
+            v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = p + e < n ? bf2f(plane[p + e]) : 0.f;
+    }
+}
+
+// Max pool 3^3, stride 2, pad 1, bf16.  Phase A: per input (h, w), the
+// maximum over the depth taps of each output plane and the first kd that
+// reaches it.  Phase B: the 3 x 3 in-plane window; a later (kh, kw) wins on a
+// larger value, or on an equal value with a smaller kd -- together the first
+// maximum in (kd, kh, kw) order, as in pool_fwd_k.
+__global__ __launch_bounds__(kEwThreads) void pool332_fwd_pl(const bf16* __restrict__ x, int D,
+                                                             int H, int W, int Do, int Ho, int Wo,
+                                                             int nblk, bf16* __restrict__ y,
+                                                             uint8_t* __restrict__ am) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int HW = H * W, HW8 = (HW + 7) & ~7;
+    bf16* mv = reinterpret_cast<bf16*>(smem);                    // [kPlanes][HW8]
+    uint8_t* mk = smem + (size_t)kPlanes * HW8 * sizeof(bf16);  // [kPlanes][HW8]
+    const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int nc = L / nblk, od0 = (L - nc * nblk) * kPlanes;
+    const bool vec = (HW & 7) == 0;
+    const bf16* xv = x + (int64_t)nc * D * HW;
+    for (int p = threadIdx.x * 8; p < HW; p += kEwThreads * 8) {
+        float best[kPlanes][8];
+        int bkd[kPlanes][8];
+#pragma unroll
+        for (int j = 0; j < kPlanes; ++j)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                best[j][e] = 0.f;
+                bkd[j][e] = -1;
+            }
+#pragma unroll
+        for (int q = 0; q < 2 * kPlanes + 1; ++q) {
+            const int id = 2 * od0 - 1 + q;
+            if (id < 0 || id >= D) continue;
+            float v[8];
+            ld8(xv + (int64_t)id * HW, p, HW, vec, v);
+#pragma unroll
+            for (int j = 0; j < kPlanes; ++j) {
+                const int kd = q - 2 * j;
+                if (kd < 0 || kd > 2) continue;
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (bkd[j][e] < 0 || v[e] > best[j][e]) {
+                        best[j][e] = v[e];
+                        bkd[j][e] = kd;
+                    }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kPlanes; ++j) {
+            uint32_t w4[4], k2[2] = {0u, 0u};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                w4[i] = (__float_as_uint(best[j][2 * i]) >> 16) |
+                        (__float_as_uint(best[j][2 * i + 1]) & 0xffff0000u);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) k2[e >> 2] |= (uint32_t)(bkd[j][e] & 0xff) << (8 * (e & 3));
+            *reinterpret_cast<uint4*>(mv + j * HW8 + p) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+            *reinterpret_cast<uint2*>(mk + j * HW8 + p) = make_uint2(k2[0], k2[1]);
+        }
+    }
+    __syncthreads();
+    const int HWo = Ho * Wo;
+    for (int it = threadIdx.x; it < kPlanes * HWo; it += kEwThreads) {
+        const int j = it / HWo, r = it - j * HWo;
+        const int od = od0 + j;
+        if (od >= Do) break;
+        const int oh = r / Wo, ow = r - oh * Wo;
+        float best = 0.f;
+        int bk = 3, arg = -1;
+#pragma unroll
+        for (int kh = 0; kh < 3; ++kh) {
+            const int ih = 2 * oh - 1 + kh;
+            if ((unsigned)ih >= (unsigned)H) continue;
+#pragma unroll
+            for (int kw = 0; kw < 3; ++kw) {
+                const int iw = 2 * ow - 1 + kw;
+                if ((unsigned)iw >= (unsigned)W) continue;
+                const int s = j * HW8 + ih * W + iw;
+                const float v = bf2f(mv[s]);
+                const int kd = mk[s];
+                if (arg < 0 || v > best || (v == best && kd < bk)) {
+                    best = v;
+                    bk = kd;
+                    arg = kh * 3 + kw;
+                }
+            }
+        }
+        const int64_t o = ((int64_t)nc * Do + od) * HWo + r;
+        y[o] = f2bf(best);
+        am[o] = (uint8_t)(bk * 9 + arg);
+    }
+}
+
+// Max-pool gradient (3^3, stride 2, pad 1), bf16, W % 8 == 0.  A block owns
+// input planes 2*j0 .. 2*j0 + 2*kPlanes - 1, whose windows lie in output
+// planes j0 .. j0 + kPlanes; their dy and argmax are staged in LDS, then
+// each thread gathers 8 consecutive input voxels of a row.
+__global__ __launch_bounds__(kEwThreads) void pool332_bwd_pl(const bf16* __restrict__ dy,
+                                                             const uint8_t* __restrict__ am, int D,
+                                                             int H, int W, int Do, int Ho, int Wo,
+                                                             int nblk, bf16* __restrict__ dx,
+                                                             int accumulate) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    constexpr int NP = kPlanes + 1;
+    const int HWo = Ho * Wo;
+    bf16* sdy = reinterpret_cast<bf16*>(smem);                  // [NP][HWo]
+    uint8_t* sam = smem + (size_t)NP * HWo * sizeof(bf16);      // [NP][HWo]
+    const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int nc = L / nblk, j0 = (L - nc * nblk) * kPlanes;
+    const int np = min(NP, Do - j0);
+    const int64_t ob = ((int64_t)nc * Do + j0) * HWo;
+    for (int i = threadIdx.x; i < np * HWo; i += kEwThreads) {
+        sdy[i] = dy[ob + i];
+        sam[i] = am[ob + i];
+    }
+    __syncthreads();
+    const int G = W >> 3;
+    for (int it = threadIdx.x; it < 2 * kPlanes * H * G; it += kEwThreads) {
+        const int dl = it / (H * G), r = it - dl * (H * G);
+        const int id = 2 * j0 + dl;
+        if (id >= D) break;
+        const int ih = r / G, g = r - ih * G;
+        int od[2], td[2], oh[2], th[2];
+        const int nd = pool332_windows(id, Do, od, td);
+        const int nh = pool332_windows(ih, Ho, oh, th);
+        float acc[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+        for (int a = 0; a < nd; ++a)
+            for (int b = 0; b < nh; ++b) {
+                const int rb = ((od[a] - j0) * Ho + oh[b]) * Wo;
+                const int plane_tap = td[a] * 3 + th[b];
+#pragma unroll
+                for (int q = 0; q < 6; ++q) {
+                    const int ow = 4 * g - 1 + q;
+                    if (ow < 0 || ow >= Wo) continue;
+                    const int arg = sam[rb + ow];
+                    if (arg / 3 != plane_tap) continue;
+                    const int e = 2 * ow - 1 + arg % 3 - 8 * g;  // argmax column within the group
+                    if (e >= 0 && e < 8) acc[e] += bf2f(sdy[rb + ow]);
+                }
+            }
+        bf16* q = dx + (((int64_t)nc * D + id) * H + ih) * W + 8 * g;
+        uint4* q4 = reinterpret_cast<uint4*>(q);
+        if (accumulate) {
+            const uint4 o = *q4;
+            const uint32_t ws[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                acc[2 * i] += __uint_as_float(ws[i] << 16);
+                acc[2 * i + 1] += __uint_as_float(ws[i] & 0xffff0000u);
+            }
+        }
+        uint32_t w4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            w4[i] = (uint32_t)f2bf(acc[2 * i]) | ((uint32_t)f2bf(acc[2 * i + 1]) << 16);
+        *q4 = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+    }
+}
+
+// Exact x2 trilinear, bf16, Wi % 4 == 0.  A block owns fine planes
+// 2*m0 .. 2*m0 + 2*kPlanes - 1.  Phase A blends coarse planes m0-1 .. m0+kPlanes
+// along depth into LDS (float32); phase B blends rows and columns and writes
+// 8 fine voxels of a row per item.
+__global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict__ x, int Di,
+                                                         int Hi, int Wi, int nblk,
+                                                         bf16* __restrict__ y) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    constexpr int NF = 2 * kPlanes;
+    const int HWi = Hi * Wi, HW8 = (HWi + 7) & ~7;
+    float* t = reinterpret_cast<float*>(smem);  // [NF][HW8]
+    const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int nc = L / nblk, m0 = (L - nc * nblk) * kPlanes;
+    const int Do = 2 * Di, Ho = 2 * Hi, Wo = 2 * Wi;
+    const bool vec = (HWi & 7) == 0;
+    const bf16* xv = x + (int64_t)nc * Di * HWi;
+    for (int p = threadIdx.x * 8; p < HWi; p += kEwThreads * 8) {
+        float acc[NF][8];
+#pragma unroll
+        for (int l = 0; l < NF; ++l)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[l][e] = 0.f;
+#pragma unroll
+        for (int q = 0; q < kPlanes + 2; ++q) {
+            const int md = m0 - 1 + q;
+            if (md < 0 || md >= Di) continue;
+            float v[8];
+            ld8(xv + (int64_t)md * HWi, p, HWi, vec, v);
+#pragma unroll
+            for (int l = 0; l < NF; ++l) {
+                const float wd = x2_w(2 * m0 + l, md, Di);
+                if (wd != 0.f)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[l][e] += wd * v[e];
+            }
+        }
+#pragma unroll
+        for (int l = 0; l < NF; ++l) {
+            float4* d4 = reinterpret_cast<float4*>(t + l * HW8 + p);
+            d4[0] = make_float4(acc[l][0], acc[l][1], acc[l][2], acc[l][3]);
+            d4[1] = make_float4(acc[l][4], acc[l][5], acc[l][6], acc[l][7]);
+        }
+    }
+    __syncthreads();
+    const int G = Wo >> 3;
+    for (int it = threadIdx.x; it < NF * Ho * G; it += kEwThreads) {
+        const int l = it / (Ho * G), r = it - l * (Ho * G);
+        const int od = 2 * m0 + l;
+        if (od >= Do) break;
+        const int oh = r / G, g = r - oh * G;
+        const int m0w = 4 * g;  // fine 8g .. 8g+7 read coarse m0w-1 .. m0w+4
+        float row[6];
+#pragma unroll
+        for (int c = 0; c < 6; ++c) row[c] = 0.f;
+        const int hlo = (oh >> 1) - 1;
+#pragma unroll
         for (int hh = 0; hh < 3; ++hh) {
             const int mh = hlo + hh;
             if (mh < 0 || mh >= Hi) continue;
-            const float wdh = wd * x2_w(oh, mh, Hi);
-            if (wdh == 0.f) continue;
-            const bf16* row = xp + ((int64_t)md * Hi + mh) * Wi;
-            float c[6];  // coarse m0-1 .. m0+4 (clamped reads; weights decide)
+            const float wh = x2_w(oh, mh, Hi);
+            if (wh == 0.f) continue;
+            const float* src = t + l * HW8 + mh * Wi;
 #pragma unroll
-            for (int j = 0; j < 6; ++j) {
-                const int m = min(max(m0 - 1 + j, 0), Wi - 1);
-                c[j] = bf2f(row[m]);
-            }
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int o = 8 * g + j;
-                float v = 0.f;
-#pragma unroll
-                for (int q = 0; q < 6; ++q) {
-                    const int m = m0 - 1 + q;
-                    if (m >= 0 && m < Wi) v += x2_w(o, m, Wi) * c[q];
-                }
-                acc[j] += wdh * v;
+            for (int c = 0; c < 6; ++c) {
+                const int m = min(max(m0w - 1 + c, 0), Wi - 1);
+                row[c] += wh * src[m];
             }
         }
-    }
-    uint32_t w4[4];
+        float out[8];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-        w4[j] = (uint32_t)f2bf(acc[2 * j]) | ((uint32_t)f2bf(acc[2 * j + 1]) << 16);
-    *reinterpret_cast<uint4*>(y + (int64_t)plane * Ho * Wo + (int64_t)oh * Wo + 8 * g) =
-        make_uint4(w4[0], w4[1], w4[2], w4[3]);
+        for (int j = 0; j < 8; ++j) {
+            const int o = 8 * g + j;
+            float v = 0.f;
+#pragma unroll
+            for (int c = 0; c < 6; ++c) {
+                const int m = m0w - 1 + c;
+                if (m >= 0 && m < Wi) v += x2_w(o, m, Wi) * row[c];
+            }
+            out[j] = v;
+        }
+        uint32_t w4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            w4[i] = (uint32_t)f2bf(out[2 * i]) | ((uint32_t)f2bf(out[2 * i + 1]) << 16);
+        *reinterpret_cast<uint4*>(y + (((int64_t)nc * Do + od) * Ho + oh) * Wo + 8 * g) =
+            make_uint4(w4[0], w4[1], w4[2], w4[3]);
+    }
 }
 
-// Backward: one thread writes 4 consecutive coarse voxels of one row, reading
-// fine columns 8g-1 .. 8g+8 of the 4 x 4 fine rows that touch them.
-__global__ __launch_bounds__(kEwThreads) void up2_bwd_k(const bf16* __restrict__ dy, int Di,
-                                                        int Hi, int Wi, bf16* __restrict__ dx,
-                                                        int accumulate) {
-    const int Do = 2 * Di, Ho = 2 * Hi, Wo = 2 * Wi, G = Wi / 4;
-    const int t = blockIdx.x * kEwThreads + threadIdx.x;
-    if (t >= Hi * G) return;
-    const int ih = t / G, g = t - ih * G;
-    const int plane = blockIdx.y;  // nc * Di + id
-    const int nc = plane / Di, id = plane - nc * Di;
-    const int m0 = 4 * g;
-    const bf16* gp = dy + (int64_t)nc * Do * Ho * Wo;
-    float rowacc[10];  // fine columns 8g-1 .. 8g+8, weighted over the (d, h) rows
+// Transpose of up2_fwd_pl, bf16, Wi % 4 == 0.  A block owns coarse planes
+// m0 .. m0 + kPlanes - 1; phase A blends fine planes 2*m0-1 .. 2*m0+2*kPlanes
+// along depth into LDS (float32), phase B gathers the 4 x 10 fine rows and
+// columns of 4 consecutive coarse voxels of a row.
+__global__ __launch_bounds__(kEwThreads) void up2_bwd_pl(const bf16* __restrict__ dy, int Di,
+                                                         int Hi, int Wi, int nblk,
+                                                         bf16* __restrict__ dx, int accumulate) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int Do = 2 * Di, Ho = 2 * Hi, Wo = 2 * Wi;
+    const int HWo = Ho * Wo;  // a multiple of 8 (Wo % 8 == 0)
+    float* t = reinterpret_cast<float*>(smem);  // [kPlanes][HWo]
+    const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int nc = L / nblk, m0 = (L - nc * nblk) * kPlanes;
+    const bf16* gv = dy + (int64_t)nc * Do * HWo;
+    for (int p = threadIdx.x * 8; p < HWo; p += kEwThreads * 8) {
+        float acc[kPlanes][8];
 #pragma unroll
-    for (int j = 0; j < 10; ++j) rowacc[j] = 0.f;
-    for (int dd = 0; dd < 4; ++dd) {
-        const int od = 2 * id - 1 + dd;
-        if (od < 0 || od >= Do) continue;
-        const float wd = x2_w(od, id, Di);
-        if (wd == 0.f) continue;
+        for (int l = 0; l < kPlanes; ++l)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[l][e] = 0.f;
+#pragma unroll
+        for (int q = 0; q < 2 * kPlanes + 2; ++q) {
+            const int od = 2 * m0 - 1 + q;
+            if (od < 0 || od >= Do) continue;
+            float v[8];
+            ld8(gv + (int64_t)od * HWo, p, HWo, true, v);
+#pragma unroll
+            for (int l = 0; l < kPlanes; ++l) {
+                if (m0 + l >= Di) continue;
+                const float wd = x2_w(od, m0 + l, Di);
+                if (wd != 0.f)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[l][e] += wd * v[e];
+            }
+        }
+#pragma unroll
+        for (int l = 0; l < kPlanes; ++l) {
+            float4* d4 = reinterpret_cast<float4*>(t + l * HWo + p);
+            d4[0] = make_float4(acc[l][0], acc[l][1], acc[l][2], acc[l][3]);
+            d4[1] = make_float4(acc[l][4], acc[l][5], acc[l][6], acc[l][7]);
+        }
+    }
+    __syncthreads();
+    const int G = Wi >> 2;
+    for (int it = threadIdx.x; it < kPlanes * Hi * G; it += kEwThreads) {
+        const int l = it / (Hi * G), r = it - l * (Hi * G);
+        const int m = m0 + l;
+        if (m >= Di) break;
+        const int ih = r / G, g = r - ih * G;
+        float rowacc[10];  // fine columns 8g-1 .. 8g+8 blended over the fine rows
+#pragma unroll
+        for (int j = 0; j < 10; ++j) rowacc[j] = 0.f;
+#pragma unroll
         for (int hh = 0; hh < 4; ++hh) {
             const int oh = 2 * ih - 1 + hh;
             if (oh < 0 || oh >= Ho) continue;
-            const float wdh = wd * x2_w(oh, ih, Hi);
-            if (wdh == 0.f) continue;
-            const bf16* row = gp + ((int64_t)od * Ho + oh) * Wo;
-            const uint4 u = *reinterpret_cast<const uint4*>(row + 8 * g);  // 8g .. 8g+7
-            const uint32_t ws[4] = {u.x, u.y, u.z, u.w};
+            const float wh = x2_w(oh, ih, Hi);
+            if (wh == 0.f) continue;
+            const float* src = t + l * HWo + oh * Wo;
+            const float4 a = *reinterpret_cast<const float4*>(src + 8 * g);
+            const float4 b = *reinterpret_cast<const float4*>(src + 8 * g + 4);
+            rowacc[1] += wh * a.x; rowacc[2] += wh * a.y; rowacc[3] += wh * a.z;
+            rowacc[4] += wh * a.w; rowacc[5] += wh * b.x; rowacc[6] += wh * b.y;
+            rowacc[7] += wh * b.z; rowacc[8] += wh * b.w;
+            if (g > 0) rowacc[0] += wh * src[8 * g - 1];
+            if (8 * g + 8 < Wo) rowacc[9] += wh * src[8 * g + 8];
+        }
+        float out[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                rowacc[1 + 2 * j] += wdh * __uint_as_float(ws[j] << 16);
-                rowacc[2 + 2 * j] += wdh * __uint_as_float(ws[j] & 0xffff0000u);
+        for (int k = 0; k < 4; ++k) {
+            const int mw = 4 * g + k;
+            float v = 0.f;
+#pragma unroll
+            for (int j = 0; j < 10; ++j) {
+                const int o = 8 * g - 1 + j;
+                if (o >= 0 && o < Wo) v += x2_w(o, mw, Wi) * rowacc[j];
             }
-            if (8 * g - 1 >= 0) rowacc[0] += wdh * bf2f(row[8 * g - 1]);
-            if (8 * g + 8 < Wo) rowacc[9] += wdh * bf2f(row[8 * g + 8]);
+            out[k] = v;
         }
-    }
-    float out[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int m = m0 + k;
-        float v = 0.f;
-#pragma unroll
-        for (int j = 0; j < 10; ++j) {
-            const int o = 8 * g - 1 + j;
-            if (o >= 0 && o < Wo) v += x2_w(o, m, Wi) * rowacc[j];
+        uint2* q2 = reinterpret_cast<uint2*>(dx + (((int64_t)nc * Di + m) * Hi + ih) * Wi + 4 * g);
+        if (accumulate) {
+            const uint2 o = *q2;
+            out[0] += __uint_as_float(o.x << 16);
+            out[1] += __uint_as_float(o.x & 0xffff0000u);
+            out[2] += __uint_as_float(o.y << 16);
+            out[3] += __uint_as_float(o.y & 0xffff0000u);
         }
-        out[k] = v;
+        *q2 = make_uint2((uint32_t)f2bf(out[0]) | ((uint32_t)f2bf(out[1]) << 16),
+                         (uint32_t)f2bf(out[2]) | ((uint32_t)f2bf(out[3]) << 16));
     }
-    bf16* q = dx + (int64_t)plane * Hi * Wi + (int64_t)ih * Wi + m0;
-    uint2* q2 = reinterpret_cast<uint2*>(q);
-    if (accumulate) {
-        const uint2 o = *q2;
-        out[0] += __uint_as_float(o.x << 16);
-        out[1] += __uint_as_float(o.x & 0xffff0000u);
-        out[2] += __uint_as_float(o.y << 16);
-        out[3] += __uint_as_float(o.y & 0xffff0000u);
-    }
-    *q2 = make_uint2((uint32_t)f2bf(out[0]) | ((uint32_t)f2bf(out[1]) << 16),
-                     (uint32_t)f2bf(out[2]) | ((uint32_t)f2bf(out[3]) << 16));
-}
-
-// Max-pool gradient (3^3, stride 2, pad 1), bf16: one thread writes 8
-// consecutive input voxels of a row; the windows along w are 4g-1 .. 4g+4.
-__global__ __launch_bounds__(kEwThreads) void pool332_bwd8_k(const bf16* __restrict__ dy,
-                                                             const uint8_t* __restrict__ am,
-                                                             int D, int H, int W, int Do, int Ho,
-                                                             int Wo, bf16* __restrict__ dx,
-                                                             int accumulate) {
-    const int G = W / 8;
-    const int t = blockIdx.x * kEwThreads + threadIdx.x;
-    if (t >= H * G) return;
-    const int ih = t / G, g = t - ih * G;
-    const int plane = blockIdx.y;  // nc * D + id
-    const int nc = plane / D, id = plane - nc * D;
-    int od[2], td[2], oh[2], th[2];
-    const int nd = pool332_windows(id, Do, od, td);
-    const int nh = pool332_windows(ih, Ho, oh, th);
-    const int64_t ob = (int64_t)nc * Do * Ho * Wo;
-    float acc[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-    for (int a = 0; a < nd; ++a)
-        for (int b = 0; b < nh; ++b) {
-            const int64_t rb = ob + ((int64_t)od[a] * Ho + oh[b]) * Wo;
-            const int base = (td[a] * 3 + th[b]) * 3;
-#pragma unroll
-            for (int q = 0; q < 6; ++q) {
-                const int ow = 4 * g - 1 + q;
-                if (ow < 0 || ow >= Wo) continue;
-                const int arg = (int)am[rb + ow];
-                if (arg / 3 != base / 3) continue;  // argmax in another (kd, kh) plane
-                // the window's argmax column iw = 2*ow - 1 + kw, kw = arg % 3
-                const int iw = 2 * ow - 1 + (arg - base);
-                const int j = iw - 8 * g;
-                if (j >= 0 && j < 8) acc[j] += bf2f(dy[rb + ow]);
-            }
-        }
-    bf16* q = dx + (int64_t)plane * H * W + (int64_t)ih * W + 8 * g;
-    uint4* q4 = reinterpret_cast<uint4*>(q);
-    if (accumulate) {
-        const uint4 o = *q4;
-        const uint32_t ws[4] = {o.x, o.y, o.z, o.w};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            acc[2 * j] += __uint_as_float(ws[j] << 16);
-            acc[2 * j + 1] += __uint_as_float(ws[j] & 0xffff0000u);
-        }
-    }
-    uint32_t w4[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        w4[j] = (uint32_t)f2bf(acc[2 * j]) | ((uint32_t)f2bf(acc[2 * j + 1]) << 16);
-    *q4 = make_uint4(w4[0], w4[1], w4[2], w4[3]);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -596,6 +796,15 @@ rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, ra
     const unsigned blocks = (unsigned)ceil_div(total, kEwThreads);
     const double es = dt == RAT3D_BF16 ? 2.0 : 4.0;
     ProfScope ps("pool_fwd", st, 0.0, es * ((double)N * C * D * H * W + total) + total);
+    const int HW8 = (H * W + 7) & ~7;
+    const size_t lds_f = (size_t)kPlanes * HW8 * 3;
+    if (k == 3 && s == 2 && p == 1 && dt == RAT3D_BF16 && lds_f <= kPlaneLds) {
+        const int nblk = (int)ceil_div(Do, kPlanes);
+        pool332_fwd_pl<<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_f, st>>>(
+            (const bf16*)x, D, H, W, Do, Ho, Wo, nblk, (bf16*)y, argmax);
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
     if (k == 3 && s == 2 && p == 1 && (int64_t)N * C * Do < 65536) {
         const dim3 grid((unsigned)ceil_div((int64_t)Ho * Wo, kEwThreads), N * C * Do);
         if (dt == RAT3D_BF16)
@@ -626,11 +835,11 @@ rat3d_status pool_bwd(int N, int C, int D, int H, int W, int k, int s, int p, ra
     const double es = dt == RAT3D_BF16 ? 2.0 : 4.0;
     const double small = (double)N * C * Do * Ho * Wo;
     ProfScope ps("pool_bwd", st, 0.0, es * (small + total * (1 + accumulate)) + small);
-    if (k == 3 && s == 2 && p == 1 && dt == RAT3D_BF16 && W % 8 == 0 &&
-        (int64_t)N * C * D < 65536) {
-        const dim3 grid((unsigned)ceil_div((int64_t)H * (W / 8), kEwThreads), N * C * D);
-        pool332_bwd8_k<<<grid, kEwThreads, 0, st>>>((const bf16*)dy, argmax, D, H, W, Do, Ho, Wo,
-                                                    (bf16*)dx, accumulate);
+    const size_t lds_b = (size_t)(kPlanes + 1) * Ho * Wo * 3;
+    if (k == 3 && s == 2 && p == 1 && dt == RAT3D_BF16 && W % 8 == 0 && lds_b <= kPlaneLds) {
+        const int nblk = (int)ceil_div(D, 2 * kPlanes);
+        pool332_bwd_pl<<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_b, st>>>(
+            (const bf16*)dy, argmax, D, H, W, Do, Ho, Wo, nblk, (bf16*)dx, accumulate);
         RAT3D_LAUNCH_CHECK();
         return RAT3D_OK;
     }
@@ -667,9 +876,11 @@ rat3d_status up_fwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
     ProfScope ps("up_fwd", st, 0.0,
                  (dt == RAT3D_BF16 ? 2.0 : 4.0) * ((double)N * C * Di * Hi * Wi + total));
     const bool x2 = Do == 2 * Di && Ho == 2 * Hi && Wo == 2 * Wi;
-    if (x2 && dt == RAT3D_BF16 && Wo % 8 == 0 && (int64_t)N * C * Do < 65536) {
-        const dim3 grid((unsigned)ceil_div((int64_t)Ho * (Wo / 8), kEwThreads), N * C * Do);
-        up2_fwd_k<<<grid, kEwThreads, 0, st>>>((const bf16*)x, Di, Hi, Wi, (bf16*)y);
+    const size_t lds_f = (size_t)2 * kPlanes * ((Hi * Wi + 7) & ~7) * sizeof(float);
+    if (x2 && dt == RAT3D_BF16 && Wi % 4 == 0 && lds_f <= kPlaneLds) {
+        const int nblk = (int)ceil_div(Di, kPlanes);
+        up2_fwd_pl<<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_f, st>>>(
+            (const bf16*)x, Di, Hi, Wi, nblk, (bf16*)y);
         RAT3D_LAUNCH_CHECK();
         return RAT3D_OK;
     }
@@ -703,10 +914,11 @@ rat3d_status up_bwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
                  (dt == RAT3D_BF16 ? 2.0 : 4.0) *
                      ((double)N * C * Do * Ho * Wo + total * (1 + accumulate)));
     const bool x2 = Do == 2 * Di && Ho == 2 * Hi && Wo == 2 * Wi;
-    if (x2 && dt == RAT3D_BF16 && Wi % 4 == 0 && (int64_t)N * C * Di < 65536) {
-        const dim3 grid((unsigned)ceil_div((int64_t)Hi * (Wi / 4), kEwThreads), N * C * Di);
-        up2_bwd_k<<<grid, kEwThreads, 0, st>>>((const bf16*)dy, Di, Hi, Wi, (bf16*)dx,
-                                               accumulate);
+    const size_t lds_b = (size_t)kPlanes * Ho * Wo * sizeof(float);
+    if (x2 && dt == RAT3D_BF16 && Wi % 4 == 0 && lds_b <= kPlaneLds) {
+        const int nblk = (int)ceil_div(Di, kPlanes);
+        up2_bwd_pl<<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_b, st>>>(
+            (const bf16*)dy, Di, Hi, Wi, nblk, (bf16*)dx, accumulate);
         RAT3D_LAUNCH_CHECK();
         return RAT3D_OK;
     }

@@ -157,7 +157,9 @@ def test_bn(case, relu, resid):
 
 POOL_CASES = [(2, 3, 9, 8, 7, "bf16"), (2, 16, 24, 28, 24, "bf16"), (1, 2, 3, 4, 3, "f32"),
               (1, 1, 2, 2, 2, "bf16"), (2, 4, 6, 7, 6, "bf16"), (1, 1, 1, 1, 1, "f32"),
-              (1, 2, 48, 56, 48, "bf16"), (1, 1, 5, 300, 7, "f32")]
+              (1, 2, 48, 56, 48, "bf16"), (1, 1, 5, 300, 7, "f32"),
+              # plane-staged bf16 paths: odd depth/height, W a multiple of 8
+              (1, 3, 7, 5, 16, "bf16"), (2, 2, 5, 3, 8, "bf16")]
 
 
 @pytest.mark.parametrize("case", POOL_CASES, ids=lambda c: "%dx%dx%dx%dx%d_%s" % c)
@@ -188,7 +190,9 @@ def test_maxpool(case):
 
 UP_CASES = [((6, 7, 6), (12, 14, 12)), ((3, 4, 3), (6, 7, 6)), ((2, 2, 2), (3, 4, 3)),
             ((12, 12, 12), (24, 24, 24)), ((5, 3, 4), (5, 9, 7)), ((1, 1, 1), (2, 3, 1)),
-            ((24, 28, 24), (48, 56, 48)), ((2, 130, 3), (4, 260, 5))]
+            ((24, 28, 24), (48, 56, 48)), ((2, 130, 3), (4, 260, 5)),
+            # exact x2 with a plane size that is not a multiple of 8, odd depth
+            ((3, 5, 4), (6, 10, 8)), ((5, 3, 8), (10, 6, 16))]
 
 
 @pytest.mark.parametrize("sizes", UP_CASES, ids=lambda s: "%s_to_%s" % s)
