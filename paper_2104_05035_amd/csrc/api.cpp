@@ -8,6 +8,24 @@
 
 namespace rat3d {
 
+int device_cus() {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cache[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n <= 0)
+            n = 256;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+}  // namespace rat3d
+
+namespace rat3d {
+
 static thread_local std::string g_last_error;
 
 void set_error(const char* fmt, ...) {

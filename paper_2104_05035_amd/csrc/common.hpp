@@ -16,12 +16,16 @@ typedef uint16_t bf16;  // bfloat16 storage (upper half of a float32)
 __device__ __forceinline__ float bf2f(bf16 h) { return __uint_as_float((uint32_t)h << 16); }
 
 __device__ __forceinline__ bf16 f2bf(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16)((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (bf16)(u >> 16);
+    // v_cvt_pk_bf16_f32: round to nearest even, NaN stays a quiet NaN
+    return __builtin_bit_cast(bf16, (__bf16)f);
 }
 
+// Two floats to packed bfloat16 (lo in bits 0-15), one instruction.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+    const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
 // Storage-type traits: load as float, store from float.
 template <typename T> struct Elt;
 template <> struct Elt<float> {
@@ -45,6 +49,26 @@ template <> struct Elt<bf16> {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 
+// Raw buffer loads: a 128-bit resource in SGPRs (base, byte size) plus a
+// per-lane byte offset (VGPR) and a wave-uniform byte offset (SGPR), so the
+// address arithmetic of the hot loops stays off the vector ALU.  Callers keep
+// every offset inside the buffer.
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                             0x00020000);
+}
+__device__ __forceinline__ uint4 buf_ld16(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                          uint32_t soff) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 buf_ld8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+    return make_uint2(v.x, v.y);
+}
+
 // Workgroup ids are dealt round-robin over the 8 XCDs; remap them so that
 // XCD x runs the contiguous ids [x * q, (x + 1) * q) of a balanced split
 // (a ragged tail keeps its place).  Neighbouring tiles then share an L2.
@@ -63,6 +87,9 @@ inline int out_dim(int in, int k, int s, int p) { return (in + 2 * p - k) / s + 
 // Launch-error check used by host launchers: returns RAT3D_EHIP from the
 // enclosing function after recording the message.
 void set_error(const char* fmt, ...);
+
+// Compute units of the current device (queried once per device; 256 on MI355X).
+int device_cus();
 #define RAT3D_LAUNCH_CHECK()                                                          \
     do {                                                                              \
         hipError_t e_ = hipGetLastError();                                            \

@@ -57,6 +57,8 @@ struct FdArgs {
     bf16* dst;         // [N][Ct][D][H][W]
     int N, Cs, Ct, D, H, W;
     int td, th, tw;    // tiles per axis
+    int cogs;          // output-channel groups of NT * 16
+    int ntiles;        // N * td * th * tw * cogs
     int accumulate;
 };
 
@@ -88,164 +90,394 @@ __global__ void prep_dgrad_weights(const bf16* __restrict__ w, int Co, int Ci, i
 }
 
 // ---------------------------------------------------------------- fwd / dgrad
-template <int KS, int NT>
-__global__ __launch_bounds__(256, 2) void conv_brick_fd(FdArgs a) {
+// LDS brick layout: voxel v = (dd * PH + hh) * PW + ww holds 64 bytes, four
+// 16-byte slots of eight channels; channel group cg sits in slot
+// cg ^ ((ww >> 1) & 3).  The swizzle depends on the brick column only, so the
+// eight rows a wave reads for one tap differ by constant offsets, and the 16
+// lanes of an MFMA row group (16 consecutive columns) hit distinct banks.
+template <int KS>
+__device__ __forceinline__ uint32_t brick_slot_off(int ww, int cg) {
+    return (uint32_t)(ww * 64 + ((cg ^ ((ww >> 1) & 3)) << 4));
+}
+
+__device__ __forceinline__ uint32_t pack_lo(uint32_t lo, uint32_t hi) {
+    return __builtin_amdgcn_perm(hi, lo, 0x05040100u);  // lo16(lo) | lo16(hi) << 16
+}
+__device__ __forceinline__ uint32_t pack_hi(uint32_t lo, uint32_t hi) {
+    return __builtin_amdgcn_perm(hi, lo, 0x07060302u);  // hi16(lo) | hi16(hi) << 16
+}
+
+// Persistent producer/consumer kernel, one 512-thread workgroup per CU.
+// Waves 0-3 (consumers) multiply: each owns one output depth slice of the
+// 4 x 8 x 16 tile, 8 rows x NT*16 channels of accumulators.  Waves 4-7
+// (producers) stage the next (tile, 32-channel chunk) step into the other of
+// two LDS brick buffers while the consumers work on the current one; a step
+// ends with one workgroup barrier.  A workgroup walks its tiles in a fixed
+// order: with a grid that is a multiple of 8, the workgroups of one XCD share
+// a contiguous range of tiles, so halo lines are reused from that XCD's L2.
+// Workgroup barrier that orders LDS accesses only (no wait for global stores).
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int KS, int NT, int RD>
+__global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     constexpr int P = (KS - 1) / 2;
     constexpr int PD = kBD + KS - 1, PH = kBH + KS - 1, PW = kBW + KS - 1;
     constexpr int NV = PD * PH * PW;
     constexpr int KT = KS * KS * KS;
-    __shared__ uint4 brick[NV * 4];
+    constexpr uint32_t BB = NV * 64;            // bytes per brick buffer
+    __shared__ __align__(16) unsigned char lds[2 * BB];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int L = xcd_remap(blockIdx.x, gridDim.x);
-    const int tw = L % a.tw;
-    int r = L / a.tw;
-    const int th = r % a.th;
-    r /= a.th;
-    const int td = r % a.td;
-    const int n = r / a.td;
-    const int d0 = td * kBD, h0 = th * kBH, w0 = tw * kBW;
-    const int co0 = blockIdx.y * NT * 16;
-    const int64_t HW = (int64_t)a.H * a.W, V = HW * a.D;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const bool consumer = wave < 4;
+    const int nchunk = a.Cs >> 5;
+    const int HW = a.H * a.W, V = HW * a.D;
+    const uint32_t Vb = (uint32_t)V * 2u;
 
-    f32x4 acc[8][NT];
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int t_first, t_stride, t_end;
+    {
+        const int G = gridDim.x, b = blockIdx.x;
+        if ((G & 7) == 0) {
+            const int x = b & 7;
+            t_first = (int)((int64_t)a.ntiles * x / 8) + (b >> 3);
+            t_stride = G >> 3;
+            t_end = (int)((int64_t)a.ntiles * (x + 1) / 8);
+        } else {
+            t_first = b;
+            t_stride = G;
+            t_end = a.ntiles;
+        }
+    }
+    const int S = (t_first < t_end ? (t_end - t_first + t_stride - 1) / t_stride : 0) * nchunk;
 
-    const int li = lane & 15, kg = lane >> 4;
-    for (int c0 = 0; c0 < a.Cs; c0 += 32) {
-        __syncthreads();
-        if (a.W % 4 == 0) {
-            // item = (channel group, brick row, aligned 4-wide column group):
-            // eight 8-byte loads (one per channel) give 4 voxels x 8 channels
-            constexpr int GS0 = -4 * ((P + 3) / 4);          // first group, relative to w0
-            constexpr int NG = (PW - P - GS0 + 3) / 4;       // groups covering the brick row
-            for (int it = tid; it < 4 * PD * PH * NG; it += 256) {
-                const int q = it % NG;
-                const int rr = it / NG;
-                const int row = rr % (PD * PH), cg = rr / (PD * PH);
-                const int hh = row % PH, dd = row / PH;
-                const int d = d0 - P + dd, h = h0 - P + hh, wg = w0 + GS0 + 4 * q;
-                uint2 v[8];
-                if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
-                    (unsigned)wg < (unsigned)a.W) {
-                    const bf16* p = a.src + ((int64_t)n * a.Cs + c0 + cg * 8) * V + d * HW +
-                                    (int64_t)h * a.W + wg;
+    struct Tile {
+        int n, d0, h0, w0, co0;
+    };
+    auto tile_of = [&](int k) {
+        int r = t_first + (k / nchunk) * t_stride;
+        Tile T;
+        T.co0 = (r % a.cogs) * NT * 16;
+        r /= a.cogs;
+        T.w0 = (r % a.tw) * kBW;
+        r /= a.tw;
+        T.h0 = (r % a.th) * kBH;
+        r /= a.th;
+        T.d0 = (r % a.td) * kBD;
+        T.n = r / a.td;
+        return T;
+    };
+
+    // ---- producer.  Staging item = (channel group cg, brick row, 8-column
+    // group q): eight 16-byte loads (one per channel) of 8 consecutive input
+    // columns, transposed in registers into 8 voxels x 8 channels.  q runs
+    // fastest, so the lanes of one load read adjacent 16-byte pieces of a row.
+    // Groups start at w0 - 8 (3^3: only its last column is the left halo) and
+    // end at w0 + 23 (3^3: only w0 + 16 is used).
+    constexpr int Q0 = KS == 3 ? -1 : 0;       // first group, in 8-column units from w0
+    constexpr int NQ = KS == 3 ? 4 : 2;        // groups per brick row
+    constexpr int NPAIR = 4 * PD * PH;         // (channel group, brick row) pairs
+    constexpr int NIT = NPAIR * NQ;            // staging items per step
+    constexpr int NRND = (NIT + 255) / 256;    // items per producer thread
+    static_assert(NPAIR * PW >= NT * 16 * kBD * kBH * 2 || KS != 3, "epilogue slots");
+    const int ptid = tid - 256;
+    auto item_of = [&](int r, int& pair, int& q) {
+        const int it = ptid + 256 * r;
+        pair = it / NQ;
+        q = it - pair * NQ;
+        return it < NIT;
+    };
+    auto stage = [&](int k, unsigned char* buf) {
+        const Tile T = tile_of(k);
+        const int c0 = (k % nchunk) * 32;
+        if ((a.W & 7) == 0) {
+            const __amdgpu_buffer_rsrc_t src_r =
+                buf_rsrc(a.src + (int64_t)T.n * a.Cs * V, (uint32_t)a.Cs * Vb);
+#pragma unroll 1
+            for (int r0 = 0; r0 < NRND; r0 += 2) {
+                uint4 v[2][8];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const uint2*>(p + j * V);
-                } else {
+                for (int i = 0; i < 2; ++i) {
+                    int pair, q;
+                    const bool live = r0 + i < NRND && item_of(r0 + i, pair, q);
+                    const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
+                    const int dd = row / PH, hh = row - dd * PH;
+                    const int d = T.d0 - P + dd, h = T.h0 - P + hh, wg = T.w0 + 8 * (q + Q0);
+                    const bool ok = live && (unsigned)d < (unsigned)a.D &&
+                                    (unsigned)h < (unsigned)a.H && (unsigned)wg < (unsigned)a.W;
+                    // an offset past the buffer end reads zeros (padding)
+                    const uint32_t vo =
+                        ok ? (uint32_t)((cg * 8 * V + d * HW + h * a.W + wg) * 2) : 0x80000000u;
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) v[j] = make_uint2(0u, 0u);
+                    for (int j = 0; j < 8; ++j)
+                        v[i][j] = buf_ld16(src_r, vo, (uint32_t)(c0 + j) * Vb);
                 }
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int ww = wg + e - (w0 - P);
-                    if (ww < 0 || ww >= PW) continue;
-                    const int vox = (dd * PH + hh) * PW + ww;
-                    uint32_t c[8];
+                for (int i = 0; i < 2; ++i) {
+                    int pair, q;
+                    if (!(r0 + i < NRND && item_of(r0 + i, pair, q))) continue;
+                    const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
+                    unsigned char* rb = buf + (uint32_t)(row * PW) * 64u;
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const uint32_t word = (e < 2) ? v[j].x : v[j].y;
-                        c[j] = (e & 1) ? (word >> 16) : (word & 0xffffu);
+                    for (int e = 0; e < 8; ++e) {
+                        const int ww = 8 * (q + Q0) + e + P;  // brick column
+                        if (ww < 0 || ww >= PW) continue;
+                        const int wd = e >> 1;
+                        uint32_t o[4];
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            const uint32_t wl = wd == 0 ? v[i][2 * c].x
+                                              : wd == 1 ? v[i][2 * c].y
+                                              : wd == 2 ? v[i][2 * c].z : v[i][2 * c].w;
+                            const uint32_t wh = wd == 0 ? v[i][2 * c + 1].x
+                                              : wd == 1 ? v[i][2 * c + 1].y
+                                              : wd == 2 ? v[i][2 * c + 1].z : v[i][2 * c + 1].w;
+                            o[c] = (e & 1) ? pack_hi(wl, wh) : pack_lo(wl, wh);
+                        }
+                        *reinterpret_cast<uint4*>(rb + brick_slot_off<KS>(ww, cg)) =
+                            make_uint4(o[0], o[1], o[2], o[3]);
                     }
-                    brick[vox * 4 + (cg ^ ((vox >> 1) & 3))] =
-                        make_uint4(c[0] | (c[1] << 16), c[2] | (c[3] << 16), c[4] | (c[5] << 16),
-                                   c[6] | (c[7] << 16));
                 }
             }
         } else {
             // item = (channel group, brick voxel), voxel fastest
-            for (int it = tid; it < NV * 4; it += 256) {
+            for (int it = ptid; it < NV * 4; it += 256) {
                 const int vox = it % NV, cg = it / NV;
                 const int ww = vox % PW, rr = vox / PW;
                 const int hh = rr % PH, dd = rr / PH;
-                const int d = d0 - P + dd, h = h0 - P + hh, w = w0 - P + ww;
+                const int d = T.d0 - P + dd, h = T.h0 - P + hh, w = T.w0 - P + ww;
                 uint4 pk = make_uint4(0u, 0u, 0u, 0u);
                 if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
                     (unsigned)w < (unsigned)a.W) {
-                    const bf16* p = a.src + ((int64_t)n * a.Cs + c0 + cg * 8) * V + d * HW +
-                                    (int64_t)h * a.W + w;
-                    uint32_t v[8];
+                    const bf16* p = a.src + ((int64_t)T.n * a.Cs + c0 + cg * 8) * V +
+                                    (int64_t)d * HW + (int64_t)h * a.W + w;
+                    uint32_t u[8];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) v[j] = p[j * V];
-                    pk.x = v[0] | (v[1] << 16);
-                    pk.y = v[2] | (v[3] << 16);
-                    pk.z = v[4] | (v[5] << 16);
-                    pk.w = v[6] | (v[7] << 16);
+                    for (int j = 0; j < 8; ++j) u[j] = p[(int64_t)j * V];
+                    pk.x = u[0] | (u[1] << 16);
+                    pk.y = u[2] | (u[3] << 16);
+                    pk.z = u[4] | (u[5] << 16);
+                    pk.w = u[6] | (u[7] << 16);
                 }
-                brick[vox * 4 + (cg ^ ((vox >> 1) & 3))] = pk;
+                *reinterpret_cast<uint4*>(buf + (uint32_t)(rr * PW) * 64u +
+                                          brick_slot_off<KS>(ww, cg)) = pk;
             }
         }
-        __syncthreads();
-        const bf16* wc = a.wt + (int64_t)(c0 >> 5) * KT * a.Ct * 32;
-        // weight fragments are double-buffered: tap t+1 loads while tap t multiplies
-        F16B bc[NT];
-#pragma unroll
-        for (int ct = 0; ct < NT; ++ct)
-            bc[ct].u = *reinterpret_cast<const uint4*>(wc + ((int64_t)(co0 + ct * 16 + li)) * 32 +
-                                                        kg * 8);
-#pragma unroll 1
-        for (int tap = 0; tap < KT; ++tap) {
-            const int kd = tap / (KS * KS), kh = (tap / KS) % KS, kw = tap % KS;
-            F16B bn[NT];
-            const int tn = tap + 1 < KT ? tap + 1 : tap;
-#pragma unroll
-            for (int ct = 0; ct < NT; ++ct)
-                bn[ct].u = *reinterpret_cast<const uint4*>(
-                    wc + ((int64_t)tn * a.Ct + co0 + ct * 16 + li) * 32 + kg * 8);
-#pragma unroll
-            for (int rw = 0; rw < 8; ++rw) {
-                const int vox = ((wave + kd) * PH + (rw + kh)) * PW + li + kw;
-                F16B av;
-                av.u = brick[vox * 4 + (kg ^ ((vox >> 1) & 3))];
-#pragma unroll
-                for (int ct = 0; ct < NT; ++ct) acc[rw][ct] = mfma(av, bc[ct], acc[rw][ct]);
-            }
-#pragma unroll
-            for (int ct = 0; ct < NT; ++ct) bc[ct] = bn[ct];
-        }
-    }
+    };
 
-    // epilogue: lane holds 4 consecutive w of one output channel per tile
-    const int d = d0 + wave;
-    if (d >= a.D) return;
-    const bool full_w = (w0 + kBW <= a.W) && ((a.W & 3) == 0);
+    // ---- consumer.  The four consumer waves split the tile as WD depth groups
+    // (RD slices of 8 rows each) x WC output-channel groups (CT x 16
+    // channels); lane (li, kg) reads brick column li + kw, channel slot kg.
+    constexpr int WD = kBD / RD, WC = 4 / WD, CT = NT / WC, NR = RD * kBH;
+    static_assert(WD * RD == kBD && WC * WD == 4 && CT * WC == NT, "wave split");
+    const int li = lane & 15, kg = lane >> 4;
+    const int wd = (wave & 3) % WD, wc = (wave & 3) / WD;
+    uint32_t sw[KS];
 #pragma unroll
-    for (int rw = 0; rw < 8; ++rw) {
-        const int h = h0 + rw;
-        if (h >= a.H) continue;
+    for (int kw = 0; kw < KS; ++kw)
+        sw[kw] = (uint32_t)(wd * RD * PH * PW) * 64u + brick_slot_off<KS>(li + kw, kg);
+    const uint32_t wlane = (uint32_t)(li * 64 + kg * 16);
+    const __amdgpu_buffer_rsrc_t wt_r =
+        buf_rsrc(a.wt, (uint32_t)(a.Cs / 32) * KT * (uint32_t)a.Ct * 64u);
+    f32x4 acc[NR][CT];
+    // brick offset of the wave's row r (depth slice r / 8, tile row r % 8)
+    auto row_off = [](int r) { return ((r / kBH) * PH + (r % kBH)) * PW * 64; };
+
+    auto compute = [&](int k, const unsigned char* buf) {
+        const Tile T = tile_of(k);
+        const int c0 = (k % nchunk) * 32;
+        if (c0 == 0) {
 #pragma unroll
-        for (int ct = 0; ct < NT; ++ct) {
-            const int co = co0 + ct * 16 + li;
-            const float bv = a.bias ? a.bias[co] : 0.f;
-            const int w = w0 + 4 * kg;
-            bf16* q = a.dst + ((int64_t)n * a.Ct + co) * V + d * HW + (int64_t)h * a.W + w;
-            float v[4];
+            for (int i = 0; i < NR; ++i)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = acc[rw][ct][e] + bv;
-            if (full_w) {
-                uint2* q2 = reinterpret_cast<uint2*>(q);
-                if (a.accumulate) {
-                    const uint2 o = *q2;
-                    v[0] += __uint_as_float(o.x << 16);
-                    v[1] += __uint_as_float(o.x & 0xffff0000u);
-                    v[2] += __uint_as_float(o.y << 16);
-                    v[3] += __uint_as_float(o.y & 0xffff0000u);
-                }
-                *q2 = make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
-                                 (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
-            } else {
+                for (int j = 0; j < CT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        // weight fragments [chunk][tap][Ct][32].  B operands of tap t+1 are
+        // fetched while tap t multiplies.  A operands stream through a ring of
+        // LA registers: operand g = tap * NR + row is read LA rows ahead of its
+        // MFMAs, into the slot the MFMAs of operand g have just released.
+        constexpr int LA = NR < 10 ? NR : 10;
+        constexpr int NG = KT * NR;
+        const uint32_t wchunk =
+            ((uint32_t)(c0 >> 5) * KT * (uint32_t)a.Ct + T.co0 + wc * CT * 16) * 64u;
+        F16B A[LA], B[2][CT];
+        auto a_ptr = [&](int g) {
+            const int tap = g / NR, r = g % NR;
+            const int kd = tap / (KS * KS), kh = (tap / KS) % KS, kw = tap % KS;
+            return buf + sw[kw] + ((kd * PH + kh) * PW) * 64 + row_off(r);
+        };
+        auto load_b = [&](int tap, F16B (&bv)[CT]) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    if (w + e >= a.W) break;
-                    float o = v[e];
-                    if (a.accumulate) o += bf2f(q[e]);
-                    q[e] = f2bf(o);
+            for (int ct = 0; ct < CT; ++ct)
+                bv[ct].u = buf_ld16(wt_r, wlane, wchunk + ((uint32_t)tap * a.Ct + ct * 16) * 64u);
+        };
+#pragma unroll
+        for (int g = 0; g < LA; ++g) A[g].u = *reinterpret_cast<const uint4*>(a_ptr(g));
+        load_b(0, B[0]);
+#pragma unroll
+        for (int tap = 0; tap < KT; ++tap) {
+            if (tap + 1 < KT) load_b(tap + 1, B[(tap + 1) & 1]);
+#pragma unroll
+            for (int r = 0; r < NR; ++r) {
+                const int g = tap * NR + r;
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct)
+                    acc[r][ct] = mfma(A[g % LA], B[tap & 1][ct], acc[r][ct]);
+                if (g + LA < NG) A[g % LA].u = *reinterpret_cast<const uint4*>(a_ptr(g + LA));
+            }
+            // issue order within a tap: the next tap's weight loads, then per
+            // row its MFMAs followed by the ring refill; nothing moves across
+            // taps (register pressure)
+            if (tap + 1 < KT) {
+                __builtin_amdgcn_sched_group_barrier(0x020, CT, 0);
+#pragma unroll
+                for (int r = 0; r < NR; ++r) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, CT, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
                 }
             }
+            __builtin_amdgcn_sched_barrier(0);
         }
+    };
+
+    // Output epilogue, staged: after a tile's last MFMA the consumers write
+    // bf16 results (bias added) into the brick buffer they just finished
+    // reading, in 16-byte units of eight w.  The units of output channel
+    // group cg (16 channels) are numbered i = ((co % 16) * 4 + d) * 16 + h * 2
+    // + half and occupy brick row i / PW, column i % PW, channel slot cg: the
+    // slot that staging item (cg, row, group of the column) writes.  The
+    // producer thread that owns that item stores the unit to global memory
+    // before it stages into the buffer again, so no producer overwrites a unit
+    // another has not drained, and the global stores (and any wait for them)
+    // stay off the consumer waves.
+    constexpr int NUNIT_CG = 16 * kBD * kBH * 2;  // units per channel group
+    static_assert(KS != 3 || NUNIT_CG <= PD * PH * PW, "staged outputs fit the brick");
+    const bool staged_epi = KS == 3 && !a.accumulate && (a.W & 7) == 0;
+    auto write_outputs = [&](int k, unsigned char* buf) {
+        const Tile T = tile_of(k);
+        float bv[CT];
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+            bv[ct] = a.bias ? a.bias[T.co0 + (wc * CT + ct) * 16 + li] : 0.f;
+        // opaque per call: keeps the slot arithmetic from being hoisted out of
+        // the step loop, where its results would stay live (register pressure)
+        int lane_u = (li * kBD + wd * RD) * kBH * 2 + (kg >> 1);
+        asm volatile("" : "+v"(lane_u));
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            const int i = lane_u + ((r / kBH) * kBH + r % kBH) * 2;
+            const int row = i / PW, ww = i - row * PW;
+            unsigned char* base = buf + (uint32_t)(row * PW + ww) * 64u + (kg & 1) * 8;
+            const int sk = (ww >> 1) & 3;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct)
+                *reinterpret_cast<uint2*>(base + (((wc * CT + ct) ^ sk) << 4)) = make_uint2(
+                    pack_bf16x2(acc[r][ct][0] + bv[ct], acc[r][ct][1] + bv[ct]),
+                    pack_bf16x2(acc[r][ct][2] + bv[ct], acc[r][ct][3] + bv[ct]));
+            __builtin_amdgcn_sched_barrier(0);  // one row at a time (register pressure)
+        }
+    };
+    auto drain = [&](int k, const unsigned char* buf) {
+        const Tile T = tile_of(k);
+#pragma unroll 1
+        for (int r = 0; r < NRND; ++r) {
+            int pair, q;
+            if (!item_of(r, pair, q)) continue;
+            const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
+            if (cg * 16 >= NT * 16) continue;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int ww = 8 * (q + Q0) + e + P;
+                if (ww < 0 || ww >= PW) continue;
+                const int i = row * PW + ww;
+                if (i >= NUNIT_CG) continue;
+                const int half = i & 1, h = (i >> 1) & (kBH - 1), d = (i >> 4) & (kBD - 1);
+                const int co = cg * 16 + (i >> 6);
+                const uint4 v = *reinterpret_cast<const uint4*>(
+                    buf + (uint32_t)(row * PW) * 64u + brick_slot_off<KS>(ww, cg));
+                const int dd = T.d0 + d, hh = T.h0 + h, w = T.w0 + 8 * half;
+                if (dd < a.D && hh < a.H && w < a.W)
+                    *reinterpret_cast<uint4*>(a.dst + ((int64_t)T.n * a.Ct + T.co0 + co) * V +
+                                              (int64_t)dd * HW + (int64_t)hh * a.W + w) = v;
+            }
+        }
+    };
+    // direct epilogue (accumulating outputs, widths not a multiple of 8, 1^3):
+    // lane holds 4 consecutive w of one output channel per tile row
+    auto direct_outputs = [&](int k) {
+        const Tile T = tile_of(k);
+        const bool full_w = (T.w0 + kBW <= a.W) && ((a.W & 3) == 0);
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            const int d = T.d0 + wd * RD + r / kBH, h = T.h0 + r % kBH;
+            if (d >= a.D || h >= a.H) continue;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                const int co = T.co0 + (wc * CT + ct) * 16 + li;
+                const float bv = a.bias ? a.bias[co] : 0.f;
+                const int w = T.w0 + 4 * kg;
+                bf16* q = a.dst + ((int64_t)T.n * a.Ct + co) * V + (int64_t)d * HW +
+                          (int64_t)h * a.W + w;
+                float v[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = acc[r][ct][e] + bv;
+                if (full_w) {
+                    uint2* q2 = reinterpret_cast<uint2*>(q);
+                    if (a.accumulate) {
+                        const uint2 o = *q2;
+                        v[0] += __uint_as_float(o.x << 16);
+                        v[1] += __uint_as_float(o.x & 0xffff0000u);
+                        v[2] += __uint_as_float(o.y << 16);
+                        v[3] += __uint_as_float(o.y & 0xffff0000u);
+                    }
+                    *q2 = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if (w + e >= a.W) break;
+                        float o = v[e];
+                        if (a.accumulate) o += bf2f(q[e]);
+                        q[e] = f2bf(o);
+                    }
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    // Both roles pass the same barriers (one per step, two on a tile's last
+    // step with the staged epilogue); the roles are wave-uniform, and the two
+    // loops keep the consumers' accumulators out of the producers' live range.
+    // The barriers order LDS only: global stores are never waited for.
+    auto tile_end = [&](int k) { return (k % nchunk) == nchunk - 1; };
+    if (consumer) {
+        lds_barrier();
+        for (int k = 0; k < S; ++k) {
+            unsigned char* buf = lds + (k & 1) * BB;
+            compute(k, buf);
+            if (tile_end(k) && staged_epi) {
+                lds_barrier();  // every consumer is done reading buf
+                write_outputs(k, buf);
+                lds_barrier();
+            } else {
+                if (tile_end(k)) direct_outputs(k);
+                lds_barrier();
+            }
+        }
+    } else {
+        if (S > 0) stage(0, lds);
+        lds_barrier();
+        for (int k = 0; k < S; ++k) {
+            if (staged_epi && k > 0 && tile_end(k - 1)) drain(k - 1, lds + ((k - 1) & 1) * BB);
+            if (k + 1 < S) stage(k + 1, lds + ((k + 1) & 1) * BB);
+            if (tile_end(k) && staged_epi) {
+                lds_barrier();
+                lds_barrier();
+            } else {
+                lds_barrier();
+            }
+        }
+        if (staged_epi && S > 0) drain(S - 1, lds + ((S - 1) & 1) * BB);
     }
 }
 
@@ -460,7 +692,9 @@ bool brick_fd_ok(const ConvGeom& g, rat3d_dtype dt, bool dgrad) {
     if (dt != RAT3D_BF16 || g.s != 1) return false;
     if (!((g.k == 3 && g.p == 1) || (g.k == 1 && g.p == 0))) return false;
     const int cs = dgrad ? g.Co : g.Ci, ct = dgrad ? g.Ci : g.Co;
-    return cs % 32 == 0 && ct % 32 == 0;
+    // one sample's source channels are addressed with 32-bit byte offsets
+    const int64_t src_bytes = (int64_t)cs * g.D * g.H * g.W * 2;
+    return cs % 32 == 0 && ct % 32 == 0 && src_bytes < ((int64_t)1 << 31);
 }
 
 bool brick_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) {
@@ -517,16 +751,19 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
     a.tw = (int)ceil_div(g.W, kBW);
     a.accumulate = accumulate;
     const int nt = a.Ct % 64 == 0 ? 4 : 2;
-    dim3 grid((unsigned)((int64_t)g.N * a.td * a.th * a.tw), (unsigned)(a.Ct / (nt * 16)));
+    a.cogs = a.Ct / (nt * 16);
+    a.ntiles = (int)((int64_t)g.N * a.td * a.th * a.tw * a.cogs);
+    // one persistent workgroup per CU (fewer when there are fewer tiles)
+    const int grid = a.ntiles < device_cus() ? a.ntiles : device_cus();
     ProfScope ps(dgrad ? (g.k == 3 ? "conv_brick3_dgrad" : "conv_brick1_dgrad")
                        : (g.k == 3 ? "conv_brick3_fwd" : "conv_brick1_fwd"),
                  st, conv_flops(g), conv_bytes(g, 2));
     if (g.k == 3) {
-        if (nt == 4) conv_brick_fd<3, 4><<<grid, 256, 0, st>>>(a);
-        else conv_brick_fd<3, 2><<<grid, 256, 0, st>>>(a);
+        if (nt == 4) conv_brick_fd<3, 4, 2><<<grid, 512, 0, st>>>(a);
+        else conv_brick_fd<3, 2, 1><<<grid, 512, 0, st>>>(a);
     } else {
-        if (nt == 4) conv_brick_fd<1, 4><<<grid, 256, 0, st>>>(a);
-        else conv_brick_fd<1, 2><<<grid, 256, 0, st>>>(a);
+        if (nt == 4) conv_brick_fd<1, 4, 2><<<grid, 512, 0, st>>>(a);
+        else conv_brick_fd<1, 2, 1><<<grid, 512, 0, st>>>(a);
     }
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;

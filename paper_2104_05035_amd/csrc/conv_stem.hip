@@ -134,8 +134,8 @@ __global__ __launch_bounds__(256, 2) void stem_fwd_k(const bf16* __restrict__ x,
             bf16* q = y + ((int64_t)n * kSCo + co) * V + ((int64_t)d * Ho + h) * Wo + w;
             if (full) {
                 *reinterpret_cast<uint2*>(q) =
-                    make_uint2((uint32_t)f2bf(acc[rw][ct][0]) | ((uint32_t)f2bf(acc[rw][ct][1]) << 16),
-                               (uint32_t)f2bf(acc[rw][ct][2]) | ((uint32_t)f2bf(acc[rw][ct][3]) << 16));
+                    make_uint2(pack_bf16x2(acc[rw][ct][0], acc[rw][ct][1]),
+                               pack_bf16x2(acc[rw][ct][2], acc[rw][ct][3]));
             } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e)

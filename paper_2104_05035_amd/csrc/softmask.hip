@@ -602,7 +602,7 @@ __global__ __launch_bounds__(kEwThreads) void pool332_bwd_pl(const bf16* __restr
         uint32_t w4[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            w4[i] = (uint32_t)f2bf(acc[2 * i]) | ((uint32_t)f2bf(acc[2 * i + 1]) << 16);
+            w4[i] = pack_bf16x2(acc[2 * i], acc[2 * i + 1]);
         *q4 = make_uint4(w4[0], w4[1], w4[2], w4[3]);
     }
 }
@@ -690,7 +690,7 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
         uint32_t w4[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            w4[i] = (uint32_t)f2bf(out[2 * i]) | ((uint32_t)f2bf(out[2 * i + 1]) << 16);
+            w4[i] = pack_bf16x2(out[2 * i], out[2 * i + 1]);
         *reinterpret_cast<uint4*>(y + (((int64_t)nc * Do + od) * Ho + oh) * Wo + 8 * g) =
             make_uint4(w4[0], w4[1], w4[2], w4[3]);
     }
@@ -783,8 +783,8 @@ __global__ __launch_bounds__(kEwThreads) void up2_bwd_pl(const bf16* __restrict_
             out[2] += __uint_as_float(o.y << 16);
             out[3] += __uint_as_float(o.y & 0xffff0000u);
         }
-        *q2 = make_uint2((uint32_t)f2bf(out[0]) | ((uint32_t)f2bf(out[1]) << 16),
-                         (uint32_t)f2bf(out[2]) | ((uint32_t)f2bf(out[3]) << 16));
+        *q2 = make_uint2(pack_bf16x2(out[0], out[1]),
+                         pack_bf16x2(out[2], out[3]));
     }
 }
 

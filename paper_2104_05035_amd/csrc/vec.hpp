@@ -35,7 +35,7 @@ __device__ __forceinline__ void vstore(T* __restrict__ p, const float (&o)[VEC])
         uint32_t w[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            w[i] = (uint32_t)f2bf(o[2 * i]) | ((uint32_t)f2bf(o[2 * i + 1]) << 16);
+            w[i] = pack_bf16x2(o[2 * i], o[2 * i + 1]);
         u.x = w[0]; u.y = w[1]; u.z = w[2]; u.w = w[3];
         *reinterpret_cast<uint4*>(p) = u;
     } else if constexpr (sizeof(T) == 4 && VEC == 4) {
