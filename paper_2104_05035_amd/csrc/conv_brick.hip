@@ -44,7 +44,7 @@ union F16B {
 };
 
 constexpr int kBD = 4, kBH = 8, kBW = 16;     // forward output tile
-constexpr int kWD = 2, kWH = 8, kWW = 16;     // weight-gradient voxel brick
+constexpr int kWD = 1, kWH = 8, kWW = 16;     // weight-gradient voxel brick
 
 __device__ __forceinline__ f32x4 mfma(const F16B& a, const F16B& b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.b, b.b, c, 0, 0, 0);
@@ -127,7 +127,11 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     constexpr int NV = PD * PH * PW;
     constexpr int KT = KS * KS * KS;
     constexpr uint32_t BB = NV * 64;            // bytes per brick buffer
-    __shared__ __align__(16) unsigned char lds[2 * BB];
+    // 1^3: the output tile does not fit a brick buffer and gets its own region
+    // (co stride padded by 16 bytes so that 16 channels hit distinct banks)
+    constexpr uint32_t OCS = kBD * kBH * kBW * 2 + 16;
+    constexpr uint32_t OB = KS == 1 ? NT * 16 * OCS : 0;
+    __shared__ __align__(16) unsigned char lds[2 * BB + OB];
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const bool consumer = wave < 4;
@@ -352,13 +356,30 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     // stay off the consumer waves.
     constexpr int NUNIT_CG = 16 * kBD * kBH * 2;  // units per channel group
     static_assert(KS != 3 || NUNIT_CG <= PD * PH * PW, "staged outputs fit the brick");
-    const bool staged_epi = KS == 3 && !a.accumulate && (a.W & 7) == 0;
+    const bool staged_epi = !a.accumulate && (a.W & 7) == 0;
     auto write_outputs = [&](int k, unsigned char* buf) {
         const Tile T = tile_of(k);
         float bv[CT];
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct)
             bv[ct] = a.bias ? a.bias[T.co0 + (wc * CT + ct) * 16 + li] : 0.f;
+        if constexpr (KS == 1) {
+            // separate region: unit (co, d, h, half) at co * OCS + ((d * 8 + h) * 2 + half) * 16
+            unsigned char* ob = lds + 2 * BB;
+            int lane_o = (int)((uint32_t)((wc * CT) * 16 + li) * OCS) +
+                         ((wd * RD * kBH) * 2 + (kg >> 1)) * 16 + (kg & 1) * 8;
+            asm volatile("" : "+v"(lane_o));
+#pragma unroll
+            for (int r = 0; r < NR; ++r) {
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct)
+                    *reinterpret_cast<uint2*>(ob + lane_o + ct * 16 * OCS + r * 32) = make_uint2(
+                        pack_bf16x2(acc[r][ct][0] + bv[ct], acc[r][ct][1] + bv[ct]),
+                        pack_bf16x2(acc[r][ct][2] + bv[ct], acc[r][ct][3] + bv[ct]));
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            return;
+        }
         // opaque per call: keeps the slot arithmetic from being hoisted out of
         // the step loop, where its results would stay live (register pressure)
         int lane_u = (li * kBD + wd * RD) * kBH * 2 + (kg >> 1);
@@ -379,6 +400,20 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     };
     auto drain = [&](int k, const unsigned char* buf) {
         const Tile T = tile_of(k);
+        if constexpr (KS == 1) {
+            const unsigned char* ob = lds + 2 * BB;
+#pragma unroll 4
+            for (int u = ptid; u < NT * 16 * kBD * kBH * 2; u += 256) {
+                const int co = u >> 6, rest = u & 63;
+                const int half = rest & 1, h = (rest >> 1) & (kBH - 1), d = rest >> 4;
+                const uint4 v = *reinterpret_cast<const uint4*>(ob + co * OCS + rest * 16);
+                const int dd = T.d0 + d, hh = T.h0 + h, w = T.w0 + 8 * half;
+                if (dd < a.D && hh < a.H && w < a.W)
+                    *reinterpret_cast<uint4*>(a.dst + ((int64_t)T.n * a.Ct + T.co0 + co) * V +
+                                              (int64_t)dd * HW + (int64_t)hh * a.W + w) = v;
+            }
+            return;
+        }
 #pragma unroll 1
         for (int r = 0; r < NRND; ++r) {
             int pair, q;
@@ -513,8 +548,12 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
     constexpr int KWS = 16 * CIS;        // bytes per kw-shifted copy
     constexpr int NTAP = (KT + 3) / 4;   // taps per wave
     static_assert(NTAP == kWgNtap, "partial layout");
-    constexpr int NIT = (16 * ROWS + 255) / 256;  // staging items per thread
-    __shared__ __align__(16) unsigned char xs[KS * KWS];
+    constexpr int NIT = (16 * ROWS + 255) / 256;  // x staging items per thread
+    constexpr int DYS = kWH * 32 + 16;            // bytes per dy channel (rows of 16 bf16) + pad
+    constexpr int NDY = 64 * kWH * 2 / 256;       // dy staging items (16 bytes) per thread
+    static_assert(kWD == 1, "one depth slice per brick: dy rows are h0 .. h0 + kWH - 1");
+    __shared__ __align__(16) unsigned char xs[KS * KWS + 64 * DYS];
+    unsigned char* const dys = xs + KS * KWS;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int L = xcd_remap(blockIdx.x, gridDim.x);
@@ -549,12 +588,15 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
         return k;
     };
 
-    // Staging item = (input channel, brick row): the row's 16 aligned voxels
-    // (two 16-byte loads) plus one halo voxel on each side, held in registers
+    // Both operands of a brick are staged through LDS; the next brick's rows
+    // are fetched into registers before the current brick's K loop so that
+    // the loads are in flight while the MFMAs run.
+    // x item = (input channel, brick row): the row's 16 aligned voxels (two
+    // 16-byte loads) plus one halo voxel on each side, held as
     // m[0] = (?, x[w0-1]), m[1..8] = x[w0 .. w0+15], m[9] = (x[w0+16], ?).
-    // The next brick's rows are fetched before the current brick's K loop so
-    // that the loads are in flight while the MFMAs run.
+    // dy item = (output channel, row, half): 8 voxels, one 16-byte load.
     uint32_t m[NIT][10];
+    uint4 dyv[NDY];
     auto fetch = [&](const Brick& k) {
 #pragma unroll
         for (int q = 0; q < NIT; ++q) {
@@ -578,6 +620,16 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
             if (k.w0 >= 1) m[q][0] = (uint32_t)p[-1] << 16;
             if (k.w0 + 16 < a.W) m[q][9] = (uint32_t)p[16];
         }
+#pragma unroll
+        for (int q = 0; q < NDY; ++q) {
+            const int it = tid + 256 * q;
+            const int co = it >> 4, row = (it >> 1) & (kWH - 1), half = it & 1;
+            const int h = k.h0 + row, w = k.w0 + 8 * half;
+            dyv[q] = make_uint4(0u, 0u, 0u, 0u);
+            if (k.d0 < a.D && h < a.H && w + 8 <= a.W)
+                dyv[q] = *reinterpret_cast<const uint4*>(
+                    a.dy + ((int64_t)k.n * a.Co + co0 + co) * V + k.d0 * HW + (int64_t)h * a.W + w);
+        }
     };
     // copy kw holds input columns w0 - 1 + kw ... as aligned 16-byte LDS rows
     auto commit = [&]() {
@@ -593,8 +645,8 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
             uint32_t s0[8], s2[8];
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                s0[i] = (m[q][i] >> 16) | (m[q][i + 1] << 16);
-                s2[i] = (m[q][i + 1] >> 16) | (m[q][i + 2] << 16);
+                s0[i] = __builtin_amdgcn_alignbit(m[q][i + 1], m[q][i], 16);
+                s2[i] = __builtin_amdgcn_alignbit(m[q][i + 2], m[q][i + 1], 16);
             }
             *reinterpret_cast<uint4*>(base) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
             *reinterpret_cast<uint4*>(base + 16) = make_uint4(s0[4], s0[5], s0[6], s0[7]);
@@ -602,39 +654,30 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
             *reinterpret_cast<uint4*>(base + 2 * KWS + 16) =
                 make_uint4(s2[4], s2[5], s2[6], s2[7]);
         }
+#pragma unroll
+        for (int q = 0; q < NDY; ++q) {
+            const int it = tid + 256 * q;
+            const int co = it >> 4, row = (it >> 1) & (kWH - 1), half = it & 1;
+            *reinterpret_cast<uint4*>(dys + co * DYS + row * 32 + half * 16) = dyv[q];
+        }
     };
 
     if (b_beg < b_end) fetch(brick_at(b_beg));
     for (int64_t b = b_beg; b < b_end; ++b) {
-        const Brick k = brick_at(b);
         __syncthreads();  // every wave is done reading the previous brick
         commit();
         __syncthreads();
         if (b + 1 < b_end) fetch(brick_at(b + 1));
-        // K step s covers rows (h0 + 2*(s%4) + {0,1}) of depth d0 + s/4; dy
-        // rows for step s+1 are fetched while step s multiplies
-        auto load_a = [&](int s, F16B (&av)[4]) {
-            const int dl = s / (kWH / 2);
-            const int hl = (s % (kWH / 2)) * 2 + hl_l;
-            const int d = k.d0 + dl, h = k.h0 + hl, w = k.w0 + wl;
-            const bool ok = d < a.D && h < a.H && w + 8 <= a.W;
+        // K step s covers brick rows 2s and 2s + 1 (32 voxels): lane (li, kg)
+        // holds 8 voxels of row 2s + kg/2, columns 8 (kg % 2) ..
 #pragma unroll
-            for (int ct = 0; ct < 4; ++ct) {
-                av[ct].u = make_uint4(0u, 0u, 0u, 0u);
-                if (ok)
-                    av[ct].u = *reinterpret_cast<const uint4*>(
-                        a.dy + ((int64_t)k.n * a.Co + co0 + ct * 16 + li) * V + d * HW +
-                        (int64_t)h * a.W + w);
-            }
-        };
-        F16B ac[4];
-        load_a(0, ac);
-#pragma unroll 1
-        for (int s = 0; s < kWD * kWH / 2; ++s) {
-            F16B an[4];
-            load_a(s + 1 < kWD * kWH / 2 ? s + 1 : s, an);
-            const int dl = s / (kWH / 2);
-            const int hl = (s % (kWH / 2)) * 2 + hl_l;
+        for (int s = 0; s < kWH / 2; ++s) {
+            const int hl = 2 * s + hl_l;
+            F16B ac[4];
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct)
+                ac[ct].u = *reinterpret_cast<const uint4*>(dys + (ct * 16 + li) * DYS + hl * 32 +
+                                                           wl * 2);
 #pragma unroll
             for (int j = 0; j < NTAP; ++j) {
                 const int t = wave + 4 * j;
@@ -642,13 +685,11 @@ __global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
                     const int kd = t / (KS * KS), kh = (t / KS) % KS, kw = t % KS;
                     F16B bv;
                     bv.u = *reinterpret_cast<const uint4*>(
-                        xs + kw * KWS + li * CIS + ((dl + kd) * PH + hl + kh) * 32 + wl * 2);
+                        xs + kw * KWS + li * CIS + (kd * PH + hl + kh) * 32 + wl * 2);
 #pragma unroll
                     for (int ct = 0; ct < 4; ++ct) acc[j][ct] = mfma(ac[ct], bv, acc[j][ct]);
                 }
             }
-#pragma unroll
-            for (int ct = 0; ct < 4; ++ct) ac[ct] = an[ct];
         }
     }
 
