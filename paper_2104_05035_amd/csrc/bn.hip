@@ -11,8 +11,10 @@
 //           apply coefficients; (3) dx = k * (g - dbeta/M - xhat * dgamma/M),
 //           dresidual = g.
 // NCDHW: one (n, c) plane is V contiguous voxels; a slice is a contiguous
-// range of the concatenation of a channel's N planes.  Everything is
-// HBM-bound: loads and stores are 16-byte vectors when V allows.
+// segment of one plane, so per-element indexing needs no division.  A
+// channel's partials are the N * SP segment sums of its planes, combined in
+// a fixed order.  Everything is HBM-bound: loads and stores are 16-byte
+// vectors when V allows.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "vec.hpp"
@@ -23,20 +25,20 @@ namespace rat3d {
 constexpr int kBnThreads = 256;
 
 struct BnSlices {
-    int per_channel;  // slices per channel
-    int64_t len;      // elements per slice (multiple of the vector width)
+    int per_plane;    // segments per (n, c) plane
+    int per_channel;  // N * per_plane partials per channel
+    int64_t len;      // elements per segment (multiple of the vector width)
 };
 
 static BnSlices bn_slices(const BnGeom& g) {
-    const int64_t M = (int64_t)g.N * g.V;
-    int64_t want = ceil_div(2048, g.C);  // aim for ~2048 blocks in total
-    int64_t by_size = ceil_div(M, 16384);  // at least ~16K elements per slice
+    int64_t want = ceil_div(2048, (int64_t)g.C * g.N);  // aim for ~2048 blocks in total
+    int64_t by_size = ceil_div(g.V, 16384);              // at least ~16K elements per segment
     int64_t s = want < by_size ? want : by_size;
     if (s < 1) s = 1;
-    int64_t len = ceil_div(M, s);
+    int64_t len = ceil_div(g.V, s);
     len = ceil_div(len, 8) * 8;
-    s = ceil_div(M, len);
-    return BnSlices{(int)s, len};
+    s = ceil_div(g.V, len);
+    return BnSlices{(int)s, (int)(s * g.N), len};
 }
 
 size_t bn_ws_bytes(const BnGeom& g) {
@@ -62,25 +64,21 @@ __device__ __forceinline__ void block_sum2(float& a, float& b) {
     b = rb[0];
 }
 
-// Element e of channel c's concatenated planes -> flat tensor index.
-__device__ __forceinline__ int64_t chan_index(int64_t e, int c, int C, int64_t V) {
-    const int64_t n = e / V;
-    return (n * C + c) * V + (e - n * V);
-}
-
+// Block (c, n * SP + seg): segment seg of plane (n, c).
 template <typename T, int VEC>
-__global__ __launch_bounds__(kBnThreads) void bn_fwd_stats(const T* __restrict__ x, int N,
-                                                           int C, int64_t V, int64_t len,
+__global__ __launch_bounds__(kBnThreads) void bn_fwd_stats(const T* __restrict__ x, int C,
+                                                           int64_t V, int SP, int64_t len,
                                                            float* __restrict__ part) {
     const int c = blockIdx.x, sidx = blockIdx.y;
-    const int64_t M = (int64_t)N * V;
+    const int n = sidx / SP, seg = sidx - n * SP;
     const float shift = Elt<T>::ld(x + (int64_t)c * V);
-    const int64_t beg = (int64_t)sidx * len;
-    const int64_t end = beg + len < M ? beg + len : M;
+    const int64_t beg = (int64_t)seg * len;
+    const int64_t cnt = (beg + len < V ? beg + len : V) - beg;
+    const T* p = x + ((int64_t)n * C + c) * V + beg;
     float s1 = 0.f, s2 = 0.f;
-    for (int64_t e = beg + (int64_t)threadIdx.x * VEC; e < end; e += (int64_t)kBnThreads * VEC) {
+    for (int64_t e = (int64_t)threadIdx.x * VEC; e < cnt; e += (int64_t)kBnThreads * VEC) {
         float v[VEC];
-        vload<T, VEC>(x + chan_index(e, c, C, V), v);
+        vload<T, VEC>(p + e, v);
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
             const float d = v[j] - shift;
@@ -130,15 +128,18 @@ __global__ void bn_fwd_finalize(const T* __restrict__ x, int N, int C, int64_t V
     }
 }
 
+// One-dimensional grid: block b covers chunk b % cpp of plane b / cpp.
 template <typename T, int VEC, bool RELU, bool RES>
 __global__ __launch_bounds__(kBnThreads) void bn_fwd_apply(const T* __restrict__ x,
                                                            const T* __restrict__ r, int C,
-                                                           int64_t V, int64_t total,
+                                                           int64_t V, unsigned cpp,
                                                            const float* __restrict__ coef,
                                                            T* __restrict__ y) {
-    const int64_t i = ((int64_t)blockIdx.x * kBnThreads + threadIdx.x) * VEC;
-    if (i >= total) return;
-    const int c = (int)((i / V) % C);
+    const int plane = (int)(blockIdx.x / cpp);  // wave-uniform
+    const int64_t e = ((int64_t)(blockIdx.x - (unsigned)plane * cpp) * kBnThreads + threadIdx.x) * VEC;
+    if (e >= V) return;
+    const int c = plane % C;
+    const int64_t i = (int64_t)plane * V + e;
     const float sc = coef[c], sh = coef[C + c];
     float v[VEC];
     vload<T, VEC>(x + i, v);
@@ -157,18 +158,19 @@ __global__ __launch_bounds__(kBnThreads) void bn_fwd_apply(const T* __restrict__
 template <typename T, int VEC, bool RELU>
 __global__ __launch_bounds__(kBnThreads) void bn_bwd_stats(const T* __restrict__ dy,
                                                            const T* __restrict__ x,
-                                                           const T* __restrict__ y, int N,
-                                                           int C, int64_t V, int64_t len,
+                                                           const T* __restrict__ y, int C,
+                                                           int64_t V, int SP, int64_t len,
                                                            const float* __restrict__ save_mean,
                                                            float* __restrict__ part) {
     const int c = blockIdx.x, sidx = blockIdx.y;
-    const int64_t M = (int64_t)N * V;
+    const int n = sidx / SP, seg = sidx - n * SP;
     const float mean = save_mean[c];
-    const int64_t beg = (int64_t)sidx * len;
-    const int64_t end = beg + len < M ? beg + len : M;
+    const int64_t beg = (int64_t)seg * len;
+    const int64_t cnt = (beg + len < V ? beg + len : V) - beg;
+    const int64_t base = ((int64_t)n * C + c) * V + beg;
     float s1 = 0.f, s2 = 0.f;
-    for (int64_t e = beg + (int64_t)threadIdx.x * VEC; e < end; e += (int64_t)kBnThreads * VEC) {
-        const int64_t idx = chan_index(e, c, C, V);
+    for (int64_t e = (int64_t)threadIdx.x * VEC; e < cnt; e += (int64_t)kBnThreads * VEC) {
+        const int64_t idx = base + e;
         float g[VEC], xv[VEC];
         vload<T, VEC>(dy + idx, g);
         vload<T, VEC>(x + idx, xv);
@@ -219,11 +221,14 @@ __global__ void bn_bwd_finalize(int N, int C, int64_t V, int slices,
 template <typename T, int VEC, bool RELU, bool DRES>
 __global__ __launch_bounds__(kBnThreads) void bn_bwd_apply(
     const T* __restrict__ dy, const T* __restrict__ x, const T* __restrict__ y, int C, int64_t V,
-    int64_t total, const float* __restrict__ save_mean, const float* __restrict__ coef,
-    T* __restrict__ dx, T* __restrict__ dres) {
-    const int64_t i = ((int64_t)blockIdx.x * kBnThreads + threadIdx.x) * VEC;
-    if (i >= total) return;
-    const int c = (int)((i / V) % C);
+    unsigned cpp, const float* __restrict__ save_mean, const float* __restrict__ coef,
+    T* __restrict__ dx,
+    T* __restrict__ dres) {
+    const int plane = (int)(blockIdx.x / cpp);  // wave-uniform
+    const int64_t e = ((int64_t)(blockIdx.x - (unsigned)plane * cpp) * kBnThreads + threadIdx.x) * VEC;
+    if (e >= V) return;
+    const int c = plane % C;
+    const int64_t i = (int64_t)plane * V + e;
     const float k = coef[c], a = coef[C + c], b = coef[2 * C + c], mean = save_mean[c];
     float g[VEC], xv[VEC];
     vload<T, VEC>(dy + i, g);
@@ -252,25 +257,25 @@ static rat3d_status bn_fwd_t(const BnGeom& g, int relu, float eps, float momentu
     const double tb = (double)g.N * g.C * g.V * sizeof(T);
     {
     ProfScope ps("bn_fwd_stats", st, 0.0, tb);
-    bn_fwd_stats<T, VEC><<<dim3(g.C, sl.per_channel), kBnThreads, 0, st>>>(x, g.N, g.C, g.V,
-                                                                          sl.len, part);
+    bn_fwd_stats<T, VEC><<<dim3(g.C, sl.per_channel), kBnThreads, 0, st>>>(
+        x, g.C, g.V, sl.per_plane, sl.len, part);
     RAT3D_LAUNCH_CHECK();
     }
     bn_fwd_finalize<T><<<(unsigned)ceil_div(g.C, 64), 64, 0, st>>>(
         x, g.N, g.C, g.V, sl.per_channel, part, gamma, beta, eps, momentum, save_mean,
         save_invstd, run_mean, run_var, coef);
     RAT3D_LAUNCH_CHECK();
-    const int64_t total = (int64_t)g.N * g.C * g.V;
-    const unsigned blocks = (unsigned)ceil_div(total / VEC, kBnThreads);
+    const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads);  // chunks per plane
+    const unsigned grid = cpp * (unsigned)(g.N * g.C);
     ProfScope ps("bn_fwd_apply", st, 0.0, tb * (r ? 3 : 2));
     if (relu && r)
-        bn_fwd_apply<T, VEC, true, true><<<blocks, kBnThreads, 0, st>>>(x, r, g.C, g.V, total, coef, y);
+        bn_fwd_apply<T, VEC, true, true><<<grid, kBnThreads, 0, st>>>(x, r, g.C, g.V, cpp, coef, y);
     else if (relu)
-        bn_fwd_apply<T, VEC, true, false><<<blocks, kBnThreads, 0, st>>>(x, r, g.C, g.V, total, coef, y);
+        bn_fwd_apply<T, VEC, true, false><<<grid, kBnThreads, 0, st>>>(x, r, g.C, g.V, cpp, coef, y);
     else if (r)
-        bn_fwd_apply<T, VEC, false, true><<<blocks, kBnThreads, 0, st>>>(x, r, g.C, g.V, total, coef, y);
+        bn_fwd_apply<T, VEC, false, true><<<grid, kBnThreads, 0, st>>>(x, r, g.C, g.V, cpp, coef, y);
     else
-        bn_fwd_apply<T, VEC, false, false><<<blocks, kBnThreads, 0, st>>>(x, r, g.C, g.V, total, coef, y);
+        bn_fwd_apply<T, VEC, false, false><<<grid, kBnThreads, 0, st>>>(x, r, g.C, g.V, cpp, coef, y);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }
@@ -288,22 +293,22 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
     {
     ProfScope ps("bn_bwd_stats", st, 0.0, tb * (relu ? 3 : 2));
     if (relu)
-        bn_bwd_stats<T, VEC, true><<<sg, kBnThreads, 0, st>>>(dy, x, y, g.N, g.C, g.V, sl.len,
-                                                              save_mean, part);
+        bn_bwd_stats<T, VEC, true><<<sg, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, sl.per_plane,
+                                                              sl.len, save_mean, part);
     else
-        bn_bwd_stats<T, VEC, false><<<sg, kBnThreads, 0, st>>>(dy, x, y, g.N, g.C, g.V, sl.len,
-                                                               save_mean, part);
+        bn_bwd_stats<T, VEC, false><<<sg, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, sl.per_plane,
+                                                               sl.len, save_mean, part);
     RAT3D_LAUNCH_CHECK();
     }
     bn_bwd_finalize<<<(unsigned)ceil_div(g.C, 64), 64, 0, st>>>(
         g.N, g.C, g.V, sl.per_channel, part, gamma, save_invstd, dgamma, dbeta, accumulate, coef);
     RAT3D_LAUNCH_CHECK();
-    const int64_t total = (int64_t)g.N * g.C * g.V;
-    const unsigned blocks = (unsigned)ceil_div(total / VEC, kBnThreads);
+    const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads);  // chunks per plane
+    const unsigned grid = cpp * (unsigned)(g.N * g.C);
     ProfScope ps("bn_bwd_apply", st, 0.0, tb * ((relu ? 4 : 3) + (dres ? 1 : 0)));
-#define RAT3D_BN_BWD(R, D)                                                                   \
-    bn_bwd_apply<T, VEC, R, D><<<blocks, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, total,     \
-                                                              save_mean, coef, dx, dres)
+#define RAT3D_BN_BWD(R, D)                                                                 \
+    bn_bwd_apply<T, VEC, R, D><<<grid, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, cpp,      \
+                                                            save_mean, coef, dx, dres)
     if (relu && dres) RAT3D_BN_BWD(true, true);
     else if (relu) RAT3D_BN_BWD(true, false);
     else if (dres) RAT3D_BN_BWD(false, true);

@@ -120,7 +120,7 @@ __device__ __forceinline__ void lds_barrier() {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int KS, int NT, int RD>
+template <int KS, int NT, int RD, bool ACC>
 __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     constexpr int P = (KS - 1) / 2;
     constexpr int PD = kBD + KS - 1, PH = kBH + KS - 1, PW = kBW + KS - 1;
@@ -356,7 +356,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     // stay off the consumer waves.
     constexpr int NUNIT_CG = 16 * kBD * kBH * 2;  // units per channel group
     static_assert(KS != 3 || NUNIT_CG <= PD * PH * PW, "staged outputs fit the brick");
-    const bool staged_epi = !a.accumulate && (a.W & 7) == 0;
+    const bool staged_epi = !ACC && (a.W & 7) == 0;
     auto write_outputs = [&](int k, unsigned char* buf) {
         const Tile T = tile_of(k);
         float bv[CT];
@@ -437,6 +437,89 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             }
         }
     };
+    // Accumulating outputs (dst += conv), staged in float32 so that each output
+    // is rounded once: the 32 channels of consumer column group wc (CT = 2)
+    // are written as 16-byte units of four w, i = ((co % 8) * 4 + d) * 32 + h * 4
+    // + w / 4 in brick row i / PW, column i % PW, channel slot (co % 32) / 8,
+    // and drained (old value added, then rounded) by the producer that owns
+    // the slot.  The groups are written one after the other; the last one is
+    // drained in the next step, the others before the next group is written.
+    const bool staged_acc = ACC && KS == 3 && CT == 2 && (a.W & 7) == 0;
+    auto write_fp32 = [&](int k, unsigned char* buf) {
+        const Tile T = tile_of(k);
+        float bv[CT];
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+            bv[ct] = a.bias ? a.bias[T.co0 + (wc * CT + ct) * 16 + li] : 0.f;
+        int ib = ((li & 7) * kBD + wd * RD) * kBH * 4 + kg;
+        asm volatile("" : "+v"(ib));
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            const int i = ib + r * 4;
+            const int row = i / PW, ww = i - row * PW;
+            unsigned char* base = buf + (uint32_t)(row * PW) * 64u;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct)
+                *reinterpret_cast<float4*>(base + brick_slot_off<KS>(ww, ct * 2 + (li >> 3))) =
+                    make_float4(acc[r][ct][0] + bv[ct], acc[r][ct][1] + bv[ct],
+                                acc[r][ct][2] + bv[ct], acc[r][ct][3] + bv[ct]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    auto drain_fp32 = [&](int k, int hf, const unsigned char* buf) {
+        const Tile T = tile_of(k);
+        // every owned unit's old value is requested at once (one round trip);
+        // units outside the tensor or the group use an offset past the buffer
+        // end, which reads zeros and is never stored
+        const __amdgpu_buffer_rsrc_t dst_r =
+            buf_rsrc(a.dst + (int64_t)T.n * a.Ct * V, (uint32_t)a.Ct * Vb);
+        constexpr int RB = 2;  // items per batch (16 old values in flight)
+#pragma unroll
+        for (int r0 = 0; r0 < NRND; r0 += RB) {
+            uint32_t off[RB][8];
+            uint2 old[RB][8];
+#pragma unroll
+            for (int ri = 0; ri < RB; ++ri) {
+                int pair, q;
+                const bool live = r0 + ri < NRND && item_of(r0 + ri, pair, q);
+                const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int ww = 8 * (q + Q0) + e + P;
+                    const int i = row * PW + ww;
+                    const int q4 = i & 3, h = (i >> 2) & (kBH - 1), d = (i >> 5) & (kBD - 1);
+                    const int co = T.co0 + hf * 32 + cg * 8 + (i >> 7);
+                    const int dd = T.d0 + d, hh = T.h0 + h, w = T.w0 + 4 * q4;
+                    const bool ok = live && ww >= 0 && ww < PW && i < 32 * kBD * kBH &&
+                                    dd < a.D && hh < a.H && w < a.W;
+                    off[ri][e] =
+                        ok ? (uint32_t)((co * V + dd * HW + hh * a.W + w) * 2) : 0x80000000u;
+                    old[ri][e] = buf_ld8(dst_r, off[ri][e], 0u);
+                }
+            }
+#pragma unroll
+            for (int ri = 0; ri < RB; ++ri) {
+                int pair, q;
+                if (!(r0 + ri < NRND && item_of(r0 + ri, pair, q))) continue;
+                const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    if (off[ri][e] == 0x80000000u) continue;
+                    const int ww = 8 * (q + Q0) + e + P;
+                    const float4 v = *reinterpret_cast<const float4*>(
+                        buf + (uint32_t)(row * PW) * 64u + brick_slot_off<KS>(ww, cg));
+                    const uint2 o = old[ri][e];
+                    buf_st8(dst_r,
+                            make_uint2(pack_bf16x2(v.x + __uint_as_float(o.x << 16),
+                                                   v.y + __uint_as_float(o.x & 0xffff0000u)),
+                                       pack_bf16x2(v.z + __uint_as_float(o.y << 16),
+                                                   v.w + __uint_as_float(o.y & 0xffff0000u))),
+                            off[ri][e], 0u);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
     // direct epilogue (accumulating outputs, widths not a multiple of 8, 1^3):
     // lane holds 4 consecutive w of one output channel per tile row
     auto direct_outputs = [&](int k) {
@@ -494,6 +577,13 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
                 lds_barrier();  // every consumer is done reading buf
                 write_outputs(k, buf);
                 lds_barrier();
+            } else if (tile_end(k) && staged_acc) {
+                lds_barrier();  // every consumer is done reading buf
+                for (int hf = 0; hf < WC; ++hf) {
+                    if (wc == hf) write_fp32(k, buf);
+                    lds_barrier();
+                    if (hf + 1 < WC) lds_barrier();  // group hf drained
+                }
             } else {
                 if (tile_end(k)) direct_outputs(k);
                 lds_barrier();
@@ -503,16 +593,37 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         if (S > 0) stage(0, lds);
         lds_barrier();
         for (int k = 0; k < S; ++k) {
-            if (staged_epi && k > 0 && tile_end(k - 1)) drain(k - 1, lds + ((k - 1) & 1) * BB);
+            if (k > 0 && tile_end(k - 1)) {
+                if (staged_epi) {
+                    drain(k - 1, lds + ((k - 1) & 1) * BB);
+                } else if (staged_acc) {
+                    drain_fp32(k - 1, WC - 1, lds + ((k - 1) & 1) * BB);
+                }
+            }
             if (k + 1 < S) stage(k + 1, lds + ((k + 1) & 1) * BB);
             if (tile_end(k) && staged_epi) {
                 lds_barrier();
                 lds_barrier();
+            } else if (tile_end(k) && staged_acc) {
+                lds_barrier();
+                for (int hf = 0; hf < WC; ++hf) {
+                    lds_barrier();
+                    if (hf + 1 < WC) {
+                        drain_fp32(k, hf, lds + (k & 1) * BB);
+                        lds_barrier();
+                    }
+                }
             } else {
                 lds_barrier();
             }
         }
-        if (staged_epi && S > 0) drain(S - 1, lds + ((S - 1) & 1) * BB);
+        if (S > 0) {
+            if (staged_epi) {
+                drain(S - 1, lds + ((S - 1) & 1) * BB);
+            } else if (staged_acc) {
+                drain_fp32(S - 1, WC - 1, lds + ((S - 1) & 1) * BB);
+            }
+        }
     }
 }
 
@@ -791,7 +902,10 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
     a.th = (int)ceil_div(g.H, kBH);
     a.tw = (int)ceil_div(g.W, kBW);
     a.accumulate = accumulate;
-    const int nt = a.Ct % 64 == 0 ? 4 : 2;
+    // 64-channel tiles, unless that leaves most CUs idle (small volumes): then
+    // 32-channel tiles double the workgroups
+    const int64_t sp_tiles = (int64_t)g.N * a.td * a.th * a.tw;
+    const int nt = (a.Ct % 64 == 0 && sp_tiles * (a.Ct / 64) >= device_cus() / 2) ? 4 : 2;
     a.cogs = a.Ct / (nt * 16);
     a.ntiles = (int)((int64_t)g.N * a.td * a.th * a.tw * a.cogs);
     // one persistent workgroup per CU (fewer when there are fewer tiles)
@@ -799,12 +913,23 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
     ProfScope ps(dgrad ? (g.k == 3 ? "conv_brick3_dgrad" : "conv_brick1_dgrad")
                        : (g.k == 3 ? "conv_brick3_fwd" : "conv_brick1_fwd"),
                  st, conv_flops(g), conv_bytes(g, 2));
+    const bool acc = accumulate != 0;
     if (g.k == 3) {
-        if (nt == 4) conv_brick_fd<3, 4, 2><<<grid, 512, 0, st>>>(a);
-        else conv_brick_fd<3, 2, 1><<<grid, 512, 0, st>>>(a);
+        if (nt == 4) {
+            if (acc) conv_brick_fd<3, 4, 2, true><<<grid, 512, 0, st>>>(a);
+            else conv_brick_fd<3, 4, 2, false><<<grid, 512, 0, st>>>(a);
+        } else {
+            if (acc) conv_brick_fd<3, 2, 1, true><<<grid, 512, 0, st>>>(a);
+            else conv_brick_fd<3, 2, 1, false><<<grid, 512, 0, st>>>(a);
+        }
     } else {
-        if (nt == 4) conv_brick_fd<1, 4, 2><<<grid, 512, 0, st>>>(a);
-        else conv_brick_fd<1, 2, 1><<<grid, 512, 0, st>>>(a);
+        if (nt == 4) {
+            if (acc) conv_brick_fd<1, 4, 2, true><<<grid, 512, 0, st>>>(a);
+            else conv_brick_fd<1, 4, 2, false><<<grid, 512, 0, st>>>(a);
+        } else {
+            if (acc) conv_brick_fd<1, 2, 1, true><<<grid, 512, 0, st>>>(a);
+            else conv_brick_fd<1, 2, 1, false><<<grid, 512, 0, st>>>(a);
+        }
     }
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;

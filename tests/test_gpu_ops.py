@@ -38,6 +38,8 @@ CONV_CASES = [
     (2, 64, 64, 5, 9, 24, 1, 1, 0, True, "bf16"),
     (1, 32, 64, 3, 3, 8, 1, 1, 0, False, "bf16"),
     (1, 96, 64, 9, 17, 48, 3, 1, 1, False, "bf16"),
+    # weight-gradient bricks on widths divisible by 4 but not 8 (ragged last tile)
+    (1, 64, 64, 5, 6, 20, 3, 1, 1, False, "bf16"),
     # the small deep-stage volumes of the full network (tiles mostly outside)
     (2, 64, 64, 12, 14, 12, 1, 1, 0, False, "bf16"),
     (2, 128, 128, 6, 7, 6, 3, 1, 1, False, "bf16"),
