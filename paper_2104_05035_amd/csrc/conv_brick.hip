@@ -44,7 +44,7 @@ union F16B {
 };
 
 constexpr int kBD = 4, kBH = 8, kBW = 16;     // forward output tile
-constexpr int kWD = 1, kWH = 8, kWW = 16;     // weight-gradient voxel brick
+constexpr int kWH = 8, kWW = 16;              // weight-gradient voxel brick (one depth slice)
 
 __device__ __forceinline__ f32x4 mfma(const F16B& a, const F16B& b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.b, b.b, c, 0, 0, 0);
@@ -632,12 +632,12 @@ namespace {
 struct WgArgs {
     const bf16* x;   // [N][Ci][D][H][W]
     const bf16* dy;  // [N][Co][D][H][W]
-    float* part;     // [ranges][Co][Ci][KT]
+    float* part;     // [ranges][groups] blocks of kWgPart floats
     int N, Ci, Co, D, H, W;
-    int td, th, tw;  // bricks per axis
-    int64_t nbricks;
-    int bpr;         // bricks per range
-    int cigs, cogs;  // input-channel groups of 16, output-channel groups of 64
+    int tds, th, tw;  // steps (depth pairs) per column, row tiles, column tiles
+    int nsteps;       // N * th * tw * tds
+    int spr;          // steps per range
+    int cigs, cogs;   // input-channel groups of 16, output-channel groups of 64
 };
 }  // namespace
 
@@ -648,160 +648,239 @@ struct WgArgs {
 constexpr int kWgNtap = 7;                       // taps per wave: wave + 4 j < 27
 constexpr int kWgPart = kWgNtap * 4 * 4 * 256;   // floats per workgroup partial
 
+// Persistent producer/consumer weight gradient, one 512-thread workgroup per
+// CU.  A workgroup owns dw for 64 C_out x 16 C_in x 27 taps and sums over a
+// range of steps; a step is two 1 x 8 x 16 voxel bricks at depths d0, d0 + 1
+// of one (n, row tile, column tile) column, steps ordered depth-fastest.
+// Waves 0-3 multiply (wave w owns taps w, w + 4, ...; GEMM K = voxels, A = dy
+// rows of 16 output channels, B = x rows of 16 input channels shifted by the
+// tap); waves 4-7 stage.  dy of a step goes to one of two LDS buffers; x
+// planes live in a ring of six LDS slots (input depth z in slot z mod 6), each
+// kept as three kw-shifted copies so that every 8-voxel operand is an aligned
+// 16-byte read.  A step needs planes d0 - 1 .. d0 + 2; its successor in the
+// same column needs two new planes, whose slots the current step does not
+// read, so the producers fill them while the consumers work.  The first step
+// of a range or column loads all four planes after the previous step is done
+// (one extra barrier).  Producers keep two register sets: the loads for step
+// k + 2 are issued during step k and written to LDS during step k + 1.
+constexpr int kWgSlots = 6;
+
 template <int KS>
-__global__ __launch_bounds__(256, 2) void conv_brick_wgrad(WgArgs a) {
+__global__ __launch_bounds__(512, 1) void conv_brick_wgrad(WgArgs a) {
     constexpr int P = (KS - 1) / 2;
     constexpr int KT = KS * KS * KS;
     static_assert(KS == 3, "the weight-gradient brick assembles kw = 0, 1, 2 copies");
-    constexpr int PD = kWD + KS - 1, PH = kWH + KS - 1;
-    constexpr int ROWS = PD * PH;
-    constexpr int CIS = ROWS * 32 + 16;  // bytes per input channel (rows of 16 bf16) + pad
-    constexpr int KWS = 16 * CIS;        // bytes per kw-shifted copy
-    constexpr int NTAP = (KT + 3) / 4;   // taps per wave
+    constexpr int PH = kWH + KS - 1;                // x rows per plane
+    constexpr int CIS = kWgSlots * PH * 32 + 16;     // bytes per input channel in a copy (+ pad)
+    constexpr int KWS = 16 * CIS;                    // bytes per kw-shifted copy
+    constexpr int DYS = 2 * kWH * 32 + 16;           // bytes per output channel of a step (+ pad)
+    constexpr int DYB = 64 * DYS;                    // bytes per dy buffer
+    constexpr int NTAP = (KT + 3) / 4;               // taps per consumer wave
     static_assert(NTAP == kWgNtap, "partial layout");
-    constexpr int NIT = (16 * ROWS + 255) / 256;  // x staging items per thread
-    constexpr int DYS = kWH * 32 + 16;            // bytes per dy channel (rows of 16 bf16) + pad
-    constexpr int NDY = 64 * kWH * 2 / 256;       // dy staging items (16 bytes) per thread
-    static_assert(kWD == 1, "one depth slice per brick: dy rows are h0 .. h0 + kWH - 1");
-    __shared__ __align__(16) unsigned char xs[KS * KWS + 64 * DYS];
-    unsigned char* const dys = xs + KS * KWS;
+    constexpr int NXI = (16 * 4 * PH + 255) / 256;   // x staging items per producer thread (full)
+    constexpr int NDY = 2 * 64 * kWH * 2 / 256;      // dy staging items (16 bytes) per thread
+    __shared__ __align__(16) unsigned char lds[KS * KWS + 2 * DYB];
+    unsigned char* const xs = lds;
+    unsigned char* const dys = lds + KS * KWS;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const bool consumer = wave < 4;
     const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int groups = a.cigs * a.cogs;
     const int cig = L % a.cigs;
-    const int rest = L / a.cigs;
-    const int cog = rest % a.cogs;
-    const int range = rest / a.cogs;
+    const int cog = (L / a.cigs) % a.cogs;
+    const int range = L / groups;
     const int ci0 = cig * 16, co0 = cog * 64;
-    const int64_t b_beg = (int64_t)range * a.bpr;
-    const int64_t b_end = b_beg + a.bpr < a.nbricks ? b_beg + a.bpr : a.nbricks;
+    const int s_beg = range * a.spr;
+    const int s_end = s_beg + a.spr < a.nsteps ? s_beg + a.spr : a.nsteps;
+    const int S = s_end > s_beg ? s_end - s_beg : 0;
     const int64_t HW = (int64_t)a.H * a.W, V = HW * a.D;
+
+    struct Step {
+        int n, d0, h0, w0;
+        bool full;  // first step of the range or of a column: all four planes
+    };
+    auto step_at = [&](int k) __attribute__((always_inline)) {
+        const int sidx = s_beg + k;
+        Step t;
+        const int dp = sidx % a.tds;
+        int r = sidx / a.tds;
+        t.d0 = 2 * dp;
+        t.w0 = (r % a.tw) * kWW;
+        r /= a.tw;
+        t.h0 = (r % a.th) * kWH;
+        t.n = r / a.th;
+        t.full = k == 0 || dp == 0;
+        return t;
+    };
+    auto slot_of = [](int z) { return (z + kWgSlots) % kWgSlots; };
+
+    // ---- producer
+    struct Regs {
+        uint32_t m[NXI][10];  // x rows: m[0] = (?, x[w0-1]), m[1..8] = x[w0..w0+15], m[9] = (x[w0+16], ?)
+        uint4 dy[NDY];
+    };
+    const int ptid = tid - 256;
+    // x item q of a step: full -> planes d0 - 1 .. d0 + 2, else planes d0 + 1, d0 + 2
+    auto x_item = [&](const Step& t, int q, int& ci, int& z, int& row) __attribute__((always_inline)) {
+        const int it = ptid + 256 * q;
+        const int np = t.full ? 4 : 2;
+        ci = it / (np * PH);
+        const int rr = it - ci * (np * PH);
+        z = (t.full ? t.d0 - P : t.d0 + 1) + rr / PH;
+        row = rr % PH;
+        return it < 16 * np * PH;
+    };
+    auto load = [&](const Step& t, Regs& R) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < NXI; ++q) {
+#pragma unroll
+            for (int j = 0; j < 10; ++j) R.m[q][j] = 0u;
+            int ci, z, row;
+            if (!x_item(t, q, ci, z, row)) continue;
+            const int h = t.h0 - P + row;
+            if ((unsigned)z >= (unsigned)a.D || (unsigned)h >= (unsigned)a.H) continue;
+            const bf16* p = a.x + ((int64_t)t.n * a.Ci + ci0 + ci) * V + z * HW +
+                            (int64_t)h * a.W + t.w0;
+            if (t.w0 + 8 <= a.W) {
+                const uint4 u = *reinterpret_cast<const uint4*>(p);
+                R.m[q][1] = u.x; R.m[q][2] = u.y; R.m[q][3] = u.z; R.m[q][4] = u.w;
+            }
+            if (t.w0 + 16 <= a.W) {
+                const uint4 u = *reinterpret_cast<const uint4*>(p + 8);
+                R.m[q][5] = u.x; R.m[q][6] = u.y; R.m[q][7] = u.z; R.m[q][8] = u.w;
+            }
+            if (t.w0 >= 1) R.m[q][0] = (uint32_t)p[-1] << 16;
+            if (t.w0 + 16 < a.W) R.m[q][9] = (uint32_t)p[16];
+        }
+#pragma unroll
+        for (int q = 0; q < NDY; ++q) {
+            const int it = ptid + 256 * q;
+            const int j = it >> 10, rem = it & 1023;
+            const int co = rem >> 4, row = (rem >> 1) & (kWH - 1), half = rem & 1;
+            const int d = t.d0 + j, h = t.h0 + row, w = t.w0 + 8 * half;
+            R.dy[q] = make_uint4(0u, 0u, 0u, 0u);
+            if (d < a.D && h < a.H && w + 8 <= a.W)
+                R.dy[q] = *reinterpret_cast<const uint4*>(
+                    a.dy + ((int64_t)t.n * a.Co + co0 + co) * V + d * HW + (int64_t)h * a.W + w);
+        }
+    };
+    auto commit_dy = [&](const Regs& R, unsigned char* db) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < NDY; ++q) {
+            const int it = ptid + 256 * q;
+            const int j = it >> 10, rem = it & 1023;
+            const int co = rem >> 4, row = (rem >> 1) & (kWH - 1), half = rem & 1;
+            *reinterpret_cast<uint4*>(db + co * DYS + (j * kWH + row) * 32 + half * 16) = R.dy[q];
+        }
+    };
+    // copy kw holds input columns w0 - 1 + kw ... as aligned 16-byte rows
+    auto commit_x = [&](const Step& t, const Regs& R) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < NXI; ++q) {
+            int ci, z, row;
+            if (!x_item(t, q, ci, z, row)) continue;
+            unsigned char* base = xs + ci * CIS + (slot_of(z) * PH + row) * 32;
+            const uint32_t* m = R.m[q];
+            *reinterpret_cast<uint4*>(base + KWS) = make_uint4(m[1], m[2], m[3], m[4]);
+            *reinterpret_cast<uint4*>(base + KWS + 16) = make_uint4(m[5], m[6], m[7], m[8]);
+            uint32_t s0[8], s2[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                s0[i] = __builtin_amdgcn_alignbit(m[i + 1], m[i], 16);
+                s2[i] = __builtin_amdgcn_alignbit(m[i + 2], m[i + 1], 16);
+            }
+            *reinterpret_cast<uint4*>(base) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
+            *reinterpret_cast<uint4*>(base + 16) = make_uint4(s0[4], s0[5], s0[6], s0[7]);
+            *reinterpret_cast<uint4*>(base + 2 * KWS) = make_uint4(s2[0], s2[1], s2[2], s2[3]);
+            *reinterpret_cast<uint4*>(base + 2 * KWS + 16) = make_uint4(s2[4], s2[5], s2[6], s2[7]);
+        }
+    };
+
+    // Barrier schedule (both roles): one prologue barrier, then per step one
+    // barrier, plus one more before a step whose x planes are all reloaded.
+    if (!consumer) {
+        Regs R0, R1;
+        if (S > 0) {
+            const Step t0 = step_at(0);
+            load(t0, R0);
+            if (S > 1) load(step_at(1), R1);
+            commit_dy(R0, dys);
+            commit_x(t0, R0);
+        }
+        lds_barrier();
+        // step k: stage step k + 1 (registers of set (k + 1) & 1), then load
+        // step k + 2 into the set just freed; unrolled by two so that the sets
+        // are static
+        auto body = [&](int k, Regs& Rn, Regs& Rf) __attribute__((always_inline)) {
+            // Rn holds step k + 1; Rf is free
+            if (k + 1 < S) {
+                const Step tn = step_at(k + 1);
+                commit_dy(Rn, dys + ((k + 1) & 1) * DYB);
+                if (!tn.full) commit_x(tn, Rn);
+                if (k + 2 < S) load(step_at(k + 2), Rf);
+                lds_barrier();
+                if (tn.full) {
+                    commit_x(tn, Rn);
+                    lds_barrier();
+                }
+            } else {
+                lds_barrier();
+            }
+        };
+        for (int k = 0; k < S; k += 2) {
+            body(k, R1, R0);
+            if (k + 1 < S) body(k + 1, R0, R1);
+        }
+        return;
+    }
+
+    // ---- consumer
     const int li = lane & 15, kg = lane >> 4;
     const int hl_l = kg >> 1, wl = (kg & 1) * 8;
-
     f32x4 acc[NTAP][4];
 #pragma unroll
     for (int j = 0; j < NTAP; ++j)
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[j][c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    struct Brick {
-        int n, d0, h0, w0;
-    };
-    auto brick_at = [&](int64_t b) {
-        Brick k;
-        k.w0 = (int)(b % a.tw) * kWW;
-        int64_t r = b / a.tw;
-        k.h0 = (int)(r % a.th) * kWH;
-        r /= a.th;
-        k.d0 = (int)(r % a.td) * kWD;
-        k.n = (int)(r / a.td);
-        return k;
-    };
-
-    // Both operands of a brick are staged through LDS; the next brick's rows
-    // are fetched into registers before the current brick's K loop so that
-    // the loads are in flight while the MFMAs run.
-    // x item = (input channel, brick row): the row's 16 aligned voxels (two
-    // 16-byte loads) plus one halo voxel on each side, held as
-    // m[0] = (?, x[w0-1]), m[1..8] = x[w0 .. w0+15], m[9] = (x[w0+16], ?).
-    // dy item = (output channel, row, half): 8 voxels, one 16-byte load.
-    uint32_t m[NIT][10];
-    uint4 dyv[NDY];
-    auto fetch = [&](const Brick& k) {
+    lds_barrier();
+    for (int k = 0; k < S; ++k) {
+        const Step t = step_at(k);
+        const unsigned char* db = dys + (k & 1) * DYB;
+#pragma unroll 1
+        for (int j = 0; j < 2; ++j) {
+            const int d = t.d0 + j;
+            if (d >= a.D) break;
+            // plane slot of tap depth kd: input depth d - 1 + kd
+            const int sl0 = slot_of(d - 1), sl1 = slot_of(d), sl2 = slot_of(d + 1);
+            // K step s covers brick rows 2s, 2s + 1 (32 voxels): lane (li, kg)
+            // holds 8 voxels of row 2s + kg/2, columns 8 (kg % 2) ..
 #pragma unroll
-        for (int q = 0; q < NIT; ++q) {
+            for (int s_ = 0; s_ < kWH / 2; ++s_) {
+                const int hl = 2 * s_ + hl_l;
+                F16B ac[4];
 #pragma unroll
-            for (int j = 0; j < 10; ++j) m[q][j] = 0u;
-            const int it = tid + 256 * q;
-            if (it >= 16 * ROWS) continue;
-            const int row = it % ROWS, ci = it / ROWS;
-            const int d = k.d0 - P + row / PH, h = k.h0 - P + row % PH;
-            if ((unsigned)d >= (unsigned)a.D || (unsigned)h >= (unsigned)a.H) continue;
-            const bf16* p = a.x + ((int64_t)k.n * a.Ci + ci0 + ci) * V + d * HW +
-                            (int64_t)h * a.W + k.w0;
-            if (k.w0 + 8 <= a.W) {
-                const uint4 u = *reinterpret_cast<const uint4*>(p);
-                m[q][1] = u.x; m[q][2] = u.y; m[q][3] = u.z; m[q][4] = u.w;
-            }
-            if (k.w0 + 16 <= a.W) {
-                const uint4 u = *reinterpret_cast<const uint4*>(p + 8);
-                m[q][5] = u.x; m[q][6] = u.y; m[q][7] = u.z; m[q][8] = u.w;
-            }
-            if (k.w0 >= 1) m[q][0] = (uint32_t)p[-1] << 16;
-            if (k.w0 + 16 < a.W) m[q][9] = (uint32_t)p[16];
-        }
+                for (int ct = 0; ct < 4; ++ct)
+                    ac[ct].u = *reinterpret_cast<const uint4*>(
+                        db + (ct * 16 + li) * DYS + (j * kWH + hl) * 32 + wl * 2);
 #pragma unroll
-        for (int q = 0; q < NDY; ++q) {
-            const int it = tid + 256 * q;
-            const int co = it >> 4, row = (it >> 1) & (kWH - 1), half = it & 1;
-            const int h = k.h0 + row, w = k.w0 + 8 * half;
-            dyv[q] = make_uint4(0u, 0u, 0u, 0u);
-            if (k.d0 < a.D && h < a.H && w + 8 <= a.W)
-                dyv[q] = *reinterpret_cast<const uint4*>(
-                    a.dy + ((int64_t)k.n * a.Co + co0 + co) * V + k.d0 * HW + (int64_t)h * a.W + w);
-        }
-    };
-    // copy kw holds input columns w0 - 1 + kw ... as aligned 16-byte LDS rows
-    auto commit = [&]() {
+                for (int jj = 0; jj < NTAP; ++jj) {
+                    const int tp = wave + 4 * jj;
+                    if (tp < KT) {
+                        const int kd = tp / (KS * KS), kh = (tp / KS) % KS, kw = tp % KS;
+                        const int sl = kd == 0 ? sl0 : (kd == 1 ? sl1 : sl2);
+                        F16B bv;
+                        bv.u = *reinterpret_cast<const uint4*>(
+                            xs + kw * KWS + li * CIS + (sl * PH + hl + kh) * 32 + wl * 2);
 #pragma unroll
-        for (int q = 0; q < NIT; ++q) {
-            const int it = tid + 256 * q;
-            if (it >= 16 * ROWS) continue;
-            const int row = it % ROWS, ci = it / ROWS;
-            unsigned char* base = xs + ci * CIS + row * 32;
-            *reinterpret_cast<uint4*>(base + KWS) = make_uint4(m[q][1], m[q][2], m[q][3], m[q][4]);
-            *reinterpret_cast<uint4*>(base + KWS + 16) =
-                make_uint4(m[q][5], m[q][6], m[q][7], m[q][8]);
-            uint32_t s0[8], s2[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                s0[i] = __builtin_amdgcn_alignbit(m[q][i + 1], m[q][i], 16);
-                s2[i] = __builtin_amdgcn_alignbit(m[q][i + 2], m[q][i + 1], 16);
-            }
-            *reinterpret_cast<uint4*>(base) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
-            *reinterpret_cast<uint4*>(base + 16) = make_uint4(s0[4], s0[5], s0[6], s0[7]);
-            *reinterpret_cast<uint4*>(base + 2 * KWS) = make_uint4(s2[0], s2[1], s2[2], s2[3]);
-            *reinterpret_cast<uint4*>(base + 2 * KWS + 16) =
-                make_uint4(s2[4], s2[5], s2[6], s2[7]);
-        }
-#pragma unroll
-        for (int q = 0; q < NDY; ++q) {
-            const int it = tid + 256 * q;
-            const int co = it >> 4, row = (it >> 1) & (kWH - 1), half = it & 1;
-            *reinterpret_cast<uint4*>(dys + co * DYS + row * 32 + half * 16) = dyv[q];
-        }
-    };
-
-    if (b_beg < b_end) fetch(brick_at(b_beg));
-    for (int64_t b = b_beg; b < b_end; ++b) {
-        __syncthreads();  // every wave is done reading the previous brick
-        commit();
-        __syncthreads();
-        if (b + 1 < b_end) fetch(brick_at(b + 1));
-        // K step s covers brick rows 2s and 2s + 1 (32 voxels): lane (li, kg)
-        // holds 8 voxels of row 2s + kg/2, columns 8 (kg % 2) ..
-#pragma unroll
-        for (int s = 0; s < kWH / 2; ++s) {
-            const int hl = 2 * s + hl_l;
-            F16B ac[4];
-#pragma unroll
-            for (int ct = 0; ct < 4; ++ct)
-                ac[ct].u = *reinterpret_cast<const uint4*>(dys + (ct * 16 + li) * DYS + hl * 32 +
-                                                           wl * 2);
-#pragma unroll
-            for (int j = 0; j < NTAP; ++j) {
-                const int t = wave + 4 * j;
-                if (t < KT) {
-                    const int kd = t / (KS * KS), kh = (t / KS) % KS, kw = t % KS;
-                    F16B bv;
-                    bv.u = *reinterpret_cast<const uint4*>(
-                        xs + kw * KWS + li * CIS + (kd * PH + hl + kh) * 32 + wl * 2);
-#pragma unroll
-                    for (int ct = 0; ct < 4; ++ct) acc[j][ct] = mfma(ac[ct], bv, acc[j][ct]);
+                        for (int ct = 0; ct < 4; ++ct) acc[jj][ct] = mfma(ac[ct], bv, acc[jj][ct]);
+                    }
                 }
             }
         }
+        lds_barrier();
+        if (k + 1 < S && step_at(k + 1).full) lds_barrier();
     }
 
     float* out = a.part + (int64_t)L * kWgPart + tid;
@@ -856,21 +935,22 @@ bool brick_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) {
 
 size_t brick_fd_ws(const ConvGeom& g) { return (size_t)g.Co * g.Ci * g.k * g.k * g.k * 2; }
 
-static int wgrad_ranges(const ConvGeom& g, int64_t nbricks) {
-    // about two workgroups per CU in one wave (256 CUs, 2 resident each)
+static int64_t wgrad_steps(const ConvGeom& g) {
+    return (int64_t)g.N * ceil_div(g.H, kWH) * ceil_div(g.W, kWW) * ceil_div(g.D, 2);
+}
+
+static int wgrad_ranges(const ConvGeom& g) {
+    // one workgroup per CU: the (C_in, C_out) groups times the step ranges
     const int64_t groups = (int64_t)(g.Ci / 16) * (g.Co / 64);
-    int64_t r = ceil_div(512, groups);
-    if (r > nbricks) r = nbricks;
+    int64_t r = device_cus() / groups;
+    const int64_t ns = wgrad_steps(g);
+    if (r > ns) r = ns;
     if (r < 1) r = 1;
     return (int)r;
 }
 
-static int64_t wgrad_bricks(const ConvGeom& g) {
-    return (int64_t)g.N * ceil_div(g.D, kWD) * ceil_div(g.H, kWH) * ceil_div(g.W, kWW);
-}
-
 size_t brick_wgrad_ws(const ConvGeom& g) {
-    const int R = wgrad_ranges(g, wgrad_bricks(g));
+    const int R = wgrad_ranges(g);
     return (size_t)R * (g.Ci / 16) * (g.Co / 64) * kWgPart * sizeof(float);
 }
 
@@ -947,18 +1027,18 @@ rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, 
     a.D = g.D;
     a.H = g.H;
     a.W = g.W;
-    a.td = (int)ceil_div(g.D, kWD);
+    a.tds = (int)ceil_div(g.D, 2);
     a.th = (int)ceil_div(g.H, kWH);
     a.tw = (int)ceil_div(g.W, kWW);
-    a.nbricks = wgrad_bricks(g);
-    const int R = wgrad_ranges(g, a.nbricks);
-    a.bpr = (int)ceil_div(a.nbricks, R);
-    const int Rreal = (int)ceil_div(a.nbricks, a.bpr);
+    a.nsteps = (int)wgrad_steps(g);
+    const int R = wgrad_ranges(g);
+    a.spr = (int)ceil_div(a.nsteps, R);
+    const int Rreal = (int)ceil_div(a.nsteps, a.spr);
     a.cigs = g.Ci / 16;
     a.cogs = g.Co / 64;
     {
         ProfScope ps("conv_brick3_wgrad", st, conv_flops(g), conv_bytes(g, 2));
-        conv_brick_wgrad<3><<<(unsigned)((int64_t)Rreal * a.cigs * a.cogs), 256, 0, st>>>(a);
+        conv_brick_wgrad<3><<<(unsigned)((int64_t)Rreal * a.cigs * a.cogs), 512, 0, st>>>(a);
         RAT3D_LAUNCH_CHECK();
     }
     const int groups = a.cigs * a.cogs;
