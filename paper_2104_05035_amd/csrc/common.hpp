@@ -68,6 +68,10 @@ __device__ __forceinline__ uint2 buf_ld8(__amdgpu_buffer_rsrc_t r, uint32_t voff
     const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
     return make_uint2(v.x, v.y);
 }
+__device__ __forceinline__ uint32_t buf_ld2(__amdgpu_buffer_rsrc_t r, uint32_t voff,
+                                            uint32_t soff) {
+    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+}
 __device__ __forceinline__ void buf_st8(__amdgpu_buffer_rsrc_t r, uint2 v, uint32_t voff,
                                         uint32_t soff) {
     const u32x2 w = {v.x, v.y};

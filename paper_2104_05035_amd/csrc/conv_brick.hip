@@ -855,29 +855,356 @@ __global__ __launch_bounds__(512, 1) void conv_brick_wgrad(WgArgs a) {
             // plane slot of tap depth kd: input depth d - 1 + kd
             const int sl0 = slot_of(d - 1), sl1 = slot_of(d), sl2 = slot_of(d + 1);
             // K step s covers brick rows 2s, 2s + 1 (32 voxels): lane (li, kg)
-            // holds 8 voxels of row 2s + kg/2, columns 8 (kg % 2) ..
+            // holds 8 voxels of row 2s + kg/2, columns 8 (kg % 2) ..  The 28
+            // operand groups (s, tap slot) run as one straight sequence: the B
+            // operand of group g + 3 and, halfway through s, the A operands of
+            // s + 1 are read while group g multiplies.  Wave 3's seventh slot
+            // repeats tap 26 (kept uniform so the sequence has no branch); its
+            // sums are never read.
+            const unsigned char* abase = db + li * DYS + (j * kWH + hl_l) * 32 + wl * 2;
+            int boff[NTAP];
 #pragma unroll
-            for (int s_ = 0; s_ < kWH / 2; ++s_) {
-                const int hl = 2 * s_ + hl_l;
-                F16B ac[4];
+            for (int jj = 0; jj < NTAP; ++jj) {
+                int tp = wave + 4 * jj;
+                tp = tp < KT ? tp : KT - 1;
+                const int kd = tp / (KS * KS), kh = (tp / KS) % KS, kw = tp % KS;
+                const int sl = kd == 0 ? sl0 : (kd == 1 ? sl1 : sl2);
+                boff[jj] = kw * KWS + li * CIS + (sl * PH + hl_l + kh) * 32 + wl * 2;
+            }
+            constexpr int G = (kWH / 2) * NTAP;
+            constexpr int LA = 3;
+            F16B A[2][4], B[4];
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct)
+                A[0][ct].u = *reinterpret_cast<const uint4*>(abase + ct * 16 * DYS);
+#pragma unroll
+            for (int g = 0; g < LA; ++g)
+                B[g].u = *reinterpret_cast<const uint4*>(xs + boff[g % NTAP] + (g / NTAP) * 64);
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const int s_ = g / NTAP, jj = g % NTAP;
+                if (g + LA < G) {
+                    const int gn = g + LA;
+                    B[gn % 4].u = *reinterpret_cast<const uint4*>(xs + boff[gn % NTAP] +
+                                                                  (gn / NTAP) * 64);
+                }
+                if (jj == 3 && s_ + 1 < kWH / 2) {
+#pragma unroll
+                    for (int ct = 0; ct < 4; ++ct)
+                        A[(s_ + 1) & 1][ct].u = *reinterpret_cast<const uint4*>(
+                            abase + ct * 16 * DYS + (s_ + 1) * 64);
+                }
 #pragma unroll
                 for (int ct = 0; ct < 4; ++ct)
-                    ac[ct].u = *reinterpret_cast<const uint4*>(
-                        db + (ct * 16 + li) * DYS + (j * kWH + hl) * 32 + wl * 2);
+                    acc[jj][ct] = mfma(A[s_ & 1][ct], B[g % 4], acc[jj][ct]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        lds_barrier();
+        if (k + 1 < S && step_at(k + 1).full) lds_barrier();
+    }
+
+    float* out = a.part + (int64_t)L * kWgPart + tid;
 #pragma unroll
-                for (int jj = 0; jj < NTAP; ++jj) {
-                    const int tp = wave + 4 * jj;
-                    if (tp < KT) {
-                        const int kd = tp / (KS * KS), kh = (tp / KS) % KS, kw = tp % KS;
-                        const int sl = kd == 0 ? sl0 : (kd == 1 ? sl1 : sl2);
-                        F16B bv;
-                        bv.u = *reinterpret_cast<const uint4*>(
-                            xs + kw * KWS + li * CIS + (sl * PH + hl + kh) * 32 + wl * 2);
+    for (int j = 0; j < NTAP; ++j)
 #pragma unroll
-                        for (int ct = 0; ct < 4; ++ct) acc[jj][ct] = mfma(ac[ct], bv, acc[jj][ct]);
-                    }
+        for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) out[((j * 4 + ct) * 4 + e) * 256] = acc[j][ct][e];
+}
+
+// ---------------------------------------------------------------- band wgrad
+// Row-band weight gradient for narrow maps (W a multiple of 8, at most 56).
+// A step is one output depth plane d of a band of hb whole rows starting at
+// h0 (hb * W <= 192 voxels), flattened row-major into the GEMM K index, so
+// every staging load reads whole contiguous rows: the dy of a step is one
+// contiguous run of hb * W voxels per output channel and an input plane of
+// the band (rows h0 - 1 .. h0 + hb) one contiguous run per input channel.
+// Each input plane is kept in LDS as three kw-shifted copies (copy kw holds
+// x[h][w + kw - 1], zero where that column is outside the map), so the B
+// operand of tap (kd, kh, kw) at flattened voxel v is the aligned 16 bytes at
+// v + kh * W of copy kw.  The planes of the current step (d - 1, d, d + 1)
+// and the next (d + 2) live in a ring of four slots; steps run plane-fastest
+// along a band, so a step's producers stage one new plane and the dy of the
+// next step while the consumers multiply.  The first step of a range or band
+// stages three planes after the previous step is done.  Voxels past hb * W
+// in the last K step meet dy = 0 (the LDS is cleared at start).
+namespace {
+struct WbArgs {
+    const bf16* x;   // [N][Ci][D][H][W]
+    const bf16* dy;  // [N][Co][D][H][W]
+    float* part;     // [ranges][groups] blocks of kWgPart floats
+    int N, Ci, Co, D, H, W;
+    int hb, nb;      // rows per band, bands per plane
+    int nsteps;      // N * nb * D, plane fastest
+    int spr;         // steps per range
+    int cigs, cogs;  // input-channel groups of 16, output-channel groups of 64
+    int sls, cis;    // LDS bytes per plane slot and per input channel (4 slots + pad)
+    // ceil(2^20 / divisor) for W, the x groups XG = (hb + 2) W / 8 of one
+    // (channel, plane), 3 XG, and the dy groups YG = hb W / 8 of one channel:
+    // (i * m) >> 20 == i / divisor for every index the kernel divides
+    uint32_t mW, mXG, m3XG, mYG;
+};
+constexpr int kBandK = 192;                                  // voxels per step (6 K steps)
+constexpr int kBandSlotVox = 288;                            // bound on (hb + 2) * W
+constexpr int kBandCisMax = 4 * kBandSlotVox * 2 + 16;       // 2320
+constexpr int kBandDys = kBandK * 2 + 16;                    // bytes per output channel
+constexpr int kBandXBytes = 3 * 16 * kBandCisMax;            // three kw copies
+constexpr int kBandLds = kBandXBytes + 2 * 64 * kBandDys;    // 162560
+}  // namespace
+
+__global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
+    constexpr int KT = 27, NTAP = kWgNtap, NK = kBandK / 32;
+    constexpr int DYB = 64 * kBandDys;
+    __shared__ __align__(16) unsigned char lds[kBandLds];
+    unsigned char* const xs = lds;
+    unsigned char* const dys = lds + kBandXBytes;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const bool consumer = wave < 4;
+    for (int i = tid; i < kBandLds / 16; i += 512)
+        reinterpret_cast<uint4*>(lds)[i] = make_uint4(0u, 0u, 0u, 0u);
+    __syncthreads();
+
+    const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int groups = a.cigs * a.cogs;
+    const int cig = L % a.cigs;
+    const int cog = (L / a.cigs) % a.cogs;
+    const int range = L / groups;
+    const int ci0 = cig * 16, co0 = cog * 64;
+    const int s_beg = range * a.spr;
+    const int s_end = s_beg + a.spr < a.nsteps ? s_beg + a.spr : a.nsteps;
+    const int S = s_end > s_beg ? s_end - s_beg : 0;
+    const int HW = a.H * a.W;
+    const int64_t V = (int64_t)HW * a.D;
+    const int KWS = 16 * a.cis;
+
+    struct Step {
+        int n, d, h0;
+        bool full;  // first step of the range or of a band: three planes
+    };
+    auto step_at = [&](int k) __attribute__((always_inline)) {
+        const int sidx = s_beg + k;
+        Step t;
+        t.d = sidx % a.D;
+        const int r = sidx / a.D;
+        t.h0 = (r % a.nb) * a.hb;
+        t.n = r / a.nb;
+        t.full = k == 0 || t.d == 0;
+        return t;
+    };
+    auto slot_of = [](int z) { return (z + 4) & 3; };
+
+    if (!consumer) {
+        const int XG = (a.hb + 2) * a.W / 8;  // 8-voxel groups of one (channel, plane)
+        const int YG = a.hb * a.W / 8;        // 8-voxel groups of one output channel
+        auto qdiv = [](int i, uint32_t m) { return (int)(((uint32_t)i * m) >> 20); };
+        // The staging index arithmetic is redone at every use (the opaque copy
+        // of the thread index keeps it from being hoisted into registers).
+        auto ptid_now = [&]() __attribute__((always_inline)) {
+            int p = tid - 256;
+            asm volatile("" : "+v"(p));
+            return p;
+        };
+        // Staging loads are raw buffer loads over one sample's tensor; an
+        // offset past the end (padding, idle item) reads zeros, so no load
+        // sits behind a branch.
+        // x group: m[0] bits 16..31 = left neighbour, m[1..4] = 8 voxels,
+        // m[5] bits 0..15 = right neighbour (zero at the row ends)
+        auto ld_x = [&](const Step& t, bool live, int ci, int z, int gi, uint32_t* m)
+            __attribute__((always_inline)) {
+            // the step is wave-uniform; saying so keeps the resource in SGPRs
+            const int n = __builtin_amdgcn_readfirstlane(t.n);
+            const __amdgpu_buffer_rsrc_t xr =
+                buf_rsrc(a.x + (int64_t)n * a.Ci * V, (uint32_t)(a.Ci * V * 2));
+            const int u = 8 * gi, rr = qdiv(u, a.mW), col = u - rr * a.W;
+            const int h = t.h0 - 1 + rr;
+            const bool ok = live && (unsigned)z < (unsigned)a.D && (unsigned)h < (unsigned)a.H;
+            const uint32_t o = ok ? (uint32_t)((ci0 + ci) * (uint32_t)V + z * HW + h * a.W + col) * 2u
+                                  : 0x80000000u;
+            const uint4 v = buf_ld16(xr, o, 0);
+            m[1] = v.x; m[2] = v.y; m[3] = v.z; m[4] = v.w;
+            m[0] = buf_ld2(xr, ok && col > 0 ? o - 2u : 0x80000000u, 0) << 16;
+            m[5] = buf_ld2(xr, ok && col + 8 < a.W ? o + 16u : 0x80000000u, 0);
+        };
+        auto st_x = [&](int ci, int z, int gi, const uint32_t* m) __attribute__((always_inline)) {
+            unsigned char* base = xs + ci * a.cis + slot_of(z) * a.sls + gi * 16;
+            uint32_t s0[4], s2[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                s0[i] = __builtin_amdgcn_alignbit(m[i + 1], m[i], 16);
+                s2[i] = __builtin_amdgcn_alignbit(m[i + 2], m[i + 1], 16);
+            }
+            *reinterpret_cast<uint4*>(base) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
+            *reinterpret_cast<uint4*>(base + KWS) = make_uint4(m[1], m[2], m[3], m[4]);
+            *reinterpret_cast<uint4*>(base + 2 * KWS) = make_uint4(s2[0], s2[1], s2[2], s2[3]);
+        };
+        auto ld_dy = [&](const Step& t, bool live, int co, int gi) __attribute__((always_inline)) {
+            const int n = __builtin_amdgcn_readfirstlane(t.n);
+            const __amdgpu_buffer_rsrc_t yr =
+                buf_rsrc(a.dy + (int64_t)n * a.Co * V, (uint32_t)(a.Co * V * 2));
+            const int u = 8 * gi, rr = qdiv(u, a.mW), col = u - rr * a.W;
+            const int h = t.h0 + rr;
+            const uint32_t o =
+                live && h < a.H
+                    ? (uint32_t)((co0 + co) * (uint32_t)V + t.d * HW + h * a.W + col) * 2u
+                    : 0x80000000u;
+            return buf_ld16(yr, o, 0);
+        };
+        constexpr int NXN = (16 * (kBandSlotVox / 8) + 255) / 256;  // x groups per thread, one plane
+        constexpr int NDY = 64 * (kBandK / 8) / 256;                // dy groups per thread
+        struct Regs {
+            uint32_t m[NXN][6];
+            uint4 dy[NDY];
+        };
+        // one new plane (d + 1 of step t) and the dy of step t, into registers
+        auto load = [&](const Step& t, Regs& R) __attribute__((always_inline)) {
+            const int pt = ptid_now();
+#pragma unroll
+            for (int q = 0; q < NXN; ++q) {
+                const int it = pt + 256 * q, ci = qdiv(it, a.mXG);
+                ld_x(t, it < 16 * XG, ci, t.d + 1, it - ci * XG, R.m[q]);
+            }
+#pragma unroll
+            for (int q = 0; q < NDY; ++q) {
+                const int it = pt + 256 * q, co = qdiv(it, a.mYG);
+                R.dy[q] = ld_dy(t, it < 64 * YG, co, it - co * YG);
+            }
+        };
+        auto commit = [&](const Step& t, const Regs& R, unsigned char* db) __attribute__((always_inline)) {
+            const int pt = ptid_now();
+#pragma unroll
+            for (int q = 0; q < NXN; ++q) {
+                const int it = pt + 256 * q, ci = qdiv(it, a.mXG);
+                if (it < 16 * XG) st_x(ci, t.d + 1, it - ci * XG, R.m[q]);
+            }
+#pragma unroll
+            for (int q = 0; q < NDY; ++q) {
+                const int it = pt + 256 * q, co = qdiv(it, a.mYG);
+                if (it < 64 * YG)
+                    *reinterpret_cast<uint4*>(db + co * kBandDys + (it - co * YG) * 16) = R.dy[q];
+            }
+        };
+        // first step of a range or band: planes d - 1 .. d + 1 and dy, synchronously
+        auto stage_full = [&](const Step& t, unsigned char* db) __attribute__((always_inline)) {
+            const int nx = 16 * 3 * XG;
+#pragma unroll 1
+            for (int it0 = ptid_now(); it0 < nx; it0 += 4 * 256) {
+                uint32_t m[4][6];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int it = it0 + 256 * i, ci = qdiv(it, a.m3XG);
+                    const int rem = it - ci * 3 * XG, pl = qdiv(rem, a.mXG);
+                    ld_x(t, it < nx, ci, t.d - 1 + pl, rem - pl * XG, m[i]);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int it = it0 + 256 * i, ci = qdiv(it, a.m3XG);
+                    const int rem = it - ci * 3 * XG, pl = qdiv(rem, a.mXG);
+                    if (it < nx) st_x(ci, t.d - 1 + pl, rem - pl * XG, m[i]);
                 }
             }
+            const int pt = ptid_now();
+            uint4 yv[NDY];
+#pragma unroll
+            for (int q = 0; q < NDY; ++q) {
+                const int it = pt + 256 * q, co = qdiv(it, a.mYG);
+                yv[q] = ld_dy(t, it < 64 * YG, co, it - co * YG);
+            }
+#pragma unroll
+            for (int q = 0; q < NDY; ++q) {
+                const int it = pt + 256 * q, co = qdiv(it, a.mYG);
+                if (it < 64 * YG)
+                    *reinterpret_cast<uint4*>(db + co * kBandDys + (it - co * YG) * 16) = yv[q];
+            }
+        };
+
+        // Barrier schedule (both roles): one prologue barrier, then per step
+        // one barrier, plus one more before a step that restages three planes.
+        // Three register sets: the loads of step k + 3 are issued during step
+        // k and written to LDS during step k + 2.
+        Regs R0, R1, R2;
+        if (S > 0) {
+            stage_full(step_at(0), dys);
+            if (S > 1 && !step_at(1).full) load(step_at(1), R1);
+            if (S > 2 && !step_at(2).full) load(step_at(2), R2);
+        }
+        lds_barrier();
+        // Rc holds step k + 1 unless that step restages; Rl takes step k + 3
+        auto body = [&](int k, Regs& Rc, Regs& Rl) __attribute__((always_inline)) {
+            if (k + 1 < S) {
+                const Step tn = step_at(k + 1);
+                unsigned char* db = dys + ((k + 1) & 1) * DYB;
+                if (!tn.full) commit(tn, Rc, db);
+                if (k + 3 < S) {
+                    const Step tf = step_at(k + 3);
+                    if (!tf.full) load(tf, Rl);
+                }
+                lds_barrier();
+                if (tn.full) {
+                    stage_full(tn, db);
+                    lds_barrier();
+                }
+            } else {
+                lds_barrier();
+            }
+        };
+        for (int k = 0; k < S; k += 3) {
+            body(k, R1, R0);
+            if (k + 1 < S) body(k + 1, R2, R1);
+            if (k + 2 < S) body(k + 2, R0, R2);
+        }
+        return;
+    }
+
+    // ---- consumer: wave w owns taps w, w + 4, ...; lane (li, kg) holds
+    // voxels 32 s + 8 kg .. + 7 of output channel / input channel li
+    const int li = lane & 15, kg = lane >> 4;
+    f32x4 acc[NTAP][4];
+#pragma unroll
+    for (int j = 0; j < NTAP; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[j][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    lds_barrier();
+    for (int k = 0; k < S; ++k) {
+        const Step t = step_at(k);
+        const unsigned char* abase = dys + (k & 1) * DYB + li * kBandDys + kg * 16;
+        int boff[NTAP];
+#pragma unroll
+        for (int jj = 0; jj < NTAP; ++jj) {
+            int tp = wave + 4 * jj;
+            tp = tp < KT ? tp : KT - 1;  // wave 3's seventh slot repeats tap 26, never read
+            const int kd = tp / 9, kh = (tp / 3) % 3, kw = tp % 3;
+            boff[jj] = kw * KWS + li * a.cis + slot_of(t.d - 1 + kd) * a.sls +
+                       (kg * 8 + kh * a.W) * 2;
+        }
+        constexpr int G = NK * NTAP;
+        constexpr int LA = 3;
+        F16B A[2][4], B[4];
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct)
+            A[0][ct].u = *reinterpret_cast<const uint4*>(abase + ct * 16 * kBandDys);
+#pragma unroll
+        for (int g = 0; g < LA; ++g)
+            B[g].u = *reinterpret_cast<const uint4*>(xs + boff[g % NTAP] + (g / NTAP) * 64);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int s_ = g / NTAP, jj = g % NTAP;
+            if (g + LA < G) {
+                const int gn = g + LA;
+                B[gn % 4].u =
+                    *reinterpret_cast<const uint4*>(xs + boff[gn % NTAP] + (gn / NTAP) * 64);
+            }
+            if (jj == 3 && s_ + 1 < NK) {
+#pragma unroll
+                for (int ct = 0; ct < 4; ++ct)
+                    A[(s_ + 1) & 1][ct].u = *reinterpret_cast<const uint4*>(
+                        abase + ct * 16 * kBandDys + (s_ + 1) * 64);
+            }
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct)
+                acc[jj][ct] = mfma(A[s_ & 1][ct], B[g % 4], acc[jj][ct]);
+            __builtin_amdgcn_sched_barrier(0);
         }
         lds_barrier();
         if (k + 1 < S && step_at(k + 1).full) lds_barrier();
@@ -935,7 +1262,21 @@ bool brick_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) {
 
 size_t brick_fd_ws(const ConvGeom& g) { return (size_t)g.Co * g.Ci * g.k * g.k * g.k * 2; }
 
+// Row bands take maps up to 56 columns wide: hb rows with hb * W <= 192 and
+// (hb + 2) * W <= 288 (the LDS slot bound).
+static int band_rows(const ConvGeom& g) {
+    // staging addresses one sample's tensor with 32-bit byte offsets
+    const int64_t v2 = (int64_t)g.D * g.H * g.W * 2;
+    if (g.W > 56 || (int64_t)g.Ci * v2 >= ((int64_t)1 << 31) ||
+        (int64_t)g.Co * v2 >= ((int64_t)1 << 31))
+        return 0;
+    const int a = kBandK / g.W, b = kBandSlotVox / g.W - 2;
+    return a < b ? a : b;
+}
+
 static int64_t wgrad_steps(const ConvGeom& g) {
+    const int hb = band_rows(g);
+    if (hb > 0) return (int64_t)g.N * ceil_div(g.H, hb) * g.D;
     return (int64_t)g.N * ceil_div(g.H, kWH) * ceil_div(g.W, kWW) * ceil_div(g.D, 2);
 }
 
@@ -1017,36 +1358,68 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
 
 rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, float* dw,
                               int accumulate, void* ws, hipStream_t st) {
-    WgArgs a;
-    a.x = (const bf16*)x;
-    a.dy = (const bf16*)dy;
-    a.part = (float*)ws;
-    a.N = g.N;
-    a.Ci = g.Ci;
-    a.Co = g.Co;
-    a.D = g.D;
-    a.H = g.H;
-    a.W = g.W;
-    a.tds = (int)ceil_div(g.D, 2);
-    a.th = (int)ceil_div(g.H, kWH);
-    a.tw = (int)ceil_div(g.W, kWW);
-    a.nsteps = (int)wgrad_steps(g);
+    const int64_t nsteps = wgrad_steps(g);
     const int R = wgrad_ranges(g);
-    a.spr = (int)ceil_div(a.nsteps, R);
-    const int Rreal = (int)ceil_div(a.nsteps, a.spr);
-    a.cigs = g.Ci / 16;
-    a.cogs = g.Co / 64;
-    {
+    const int spr = (int)ceil_div(nsteps, R);
+    const int Rreal = (int)ceil_div(nsteps, spr);
+    const int cigs = g.Ci / 16, cogs = g.Co / 64;
+    const int hb = band_rows(g);
+    if (hb > 0) {
+        WbArgs a;
+        a.x = (const bf16*)x;
+        a.dy = (const bf16*)dy;
+        a.part = (float*)ws;
+        a.N = g.N;
+        a.Ci = g.Ci;
+        a.Co = g.Co;
+        a.D = g.D;
+        a.H = g.H;
+        a.W = g.W;
+        a.hb = hb;
+        a.nb = (int)ceil_div(g.H, hb);
+        a.nsteps = (int)nsteps;
+        a.spr = spr;
+        a.cigs = cigs;
+        a.cogs = cogs;
+        a.sls = (hb + 2) * g.W * 2;
+        a.cis = ((4 * a.sls + 127) & ~127) + 16;  // 16 input channels on distinct banks
+        const int XG = (hb + 2) * g.W / 8, YG = hb * g.W / 8;
+        auto magic = [](int d) { return (uint32_t)(((1u << 20) + d - 1) / d); };
+        a.mW = magic(g.W);
+        a.mXG = magic(XG);
+        a.m3XG = magic(3 * XG);
+        a.mYG = magic(YG);
         ProfScope ps("conv_brick3_wgrad", st, conv_flops(g), conv_bytes(g, 2));
-        conv_brick_wgrad<3><<<(unsigned)((int64_t)Rreal * a.cigs * a.cogs), 512, 0, st>>>(a);
+        conv_band_wgrad<<<(unsigned)((int64_t)Rreal * cigs * cogs), 512, 0, st>>>(a);
+        RAT3D_LAUNCH_CHECK();
+    } else {
+        WgArgs a;
+        a.x = (const bf16*)x;
+        a.dy = (const bf16*)dy;
+        a.part = (float*)ws;
+        a.N = g.N;
+        a.Ci = g.Ci;
+        a.Co = g.Co;
+        a.D = g.D;
+        a.H = g.H;
+        a.W = g.W;
+        a.tds = (int)ceil_div(g.D, 2);
+        a.th = (int)ceil_div(g.H, kWH);
+        a.tw = (int)ceil_div(g.W, kWW);
+        a.nsteps = (int)nsteps;
+        a.spr = spr;
+        a.cigs = cigs;
+        a.cogs = cogs;
+        ProfScope ps("conv_brick3_wgrad", st, conv_flops(g), conv_bytes(g, 2));
+        conv_brick_wgrad<3><<<(unsigned)((int64_t)Rreal * cigs * cogs), 512, 0, st>>>(a);
         RAT3D_LAUNCH_CHECK();
     }
-    const int groups = a.cigs * a.cogs;
+    const int groups = cigs * cogs;
     const int64_t count = (int64_t)groups * kWgPart;
     ProfScope ps("wgrad_reduce", st, 0.0,
                  4.0 * (count * Rreal + (double)g.Co * g.Ci * 27 * (1 + accumulate)));
     wgrad_brick_reduce<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(
-        a.part, Rreal, groups, a.cigs, g.Ci, dw, accumulate);
+        (const float*)ws, Rreal, groups, cigs, g.Ci, dw, accumulate);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }

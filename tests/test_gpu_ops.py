@@ -30,7 +30,7 @@ CONV_CASES = [
     (3, 5, 70, 5, 3, 4, 3, 1, 1, True, "bf16"),
     (2, 128, 256, 6, 7, 6, 3, 2, 1, False, "bf16"),
     # LDS-brick paths: full and ragged tiles, 32- and 64-channel output tiles,
-    # 1^3 kernels, weight-gradient bricks (W multiple of 8)
+    # 1^3 kernels, weight-gradient row bands (W multiple of 8)
     (2, 64, 64, 6, 10, 32, 3, 1, 1, False, "bf16"),
     (1, 32, 64, 5, 9, 24, 3, 1, 1, False, "bf16"),
     (2, 64, 32, 4, 8, 16, 3, 1, 1, False, "bf16"),
@@ -38,7 +38,14 @@ CONV_CASES = [
     (2, 64, 64, 5, 9, 24, 1, 1, 0, True, "bf16"),
     (1, 32, 64, 3, 3, 8, 1, 1, 0, False, "bf16"),
     (1, 96, 64, 9, 17, 48, 3, 1, 1, False, "bf16"),
-    # weight-gradient bricks on widths divisible by 4 but not 8 (ragged last tile)
+    # weight gradient over row bands (W a multiple of 8, at most 56): the widest
+    # band, one-row-per-group widths, a single plane, ragged last bands
+    (1, 32, 64, 4, 5, 56, 3, 1, 1, False, "bf16"),
+    (2, 16, 64, 5, 20, 8, 3, 1, 1, False, "bf16"),
+    (1, 64, 64, 1, 12, 16, 3, 1, 1, False, "bf16"),
+    # weight-gradient bricks on maps wider than a band
+    (1, 64, 64, 3, 9, 64, 3, 1, 1, False, "bf16"),
+    # weight-gradient gather on widths divisible by 4 but not 8
     (1, 64, 64, 5, 6, 20, 3, 1, 1, False, "bf16"),
     # the small deep-stage volumes of the full network (tiles mostly outside)
     (2, 64, 64, 12, 14, 12, 1, 1, 0, False, "bf16"),
