@@ -93,11 +93,13 @@ __global__ void prep_dgrad_weights(const bf16* __restrict__ w, int Co, int Ci, i
 // LDS brick layout: voxel v = (dd * PH + hh) * PW + ww holds 64 bytes, four
 // 16-byte slots of eight channels; channel group cg sits in slot
 // cg ^ ((ww >> 1) & 3).  The swizzle depends on the brick column only, so the
-// eight rows a wave reads for one tap differ by constant offsets, and the 16
-// lanes of an MFMA row group (16 consecutive columns) hit distinct banks.
+// eight rows a wave reads for one tap differ by constant offsets, and any
+// eight consecutive columns (64 bytes apart) get distinct (column parity,
+// slot) pairs: distinct 16-byte bank groups of a 128-byte bank row.
+__device__ __forceinline__ int brick_swizzle(int ww) { return (ww >> 1) & 3; }
 template <int KS>
 __device__ __forceinline__ uint32_t brick_slot_off(int ww, int cg) {
-    return (uint32_t)(ww * 64 + ((cg ^ ((ww >> 1) & 3)) << 4));
+    return (uint32_t)(ww * 64 + ((cg ^ brick_swizzle(ww)) << 4));
 }
 
 __device__ __forceinline__ uint32_t pack_lo(uint32_t lo, uint32_t hi) {
@@ -304,7 +306,8 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         constexpr int NG = KT * NR;
         const uint32_t wchunk =
             ((uint32_t)(c0 >> 5) * KT * (uint32_t)a.Ct + T.co0 + wc * CT * 16) * 64u;
-        F16B A[LA], B[2][CT];
+        constexpr int LB = ACC ? 1 : 2;  // weight taps loaded ahead of the current one
+        F16B A[LA], B[LB + 1][CT];
         auto a_ptr = [&](int g) {
             const int tap = g / NR, r = g % NR;
             const int kd = tap / (KS * KS), kh = (tap / KS) % KS, kw = tap % KS;
@@ -317,22 +320,23 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         };
 #pragma unroll
         for (int g = 0; g < LA; ++g) A[g].u = *reinterpret_cast<const uint4*>(a_ptr(g));
-        load_b(0, B[0]);
+#pragma unroll
+        for (int tap = 0; tap < LB && tap < KT; ++tap) load_b(tap, B[tap]);
 #pragma unroll
         for (int tap = 0; tap < KT; ++tap) {
-            if (tap + 1 < KT) load_b(tap + 1, B[(tap + 1) & 1]);
+            if (tap + LB < KT) load_b(tap + LB, B[(tap + LB) % (LB + 1)]);
 #pragma unroll
             for (int r = 0; r < NR; ++r) {
                 const int g = tap * NR + r;
 #pragma unroll
                 for (int ct = 0; ct < CT; ++ct)
-                    acc[r][ct] = mfma(A[g % LA], B[tap & 1][ct], acc[r][ct]);
+                    acc[r][ct] = mfma(A[g % LA], B[tap % (LB + 1)][ct], acc[r][ct]);
                 if (g + LA < NG) A[g % LA].u = *reinterpret_cast<const uint4*>(a_ptr(g + LA));
             }
             // issue order within a tap: the next tap's weight loads, then per
             // row its MFMAs followed by the ring refill; nothing moves across
             // taps (register pressure)
-            if (tap + 1 < KT) {
+            if (tap + LB < KT) {
                 __builtin_amdgcn_sched_group_barrier(0x020, CT, 0);
 #pragma unroll
                 for (int r = 0; r < NR; ++r) {
@@ -389,7 +393,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             const int i = lane_u + ((r / kBH) * kBH + r % kBH) * 2;
             const int row = i / PW, ww = i - row * PW;
             unsigned char* base = buf + (uint32_t)(row * PW + ww) * 64u + (kg & 1) * 8;
-            const int sk = (ww >> 1) & 3;
+            const int sk = brick_swizzle(ww);
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
                 *reinterpret_cast<uint2*>(base + (((wc * CT + ct) ^ sk) << 4)) = make_uint2(
