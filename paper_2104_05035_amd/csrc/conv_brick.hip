@@ -918,16 +918,17 @@ __global__ __launch_bounds__(512, 1) void conv_brick_wgrad(WgArgs a) {
 }
 
 // ---------------------------------------------------------------- band wgrad
-// Row-band weight gradient for narrow maps (W a multiple of 8, at most 56).
+// Row-band weight gradient for narrow maps (W a multiple of 4, at most 56).
 // A step is one output depth plane d of a band of hb whole rows starting at
-// h0 (hb * W <= 192 voxels), flattened row-major into the GEMM K index, so
+// h0, flattened row-major with a row pitch Wp = W rounded up to 8 into the
+// GEMM K index (hb * Wp <= NK * 32; pad columns hold dy = 0), so
 // every staging load reads whole contiguous rows: the dy of a step is one
 // contiguous run of hb * W voxels per output channel and an input plane of
 // the band (rows h0 - 1 .. h0 + hb) one contiguous run per input channel.
 // Each input plane is kept in LDS as three kw-shifted copies (copy kw holds
 // x[h][w + kw - 1], zero where that column is outside the map), so the B
 // operand of tap (kd, kh, kw) at flattened voxel v is the aligned 16 bytes at
-// v + kh * W of copy kw.  The planes of the current step (d - 1, d, d + 1)
+// v + kh * Wp of copy kw.  The planes of the current step (d - 1, d, d + 1)
 // and the next (d + 2) live in a ring of four slots; steps run plane-fastest
 // along a band, so a step's producers stage one new plane and the dy of the
 // next step while the consumers multiply.  The first step of a range or band
@@ -939,17 +940,17 @@ struct WbArgs {
     const bf16* dy;  // [N][Co][D][H][W]
     float* part;     // [ranges][groups] blocks of kWgPart floats
     int N, Ci, Co, D, H, W;
-    int hb, nb;      // rows per band, bands per plane
+    int Wp, hb, nb;  // LDS row pitch (W rounded up to 8), rows per band, bands per plane
     int nsteps;      // N * nb * D, plane fastest
     int spr;         // steps per range
     int cigs, cogs;  // input-channel groups of 16, output-channel groups of 64
     int sls, cis;    // LDS bytes per plane slot and per input channel (4 slots + pad)
-    // ceil(2^20 / divisor) for W, the x groups XG = (hb + 2) W / 8 of one
-    // (channel, plane), 3 XG, and the dy groups YG = hb W / 8 of one channel:
+    // ceil(2^20 / divisor) for Wp, the x groups XG = (hb + 2) Wp / 8 of one
+    // (channel, plane), 3 XG, and the dy groups YG = hb Wp / 8 of one channel:
     // (i * m) >> 20 == i / divisor for every index the kernel divides
-    uint32_t mW, mXG, m3XG, mYG;
+    uint32_t mWp, mXG, m3XG, mYG;
 };
-constexpr int kBandK = 192;                                  // voxels per step (6 K steps)
+constexpr int kBandK = 192;                                  // voxels per step, at most
 constexpr int kBandSlotVox = 288;                            // bound on (hb + 2) * W
 constexpr int kBandCisMax = 4 * kBandSlotVox * 2 + 16;       // 2320
 constexpr int kBandDys = kBandK * 2 + 16;                    // bytes per output channel
@@ -957,8 +958,10 @@ constexpr int kBandXBytes = 3 * 16 * kBandCisMax;            // three kw copies
 constexpr int kBandLds = kBandXBytes + 2 * 64 * kBandDys;    // 162560
 }  // namespace
 
+template <int NK, bool PART>
 __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
-    constexpr int KT = 27, NTAP = kWgNtap, NK = kBandK / 32;
+    constexpr int KT = 27, NTAP = kWgNtap;
+    static_assert(NK * 32 <= kBandK, "K steps per band");
     constexpr int DYB = 64 * kBandDys;
     __shared__ __align__(16) unsigned char lds[kBandLds];
     unsigned char* const xs = lds;
@@ -999,8 +1002,9 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
     auto slot_of = [](int z) { return (z + 4) & 3; };
 
     if (!consumer) {
-        const int XG = (a.hb + 2) * a.W / 8;  // 8-voxel groups of one (channel, plane)
-        const int YG = a.hb * a.W / 8;        // 8-voxel groups of one output channel
+        const int XG = (a.hb + 2) * a.Wp / 8;  // 8-voxel groups of one (channel, plane)
+        const int YG = a.hb * a.Wp / 8;        // 8-voxel groups of one output channel
+        // PART (W % 8 == 4): the last group of a row holds four voxels (8-byte load)
         auto qdiv = [](int i, uint32_t m) { return (int)(((uint32_t)i * m) >> 20); };
         // The staging index arithmetic is redone at every use (the opaque copy
         // of the thread index keeps it from being hoisted into registers).
@@ -1013,20 +1017,27 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
         // offset past the end (padding, idle item) reads zeros, so no load
         // sits behind a branch.
         // x group: m[0] bits 16..31 = left neighbour, m[1..4] = 8 voxels,
-        // m[5] bits 0..15 = right neighbour (zero at the row ends)
+        // m[5] bits 0..15 = right neighbour (zero at the row ends and past W)
         auto ld_x = [&](const Step& t, bool live, int ci, int z, int gi, uint32_t* m)
             __attribute__((always_inline)) {
             // the step is wave-uniform; saying so keeps the resource in SGPRs
             const int n = __builtin_amdgcn_readfirstlane(t.n);
             const __amdgpu_buffer_rsrc_t xr =
                 buf_rsrc(a.x + (int64_t)n * a.Ci * V, (uint32_t)(a.Ci * V * 2));
-            const int u = 8 * gi, rr = qdiv(u, a.mW), col = u - rr * a.W;
+            const int u = 8 * gi, rr = qdiv(u, a.mWp), col = u - rr * a.Wp;
             const int h = t.h0 - 1 + rr;
             const bool ok = live && (unsigned)z < (unsigned)a.D && (unsigned)h < (unsigned)a.H;
             const uint32_t o = ok ? (uint32_t)((ci0 + ci) * (uint32_t)V + z * HW + h * a.W + col) * 2u
                                   : 0x80000000u;
-            const uint4 v = buf_ld16(xr, o, 0);
-            m[1] = v.x; m[2] = v.y; m[3] = v.z; m[4] = v.w;
+            if constexpr (PART) {
+                const bool full = col + 8 <= a.W;
+                const uint4 v = buf_ld16(xr, full ? o : 0x80000000u, 0);
+                const uint2 w = buf_ld8(xr, full ? 0x80000000u : o, 0);
+                m[1] = v.x | w.x; m[2] = v.y | w.y; m[3] = v.z; m[4] = v.w;
+            } else {
+                const uint4 v = buf_ld16(xr, o, 0);
+                m[1] = v.x; m[2] = v.y; m[3] = v.z; m[4] = v.w;
+            }
             m[0] = buf_ld2(xr, ok && col > 0 ? o - 2u : 0x80000000u, 0) << 16;
             m[5] = buf_ld2(xr, ok && col + 8 < a.W ? o + 16u : 0x80000000u, 0);
         };
@@ -1046,12 +1057,20 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
             const int n = __builtin_amdgcn_readfirstlane(t.n);
             const __amdgpu_buffer_rsrc_t yr =
                 buf_rsrc(a.dy + (int64_t)n * a.Co * V, (uint32_t)(a.Co * V * 2));
-            const int u = 8 * gi, rr = qdiv(u, a.mW), col = u - rr * a.W;
+            const int u = 8 * gi, rr = qdiv(u, a.mWp), col = u - rr * a.Wp;
             const int h = t.h0 + rr;
             const uint32_t o =
                 live && h < a.H
                     ? (uint32_t)((co0 + co) * (uint32_t)V + t.d * HW + h * a.W + col) * 2u
                     : 0x80000000u;
+            if constexpr (PART) {
+                const bool full = col + 8 <= a.W;
+                uint4 v = buf_ld16(yr, full ? o : 0x80000000u, 0);
+                const uint2 w = buf_ld8(yr, full ? 0x80000000u : o, 0);
+                v.x |= w.x;
+                v.y |= w.y;
+                return v;
+            }
             return buf_ld16(yr, o, 0);
         };
         constexpr int NXN = (16 * (kBandSlotVox / 8) + 255) / 256;  // x groups per thread, one plane
@@ -1180,7 +1199,7 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
             tp = tp < KT ? tp : KT - 1;  // wave 3's seventh slot repeats tap 26, never read
             const int kd = tp / 9, kh = (tp / 3) % 3, kw = tp % 3;
             boff[jj] = kw * KWS + li * a.cis + slot_of(t.d - 1 + kd) * a.sls +
-                       (kg * 8 + kh * a.W) * 2;
+                       (kg * 8 + kh * a.Wp) * 2;
         }
         constexpr int G = NK * NTAP;
         constexpr int LA = 3;
@@ -1259,27 +1278,45 @@ bool brick_fd_ok(const ConvGeom& g, rat3d_dtype dt, bool dgrad) {
     return cs % 32 == 0 && ct % 32 == 0 && src_bytes < ((int64_t)1 << 31);
 }
 
+// Row bands take maps up to 56 columns wide (W a multiple of 4): hb rows of
+// pitch Wp with hb * Wp <= NK * 32 and (hb + 2) * Wp <= 288 (the LDS slot
+// bound); NK in {6, 4} is picked for the fewest K steps per plane.
+struct BandCfg {
+    int hb = 0, nk = 0, Wp = 0;
+};
+static BandCfg band_cfg(const ConvGeom& g) {
+    BandCfg c;
+    const int Wp = (g.W + 7) & ~7;
+    // staging addresses one sample's tensor with 32-bit byte offsets
+    const int64_t v2 = (int64_t)g.D * g.H * g.W * 2;
+    if (g.W % 4 != 0 || Wp > 56 || (int64_t)g.Ci * v2 >= ((int64_t)1 << 31) ||
+        (int64_t)g.Co * v2 >= ((int64_t)1 << 31))
+        return c;
+    int64_t best = -1;
+    for (int nk : {6, 4}) {
+        const int a = nk * 32 / Wp, b = kBandSlotVox / Wp - 2;
+        const int hb = a < b ? a : b;
+        if (hb < 1) continue;
+        const int64_t cost = ceil_div(g.H, hb) * nk;
+        if (best < 0 || cost < best) {
+            best = cost;
+            c.hb = hb;
+            c.nk = nk;
+            c.Wp = Wp;
+        }
+    }
+    return c;
+}
+
 bool brick_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) {
     return dt == RAT3D_BF16 && g.s == 1 && g.k == 3 && g.p == 1 && g.Ci % 16 == 0 &&
-           g.Co % 64 == 0 && g.W % 8 == 0;
+           g.Co % 64 == 0 && (g.W % 8 == 0 || band_cfg(g).hb > 0);
 }
 
 size_t brick_fd_ws(const ConvGeom& g) { return (size_t)g.Co * g.Ci * g.k * g.k * g.k * 2; }
 
-// Row bands take maps up to 56 columns wide: hb rows with hb * W <= 192 and
-// (hb + 2) * W <= 288 (the LDS slot bound).
-static int band_rows(const ConvGeom& g) {
-    // staging addresses one sample's tensor with 32-bit byte offsets
-    const int64_t v2 = (int64_t)g.D * g.H * g.W * 2;
-    if (g.W > 56 || (int64_t)g.Ci * v2 >= ((int64_t)1 << 31) ||
-        (int64_t)g.Co * v2 >= ((int64_t)1 << 31))
-        return 0;
-    const int a = kBandK / g.W, b = kBandSlotVox / g.W - 2;
-    return a < b ? a : b;
-}
-
 static int64_t wgrad_steps(const ConvGeom& g) {
-    const int hb = band_rows(g);
+    const int hb = band_cfg(g).hb;
     if (hb > 0) return (int64_t)g.N * ceil_div(g.H, hb) * g.D;
     return (int64_t)g.N * ceil_div(g.H, kWH) * ceil_div(g.W, kWW) * ceil_div(g.D, 2);
 }
@@ -1367,7 +1404,8 @@ rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, 
     const int spr = (int)ceil_div(nsteps, R);
     const int Rreal = (int)ceil_div(nsteps, spr);
     const int cigs = g.Ci / 16, cogs = g.Co / 64;
-    const int hb = band_rows(g);
+    const BandCfg bc = band_cfg(g);
+    const int hb = bc.hb;
     if (hb > 0) {
         WbArgs a;
         a.x = (const bf16*)x;
@@ -1379,22 +1417,31 @@ rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, 
         a.D = g.D;
         a.H = g.H;
         a.W = g.W;
+        a.Wp = bc.Wp;
         a.hb = hb;
         a.nb = (int)ceil_div(g.H, hb);
         a.nsteps = (int)nsteps;
         a.spr = spr;
         a.cigs = cigs;
         a.cogs = cogs;
-        a.sls = (hb + 2) * g.W * 2;
+        a.sls = (hb + 2) * bc.Wp * 2;
         a.cis = ((4 * a.sls + 127) & ~127) + 16;  // 16 input channels on distinct banks
-        const int XG = (hb + 2) * g.W / 8, YG = hb * g.W / 8;
+        const int XG = (hb + 2) * bc.Wp / 8, YG = hb * bc.Wp / 8;
         auto magic = [](int d) { return (uint32_t)(((1u << 20) + d - 1) / d); };
-        a.mW = magic(g.W);
+        a.mWp = magic(bc.Wp);
         a.mXG = magic(XG);
         a.m3XG = magic(3 * XG);
         a.mYG = magic(YG);
         ProfScope ps("conv_brick3_wgrad", st, conv_flops(g), conv_bytes(g, 2));
-        conv_band_wgrad<<<(unsigned)((int64_t)Rreal * cigs * cogs), 512, 0, st>>>(a);
+        const unsigned grid = (unsigned)((int64_t)Rreal * cigs * cogs);
+        const bool part = (g.W & 7) != 0;
+        if (bc.nk == 6) {
+            if (part) conv_band_wgrad<6, true><<<grid, 512, 0, st>>>(a);
+            else conv_band_wgrad<6, false><<<grid, 512, 0, st>>>(a);
+        } else {
+            if (part) conv_band_wgrad<4, true><<<grid, 512, 0, st>>>(a);
+            else conv_band_wgrad<4, false><<<grid, 512, 0, st>>>(a);
+        }
         RAT3D_LAUNCH_CHECK();
     } else {
         WgArgs a;

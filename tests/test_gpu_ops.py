@@ -45,8 +45,10 @@ CONV_CASES = [
     (1, 64, 64, 1, 12, 16, 3, 1, 1, False, "bf16"),
     # weight-gradient bricks on maps wider than a band
     (1, 64, 64, 3, 9, 64, 3, 1, 1, False, "bf16"),
-    # weight-gradient gather on widths divisible by 4 but not 8
+    # row bands on widths divisible by 4 but not 8 (half-filled last group of a row)
     (1, 64, 64, 5, 6, 20, 3, 1, 1, False, "bf16"),
+    (1, 16, 64, 3, 9, 4, 3, 1, 1, False, "bf16"),
+    (1, 32, 64, 3, 7, 52, 3, 1, 1, False, "bf16"),
     # the small deep-stage volumes of the full network (tiles mostly outside)
     (2, 64, 64, 12, 14, 12, 1, 1, 0, False, "bf16"),
     (2, 128, 128, 6, 7, 6, 3, 1, 1, False, "bf16"),
