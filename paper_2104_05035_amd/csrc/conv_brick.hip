@@ -30,6 +30,8 @@
 // Grid mapping is XCD-aware: consecutive workgroup ids are dealt round-robin
 // to the 8 XCDs, so ids are remapped to give each XCD a contiguous range of
 // tiles (neighbouring bricks share halo lines in that XCD's L2).
+#include <cstdio>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "prof.hpp"
@@ -122,7 +124,7 @@ __device__ __forceinline__ void lds_barrier() {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int KS, int NT, int RD, bool ACC>
+template <int KS, int NT, int RD, bool ACC, bool DG>
 __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     constexpr int P = (KS - 1) / 2;
     constexpr int PD = kBD + KS - 1, PH = kBH + KS - 1, PW = kBW + KS - 1;
@@ -366,7 +368,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         float bv[CT];
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct)
-            bv[ct] = a.bias ? a.bias[T.co0 + (wc * CT + ct) * 16 + li] : 0.f;
+            bv[ct] = !DG && a.bias ? a.bias[T.co0 + (wc * CT + ct) * 16 + li] : 0.f;
         if constexpr (KS == 1) {
             // separate region: unit (co, d, h, half) at co * OCS + ((d * 8 + h) * 2 + half) * 16
             unsigned char* ob = lds + 2 * BB;
@@ -454,7 +456,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         float bv[CT];
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct)
-            bv[ct] = a.bias ? a.bias[T.co0 + (wc * CT + ct) * 16 + li] : 0.f;
+            bv[ct] = !DG && a.bias ? a.bias[T.co0 + (wc * CT + ct) * 16 + li] : 0.f;
         int ib = ((li & 7) * kBD + wd * RD) * kBH * 4 + kg;
         asm volatile("" : "+v"(ib));
 #pragma unroll
@@ -536,7 +538,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct) {
                 const int co = T.co0 + (wc * CT + ct) * 16 + li;
-                const float bv = a.bias ? a.bias[co] : 0.f;
+                const float bv = !DG && a.bias ? a.bias[co] : 0.f;
                 const int w = T.w0 + 4 * kg;
                 bf16* q = a.dst + ((int64_t)T.n * a.Ct + co) * V + (int64_t)d * HW +
                           (int64_t)h * a.W + w;
@@ -1372,27 +1374,37 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
     a.ntiles = (int)((int64_t)g.N * a.td * a.th * a.tw * a.cogs);
     // one persistent workgroup per CU (fewer when there are fewer tiles)
     const int grid = a.ntiles < device_cus() ? a.ntiles : device_cus();
-    ProfScope ps(dgrad ? (g.k == 3 ? "conv_brick3_dgrad" : "conv_brick1_dgrad")
-                       : (g.k == 3 ? "conv_brick3_fwd" : "conv_brick1_fwd"),
-                 st, conv_flops(g), conv_bytes(g, 2));
+    // one tag (and one kernel symbol) per variant, so that live timings and
+    // profiler counters describe the same launches
     const bool acc = accumulate != 0;
-    if (g.k == 3) {
-        if (nt == 4) {
-            if (acc) conv_brick_fd<3, 4, 2, true><<<grid, 512, 0, st>>>(a);
-            else conv_brick_fd<3, 4, 2, false><<<grid, 512, 0, st>>>(a);
-        } else {
-            if (acc) conv_brick_fd<3, 2, 1, true><<<grid, 512, 0, st>>>(a);
-            else conv_brick_fd<3, 2, 1, false><<<grid, 512, 0, st>>>(a);
-        }
-    } else {
-        if (nt == 4) {
-            if (acc) conv_brick_fd<1, 4, 2, true><<<grid, 512, 0, st>>>(a);
-            else conv_brick_fd<1, 4, 2, false><<<grid, 512, 0, st>>>(a);
-        } else {
-            if (acc) conv_brick_fd<1, 2, 1, true><<<grid, 512, 0, st>>>(a);
-            else conv_brick_fd<1, 2, 1, false><<<grid, 512, 0, st>>>(a);
-        }
+    const char* tag = g.k == 3 ? (dgrad ? (acc ? "conv_brick3_dgrad_acc" : "conv_brick3_dgrad")
+                                        : "conv_brick3_fwd")
+                               : (dgrad ? (acc ? "conv_brick1_dgrad_acc" : "conv_brick1_dgrad")
+                                        : "conv_brick1_fwd");
+    char tagbuf[40];
+    if (nt == 2) {
+        snprintf(tagbuf, sizeof tagbuf, "%s_c32", tag);
+        tag = tagbuf;
     }
+    ProfScope ps(tag, st, conv_flops(g), conv_bytes(g, 2));
+#define RAT3D_FD(K, N, R)                                                          \
+    do {                                                                           \
+        if (dgrad) {                                                               \
+            if (acc) conv_brick_fd<K, N, R, true, true><<<grid, 512, 0, st>>>(a);  \
+            else conv_brick_fd<K, N, R, false, true><<<grid, 512, 0, st>>>(a);     \
+        } else {                                                                   \
+            if (acc) conv_brick_fd<K, N, R, true, false><<<grid, 512, 0, st>>>(a); \
+            else conv_brick_fd<K, N, R, false, false><<<grid, 512, 0, st>>>(a);    \
+        }                                                                          \
+    } while (0)
+    if (g.k == 3) {
+        if (nt == 4) RAT3D_FD(3, 4, 2);
+        else RAT3D_FD(3, 2, 1);
+    } else {
+        if (nt == 4) RAT3D_FD(1, 4, 2);
+        else RAT3D_FD(1, 2, 1);
+    }
+#undef RAT3D_FD
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }
@@ -1432,9 +1444,11 @@ rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, 
         a.mXG = magic(XG);
         a.m3XG = magic(3 * XG);
         a.mYG = magic(YG);
-        ProfScope ps("conv_brick3_wgrad", st, conv_flops(g), conv_bytes(g, 2));
-        const unsigned grid = (unsigned)((int64_t)Rreal * cigs * cogs);
         const bool part = (g.W & 7) != 0;
+        const char* tag = bc.nk == 6 ? (part ? "conv_band3_wgrad_w4" : "conv_band3_wgrad")
+                                     : (part ? "conv_band3_wgrad_k128_w4" : "conv_band3_wgrad_k128");
+        ProfScope ps(tag, st, conv_flops(g), conv_bytes(g, 2));
+        const unsigned grid = (unsigned)((int64_t)Rreal * cigs * cogs);
         if (bc.nk == 6) {
             if (part) conv_band_wgrad<6, true><<<grid, 512, 0, st>>>(a);
             else conv_band_wgrad<6, false><<<grid, 512, 0, st>>>(a);
