@@ -190,7 +190,8 @@ rat3d_status rat3d_bn_relu_fwd(const rat3d_bn_desc* desc, const void* x, const v
     s = check_ws(ws, ws_bytes, bn_ws_bytes(g));
     if (s != RAT3D_OK) return s;
     return bn_fwd(g, desc->dtype, desc->relu, desc->eps, desc->momentum, x, residual, gamma, beta,
-                  y, save_mean, save_invstd, run_mean, run_var, ws, (hipStream_t)stream);
+                  y, save_mean, save_invstd, run_mean, run_var, nullptr, ws,
+                  (hipStream_t)stream);
 }
 
 rat3d_status rat3d_bn_relu_bwd(const rat3d_bn_desc* desc, const void* dy, const void* x,
@@ -210,8 +211,8 @@ rat3d_status rat3d_bn_relu_bwd(const rat3d_bn_desc* desc, const void* dy, const 
                   "gamma, save_mean, save_invstd, dgamma and dbeta are required");
     s = check_ws(ws, ws_bytes, bn_ws_bytes(g));
     if (s != RAT3D_OK) return s;
-    return bn_bwd(g, desc->dtype, desc->relu, dy, x, y, gamma, save_mean, save_invstd, dx,
-                  dresidual, dgamma, dbeta, accumulate ? 1 : 0, ws, (hipStream_t)stream);
+    return bn_bwd(g, desc->dtype, desc->relu, dy, x, y, gamma, save_mean, save_invstd, nullptr,
+                  dx, dresidual, dgamma, dbeta, accumulate ? 1 : 0, ws, (hipStream_t)stream);
 }
 
 static rat3d_status check_pool(const rat3d_pool_desc* d) {

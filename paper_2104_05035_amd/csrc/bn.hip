@@ -9,7 +9,10 @@
 // Backward: (1) per (channel, slice) partial sums of g and g * (x - mean),
 //           g = dy masked by y > 0; (2) per channel dbeta, dgamma and the
 //           apply coefficients; (3) dx = k * (g - dbeta/M - xhat * dgamma/M),
-//           dresidual = g.
+//           dresidual = g.  Without a residual, y > 0 is the same test as
+//           x * scale + shift > 0 with the forward's own float coefficients
+//           (the apply computes exactly that value before the max with 0), so
+//           given those coefficients the backward reads x instead of x and y.
 // NCDHW: one (n, c) plane is V contiguous voxels; a slice is a contiguous
 // segment of one plane, so per-element indexing needs no division.  A
 // channel's partials are the N * SP segment sums of its planes, combined in
@@ -101,7 +104,7 @@ __global__ void bn_fwd_finalize(const T* __restrict__ x, int N, int C, int64_t V
                                 const float* __restrict__ beta, float eps, float momentum,
                                 float* __restrict__ save_mean, float* __restrict__ save_invstd,
                                 float* __restrict__ run_mean, float* __restrict__ run_var,
-                                float* __restrict__ coef) {
+                                float* __restrict__ coef, float* __restrict__ save_coef) {
     const int c = blockIdx.x * blockDim.x + threadIdx.x;
     if (c >= C) return;
     const double shift = (double)Elt<T>::ld(x + (int64_t)c * V);
@@ -119,8 +122,13 @@ __global__ void bn_fwd_finalize(const T* __restrict__ x, int N, int C, int64_t V
     save_mean[c] = (float)mean;
     save_invstd[c] = (float)invstd;
     const float scale = (float)((double)gamma[c] * invstd);
+    const float bias = (float)((double)beta[c] - mean * (double)scale);
     coef[c] = scale;
-    coef[C + c] = (float)((double)beta[c] - mean * (double)scale);
+    coef[C + c] = bias;
+    if (save_coef) {
+        save_coef[c] = scale;
+        save_coef[C + c] = bias;
+    }
     if (run_mean) run_mean[c] = (float)((1.0 - momentum) * run_mean[c] + momentum * mean);
     if (run_var) {
         const double unb = M > 1.0 ? var * M / (M - 1.0) : var;
@@ -155,16 +163,21 @@ __global__ __launch_bounds__(kBnThreads) void bn_fwd_apply(const T* __restrict__
     vstore<T, VEC>(y + i, v);
 }
 
-template <typename T, int VEC, bool RELU>
+// ReLU mask of the backward: none, y > 0, or x * scale + shift > 0.
+enum { kMaskNone = 0, kMaskY = 1, kMaskX = 2 };
+
+template <typename T, int VEC, int MASK>
 __global__ __launch_bounds__(kBnThreads) void bn_bwd_stats(const T* __restrict__ dy,
                                                            const T* __restrict__ x,
                                                            const T* __restrict__ y, int C,
                                                            int64_t V, int SP, int64_t len,
                                                            const float* __restrict__ save_mean,
+                                                           const float* __restrict__ fcoef,
                                                            float* __restrict__ part) {
     const int c = blockIdx.x, sidx = blockIdx.y;
     const int n = sidx / SP, seg = sidx - n * SP;
     const float mean = save_mean[c];
+    const float fsc = MASK == kMaskX ? fcoef[c] : 0.f, fsh = MASK == kMaskX ? fcoef[C + c] : 0.f;
     const int64_t beg = (int64_t)seg * len;
     const int64_t cnt = (beg + len < V ? beg + len : V) - beg;
     const int64_t base = ((int64_t)n * C + c) * V + beg;
@@ -174,11 +187,14 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_stats(const T* __restrict__
         float g[VEC], xv[VEC];
         vload<T, VEC>(dy + idx, g);
         vload<T, VEC>(x + idx, xv);
-        if constexpr (RELU) {
+        if constexpr (MASK == kMaskY) {
             float yv[VEC];
             vload<T, VEC>(y + idx, yv);
 #pragma unroll
             for (int j = 0; j < VEC; ++j) g[j] = yv[j] > 0.f ? g[j] : 0.f;
+        } else if constexpr (MASK == kMaskX) {
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) g[j] = fmaf(xv[j], fsc, fsh) > 0.f ? g[j] : 0.f;
         }
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
@@ -218,12 +234,11 @@ __global__ void bn_bwd_finalize(int N, int C, int64_t V, int slices,
     coef[2 * C + c] = (float)(invstd * dg / M);
 }
 
-template <typename T, int VEC, bool RELU, bool DRES>
+template <typename T, int VEC, int MASK, bool DRES>
 __global__ __launch_bounds__(kBnThreads) void bn_bwd_apply(
     const T* __restrict__ dy, const T* __restrict__ x, const T* __restrict__ y, int C, int64_t V,
-    unsigned cpp, const float* __restrict__ save_mean, const float* __restrict__ coef,
-    T* __restrict__ dx,
-    T* __restrict__ dres) {
+    unsigned cpp, const float* __restrict__ save_mean, const float* __restrict__ fcoef,
+    const float* __restrict__ coef, T* __restrict__ dx, T* __restrict__ dres) {
     const int plane = (int)(blockIdx.x / cpp);  // wave-uniform
     const int64_t e = ((int64_t)(blockIdx.x - (unsigned)plane * cpp) * kBnThreads + threadIdx.x) * VEC;
     if (e >= V) return;
@@ -233,11 +248,15 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_apply(
     float g[VEC], xv[VEC];
     vload<T, VEC>(dy + i, g);
     vload<T, VEC>(x + i, xv);
-    if constexpr (RELU) {
+    if constexpr (MASK == kMaskY) {
         float yv[VEC];
         vload<T, VEC>(y + i, yv);
 #pragma unroll
         for (int j = 0; j < VEC; ++j) g[j] = yv[j] > 0.f ? g[j] : 0.f;
+    } else if constexpr (MASK == kMaskX) {
+        const float fsc = fcoef[c], fsh = fcoef[C + c];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) g[j] = fmaf(xv[j], fsc, fsh) > 0.f ? g[j] : 0.f;
     }
     if constexpr (DRES) vstore<T, VEC>(dres + i, g);
 #pragma unroll
@@ -250,7 +269,7 @@ template <typename T, int VEC>
 static rat3d_status bn_fwd_t(const BnGeom& g, int relu, float eps, float momentum, const T* x,
                              const T* r, const float* gamma, const float* beta, T* y,
                              float* save_mean, float* save_invstd, float* run_mean,
-                             float* run_var, void* ws, hipStream_t st) {
+                             float* run_var, float* save_coef, void* ws, hipStream_t st) {
     const BnSlices sl = bn_slices(g);
     float* part = (float*)ws;
     float* coef = part + (size_t)g.C * sl.per_channel * 2;
@@ -263,7 +282,7 @@ static rat3d_status bn_fwd_t(const BnGeom& g, int relu, float eps, float momentu
     }
     bn_fwd_finalize<T><<<(unsigned)ceil_div(g.C, 64), 64, 0, st>>>(
         x, g.N, g.C, g.V, sl.per_channel, part, gamma, beta, eps, momentum, save_mean,
-        save_invstd, run_mean, run_var, coef);
+        save_invstd, run_mean, run_var, coef, save_coef);
     RAT3D_LAUNCH_CHECK();
     const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads);  // chunks per plane
     const unsigned grid = cpp * (unsigned)(g.N * g.C);
@@ -283,21 +302,24 @@ static rat3d_status bn_fwd_t(const BnGeom& g, int relu, float eps, float momentu
 template <typename T, int VEC>
 static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x, const T* y,
                              const float* gamma, const float* save_mean,
-                             const float* save_invstd, T* dx, T* dres, float* dgamma,
-                             float* dbeta, int accumulate, void* ws, hipStream_t st) {
+                             const float* save_invstd, const float* fwd_coef, T* dx, T* dres,
+                             float* dgamma, float* dbeta, int accumulate, void* ws,
+                             hipStream_t st) {
     const BnSlices sl = bn_slices(g);
     float* part = (float*)ws;
     float* coef = part + (size_t)g.C * sl.per_channel * 2;
     const dim3 sg(g.C, sl.per_channel);
     const double tb = (double)g.N * g.C * g.V * sizeof(T);
+    const int mask = !relu ? kMaskNone : (fwd_coef ? kMaskX : kMaskY);
     {
-    ProfScope ps("bn_bwd_stats", st, 0.0, tb * (relu ? 3 : 2));
-    if (relu)
-        bn_bwd_stats<T, VEC, true><<<sg, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, sl.per_plane,
-                                                              sl.len, save_mean, part);
-    else
-        bn_bwd_stats<T, VEC, false><<<sg, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, sl.per_plane,
-                                                               sl.len, save_mean, part);
+    ProfScope ps("bn_bwd_stats", st, 0.0, tb * (mask == kMaskY ? 3 : 2));
+#define RAT3D_BN_ST(M)                                                                       \
+    bn_bwd_stats<T, VEC, M><<<sg, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, sl.per_plane,     \
+                                                       sl.len, save_mean, fwd_coef, part)
+    if (mask == kMaskY) RAT3D_BN_ST(kMaskY);
+    else if (mask == kMaskX) RAT3D_BN_ST(kMaskX);
+    else RAT3D_BN_ST(kMaskNone);
+#undef RAT3D_BN_ST
     RAT3D_LAUNCH_CHECK();
     }
     bn_bwd_finalize<<<(unsigned)ceil_div(g.C, 64), 64, 0, st>>>(
@@ -305,14 +327,17 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
     RAT3D_LAUNCH_CHECK();
     const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads);  // chunks per plane
     const unsigned grid = cpp * (unsigned)(g.N * g.C);
-    ProfScope ps("bn_bwd_apply", st, 0.0, tb * ((relu ? 4 : 3) + (dres ? 1 : 0)));
-#define RAT3D_BN_BWD(R, D)                                                                 \
-    bn_bwd_apply<T, VEC, R, D><<<grid, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, cpp,      \
-                                                            save_mean, coef, dx, dres)
-    if (relu && dres) RAT3D_BN_BWD(true, true);
-    else if (relu) RAT3D_BN_BWD(true, false);
-    else if (dres) RAT3D_BN_BWD(false, true);
-    else RAT3D_BN_BWD(false, false);
+    ProfScope ps("bn_bwd_apply", st, 0.0,
+                 tb * ((mask == kMaskY ? 4 : 3) + (dres ? 1 : 0)));
+#define RAT3D_BN_BWD(M, D)                                                                 \
+    bn_bwd_apply<T, VEC, M, D><<<grid, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, cpp,      \
+                                                            save_mean, fwd_coef, coef, dx, dres)
+    if (mask == kMaskY && dres) RAT3D_BN_BWD(kMaskY, true);
+    else if (mask == kMaskY) RAT3D_BN_BWD(kMaskY, false);
+    else if (mask == kMaskX && dres) RAT3D_BN_BWD(kMaskX, true);
+    else if (mask == kMaskX) RAT3D_BN_BWD(kMaskX, false);
+    else if (dres) RAT3D_BN_BWD(kMaskNone, true);
+    else RAT3D_BN_BWD(kMaskNone, false);
 #undef RAT3D_BN_BWD
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
@@ -321,45 +346,45 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
 rat3d_status bn_fwd(const BnGeom& g, rat3d_dtype dt, int relu, float eps, float momentum,
                     const void* x, const void* residual, const float* gamma, const float* beta,
                     void* y, float* save_mean, float* save_invstd, float* run_mean,
-                    float* run_var, void* ws, hipStream_t st) {
+                    float* run_var, float* save_coef, void* ws, hipStream_t st) {
     if (dt == RAT3D_BF16) {
         if (g.V % 8 == 0)
             return bn_fwd_t<bf16, 8>(g, relu, eps, momentum, (const bf16*)x, (const bf16*)residual,
                                      gamma, beta, (bf16*)y, save_mean, save_invstd, run_mean,
-                                     run_var, ws, st);
+                                     run_var, save_coef, ws, st);
         return bn_fwd_t<bf16, 1>(g, relu, eps, momentum, (const bf16*)x, (const bf16*)residual,
                                  gamma, beta, (bf16*)y, save_mean, save_invstd, run_mean, run_var,
-                                 ws, st);
+                                 save_coef, ws, st);
     }
     if (g.V % 4 == 0)
         return bn_fwd_t<float, 4>(g, relu, eps, momentum, (const float*)x, (const float*)residual,
                                   gamma, beta, (float*)y, save_mean, save_invstd, run_mean,
-                                  run_var, ws, st);
+                                  run_var, save_coef, ws, st);
     return bn_fwd_t<float, 1>(g, relu, eps, momentum, (const float*)x, (const float*)residual,
                               gamma, beta, (float*)y, save_mean, save_invstd, run_mean, run_var,
-                              ws, st);
+                              save_coef, ws, st);
 }
 
 rat3d_status bn_bwd(const BnGeom& g, rat3d_dtype dt, int relu, const void* dy, const void* x,
                     const void* y, const float* gamma, const float* save_mean,
-                    const float* save_invstd, void* dx, void* dres, float* dgamma,
-                    float* dbeta, int accumulate, void* ws, hipStream_t st) {
+                    const float* save_invstd, const float* fwd_coef, void* dx, void* dres,
+                    float* dgamma, float* dbeta, int accumulate, void* ws, hipStream_t st) {
     if (dt == RAT3D_BF16) {
         if (g.V % 8 == 0)
             return bn_bwd_t<bf16, 8>(g, relu, (const bf16*)dy, (const bf16*)x, (const bf16*)y,
-                                     gamma, save_mean, save_invstd, (bf16*)dx, (bf16*)dres,
-                                     dgamma, dbeta, accumulate, ws, st);
+                                     gamma, save_mean, save_invstd, fwd_coef, (bf16*)dx,
+                                     (bf16*)dres, dgamma, dbeta, accumulate, ws, st);
         return bn_bwd_t<bf16, 1>(g, relu, (const bf16*)dy, (const bf16*)x, (const bf16*)y, gamma,
-                                 save_mean, save_invstd, (bf16*)dx, (bf16*)dres, dgamma, dbeta,
-                                 accumulate, ws, st);
+                                 save_mean, save_invstd, fwd_coef, (bf16*)dx, (bf16*)dres, dgamma,
+                                 dbeta, accumulate, ws, st);
     }
     if (g.V % 4 == 0)
         return bn_bwd_t<float, 4>(g, relu, (const float*)dy, (const float*)x, (const float*)y,
-                                  gamma, save_mean, save_invstd, (float*)dx, (float*)dres, dgamma,
-                                  dbeta, accumulate, ws, st);
+                                  gamma, save_mean, save_invstd, fwd_coef, (float*)dx,
+                                  (float*)dres, dgamma, dbeta, accumulate, ws, st);
     return bn_bwd_t<float, 1>(g, relu, (const float*)dy, (const float*)x, (const float*)y, gamma,
-                              save_mean, save_invstd, (float*)dx, (float*)dres, dgamma, dbeta,
-                              accumulate, ws, st);
+                              save_mean, save_invstd, fwd_coef, (float*)dx, (float*)dres, dgamma,
+                              dbeta, accumulate, ws, st);
 }
 
 }  // namespace rat3d

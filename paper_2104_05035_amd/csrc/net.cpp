@@ -50,7 +50,7 @@ struct ConvL {
 struct BnL {
     int c = 0;
     size_t g_off = 0, b_off = 0;  // arena offsets of gamma, beta
-    int64_t stat_off = 0;         // ws bytes: mean [c], invstd [c]
+    int64_t stat_off = 0;         // ws bytes: mean [c], invstd [c], apply scale [c], shift [c]
     size_t run_idx = 0;           // index into the running-statistics regions
 };
 
@@ -182,7 +182,7 @@ struct Builder {
         b.c = c;
         b.g_off = param(name + ".g", {c});
         b.b_off = param(name + ".b", {c});
-        b.stat_off = (int64_t)alloc((size_t)2 * c * sizeof(float));
+        b.stat_off = (int64_t)alloc((size_t)4 * c * sizeof(float));
         record(name + ".mean", (size_t)b.stat_off, RAT3D_F32, Shape{1, c, 1, 1, 1});
         record(name + ".invstd", (size_t)b.stat_off + c * sizeof(float), RAT3D_F32,
                Shape{1, c, 1, 1, 1});
@@ -281,6 +281,7 @@ struct Exec {
     void* bn_scr() const { return n->ws + n->bn_scr_off; }
     float* mean(const BnL& b) const { return (float*)(n->ws + b.stat_off); }
     float* invstd(const BnL& b) const { return (float*)(n->ws + b.stat_off) + b.c; }
+    float* fcoef(const BnL& b) const { return (float*)(n->ws + b.stat_off) + 2 * b.c; }
     float* rmean(const BnL& b) const { return (float*)(n->ws + n->run_mean_off) + b.run_idx; }
     float* rvar(const BnL& b) const { return (float*)(n->ws + n->run_var_off) + b.run_idx; }
 
@@ -296,16 +297,23 @@ struct Exec {
         return conv_wgrad(c.g, n->dt, x, dy, grd(c.w_off), c.bias ? grd(c.b_off) : nullptr, acc,
                           conv_scr(), n->conv_scr_bytes, st);
     }
+    // The forward keeps the apply's scale and shift; a BN + ReLU without a
+    // residual recomputes its backward mask from x with them (bn_bwd_x).
     rat3d_status bn_f(const BnL& b, const TRef& x, const void* res, int relu, void* y) const {
         return bn_fwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, relu, n->d.bn_eps, n->d.bn_momentum,
                       a(x), res, par(b.g_off), par(b.b_off), y, mean(b), invstd(b), rmean(b),
-                      rvar(b), bn_scr(), st);
+                      rvar(b), fcoef(b), bn_scr(), st);
     }
     rat3d_status bn_b(const BnL& b, const void* dy, const TRef& x, const void* y, int relu,
                       void* dx, void* dres) const {
         return bn_bwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, relu, dy, a(x), y, par(b.g_off),
-                      mean(b), invstd(b), dx, dres, grd(b.g_off), grd(b.b_off), acc, bn_scr(),
-                      st);
+                      mean(b), invstd(b), nullptr, dx, dres, grd(b.g_off), grd(b.b_off), acc,
+                      bn_scr(), st);
+    }
+    rat3d_status bn_bwd_x(const BnL& b, const void* dy, const TRef& x, void* dx) const {
+        return bn_bwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, 1, dy, a(x), nullptr, par(b.g_off),
+                      mean(b), invstd(b), fcoef(b), dx, nullptr, grd(b.g_off), grd(b.b_off), acc,
+                      bn_scr(), st);
     }
 };
 
@@ -337,7 +345,7 @@ rat3d_status ru_bwd(const Exec& e, const RUPlan& r, bool acc_dx, bool need_dx = 
     RAT3D_TRY(e.bn_b(r.b2, e.g(r.y), r.h2, e.a(r.y), 1, e.g(r.h2), skip_direct ? dx : dskip));
     RAT3D_TRY(e.conv_d(r.c2, e.g(r.h2), e.g(r.a1), 0));
     RAT3D_TRY(e.conv_w(r.c2, e.a(r.a1), e.g(r.h2)));
-    RAT3D_TRY(e.bn_b(r.b1, e.g(r.a1), r.h1, e.a(r.a1), 1, e.g(r.h1), nullptr));
+    RAT3D_TRY(e.bn_bwd_x(r.b1, e.g(r.a1), r.h1, e.g(r.h1)));
     if (r.proj) {
         RAT3D_TRY(e.bn_b(r.bp, dskip, r.hp, nullptr, 0, e.g(r.hp), nullptr));
         if (need_dx) RAT3D_TRY(e.conv_d(r.cp, e.g(r.hp), dx, acc_dx ? 1 : 0));
@@ -383,7 +391,7 @@ rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
                            e.g(m.z), e.st));
     RAT3D_TRY(e.conv_d(m.c2, e.g(m.z), e.g(m.a), 0));
     RAT3D_TRY(e.conv_w(m.c2, e.a(m.a), e.g(m.z)));
-    RAT3D_TRY(e.bn_b(m.bn, e.g(m.a), m.h1, e.a(m.a), 1, e.g(m.h1), nullptr));
+    RAT3D_TRY(e.bn_bwd_x(m.bn, e.g(m.a), m.h1, e.g(m.h1)));
     RAT3D_TRY(e.conv_d(m.c1, e.g(m.h1), e.g(m.u2), 0));
     RAT3D_TRY(e.conv_w(m.c1, e.a(m.u2), e.g(m.h1)));
     RAT3D_TRY(up_bwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.g(m.u2), e.g(m.m4.y), 0,
@@ -420,8 +428,7 @@ rat3d_status stem_bwd(const Exec& e, bool pool) {
         RAT3D_TRY(pool_bwd(s.n, s.c, s.d, s.h, s.w, 3, 2, 1, n->dt, e.g(n->stem_p),
                            (const uint8_t*)e.p(n->stem_am), e.g(n->stem_a), 0, e.st));
     }
-    RAT3D_TRY(e.bn_b(n->stem_bn, e.g(n->stem_a), n->stem_h, e.a(n->stem_a), 1, e.g(n->stem_h),
-                     nullptr));
+    RAT3D_TRY(e.bn_bwd_x(n->stem_bn, e.g(n->stem_a), n->stem_h, e.g(n->stem_h)));
     return e.conv_w(n->stem_conv, n->ext_x, e.g(n->stem_h));
 }
 
