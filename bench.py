@@ -158,7 +158,7 @@ def main():
 
     tflops = conv_flops / (ms_step * 1e-3) / 1e12
     vols = n * mb / (ms_step * 1e-3)
-    kernels = sorted(tags, key=lambda t: -t[2])[:8]
+    kernels = sorted(tags, key=lambda t: -t[2])[:16]
     out = {
         "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 3),

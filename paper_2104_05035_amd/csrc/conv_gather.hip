@@ -319,20 +319,43 @@ __global__ __launch_bounds__(256) void conv_gather_wgrad(ConvGeom g, const T* __
 
 // Sums `splits` partial weight-gradient slabs in split order into dw; four
 // consecutive elements per thread (count is a multiple of 4 on that path).
-__global__ void wgrad_reduce4(const float4* __restrict__ part, int splits, int64_t count4,
-                              float4* __restrict__ dw, int accumulate) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= count4) return;
-    float4 s = accumulate ? dw[i] : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 8
-    for (int z = 0; z < splits; ++z) {
-        const float4 v = part[(int64_t)z * count4 + i];
-        s.x += v.x;
-        s.y += v.y;
-        s.z += v.z;
-        s.w += v.w;
+// dw (+)= sum of the split partials, float4 lanes.  A block owns 16
+// consecutive float4 outputs; its 256 threads cut the splits into 16
+// contiguous chunks (thread t: output t % 16, chunk t / 16), sum them in
+// split order, and the chunk sums are combined in chunk order through LDS:
+// a fixed summation order with every split read by a different thread.
+__global__ __launch_bounds__(256) void wgrad_reduce4(const float4* __restrict__ part, int splits,
+                                                     int64_t count4, float4* __restrict__ dw,
+                                                     int accumulate) {
+    __shared__ float4 red[16][16];
+    const int j = threadIdx.x & 15, c = threadIdx.x >> 4;
+    const int64_t i = (int64_t)blockIdx.x * 16 + j;
+    const int per = (splits + 15) / 16;
+    const int z0 = c * per, z1 = z0 + per < splits ? z0 + per : splits;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i < count4) {
+#pragma unroll 4
+        for (int z = z0; z < z1; ++z) {
+            const float4 v = part[(int64_t)z * count4 + i];
+            s.x += v.x;
+            s.y += v.y;
+            s.z += v.z;
+            s.w += v.w;
+        }
     }
-    dw[i] = s;
+    red[c][j] = s;
+    __syncthreads();
+    if (c == 0 && i < count4) {
+        float4 t = accumulate ? dw[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            t.x += red[k][j].x;
+            t.y += red[k][j].y;
+            t.z += red[k][j].z;
+            t.w += red[k][j].w;
+        }
+        dw[i] = t;
+    }
 }
 
 __global__ void wgrad_reduce(const float* __restrict__ part, int splits, int64_t count,
@@ -472,7 +495,7 @@ rat3d_status conv_wgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* x,
 rat3d_status wgrad_reduce_launch(const float* part, int splits, int64_t count, float* dw,
                                  int accumulate, hipStream_t st) {
     if (count % 4 == 0 && ((uintptr_t)dw & 15u) == 0 && ((uintptr_t)part & 15u) == 0)
-        wgrad_reduce4<<<(unsigned)ceil_div(count / 4, 256), 256, 0, st>>>(
+        wgrad_reduce4<<<(unsigned)ceil_div(count / 4, 16), 256, 0, st>>>(
             (const float4*)part, splits, count / 4, (float4*)dw, accumulate);
     else
         wgrad_reduce<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(part, splits, count, dw,

@@ -31,7 +31,8 @@ struct PwArgs {
 
 __global__ __launch_bounds__(256) void conv_pw_wgrad(PwArgs a) {
     __shared__ float red[4][64 * 64];  // each wave's 64 x 64 partial tile
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int li = lane & 15, kg = lane >> 4;
     const int co0 = blockIdx.y * 64, ci0 = blockIdx.z * 64;
     const int nco = min(64, a.Co - co0) / 16, nci = min(64, a.Ci - ci0) / 16;
@@ -45,39 +46,44 @@ __global__ __launch_bounds__(256) void conv_pw_wgrad(PwArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // Channel tiles past the tensor re-read its last channel: their sums are
+    // never stored, and no load sits behind a branch.
     auto load = [&](int64_t st, F16B (&av)[4], F16B (&bv)[4]) {
         const int64_t n = st / spp;
         const int64_t v = (st - n * spp) * 32 + kg * 8;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            av[t].u = make_uint4(0u, 0u, 0u, 0u);
-            bv[t].u = make_uint4(0u, 0u, 0u, 0u);
-            if (t < nco)
-                av[t].u = *reinterpret_cast<const uint4*>(
-                    a.dy + ((int64_t)n * a.Co + co0 + t * 16 + li) * a.V + v);
-            if (t < nci)
-                bv[t].u = *reinterpret_cast<const uint4*>(
-                    a.x + ((int64_t)n * a.Ci + ci0 + t * 16 + li) * a.V + v);
+            const int co = min(co0 + t * 16 + li, a.Co - 1), ci = min(ci0 + t * 16 + li, a.Ci - 1);
+            av[t].u = *reinterpret_cast<const uint4*>(a.dy + ((int64_t)n * a.Co + co) * a.V + v);
+            bv[t].u = *reinterpret_cast<const uint4*>(a.x + ((int64_t)n * a.Ci + ci) * a.V + v);
         }
     };
 
-    int64_t st = s_beg + wave;
-    F16B ac[4], bc[4];
-    if (st < s_end) load(st, ac, bc);
-    for (; st < s_end; st += 4) {
-        F16B an[4], bn[4];
-        const int64_t nx = st + 4 < s_end ? st + 4 : st;
-        load(nx, an, bn);
+    // Three register sets: the operands of a wave's step are loaded three of
+    // its steps ahead.  Loads past the range re-read its last step (never a
+    // load behind a branch, which would be waited for on the spot).
+    constexpr int PD = 3;
+    F16B av[PD][4], bv[PD][4];
+    const int64_t last = s_end - 1;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+    for (int r = 0; r < PD; ++r) {
+        const int64_t sr = s_beg + wave + 4 * r;
+        load(sr < s_end ? sr : last, av[r], bv[r]);
+    }
+    for (int64_t st = s_beg + wave; st < s_end; st += 4 * PD) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ac[i].b, bc[j].b, acc[i][j], 0,
-                                                                   0, 0);
+        for (int r = 0; r < PD; ++r) {
+            const int64_t sc = st + 4 * r;
+            if (sc < s_end) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            ac[t] = an[t];
-            bc[t] = bn[t];
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[r][i].b, bv[r][j].b,
+                                                                           acc[i][j], 0, 0, 0);
+            }
+            const int64_t sn = sc + 4 * PD;
+            load(sn < s_end ? sn : last, av[r], bv[r]);
         }
     }
 
@@ -108,7 +114,7 @@ bool pw_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) {
 static int pw_splits(const ConvGeom& g) {
     const int64_t steps = (int64_t)g.N * g.D * g.H * g.W / 32;
     const int64_t tiles = ceil_div(g.Co, 64) * ceil_div(g.Ci, 64);
-    int64_t s = ceil_div(1024, tiles);
+    int64_t s = ceil_div(2 * device_cus(), tiles);  // two workgroups per CU (LDS)
     if (s > steps) s = steps;
     if (s < 1) s = 1;
     return (int)s;
