@@ -18,6 +18,7 @@
 // float32 uses four v_mfma_f32_16x16x4_f32 (4 K values per lane).
 #include "common.hpp"
 #include "kernels.hpp"
+#include "vec.hpp"
 #include "prof.hpp"
 
 namespace rat3d {
@@ -376,17 +377,40 @@ static int bias_segments(const ConvGeom& g) {
     return sp < 1 ? 1 : sp;
 }
 
+// Block (c, n * SP + segment): the sum of one segment of plane (n, c).
+// Segments are multiples of 8 elements; with V % 8 == 0 every thread reads
+// 8 elements per 16-byte load, four loads in flight (clamped in-segment
+// addresses, out-of-segment lanes masked), else one element per load.
 template <typename T>
 __global__ __launch_bounds__(256) void bias_grad_part(const T* __restrict__ dy, int C, int64_t V,
                                                       int SP, float* __restrict__ part) {
     __shared__ float red[256];
     const int c = blockIdx.x, sl = blockIdx.y;  // sl = n * SP + segment
     const int n = sl / SP, seg = sl - n * SP;
-    const int64_t len = (V + SP - 1) / SP;
+    const int64_t len = ((V + SP - 1) / SP + 7) & ~(int64_t)7;
     const int64_t beg = seg * len, end = beg + len < V ? beg + len : V;
     const T* p = dy + ((int64_t)n * C + c) * V;
     float s = 0.f;
-    for (int64_t e = beg + threadIdx.x; e < end; e += 256) s += Elt<T>::ld(p + e);
+    constexpr int VEC = 16 / (int)sizeof(T);
+    if (V % VEC == 0 && end > beg) {
+        constexpr int64_t STEP = 256 * VEC;
+        for (int64_t e0 = beg + threadIdx.x * VEC; e0 < end; e0 += 4 * STEP) {
+            float v[4][VEC];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t e = e0 + u * STEP;
+                vload<T, VEC>(p + (e < end ? e : end - VEC), v[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool ok = e0 + u * STEP < end;
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) s += ok ? v[u][j] : 0.f;
+            }
+        }
+    } else {
+        for (int64_t e = beg + threadIdx.x; e < end; e += 256) s += Elt<T>::ld(p + e);
+    }
     red[threadIdx.x] = s;
     __syncthreads();
     for (int w = 128; w > 0; w >>= 1) {

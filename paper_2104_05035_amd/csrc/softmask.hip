@@ -475,12 +475,32 @@ __global__ __launch_bounds__(kEwThreads) void pool332_fwd_pl(const bf16* __restr
                 best[j][e] = 0.f;
                 bkd[j][e] = -1;
             }
+        // all source planes are requested before any is used (clamped plane
+        // index, so no load waits behind a branch)
+        constexpr int NQ = 2 * kPlanes + 1;
+        uint4 raw[NQ];
+        if (vec) {
 #pragma unroll
-        for (int q = 0; q < 2 * kPlanes + 1; ++q) {
+            for (int q = 0; q < NQ; ++q) {
+                const int id = min(max(2 * od0 - 1 + q, 0), D - 1);
+                raw[q] = *reinterpret_cast<const uint4*>(xv + (int64_t)id * HW + p);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
             const int id = 2 * od0 - 1 + q;
             if (id < 0 || id >= D) continue;
             float v[8];
-            ld8(xv + (int64_t)id * HW, p, HW, vec, v);
+            if (vec) {
+                const uint32_t w[4] = {raw[q].x, raw[q].y, raw[q].z, raw[q].w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    v[2 * i] = __uint_as_float(w[i] << 16);
+                    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+                }
+            } else {
+                ld8(xv + (int64_t)id * HW, p, HW, false, v);
+            }
 #pragma unroll
             for (int j = 0; j < kPlanes; ++j) {
                 const int kd = q - 2 * j;
@@ -629,12 +649,32 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
         for (int l = 0; l < NF; ++l)
 #pragma unroll
             for (int e = 0; e < 8; ++e) acc[l][e] = 0.f;
+        // all coarse planes are requested before any is used (clamped plane
+        // index, so no load waits behind a branch)
+        constexpr int NQ = kPlanes + 2;
+        uint4 raw[NQ];
+        if (vec) {
 #pragma unroll
-        for (int q = 0; q < kPlanes + 2; ++q) {
+            for (int q = 0; q < NQ; ++q) {
+                const int md = min(max(m0 - 1 + q, 0), Di - 1);
+                raw[q] = *reinterpret_cast<const uint4*>(xv + (int64_t)md * HWi + p);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
             const int md = m0 - 1 + q;
             if (md < 0 || md >= Di) continue;
             float v[8];
-            ld8(xv + (int64_t)md * HWi, p, HWi, vec, v);
+            if (vec) {
+                const uint32_t w[4] = {raw[q].x, raw[q].y, raw[q].z, raw[q].w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    v[2 * i] = __uint_as_float(w[i] << 16);
+                    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+                }
+            } else {
+                ld8(xv + (int64_t)md * HWi, p, HWi, false, v);
+            }
 #pragma unroll
             for (int l = 0; l < NF; ++l) {
                 const float wd = x2_w(2 * m0 + l, md, Di);
@@ -716,12 +756,27 @@ __global__ __launch_bounds__(kEwThreads) void up2_bwd_pl(const bf16* __restrict_
         for (int l = 0; l < kPlanes; ++l)
 #pragma unroll
             for (int e = 0; e < 8; ++e) acc[l][e] = 0.f;
+        // all fine planes are requested before any is used (clamped index)
+        constexpr int NQ = 2 * kPlanes + 2;
+        uint4 raw[NQ];
 #pragma unroll
-        for (int q = 0; q < 2 * kPlanes + 2; ++q) {
+        for (int q = 0; q < NQ; ++q) {
+            const int od = min(max(2 * m0 - 1 + q, 0), Do - 1);
+            raw[q] = *reinterpret_cast<const uint4*>(gv + (int64_t)od * HWo + p);
+        }
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
             const int od = 2 * m0 - 1 + q;
             if (od < 0 || od >= Do) continue;
             float v[8];
-            ld8(gv + (int64_t)od * HWo, p, HWo, true, v);
+            {
+                const uint32_t w[4] = {raw[q].x, raw[q].y, raw[q].z, raw[q].w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    v[2 * i] = __uint_as_float(w[i] << 16);
+                    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+                }
+            }
 #pragma unroll
             for (int l = 0; l < kPlanes; ++l) {
                 if (m0 + l >= Di) continue;
