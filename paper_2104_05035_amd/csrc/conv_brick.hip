@@ -1351,6 +1351,8 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
         prep_fwd_weights<<<(unsigned)ceil_div(wn, 256), 256, 0, st>>>((const bf16*)w, g.Co, g.Ci,
                                                                       KT, wt);
     RAT3D_LAUNCH_CHECK();
+    if (pw_fd_ok(g, RAT3D_BF16, dgrad))
+        return conv_fd_pw(g, dgrad, src, wt, bias, dst, accumulate, st);
     FdArgs a;
     a.src = (const bf16*)src;
     a.wt = wt;

@@ -105,6 +105,199 @@ __global__ __launch_bounds__(256) void conv_pw_wgrad(PwArgs a) {
     }
 }
 
+// ---------------------------------------------------------------- fwd / dgrad
+// Forward (and input gradient) of 1x1x1, stride-1 convolutions with at most
+// 64 source and 64 target channels, as a streaming GEMM: a workgroup owns
+// 256 voxels of one sample, loads all their source channels (16-byte loads of
+// 8 voxels of one channel), transposes 8 x 8 blocks in registers into
+// voxel-major rows of LDS (16-byte slot of channel group cg in voxel v at
+// cg ^ (v & 7)), and each wave multiplies 64-voxel blocks by every target channel:
+// A = the voxel rows (K = source channels), B = weight fragments from the
+// prepared [K / 32][target][32] layout, which serves the forward (K = C_in)
+// and the input gradient (K = C_out) alike.  An accumulator row block is four
+// consecutive voxels of one target channel: stored as 8 bytes (old value
+// added first when accumulating, one rounding).  HBM-bound: each source and
+// target element moves once.
+namespace {
+struct PfArgs {
+    const bf16* src;   // [N][Cs][V]
+    const bf16* wt;    // [Cs / 32][Ct][32]
+    const float* bias; // [Ct] or null
+    bf16* dst;         // [N][Ct][V]
+    int Cs, Ct;
+    int64_t V;
+    int64_t cpv;       // 256-voxel chunks per sample
+    int accumulate;
+};
+constexpr int kPfVox = 256;
+constexpr int kPfOutPitch = kPfVox * 2 + 16;  // bytes per target channel of a staged output tile
+__device__ __forceinline__ uint32_t pf_lo(uint32_t lo, uint32_t hi) {
+    return __builtin_amdgcn_perm(hi, lo, 0x05040100u);  // lo16(lo) | lo16(hi) << 16
+}
+__device__ __forceinline__ uint32_t pf_hi(uint32_t lo, uint32_t hi) {
+    return __builtin_amdgcn_perm(hi, lo, 0x07060302u);  // hi16(lo) | hi16(hi) << 16
+}
+}  // namespace
+
+__global__ __launch_bounds__(256) void conv_pw_fd(PfArgs a) {
+    // one 256-voxel round: the staged output tile reuses the input rows
+    static_assert(kPfVox == 256, "outputs are staged over the input tile");
+    constexpr int kLds = kPfVox * 128 > 64 * kPfOutPitch ? kPfVox * 128 : 64 * kPfOutPitch;
+    __shared__ __align__(16) unsigned char xs[kLds];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t n = blockIdx.x / a.cpv;
+    const int64_t v0 = (blockIdx.x - n * a.cpv) * kPfVox;
+    const int ncg = a.Cs >> 3;  // source channel groups of 8
+    // staging: thread (cg = tid % 8, voxel group g = tid / 8 + 32 r)
+    const int cg = tid & 7;
+    const bf16* sp = a.src + (n * a.Cs + (int64_t)cg * 8) * a.V;
+#pragma unroll
+    for (int r = 0; r < kPfVox / 8 / 32; ++r) {
+        const int g = (tid >> 3) + 32 * r;
+        const int64_t v = v0 + 8 * g;
+        const bool live = cg < ncg && v < a.V;
+        // idle or past-the-end items re-read the first group (never stored)
+        const int64_t off = live ? v : 0;
+        const int cgc = live ? 0 : -cg;  // keep the channel inside the tensor
+        uint4 u[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            u[j] = *reinterpret_cast<const uint4*>(sp + ((int64_t)cgc * 8 + j) * a.V + off);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int wd = e >> 1;
+            uint32_t o[4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t wl = wd == 0 ? u[2 * c].x : wd == 1 ? u[2 * c].y
+                                  : wd == 2 ? u[2 * c].z : u[2 * c].w;
+                const uint32_t wh = wd == 0 ? u[2 * c + 1].x : wd == 1 ? u[2 * c + 1].y
+                                  : wd == 2 ? u[2 * c + 1].z : u[2 * c + 1].w;
+                o[c] = (e & 1) ? pf_hi(wl, wh) : pf_lo(wl, wh);
+            }
+            const int vl = 8 * g + e;
+            *reinterpret_cast<uint4*>(xs + vl * 128 + ((cg ^ (vl & 7)) << 4)) =
+                make_uint4(o[0], o[1], o[2], o[3]);
+        }
+    }
+    __syncthreads();
+
+    const int li = lane & 15, kg = lane >> 4;
+    const int nks = a.Cs >> 5, nnt = a.Ct >> 4;
+    bf16x8 B[2][4];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            // tiles past Cs / Ct re-read tile 0 (their sums are never used)
+            const int kc = ks < nks ? ks : 0, nt = t < nnt ? t : 0;
+            B[ks][t] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const uint4*>(
+                            a.wt + ((int64_t)(kc * a.Ct + nt * 16 + li) * 32 + kg * 8)));
+        }
+    // wave w multiplies voxels 256 rr + 64 w .. + 63 of the chunk
+#pragma unroll 1
+    for (int rr = 0; rr < kPfVox / 256; ++rr) {
+        const int vb = rr * 256 + wave * 64;
+        f32x4 acc[4][4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) acc[m][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            if (ks >= nks) break;
+            bf16x8 A[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const int vl = vb + m * 16 + li;
+                const int c8 = ks * 4 + kg;
+                A[m] = __builtin_bit_cast(
+                    bf16x8,
+                    *reinterpret_cast<const uint4*>(xs + vl * 128 + ((c8 ^ (vl & 7)) << 4)));
+            }
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    acc[m][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[m], B[ks][t], acc[m][t],
+                                                                       0, 0, 0);
+        }
+        // acc[m][t][j]: voxel v0 + vb + 16 m + 4 kg + j, target channel 16 t + li
+        if (a.accumulate) {
+            // old value added before the one rounding: stored from the lanes
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                if (t >= nnt) break;
+                const int co = t * 16 + li;
+                bf16* dp = a.dst + (n * a.Ct + co) * a.V;
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const int64_t v = v0 + vb + m * 16 + kg * 4;
+                    if (v >= a.V) continue;
+                    uint2* q = reinterpret_cast<uint2*>(dp + v);
+                    const uint2 o = *q;
+                    const float r0 = acc[m][t][0] + __uint_as_float(o.x << 16);
+                    const float r1 = acc[m][t][1] + __uint_as_float(o.x & 0xffff0000u);
+                    const float r2 = acc[m][t][2] + __uint_as_float(o.y << 16);
+                    const float r3 = acc[m][t][3] + __uint_as_float(o.y & 0xffff0000u);
+                    *q = make_uint2(pack_bf16x2(r0, r1), pack_bf16x2(r2, r3));
+                }
+            }
+            continue;
+        }
+        // staged through LDS as [target channel][voxel] rows, then stored as
+        // 16-byte pieces of whole rows
+        __syncthreads();  // every wave has read its operands of this round
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            if (t >= nnt) break;
+            const int co = t * 16 + li;
+            const float bv = a.bias ? a.bias[co] : 0.f;
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                *reinterpret_cast<uint2*>(xs + co * kPfOutPitch + (wave * 64 + m * 16 + kg * 4) * 2) =
+                    make_uint2(pack_bf16x2(acc[m][t][0] + bv, acc[m][t][1] + bv),
+                               pack_bf16x2(acc[m][t][2] + bv, acc[m][t][3] + bv));
+        }
+        __syncthreads();
+        for (int it = tid; it < a.Ct * (256 / 8); it += 256) {
+            const int co = it >> 5, pc = it & 31;
+            const int64_t v = v0 + rr * 256 + pc * 8;
+            if (v < a.V)
+                *reinterpret_cast<uint4*>(a.dst + (n * a.Ct + co) * a.V + v) =
+                    *reinterpret_cast<const uint4*>(xs + co * kPfOutPitch + pc * 16);
+        }
+    }
+}
+
+bool pw_fd_ok(const ConvGeom& g, rat3d_dtype dt, bool dgrad) {
+    const int cs = dgrad ? g.Co : g.Ci, ct = dgrad ? g.Ci : g.Co;
+    const int64_t V = (int64_t)g.D * g.H * g.W;
+    return dt == RAT3D_BF16 && g.k == 1 && g.s == 1 && g.p == 0 && (cs == 32 || cs == 64) &&
+           ct % 16 == 0 && ct <= 64 && V % 8 == 0;
+}
+
+rat3d_status conv_fd_pw(const ConvGeom& g, bool dgrad, const void* src, const void* wt,
+                        const float* bias, void* dst, int accumulate, hipStream_t st) {
+    PfArgs a;
+    a.src = (const bf16*)src;
+    a.wt = (const bf16*)wt;
+    a.bias = dgrad ? nullptr : bias;
+    a.dst = (bf16*)dst;
+    a.Cs = dgrad ? g.Co : g.Ci;
+    a.Ct = dgrad ? g.Ci : g.Co;
+    a.V = (int64_t)g.D * g.H * g.W;
+    a.cpv = ceil_div(a.V, kPfVox);
+    a.accumulate = accumulate;
+    const char* tag = dgrad ? (accumulate ? "conv_pw_dgrad_acc" : "conv_pw_dgrad") : "conv_pw_fwd";
+    ProfScope ps(tag, st, conv_flops(g), conv_bytes(g, 2));
+    conv_pw_fd<<<(unsigned)(g.N * a.cpv), 256, 0, st>>>(a);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
 bool pw_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) {
     const int64_t V = (int64_t)g.D * g.H * g.W;
     return dt == RAT3D_BF16 && g.k == 1 && g.s == 1 && g.p == 0 && g.Ci % 16 == 0 &&

@@ -76,6 +76,11 @@ rat3d_status conv_wgrad_stem(const ConvGeom& g, const void* x, const void* dy, f
 
 // ---- 1x1x1 weight gradient as a direct GEMM (conv_pw.hip) ---------------
 bool pw_wgrad_ok(const ConvGeom& g, rat3d_dtype dt);
+// forward / input gradient with at most 64 source and target channels; wt is
+// the brick kernels' prepared weight layout for k = 1
+bool pw_fd_ok(const ConvGeom& g, rat3d_dtype dt, bool dgrad);
+rat3d_status conv_fd_pw(const ConvGeom& g, bool dgrad, const void* src, const void* wt,
+                        const float* bias, void* dst, int accumulate, hipStream_t st);
 size_t pw_wgrad_ws(const ConvGeom& g);
 rat3d_status conv_wgrad_pw(const ConvGeom& g, const void* x, const void* dy, float* dw,
                            int accumulate, void* ws, hipStream_t st);
