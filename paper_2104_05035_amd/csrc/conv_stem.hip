@@ -73,16 +73,51 @@ __global__ __launch_bounds__(256, 2) void stem_fwd_k(const bf16* __restrict__ x,
     const int64_t HW = (int64_t)H * W;
     const bf16* xp = x + (int64_t)n * D * HW;
 
-    for (int it = tid; it < kFBD * kFBH * kFBW; it += 256) {
-        const int c = it % kFBW, r = it / kFBW;
-        const int hh = r % kFBH, dd = r / kFBH;
-        const int d = bd + dd, h = bh + hh, w = bw + c;
-        bf16 v = 0;
-        if ((unsigned)d < (unsigned)D && (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W)
-            v = xp[d * HW + (int64_t)h * W + w];
-        brick[0][it] = v;
-        if (c >= 2) brick[1][it - 2] = v;  // copy 1 column c' holds column c' + 2
-        if (c >= kFBW - 2) brick[1][it] = 0;
+    // Staging (W % 8 == 0): brick column c is input column bw + c with
+    // bw = 2 w0 - 3 = a0 + 5, a0 a multiple of 8.  A brick row is five
+    // 16-byte chunks; chunk k of copy 0 holds input dwords G[4k + 2 ..] moved
+    // by one bf16 (G = the row's dwords from a0), chunk k of copy 1 the same
+    // one dword further.  Each item loads the two aligned 16-byte groups that
+    // cover it (unconditionally: rows or groups outside the volume load from
+    // a clamped address and are zeroed) and writes both copies.
+    {
+        const int a0 = bw - 5;
+        constexpr int NCH = kFBW / 8;                     // 5 chunks per row
+        constexpr int NIT = kFBD * kFBH * NCH;            // 1365 items
+        const int64_t plane = (int64_t)D * HW;
+#pragma unroll 2
+        for (int it = tid; it < NIT; it += 256) {
+            const int k = it % NCH, r = it / NCH;
+            const int hh = r % kFBH, dd = r / kFBH;
+            const int d = bd + dd, h = bh + hh;
+            const bool rok = (unsigned)d < (unsigned)D && (unsigned)h < (unsigned)H;
+            uint32_t g[8];
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const int c0 = a0 + 8 * (k + q);
+                const bool ok = rok && c0 >= 0 && c0 < W;
+                const int64_t off = ok ? (int64_t)d * HW + (int64_t)h * W + c0 : 0;
+                const uint4 u = *reinterpret_cast<const uint4*>(xp + (off < plane ? off : 0));
+                g[4 * q + 0] = ok ? u.x : 0u;
+                g[4 * q + 1] = ok ? u.y : 0u;
+                g[4 * q + 2] = ok ? u.z : 0u;
+                g[4 * q + 3] = ok ? u.w : 0u;
+            }
+            // brick dword j (columns 2j, 2j + 1) = high half of G[j + 2], low half of G[j + 3]
+            uint32_t o0[4], o1[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                o0[j] = __builtin_amdgcn_alignbit(g[j + 3], g[j + 2], 16);
+                o1[j] = __builtin_amdgcn_alignbit(g[j + 4], g[j + 3], 16);
+            }
+            // the last chunk's copy 1 would read past the loaded groups: its
+            // final dword (columns 38, 39 of copy 0 + 2) lies outside the brick
+            if (k == NCH - 1) o1[3] = 0u;
+            bf16* row0 = &brick[0][r * kFBW + 8 * k];
+            bf16* row1 = &brick[1][r * kFBW + 8 * k];
+            *reinterpret_cast<uint4*>(row0) = make_uint4(o0[0], o0[1], o0[2], o0[3]);
+            *reinterpret_cast<uint4*>(row1) = make_uint4(o1[0], o1[1], o1[2], o1[3]);
+        }
     }
     __syncthreads();
 
@@ -266,21 +301,39 @@ __global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
     }
 }
 
-// part is [ranges][32][49*8]; dw is [32][1][7][7][7] (padding column kw = 7 dropped)
-__global__ void stem_wgrad_reduce(const float* __restrict__ part, int ranges,
-                                  float* __restrict__ dw, int accumulate) {
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= kSCo * kSRows * kSK) return;
+// part is [ranges][32][49*8]; dw is [32][1][7][7][7] (padding column kw = 7
+// dropped).  A block owns 16 consecutive outputs; its 256 threads cut the
+// ranges into 16 contiguous chunks (thread t: output t % 16, chunk t / 16),
+// sum them in range order, and the chunk sums are combined in chunk order.
+__global__ __launch_bounds__(256) void stem_wgrad_reduce(const float* __restrict__ part,
+                                                         int ranges, float* __restrict__ dw,
+                                                         int accumulate) {
+    __shared__ float red[16][16];
+    const int j = threadIdx.x & 15, c = threadIdx.x >> 4;
+    const int i = blockIdx.x * 16 + j;
+    const bool live = i < kSCo * kSRows * kSK;
     const int kw = i % kSK, r = (i / kSK) % kSRows, co = i / (kSK * kSRows);
     const int64_t src = (int64_t)co * kSRows * 8 + r * 8 + kw;
-    float s = accumulate ? dw[i] : 0.f;
-    for (int z = 0; z < ranges; ++z) s += part[(int64_t)z * kSCo * kSRows * 8 + src];
-    dw[i] = s;
+    const int per = (ranges + 15) / 16;
+    const int z0 = c * per, z1 = z0 + per < ranges ? z0 + per : ranges;
+    float s = 0.f;
+    if (live) {
+#pragma unroll 4
+        for (int z = z0; z < z1; ++z) s += part[(int64_t)z * kSCo * kSRows * 8 + src];
+    }
+    red[c][j] = s;
+    __syncthreads();
+    if (c == 0 && live) {
+        float t = accumulate ? dw[i] : 0.f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) t += red[k][j];
+        dw[i] = t;
+    }
 }
 
 bool stem_ok(const ConvGeom& g, rat3d_dtype dt) {
     return dt == RAT3D_BF16 && g.Ci == 1 && g.Co == kSCo && g.k == kSK && g.s == kSS &&
-           g.p == kSP;
+           g.p == kSP && g.W % 8 == 0;
 }
 
 size_t stem_fwd_ws() { return (size_t)kSCo * kSRowsPad * 8 * 2; }
@@ -342,8 +395,8 @@ rat3d_status conv_wgrad_stem(const ConvGeom& g, const void* x, const void* dy, f
         RAT3D_LAUNCH_CHECK();
     }
     ProfScope ps("wgrad_reduce", st, 0.0, 4.0 * kSCo * kSRows * 8 * (Rreal + 1 + accumulate));
-    stem_wgrad_reduce<<<(unsigned)ceil_div(kSCo * kSRows * kSK, 256), 256, 0, st>>>(a.part, Rreal,
-                                                                                   dw, accumulate);
+    stem_wgrad_reduce<<<(unsigned)ceil_div(kSCo * kSRows * kSK, 16), 256, 0, st>>>(a.part, Rreal,
+                                                                                  dw, accumulate);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }
