@@ -229,18 +229,52 @@ __global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
         const int bd = d0 * kSS - kSP, bh = h0 * kSS - kSP, bw = w0 * kSS - kSP;
         const bf16* xp = a.x + (int64_t)n * a.D * HW;
         __syncthreads();
-        for (int it = tid; it < kGBD * kGBH * 2 * kGHalf; it += 256) {
-            const int c = it % (2 * kGHalf), row = it / (2 * kGHalf);
-            const int hh = row % kGBH, dd = row / kGBH;
-            const int d = bd + dd, h = bh + hh, w = bw + c;
-            bf16 v = 0;
-            if ((unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
-                (unsigned)w < (unsigned)a.W)
-                v = xp[d * HW + (int64_t)h * a.W + w];
-            const int p = c & 1, cc = c >> 1;
-            xs[p][0][row][cc] = v;
-            if (cc >= 1) xs[p][1][row][cc - 1] = v;
-            if (cc == kGHalf - 1) xs[p][1][row][cc] = 0;
+        // Staging (W % 8 == 0): brick column c is input column a0 + 5 + c
+        // (a0 = bw - 5, a multiple of 8).  With G the row's dwords from a0,
+        // plane 0 column cc = high half of G[cc + 2], plane 1 column cc = low
+        // half of G[cc + 3]; the shifted copies start one column later.  An
+        // item (row, k) builds dwords 4k .. 4k + 3 of the four plane copies
+        // from the three aligned 16-byte groups G[8k .. 8k + 11], loaded
+        // unconditionally (rows or groups outside the volume: clamped address,
+        // zeroed).
+        {
+            const int a0 = bw - 5;
+            constexpr int NIT = kGBD * kGBH * 3;
+            const int64_t plane = (int64_t)a.D * HW;
+#pragma unroll 2
+            for (int it = tid; it < NIT; it += 256) {
+                const int k = it % 3, row = it / 3;
+                const int hh = row % kGBH, dd = row / kGBH;
+                const int d = bd + dd, h = bh + hh;
+                const bool rok = (unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H;
+                uint32_t g[12];
+#pragma unroll
+                for (int q = 0; q < 3; ++q) {
+                    const int c0 = a0 + 8 * (2 * k + q);
+                    const bool ok = rok && c0 >= 0 && c0 < a.W;
+                    const int64_t off = ok ? (int64_t)d * HW + (int64_t)h * a.W + c0 : 0;
+                    const uint4 u = *reinterpret_cast<const uint4*>(xp + (off < plane ? off : 0));
+                    g[4 * q + 0] = ok ? u.x : 0u;
+                    g[4 * q + 1] = ok ? u.y : 0u;
+                    g[4 * q + 2] = ok ? u.z : 0u;
+                    g[4 * q + 3] = ok ? u.w : 0u;
+                }
+                // plane dword m = 4k + j uses G[2m + 2 .. 2m + 5] = g[2j + 2 .. 2j + 5]
+                uint32_t p0[4], p1[4], s0[4], s1[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t a2 = g[2 * j + 2], a3 = g[2 * j + 3], a4 = g[2 * j + 4],
+                                   a5 = g[2 * j + 5];
+                    p0[j] = __builtin_amdgcn_perm(a3, a2, 0x07060302u);  // hi(a2) | hi(a3) << 16
+                    p1[j] = __builtin_amdgcn_perm(a4, a3, 0x05040100u);  // lo(a3) | lo(a4) << 16
+                    s0[j] = __builtin_amdgcn_perm(a4, a3, 0x07060302u);  // hi(a3) | hi(a4) << 16
+                    s1[j] = __builtin_amdgcn_perm(a5, a4, 0x05040100u);  // lo(a4) | lo(a5) << 16
+                }
+                *reinterpret_cast<uint4*>(&xs[0][0][row][8 * k]) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
+                *reinterpret_cast<uint4*>(&xs[1][0][row][8 * k]) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
+                *reinterpret_cast<uint4*>(&xs[0][1][row][8 * k]) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
+                *reinterpret_cast<uint4*>(&xs[1][1][row][8 * k]) = make_uint4(s1[0], s1[1], s1[2], s1[3]);
+            }
         }
         __syncthreads();
 #pragma unroll 1
@@ -249,14 +283,15 @@ __global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
             const int hl = (s % (kGH / 2)) * 2 + hl_l;
             const int d = d0 + dl, h = h0 + hl, w = w0 + wl;
             const bool ok = d < a.Do && h < a.Ho && w + 8 <= a.Wo;
+            // unconditional load (outside the volume: the plane's first
+            // voxels, zeroed), so it is not waited for on the spot
+            const int64_t vo = ok ? ((int64_t)d * a.Ho + h) * a.Wo + w : 0;
             F16B av[2];
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) {
-                av[ct].u = make_uint4(0u, 0u, 0u, 0u);
-                if (ok)
-                    av[ct].u = *reinterpret_cast<const uint4*>(
-                        a.dy + ((int64_t)n * kSCo + ct * 16 + li) * Vo +
-                        ((int64_t)d * a.Ho + h) * a.Wo + w);
+                const uint4 u = *reinterpret_cast<const uint4*>(
+                    a.dy + ((int64_t)n * kSCo + ct * 16 + li) * Vo + vo);
+                av[ct].u = ok ? u : make_uint4(0u, 0u, 0u, 0u);
             }
 #pragma unroll
             for (int j = 0; j < kTilesPerWave; ++j) {
@@ -265,16 +300,19 @@ __global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
                 // this lane's B column: padded tap t = tile*16 + li
                 const int t = tile * 16 + li;
                 const int rrow = t >> 3, kw = t & 7;
+                // padding taps (kw = 7, rows past 49) read a valid tap; their
+                // sums are never stored
                 F16B bv;
-                bv.u = make_uint4(0u, 0u, 0u, 0u);
-                if (rrow < kSRows && kw < kSK) {
-                    const int kd = rrow / kSK, kh = rrow - kd * kSK;
+                {
+                    const int rr = rrow < kSRows ? rrow : kSRows - 1;
+                    const int kwc = kw < kSK ? kw : kSK - 1;
+                    const int kd = rr / kSK, kh = rr - kd * kSK;
                     // input column (brick) for output column wl + i: 2*(wl + i) + kw
                     // = parity kw & 1, plane column wl + i + (kw >> 1)
-                    const int start = wl + (kw >> 1);
+                    const int start = wl + (kwc >> 1);
                     const int sh = start & 1;
                     const bf16* src =
-                        &xs[kw & 1][sh][(dl * kSS + kd) * kGBH + hl * kSS + kh][start - sh];
+                        &xs[kwc & 1][sh][(dl * kSS + kd) * kGBH + hl * kSS + kh][start - sh];
 #pragma unroll
                     for (int q = 0; q < 4; ++q) bv.w[q] = reinterpret_cast<const uint32_t*>(src)[q];
                 }
