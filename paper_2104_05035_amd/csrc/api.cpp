@@ -212,7 +212,7 @@ rat3d_status rat3d_bn_relu_bwd(const rat3d_bn_desc* desc, const void* dy, const 
     s = check_ws(ws, ws_bytes, bn_ws_bytes(g));
     if (s != RAT3D_OK) return s;
     return bn_bwd(g, desc->dtype, desc->relu, dy, x, y, gamma, save_mean, save_invstd, nullptr,
-                  dx, dresidual, dgamma, dbeta, accumulate ? 1 : 0, ws, (hipStream_t)stream);
+                  dx, dresidual, 0, dgamma, dbeta, accumulate ? 1 : 0, ws, (hipStream_t)stream);
 }
 
 static rat3d_status check_pool(const rat3d_pool_desc* d) {

@@ -9,7 +9,7 @@
 // Backward: (1) per (channel, slice) partial sums of g and g * (x - mean),
 //           g = dy masked by y > 0; (2) per channel dbeta, dgamma and the
 //           apply coefficients; (3) dx = k * (g - dbeta/M - xhat * dgamma/M),
-//           dresidual = g.  Without a residual, y > 0 is the same test as
+//           dresidual = g (or dresidual += g, one rounding).  Without a residual, y > 0 is the same test as
 //           x * scale + shift > 0 with the forward's own float coefficients
 //           (the apply computes exactly that value before the max with 0), so
 //           given those coefficients the backward reads x instead of x and y.
@@ -234,7 +234,8 @@ __global__ void bn_bwd_finalize(int N, int C, int64_t V, int slices,
     coef[2 * C + c] = (float)(invstd * dg / M);
 }
 
-template <typename T, int VEC, int MASK, bool DRES>
+// DRES: 0 no residual gradient, 1 dres = g, 2 dres += g (one rounding).
+template <typename T, int VEC, int MASK, int DRES>
 __global__ __launch_bounds__(kBnThreads) void bn_bwd_apply(
     const T* __restrict__ dy, const T* __restrict__ x, const T* __restrict__ y, int C, int64_t V,
     unsigned cpp, const float* __restrict__ save_mean, const float* __restrict__ fcoef,
@@ -258,7 +259,14 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_apply(
 #pragma unroll
         for (int j = 0; j < VEC; ++j) g[j] = fmaf(xv[j], fsc, fsh) > 0.f ? g[j] : 0.f;
     }
-    if constexpr (DRES) vstore<T, VEC>(dres + i, g);
+    if constexpr (DRES == 1) vstore<T, VEC>(dres + i, g);
+    if constexpr (DRES == 2) {
+        float o[VEC];
+        vload<T, VEC>(dres + i, o);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) o[j] += g[j];
+        vstore<T, VEC>(dres + i, o);
+    }
 #pragma unroll
     for (int j = 0; j < VEC; ++j) xv[j] = k * (g[j] - a - (xv[j] - mean) * b);
     vstore<T, VEC>(dx + i, xv);
@@ -303,7 +311,7 @@ template <typename T, int VEC>
 static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x, const T* y,
                              const float* gamma, const float* save_mean,
                              const float* save_invstd, const float* fwd_coef, T* dx, T* dres,
-                             float* dgamma, float* dbeta, int accumulate, void* ws,
+                             int dres_acc, float* dgamma, float* dbeta, int accumulate, void* ws,
                              hipStream_t st) {
     const BnSlices sl = bn_slices(g);
     float* part = (float*)ws;
@@ -328,16 +336,20 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
     const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads);  // chunks per plane
     const unsigned grid = cpp * (unsigned)(g.N * g.C);
     ProfScope ps("bn_bwd_apply", st, 0.0,
-                 tb * ((mask == kMaskY ? 4 : 3) + (dres ? 1 : 0)));
+                 tb * ((mask == kMaskY ? 4 : 3) + (dres ? (dres_acc ? 2 : 1) : 0)));
 #define RAT3D_BN_BWD(M, D)                                                                 \
     bn_bwd_apply<T, VEC, M, D><<<grid, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, cpp,      \
                                                             save_mean, fwd_coef, coef, dx, dres)
-    if (mask == kMaskY && dres) RAT3D_BN_BWD(kMaskY, true);
-    else if (mask == kMaskY) RAT3D_BN_BWD(kMaskY, false);
-    else if (mask == kMaskX && dres) RAT3D_BN_BWD(kMaskX, true);
-    else if (mask == kMaskX) RAT3D_BN_BWD(kMaskX, false);
-    else if (dres) RAT3D_BN_BWD(kMaskNone, true);
-    else RAT3D_BN_BWD(kMaskNone, false);
+    const int dmode = dres ? (dres_acc ? 2 : 1) : 0;
+    if (mask == kMaskY && dmode == 2) RAT3D_BN_BWD(kMaskY, 2);
+    else if (mask == kMaskY && dmode == 1) RAT3D_BN_BWD(kMaskY, 1);
+    else if (mask == kMaskY) RAT3D_BN_BWD(kMaskY, 0);
+    else if (mask == kMaskX && dmode == 2) RAT3D_BN_BWD(kMaskX, 2);
+    else if (mask == kMaskX && dmode == 1) RAT3D_BN_BWD(kMaskX, 1);
+    else if (mask == kMaskX) RAT3D_BN_BWD(kMaskX, 0);
+    else if (dmode == 2) RAT3D_BN_BWD(kMaskNone, 2);
+    else if (dmode == 1) RAT3D_BN_BWD(kMaskNone, 1);
+    else RAT3D_BN_BWD(kMaskNone, 0);
 #undef RAT3D_BN_BWD
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
@@ -368,23 +380,24 @@ rat3d_status bn_fwd(const BnGeom& g, rat3d_dtype dt, int relu, float eps, float 
 rat3d_status bn_bwd(const BnGeom& g, rat3d_dtype dt, int relu, const void* dy, const void* x,
                     const void* y, const float* gamma, const float* save_mean,
                     const float* save_invstd, const float* fwd_coef, void* dx, void* dres,
-                    float* dgamma, float* dbeta, int accumulate, void* ws, hipStream_t st) {
+                    int dres_acc, float* dgamma, float* dbeta, int accumulate, void* ws,
+                    hipStream_t st) {
     if (dt == RAT3D_BF16) {
         if (g.V % 8 == 0)
             return bn_bwd_t<bf16, 8>(g, relu, (const bf16*)dy, (const bf16*)x, (const bf16*)y,
                                      gamma, save_mean, save_invstd, fwd_coef, (bf16*)dx,
-                                     (bf16*)dres, dgamma, dbeta, accumulate, ws, st);
+                                     (bf16*)dres, dres_acc, dgamma, dbeta, accumulate, ws, st);
         return bn_bwd_t<bf16, 1>(g, relu, (const bf16*)dy, (const bf16*)x, (const bf16*)y, gamma,
-                                 save_mean, save_invstd, fwd_coef, (bf16*)dx, (bf16*)dres, dgamma,
-                                 dbeta, accumulate, ws, st);
+                                 save_mean, save_invstd, fwd_coef, (bf16*)dx, (bf16*)dres,
+                                 dres_acc, dgamma, dbeta, accumulate, ws, st);
     }
     if (g.V % 4 == 0)
         return bn_bwd_t<float, 4>(g, relu, (const float*)dy, (const float*)x, (const float*)y,
                                   gamma, save_mean, save_invstd, fwd_coef, (float*)dx,
-                                  (float*)dres, dgamma, dbeta, accumulate, ws, st);
+                                  (float*)dres, dres_acc, dgamma, dbeta, accumulate, ws, st);
     return bn_bwd_t<float, 1>(g, relu, (const float*)dy, (const float*)x, (const float*)y, gamma,
-                              save_mean, save_invstd, fwd_coef, (float*)dx, (float*)dres, dgamma,
-                              dbeta, accumulate, ws, st);
+                              save_mean, save_invstd, fwd_coef, (float*)dx, (float*)dres,
+                              dres_acc, dgamma, dbeta, accumulate, ws, st);
 }
 
 }  // namespace rat3d

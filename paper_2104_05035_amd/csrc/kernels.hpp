@@ -98,10 +98,13 @@ rat3d_status bn_fwd(const BnGeom& g, rat3d_dtype dt, int relu, float eps, float 
                     float* run_var, float* save_coef, void* ws, hipStream_t st);
 // fwd_coef (may be null): the forward's scale/shift of a BN + ReLU without a
 // residual; the ReLU mask is then recomputed from x and y is not read.
+// dres_acc: the residual gradient is added to dres (one rounding) instead of
+// stored.
 rat3d_status bn_bwd(const BnGeom& g, rat3d_dtype dt, int relu, const void* dy, const void* x,
                     const void* y, const float* gamma, const float* save_mean,
                     const float* save_invstd, const float* fwd_coef, void* dx, void* dres,
-                    float* dgamma, float* dbeta, int accumulate, void* ws, hipStream_t st);
+                    int dres_acc, float* dgamma, float* dbeta, int accumulate, void* ws,
+                    hipStream_t st);
 
 // ---- soft-mask branch (softmask.hip) -----------------------------------
 rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, rat3d_dtype dt,

@@ -304,16 +304,17 @@ struct Exec {
                       a(x), res, par(b.g_off), par(b.b_off), y, mean(b), invstd(b), rmean(b),
                       rvar(b), fcoef(b), bn_scr(), st);
     }
+    // dres_acc: add the residual gradient to dres (one rounding) instead of storing it
     rat3d_status bn_b(const BnL& b, const void* dy, const TRef& x, const void* y, int relu,
-                      void* dx, void* dres) const {
+                      void* dx, void* dres, int dres_acc = 0) const {
         return bn_bwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, relu, dy, a(x), y, par(b.g_off),
-                      mean(b), invstd(b), nullptr, dx, dres, grd(b.g_off), grd(b.b_off), acc,
-                      bn_scr(), st);
+                      mean(b), invstd(b), nullptr, dx, dres, dres_acc, grd(b.g_off),
+                      grd(b.b_off), acc, bn_scr(), st);
     }
     rat3d_status bn_bwd_x(const BnL& b, const void* dy, const TRef& x, void* dx) const {
         return bn_bwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, 1, dy, a(x), nullptr, par(b.g_off),
-                      mean(b), invstd(b), fcoef(b), dx, nullptr, grd(b.g_off), grd(b.b_off), acc,
-                      bn_scr(), st);
+                      mean(b), invstd(b), fcoef(b), dx, nullptr, 0, grd(b.g_off), grd(b.b_off),
+                      acc, bn_scr(), st);
     }
 };
 
@@ -341,8 +342,11 @@ rat3d_status ru_fwd(const Exec& e, const RUPlan& r) {
 rat3d_status ru_bwd(const Exec& e, const RUPlan& r, bool acc_dx, bool need_dx = true) {
     void* dskip = e.p(r.dskip);
     void* dx = need_dx ? e.g(r.x) : nullptr;
-    const bool skip_direct = !r.proj && !acc_dx && need_dx;
-    RAT3D_TRY(e.bn_b(r.b2, e.g(r.y), r.h2, e.a(r.y), 1, e.g(r.h2), skip_direct ? dx : dskip));
+    // identity skip: the skip gradient goes straight into dx (added to the
+    // partial sum already there when acc_dx, one rounding)
+    const bool skip_direct = !r.proj && need_dx;
+    RAT3D_TRY(e.bn_b(r.b2, e.g(r.y), r.h2, e.a(r.y), 1, e.g(r.h2), skip_direct ? dx : dskip,
+                     skip_direct && acc_dx ? 1 : 0));
     RAT3D_TRY(e.conv_d(r.c2, e.g(r.h2), e.g(r.a1), 0));
     RAT3D_TRY(e.conv_w(r.c2, e.a(r.a1), e.g(r.h2)));
     RAT3D_TRY(e.bn_bwd_x(r.b1, e.g(r.a1), r.h1, e.g(r.h1)));
@@ -350,8 +354,6 @@ rat3d_status ru_bwd(const Exec& e, const RUPlan& r, bool acc_dx, bool need_dx = 
         RAT3D_TRY(e.bn_b(r.bp, dskip, r.hp, nullptr, 0, e.g(r.hp), nullptr));
         if (need_dx) RAT3D_TRY(e.conv_d(r.cp, e.g(r.hp), dx, acc_dx ? 1 : 0));
         RAT3D_TRY(e.conv_w(r.cp, e.a(r.x), e.g(r.hp)));
-    } else if (need_dx && acc_dx) {
-        RAT3D_TRY(add_tensors(r.x.s.count(), e.n->dt, dx, dskip, dx, e.st));
     }
     if (need_dx) RAT3D_TRY(e.conv_d(r.c1, e.g(r.h1), dx, 1));
     return e.conv_w(r.c1, e.a(r.x), e.g(r.h1));
