@@ -41,6 +41,38 @@ rat3d_status conv_dgrad(const ConvGeom& g, rat3d_dtype dt, const void* dy, const
     return conv_dgrad_gather(g, dt, dy, w, dx, accumulate, st);
 }
 
+bool conv_uses_prepared(const ConvGeom& g, rat3d_dtype dt, int pass) {
+    if (pass == 0) return !(stem_ok(g, dt)) && brick_fd_ok(g, dt, false);
+    if (pass == 1) return brick_fd_ok(g, dt, true);
+    return false;
+}
+
+size_t conv_prepared_bytes(const ConvGeom& g) {
+    return (size_t)g.Co * g.Ci * g.k * g.k * g.k * 2;
+}
+
+rat3d_status conv_prepare(const ConvGeom& g, rat3d_dtype dt, int pass, const void* w, void* wt,
+                          hipStream_t st) {
+    if (!conv_uses_prepared(g, dt, pass)) return RAT3D_OK;
+    return brick_prep_weights(g, pass == 1, w, wt, st);
+}
+
+rat3d_status conv_fwd_prepared(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* w,
+                               const void* wt, const float* bias, void* y, void* ws,
+                               size_t ws_bytes, hipStream_t st) {
+    if (wt && conv_uses_prepared(g, dt, 0))
+        return conv_fd_brick(g, false, x, wt, bias, y, 0, ws, st, true);
+    return conv_fwd(g, dt, x, w, bias, y, ws, ws_bytes, st);
+}
+
+rat3d_status conv_dgrad_prepared(const ConvGeom& g, rat3d_dtype dt, const void* dy,
+                                 const void* w, const void* wt, void* dx, int accumulate,
+                                 void* ws, size_t ws_bytes, hipStream_t st) {
+    if (wt && conv_uses_prepared(g, dt, 1))
+        return conv_fd_brick(g, true, dy, wt, nullptr, dx, accumulate, ws, st, true);
+    return conv_dgrad(g, dt, dy, w, dx, accumulate, ws, ws_bytes, st);
+}
+
 rat3d_status conv_wgrad(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* dy,
                         float* dw, float* db, int accumulate, void* ws, size_t ws_bytes,
                         hipStream_t st) {

@@ -1338,19 +1338,29 @@ size_t brick_wgrad_ws(const ConvGeom& g) {
     return (size_t)R * (g.Ci / 16) * (g.Co / 64) * kWgPart * sizeof(float);
 }
 
-rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const void* w,
-                           const float* bias, void* dst, int accumulate, void* ws,
-                           hipStream_t st) {
+rat3d_status brick_prep_weights(const ConvGeom& g, bool dgrad, const void* w, void* wt,
+                                hipStream_t st) {
     const int KT = g.k * g.k * g.k;
-    bf16* wt = (bf16*)ws;
     const int64_t wn = (int64_t)g.Co * g.Ci * KT;
     if (dgrad)
         prep_dgrad_weights<<<(unsigned)ceil_div(wn, 256), 256, 0, st>>>((const bf16*)w, g.Co,
-                                                                        g.Ci, KT, wt);
+                                                                        g.Ci, KT, (bf16*)wt);
     else
         prep_fwd_weights<<<(unsigned)ceil_div(wn, 256), 256, 0, st>>>((const bf16*)w, g.Co, g.Ci,
-                                                                      KT, wt);
+                                                                      KT, (bf16*)wt);
     RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
+rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const void* w,
+                           const float* bias, void* dst, int accumulate, void* ws,
+                           hipStream_t st, bool w_prepared) {
+    const bf16* wt = (const bf16*)w;
+    if (!w_prepared) {
+        const rat3d_status s = brick_prep_weights(g, dgrad, w, ws, st);
+        if (s != RAT3D_OK) return s;
+        wt = (const bf16*)ws;
+    }
     if (pw_fd_ok(g, RAT3D_BF16, dgrad))
         return conv_fd_pw(g, dgrad, src, wt, bias, dst, accumulate, st);
     FdArgs a;

@@ -32,6 +32,20 @@ rat3d_status conv_dgrad(const ConvGeom& g, rat3d_dtype dt, const void* dy, const
 rat3d_status conv_wgrad(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* dy,
                         float* dw, float* db, int accumulate, void* ws, size_t ws_bytes,
                         hipStream_t st);
+// Prepared weights: whether the forward (pass 0) or input-gradient (pass 1)
+// kernel of a shape reads a prepared weight layout; the layout's bytes; the
+// preparation; and the two passes taking already prepared weights wt (other
+// shapes ignore wt and use w).
+bool conv_uses_prepared(const ConvGeom& g, rat3d_dtype dt, int pass);
+size_t conv_prepared_bytes(const ConvGeom& g);
+rat3d_status conv_prepare(const ConvGeom& g, rat3d_dtype dt, int pass, const void* w, void* wt,
+                          hipStream_t st);
+rat3d_status conv_fwd_prepared(const ConvGeom& g, rat3d_dtype dt, const void* x, const void* w,
+                               const void* wt, const float* bias, void* y, void* ws,
+                               size_t ws_bytes, hipStream_t st);
+rat3d_status conv_dgrad_prepared(const ConvGeom& g, rat3d_dtype dt, const void* dy,
+                                 const void* w, const void* wt, void* dx, int accumulate,
+                                 void* ws, size_t ws_bytes, hipStream_t st);
 
 // Algorithmic work of one conv pass: 2 * N * Co * Ci * k^3 * Vout flops, and
 // one read of the input and weights plus one write of the output.
@@ -58,9 +72,15 @@ bool brick_fd_ok(const ConvGeom& g, rat3d_dtype dt, bool dgrad);
 bool brick_wgrad_ok(const ConvGeom& g, rat3d_dtype dt);
 size_t brick_fd_ws(const ConvGeom& g);
 size_t brick_wgrad_ws(const ConvGeom& g);
+// w_prepared: w already holds the layout brick_prep_weights writes for this
+// pass (the workspace is then unused); otherwise it is prepared into ws.
 rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const void* w,
                            const float* bias, void* dst, int accumulate, void* ws,
-                           hipStream_t st);
+                           hipStream_t st, bool w_prepared = false);
+// Writes the brick kernels' weight layout of the forward or input-gradient
+// pass (Co * Ci * k^3 bf16 elements) from w [Co][Ci][k^3].
+rat3d_status brick_prep_weights(const ConvGeom& g, bool dgrad, const void* w, void* wt,
+                                hipStream_t st);
 rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, float* dw,
                               int accumulate, void* ws, hipStream_t st);
 

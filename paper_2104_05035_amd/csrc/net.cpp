@@ -45,6 +45,7 @@ struct ConvL {
     ConvGeom g{};
     size_t w_off = 0, b_off = 0;  // parameter-arena offsets (elements)
     bool bias = false;
+    int64_t wt_off[2] = {-1, -1};  // ws bytes: prepared forward / input-gradient weights
 };
 
 struct BnL {
@@ -103,6 +104,7 @@ struct rat3d_net {
     ConvL stem_conv;
     BnL stem_bn;
     int64_t stem_am = 0;
+    std::vector<ConvL> convs;  // every conv layer (weight preparation)
     std::vector<RUPlan> rus;   // RESATTNET: 3 stage units; PARTITION1: 1; RESUNIT: 1
     std::vector<AMPlan> ams;   // RESATTNET: 3; PARTITION1 / ATTN: 1
     ConvL fc;                  // only offsets used (FC weight [2][C], bias [2])
@@ -175,6 +177,12 @@ struct Builder {
             if (b > need) need = b;
         }
         if (need > net->conv_scr_bytes) net->conv_scr_bytes = need;
+        // weights of the brick passes are prepared once per call (they do
+        // not change between micro-batches)
+        for (int pass = 0; pass < 2; ++pass)
+            if (conv_uses_prepared(c.g, net->dt, pass))
+                c.wt_off[pass] = (int64_t)alloc(conv_prepared_bytes(c.g));
+        net->convs.push_back(c);
         return c;
     }
     BnL bn(const std::string& name, int c, Shape s) {
@@ -285,13 +293,16 @@ struct Exec {
     float* rmean(const BnL& b) const { return (float*)(n->ws + n->run_mean_off) + b.run_idx; }
     float* rvar(const BnL& b) const { return (float*)(n->ws + n->run_var_off) + b.run_idx; }
 
+    const void* wt(const ConvL& c, int pass) const {
+        return c.wt_off[pass] >= 0 ? n->ws + c.wt_off[pass] : nullptr;
+    }
     rat3d_status conv_f(const ConvL& c, const void* x, void* y) const {
-        return conv_fwd(c.g, n->dt, x, w(c), c.bias ? par(c.b_off) : nullptr, y, conv_scr(),
-                        n->conv_scr_bytes, st);
+        return conv_fwd_prepared(c.g, n->dt, x, w(c), wt(c, 0), c.bias ? par(c.b_off) : nullptr,
+                                 y, conv_scr(), n->conv_scr_bytes, st);
     }
     rat3d_status conv_d(const ConvL& c, const void* dy, void* dx, int accumulate) const {
-        return conv_dgrad(c.g, n->dt, dy, w(c), dx, accumulate, conv_scr(), n->conv_scr_bytes,
-                          st);
+        return conv_dgrad_prepared(c.g, n->dt, dy, w(c), wt(c, 1), dx, accumulate, conv_scr(),
+                                   n->conv_scr_bytes, st);
     }
     rat3d_status conv_w(const ConvL& c, const void* x, const void* dy) const {
         return conv_wgrad(c.g, n->dt, x, dy, grd(c.w_off), c.bias ? grd(c.b_off) : nullptr, acc,
@@ -446,6 +457,13 @@ rat3d_status prepare_call(rat3d_net* n, hipStream_t st) {
     }
     if (n->dt == RAT3D_BF16)
         RAT3D_TRY(cast_f32_bf16((int64_t)n->param_count, n->P, (bf16*)(n->ws + n->mirror_off), st));
+    for (const ConvL& c : n->convs) {
+        const void* w = n->dt == RAT3D_BF16 ? (const void*)(n->ws + n->mirror_off + c.w_off * 2)
+                                            : (const void*)(n->P + c.w_off);
+        for (int pass = 0; pass < 2; ++pass)
+            if (c.wt_off[pass] >= 0)
+                RAT3D_TRY(conv_prepare(c.g, n->dt, pass, w, n->ws + c.wt_off[pass], st));
+    }
     return RAT3D_OK;
 }
 
