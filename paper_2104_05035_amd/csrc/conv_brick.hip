@@ -137,7 +137,9 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     constexpr uint32_t OB = KS == 1 ? NT * 16 * OCS : 0;
     __shared__ __align__(16) unsigned char lds[2 * BB + OB];
 
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    // wave index made explicitly uniform: values derived from it (weight offsets)
+    // then stay in scalar registers instead of forcing per-lane loops
+    const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const bool consumer = wave < 4;
     const int nchunk = a.Cs >> 5;
     const int HW = a.H * a.W, V = HW * a.D;
@@ -352,16 +354,24 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
 
     // Output epilogue, staged: after a tile's last MFMA the consumers write
     // bf16 results (bias added) into the brick buffer they just finished
-    // reading, in 16-byte units of eight w.  The units of output channel
-    // group cg (16 channels) are numbered i = ((co % 16) * 4 + d) * 16 + h * 2
-    // + half and occupy brick row i / PW, column i % PW, channel slot cg: the
-    // slot that staging item (cg, row, group of the column) writes.  The
-    // producer thread that owns that item stores the unit to global memory
-    // before it stages into the buffer again, so no producer overwrites a unit
-    // another has not drained, and the global stores (and any wait for them)
-    // stay off the consumer waves.
-    constexpr int NUNIT_CG = 16 * kBD * kBH * 2;  // units per channel group
-    static_assert(KS != 3 || NUNIT_CG <= PD * PH * PW, "staged outputs fit the brick");
+    // reading, in 16-byte units of eight w.  Channel group cg (16 channels)
+    // uses channel slot cg; its output rows rho = (d * 8 + h) * 16 + co % 16
+    // (16 w = two units each) are placed so that the producer lanes of one
+    // store instruction hold both units of a row, which makes every global
+    // store cover whole 32-byte row pieces:
+    //   rho < 480        units in brick row rho / 8, columns rho % 8 + 1 and
+    //                    rho % 8 + 9 (the column groups of staging items q = 1
+    //                    and q = 2 of one brick row, same column offset);
+    //   rho = 480 + j    column 0 of brick rows 2j and 2j + 1 (j < 30), or
+    //                    column 17 of brick rows 2(j - 30) and 2(j - 30) + 1.
+    // Each unit sits in a slot that one staging item writes; the producer
+    // thread that owns the item stores the unit to global memory before it
+    // stages into the buffer again, so no producer overwrites a unit another
+    // has not drained, and the global stores (and any wait for them) stay off
+    // the consumer waves.
+    constexpr int kRowsMain = PD * PH * 8;  // rows in columns 1 .. 16
+    static_assert(KS != 3 || (PW == 18 && kRowsMain + PD * PH / 2 + 2 >= 16 * kBD * kBH),
+                  "staged outputs fit the brick");
     const bool staged_epi = !ACC && (a.W & 7) == 0;
     auto write_outputs = [&](int k, unsigned char* buf) {
         const Tile T = tile_of(k);
@@ -388,14 +398,25 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         }
         // opaque per call: keeps the slot arithmetic from being hoisted out of
         // the step loop, where its results would stay live (register pressure)
-        int lane_u = (li * kBD + wd * RD) * kBH * 2 + (kg >> 1);
-        asm volatile("" : "+v"(lane_u));
+        int lane_r = li;
+        asm volatile("" : "+v"(lane_r));
+        const int half = kg >> 1;
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
-            const int i = lane_u + ((r / kBH) * kBH + r % kBH) * 2;
-            const int row = i / PW, ww = i - row * PW;
-            unsigned char* base = buf + (uint32_t)(row * PW + ww) * 64u + (kg & 1) * 8;
-            const int sk = brick_swizzle(ww);
+            const int dh = (wd * RD + r / kBH) * kBH + r % kBH;  // wave-uniform
+            const int rho = dh * 16 + lane_r;
+            int row, col;
+            if (dh * 16 < kRowsMain) {
+                row = rho >> 3;
+                col = (rho & 7) + 1 + 8 * half;
+            } else {
+                const int j = rho - kRowsMain;
+                const bool c0 = j < PD * PH / 2;
+                row = (c0 ? 2 * j : 2 * (j - PD * PH / 2)) + half;
+                col = c0 ? 0 : PW - 1;
+            }
+            unsigned char* base = buf + (uint32_t)(row * PW + col) * 64u + (kg & 1) * 8;
+            const int sk = brick_swizzle(col);
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
                 *reinterpret_cast<uint2*>(base + (((wc * CT + ct) ^ sk) << 4)) = make_uint2(
@@ -425,20 +446,30 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             int pair, q;
             if (!item_of(r, pair, q)) continue;
             const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
-            if (cg * 16 >= NT * 16) continue;
+            if (cg >= NT) continue;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const int ww = 8 * (q + Q0) + e + P;
-                if (ww < 0 || ww >= PW) continue;
-                const int i = row * PW + ww;
-                if (i >= NUNIT_CG) continue;
-                const int half = i & 1, h = (i >> 1) & (kBH - 1), d = (i >> 4) & (kBD - 1);
-                const int co = cg * 16 + (i >> 6);
+                const int col = 8 * (q + Q0) + e + P;
+                if (col < 0 || col >= PW) continue;
+                int rho, half;
+                if (col == 0) {
+                    rho = kRowsMain + (row >> 1);
+                    half = row & 1;
+                } else if (col == PW - 1) {
+                    if (row >= 4) continue;
+                    rho = kRowsMain + PD * PH / 2 + (row >> 1);
+                    half = row & 1;
+                } else {
+                    rho = row * 8 + ((col - 1) & 7);
+                    half = col > 8;
+                }
+                const int li_o = rho & 15, h = (rho >> 4) & (kBH - 1), d = rho >> 7;
                 const uint4 v = *reinterpret_cast<const uint4*>(
-                    buf + (uint32_t)(row * PW) * 64u + brick_slot_off<KS>(ww, cg));
+                    buf + (uint32_t)(row * PW) * 64u + brick_slot_off<KS>(col, cg));
                 const int dd = T.d0 + d, hh = T.h0 + h, w = T.w0 + 8 * half;
                 if (dd < a.D && hh < a.H && w < a.W)
-                    *reinterpret_cast<uint4*>(a.dst + ((int64_t)T.n * a.Ct + T.co0 + co) * V +
+                    *reinterpret_cast<uint4*>(a.dst +
+                                              ((int64_t)T.n * a.Ct + T.co0 + cg * 16 + li_o) * V +
                                               (int64_t)dd * HW + (int64_t)hh * a.W + w) = v;
             }
         }
