@@ -77,6 +77,11 @@ __device__ __forceinline__ void buf_st8(__amdgpu_buffer_rsrc_t r, uint2 v, uint3
     const u32x2 w = {v.x, v.y};
     __builtin_amdgcn_raw_buffer_store_b64(w, r, voff, soff, 0);
 }
+__device__ __forceinline__ void buf_st16(__amdgpu_buffer_rsrc_t r, uint4 v, uint32_t voff,
+                                         uint32_t soff) {
+    const u32x4 w = {v.x, v.y, v.z, v.w};
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, voff, soff, 0);
+}
 
 // Workgroup ids are dealt round-robin over the 8 XCDs; remap them so that
 // XCD x runs the contiguous ids [x * q, (x + 1) * q) of a balanced split

@@ -197,59 +197,67 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         q = it - pair * NQ;
         return it < NIT;
     };
-    auto stage = [&](int k, unsigned char* buf) {
+    // Aligned widths: stage_load issues the loads of a block of the step's
+    // items (registers v, items i0 ..), stage_write transposes them into the
+    // buffer.  The producer stages in blocks of two items after it has
+    // drained the previous tile's outputs (issuing all loads before the drain
+    // measured slower).
+    auto stage_load = [&](int k, auto& v, int i0) {
+        constexpr int NB = sizeof(v) / sizeof(v[0]);
         const Tile T = tile_of(k);
         const int c0 = (k % nchunk) * 32;
-        if ((a.W & 7) == 0) {
-            const __amdgpu_buffer_rsrc_t src_r =
-                buf_rsrc(a.src + (int64_t)T.n * a.Cs * V, (uint32_t)a.Cs * Vb);
-#pragma unroll 1
-            for (int r0 = 0; r0 < NRND; r0 += 2) {
-                uint4 v[2][8];
+        const __amdgpu_buffer_rsrc_t src_r =
+            buf_rsrc(a.src + (int64_t)T.n * a.Cs * V, (uint32_t)a.Cs * Vb);
 #pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    int pair, q;
-                    const bool live = r0 + i < NRND && item_of(r0 + i, pair, q);
-                    const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
-                    const int dd = row / PH, hh = row - dd * PH;
-                    const int d = T.d0 - P + dd, h = T.h0 - P + hh, wg = T.w0 + 8 * (q + Q0);
-                    const bool ok = live && (unsigned)d < (unsigned)a.D &&
-                                    (unsigned)h < (unsigned)a.H && (unsigned)wg < (unsigned)a.W;
-                    // an offset past the buffer end reads zeros (padding)
-                    const uint32_t vo =
-                        ok ? (uint32_t)((cg * 8 * V + d * HW + h * a.W + wg) * 2) : 0x80000000u;
+        for (int ii = 0; ii < NB; ++ii) {
+            int pair, q;
+            const bool live = i0 + ii < NRND && item_of(i0 + ii, pair, q);
+            const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
+            const int dd = row / PH, hh = row - dd * PH;
+            const int d = T.d0 - P + dd, h = T.h0 - P + hh, wg = T.w0 + 8 * (q + Q0);
+            const bool ok = live && (unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H &&
+                            (unsigned)wg < (unsigned)a.W;
+            // an offset past the buffer end reads zeros (padding)
+            const uint32_t vo = ok ? (uint32_t)((cg * 8 * V + d * HW + h * a.W + wg) * 2) : 0x80000000u;
 #pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        v[i][j] = buf_ld16(src_r, vo, (uint32_t)(c0 + j) * Vb);
+            for (int j = 0; j < 8; ++j) v[ii][j] = buf_ld16(src_r, vo, (uint32_t)(c0 + j) * Vb);
+        }
+    };
+    auto stage_write = [&](unsigned char* buf, const auto& v, int i0) {
+        constexpr int NB = sizeof(v) / sizeof(v[0]);
+#pragma unroll
+        for (int ii = 0; ii < NB; ++ii) {
+            int pair, q;
+            if (!(i0 + ii < NRND && item_of(i0 + ii, pair, q))) continue;
+            const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
+            unsigned char* rb = buf + (uint32_t)(row * PW) * 64u;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int ww = 8 * (q + Q0) + e + P;  // brick column
+                if (ww < 0 || ww >= PW) continue;
+                const int wd = e >> 1;
+                uint32_t o[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint32_t wl = wd == 0 ? v[ii][2 * c].x
+                                      : wd == 1 ? v[ii][2 * c].y
+                                      : wd == 2 ? v[ii][2 * c].z : v[ii][2 * c].w;
+                    const uint32_t wh = wd == 0 ? v[ii][2 * c + 1].x
+                                      : wd == 1 ? v[ii][2 * c + 1].y
+                                      : wd == 2 ? v[ii][2 * c + 1].z : v[ii][2 * c + 1].w;
+                    o[c] = (e & 1) ? pack_hi(wl, wh) : pack_lo(wl, wh);
                 }
-#pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    int pair, q;
-                    if (!(r0 + i < NRND && item_of(r0 + i, pair, q))) continue;
-                    const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
-                    unsigned char* rb = buf + (uint32_t)(row * PW) * 64u;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int ww = 8 * (q + Q0) + e + P;  // brick column
-                        if (ww < 0 || ww >= PW) continue;
-                        const int wd = e >> 1;
-                        uint32_t o[4];
-#pragma unroll
-                        for (int c = 0; c < 4; ++c) {
-                            const uint32_t wl = wd == 0 ? v[i][2 * c].x
-                                              : wd == 1 ? v[i][2 * c].y
-                                              : wd == 2 ? v[i][2 * c].z : v[i][2 * c].w;
-                            const uint32_t wh = wd == 0 ? v[i][2 * c + 1].x
-                                              : wd == 1 ? v[i][2 * c + 1].y
-                                              : wd == 2 ? v[i][2 * c + 1].z : v[i][2 * c + 1].w;
-                            o[c] = (e & 1) ? pack_hi(wl, wh) : pack_lo(wl, wh);
-                        }
-                        *reinterpret_cast<uint4*>(rb + brick_slot_off<KS>(ww, cg)) =
-                            make_uint4(o[0], o[1], o[2], o[3]);
-                    }
-                }
+                *reinterpret_cast<uint4*>(rb + brick_slot_off<KS>(ww, cg)) =
+                    make_uint4(o[0], o[1], o[2], o[3]);
             }
-        } else {
+        }
+    };
+    // Widths that are not a multiple of 8: item = (channel group, brick
+    // voxel), voxel fastest, loaded and written in one pass.
+    auto stage_generic = [&](int k, unsigned char* buf) {
+        const Tile T = tile_of(k);
+        const int c0 = (k % nchunk) * 32;
+        {
             // item = (channel group, brick voxel), voxel fastest
             for (int it = ptid; it < NV * 4; it += 256) {
                 const int vox = it % NV, cg = it / NV;
@@ -425,6 +433,57 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             __builtin_amdgcn_sched_barrier(0);  // one row at a time (register pressure)
         }
     };
+    // The units of staging item r: LDS offsets read into v, global byte
+    // offsets (within sample T.n) into go; units outside the tile's valid
+    // range get go = 0x80000000 and are not stored.  The eight LDS reads of an
+    // item are issued together.
+    auto unit_read = [&](const Tile& T, const unsigned char* buf, int r, uint4 (&v)[8],
+                         uint32_t (&go)[8]) {
+        int pair, q;
+        const bool live = item_of(r, pair, q);
+        const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int col = 8 * (q + Q0) + e + P;
+            int rho, half;
+            if (col == 0) {
+                rho = kRowsMain + (row >> 1);
+                half = row & 1;
+            } else if (col == PW - 1) {
+                rho = kRowsMain + PD * PH / 2 + (row >> 1);
+                half = row & 1;
+            } else {
+                rho = row * 8 + ((col - 1) & 7);
+                half = col > 8;
+            }
+            const int li_o = rho & 15, h = (rho >> 4) & (kBH - 1), d = rho >> 7;
+            const int dd = T.d0 + d, hh = T.h0 + h, w = T.w0 + 8 * half;
+            const bool ok = live && cg < NT && col >= 0 && col < PW &&
+                            !(col == PW - 1 && row >= 4) && dd < a.D && hh < a.H && w < a.W;
+            go[e] = ok ? (uint32_t)(((T.co0 + cg * 16 + li_o) * V + dd * HW + hh * a.W + w) * 2)
+                       : 0x80000000u;
+            const uint32_t lo = ok ? (uint32_t)(row * PW) * 64u + brick_slot_off<KS>(col, cg) : 0u;
+            v[e] = *reinterpret_cast<const uint4*>(buf + lo);
+        }
+    };
+    auto dst_rsrc = [&](const Tile& T) {
+        return buf_rsrc(a.dst + (int64_t)T.n * a.Ct * V, (uint32_t)a.Ct * Vb);
+    };
+    auto unit_store = [&](__amdgpu_buffer_rsrc_t dst_r, const uint4 (&v)[8], const uint32_t (&go)[8]) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            if (go[e] != 0x80000000u) buf_st16(dst_r, v[e], go[e], 0u);
+    };
+    auto drain_items = [&](const Tile& T, const unsigned char* buf, int r0, int r1) {
+        const __amdgpu_buffer_rsrc_t dst_r = dst_rsrc(T);
+#pragma unroll 1
+        for (int r = r0; r < r1; ++r) {
+            uint4 v[8];
+            uint32_t go[8];
+            unit_read(T, buf, r, v, go);
+            unit_store(dst_r, v, go);
+        }
+    };
     auto drain = [&](int k, const unsigned char* buf) {
         const Tile T = tile_of(k);
         if constexpr (KS == 1) {
@@ -441,38 +500,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             }
             return;
         }
-#pragma unroll 1
-        for (int r = 0; r < NRND; ++r) {
-            int pair, q;
-            if (!item_of(r, pair, q)) continue;
-            const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
-            if (cg >= NT) continue;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int col = 8 * (q + Q0) + e + P;
-                if (col < 0 || col >= PW) continue;
-                int rho, half;
-                if (col == 0) {
-                    rho = kRowsMain + (row >> 1);
-                    half = row & 1;
-                } else if (col == PW - 1) {
-                    if (row >= 4) continue;
-                    rho = kRowsMain + PD * PH / 2 + (row >> 1);
-                    half = row & 1;
-                } else {
-                    rho = row * 8 + ((col - 1) & 7);
-                    half = col > 8;
-                }
-                const int li_o = rho & 15, h = (rho >> 4) & (kBH - 1), d = rho >> 7;
-                const uint4 v = *reinterpret_cast<const uint4*>(
-                    buf + (uint32_t)(row * PW) * 64u + brick_slot_off<KS>(col, cg));
-                const int dd = T.d0 + d, hh = T.h0 + h, w = T.w0 + 8 * half;
-                if (dd < a.D && hh < a.H && w < a.W)
-                    *reinterpret_cast<uint4*>(a.dst +
-                                              ((int64_t)T.n * a.Ct + T.co0 + cg * 16 + li_o) * V +
-                                              (int64_t)dd * HW + (int64_t)hh * a.W + w) = v;
-            }
-        }
+        drain_items(T, buf, 0, NRND);
     };
     // Accumulating outputs (dst += conv), staged in float32 so that each output
     // is rounded once: the 32 channels of consumer column group wc (CT = 2)
@@ -627,17 +655,58 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             }
         }
     } else {
-        if (S > 0) stage(0, lds);
+        const bool aligned = (a.W & 7) == 0;
+        auto stage_all = [&](int k, unsigned char* buf) {
+            if (!aligned) {
+                stage_generic(k, buf);
+                return;
+            }
+#pragma unroll 1
+            for (int i0 = 0; i0 < NRND; i0 += 2) {
+                uint4 v[2][8];
+                stage_load(k, v, i0);
+                stage_write(buf, v, i0);
+            }
+        };
+        // bf16 epilogue of 3^3 tiles: a tile's drain is split over two steps.
+        // Items 0 .. NE-1 are stored at once; the units of the other items are
+        // read into registers before the buffer is staged again and stored at
+        // the start of the next step.  Every workgroup drains at the same
+        // steps, so this halves the store burst that meets the next staging.
+        constexpr int NE = (NRND + 1) / 2, NL = NRND - NE > 0 ? NRND - NE : 1;
+        const bool split = KS == 3 && staged_epi && NRND > 1;
+        uint4 late_v[NL][8];
+        uint32_t late_go[NL][8];
+        int late_k = -1;
+        auto late_store = [&]() {
+            if (late_k < 0) return;
+            const __amdgpu_buffer_rsrc_t dst_r = dst_rsrc(tile_of(late_k));
+#pragma unroll
+            for (int i = 0; i < NL; ++i) unit_store(dst_r, late_v[i], late_go[i]);
+            late_k = -1;
+        };
+        auto drain_split = [&](int kd, const unsigned char* buf) {
+            const Tile T = tile_of(kd);
+#pragma unroll
+            for (int i = 0; i < NL; ++i) unit_read(T, buf, NE + i, late_v[i], late_go[i]);
+            drain_items(T, buf, 0, NE);
+            late_k = kd;
+        };
+        if (S > 0) stage_all(0, lds);
         lds_barrier();
         for (int k = 0; k < S; ++k) {
+            const bool more = k + 1 < S;
+            if (split) late_store();
             if (k > 0 && tile_end(k - 1)) {
-                if (staged_epi) {
+                if (split) {
+                    drain_split(k - 1, lds + ((k - 1) & 1) * BB);
+                } else if (staged_epi) {
                     drain(k - 1, lds + ((k - 1) & 1) * BB);
                 } else if (staged_acc) {
                     drain_fp32(k - 1, WC - 1, lds + ((k - 1) & 1) * BB);
                 }
             }
-            if (k + 1 < S) stage(k + 1, lds + ((k + 1) & 1) * BB);
+            if (more) stage_all(k + 1, lds + ((k + 1) & 1) * BB);
             if (tile_end(k) && staged_epi) {
                 lds_barrier();
                 lds_barrier();
@@ -655,6 +724,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             }
         }
         if (S > 0) {
+            if (split) late_store();
             if (staged_epi) {
                 drain(S - 1, lds + ((S - 1) & 1) * BB);
             } else if (staged_acc) {
@@ -1306,9 +1376,11 @@ bool brick_fd_ok(const ConvGeom& g, rat3d_dtype dt, bool dgrad) {
     if (dt != RAT3D_BF16 || g.s != 1) return false;
     if (!((g.k == 3 && g.p == 1) || (g.k == 1 && g.p == 0))) return false;
     const int cs = dgrad ? g.Co : g.Ci, ct = dgrad ? g.Ci : g.Co;
-    // one sample's source channels are addressed with 32-bit byte offsets
-    const int64_t src_bytes = (int64_t)cs * g.D * g.H * g.W * 2;
-    return cs % 32 == 0 && ct % 32 == 0 && src_bytes < ((int64_t)1 << 31);
+    // one sample's source and target channels are addressed with 32-bit
+    // byte offsets
+    const int64_t vox_bytes = (int64_t)g.D * g.H * g.W * 2;
+    return cs % 32 == 0 && ct % 32 == 0 && cs * vox_bytes < ((int64_t)1 << 31) &&
+           ct * vox_bytes < ((int64_t)1 << 31);
 }
 
 // Row bands take maps up to 56 columns wide (W a multiple of 4): hb rows of
