@@ -207,7 +207,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         const Tile T = tile_of(k);
         const int c0 = (k % nchunk) * 32;
         const __amdgpu_buffer_rsrc_t src_r =
-            buf_rsrc(a.src + (int64_t)T.n * a.Cs * V, (uint32_t)a.Cs * Vb);
+            buf_rsrc_u(a.src + (int64_t)T.n * a.Cs * V, (uint32_t)a.Cs * Vb);
 #pragma unroll
         for (int ii = 0; ii < NB; ++ii) {
             int pair, q;
@@ -467,7 +467,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         }
     };
     auto dst_rsrc = [&](const Tile& T) {
-        return buf_rsrc(a.dst + (int64_t)T.n * a.Ct * V, (uint32_t)a.Ct * Vb);
+        return buf_rsrc_u(a.dst + (int64_t)T.n * a.Ct * V, (uint32_t)a.Ct * Vb);
     };
     auto unit_store = [&](__amdgpu_buffer_rsrc_t dst_r, const uint4 (&v)[8], const uint32_t (&go)[8]) {
 #pragma unroll
@@ -537,7 +537,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         // units outside the tensor or the group use an offset past the buffer
         // end, which reads zeros and is never stored
         const __amdgpu_buffer_rsrc_t dst_r =
-            buf_rsrc(a.dst + (int64_t)T.n * a.Ct * V, (uint32_t)a.Ct * Vb);
+            buf_rsrc_u(a.dst + (int64_t)T.n * a.Ct * V, (uint32_t)a.Ct * Vb);
         constexpr int RB = 2;  // items per batch (16 old values in flight)
 #pragma unroll
         for (int r0 = 0; r0 < NRND; r0 += RB) {
@@ -1126,7 +1126,7 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
             // the step is wave-uniform; saying so keeps the resource in SGPRs
             const int n = __builtin_amdgcn_readfirstlane(t.n);
             const __amdgpu_buffer_rsrc_t xr =
-                buf_rsrc(a.x + (int64_t)n * a.Ci * V, (uint32_t)(a.Ci * V * 2));
+                buf_rsrc_u(a.x + (int64_t)n * a.Ci * V, (uint32_t)(a.Ci * V * 2));
             const int u = 8 * gi, rr = qdiv(u, a.mWp), col = u - rr * a.Wp;
             const int h = t.h0 - 1 + rr;
             const bool ok = live && (unsigned)z < (unsigned)a.D && (unsigned)h < (unsigned)a.H;
@@ -1159,7 +1159,7 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
         auto ld_dy = [&](const Step& t, bool live, int co, int gi) __attribute__((always_inline)) {
             const int n = __builtin_amdgcn_readfirstlane(t.n);
             const __amdgpu_buffer_rsrc_t yr =
-                buf_rsrc(a.dy + (int64_t)n * a.Co * V, (uint32_t)(a.Co * V * 2));
+                buf_rsrc_u(a.dy + (int64_t)n * a.Co * V, (uint32_t)(a.Co * V * 2));
             const int u = 8 * gi, rr = qdiv(u, a.mWp), col = u - rr * a.Wp;
             const int h = t.h0 + rr;
             const uint32_t o =

@@ -43,6 +43,12 @@ CONV_CASES = [
     (1, 32, 64, 4, 5, 56, 3, 1, 1, False, "bf16"),
     (2, 16, 64, 5, 20, 8, 3, 1, 1, False, "bf16"),
     (1, 64, 64, 1, 12, 16, 3, 1, 1, False, "bf16"),
+    # many short step ranges over shallow volumes: with 256 workgroups a range
+    # holds 3, 7 or 8 planes, so bands begin at every step position of a
+    # range (the first step, the prefetched second and third, and later ones)
+    (192, 16, 64, 4, 1, 4, 3, 1, 1, False, "bf16"),
+    (448, 16, 64, 4, 1, 8, 3, 1, 1, False, "bf16"),
+    (320, 16, 64, 6, 2, 16, 3, 1, 1, False, "bf16"),
     # weight-gradient bricks on maps wider than a band
     (1, 64, 64, 3, 9, 64, 3, 1, 1, False, "bf16"),
     # row bands on widths divisible by 4 but not 8 (half-filled last group of a row)
