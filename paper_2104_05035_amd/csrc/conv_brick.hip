@@ -1182,33 +1182,109 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
             uint32_t m[NXN][6];
             uint4 dy[NDY];
         };
-        // one new plane (d + 1 of step t) and the dy of step t, into registers
-        auto load = [&](const Step& t, Regs& R) __attribute__((always_inline)) {
-            const int pt = ptid_now();
+        // A thread's staging items are the same at every step, so their
+        // element offsets within a sample (x: at plane 0 of a band starting
+        // at row 0; dy: likewise), their LDS offsets and their row / edge
+        // flags are computed once; a step adds its wave-uniform plane and band
+        // offsets.  Flags: bits 0..15 the item's row in the band, 16 live,
+        // 17 a left neighbour exists, 18 a right neighbour exists, 19 eight
+        // whole voxels (else four).
+        uint32_t xo[NXN], xl[NXN], xf[NXN], yo[NDY], yl[NDY], yf[NDY];
+        {
+            const int pt = tid - 256;
 #pragma unroll
             for (int q = 0; q < NXN; ++q) {
-                const int it = pt + 256 * q, ci = qdiv(it, a.mXG);
-                ld_x(t, it < 16 * XG, ci, t.d + 1, it - ci * XG, R.m[q]);
+                const int it = pt + 256 * q;
+                const bool live = it < 16 * XG;
+                const int ci = live ? qdiv(it, a.mXG) : 0, gi = live ? it - ci * XG : 0;
+                const int u = 8 * gi, rr = qdiv(u, a.mWp), col = u - rr * a.Wp;
+                xo[q] = (uint32_t)(ci0 + ci) * (uint32_t)V + (uint32_t)(rr * a.W + col);
+                xl[q] = (uint32_t)(ci * a.cis + gi * 16);
+                xf[q] = (uint32_t)rr | (live ? 1u << 16 : 0u) | (col > 0 ? 1u << 17 : 0u) |
+                        (col + 8 < a.W ? 1u << 18 : 0u) | (col + 8 <= a.W ? 1u << 19 : 0u);
             }
 #pragma unroll
             for (int q = 0; q < NDY; ++q) {
-                const int it = pt + 256 * q, co = qdiv(it, a.mYG);
-                R.dy[q] = ld_dy(t, it < 64 * YG, co, it - co * YG);
+                const int it = pt + 256 * q;
+                const bool live = it < 64 * YG;
+                const int co = live ? qdiv(it, a.mYG) : 0, gi = live ? it - co * YG : 0;
+                const int u = 8 * gi, rr = qdiv(u, a.mWp), col = u - rr * a.Wp;
+                yo[q] = (uint32_t)(co0 + co) * (uint32_t)V + (uint32_t)(rr * a.W + col);
+                yl[q] = (uint32_t)(co * kBandDys + gi * 16);
+                yf[q] = (uint32_t)rr | (live ? 1u << 16 : 0u) | (col + 8 <= a.W ? 1u << 19 : 0u);
+            }
+        }
+        // one new plane (d + 1 of step t) and the dy of step t, into registers
+        auto load = [&](const Step& t, Regs& R) __attribute__((always_inline)) {
+            const int n = __builtin_amdgcn_readfirstlane(t.n);
+            const __amdgpu_buffer_rsrc_t xr =
+                buf_rsrc_u(a.x + (int64_t)n * a.Ci * V, (uint32_t)(a.Ci * V * 2));
+            const __amdgpu_buffer_rsrc_t yr =
+                buf_rsrc_u(a.dy + (int64_t)n * a.Co * V, (uint32_t)(a.Co * V * 2));
+            const int z = t.d + 1;
+            const bool zok = (unsigned)z < (unsigned)a.D;
+            // uniform parts (the band's first x row is h0 - 1; unsigned wrap-around
+            // cancels against the item's row term)
+            const uint32_t xb = (uint32_t)(z * HW) + (uint32_t)((t.h0 - 1) * a.W);
+            const uint32_t yb = (uint32_t)(t.d * HW) + (uint32_t)(t.h0 * a.W);
+            const int hy = a.H - t.h0;  // dy rows left in the map
+#pragma unroll
+            for (int q = 0; q < NXN; ++q) {
+                const uint32_t f = xf[q];
+                const int rr = (int)(f & 0xffffu);
+                const bool ok = (f & (1u << 16)) && zok && (unsigned)(rr - 1 + t.h0) < (unsigned)a.H;
+                const uint32_t o = ok ? (xo[q] + xb) * 2u : 0x80000000u;
+                uint32_t* m = R.m[q];
+                if constexpr (PART) {
+                    const bool full = f & (1u << 19);
+                    const uint4 v = buf_ld16(xr, full ? o : 0x80000000u, 0);
+                    const uint2 w = buf_ld8(xr, full ? 0x80000000u : o, 0);
+                    m[1] = v.x | w.x; m[2] = v.y | w.y; m[3] = v.z; m[4] = v.w;
+                } else {
+                    const uint4 v = buf_ld16(xr, o, 0);
+                    m[1] = v.x; m[2] = v.y; m[3] = v.z; m[4] = v.w;
+                }
+                m[0] = buf_ld2(xr, ok && (f & (1u << 17)) ? o - 2u : 0x80000000u, 0) << 16;
+                m[5] = buf_ld2(xr, ok && (f & (1u << 18)) ? o + 16u : 0x80000000u, 0);
+            }
+#pragma unroll
+            for (int q = 0; q < NDY; ++q) {
+                const uint32_t f = yf[q];
+                const int rr = (int)(f & 0xffffu);
+                const bool ok = (f & (1u << 16)) && rr < hy;
+                const uint32_t o = ok ? (yo[q] + yb) * 2u : 0x80000000u;
+                if constexpr (PART) {
+                    const bool full = f & (1u << 19);
+                    uint4 v = buf_ld16(yr, full ? o : 0x80000000u, 0);
+                    const uint2 w = buf_ld8(yr, full ? 0x80000000u : o, 0);
+                    v.x |= w.x;
+                    v.y |= w.y;
+                    R.dy[q] = v;
+                } else {
+                    R.dy[q] = buf_ld16(yr, o, 0);
+                }
             }
         };
         auto commit = [&](const Step& t, const Regs& R, unsigned char* db) __attribute__((always_inline)) {
-            const int pt = ptid_now();
+            unsigned char* xb = xs + slot_of(t.d + 1) * a.sls;
 #pragma unroll
             for (int q = 0; q < NXN; ++q) {
-                const int it = pt + 256 * q, ci = qdiv(it, a.mXG);
-                if (it < 16 * XG) st_x(ci, t.d + 1, it - ci * XG, R.m[q]);
+                if (!(xf[q] & (1u << 16))) continue;
+                const uint32_t* m = R.m[q];
+                unsigned char* base = xb + xl[q];
+                uint32_t s0[4], s2[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    s0[i] = __builtin_amdgcn_alignbit(m[i + 1], m[i], 16);
+                    s2[i] = __builtin_amdgcn_alignbit(m[i + 2], m[i + 1], 16);
+                }
+                *reinterpret_cast<uint4*>(base) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
+                *reinterpret_cast<uint4*>(base + KWS) = make_uint4(m[1], m[2], m[3], m[4]);
+                *reinterpret_cast<uint4*>(base + 2 * KWS) = make_uint4(s2[0], s2[1], s2[2], s2[3]);
             }
 #pragma unroll
-            for (int q = 0; q < NDY; ++q) {
-                const int it = pt + 256 * q, co = qdiv(it, a.mYG);
-                if (it < 64 * YG)
-                    *reinterpret_cast<uint4*>(db + co * kBandDys + (it - co * YG) * 16) = R.dy[q];
-            }
+            for (int q = 0; q < NDY; ++q)
+                if (yf[q] & (1u << 16)) *reinterpret_cast<uint4*>(db + yl[q]) = R.dy[q];
         };
         // first step of a range or band: planes d - 1 .. d + 1 and dy, synchronously
         auto stage_full = [&](const Step& t, unsigned char* db) __attribute__((always_inline)) {
