@@ -322,6 +322,11 @@ rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labe
  * its pending events.  Not for use while another thread launches work.
  * ------------------------------------------------------------------------ */
 rat3d_status rat3d_profile_enable(int enable);
+/* Restricts the brackets to launches whose tag equals `tag` (a copy is kept);
+ * NULL or "" brackets every tagged launch again.  Other launches record no
+ * events and add nothing, so one kernel can be timed inside a region without
+ * an event pair around every other launch. */
+rat3d_status rat3d_profile_filter(const char* tag);
 rat3d_status rat3d_profile_reset(void);
 int rat3d_profile_count(void);
 rat3d_status rat3d_profile_read(int i, const char** name, int64_t* launches, double* total_ms,

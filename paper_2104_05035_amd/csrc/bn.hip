@@ -9,6 +9,10 @@
 // Backward: (1) per (channel, slice) partial sums of g and g * (x - mean),
 //           g = dy masked by y > 0; (2) per channel dbeta, dgamma and the
 //           apply coefficients; (3) dx = k * (g - dbeta/M - xhat * dgamma/M),
+// Step (2) runs at the start of every block of step (3): each block combines
+// its channel's partials itself (the same fixed order everywhere, so every
+// block gets the same coefficients) and one block per channel stores the
+// per-channel outputs -- no separate per-channel kernel between the passes.
 //           dresidual = g (or dresidual += g, one rounding).  Without a residual, y > 0 is the same test as
 //           x * scale + shift > 0 with the forward's own float coefficients
 //           (the apply computes exactly that value before the max with 0), so
@@ -18,6 +22,8 @@
 // channel's partials are the N * SP segment sums of its planes, combined in
 // a fixed order.  Everything is HBM-bound: loads and stores are 16-byte
 // vectors when V allows.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "vec.hpp"
@@ -26,6 +32,12 @@
 namespace rat3d {
 
 constexpr int kBnThreads = 256;
+constexpr int kStatsUnroll = 4;  // vectors per tensor in flight per thread in the statistics passes
+// vectors per thread in the apply passes (measured: only the two-stream
+// forward apply, which has the least work per wave to hide its coefficient
+// reduction behind, gains from more than one)
+template <bool RES> constexpr int fwd_apply_u() { return RES ? 1 : 4; }
+constexpr int kBwdApplyU = 1;
 
 struct BnSlices {
     int per_plane;    // segments per (n, c) plane
@@ -34,8 +46,10 @@ struct BnSlices {
 };
 
 static BnSlices bn_slices(const BnGeom& g) {
-    int64_t want = ceil_div(2048, (int64_t)g.C * g.N);  // aim for ~2048 blocks in total
-    int64_t by_size = ceil_div(g.V, 16384);              // at least ~16K elements per segment
+    // many short segments stream faster than a few long ones (measured on
+    // 264 MB reads): aim for ~16K blocks of at least ~8K elements
+    int64_t want = ceil_div(16384, (int64_t)g.C * g.N);
+    int64_t by_size = ceil_div(g.V, 8192);
     int64_t s = want < by_size ? want : by_size;
     if (s < 1) s = 1;
     int64_t len = ceil_div(g.V, s);
@@ -46,8 +60,8 @@ static BnSlices bn_slices(const BnGeom& g) {
 
 size_t bn_ws_bytes(const BnGeom& g) {
     const BnSlices sl = bn_slices(g);
-    // partial pairs (2 floats per slice) + 4 floats of coefficients per channel
-    return ((size_t)g.C * sl.per_channel * 2 + (size_t)g.C * 4) * sizeof(float);
+    // partial pairs (2 floats per slice) + the forward's shift per channel
+    return ((size_t)g.C * sl.per_channel * 2 + (size_t)g.C) * sizeof(float);
 }
 
 // Block reduction of two floats; result valid in thread 0.
@@ -79,14 +93,25 @@ __global__ __launch_bounds__(kBnThreads) void bn_fwd_stats(const T* __restrict__
     const int64_t cnt = (beg + len < V ? beg + len : V) - beg;
     const T* p = x + ((int64_t)n * C + c) * V + beg;
     float s1 = 0.f, s2 = 0.f;
-    for (int64_t e = (int64_t)threadIdx.x * VEC; e < cnt; e += (int64_t)kBnThreads * VEC) {
-        float v[VEC];
-        vload<T, VEC>(p + e, v);
+    constexpr int64_t kStep = (int64_t)kBnThreads * VEC;
+    // kStatsUnroll vectors in flight per thread; vectors past the segment end
+    // load its last vector (clamped address, cnt % VEC == 0) and add nothing
+    for (int64_t e = (int64_t)threadIdx.x * VEC; e < cnt; e += kStatsUnroll * kStep) {
+        float v[kStatsUnroll][VEC];
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) {
-            const float d = v[j] - shift;
-            s1 += d;
-            s2 += d * d;
+        for (int u = 0; u < kStatsUnroll; ++u) {
+            const int64_t eu = e + u * kStep;
+            vload<T, VEC>(p + (eu < cnt ? eu : cnt - VEC), v[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kStatsUnroll; ++u) {
+            const bool in = e + u * kStep < cnt;
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) {
+                const float d = in ? v[u][j] - shift : 0.f;
+                s1 += d;
+                s2 += d * d;
+            }
         }
     }
     block_sum2(s1, s2);
@@ -94,37 +119,72 @@ __global__ __launch_bounds__(kBnThreads) void bn_fwd_stats(const T* __restrict__
         float* o = part + ((int64_t)c * gridDim.y + sidx) * 2;
         o[0] = s1;
         o[1] = s2;
+        // the shift, kept beside the partials so the apply never reads x for
+        // it (x may be overwritten by an in-place apply)
+        if (sidx == 0) part[(int64_t)C * gridDim.y * 2 + c] = shift;
     }
 }
 
-// One thread per channel: combine slice partials (fixed order, float64).
-template <typename T>
-__global__ void bn_fwd_finalize(const T* __restrict__ x, int N, int C, int64_t V, int slices,
-                                const float* __restrict__ part, const float* __restrict__ gamma,
-                                const float* __restrict__ beta, float eps, float momentum,
-                                float* __restrict__ save_mean, float* __restrict__ save_invstd,
-                                float* __restrict__ run_mean, float* __restrict__ run_var,
-                                float* __restrict__ coef, float* __restrict__ save_coef) {
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
-    const double shift = (double)Elt<T>::ld(x + (int64_t)c * V);
-    double s1 = 0.0, s2 = 0.0;
-    for (int i = 0; i < slices; ++i) {
-        s1 += (double)part[((int64_t)c * slices + i) * 2];
-        s2 += (double)part[((int64_t)c * slices + i) * 2 + 1];
+// Sums the slice partial pairs of channel c in float64 in a fixed order:
+// lane l adds slices l, l + 64, ... in turn, then an xor butterfly over the
+// wave; every lane of every wave ends with the same bits (each butterfly
+// level adds the same pairs of values, and float addition commutes).  All
+// 64 lanes must be active.
+__device__ __forceinline__ void wave_sum_partials(const float* __restrict__ part, int c,
+                                                  int slices, double& s1, double& s2) {
+    const int lane = (int)(threadIdx.x & 63);
+    const float2* pc = reinterpret_cast<const float2*>(part + (int64_t)c * slices * 2);
+    double a = 0.0, b = 0.0;
+    // four loads in flight per lane; slices past the end add nothing
+    for (int i = lane; i < slices; i += 256) {
+        float2 q[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) q[u] = pc[i + 64 * u < slices ? i + 64 * u : i];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const bool in = i + 64 * u < slices;
+            a += in ? (double)q[u].x : 0.0;
+            b += in ? (double)q[u].y : 0.0;
+        }
     }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        a += __shfl_xor(a, m, 64);
+        b += __shfl_xor(b, m, 64);
+    }
+    s1 = a;
+    s2 = b;
+}
+
+// Per channel: combine the slice partials in a fixed order in float64 into
+// the apply coefficients (scale, shift).  Every apply block of the channel
+// evaluates this identically; the block given `owner` also stores mean,
+// invstd, the coefficients and the running statistics.
+__device__ __forceinline__ void bn_fwd_coefs(int N, int C, int64_t V,
+                                             int slices, int c, const float* __restrict__ part,
+                                             const float* __restrict__ gamma,
+                                             const float* __restrict__ beta, float eps,
+                                             float momentum, bool owner,
+                                             float* __restrict__ save_mean,
+                                             float* __restrict__ save_invstd,
+                                             float* __restrict__ run_mean,
+                                             float* __restrict__ run_var,
+                                             float* __restrict__ save_coef, float& scale,
+                                             float& bias) {
+    const double shift = (double)part[(int64_t)C * slices * 2 + c];
+    double s1, s2;
+    wave_sum_partials(part, c, slices, s1, s2);
     const double M = (double)N * (double)V;
     const double dm = s1 / M;
     double var = s2 / M - dm * dm;
     if (var < 0.0) var = 0.0;
     const double mean = shift + dm;
     const double invstd = 1.0 / sqrt(var + (double)eps);
+    scale = (float)((double)gamma[c] * invstd);
+    bias = (float)((double)beta[c] - mean * (double)scale);
+    if (!owner) return;
     save_mean[c] = (float)mean;
     save_invstd[c] = (float)invstd;
-    const float scale = (float)((double)gamma[c] * invstd);
-    const float bias = (float)((double)beta[c] - mean * (double)scale);
-    coef[c] = scale;
-    coef[C + c] = bias;
     if (save_coef) {
         save_coef[c] = scale;
         save_coef[C + c] = bias;
@@ -136,31 +196,59 @@ __global__ void bn_fwd_finalize(const T* __restrict__ x, int N, int C, int64_t V
     }
 }
 
-// One-dimensional grid: block b covers chunk b % cpp of plane b / cpp.
+struct BnFwdStats {
+    const float* part;
+    int slices;
+    const float* gamma;
+    const float* beta;
+    float eps, momentum;
+    float *save_mean, *save_invstd, *run_mean, *run_var, *save_coef;
+};
+
+// One-dimensional grid: block b covers chunk b % cpp of plane b / cpp.  The
+// block first loads its elements, then derives its channel's coefficients
+// from the statistics partials (the first chunk of plane (0, c) stores them).
 template <typename T, int VEC, bool RELU, bool RES>
 __global__ __launch_bounds__(kBnThreads) void bn_fwd_apply(const T* __restrict__ x,
-                                                           const T* __restrict__ r, int C,
+                                                           const T* __restrict__ r, int N, int C,
                                                            int64_t V, unsigned cpp,
-                                                           const float* __restrict__ coef,
-                                                           T* __restrict__ y) {
+                                                           BnFwdStats st, T* __restrict__ y) {
+    constexpr int U = fwd_apply_u<RES>();
+    constexpr int64_t kStep = (int64_t)kBnThreads * VEC;
     const int plane = (int)(blockIdx.x / cpp);  // wave-uniform
-    const int64_t e = ((int64_t)(blockIdx.x - (unsigned)plane * cpp) * kBnThreads + threadIdx.x) * VEC;
-    if (e >= V) return;
+    const unsigned chunk = blockIdx.x - (unsigned)plane * cpp;
+    const int64_t e0 = (int64_t)chunk * kStep * U + (int64_t)threadIdx.x * VEC;
     const int c = plane % C;
-    const int64_t i = (int64_t)plane * V + e;
-    const float sc = coef[c], sh = coef[C + c];
-    float v[VEC];
-    vload<T, VEC>(x + i, v);
-    float rv[VEC];
-    if constexpr (RES) vload<T, VEC>(r + i, rv);
+    const int64_t base = (int64_t)plane * V;
+    // every vector is loaded before the coefficients are formed; vectors past
+    // the end load the plane's last vector (V % VEC == 0), so every lane takes
+    // part in the coefficient reduction, and store nothing
+    float v[U][VEC];
+    [[maybe_unused]] float rv[U][VEC];
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) {
-        float o = fmaf(v[j], sc, sh);
-        if constexpr (RES) o += rv[j];
-        if constexpr (RELU) o = fmaxf(o, 0.f);
-        v[j] = o;
+    for (int u = 0; u < U; ++u) {
+        const int64_t e = e0 + u * kStep;
+        const int64_t i = base + (e < V ? e : V - VEC);
+        vload<T, VEC>(x + i, v[u]);
+        if constexpr (RES) vload<T, VEC>(r + i, rv[u]);
     }
-    vstore<T, VEC>(y + i, v);
+    float sc, sh;
+    bn_fwd_coefs(N, C, V, st.slices, c, st.part, st.gamma, st.beta, st.eps, st.momentum,
+                 plane < C && chunk == 0 && threadIdx.x == 0, st.save_mean, st.save_invstd,
+                 st.run_mean, st.run_var, st.save_coef, sc, sh);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t e = e0 + u * kStep;
+        if (e >= V) break;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            float o = fmaf(v[u][j], sc, sh);
+            if constexpr (RES) o += rv[u][j];
+            if constexpr (RELU) o = fmaxf(o, 0.f);
+            v[u][j] = o;
+        }
+        vstore<T, VEC>(y + base + e, v[u]);
+    }
 }
 
 // ReLU mask of the backward: none, y > 0, or x * scale + shift > 0.
@@ -182,24 +270,38 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_stats(const T* __restrict__
     const int64_t cnt = (beg + len < V ? beg + len : V) - beg;
     const int64_t base = ((int64_t)n * C + c) * V + beg;
     float s1 = 0.f, s2 = 0.f;
-    for (int64_t e = (int64_t)threadIdx.x * VEC; e < cnt; e += (int64_t)kBnThreads * VEC) {
-        const int64_t idx = base + e;
-        float g[VEC], xv[VEC];
-        vload<T, VEC>(dy + idx, g);
-        vload<T, VEC>(x + idx, xv);
-        if constexpr (MASK == kMaskY) {
-            float yv[VEC];
-            vload<T, VEC>(y + idx, yv);
+    // kStatsUnroll vectors of each tensor in flight per thread, all loads
+    // issued before any is used; past the segment end the last vector is
+    // loaded (clamped) and adds nothing
+    constexpr int64_t kStep = (int64_t)kBnThreads * VEC;
+    constexpr int U = kStatsUnroll;
+    for (int64_t e = (int64_t)threadIdx.x * VEC; e < cnt; e += U * kStep) {
+        float g[U][VEC], xv[U][VEC];
+        [[maybe_unused]] float yv[U][VEC];
 #pragma unroll
-            for (int j = 0; j < VEC; ++j) g[j] = yv[j] > 0.f ? g[j] : 0.f;
-        } else if constexpr (MASK == kMaskX) {
-#pragma unroll
-            for (int j = 0; j < VEC; ++j) g[j] = fmaf(xv[j], fsc, fsh) > 0.f ? g[j] : 0.f;
+        for (int u = 0; u < U; ++u) {
+            const int64_t eu = e + u * kStep;
+            const int64_t idx = base + (eu < cnt ? eu : cnt - VEC);
+            vload<T, VEC>(dy + idx, g[u]);
+            vload<T, VEC>(x + idx, xv[u]);
+            if constexpr (MASK == kMaskY) vload<T, VEC>(y + idx, yv[u]);
         }
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) {
-            s1 += g[j];
-            s2 += g[j] * (xv[j] - mean);
+        for (int u = 0; u < U; ++u) {
+            const bool in = e + u * kStep < cnt;
+            if constexpr (MASK == kMaskY) {
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) g[u][j] = yv[u][j] > 0.f ? g[u][j] : 0.f;
+            } else if constexpr (MASK == kMaskX) {
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) g[u][j] = fmaf(xv[u][j], fsc, fsh) > 0.f ? g[u][j] : 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) {
+                const float gj = in ? g[u][j] : 0.f;
+                s1 += gj;
+                s2 += gj * (xv[u][j] - mean);
+            }
         }
     }
     block_sum2(s1, s2);
@@ -210,66 +312,88 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_stats(const T* __restrict__
     }
 }
 
-__global__ void bn_bwd_finalize(int N, int C, int64_t V, int slices,
-                                const float* __restrict__ part, const float* __restrict__ gamma,
-                                const float* __restrict__ save_invstd,
-                                float* __restrict__ dgamma, float* __restrict__ dbeta,
-                                int accumulate, float* __restrict__ coef) {
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
-    double s1 = 0.0, s2 = 0.0;
-    for (int i = 0; i < slices; ++i) {
-        s1 += (double)part[((int64_t)c * slices + i) * 2];
-        s2 += (double)part[((int64_t)c * slices + i) * 2 + 1];
-    }
-    const double invstd = save_invstd[c];
+struct BnBwdStats {
+    const float* part;
+    int slices;
+    const float* gamma;
+    const float* save_invstd;
+    float *dgamma, *dbeta;
+    int accumulate;
+};
+
+// Per channel: dbeta, dgamma and the apply coefficients from the slice
+// partials (fixed order, float64).  Every apply block of the channel
+// evaluates this identically; the block given `owner` stores dgamma, dbeta.
+__device__ __forceinline__ void bn_bwd_coefs(int N, int64_t V, int c, const BnBwdStats& st,
+                                             bool owner, float& k, float& a, float& b) {
+    double s1, s2;
+    wave_sum_partials(st.part, c, st.slices, s1, s2);
+    const double invstd = st.save_invstd[c];
     const double db = s1, dg = s2 * invstd;
-    dbeta[c] = (float)(accumulate ? (double)dbeta[c] + db : db);
-    dgamma[c] = (float)(accumulate ? (double)dgamma[c] + dg : dg);
+    if (owner) {
+        st.dbeta[c] = (float)(st.accumulate ? (double)st.dbeta[c] + db : db);
+        st.dgamma[c] = (float)(st.accumulate ? (double)st.dgamma[c] + dg : dg);
+    }
     const double M = (double)N * (double)V;
     // dx = k * (g - db/M - (x - mean) * invstd * dg/M)
-    const double k = (double)gamma[c] * invstd;
-    coef[c] = (float)k;
-    coef[C + c] = (float)(db / M);
-    coef[2 * C + c] = (float)(invstd * dg / M);
+    k = (float)((double)st.gamma[c] * invstd);
+    a = (float)(db / M);
+    b = (float)(invstd * dg / M);
 }
 
 // DRES: 0 no residual gradient, 1 dres = g, 2 dres += g (one rounding).
 template <typename T, int VEC, int MASK, int DRES>
 __global__ __launch_bounds__(kBnThreads) void bn_bwd_apply(
-    const T* __restrict__ dy, const T* __restrict__ x, const T* __restrict__ y, int C, int64_t V,
-    unsigned cpp, const float* __restrict__ save_mean, const float* __restrict__ fcoef,
-    const float* __restrict__ coef, T* __restrict__ dx, T* __restrict__ dres) {
+    const T* __restrict__ dy, const T* __restrict__ x, const T* __restrict__ y, int N, int C,
+    int64_t V, unsigned cpp, const float* __restrict__ save_mean, const float* __restrict__ fcoef,
+    BnBwdStats st, T* __restrict__ dx, T* __restrict__ dres) {
+    constexpr int U = kBwdApplyU;
+    constexpr int64_t kStep = (int64_t)kBnThreads * VEC;
     const int plane = (int)(blockIdx.x / cpp);  // wave-uniform
-    const int64_t e = ((int64_t)(blockIdx.x - (unsigned)plane * cpp) * kBnThreads + threadIdx.x) * VEC;
-    if (e >= V) return;
+    const unsigned chunk = blockIdx.x - (unsigned)plane * cpp;
+    const int64_t e0 = (int64_t)chunk * kStep * U + (int64_t)threadIdx.x * VEC;
     const int c = plane % C;
-    const int64_t i = (int64_t)plane * V + e;
-    const float k = coef[c], a = coef[C + c], b = coef[2 * C + c], mean = save_mean[c];
-    float g[VEC], xv[VEC];
-    vload<T, VEC>(dy + i, g);
-    vload<T, VEC>(x + i, xv);
-    if constexpr (MASK == kMaskY) {
-        float yv[VEC];
-        vload<T, VEC>(y + i, yv);
+    const int64_t base = (int64_t)plane * V;
+    // as in the forward apply: every load first (clamped), every lane in the
+    // coefficient reduction
+    float g[U][VEC], xv[U][VEC];
+    [[maybe_unused]] float yv[U][VEC], ov[U][VEC];
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) g[j] = yv[j] > 0.f ? g[j] : 0.f;
-    } else if constexpr (MASK == kMaskX) {
-        const float fsc = fcoef[c], fsh = fcoef[C + c];
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) g[j] = fmaf(xv[j], fsc, fsh) > 0.f ? g[j] : 0.f;
+    for (int u = 0; u < U; ++u) {
+        const int64_t e = e0 + u * kStep;
+        const int64_t i = base + (e < V ? e : V - VEC);
+        vload<T, VEC>(dy + i, g[u]);
+        vload<T, VEC>(x + i, xv[u]);
+        if constexpr (MASK == kMaskY) vload<T, VEC>(y + i, yv[u]);
+        if constexpr (DRES == 2) vload<T, VEC>(dres + i, ov[u]);
     }
-    if constexpr (DRES == 1) vstore<T, VEC>(dres + i, g);
-    if constexpr (DRES == 2) {
-        float o[VEC];
-        vload<T, VEC>(dres + i, o);
+    float k, a, b;
+    bn_bwd_coefs(N, V, c, st, plane < C && chunk == 0 && threadIdx.x == 0, k, a, b);
+    const float mean = save_mean[c];
+    [[maybe_unused]] const float fsc = MASK == kMaskX ? fcoef[c] : 0.f;
+    [[maybe_unused]] const float fsh = MASK == kMaskX ? fcoef[C + c] : 0.f;
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) o[j] += g[j];
-        vstore<T, VEC>(dres + i, o);
+    for (int u = 0; u < U; ++u) {
+        const int64_t e = e0 + u * kStep;
+        if (e >= V) break;
+        const int64_t i = base + e;
+        if constexpr (MASK == kMaskY) {
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) g[u][j] = yv[u][j] > 0.f ? g[u][j] : 0.f;
+        } else if constexpr (MASK == kMaskX) {
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) g[u][j] = fmaf(xv[u][j], fsc, fsh) > 0.f ? g[u][j] : 0.f;
+        }
+        if constexpr (DRES == 1) vstore<T, VEC>(dres + i, g[u]);
+        if constexpr (DRES == 2) {
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) ov[u][j] += g[u][j];
+            vstore<T, VEC>(dres + i, ov[u]);
+        }
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) xv[u][j] = k * (g[u][j] - a - (xv[u][j] - mean) * b);
+        vstore<T, VEC>(dx + i, xv[u]);
     }
-#pragma unroll
-    for (int j = 0; j < VEC; ++j) xv[j] = k * (g[j] - a - (xv[j] - mean) * b);
-    vstore<T, VEC>(dx + i, xv);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -280,7 +404,6 @@ static rat3d_status bn_fwd_t(const BnGeom& g, int relu, float eps, float momentu
                              float* run_var, float* save_coef, void* ws, hipStream_t st) {
     const BnSlices sl = bn_slices(g);
     float* part = (float*)ws;
-    float* coef = part + (size_t)g.C * sl.per_channel * 2;
     const double tb = (double)g.N * g.C * g.V * sizeof(T);
     {
     ProfScope ps("bn_fwd_stats", st, 0.0, tb);
@@ -288,21 +411,20 @@ static rat3d_status bn_fwd_t(const BnGeom& g, int relu, float eps, float momentu
         x, g.C, g.V, sl.per_plane, sl.len, part);
     RAT3D_LAUNCH_CHECK();
     }
-    bn_fwd_finalize<T><<<(unsigned)ceil_div(g.C, 64), 64, 0, st>>>(
-        x, g.N, g.C, g.V, sl.per_channel, part, gamma, beta, eps, momentum, save_mean,
-        save_invstd, run_mean, run_var, coef, save_coef);
-    RAT3D_LAUNCH_CHECK();
-    const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads);  // chunks per plane
+    const BnFwdStats fs{part,     sl.per_channel, gamma,   beta,   eps,      momentum,
+                        save_mean, save_invstd,   run_mean, run_var, save_coef};
+    const int fu = r ? fwd_apply_u<true>() : fwd_apply_u<false>();
+    const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads * fu);  // chunks per plane
     const unsigned grid = cpp * (unsigned)(g.N * g.C);
     ProfScope ps("bn_fwd_apply", st, 0.0, tb * (r ? 3 : 2));
     if (relu && r)
-        bn_fwd_apply<T, VEC, true, true><<<grid, kBnThreads, 0, st>>>(x, r, g.C, g.V, cpp, coef, y);
+        bn_fwd_apply<T, VEC, true, true><<<grid, kBnThreads, 0, st>>>(x, r, g.N, g.C, g.V, cpp, fs, y);
     else if (relu)
-        bn_fwd_apply<T, VEC, true, false><<<grid, kBnThreads, 0, st>>>(x, r, g.C, g.V, cpp, coef, y);
+        bn_fwd_apply<T, VEC, true, false><<<grid, kBnThreads, 0, st>>>(x, r, g.N, g.C, g.V, cpp, fs, y);
     else if (r)
-        bn_fwd_apply<T, VEC, false, true><<<grid, kBnThreads, 0, st>>>(x, r, g.C, g.V, cpp, coef, y);
+        bn_fwd_apply<T, VEC, false, true><<<grid, kBnThreads, 0, st>>>(x, r, g.N, g.C, g.V, cpp, fs, y);
     else
-        bn_fwd_apply<T, VEC, false, false><<<grid, kBnThreads, 0, st>>>(x, r, g.C, g.V, cpp, coef, y);
+        bn_fwd_apply<T, VEC, false, false><<<grid, kBnThreads, 0, st>>>(x, r, g.N, g.C, g.V, cpp, fs, y);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }
@@ -315,7 +437,6 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
                              hipStream_t st) {
     const BnSlices sl = bn_slices(g);
     float* part = (float*)ws;
-    float* coef = part + (size_t)g.C * sl.per_channel * 2;
     const dim3 sg(g.C, sl.per_channel);
     const double tb = (double)g.N * g.C * g.V * sizeof(T);
     const int mask = !relu ? kMaskNone : (fwd_coef ? kMaskX : kMaskY);
@@ -330,16 +451,14 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
 #undef RAT3D_BN_ST
     RAT3D_LAUNCH_CHECK();
     }
-    bn_bwd_finalize<<<(unsigned)ceil_div(g.C, 64), 64, 0, st>>>(
-        g.N, g.C, g.V, sl.per_channel, part, gamma, save_invstd, dgamma, dbeta, accumulate, coef);
-    RAT3D_LAUNCH_CHECK();
-    const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads);  // chunks per plane
+    const BnBwdStats bs{part, sl.per_channel, gamma, save_invstd, dgamma, dbeta, accumulate};
+    const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads * kBwdApplyU);  // chunks per plane
     const unsigned grid = cpp * (unsigned)(g.N * g.C);
     ProfScope ps("bn_bwd_apply", st, 0.0,
                  tb * ((mask == kMaskY ? 4 : 3) + (dres ? (dres_acc ? 2 : 1) : 0)));
 #define RAT3D_BN_BWD(M, D)                                                                 \
-    bn_bwd_apply<T, VEC, M, D><<<grid, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, cpp,      \
-                                                            save_mean, fwd_coef, coef, dx, dres)
+    bn_bwd_apply<T, VEC, M, D><<<grid, kBnThreads, 0, st>>>(dy, x, y, g.N, g.C, g.V, cpp, \
+                                                            save_mean, fwd_coef, bs, dx, dres)
     const int dmode = dres ? (dres_acc ? 2 : 1) : 0;
     if (mask == kMaskY && dmode == 2) RAT3D_BN_BWD(kMaskY, 2);
     else if (mask == kMaskY && dmode == 1) RAT3D_BN_BWD(kMaskY, 1);

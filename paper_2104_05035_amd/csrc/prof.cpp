@@ -21,6 +21,7 @@ struct Tag {
 
 std::mutex g_mu;
 bool g_on = false;
+std::string g_filter;  // empty: every tag
 std::vector<Tag> g_tags;
 std::vector<hipEvent_t> g_free;
 
@@ -53,6 +54,7 @@ bool prof_on() { return g_on; }
 
 int prof_begin(const char* tag, hipStream_t st) {
     std::lock_guard<std::mutex> lk(g_mu);
+    if (!g_filter.empty() && g_filter != tag) return -1;
     int slot = -1;
     for (size_t i = 0; i < g_tags.size(); ++i)
         if (g_tags[i].name == tag) slot = (int)i;
@@ -87,6 +89,12 @@ extern "C" {
 rat3d_status rat3d_profile_enable(int enable) {
     std::lock_guard<std::mutex> lk(g_mu);
     g_on = enable != 0;
+    return RAT3D_OK;
+}
+
+rat3d_status rat3d_profile_filter(const char* tag) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_filter = tag ? tag : "";
     return RAT3D_OK;
 }
 

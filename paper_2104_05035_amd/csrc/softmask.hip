@@ -577,37 +577,88 @@ __global__ __launch_bounds__(kEwThreads) void pool332_bwd_pl(const bf16* __restr
     const int nc = L / nblk, j0 = (L - nc * nblk) * kPlanes;
     const int np = min(NP, Do - j0);
     const int64_t ob = ((int64_t)nc * Do + j0) * HWo;
-    for (int i = threadIdx.x; i < np * HWo; i += kEwThreads) {
-        sdy[i] = dy[ob + i];
-        sam[i] = am[ob + i];
+    const int cnt = np * HWo;
+    // dy and argmax of the block's output planes are one contiguous run each:
+    // staged with 16-byte loads when the run and the LDS rows allow, every
+    // load issued before the LDS writes
+    const bool v_dy = (((uintptr_t)(dy + ob) | (uintptr_t)cnt * 2) & 15) == 0;
+    const bool v_am = (((uintptr_t)(am + ob) | (uintptr_t)cnt | (uintptr_t)sam) & 15) == 0;
+    if (v_dy && v_am) {
+        const int ndy = cnt >> 3, nam = cnt >> 4;
+        const uint4* gdy = reinterpret_cast<const uint4*>(dy + ob);
+        const uint4* gam = reinterpret_cast<const uint4*>(am + ob);
+        for (int i = threadIdx.x; i < ndy; i += kEwThreads) {
+            const bool ha = i < nam;
+            const uint4 d = gdy[i];
+            const uint4 a = gam[ha ? i : 0];
+            reinterpret_cast<uint4*>(sdy)[i] = d;
+            if (ha) reinterpret_cast<uint4*>(sam)[i] = a;
+        }
+    } else {
+        for (int i = threadIdx.x; i < cnt; i += kEwThreads) {
+            sdy[i] = dy[ob + i];
+            sam[i] = am[ob + i];
+        }
     }
     __syncthreads();
     const int G = W >> 3;
-    for (int it = threadIdx.x; it < 2 * kPlanes * H * G; it += kEwThreads) {
-        const int dl = it / (H * G), r = it - dl * (H * G);
+    const int per_plane = H * G, ne = ((H + 1) >> 1) * G;  // items per plane, of even rows
+    for (int it = threadIdx.x; it < 2 * kPlanes * per_plane; it += kEwThreads) {
+        const int dl = it / per_plane;
         const int id = 2 * j0 + dl;
         if (id >= D) break;
-        const int ih = r / G, g = r - ih * G;
-        int od[2], td[2], oh[2], th[2];
-        const int nd = pool332_windows(id, Do, od, td);
-        const int nh = pool332_windows(ih, Ho, oh, th);
+        // even rows first, then odd rows, so a wave mostly shares the row
+        // parity (and with it the number of h windows)
+        int r = it - dl * per_plane, ih;
+        if (r < ne) {
+            ih = 2 * (r / G);
+        } else {
+            r -= ne;
+            ih = 2 * (r / G) + 1;
+        }
+        const int g = r - (r / G) * G;
+        const bool q4ok = 4 * g + 4 < Wo;  // the fifth window (ow = 4g + 4) exists
         float acc[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-        for (int a = 0; a < nd; ++a)
-            for (int b = 0; b < nh; ++b) {
-                const int rb = ((od[a] - j0) * Ho + oh[b]) * Wo;
-                const int plane_tap = td[a] * 3 + th[b];
+        // windows along an axis, in summation order: odd i -> (i-1)/2 with
+        // tap 2, then (i+1)/2 with tap 0; even i -> i/2 with tap 1
+        const int nd = (id & 1) ? 2 : 1, nh = (ih & 1) ? 2 : 1;
 #pragma unroll
-                for (int q = 0; q < 6; ++q) {
-                    const int ow = 4 * g - 1 + q;
-                    if (ow < 0 || ow >= Wo) continue;
-                    const int arg = sam[rb + ow];
-                    if (arg / 3 != plane_tap) continue;
-                    const int e = 2 * ow - 1 + arg % 3 - 8 * g;  // argmax column within the group
-                    if (e >= 0 && e < 8) acc[e] += bf2f(sdy[rb + ow]);
+        for (int a = 0; a < 2; ++a) {
+            if (a >= nd) break;
+            const int od = (id & 1) ? (id - 1 + 2 * a) >> 1 : id >> 1;
+            const int td = (id & 1) ? 2 - 2 * a : 1;
+            if (od >= Do) continue;
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                if (b >= nh) break;
+                const int oh = (ih & 1) ? (ih - 1 + 2 * b) >> 1 : ih >> 1;
+                const int th = (ih & 1) ? 2 - 2 * b : 1;
+                if (oh >= Ho) continue;
+                // windows ow = 4g .. 4g+4 of output row (od, oh): target column
+                // within the group e = 2q - 1 + kw
+                const int rb = ((od - j0) * Ho + oh) * Wo + 4 * g;
+                const int ptap = td * 3 + th;
+                const uint32_t am4 = *reinterpret_cast<const uint32_t*>(sam + rb);
+                const uint2 dy4 = *reinterpret_cast<const uint2*>(sdy + rb);
+                const int am_4 = sam[q4ok ? rb + 4 : rb];
+                const float dy_4 = bf2f(sdy[q4ok ? rb + 4 : rb]);
+#pragma unroll
+                for (int q = 0; q < 5; ++q) {
+                    const int arg = q < 4 ? (int)((am4 >> (8 * q)) & 0xffu) : am_4;
+                    const uint32_t half = q < 2 ? dy4.x : dy4.y;
+                    const float v = q == 4 ? dy_4
+                                           : __uint_as_float((q & 1) ? (half & 0xffff0000u)
+                                                                     : (half << 16));
+                    const int row = arg / 3, kw = arg - row * 3;
+                    const float vm = (row == ptap && (q < 4 || q4ok)) ? v : 0.f;
+                    if (2 * q - 1 >= 0) acc[2 * q - 1 < 0 ? 0 : 2 * q - 1] += kw == 0 ? vm : 0.f;
+                    if (2 * q <= 7) acc[2 * q > 7 ? 7 : 2 * q] += kw == 1 ? vm : 0.f;
+                    if (2 * q + 1 <= 7) acc[2 * q + 1 > 7 ? 7 : 2 * q + 1] += kw == 2 ? vm : 0.f;
                 }
             }
+        }
         bf16* q = dx + (((int64_t)nc * D + id) * H + ih) * W + 8 * g;
         uint4* q4 = reinterpret_cast<uint4*>(q);
         if (accumulate) {
@@ -698,34 +749,37 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
         if (od >= Do) break;
         const int oh = r / G, g = r - oh * G;
         const int m0w = 4 * g;  // fine 8g .. 8g+7 read coarse m0w-1 .. m0w+4
+        // row blend: fine oh = 2m reads m-1 (1/4) and m (3/4), oh = 2m+1 reads
+        // m (3/4) and m+1 (1/4); at the first / last coarse row the one
+        // existing neighbour takes weight 1
+        const int mh = oh >> 1;
+        int ha, hb;
+        float wa, wb;
+        if ((oh & 1) == 0) {
+            ha = mh - 1; hb = mh; wa = 0.25f; wb = 0.75f;
+            if (mh == 0) { ha = 0; wa = 0.f; wb = 1.f; }
+        } else {
+            ha = mh; hb = mh + 1; wa = 0.75f; wb = 0.25f;
+            if (mh == Hi - 1) { hb = mh; wa = 1.f; wb = 0.f; }
+        }
+        const float* sa = t + l * HW8 + ha * Wi;
+        const float* sb = t + l * HW8 + hb * Wi;
         float row[6];
 #pragma unroll
-        for (int c = 0; c < 6; ++c) row[c] = 0.f;
-        const int hlo = (oh >> 1) - 1;
-#pragma unroll
-        for (int hh = 0; hh < 3; ++hh) {
-            const int mh = hlo + hh;
-            if (mh < 0 || mh >= Hi) continue;
-            const float wh = x2_w(oh, mh, Hi);
-            if (wh == 0.f) continue;
-            const float* src = t + l * HW8 + mh * Wi;
-#pragma unroll
-            for (int c = 0; c < 6; ++c) {
-                const int m = min(max(m0w - 1 + c, 0), Wi - 1);
-                row[c] += wh * src[m];
-            }
+        for (int c = 0; c < 6; ++c) {
+            const int m = min(max(m0w - 1 + c, 0), Wi - 1);
+            row[c] = wa * sa[m];
+            row[c] += wb * sb[m];
         }
+        // column blend, same weights: fine 8g + 2k reads coarse 4g+k-1, 4g+k
+        // (row[k], row[k+1]); fine 8g + 2k + 1 reads 4g+k, 4g+k+1 (row[k+1],
+        // row[k+2]); the borders clamp as above
         float out[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int o = 8 * g + j;
-            float v = 0.f;
-#pragma unroll
-            for (int c = 0; c < 6; ++c) {
-                const int m = m0w - 1 + c;
-                if (m >= 0 && m < Wi) v += x2_w(o, m, Wi) * row[c];
-            }
-            out[j] = v;
+        for (int k = 0; k < 4; ++k) {
+            const int m = m0w + k;
+            out[2 * k] = m == 0 ? row[k + 1] : 0.25f * row[k] + 0.75f * row[k + 1];
+            out[2 * k + 1] = m == Wi - 1 ? row[k + 1] : 0.75f * row[k + 1] + 0.25f * row[k + 2];
         }
         uint32_t w4[4];
 #pragma unroll
@@ -803,12 +857,15 @@ __global__ __launch_bounds__(kEwThreads) void up2_bwd_pl(const bf16* __restrict_
         float rowacc[10];  // fine columns 8g-1 .. 8g+8 blended over the fine rows
 #pragma unroll
         for (int j = 0; j < 10; ++j) rowacc[j] = 0.f;
+        // transpose weights of coarse index i over fine 2i-1, 2i, 2i+1, 2i+2:
+        // 1/4, 3/4, 3/4, 1/4, with the missing fine neighbour at a border
+        // folded into the middle weight (1)
 #pragma unroll
         for (int hh = 0; hh < 4; ++hh) {
             const int oh = 2 * ih - 1 + hh;
             if (oh < 0 || oh >= Ho) continue;
-            const float wh = x2_w(oh, ih, Hi);
-            if (wh == 0.f) continue;
+            const float wh = (hh == 0 || hh == 3) ? 0.25f
+                             : (hh == 1 ? (ih == 0 ? 1.f : 0.75f) : (ih == Hi - 1 ? 1.f : 0.75f));
             const float* src = t + l * HWo + oh * Wo;
             const float4 a = *reinterpret_cast<const float4*>(src + 8 * g);
             const float4 b = *reinterpret_cast<const float4*>(src + 8 * g + 4);
@@ -821,13 +878,14 @@ __global__ __launch_bounds__(kEwThreads) void up2_bwd_pl(const bf16* __restrict_
         float out[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
+            // fine columns 2mw-1 .. 2mw+2 are rowacc[2k .. 2k+3]; rowacc[0]
+            // and rowacc[9] stay 0 where those columns do not exist
             const int mw = 4 * g + k;
             float v = 0.f;
-#pragma unroll
-            for (int j = 0; j < 10; ++j) {
-                const int o = 8 * g - 1 + j;
-                if (o >= 0 && o < Wo) v += x2_w(o, mw, Wi) * rowacc[j];
-            }
+            v += 0.25f * rowacc[2 * k];
+            v += (mw == 0 ? 1.f : 0.75f) * rowacc[2 * k + 1];
+            v += (mw == Wi - 1 ? 1.f : 0.75f) * rowacc[2 * k + 2];
+            v += 0.25f * rowacc[2 * k + 3];
             out[k] = v;
         }
         uint2* q2 = reinterpret_cast<uint2*>(dx + (((int64_t)nc * Di + m) * Hi + ih) * Wi + 4 * g);

@@ -97,6 +97,7 @@ _SIGS = {
     "rat3d_block_fwd_bwd": (_I, [_VP] * 6),
     "rat3d_train_step": (_I, [_VP] * 6),
     "rat3d_profile_enable": (_I, [_I]),
+    "rat3d_profile_filter": (_I, [ctypes.c_char_p]),
     "rat3d_profile_reset": (_I, []),
     "rat3d_profile_count": (_I, []),
     "rat3d_profile_read": (_I, [_I, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(_I64),
@@ -256,6 +257,10 @@ def rat3d_sgd(count, lr, params, grads, stream=None):
 # ---------------------------------------------------------------- measurement
 def rat3d_profile_enable(enable):
     _check(lib().rat3d_profile_enable(int(enable)))
+
+
+def rat3d_profile_filter(tag=None):
+    _check(lib().rat3d_profile_filter(tag.encode() if tag else None))
 
 
 def rat3d_profile_reset():
