@@ -190,7 +190,7 @@ rat3d_status rat3d_bn_relu_fwd(const rat3d_bn_desc* desc, const void* x, const v
     s = check_ws(ws, ws_bytes, bn_ws_bytes(g));
     if (s != RAT3D_OK) return s;
     return bn_fwd(g, desc->dtype, desc->relu, desc->eps, desc->momentum, x, residual, gamma, beta,
-                  y, save_mean, save_invstd, run_mean, run_var, nullptr, ws,
+                  y, save_mean, save_invstd, run_mean, run_var, nullptr, nullptr, ws,
                   (hipStream_t)stream);
 }
 
@@ -211,7 +211,8 @@ rat3d_status rat3d_bn_relu_bwd(const rat3d_bn_desc* desc, const void* dy, const 
                   "gamma, save_mean, save_invstd, dgamma and dbeta are required");
     s = check_ws(ws, ws_bytes, bn_ws_bytes(g));
     if (s != RAT3D_OK) return s;
-    return bn_bwd(g, desc->dtype, desc->relu, dy, x, y, gamma, save_mean, save_invstd, nullptr,
+    return bn_bwd(g, desc->dtype, desc->relu, dy, x, y, nullptr, gamma, save_mean, save_invstd,
+                  nullptr,
                   dx, dresidual, 0, dgamma, dbeta, accumulate ? 1 : 0, ws, (hipStream_t)stream);
 }
 

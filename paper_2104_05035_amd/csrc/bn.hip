@@ -212,7 +212,8 @@ template <typename T, int VEC, bool RELU, bool RES>
 __global__ __launch_bounds__(kBnThreads) void bn_fwd_apply(const T* __restrict__ x,
                                                            const T* __restrict__ r, int N, int C,
                                                            int64_t V, unsigned cpp,
-                                                           BnFwdStats st, T* __restrict__ y) {
+                                                           BnFwdStats st, T* __restrict__ y,
+                                                           uint8_t* __restrict__ ybits) {
     constexpr int U = fwd_apply_u<RES>();
     constexpr int64_t kStep = (int64_t)kBnThreads * VEC;
     const int plane = (int)(blockIdx.x / cpp);  // wave-uniform
@@ -247,18 +248,39 @@ __global__ __launch_bounds__(kBnThreads) void bn_fwd_apply(const T* __restrict__
             if constexpr (RELU) o = fmaxf(o, 0.f);
             v[u][j] = o;
         }
+        if constexpr (sizeof(T) == 2 && VEC == 8) {
+            if (ybits) {
+                // the stored bf16 values, and bit j = (y_j > 0) of them
+                uint32_t w[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) w[q] = pack_bf16x2(v[u][2 * q], v[u][2 * q + 1]);
+                *reinterpret_cast<uint4*>(y + base + e) = make_uint4(w[0], w[1], w[2], w[3]);
+                uint32_t byte = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    byte |= ((int16_t)(w[q] & 0xffffu) > 0 ? 1u : 0u) << (2 * q);
+                    byte |= ((int16_t)(w[q] >> 16) > 0 ? 1u : 0u) << (2 * q + 1);
+                }
+                ybits[(base + e) >> 3] = (uint8_t)byte;
+                continue;
+            }
+        }
         vstore<T, VEC>(y + base + e, v[u]);
     }
 }
 
-// ReLU mask of the backward: none, y > 0, or x * scale + shift > 0.
-enum { kMaskNone = 0, kMaskY = 1, kMaskX = 2 };
+// ReLU mask of the backward: none, y > 0, x * scale + shift > 0, or the
+// forward's y > 0 bits (bf16, VEC 8: one byte per vector).
+enum { kMaskNone = 0, kMaskY = 1, kMaskX = 2, kMaskBits = 3 };
+
+bool bn_bits_ok(const BnGeom& g, rat3d_dtype dt) { return dt == RAT3D_BF16 && g.V % 8 == 0; }
 
 template <typename T, int VEC, int MASK>
 __global__ __launch_bounds__(kBnThreads) void bn_bwd_stats(const T* __restrict__ dy,
                                                            const T* __restrict__ x,
-                                                           const T* __restrict__ y, int C,
-                                                           int64_t V, int SP, int64_t len,
+                                                           const T* __restrict__ y,
+                                                           const uint8_t* __restrict__ ybits,
+                                                           int C, int64_t V, int SP, int64_t len,
                                                            const float* __restrict__ save_mean,
                                                            const float* __restrict__ fcoef,
                                                            float* __restrict__ part) {
@@ -278,6 +300,7 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_stats(const T* __restrict__
     for (int64_t e = (int64_t)threadIdx.x * VEC; e < cnt; e += U * kStep) {
         float g[U][VEC], xv[U][VEC];
         [[maybe_unused]] float yv[U][VEC];
+        [[maybe_unused]] uint32_t yb[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t eu = e + u * kStep;
@@ -285,6 +308,7 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_stats(const T* __restrict__
             vload<T, VEC>(dy + idx, g[u]);
             vload<T, VEC>(x + idx, xv[u]);
             if constexpr (MASK == kMaskY) vload<T, VEC>(y + idx, yv[u]);
+            if constexpr (MASK == kMaskBits) yb[u] = ybits[idx >> 3];
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -292,6 +316,9 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_stats(const T* __restrict__
             if constexpr (MASK == kMaskY) {
 #pragma unroll
                 for (int j = 0; j < VEC; ++j) g[u][j] = yv[u][j] > 0.f ? g[u][j] : 0.f;
+            } else if constexpr (MASK == kMaskBits) {
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) g[u][j] = (yb[u] >> j) & 1u ? g[u][j] : 0.f;
             } else if constexpr (MASK == kMaskX) {
 #pragma unroll
                 for (int j = 0; j < VEC; ++j) g[u][j] = fmaf(xv[u][j], fsc, fsh) > 0.f ? g[u][j] : 0.f;
@@ -344,9 +371,10 @@ __device__ __forceinline__ void bn_bwd_coefs(int N, int64_t V, int c, const BnBw
 // DRES: 0 no residual gradient, 1 dres = g, 2 dres += g (one rounding).
 template <typename T, int VEC, int MASK, int DRES>
 __global__ __launch_bounds__(kBnThreads) void bn_bwd_apply(
-    const T* __restrict__ dy, const T* __restrict__ x, const T* __restrict__ y, int N, int C,
-    int64_t V, unsigned cpp, const float* __restrict__ save_mean, const float* __restrict__ fcoef,
-    BnBwdStats st, T* __restrict__ dx, T* __restrict__ dres) {
+    const T* __restrict__ dy, const T* __restrict__ x, const T* __restrict__ y,
+    const uint8_t* __restrict__ ybits, int N, int C, int64_t V, unsigned cpp,
+    const float* __restrict__ save_mean, const float* __restrict__ fcoef, BnBwdStats st,
+    T* __restrict__ dx, T* __restrict__ dres) {
     constexpr int U = kBwdApplyU;
     constexpr int64_t kStep = (int64_t)kBnThreads * VEC;
     const int plane = (int)(blockIdx.x / cpp);  // wave-uniform
@@ -358,6 +386,7 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_apply(
     // coefficient reduction
     float g[U][VEC], xv[U][VEC];
     [[maybe_unused]] float yv[U][VEC], ov[U][VEC];
+    [[maybe_unused]] uint32_t yb[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int64_t e = e0 + u * kStep;
@@ -365,6 +394,7 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_apply(
         vload<T, VEC>(dy + i, g[u]);
         vload<T, VEC>(x + i, xv[u]);
         if constexpr (MASK == kMaskY) vload<T, VEC>(y + i, yv[u]);
+        if constexpr (MASK == kMaskBits) yb[u] = ybits[i >> 3];
         if constexpr (DRES == 2) vload<T, VEC>(dres + i, ov[u]);
     }
     float k, a, b;
@@ -380,6 +410,9 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_apply(
         if constexpr (MASK == kMaskY) {
 #pragma unroll
             for (int j = 0; j < VEC; ++j) g[u][j] = yv[u][j] > 0.f ? g[u][j] : 0.f;
+        } else if constexpr (MASK == kMaskBits) {
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) g[u][j] = (yb[u] >> j) & 1u ? g[u][j] : 0.f;
         } else if constexpr (MASK == kMaskX) {
 #pragma unroll
             for (int j = 0; j < VEC; ++j) g[u][j] = fmaf(xv[u][j], fsc, fsh) > 0.f ? g[u][j] : 0.f;
@@ -401,7 +434,8 @@ template <typename T, int VEC>
 static rat3d_status bn_fwd_t(const BnGeom& g, int relu, float eps, float momentum, const T* x,
                              const T* r, const float* gamma, const float* beta, T* y,
                              float* save_mean, float* save_invstd, float* run_mean,
-                             float* run_var, float* save_coef, void* ws, hipStream_t st) {
+                             float* run_var, float* save_coef, uint8_t* ybits, void* ws,
+                             hipStream_t st) {
     const BnSlices sl = bn_slices(g);
     float* part = (float*)ws;
     const double tb = (double)g.N * g.C * g.V * sizeof(T);
@@ -416,22 +450,22 @@ static rat3d_status bn_fwd_t(const BnGeom& g, int relu, float eps, float momentu
     const int fu = r ? fwd_apply_u<true>() : fwd_apply_u<false>();
     const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads * fu);  // chunks per plane
     const unsigned grid = cpp * (unsigned)(g.N * g.C);
-    ProfScope ps("bn_fwd_apply", st, 0.0, tb * (r ? 3 : 2));
-    if (relu && r)
-        bn_fwd_apply<T, VEC, true, true><<<grid, kBnThreads, 0, st>>>(x, r, g.N, g.C, g.V, cpp, fs, y);
-    else if (relu)
-        bn_fwd_apply<T, VEC, true, false><<<grid, kBnThreads, 0, st>>>(x, r, g.N, g.C, g.V, cpp, fs, y);
-    else if (r)
-        bn_fwd_apply<T, VEC, false, true><<<grid, kBnThreads, 0, st>>>(x, r, g.N, g.C, g.V, cpp, fs, y);
-    else
-        bn_fwd_apply<T, VEC, false, false><<<grid, kBnThreads, 0, st>>>(x, r, g.N, g.C, g.V, cpp, fs, y);
+    ProfScope ps("bn_fwd_apply", st, 0.0, tb * (r ? 3 : 2) + (ybits ? tb / 16 : 0.0));
+#define RAT3D_BN_FWD(RL, RS)                                                                 \
+    bn_fwd_apply<T, VEC, RL, RS><<<grid, kBnThreads, 0, st>>>(x, r, g.N, g.C, g.V, cpp, fs, y, \
+                                                              ybits)
+    if (relu && r) RAT3D_BN_FWD(true, true);
+    else if (relu) RAT3D_BN_FWD(true, false);
+    else if (r) RAT3D_BN_FWD(false, true);
+    else RAT3D_BN_FWD(false, false);
+#undef RAT3D_BN_FWD
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }
 
 template <typename T, int VEC>
 static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x, const T* y,
-                             const float* gamma, const float* save_mean,
+                             const uint8_t* ybits, const float* gamma, const float* save_mean,
                              const float* save_invstd, const float* fwd_coef, T* dx, T* dres,
                              int dres_acc, float* dgamma, float* dbeta, int accumulate, void* ws,
                              hipStream_t st) {
@@ -439,14 +473,17 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
     float* part = (float*)ws;
     const dim3 sg(g.C, sl.per_channel);
     const double tb = (double)g.N * g.C * g.V * sizeof(T);
-    const int mask = !relu ? kMaskNone : (fwd_coef ? kMaskX : kMaskY);
+    const int mask = !relu ? kMaskNone : (fwd_coef ? kMaskX : (ybits ? kMaskBits : kMaskY));
+    // bytes of the mask operand: y, its bits, or nothing
+    const double mb = mask == kMaskY ? tb : (mask == kMaskBits ? tb / 16 : 0.0);
     {
-    ProfScope ps("bn_bwd_stats", st, 0.0, tb * (mask == kMaskY ? 3 : 2));
-#define RAT3D_BN_ST(M)                                                                       \
-    bn_bwd_stats<T, VEC, M><<<sg, kBnThreads, 0, st>>>(dy, x, y, g.C, g.V, sl.per_plane,     \
+    ProfScope ps("bn_bwd_stats", st, 0.0, tb * 2 + mb);
+#define RAT3D_BN_ST(M)                                                                        \
+    bn_bwd_stats<T, VEC, M><<<sg, kBnThreads, 0, st>>>(dy, x, y, ybits, g.C, g.V, sl.per_plane, \
                                                        sl.len, save_mean, fwd_coef, part)
     if (mask == kMaskY) RAT3D_BN_ST(kMaskY);
     else if (mask == kMaskX) RAT3D_BN_ST(kMaskX);
+    else if (mask == kMaskBits) RAT3D_BN_ST(kMaskBits);
     else RAT3D_BN_ST(kMaskNone);
 #undef RAT3D_BN_ST
     RAT3D_LAUNCH_CHECK();
@@ -455,20 +492,25 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
     const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads * kBwdApplyU);  // chunks per plane
     const unsigned grid = cpp * (unsigned)(g.N * g.C);
     ProfScope ps("bn_bwd_apply", st, 0.0,
-                 tb * ((mask == kMaskY ? 4 : 3) + (dres ? (dres_acc ? 2 : 1) : 0)));
-#define RAT3D_BN_BWD(M, D)                                                                 \
-    bn_bwd_apply<T, VEC, M, D><<<grid, kBnThreads, 0, st>>>(dy, x, y, g.N, g.C, g.V, cpp, \
+                 tb * (3 + (dres ? (dres_acc ? 2 : 1) : 0)) + mb);
+#define RAT3D_BN_BWD(M, D)                                                                    \
+    bn_bwd_apply<T, VEC, M, D><<<grid, kBnThreads, 0, st>>>(dy, x, y, ybits, g.N, g.C, g.V, cpp, \
                                                             save_mean, fwd_coef, bs, dx, dres)
+#define RAT3D_BN_BWD_M(M)                      \
+    if (dmode == 2) RAT3D_BN_BWD(M, 2);        \
+    else if (dmode == 1) RAT3D_BN_BWD(M, 1);   \
+    else RAT3D_BN_BWD(M, 0);
     const int dmode = dres ? (dres_acc ? 2 : 1) : 0;
-    if (mask == kMaskY && dmode == 2) RAT3D_BN_BWD(kMaskY, 2);
-    else if (mask == kMaskY && dmode == 1) RAT3D_BN_BWD(kMaskY, 1);
-    else if (mask == kMaskY) RAT3D_BN_BWD(kMaskY, 0);
-    else if (mask == kMaskX && dmode == 2) RAT3D_BN_BWD(kMaskX, 2);
-    else if (mask == kMaskX && dmode == 1) RAT3D_BN_BWD(kMaskX, 1);
-    else if (mask == kMaskX) RAT3D_BN_BWD(kMaskX, 0);
-    else if (dmode == 2) RAT3D_BN_BWD(kMaskNone, 2);
-    else if (dmode == 1) RAT3D_BN_BWD(kMaskNone, 1);
-    else RAT3D_BN_BWD(kMaskNone, 0);
+    if (mask == kMaskY) {
+        RAT3D_BN_BWD_M(kMaskY)
+    } else if (mask == kMaskX) {
+        RAT3D_BN_BWD_M(kMaskX)
+    } else if (mask == kMaskBits) {
+        RAT3D_BN_BWD_M(kMaskBits)
+    } else {
+        RAT3D_BN_BWD_M(kMaskNone)
+    }
+#undef RAT3D_BN_BWD_M
 #undef RAT3D_BN_BWD
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
@@ -477,46 +519,54 @@ static rat3d_status bn_bwd_t(const BnGeom& g, int relu, const T* dy, const T* x,
 rat3d_status bn_fwd(const BnGeom& g, rat3d_dtype dt, int relu, float eps, float momentum,
                     const void* x, const void* residual, const float* gamma, const float* beta,
                     void* y, float* save_mean, float* save_invstd, float* run_mean,
-                    float* run_var, float* save_coef, void* ws, hipStream_t st) {
+                    float* run_var, float* save_coef, uint8_t* ybits, void* ws, hipStream_t st) {
+    if (ybits && !(relu && bn_bits_ok(g, dt))) {
+        set_error("bn_fwd: y > 0 bits need bf16, a ReLU and V % 8 == 0");
+        return RAT3D_EUNSUPPORTED;
+    }
     if (dt == RAT3D_BF16) {
         if (g.V % 8 == 0)
             return bn_fwd_t<bf16, 8>(g, relu, eps, momentum, (const bf16*)x, (const bf16*)residual,
                                      gamma, beta, (bf16*)y, save_mean, save_invstd, run_mean,
-                                     run_var, save_coef, ws, st);
+                                     run_var, save_coef, ybits, ws, st);
         return bn_fwd_t<bf16, 1>(g, relu, eps, momentum, (const bf16*)x, (const bf16*)residual,
                                  gamma, beta, (bf16*)y, save_mean, save_invstd, run_mean, run_var,
-                                 save_coef, ws, st);
+                                 save_coef, nullptr, ws, st);
     }
     if (g.V % 4 == 0)
         return bn_fwd_t<float, 4>(g, relu, eps, momentum, (const float*)x, (const float*)residual,
                                   gamma, beta, (float*)y, save_mean, save_invstd, run_mean,
-                                  run_var, save_coef, ws, st);
+                                  run_var, save_coef, nullptr, ws, st);
     return bn_fwd_t<float, 1>(g, relu, eps, momentum, (const float*)x, (const float*)residual,
                               gamma, beta, (float*)y, save_mean, save_invstd, run_mean, run_var,
-                              save_coef, ws, st);
+                              save_coef, nullptr, ws, st);
 }
 
 rat3d_status bn_bwd(const BnGeom& g, rat3d_dtype dt, int relu, const void* dy, const void* x,
-                    const void* y, const float* gamma, const float* save_mean,
-                    const float* save_invstd, const float* fwd_coef, void* dx, void* dres,
-                    int dres_acc, float* dgamma, float* dbeta, int accumulate, void* ws,
-                    hipStream_t st) {
+                    const void* y, const uint8_t* ybits, const float* gamma,
+                    const float* save_mean, const float* save_invstd, const float* fwd_coef,
+                    void* dx, void* dres, int dres_acc, float* dgamma, float* dbeta,
+                    int accumulate, void* ws, hipStream_t st) {
+    if (ybits && !(relu && bn_bits_ok(g, dt))) {
+        set_error("bn_bwd: y > 0 bits need bf16, a ReLU and V % 8 == 0");
+        return RAT3D_EUNSUPPORTED;
+    }
     if (dt == RAT3D_BF16) {
         if (g.V % 8 == 0)
             return bn_bwd_t<bf16, 8>(g, relu, (const bf16*)dy, (const bf16*)x, (const bf16*)y,
-                                     gamma, save_mean, save_invstd, fwd_coef, (bf16*)dx,
+                                     ybits, gamma, save_mean, save_invstd, fwd_coef, (bf16*)dx,
                                      (bf16*)dres, dres_acc, dgamma, dbeta, accumulate, ws, st);
-        return bn_bwd_t<bf16, 1>(g, relu, (const bf16*)dy, (const bf16*)x, (const bf16*)y, gamma,
-                                 save_mean, save_invstd, fwd_coef, (bf16*)dx, (bf16*)dres,
-                                 dres_acc, dgamma, dbeta, accumulate, ws, st);
+        return bn_bwd_t<bf16, 1>(g, relu, (const bf16*)dy, (const bf16*)x, (const bf16*)y,
+                                 nullptr, gamma, save_mean, save_invstd, fwd_coef, (bf16*)dx,
+                                 (bf16*)dres, dres_acc, dgamma, dbeta, accumulate, ws, st);
     }
     if (g.V % 4 == 0)
         return bn_bwd_t<float, 4>(g, relu, (const float*)dy, (const float*)x, (const float*)y,
-                                  gamma, save_mean, save_invstd, fwd_coef, (float*)dx,
+                                  nullptr, gamma, save_mean, save_invstd, fwd_coef, (float*)dx,
                                   (float*)dres, dres_acc, dgamma, dbeta, accumulate, ws, st);
-    return bn_bwd_t<float, 1>(g, relu, (const float*)dy, (const float*)x, (const float*)y, gamma,
-                              save_mean, save_invstd, fwd_coef, (float*)dx, (float*)dres,
-                              dres_acc, dgamma, dbeta, accumulate, ws, st);
+    return bn_bwd_t<float, 1>(g, relu, (const float*)dy, (const float*)x, (const float*)y,
+                              nullptr, gamma, save_mean, save_invstd, fwd_coef, (float*)dx,
+                              (float*)dres, dres_acc, dgamma, dbeta, accumulate, ws, st);
 }
 
 }  // namespace rat3d

@@ -112,19 +112,23 @@ struct BnGeom {
 };
 size_t bn_ws_bytes(const BnGeom& g);
 // save_coef (may be null): receives the apply's float scale [C] and shift [C].
+// ybits (may be null; bf16 with V % 8 == 0 and relu only): receives y > 0 of
+// the stored y, one bit per element (byte i/8, bit i%8).
+bool bn_bits_ok(const BnGeom& g, rat3d_dtype dt);
 rat3d_status bn_fwd(const BnGeom& g, rat3d_dtype dt, int relu, float eps, float momentum,
                     const void* x, const void* residual, const float* gamma, const float* beta,
                     void* y, float* save_mean, float* save_invstd, float* run_mean,
-                    float* run_var, float* save_coef, void* ws, hipStream_t st);
+                    float* run_var, float* save_coef, uint8_t* ybits, void* ws, hipStream_t st);
 // fwd_coef (may be null): the forward's scale/shift of a BN + ReLU without a
 // residual; the ReLU mask is then recomputed from x and y is not read.
+// ybits (may be null): the forward's y > 0 bits; read instead of y.
 // dres_acc: the residual gradient is added to dres (one rounding) instead of
 // stored.
 rat3d_status bn_bwd(const BnGeom& g, rat3d_dtype dt, int relu, const void* dy, const void* x,
-                    const void* y, const float* gamma, const float* save_mean,
-                    const float* save_invstd, const float* fwd_coef, void* dx, void* dres,
-                    int dres_acc, float* dgamma, float* dbeta, int accumulate, void* ws,
-                    hipStream_t st);
+                    const void* y, const uint8_t* ybits, const float* gamma,
+                    const float* save_mean, const float* save_invstd, const float* fwd_coef,
+                    void* dx, void* dres, int dres_acc, float* dgamma, float* dbeta,
+                    int accumulate, void* ws, hipStream_t st);
 
 // ---- soft-mask branch (softmask.hip) -----------------------------------
 rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, rat3d_dtype dt,

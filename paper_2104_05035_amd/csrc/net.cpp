@@ -61,6 +61,7 @@ struct RUPlan {
     bool proj = false;
     TRef x, h1, a1, h2, hp, sp, y;
     int64_t dskip = kNone;  // ws offset of the skip-branch gradient
+    int64_t ybits = kNone;  // ws offset of the output's y > 0 bits (kNone: read y)
 };
 
 struct AMPlan {
@@ -223,6 +224,9 @@ struct Builder {
             r.sp = act(pre + "sp", o, false);
         }
         r.y = act(pre + "y", o);
+        // the output BN's ReLU mask, one bit per element
+        if (bn_bits_ok(BnGeom{o.n, cout, o.vox()}, net->dt))
+            r.ybits = (int64_t)alloc((size_t)(o.count() / 8));
         r.dskip = (int64_t)alloc((size_t)o.count() * net->esz);
         record("d:" + pre + "skip", (size_t)r.dskip, net->dt, o);
         return r;
@@ -310,23 +314,28 @@ struct Exec {
     }
     // The forward keeps the apply's scale and shift; a BN + ReLU without a
     // residual recomputes its backward mask from x with them (bn_bwd_x).
-    rat3d_status bn_f(const BnL& b, const TRef& x, const void* res, int relu, void* y) const {
+    // ybits (nullable): where the forward stores the y > 0 bits of a BN +
+    // residual + ReLU, so that its backward reads bits instead of y
+    rat3d_status bn_f(const BnL& b, const TRef& x, const void* res, int relu, void* y,
+                      uint8_t* ybits = nullptr) const {
         return bn_fwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, relu, n->d.bn_eps, n->d.bn_momentum,
                       a(x), res, par(b.g_off), par(b.b_off), y, mean(b), invstd(b), rmean(b),
-                      rvar(b), fcoef(b), bn_scr(), st);
+                      rvar(b), fcoef(b), ybits, bn_scr(), st);
     }
     // dres_acc: add the residual gradient to dres (one rounding) instead of storing it
     rat3d_status bn_b(const BnL& b, const void* dy, const TRef& x, const void* y, int relu,
-                      void* dx, void* dres, int dres_acc = 0) const {
-        return bn_bwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, relu, dy, a(x), y, par(b.g_off),
-                      mean(b), invstd(b), nullptr, dx, dres, dres_acc, grd(b.g_off),
-                      grd(b.b_off), acc, bn_scr(), st);
+                      void* dx, void* dres, int dres_acc = 0,
+                      const uint8_t* ybits = nullptr) const {
+        return bn_bwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, relu, dy, a(x), y, ybits,
+                      par(b.g_off), mean(b), invstd(b), nullptr, dx, dres, dres_acc,
+                      grd(b.g_off), grd(b.b_off), acc, bn_scr(), st);
     }
     rat3d_status bn_bwd_x(const BnL& b, const void* dy, const TRef& x, void* dx) const {
-        return bn_bwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, 1, dy, a(x), nullptr, par(b.g_off),
-                      mean(b), invstd(b), fcoef(b), dx, nullptr, 0, grd(b.g_off), grd(b.b_off),
-                      acc, bn_scr(), st);
+        return bn_bwd(BnGeom{x.s.n, b.c, x.s.vox()}, n->dt, 1, dy, a(x), nullptr, nullptr,
+                      par(b.g_off), mean(b), invstd(b), fcoef(b), dx, nullptr, 0, grd(b.g_off),
+                      grd(b.b_off), acc, bn_scr(), st);
     }
+    uint8_t* bits(int64_t off) const { return off >= 0 ? (uint8_t*)(n->ws + off) : nullptr; }
 };
 
 #define RAT3D_TRY(expr)                       \
@@ -345,7 +354,7 @@ rat3d_status ru_fwd(const Exec& e, const RUPlan& r) {
         RAT3D_TRY(e.bn_f(r.bp, r.hp, nullptr, 0, e.a(r.sp)));
         skip = e.a(r.sp);
     }
-    return e.bn_f(r.b2, r.h2, skip, 1, e.a(r.y));
+    return e.bn_f(r.b2, r.h2, skip, 1, e.a(r.y), e.bits(r.ybits));
 }
 
 // Backward of a residual unit from y's gradient to x's gradient.  acc_dx: the
@@ -357,7 +366,7 @@ rat3d_status ru_bwd(const Exec& e, const RUPlan& r, bool acc_dx, bool need_dx = 
     // partial sum already there when acc_dx, one rounding)
     const bool skip_direct = !r.proj && need_dx;
     RAT3D_TRY(e.bn_b(r.b2, e.g(r.y), r.h2, e.a(r.y), 1, e.g(r.h2), skip_direct ? dx : dskip,
-                     skip_direct && acc_dx ? 1 : 0));
+                     skip_direct && acc_dx ? 1 : 0, e.bits(r.ybits)));
     RAT3D_TRY(e.conv_d(r.c2, e.g(r.h2), e.g(r.a1), 0));
     RAT3D_TRY(e.conv_w(r.c2, e.a(r.a1), e.g(r.h2)));
     RAT3D_TRY(e.bn_bwd_x(r.b1, e.g(r.a1), r.h1, e.g(r.h1)));
