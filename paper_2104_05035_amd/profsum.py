@@ -41,7 +41,7 @@ def stats(csv_path, bench_log, out, title, cmd):
              "Workload: stem 7^3 s2 1->32, RU 32->64, attention module 64 on 48x56x48; "
              "4 micro-batches x 16 volumes 96x112x96, bf16 storage, fp32 accumulation.", "",
              "Command (repository root, one MI355X):", "", "    " + cmd, "",
-             "Calls cover 1 warm-up + 3 timed steps.  Dominant kernel per bench.py's live "
+             "Calls cover 1 warm-up, 3 breakdown and 3 timed steps.  Dominant kernel per bench.py's live "
              "hipEvents: `%s`, %.1f us/launch (rocprofv3 average in the table)."
              % (b["roofline"]["kernel"], b["roofline"]["avg_launch_us"]), "",
              "| kernel | calls | total ms | avg us | % |", "|---|---|---|---|---|"]
