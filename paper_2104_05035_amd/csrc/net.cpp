@@ -68,7 +68,7 @@ struct AMPlan {
     RUPlan t1, t2, m1, m2, m3, m4;
     ConvL c1, c2;
     BnL bn;
-    TRef x, p1, p2, u1, u2, h1, a, z, out, m;
+    TRef x, p1, p2, u1, h1c, h1, a, z, out, m;
     int64_t am1 = 0, am2 = 0;  // argmax byte offsets
 };
 
@@ -253,10 +253,14 @@ struct Builder {
         a.m3 = ru(pre + "m3.", a.m2.y, c, 1);
         a.u1 = act(pre + "u1", s1);
         a.m4 = ru(pre + "m4.", a.u1, c, 1);
-        a.u2 = act(pre + "u2", x.s);
-        a.c1 = conv(pre + "c1", c, c, 1, 1, 0, false, x.s);
+        // The first 1^3 conv (no bias) runs before the last upsampling: both
+        // are linear, one mixes channels and the other voxels, so
+        // conv(up(y)) = up(conv(y)) and the conv and its gradients work on the
+        // coarse map.  c1out is the upsampled conv output.
+        a.c1 = conv(pre + "c1", c, c, 1, 1, 0, false, s1);
         a.bn = bn(pre + "bn", c, x.s);
         a.c2 = conv(pre + "c2", c, c, 1, 1, 0, true, x.s);
+        a.h1c = act(pre + "c1out.coarse", s1);
         a.h1 = act(pre + "c1out", x.s);
         a.a = act(pre + "a", x.s);
         a.z = act(pre + "z", x.s);
@@ -396,9 +400,9 @@ rat3d_status am_fwd(const Exec& e, const AMPlan& m) {
     RAT3D_TRY(up_fwd(s.n, s.c, s2.d, s2.h, s2.w, s1.d, s1.h, s1.w, dt, e.a(m.m3.y), e.a(m.u1),
                      e.st));
     RAT3D_TRY(ru_fwd(e, m.m4));
-    RAT3D_TRY(up_fwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.a(m.m4.y), e.a(m.u2),
+    RAT3D_TRY(e.conv_f(m.c1, e.a(m.m4.y), e.a(m.h1c)));
+    RAT3D_TRY(up_fwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.a(m.h1c), e.a(m.h1),
                      e.st));
-    RAT3D_TRY(e.conv_f(m.c1, e.a(m.u2), e.a(m.h1)));
     RAT3D_TRY(e.bn_f(m.bn, m.h1, nullptr, 1, e.a(m.a)));
     RAT3D_TRY(e.conv_f(m.c2, e.a(m.a), e.a(m.z)));
     return softmask_fwd(s.count(), dt, e.a(m.z), e.a(m.t2.y), e.a(m.out), e.a(m.m), e.st);
@@ -414,10 +418,10 @@ rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
     RAT3D_TRY(e.conv_d(m.c2, e.g(m.z), e.g(m.a), 0));
     RAT3D_TRY(e.conv_w(m.c2, e.a(m.a), e.g(m.z)));
     RAT3D_TRY(e.bn_bwd_x(m.bn, e.g(m.a), m.h1, e.g(m.h1)));
-    RAT3D_TRY(e.conv_d(m.c1, e.g(m.h1), e.g(m.u2), 0));
-    RAT3D_TRY(e.conv_w(m.c1, e.a(m.u2), e.g(m.h1)));
-    RAT3D_TRY(up_bwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.g(m.u2), e.g(m.m4.y), 0,
+    RAT3D_TRY(up_bwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.g(m.h1), e.g(m.h1c), 0,
                      e.st));
+    RAT3D_TRY(e.conv_d(m.c1, e.g(m.h1c), e.g(m.m4.y), 0));
+    RAT3D_TRY(e.conv_w(m.c1, e.a(m.m4.y), e.g(m.h1c)));
     RAT3D_TRY(ru_bwd(e, m.m4, false));
     RAT3D_TRY(up_bwd(s.n, s.c, s2.d, s2.h, s2.w, s1.d, s1.h, s1.w, dt, e.g(m.u1), e.g(m.m3.y), 0,
                      e.st));
