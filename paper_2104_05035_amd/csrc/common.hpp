@@ -35,6 +35,8 @@ template <> struct Elt<float> {
     __device__ __forceinline__ static void st(float* p, float v) { *p = v; }
     __device__ __forceinline__ static float from_bits(float v) { return v; }
     __device__ __forceinline__ static float to_bits(float v) { return v; }
+    // the value a store of v holds
+    __device__ __forceinline__ static float round(float v) { return v; }
 };
 template <> struct Elt<bf16> {
     static constexpr rat3d_dtype dtype = RAT3D_BF16;
@@ -43,6 +45,7 @@ template <> struct Elt<bf16> {
     __device__ __forceinline__ static void st(bf16* p, float v) { *p = f2bf(v); }
     __device__ __forceinline__ static float from_bits(bf16 v) { return bf2f(v); }
     __device__ __forceinline__ static bf16 to_bits(float v) { return f2bf(v); }
+    __device__ __forceinline__ static float round(float v) { return bf2f(f2bf(v)); }
 };
 
 // MFMA operand / accumulator vector types.

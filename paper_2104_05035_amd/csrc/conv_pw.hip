@@ -59,10 +59,10 @@ __global__ __launch_bounds__(256) void conv_pw_wgrad(PwArgs a) {
         }
     };
 
-    // Three register sets: the operands of a wave's step are loaded three of
+    // Four register sets: the operands of a wave's step are loaded four of
     // its steps ahead.  Loads past the range re-read its last step (never a
     // load behind a branch, which would be waited for on the spot).
-    constexpr int PD = 3;
+    constexpr int PD = 4;
     F16B av[PD][4], bv[PD][4];
     const int64_t last = s_end - 1;
 #pragma unroll

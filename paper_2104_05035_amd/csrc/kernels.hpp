@@ -142,9 +142,11 @@ rat3d_status up_bwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
                     rat3d_dtype dt, const void* dy, void* dx, int accumulate, hipStream_t st);
 rat3d_status softmask_fwd(int64_t count, rat3d_dtype dt, const void* z, const void* t,
                           void* out, void* m, hipStream_t st);
+// m_is_z: `m` holds z (m was not stored) and m is recomputed and rounded as a
+// store of it would be.
 rat3d_status softmask_bwd(int64_t count, rat3d_dtype dt, const void* dout, const void* t,
                           const void* m, void* dt_out, int accumulate_dt, void* dz,
-                          hipStream_t st);
+                          hipStream_t st, int m_is_z = 0);
 
 // ---- head, update, casts (head.hip) ------------------------------------
 size_t head_ws_bytes(int N, int C, int classes);

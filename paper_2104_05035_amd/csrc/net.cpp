@@ -68,7 +68,7 @@ struct AMPlan {
     RUPlan t1, t2, m1, m2, m3, m4;
     ConvL c1, c2;
     BnL bn;
-    TRef x, p1, p2, u1, h1c, h1, a, z, out, m;
+    TRef x, p1, p2, u1, h1c, h1, a, z, out;
     int64_t am1 = 0, am2 = 0;  // argmax byte offsets
 };
 
@@ -264,7 +264,6 @@ struct Builder {
         a.h1 = act(pre + "c1out", x.s);
         a.a = act(pre + "a", x.s);
         a.z = act(pre + "z", x.s);
-        a.m = act(pre + "m", x.s, false);
         a.out = act(pre + "out", x.s);
         return a;
     }
@@ -405,7 +404,8 @@ rat3d_status am_fwd(const Exec& e, const AMPlan& m) {
                      e.st));
     RAT3D_TRY(e.bn_f(m.bn, m.h1, nullptr, 1, e.a(m.a)));
     RAT3D_TRY(e.conv_f(m.c2, e.a(m.a), e.a(m.z)));
-    return softmask_fwd(s.count(), dt, e.a(m.z), e.a(m.t2.y), e.a(m.out), e.a(m.m), e.st);
+    // m is not stored: the backward recomputes it from z (same bits)
+    return softmask_fwd(s.count(), dt, e.a(m.z), e.a(m.t2.y), e.a(m.out), nullptr, e.st);
 }
 
 rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
@@ -413,8 +413,8 @@ rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
     const Shape& s1 = m.p1.s;
     const Shape& s2 = m.p2.s;
     const rat3d_dtype dt = e.n->dt;
-    RAT3D_TRY(softmask_bwd(s.count(), dt, e.g(m.out), e.a(m.t2.y), e.a(m.m), e.g(m.t2.y), 0,
-                           e.g(m.z), e.st));
+    RAT3D_TRY(softmask_bwd(s.count(), dt, e.g(m.out), e.a(m.t2.y), e.a(m.z), e.g(m.t2.y), 0,
+                           e.g(m.z), e.st, 1));
     RAT3D_TRY(e.conv_d(m.c2, e.g(m.z), e.g(m.a), 0));
     RAT3D_TRY(e.conv_w(m.c2, e.a(m.a), e.g(m.z)));
     RAT3D_TRY(e.bn_bwd_x(m.bn, e.g(m.a), m.h1, e.g(m.h1)));

@@ -209,7 +209,7 @@ __global__ __launch_bounds__(kEwThreads) void softmask_fwd_k(const T* __restrict
 template <typename T, int VEC>
 __global__ __launch_bounds__(kEwThreads) void softmask_bwd_k(
     const T* __restrict__ dout, const T* __restrict__ t, const T* __restrict__ m, int64_t count,
-    T* __restrict__ dt, int accumulate_dt, T* __restrict__ dz) {
+    T* __restrict__ dt, int accumulate_dt, T* __restrict__ dz, int m_is_z) {
     const int64_t i = ((int64_t)blockIdx.x * kEwThreads + threadIdx.x) * VEC;
     if (i >= count) return;
     float g[VEC], tv[VEC], mv[VEC], a[VEC], b[VEC];
@@ -217,6 +217,12 @@ __global__ __launch_bounds__(kEwThreads) void softmask_bwd_k(
     vload<T, VEC>(t + i, tv);
     vload<T, VEC>(m + i, mv);
     if (accumulate_dt) vload<T, VEC>(dt + i, b);
+    if (m_is_z) {
+        // m was not stored: recompute it from z and round it as the forward's
+        // store would have (same sigmoid, same rounding), so the bits match
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) mv[j] = Elt<T>::round(sigmoidf(mv[j]));
+    }
 #pragma unroll
     for (int j = 0; j < VEC; ++j) {
         a[j] = (1.f + mv[j]) * g[j];
@@ -1086,29 +1092,29 @@ rat3d_status softmask_fwd(int64_t count, rat3d_dtype dt, const void* z, const vo
 
 rat3d_status softmask_bwd(int64_t count, rat3d_dtype dt, const void* dout, const void* t,
                           const void* m, void* dt_out, int accumulate_dt, void* dz,
-                          hipStream_t st) {
+                          hipStream_t st, int m_is_z) {
     ProfScope ps("softmask_bwd", st, 0.0,
                  (dt == RAT3D_BF16 ? 2.0 : 4.0) * count * (5 + accumulate_dt));
     if (dt == RAT3D_BF16) {
         if (count % 8 == 0)
             softmask_bwd_k<bf16, 8><<<(unsigned)ceil_div(count / 8, kEwThreads), kEwThreads, 0,
                                       st>>>((const bf16*)dout, (const bf16*)t, (const bf16*)m,
-                                            count, (bf16*)dt_out, accumulate_dt, (bf16*)dz);
+                                            count, (bf16*)dt_out, accumulate_dt, (bf16*)dz, m_is_z);
         else
             softmask_bwd_k<bf16, 1><<<(unsigned)ceil_div(count, kEwThreads), kEwThreads, 0,
                                       st>>>((const bf16*)dout, (const bf16*)t, (const bf16*)m,
-                                            count, (bf16*)dt_out, accumulate_dt, (bf16*)dz);
+                                            count, (bf16*)dt_out, accumulate_dt, (bf16*)dz, m_is_z);
     } else {
         if (count % 4 == 0)
             softmask_bwd_k<float, 4><<<(unsigned)ceil_div(count / 4, kEwThreads), kEwThreads, 0,
                                        st>>>((const float*)dout, (const float*)t,
                                              (const float*)m, count, (float*)dt_out,
-                                             accumulate_dt, (float*)dz);
+                                             accumulate_dt, (float*)dz, m_is_z);
         else
             softmask_bwd_k<float, 1><<<(unsigned)ceil_div(count, kEwThreads), kEwThreads, 0,
                                        st>>>((const float*)dout, (const float*)t,
                                              (const float*)m, count, (float*)dt_out,
-                                             accumulate_dt, (float*)dz);
+                                             accumulate_dt, (float*)dz, m_is_z);
     }
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
