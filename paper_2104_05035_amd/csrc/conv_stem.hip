@@ -228,6 +228,25 @@ __global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
         const int d0 = tdi * kGD, h0 = thi * kGH, w0 = twi * kGW;
         const int bd = d0 * kSS - kSP, bh = h0 * kSS - kSP, bw = w0 * kSS - kSP;
         const bf16* xp = a.x + (int64_t)n * a.D * HW;
+        // The dy fragments of the brick's steps are requested before the
+        // staging, so their round trip overlaps it and the MFMA loop below
+        // waits for no global load (outside the volume: the plane's first
+        // voxels, zeroed at their use).
+        constexpr int kSteps = kGD * kGH / 2;
+        uint4 dyr[kSteps][2];
+        bool dok[kSteps];
+#pragma unroll
+        for (int s = 0; s < kSteps; ++s) {
+            const int dl = s / (kGH / 2);
+            const int hl = (s % (kGH / 2)) * 2 + hl_l;
+            const int d = d0 + dl, h = h0 + hl, w = w0 + wl;
+            dok[s] = d < a.Do && h < a.Ho && w + 8 <= a.Wo;
+            const int64_t vo = dok[s] ? ((int64_t)d * a.Ho + h) * a.Wo + w : 0;
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct)
+                dyr[s][ct] = *reinterpret_cast<const uint4*>(
+                    a.dy + ((int64_t)n * kSCo + ct * 16 + li) * Vo + vo);
+        }
         __syncthreads();
         // Staging (W % 8 == 0): brick column c is input column a0 + 5 + c
         // (a0 = bw - 5, a multiple of 8).  With G the row's dwords from a0,
@@ -277,22 +296,13 @@ __global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
             }
         }
         __syncthreads();
-#pragma unroll 1
-        for (int s = 0; s < kGD * kGH / 2; ++s) {
+#pragma unroll
+        for (int s = 0; s < kSteps; ++s) {
             const int dl = s / (kGH / 2);
             const int hl = (s % (kGH / 2)) * 2 + hl_l;
-            const int d = d0 + dl, h = h0 + hl, w = w0 + wl;
-            const bool ok = d < a.Do && h < a.Ho && w + 8 <= a.Wo;
-            // unconditional load (outside the volume: the plane's first
-            // voxels, zeroed), so it is not waited for on the spot
-            const int64_t vo = ok ? ((int64_t)d * a.Ho + h) * a.Wo + w : 0;
             F16B av[2];
 #pragma unroll
-            for (int ct = 0; ct < 2; ++ct) {
-                const uint4 u = *reinterpret_cast<const uint4*>(
-                    a.dy + ((int64_t)n * kSCo + ct * 16 + li) * Vo + vo);
-                av[ct].u = ok ? u : make_uint4(0u, 0u, 0u, 0u);
-            }
+            for (int ct = 0; ct < 2; ++ct) av[ct].u = dok[s] ? dyr[s][ct] : make_uint4(0u, 0u, 0u, 0u);
 #pragma unroll
             for (int j = 0; j < kTilesPerWave; ++j) {
                 const int tile = wave + 4 * j;
