@@ -28,6 +28,7 @@
 #include "kernels.hpp"
 #include "vec.hpp"
 #include "prof.hpp"
+#include "bn_coef.hpp"
 
 namespace rat3d {
 
@@ -125,85 +126,6 @@ __global__ __launch_bounds__(kBnThreads) void bn_fwd_stats(const T* __restrict__
     }
 }
 
-// Sums the slice partial pairs of channel c in float64 in a fixed order:
-// lane l adds slices l, l + 64, ... in turn, then an xor butterfly over the
-// wave; every lane of every wave ends with the same bits (each butterfly
-// level adds the same pairs of values, and float addition commutes).  All
-// 64 lanes must be active.
-__device__ __forceinline__ void wave_sum_partials(const float* __restrict__ part, int c,
-                                                  int slices, double& s1, double& s2) {
-    const int lane = (int)(threadIdx.x & 63);
-    const float2* pc = reinterpret_cast<const float2*>(part + (int64_t)c * slices * 2);
-    double a = 0.0, b = 0.0;
-    // four loads in flight per lane; slices past the end add nothing
-    for (int i = lane; i < slices; i += 256) {
-        float2 q[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) q[u] = pc[i + 64 * u < slices ? i + 64 * u : i];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const bool in = i + 64 * u < slices;
-            a += in ? (double)q[u].x : 0.0;
-            b += in ? (double)q[u].y : 0.0;
-        }
-    }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-        a += __shfl_xor(a, m, 64);
-        b += __shfl_xor(b, m, 64);
-    }
-    s1 = a;
-    s2 = b;
-}
-
-// Per channel: combine the slice partials in a fixed order in float64 into
-// the apply coefficients (scale, shift).  Every apply block of the channel
-// evaluates this identically; the block given `owner` also stores mean,
-// invstd, the coefficients and the running statistics.
-__device__ __forceinline__ void bn_fwd_coefs(int N, int C, int64_t V,
-                                             int slices, int c, const float* __restrict__ part,
-                                             const float* __restrict__ gamma,
-                                             const float* __restrict__ beta, float eps,
-                                             float momentum, bool owner,
-                                             float* __restrict__ save_mean,
-                                             float* __restrict__ save_invstd,
-                                             float* __restrict__ run_mean,
-                                             float* __restrict__ run_var,
-                                             float* __restrict__ save_coef, float& scale,
-                                             float& bias) {
-    const double shift = (double)part[(int64_t)C * slices * 2 + c];
-    double s1, s2;
-    wave_sum_partials(part, c, slices, s1, s2);
-    const double M = (double)N * (double)V;
-    const double dm = s1 / M;
-    double var = s2 / M - dm * dm;
-    if (var < 0.0) var = 0.0;
-    const double mean = shift + dm;
-    const double invstd = 1.0 / sqrt(var + (double)eps);
-    scale = (float)((double)gamma[c] * invstd);
-    bias = (float)((double)beta[c] - mean * (double)scale);
-    if (!owner) return;
-    save_mean[c] = (float)mean;
-    save_invstd[c] = (float)invstd;
-    if (save_coef) {
-        save_coef[c] = scale;
-        save_coef[C + c] = bias;
-    }
-    if (run_mean) run_mean[c] = (float)((1.0 - momentum) * run_mean[c] + momentum * mean);
-    if (run_var) {
-        const double unb = M > 1.0 ? var * M / (M - 1.0) : var;
-        run_var[c] = (float)((1.0 - momentum) * run_var[c] + momentum * unb);
-    }
-}
-
-struct BnFwdStats {
-    const float* part;
-    int slices;
-    const float* gamma;
-    const float* beta;
-    float eps, momentum;
-    float *save_mean, *save_invstd, *run_mean, *run_var, *save_coef;
-};
 
 // One-dimensional grid: block b covers chunk b % cpp of plane b / cpp.  The
 // block first loads its elements, then derives its channel's coefficients
@@ -337,35 +259,6 @@ __global__ __launch_bounds__(kBnThreads) void bn_bwd_stats(const T* __restrict__
         o[0] = s1;
         o[1] = s2;
     }
-}
-
-struct BnBwdStats {
-    const float* part;
-    int slices;
-    const float* gamma;
-    const float* save_invstd;
-    float *dgamma, *dbeta;
-    int accumulate;
-};
-
-// Per channel: dbeta, dgamma and the apply coefficients from the slice
-// partials (fixed order, float64).  Every apply block of the channel
-// evaluates this identically; the block given `owner` stores dgamma, dbeta.
-__device__ __forceinline__ void bn_bwd_coefs(int N, int64_t V, int c, const BnBwdStats& st,
-                                             bool owner, float& k, float& a, float& b) {
-    double s1, s2;
-    wave_sum_partials(st.part, c, st.slices, s1, s2);
-    const double invstd = st.save_invstd[c];
-    const double db = s1, dg = s2 * invstd;
-    if (owner) {
-        st.dbeta[c] = (float)(st.accumulate ? (double)st.dbeta[c] + db : db);
-        st.dgamma[c] = (float)(st.accumulate ? (double)st.dgamma[c] + dg : dg);
-    }
-    const double M = (double)N * (double)V;
-    // dx = k * (g - db/M - (x - mean) * invstd * dg/M)
-    k = (float)((double)st.gamma[c] * invstd);
-    a = (float)(db / M);
-    b = (float)(invstd * dg / M);
 }
 
 // DRES: 0 no residual gradient, 1 dres = g, 2 dres += g (one rounding).
@@ -567,6 +460,56 @@ rat3d_status bn_bwd(const BnGeom& g, rat3d_dtype dt, int relu, const void* dy, c
     return bn_bwd_t<float, 1>(g, relu, (const float*)dy, (const float*)x, (const float*)y,
                               nullptr, gamma, save_mean, save_invstd, fwd_coef, (float*)dx,
                               (float*)dres, dres_acc, dgamma, dbeta, accumulate, ws, st);
+}
+
+// ---------------------------------------------------------------- pieces for fused passes
+// The backward statistics pass alone (bf16, V % 8 == 0, mask from x with the
+// forward's coefficients); *bs receives what an apply done elsewhere needs.
+rat3d_status bn_bwd_stats_x(const BnGeom& g, const void* dy, const void* x, const float* gamma,
+                            const float* save_mean, const float* save_invstd,
+                            const float* fwd_coef, float* dgamma, float* dbeta, int accumulate,
+                            void* ws, hipStream_t st, BnBwdStats* bs) {
+    if (g.V % 8 != 0 || !fwd_coef) {
+        set_error("bn_bwd_stats_x: needs V %% 8 == 0 and the forward's coefficients");
+        return RAT3D_EUNSUPPORTED;
+    }
+    const BnSlices sl = bn_slices(g);
+    float* part = (float*)ws;
+    const double tb = (double)g.N * g.C * g.V * sizeof(bf16);
+    ProfScope ps("bn_bwd_stats", st, 0.0, tb * 2);
+    bn_bwd_stats<bf16, 8, kMaskX><<<dim3(g.C, sl.per_channel), kBnThreads, 0, st>>>(
+        (const bf16*)dy, (const bf16*)x, nullptr, nullptr, g.C, g.V, sl.per_plane, sl.len,
+        save_mean, fwd_coef, part);
+    RAT3D_LAUNCH_CHECK();
+    *bs = BnBwdStats{part, sl.per_channel, gamma, save_invstd, dgamma, dbeta, accumulate};
+    return RAT3D_OK;
+}
+
+size_t bn_max_slices(const BnGeom& g) { return (size_t)bn_slices(g).per_channel; }
+
+// The forward apply (BN + ReLU, no residual, bf16, V % 8 == 0) from statistics
+// partials someone else produced: `slices` pairs per channel at part, the
+// shift of channel c at part[C * slices * 2 + c].
+rat3d_status bn_fwd_apply_from(const BnGeom& g, float eps, float momentum, const void* x,
+                               const float* gamma, const float* beta, void* y,
+                               float* save_mean, float* save_invstd, float* run_mean,
+                               float* run_var, float* save_coef, const float* part, int slices,
+                               hipStream_t st) {
+    if (g.V % 8 != 0) {
+        set_error("bn_fwd_apply_from: needs V %% 8 == 0");
+        return RAT3D_EUNSUPPORTED;
+    }
+    const BnFwdStats fs{part,     slices,      gamma,    beta,    eps,      momentum,
+                        save_mean, save_invstd, run_mean, run_var, save_coef};
+    const int fu = fwd_apply_u<false>();
+    const unsigned cpp = (unsigned)ceil_div(g.V / 8, kBnThreads * fu);
+    const unsigned grid = cpp * (unsigned)(g.N * g.C);
+    const double tb = (double)g.N * g.C * g.V * sizeof(bf16);
+    ProfScope ps("bn_fwd_apply", st, 0.0, tb * 2);
+    bn_fwd_apply<bf16, 8, true, false><<<grid, kBnThreads, 0, st>>>(
+        (const bf16*)x, nullptr, g.N, g.C, g.V, cpp, fs, (bf16*)y, nullptr);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
 }
 
 }  // namespace rat3d

@@ -130,6 +130,19 @@ rat3d_status bn_bwd(const BnGeom& g, rat3d_dtype dt, int relu, const void* dy, c
                     void* dx, void* dres, int dres_acc, float* dgamma, float* dbeta,
                     int accumulate, void* ws, hipStream_t st);
 
+// Pieces for the fused passes of the soft-mask branch (bf16, V % 8 == 0).
+struct BnBwdStats;
+rat3d_status bn_bwd_stats_x(const BnGeom& g, const void* dy, const void* x, const float* gamma,
+                            const float* save_mean, const float* save_invstd,
+                            const float* fwd_coef, float* dgamma, float* dbeta, int accumulate,
+                            void* ws, hipStream_t st, BnBwdStats* bs);
+size_t bn_max_slices(const BnGeom& g);
+rat3d_status bn_fwd_apply_from(const BnGeom& g, float eps, float momentum, const void* x,
+                               const float* gamma, const float* beta, void* y,
+                               float* save_mean, float* save_invstd, float* run_mean,
+                               float* run_var, float* save_coef, const float* part, int slices,
+                               hipStream_t st);
+
 // ---- soft-mask branch (softmask.hip) -----------------------------------
 rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, rat3d_dtype dt,
                       const void* x, void* y, uint8_t* argmax, hipStream_t st);
@@ -147,6 +160,19 @@ rat3d_status softmask_fwd(int64_t count, rat3d_dtype dt, const void* z, const vo
 rat3d_status softmask_bwd(int64_t count, rat3d_dtype dt, const void* dout, const void* t,
                           const void* m, void* dt_out, int accumulate_dt, void* dz,
                           hipStream_t st, int m_is_z = 0);
+// relu(BN(up(xc))) with an exact x2 upsampling (bf16): the upsampling pass
+// also yields the BN statistics (h = up(xc) is written for the backward);
+// the backward forms h's gradient inside the upsampling transpose.
+bool up2_bn_ok(int N, int C, int Di, int Hi, int Wi, rat3d_dtype dt);
+rat3d_status up2_bn_relu_fwd(int N, int C, int Di, int Hi, int Wi, const void* xc, void* h,
+                             float eps, float momentum, const float* gamma, const float* beta,
+                             void* y, float* save_mean, float* save_invstd, float* run_mean,
+                             float* run_var, float* save_coef, void* bn_ws, hipStream_t st);
+rat3d_status bn_relu_bwd_up2(int N, int C, int Di, int Hi, int Wi, const void* dy, const void* h,
+                             const float* gamma, const float* save_mean,
+                             const float* save_invstd, const float* fwd_coef, float* dgamma,
+                             float* dbeta, int accumulate, void* bn_ws, void* dxc,
+                             hipStream_t st);
 
 // ---- head, update, casts (head.hip) ------------------------------------
 size_t head_ws_bytes(int N, int C, int classes);

@@ -382,6 +382,15 @@ rat3d_status ru_bwd(const Exec& e, const RUPlan& r, bool acc_dx, bool need_dx = 
     return e.conv_w(r.c1, e.a(r.x), e.g(r.h1));
 }
 
+// The mask tail's upsampling and BN run fused when the upsampling is an exact
+// x2 of a bf16 map the plane kernels take.
+static bool fuse_up_bn(const AMPlan& m, rat3d_dtype dt) {
+    const Shape& s = m.x.s;
+    const Shape& s1 = m.p1.s;
+    return s.d == 2 * s1.d && s.h == 2 * s1.h && s.w == 2 * s1.w &&
+           up2_bn_ok(s.n, s.c, s1.d, s1.h, s1.w, dt);
+}
+
 rat3d_status am_fwd(const Exec& e, const AMPlan& m) {
     const Shape& s = m.x.s;
     const rat3d_dtype dt = e.n->dt;
@@ -400,9 +409,17 @@ rat3d_status am_fwd(const Exec& e, const AMPlan& m) {
                      e.st));
     RAT3D_TRY(ru_fwd(e, m.m4));
     RAT3D_TRY(e.conv_f(m.c1, e.a(m.m4.y), e.a(m.h1c)));
-    RAT3D_TRY(up_fwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.a(m.h1c), e.a(m.h1),
-                     e.st));
-    RAT3D_TRY(e.bn_f(m.bn, m.h1, nullptr, 1, e.a(m.a)));
+    if (fuse_up_bn(m, dt)) {
+        // the x2 upsampling also yields the BN statistics of its output
+        RAT3D_TRY(up2_bn_relu_fwd(s.n, s.c, s1.d, s1.h, s1.w, e.a(m.h1c), e.a(m.h1),
+                                  e.n->d.bn_eps, e.n->d.bn_momentum, e.par(m.bn.g_off),
+                                  e.par(m.bn.b_off), e.a(m.a), e.mean(m.bn), e.invstd(m.bn),
+                                  e.rmean(m.bn), e.rvar(m.bn), e.fcoef(m.bn), e.bn_scr(), e.st));
+    } else {
+        RAT3D_TRY(up_fwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.a(m.h1c), e.a(m.h1),
+                         e.st));
+        RAT3D_TRY(e.bn_f(m.bn, m.h1, nullptr, 1, e.a(m.a)));
+    }
     RAT3D_TRY(e.conv_f(m.c2, e.a(m.a), e.a(m.z)));
     // m is not stored: the backward recomputes it from z (same bits)
     return softmask_fwd(s.count(), dt, e.a(m.z), e.a(m.t2.y), e.a(m.out), nullptr, e.st);
@@ -417,9 +434,18 @@ rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
                            e.g(m.z), e.st, 1));
     RAT3D_TRY(e.conv_d(m.c2, e.g(m.z), e.g(m.a), 0));
     RAT3D_TRY(e.conv_w(m.c2, e.a(m.a), e.g(m.z)));
-    RAT3D_TRY(e.bn_bwd_x(m.bn, e.g(m.a), m.h1, e.g(m.h1)));
-    RAT3D_TRY(up_bwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.g(m.h1), e.g(m.h1c), 0,
-                     e.st));
+    if (fuse_up_bn(m, dt)) {
+        // the BN apply happens inside the upsampling transpose: h1's gradient
+        // is never stored
+        RAT3D_TRY(bn_relu_bwd_up2(s.n, s.c, s1.d, s1.h, s1.w, e.g(m.a), e.a(m.h1),
+                                  e.par(m.bn.g_off), e.mean(m.bn), e.invstd(m.bn), e.fcoef(m.bn),
+                                  e.grd(m.bn.g_off), e.grd(m.bn.b_off), e.acc, e.bn_scr(),
+                                  e.g(m.h1c), e.st));
+    } else {
+        RAT3D_TRY(e.bn_bwd_x(m.bn, e.g(m.a), m.h1, e.g(m.h1)));
+        RAT3D_TRY(up_bwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.g(m.h1), e.g(m.h1c),
+                         0, e.st));
+    }
     RAT3D_TRY(e.conv_d(m.c1, e.g(m.h1c), e.g(m.m4.y), 0));
     RAT3D_TRY(e.conv_w(m.c1, e.a(m.m4.y), e.g(m.h1c)));
     RAT3D_TRY(ru_bwd(e, m.m4, false));

@@ -7,6 +7,7 @@
 #include "kernels.hpp"
 #include "vec.hpp"
 #include "prof.hpp"
+#include "bn_coef.hpp"
 
 namespace rat3d {
 
@@ -688,9 +689,20 @@ __global__ __launch_bounds__(kEwThreads) void pool332_bwd_pl(const bf16* __restr
 // 2*m0 .. 2*m0 + 2*kPlanes - 1.  Phase A blends coarse planes m0-1 .. m0+kPlanes
 // along depth into LDS (float32); phase B blends rows and columns and writes
 // 8 fine voxels of a row per item.
+// With STATS, the block also sums (y - shift) and its square over the fine
+// values it stores (as stored, bf16), shift = the first fine value of sample
+// 0 of its channel (= the coarse value there), into the BN statistics
+// partial (c, n * nblk + block): the statistics pass of a batch norm applied
+// to y, without reading y again.
+struct UpStats {
+    float* part;  // [C][N * nblk] pairs, then the C shifts
+    int C, N;
+};
+
+template <bool STATS>
 __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict__ x, int Di,
                                                          int Hi, int Wi, int nblk,
-                                                         bf16* __restrict__ y) {
+                                                         bf16* __restrict__ y, UpStats us) {
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int NF = 2 * kPlanes;
     const int HWi = Hi * Wi, HW8 = (HWi + 7) & ~7;
@@ -698,6 +710,8 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
     const int L = xcd_remap(blockIdx.x, gridDim.x);
     const int nc = L / nblk, m0 = (L - nc * nblk) * kPlanes;
     const int Do = 2 * Di, Ho = 2 * Hi, Wo = 2 * Wi;
+    [[maybe_unused]] float s1 = 0.f, s2 = 0.f, shift = 0.f;
+    if constexpr (STATS) shift = bf2f(x[(int64_t)(nc % us.C) * Di * Hi * Wi]);
     const bool vec = (HWi & 7) == 0;
     const bf16* xv = x + (int64_t)nc * Di * HWi;
     for (int p = threadIdx.x * 8; p < HWi; p += kEwThreads * 8) {
@@ -793,6 +807,45 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
             w4[i] = pack_bf16x2(out[2 * i], out[2 * i + 1]);
         *reinterpret_cast<uint4*>(y + (((int64_t)nc * Do + od) * Ho + oh) * Wo + 8 * g) =
             make_uint4(w4[0], w4[1], w4[2], w4[3]);
+        if constexpr (STATS) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float lo = __uint_as_float(w4[i] << 16) - shift;
+                const float hi = __uint_as_float(w4[i] & 0xffff0000u) - shift;
+                s1 += lo;
+                s2 += lo * lo;
+                s1 += hi;
+                s2 += hi * hi;
+            }
+        }
+    }
+    if constexpr (STATS) {
+        // fixed-order block sum: xor butterfly in each wave, then the waves in order
+        __shared__ float red[2][kEwThreads / 64];
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) {
+            s1 += __shfl_xor(s1, m, 64);
+            s2 += __shfl_xor(s2, m, 64);
+        }
+        if ((threadIdx.x & 63) == 0) {
+            red[0][threadIdx.x >> 6] = s1;
+            red[1][threadIdx.x >> 6] = s2;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            float a = 0.f, b = 0.f;
+#pragma unroll
+            for (int wv = 0; wv < kEwThreads / 64; ++wv) {
+                a += red[0][wv];
+                b += red[1][wv];
+            }
+            const int c = nc % us.C, n = nc / us.C, blk = L - nc * nblk;
+            const int slices = us.N * nblk;
+            float* o = us.part + ((int64_t)c * slices + (int64_t)n * nblk + blk) * 2;
+            o[0] = a;
+            o[1] = b;
+            if (n == 0 && blk == 0) us.part[(int64_t)us.C * slices * 2 + c] = shift;
+        }
     }
 }
 
@@ -800,9 +853,24 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
 // m0 .. m0 + kPlanes - 1; phase A blends fine planes 2*m0-1 .. 2*m0+2*kPlanes
 // along depth into LDS (float32), phase B gathers the 4 x 10 fine rows and
 // columns of 4 consecutive coarse voxels of a row.
+// With BN, the fine gradient is not read but formed on the fly: dy holds the
+// gradient of a = relu(BN(h)) and the fine input is the BN backward's dh =
+// k (g - a - (h - mean) b), g = dy where h * scale + shift > 0 (the forward's
+// coefficients), rounded as its store would be -- the batch norm's apply pass
+// and this transpose in one kernel (h and dh at the fine size).
+struct UpBn {
+    const bf16* h;       // BN input, fine
+    const float* mean;   // saved batch mean [C]
+    const float* fcoef;  // forward scale [C], shift [C]
+    BnBwdStats st;
+    int C, N;
+};
+
+template <bool BN>
 __global__ __launch_bounds__(kEwThreads) void up2_bwd_pl(const bf16* __restrict__ dy, int Di,
                                                          int Hi, int Wi, int nblk,
-                                                         bf16* __restrict__ dx, int accumulate) {
+                                                         bf16* __restrict__ dx, int accumulate,
+                                                         UpBn ub) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int Do = 2 * Di, Ho = 2 * Hi, Wo = 2 * Wi;
     const int HWo = Ho * Wo;  // a multiple of 8 (Wo % 8 == 0)
@@ -810,6 +878,18 @@ __global__ __launch_bounds__(kEwThreads) void up2_bwd_pl(const bf16* __restrict_
     const int L = xcd_remap(blockIdx.x, gridDim.x);
     const int nc = L / nblk, m0 = (L - nc * nblk) * kPlanes;
     const bf16* gv = dy + (int64_t)nc * Do * HWo;
+    [[maybe_unused]] float bk = 0.f, ba = 0.f, bb = 0.f, bmean = 0.f, fsc = 0.f, fsh = 0.f;
+    [[maybe_unused]] const bf16* hv = nullptr;
+    if constexpr (BN) {
+        // every lane is active here, as the coefficient reduction needs
+        const int c = nc % ub.C;
+        bn_bwd_coefs(ub.N, (int64_t)Do * HWo, c, ub.st,
+                     nc < ub.C && L - nc * nblk == 0 && threadIdx.x == 0, bk, ba, bb);
+        bmean = ub.mean[c];
+        fsc = ub.fcoef[c];
+        fsh = ub.fcoef[ub.C + c];
+        hv = ub.h + (int64_t)nc * Do * HWo;
+    }
     for (int p = threadIdx.x * 8; p < HWo; p += kEwThreads * 8) {
         float acc[kPlanes][8];
 #pragma unroll
@@ -819,10 +899,12 @@ __global__ __launch_bounds__(kEwThreads) void up2_bwd_pl(const bf16* __restrict_
         // all fine planes are requested before any is used (clamped index)
         constexpr int NQ = 2 * kPlanes + 2;
         uint4 raw[NQ];
+        [[maybe_unused]] uint4 rawh[NQ];
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int od = min(max(2 * m0 - 1 + q, 0), Do - 1);
             raw[q] = *reinterpret_cast<const uint4*>(gv + (int64_t)od * HWo + p);
+            if constexpr (BN) rawh[q] = *reinterpret_cast<const uint4*>(hv + (int64_t)od * HWo + p);
         }
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
@@ -835,6 +917,18 @@ __global__ __launch_bounds__(kEwThreads) void up2_bwd_pl(const bf16* __restrict_
                 for (int i = 0; i < 4; ++i) {
                     v[2 * i] = __uint_as_float(w[i] << 16);
                     v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+                }
+                if constexpr (BN) {
+                    const uint32_t hw[4] = {rawh[q].x, rawh[q].y, rawh[q].z, rawh[q].w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float h0 = __uint_as_float(hw[i] << 16);
+                        const float h1 = __uint_as_float(hw[i] & 0xffff0000u);
+                        const float g0 = fmaf(h0, fsc, fsh) > 0.f ? v[2 * i] : 0.f;
+                        const float g1 = fmaf(h1, fsc, fsh) > 0.f ? v[2 * i + 1] : 0.f;
+                        v[2 * i] = Elt<bf16>::round(bk * (g0 - ba - (h0 - bmean) * bb));
+                        v[2 * i + 1] = Elt<bf16>::round(bk * (g1 - ba - (h1 - bmean) * bb));
+                    }
                 }
             }
 #pragma unroll
@@ -998,8 +1092,8 @@ rat3d_status up_fwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
     const size_t lds_f = (size_t)2 * kPlanes * ((Hi * Wi + 7) & ~7) * sizeof(float);
     if (x2 && dt == RAT3D_BF16 && Wi % 4 == 0 && lds_f <= kPlaneLds) {
         const int nblk = (int)ceil_div(Di, kPlanes);
-        up2_fwd_pl<<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_f, st>>>(
-            (const bf16*)x, Di, Hi, Wi, nblk, (bf16*)y);
+        up2_fwd_pl<false><<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_f, st>>>(
+            (const bf16*)x, Di, Hi, Wi, nblk, (bf16*)y, UpStats{});
         RAT3D_LAUNCH_CHECK();
         return RAT3D_OK;
     }
@@ -1036,8 +1130,8 @@ rat3d_status up_bwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
     const size_t lds_b = (size_t)kPlanes * Ho * Wo * sizeof(float);
     if (x2 && dt == RAT3D_BF16 && Wi % 4 == 0 && lds_b <= kPlaneLds) {
         const int nblk = (int)ceil_div(Di, kPlanes);
-        up2_bwd_pl<<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_b, st>>>(
-            (const bf16*)dy, Di, Hi, Wi, nblk, (bf16*)dx, accumulate);
+        up2_bwd_pl<false><<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_b, st>>>(
+            (const bf16*)dy, Di, Hi, Wi, nblk, (bf16*)dx, accumulate, UpBn{});
         RAT3D_LAUNCH_CHECK();
         return RAT3D_OK;
     }
@@ -1138,6 +1232,73 @@ rat3d_status add_tensors(int64_t count, rat3d_dtype dt, const void* a, const voi
             add_k<float, 1><<<(unsigned)ceil_div(count, kEwThreads), kEwThreads, 0, st>>>(
                 (const float*)a, (const float*)b, count, (float*)dst);
     }
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
+// ---------------------------------------------------------------- x2 upsampling + BN + ReLU
+// The soft-mask branch's y = relu(BN(up(xc))) with an exact x2 upsampling:
+// the forward writes h = up(xc) (kept: the backward needs it) and takes the
+// BN statistics partials from the same pass; the backward forms the
+// gradient of h on the fly inside the upsampling transpose (see up2_fwd_pl
+// and up2_bwd_pl).  bf16, Wi % 4 == 0, one workspace as batch norm's.
+static int up2_nblk(int Di) { return (int)ceil_div(Di, kPlanes); }
+
+bool up2_bn_ok(int N, int C, int Di, int Hi, int Wi, rat3d_dtype dt) {
+    const int64_t V = (int64_t)8 * Di * Hi * Wi;
+    const size_t lds_f = (size_t)2 * kPlanes * ((Hi * Wi + 7) & ~7) * sizeof(float);
+    const size_t lds_b = (size_t)kPlanes * 4 * Hi * Wi * sizeof(float);
+    return dt == RAT3D_BF16 && Wi % 4 == 0 && V % 8 == 0 && lds_f <= kPlaneLds &&
+           lds_b <= kPlaneLds &&
+           (size_t)N * up2_nblk(Di) <= bn_max_slices(BnGeom{N, C, V});
+}
+
+rat3d_status up2_bn_relu_fwd(int N, int C, int Di, int Hi, int Wi, const void* xc, void* h,
+                             float eps, float momentum, const float* gamma, const float* beta,
+                             void* y, float* save_mean, float* save_invstd, float* run_mean,
+                             float* run_var, float* save_coef, void* bn_ws, hipStream_t st) {
+    if (!up2_bn_ok(N, C, Di, Hi, Wi, RAT3D_BF16)) {
+        set_error("up2_bn_relu_fwd: unsupported shape");
+        return RAT3D_EUNSUPPORTED;
+    }
+    const int nblk = up2_nblk(Di);
+    const BnGeom g{N, C, (int64_t)8 * Di * Hi * Wi};
+    const size_t lds_f = (size_t)2 * kPlanes * ((Hi * Wi + 7) & ~7) * sizeof(float);
+    {
+        ProfScope ps("up_fwd", st, 0.0, 2.0 * ((double)N * C * Di * Hi * Wi + (double)N * C * g.V));
+        up2_fwd_pl<true><<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_f, st>>>(
+            (const bf16*)xc, Di, Hi, Wi, nblk, (bf16*)h, UpStats{(float*)bn_ws, C, N});
+        RAT3D_LAUNCH_CHECK();
+    }
+    return bn_fwd_apply_from(g, eps, momentum, h, gamma, beta, y, save_mean, save_invstd,
+                             run_mean, run_var, save_coef, (const float*)bn_ws, N * nblk, st);
+}
+
+rat3d_status bn_relu_bwd_up2(int N, int C, int Di, int Hi, int Wi, const void* dy, const void* h,
+                             const float* gamma, const float* save_mean,
+                             const float* save_invstd, const float* fwd_coef, float* dgamma,
+                             float* dbeta, int accumulate, void* bn_ws, void* dxc,
+                             hipStream_t st) {
+    if (!up2_bn_ok(N, C, Di, Hi, Wi, RAT3D_BF16) || !fwd_coef) {
+        set_error("bn_relu_bwd_up2: unsupported shape");
+        return RAT3D_EUNSUPPORTED;
+    }
+    const BnGeom g{N, C, (int64_t)8 * Di * Hi * Wi};
+    UpBn ub;
+    ub.h = (const bf16*)h;
+    ub.mean = save_mean;
+    ub.fcoef = fwd_coef;
+    ub.C = C;
+    ub.N = N;
+    const rat3d_status s0 = bn_bwd_stats_x(g, dy, h, gamma, save_mean, save_invstd, fwd_coef,
+                                           dgamma, dbeta, accumulate, bn_ws, st, &ub.st);
+    if (s0 != RAT3D_OK) return s0;
+    const int nblk = up2_nblk(Di);
+    const size_t lds_b = (size_t)kPlanes * 4 * Hi * Wi * sizeof(float);
+    ProfScope ps("bn_bwd_apply_up", st, 0.0,
+                 2.0 * (2.0 * N * C * g.V + (double)N * C * Di * Hi * Wi));
+    up2_bwd_pl<true><<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_b, st>>>(
+        (const bf16*)dy, Di, Hi, Wi, nblk, (bf16*)dxc, 0, ub);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }

@@ -9,7 +9,8 @@ checked on what the step left in the workspace (the last micro-batch's
 activations and gradients): the oracle applies the layer to the GPU's own
 stored inputs and is compared with the GPU's stored output -- convolutions at
 sampled output points (the oracle's point-evaluated loops), batch norm,
-pooling, upsampling and the soft-mask fuse over whole channels, the weight
+pooling, upsampling (with the fused BN) and the soft-mask fuse over whole
+channels, the weight
 gradient of a 3^3 layer at sampled entries (the C ABI's wgrad on the step's
 tensors), and the SGD update over the whole arena.  Gates as everywhere:
 2e-2 norm-wise for bf16 outputs, 1e-4 for float32 statistics, bit-exact for
@@ -213,13 +214,26 @@ def test_full_maxpool(full):
     chk(full.host("d:am.m1.y", cs), dref, "bf16", "pool gradient")
 
 
-def test_full_upsample(full):
-    """x2 trilinear 24x28x24 -> 48x56x48 and its transpose over whole channels."""
+def test_full_upsample_bn(full):
+    """Mask tail: x2 trilinear 24x28x24 -> 48x56x48 of the first 1^3 conv's
+    output, whose pass also yields the following BN's statistics, then BN +
+    ReLU; backward: the BN's input gradient formed inside the upsampling
+    transpose.  Whole channels, plus every channel's saved statistics."""
     cs = list(CHANNELS)
-    ref = ops.trilinear_fwd(full.host("am.c1out.coarse", cs), (48, 56, 48))
-    chk(full.host("am.c1out", cs), ref, "bf16", "upsampled c1 output")
-    ref = ops.trilinear_bwd(full.host("d:am.c1out", cs), (24, 28, 24))
-    chk(full.host("d:am.c1out.coarse", cs), ref, "bf16", "upsampling gradient")
+    h = full.host("am.c1out")
+    chk(full.host("am.c1out", cs), ops.trilinear_fwd(full.host("am.c1out.coarse", cs),
+                                                      (48, 56, 48)), "bf16", "upsampled c1 output")
+    mean, var = ops.bn_stats(h)
+    chk(full.host("am.bn.mean").ravel(), mean, "f32", "mask bn mean")
+    chk(full.host("am.bn.invstd").ravel(), 1.0 / np.sqrt(var + EPS), "f32", "mask bn invstd")
+    del h
+    hc = full.host("am.c1out", cs)
+    y, mc, _, ic = ops.bn_fwd(hc, full.old["am.bn.g"][cs], full.old["am.bn.b"][cs], EPS, True)
+    a = full.host("am.a", cs)
+    chk(a, y, "bf16", "mask bn + relu output")
+    dh, _, _, _ = ops.bn_bwd(full.host("d:am.a", cs), hc, a, full.old["am.bn.g"][cs], mc, ic, True)
+    chk(full.host("d:am.c1out.coarse", cs), ops.trilinear_bwd(dh, (24, 28, 24)), "bf16",
+        "mask bn + upsampling gradient")
 
 
 def test_full_softmask(full):
