@@ -644,11 +644,20 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
                 lds_barrier();
             } else if (tile_end(k) && staged_acc) {
                 lds_barrier();  // every consumer is done reading buf
-                for (int hf = 0; hf < WC; ++hf) {
-                    if (wc == hf) write_fp32(k, buf);
+                // column group wc is written after the groups before it were
+                // written and drained (two barriers each), then waits out the
+                // later ones: one write_fp32 call site, so the accumulators
+                // stay where the step loop keeps them
+                for (int hf = 0; hf < wc; ++hf) {
                     lds_barrier();
-                    if (hf + 1 < WC) lds_barrier();  // group hf drained
+                    lds_barrier();
                 }
+                write_fp32(k, buf);
+                for (int hf = wc; hf + 1 < WC; ++hf) {
+                    lds_barrier();
+                    lds_barrier();
+                }
+                lds_barrier();
             } else {
                 if (tile_end(k)) direct_outputs(k);
                 lds_barrier();
