@@ -26,6 +26,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
     return __builtin_bit_cast(uint32_t, v);
 }
+// The soft mask's sigmoid: one definition for every kernel that forms it, so
+// that a mask recomputed elsewhere has the same bits.
+__device__ __forceinline__ float sigmoidf(float z) { return 1.f / (1.f + expf(-z)); }
+
 // Storage-type traits: load as float, store from float.
 template <typename T> struct Elt;
 template <> struct Elt<float> {

@@ -185,7 +185,6 @@ __global__ __launch_bounds__(kEwThreads) void up_bwd_k(const T* __restrict__ dy,
 }
 
 // ---------------------------------------------------------------- sigmoid fuse
-__device__ __forceinline__ float sigmoidf(float z) { return 1.f / (1.f + expf(-z)); }
 
 template <typename T, int VEC>
 __global__ __launch_bounds__(kEwThreads) void softmask_fwd_k(const T* __restrict__ z,
