@@ -37,7 +37,7 @@ constexpr int kStatsUnroll = 4;  // vectors per tensor in flight per thread in t
 // vectors per thread in the apply passes (measured: only the two-stream
 // forward apply, which has the least work per wave to hide its coefficient
 // reduction behind, gains from more than one)
-template <bool RES> constexpr int fwd_apply_u() { return RES ? 1 : 4; }
+template <int RES> constexpr int fwd_apply_u() { return RES ? 1 : 4; }
 constexpr int kBwdApplyU = 1;
 
 struct BnSlices {
@@ -130,12 +130,16 @@ __global__ __launch_bounds__(kBnThreads) void bn_fwd_stats(const T* __restrict__
 // One-dimensional grid: block b covers chunk b % cpp of plane b / cpp.  The
 // block first loads its elements, then derives its channel's coefficients
 // from the statistics partials (the first chunk of plane (0, c) stores them).
-template <typename T, int VEC, bool RELU, bool RES>
+// RES: 0 no residual, 1 y += r, 2 y += BN_r(r) with the residual's own batch
+// norm (no ReLU) formed here from its statistics partials `rst` and rounded as
+// its own apply would store it.
+template <typename T, int VEC, bool RELU, int RES>
 __global__ __launch_bounds__(kBnThreads) void bn_fwd_apply(const T* __restrict__ x,
                                                            const T* __restrict__ r, int N, int C,
                                                            int64_t V, unsigned cpp,
                                                            BnFwdStats st, T* __restrict__ y,
-                                                           uint8_t* __restrict__ ybits) {
+                                                           uint8_t* __restrict__ ybits,
+                                                           BnFwdStats rst) {
     constexpr int U = fwd_apply_u<RES>();
     constexpr int64_t kStep = (int64_t)kBnThreads * VEC;
     const int plane = (int)(blockIdx.x / cpp);  // wave-uniform
@@ -156,9 +160,14 @@ __global__ __launch_bounds__(kBnThreads) void bn_fwd_apply(const T* __restrict__
         if constexpr (RES) vload<T, VEC>(r + i, rv[u]);
     }
     float sc, sh;
-    bn_fwd_coefs(N, C, V, st.slices, c, st.part, st.gamma, st.beta, st.eps, st.momentum,
-                 plane < C && chunk == 0 && threadIdx.x == 0, st.save_mean, st.save_invstd,
-                 st.run_mean, st.run_var, st.save_coef, sc, sh);
+    const bool owner = plane < C && chunk == 0 && threadIdx.x == 0;
+    bn_fwd_coefs(N, C, V, st.slices, c, st.part, st.gamma, st.beta, st.eps, st.momentum, owner,
+                 st.save_mean, st.save_invstd, st.run_mean, st.run_var, st.save_coef, sc, sh);
+    [[maybe_unused]] float rsc = 1.f, rsh = 0.f;
+    if constexpr (RES == 2)
+        bn_fwd_coefs(N, C, V, rst.slices, c, rst.part, rst.gamma, rst.beta, rst.eps,
+                     rst.momentum, owner, rst.save_mean, rst.save_invstd, rst.run_mean,
+                     rst.run_var, rst.save_coef, rsc, rsh);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int64_t e = e0 + u * kStep;
@@ -166,7 +175,8 @@ __global__ __launch_bounds__(kBnThreads) void bn_fwd_apply(const T* __restrict__
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
             float o = fmaf(v[u][j], sc, sh);
-            if constexpr (RES) o += rv[u][j];
+            if constexpr (RES == 1) o += rv[u][j];
+            if constexpr (RES == 2) o += Elt<T>::round(fmaf(rv[u][j], rsc, rsh));
             if constexpr (RELU) o = fmaxf(o, 0.f);
             v[u][j] = o;
         }
@@ -340,17 +350,17 @@ static rat3d_status bn_fwd_t(const BnGeom& g, int relu, float eps, float momentu
     }
     const BnFwdStats fs{part,     sl.per_channel, gamma,   beta,   eps,      momentum,
                         save_mean, save_invstd,   run_mean, run_var, save_coef};
-    const int fu = r ? fwd_apply_u<true>() : fwd_apply_u<false>();
+    const int fu = r ? fwd_apply_u<1>() : fwd_apply_u<0>();
     const unsigned cpp = (unsigned)ceil_div(g.V / VEC, kBnThreads * fu);  // chunks per plane
     const unsigned grid = cpp * (unsigned)(g.N * g.C);
     ProfScope ps("bn_fwd_apply", st, 0.0, tb * (r ? 3 : 2) + (ybits ? tb / 16 : 0.0));
 #define RAT3D_BN_FWD(RL, RS)                                                                 \
     bn_fwd_apply<T, VEC, RL, RS><<<grid, kBnThreads, 0, st>>>(x, r, g.N, g.C, g.V, cpp, fs, y, \
-                                                              ybits)
-    if (relu && r) RAT3D_BN_FWD(true, true);
-    else if (relu) RAT3D_BN_FWD(true, false);
-    else if (r) RAT3D_BN_FWD(false, true);
-    else RAT3D_BN_FWD(false, false);
+                                                              ybits, BnFwdStats{})
+    if (relu && r) RAT3D_BN_FWD(true, 1);
+    else if (relu) RAT3D_BN_FWD(true, 0);
+    else if (r) RAT3D_BN_FWD(false, 1);
+    else RAT3D_BN_FWD(false, 0);
 #undef RAT3D_BN_FWD
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
@@ -501,13 +511,52 @@ rat3d_status bn_fwd_apply_from(const BnGeom& g, float eps, float momentum, const
     }
     const BnFwdStats fs{part,     slices,      gamma,    beta,    eps,      momentum,
                         save_mean, save_invstd, run_mean, run_var, save_coef};
-    const int fu = fwd_apply_u<false>();
+    const int fu = fwd_apply_u<0>();
     const unsigned cpp = (unsigned)ceil_div(g.V / 8, kBnThreads * fu);
     const unsigned grid = cpp * (unsigned)(g.N * g.C);
     const double tb = (double)g.N * g.C * g.V * sizeof(bf16);
     ProfScope ps("bn_fwd_apply", st, 0.0, tb * 2);
-    bn_fwd_apply<bf16, 8, true, false><<<grid, kBnThreads, 0, st>>>(
-        (const bf16*)x, nullptr, g.N, g.C, g.V, cpp, fs, (bf16*)y, nullptr);
+    bn_fwd_apply<bf16, 8, true, 0><<<grid, kBnThreads, 0, st>>>(
+        (const bf16*)x, nullptr, g.N, g.C, g.V, cpp, fs, (bf16*)y, nullptr, BnFwdStats{});
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
+// y = relu(BN(x) + BN_r(r)): the residual passes through its own batch norm
+// (no ReLU) whose apply happens inside this one (bf16, V % 8 == 0); both
+// statistics passes first, each into its own workspace (bn_ws_bytes each).
+// The residual's BN stores its mean, invstd and running statistics as its own
+// forward would; its normalised values are never stored.
+rat3d_status bn_fwd_res_bn(const BnGeom& g, float eps, float momentum, const void* x,
+                           const float* gamma, const float* beta, void* y, float* save_mean,
+                           float* save_invstd, float* run_mean, float* run_var,
+                           uint8_t* ybits, void* ws, const void* r, const float* rgamma,
+                           const float* rbeta, float* rsave_mean, float* rsave_invstd,
+                           float* rrun_mean, float* rrun_var, void* rws, hipStream_t st) {
+    if (g.V % 8 != 0 || (ybits && !bn_bits_ok(g, RAT3D_BF16))) {
+        set_error("bn_fwd_res_bn: needs V %% 8 == 0");
+        return RAT3D_EUNSUPPORTED;
+    }
+    const BnSlices sl = bn_slices(g);
+    const double tb = (double)g.N * g.C * g.V * sizeof(bf16);
+    {
+        ProfScope ps("bn_fwd_stats", st, 0.0, tb * 2);
+        bn_fwd_stats<bf16, 8><<<dim3(g.C, sl.per_channel), kBnThreads, 0, st>>>(
+            (const bf16*)x, g.C, g.V, sl.per_plane, sl.len, (float*)ws);
+        RAT3D_LAUNCH_CHECK();
+        bn_fwd_stats<bf16, 8><<<dim3(g.C, sl.per_channel), kBnThreads, 0, st>>>(
+            (const bf16*)r, g.C, g.V, sl.per_plane, sl.len, (float*)rws);
+        RAT3D_LAUNCH_CHECK();
+    }
+    const BnFwdStats fs{(const float*)ws, sl.per_channel, gamma,    beta,    eps,    momentum,
+                        save_mean,        save_invstd,    run_mean, run_var, nullptr};
+    const BnFwdStats rs{(const float*)rws, sl.per_channel, rgamma,    rbeta,    eps,    momentum,
+                        rsave_mean,        rsave_invstd,   rrun_mean, rrun_var, nullptr};
+    const unsigned cpp = (unsigned)ceil_div(g.V / 8, kBnThreads * fwd_apply_u<2>());
+    const unsigned grid = cpp * (unsigned)(g.N * g.C);
+    ProfScope ps("bn_fwd_apply", st, 0.0, tb * 3 + (ybits ? tb / 16 : 0.0));
+    bn_fwd_apply<bf16, 8, true, 2><<<grid, kBnThreads, 0, st>>>(
+        (const bf16*)x, (const bf16*)r, g.N, g.C, g.V, cpp, fs, (bf16*)y, ybits, rs);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }

@@ -137,6 +137,14 @@ rat3d_status bn_bwd_stats_x(const BnGeom& g, const void* dy, const void* x, cons
                             const float* fwd_coef, float* dgamma, float* dbeta, int accumulate,
                             void* ws, hipStream_t st, BnBwdStats* bs);
 size_t bn_max_slices(const BnGeom& g);
+// relu(BN(x) + BN_r(r)) with the residual's BN applied inside (ws, rws: one
+// bn_ws_bytes workspace each)
+rat3d_status bn_fwd_res_bn(const BnGeom& g, float eps, float momentum, const void* x,
+                           const float* gamma, const float* beta, void* y, float* save_mean,
+                           float* save_invstd, float* run_mean, float* run_var,
+                           uint8_t* ybits, void* ws, const void* r, const float* rgamma,
+                           const float* rbeta, float* rsave_mean, float* rsave_invstd,
+                           float* rrun_mean, float* rrun_var, void* rws, hipStream_t st);
 rat3d_status bn_fwd_apply_from(const BnGeom& g, float eps, float momentum, const void* x,
                                const float* gamma, const float* beta, void* y,
                                float* save_mean, float* save_invstd, float* run_mean,

@@ -96,6 +96,7 @@ struct rat3d_net {
     std::vector<TensorRec> tensors;
     size_t param_count = 0, ws_bytes = 0;
     // layout
+    size_t bn_scr2_off = 0;
     size_t mirror_off = 0, conv_scr_off = 0, conv_scr_bytes = 0, bn_scr_off = 0,
            bn_scr_bytes = 0, head_scr_off = 0, run_mean_off = 0, run_var_off = 0,
            logits_off = 0, loss_off = 0;
@@ -294,6 +295,7 @@ struct Exec {
     float* grd(size_t off) const { return n->G + off; }
     void* conv_scr() const { return n->ws + n->conv_scr_off; }
     void* bn_scr() const { return n->ws + n->bn_scr_off; }
+    void* bn_scr2() const { return n->ws + n->bn_scr2_off; }
     float* mean(const BnL& b) const { return (float*)(n->ws + b.stat_off); }
     float* invstd(const BnL& b) const { return (float*)(n->ws + b.stat_off) + b.c; }
     float* fcoef(const BnL& b) const { return (float*)(n->ws + b.stat_off) + 2 * b.c; }
@@ -354,6 +356,16 @@ rat3d_status ru_fwd(const Exec& e, const RUPlan& r) {
     const void* skip = e.a(r.x);
     if (r.proj) {
         RAT3D_TRY(e.conv_f(r.cp, e.a(r.x), e.a(r.hp)));
+        const BnGeom g{r.h2.s.n, r.b2.c, r.h2.s.vox()};
+        if (e.n->dt == RAT3D_BF16 && g.V % 8 == 0) {
+            // the projection's BN is applied inside the output BN's apply
+            const rat3d_net* n = e.n;
+            return bn_fwd_res_bn(g, n->d.bn_eps, n->d.bn_momentum, e.a(r.h2), e.par(r.b2.g_off),
+                                 e.par(r.b2.b_off), e.a(r.y), e.mean(r.b2), e.invstd(r.b2),
+                                 e.rmean(r.b2), e.rvar(r.b2), e.bits(r.ybits), e.bn_scr(),
+                                 e.a(r.hp), e.par(r.bp.g_off), e.par(r.bp.b_off), e.mean(r.bp),
+                                 e.invstd(r.bp), e.rmean(r.bp), e.rvar(r.bp), e.bn_scr2(), e.st);
+        }
         RAT3D_TRY(e.bn_f(r.bp, r.hp, nullptr, 0, e.a(r.sp)));
         skip = e.a(r.sp);
     }
@@ -610,6 +622,7 @@ rat3d_status rat3d_net_create(const rat3d_net_desc* desc, rat3d_net** out) {
     if (n->dt == RAT3D_BF16) n->mirror_off = b.alloc(n->param_count * 2);
     n->conv_scr_off = b.alloc(n->conv_scr_bytes);
     n->bn_scr_off = b.alloc(n->bn_scr_bytes);
+    n->bn_scr2_off = b.alloc(n->bn_scr_bytes);  // a second BN's partials (projection skip)
     n->head_scr_off = b.alloc(head_ws_bytes(d.n, 256, 2));
     n->run_mean_off = b.alloc(n->run_count * sizeof(float));
     n->run_var_off = b.alloc(n->run_count * sizeof(float));
