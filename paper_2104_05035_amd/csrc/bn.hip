@@ -34,10 +34,11 @@ namespace rat3d {
 
 constexpr int kBnThreads = 256;
 constexpr int kStatsUnroll = 4;  // vectors per tensor in flight per thread in the statistics passes
-// vectors per thread in the apply passes (measured: only the two-stream
-// forward apply, which has the least work per wave to hide its coefficient
-// reduction behind, gains from more than one)
-template <int RES> constexpr int fwd_apply_u() { return RES ? 1 : 4; }
+// vectors per thread in the apply passes, measured per variant: the two-stream
+// forward apply (least work per wave to hide its coefficient reduction
+// behind) and the one that also reduces its residual's BN coefficients gain
+// from four; the plain residual apply runs best with one
+template <int RES> constexpr int fwd_apply_u() { return RES == 1 ? 1 : 4; }
 constexpr int kBwdApplyU = 1;
 
 struct BnSlices {
