@@ -55,26 +55,28 @@ def build_inputs(torch, R, synth, n, mb, vol, c):
     return net, P, G, ws, x, dy
 
 
-def cpu_baseline(budget_s=30.0):
+def cpu_baseline(volumes=2):
     """The oracle as it stands, on a bounded sample of the same workload: the
-    partition's forward and backward for ONE volume (same graph and shapes,
-    BN statistics over that volume), bf16 store points, float64 arithmetic."""
+    partition's forward and backward for `volumes` volumes (same graph and
+    shapes, BN statistics over those volumes), bf16 store points, float64
+    arithmetic; about 15 s on 16 host cores."""
     import numpy as np
     from oracle import net as onet, ops
     from paper_2104_05035_amd import synth
     rng_p, rng_x, rng_dy = synth.streams(4, 3)
     L = onet.param_layout("partition1", 1, 64)
     P = {k: v.astype(np.float32).astype(np.float64) for k, v in synth.init_params(rng_p, L).items()}
-    x = ops.round_bf16(synth.mri_volumes(rng_x, 1, (96, 112, 96)))
-    dy = ops.round_bf16(rng_dy.standard_normal((1, 64, 48, 56, 48), dtype=np.float32))
+    x = ops.round_bf16(synth.mri_volumes(rng_x, volumes, (96, 112, 96)))
+    dy = ops.round_bf16(rng_dy.standard_normal((volumes, 64, 48, 56, 48), dtype=np.float32))
     t0 = time.perf_counter()
     onet.partition1_fwd_bwd(P, x, dy, bf16=True)
     dt = time.perf_counter() - t0
-    flops = 8.522e12 / 16.0  # conv flops of one volume through the partition
+    flops = 8.522e12 / 16.0 * volumes  # conv flops of the volumes through the partition
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": ops.num_threads(),
-            "kind": "oracle", "volumes_per_s": round(1.0 / dt, 6), "seconds": round(dt, 2),
-            "sample": "oracle forward+backward of the partition for 1 volume 96x112x96 "
-                      "(0.533 TFLOP of conv work), float64 loops, bf16 store points"}
+            "kind": "oracle", "volumes_per_s": round(volumes / dt, 6), "seconds": round(dt, 2),
+            "sample": "oracle forward+backward of the partition for %d volumes 96x112x96 "
+                      "(%.3f TFLOP of conv work), float64 loops, bf16 store points"
+                      % (volumes, flops / 1e12)}
 
 
 def elementwise_hbm(tags):
