@@ -546,4 +546,24 @@ rat3d_status conv_bias_grad(const ConvGeom& g, rat3d_dtype dt, const void* dy, f
     return RAT3D_OK;
 }
 
+// One wave per channel: lane l adds partials l, l + 64, ... in turn, then an
+// xor butterfly (a fixed order for a given S).
+__global__ __launch_bounds__(64) void bias_sum_wave(const float* __restrict__ part, int S,
+                                                    float* __restrict__ db, int accumulate) {
+    const int c = blockIdx.x, lane = threadIdx.x;
+    const float* p = part + (int64_t)c * S;
+    float s = 0.f;
+    for (int i = lane; i < S; i += 64) s += p[i];
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
+    if (lane == 0) db[c] = accumulate ? db[c] + s : s;
+}
+
+rat3d_status bias_grad_from_partials(const float* part, int C, int S, float* db, int accumulate,
+                                     hipStream_t st) {
+    bias_sum_wave<<<(unsigned)C, 64, 0, st>>>(part, S, db, accumulate);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
 }  // namespace rat3d

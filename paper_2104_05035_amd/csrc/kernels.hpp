@@ -105,6 +105,10 @@ size_t pw_wgrad_ws(const ConvGeom& g);
 rat3d_status conv_wgrad_pw(const ConvGeom& g, const void* x, const void* dy, float* dw,
                            int accumulate, void* ws, hipStream_t st);
 
+// db (+)= the per-channel sums of `part` ([C][S] floats, summed in order)
+rat3d_status bias_grad_from_partials(const float* part, int C, int S, float* db, int accumulate,
+                                     hipStream_t st);
+
 // ---- batch norm (bn.hip) -----------------------------------------------
 struct BnGeom {
     int N, C;
@@ -164,10 +168,13 @@ rat3d_status up_bwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
 rat3d_status softmask_fwd(int64_t count, rat3d_dtype dt, const void* z, const void* t,
                           void* out, void* m, hipStream_t st);
 // m_is_z: `m` holds z (m was not stored) and m is recomputed and rounded as a
-// store of it would be.
+// store of it would be.  bias_part (bf16, count = N * C * V, V a multiple of
+// 2048): per-block sums of the stored dz, [C][N * V / 2048], for
+// bias_grad_from_partials.
 rat3d_status softmask_bwd(int64_t count, rat3d_dtype dt, const void* dout, const void* t,
                           const void* m, void* dt_out, int accumulate_dt, void* dz,
-                          hipStream_t st, int m_is_z = 0);
+                          hipStream_t st, int m_is_z = 0,
+                          float* bias_part = nullptr, int N = 0, int C = 0, int64_t V = 0);
 // relu(BN(up(xc))) with an exact x2 upsampling (bf16): the upsampling pass
 // also yields the BN statistics (h = up(xc) is written for the backward);
 // the backward forms h's gradient inside the upsampling transpose.

@@ -69,6 +69,7 @@ struct AMPlan {
     ConvL c1, c2;
     BnL bn;
     TRef x, p1, p2, u1, h1c, h1, a, z, out;
+    int64_t zsum = kNone;  // per-block sums of dz (the c2 bias gradient), or kNone
     int64_t am1 = 0, am2 = 0;  // argmax byte offsets
 };
 
@@ -266,6 +267,10 @@ struct Builder {
         a.a = act(pre + "a", x.s);
         a.z = act(pre + "z", x.s);
         a.out = act(pre + "out", x.s);
+        // the soft-mask backward also sums dz per channel when blocks of 2048
+        // elements tile the planes (bf16)
+        if (net->dt == RAT3D_BF16 && x.s.vox() % 2048 == 0)
+            a.zsum = (int64_t)alloc((size_t)c * x.s.n * (x.s.vox() / 2048) * sizeof(float));
         return a;
     }
 };
@@ -442,10 +447,19 @@ rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
     const Shape& s1 = m.p1.s;
     const Shape& s2 = m.p2.s;
     const rat3d_dtype dt = e.n->dt;
+    float* zsum = m.zsum >= 0 ? (float*)e.p(m.zsum) : nullptr;
     RAT3D_TRY(softmask_bwd(s.count(), dt, e.g(m.out), e.a(m.t2.y), e.a(m.z), e.g(m.t2.y), 0,
-                           e.g(m.z), e.st, 1));
+                           e.g(m.z), e.st, 1, zsum, s.n, s.c, s.vox()));
     RAT3D_TRY(e.conv_d(m.c2, e.g(m.z), e.g(m.a), 0));
-    RAT3D_TRY(e.conv_w(m.c2, e.a(m.a), e.g(m.z)));
+    if (zsum) {
+        // c2's bias gradient from the soft-mask backward's dz sums
+        RAT3D_TRY(conv_wgrad(m.c2.g, dt, e.a(m.a), e.g(m.z), e.grd(m.c2.w_off), nullptr, e.acc,
+                             e.conv_scr(), e.n->conv_scr_bytes, e.st));
+        RAT3D_TRY(bias_grad_from_partials(zsum, s.c, (int)(s.n * (s.vox() / 2048)),
+                                          e.grd(m.c2.b_off), e.acc, e.st));
+    } else {
+        RAT3D_TRY(e.conv_w(m.c2, e.a(m.a), e.g(m.z)));
+    }
     if (fuse_up_bn(m, dt)) {
         // the BN apply happens inside the upsampling transpose: h1's gradient
         // is never stored

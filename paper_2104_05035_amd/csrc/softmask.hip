@@ -206,12 +206,23 @@ __global__ __launch_bounds__(kEwThreads) void softmask_fwd_k(const T* __restrict
     if (m) vstore<T, VEC>(m + i, zv);
 }
 
+// Optional per-channel sums of the stored dz (the bias gradient of the conv
+// that produced z): one partial per block at part[c][n * chunks + chunk],
+// chunks = V / (block elements); needs V to be a multiple of a block's
+// elements.
+struct SmBias {
+    float* part;
+    int64_t V;
+    int C, N;
+};
+
+// One vector of the soft-mask backward; returns the sum of the stored dz.
 template <typename T, int VEC>
-__global__ __launch_bounds__(kEwThreads) void softmask_bwd_k(
-    const T* __restrict__ dout, const T* __restrict__ t, const T* __restrict__ m, int64_t count,
-    T* __restrict__ dt, int accumulate_dt, T* __restrict__ dz, int m_is_z) {
-    const int64_t i = ((int64_t)blockIdx.x * kEwThreads + threadIdx.x) * VEC;
-    if (i >= count) return;
+__device__ __forceinline__ float softmask_bwd_body(const T* __restrict__ dout,
+                                                   const T* __restrict__ t,
+                                                   const T* __restrict__ m, int64_t i,
+                                                   T* __restrict__ dt, int accumulate_dt,
+                                                   T* __restrict__ dz, int m_is_z) {
     float g[VEC], tv[VEC], mv[VEC], a[VEC], b[VEC];
     vload<T, VEC>(dout + i, g);
     vload<T, VEC>(t + i, tv);
@@ -231,6 +242,42 @@ __global__ __launch_bounds__(kEwThreads) void softmask_bwd_k(
     }
     vstore<T, VEC>(dt + i, a);
     vstore<T, VEC>(dz + i, b);
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) s += Elt<T>::round(b[j]);
+    return s;
+}
+
+template <typename T, int VEC>
+__global__ __launch_bounds__(kEwThreads) void softmask_bwd_k(
+    const T* __restrict__ dout, const T* __restrict__ t, const T* __restrict__ m, int64_t count,
+    T* __restrict__ dt, int accumulate_dt, T* __restrict__ dz, int m_is_z, SmBias sb) {
+    const int64_t i = ((int64_t)blockIdx.x * kEwThreads + threadIdx.x) * VEC;
+    if (sb.part) {
+        // the block's share of dz's per-channel sum (the bias gradient of the
+        // conv that produced z), over the stored values; V is a multiple of
+        // the block's elements, so a block lies in one (n, c) plane
+        float s = 0.f;
+        if (i < count) s = softmask_bwd_body<T, VEC>(dout, t, m, i, dt, accumulate_dt, dz, m_is_z);
+#pragma unroll
+        for (int w = 32; w >= 1; w >>= 1) s += __shfl_xor(s, w, 64);
+        __shared__ float red[kEwThreads / 64];
+        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            float a = 0.f;
+#pragma unroll
+            for (int w = 0; w < kEwThreads / 64; ++w) a += red[w];
+            const int64_t e0 = (int64_t)blockIdx.x * kEwThreads * VEC;
+            const int64_t plane = e0 / sb.V, chunk = (e0 - plane * sb.V) / (kEwThreads * VEC);
+            const int64_t chunks = sb.V / (kEwThreads * VEC);
+            const int64_t n = plane / sb.C, c = plane - n * sb.C;
+            sb.part[c * (sb.N * chunks) + n * chunks + chunk] = a;
+        }
+        return;
+    }
+    if (i >= count) return;
+    softmask_bwd_body<T, VEC>(dout, t, m, i, dt, accumulate_dt, dz, m_is_z);
 }
 
 template <typename T, int VEC>
@@ -1185,29 +1232,36 @@ rat3d_status softmask_fwd(int64_t count, rat3d_dtype dt, const void* z, const vo
 
 rat3d_status softmask_bwd(int64_t count, rat3d_dtype dt, const void* dout, const void* t,
                           const void* m, void* dt_out, int accumulate_dt, void* dz,
-                          hipStream_t st, int m_is_z) {
+                          hipStream_t st, int m_is_z, float* bias_part, int N, int C,
+                          int64_t V) {
+    if (bias_part && !(dt == RAT3D_BF16 && V > 0 && V % (kEwThreads * 8) == 0 &&
+                       count == (int64_t)N * C * V)) {
+        set_error("softmask_bwd: per-channel dz sums need bf16 planes of whole blocks");
+        return RAT3D_EUNSUPPORTED;
+    }
+    const SmBias sb{bias_part, V, C, N};
     ProfScope ps("softmask_bwd", st, 0.0,
                  (dt == RAT3D_BF16 ? 2.0 : 4.0) * count * (5 + accumulate_dt));
     if (dt == RAT3D_BF16) {
         if (count % 8 == 0)
             softmask_bwd_k<bf16, 8><<<(unsigned)ceil_div(count / 8, kEwThreads), kEwThreads, 0,
                                       st>>>((const bf16*)dout, (const bf16*)t, (const bf16*)m,
-                                            count, (bf16*)dt_out, accumulate_dt, (bf16*)dz, m_is_z);
+                                            count, (bf16*)dt_out, accumulate_dt, (bf16*)dz, m_is_z, sb);
         else
             softmask_bwd_k<bf16, 1><<<(unsigned)ceil_div(count, kEwThreads), kEwThreads, 0,
                                       st>>>((const bf16*)dout, (const bf16*)t, (const bf16*)m,
-                                            count, (bf16*)dt_out, accumulate_dt, (bf16*)dz, m_is_z);
+                                            count, (bf16*)dt_out, accumulate_dt, (bf16*)dz, m_is_z, SmBias{});
     } else {
         if (count % 4 == 0)
             softmask_bwd_k<float, 4><<<(unsigned)ceil_div(count / 4, kEwThreads), kEwThreads, 0,
                                        st>>>((const float*)dout, (const float*)t,
                                              (const float*)m, count, (float*)dt_out,
-                                             accumulate_dt, (float*)dz, m_is_z);
+                                             accumulate_dt, (float*)dz, m_is_z, SmBias{});
         else
             softmask_bwd_k<float, 1><<<(unsigned)ceil_div(count, kEwThreads), kEwThreads, 0,
                                        st>>>((const float*)dout, (const float*)t,
                                              (const float*)m, count, (float*)dt_out,
-                                             accumulate_dt, (float*)dz, m_is_z);
+                                             accumulate_dt, (float*)dz, m_is_z, SmBias{});
     }
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
