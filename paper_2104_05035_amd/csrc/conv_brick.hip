@@ -318,7 +318,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         constexpr int NG = KT * NR;
         const uint32_t wchunk =
             ((uint32_t)(c0 >> 5) * KT * (uint32_t)a.Ct + T.co0 + wc * CT * 16) * 64u;
-        constexpr int LB = ACC ? 1 : 2;  // weight taps loaded ahead of the current one
+        constexpr int LB = 2;  // weight taps loaded ahead of the current one
         F16B A[LA], B[LB + 1][CT];
         auto a_ptr = [&](int g) {
             const int tap = g / NR, r = g % NR;
