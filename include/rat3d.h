@@ -312,6 +312,34 @@ rat3d_status rat3d_block_fwd_bwd(rat3d_net* net, const void* x, const void* dy, 
 rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labels,
                               const void* dy_upstream, float* loss_dev, void* stream);
 
+/* PARTITION1, one micro-batch at a time (model-parallelisation section: a
+ * partition processes micro-batches one after another, computing its weight
+ * gradients from the gradient received at its output and accumulating them
+ * before the update).  x [n][1][d][h][w] is one micro-batch, dy_upstream
+ * [n][c][d/2][h/2][w/2] its output gradient.  Forward and backward of the
+ * micro-batch; the gradient arena is overwritten (accumulate == 0) or added
+ * to (accumulate != 0).  No update: rat3d_net_update applies it.  The saved
+ * activations and gradients in the workspace are those of this micro-batch.
+ * rat3d_train_step runs exactly these calls (accumulate = 0 for the first
+ * micro-batch, 1 after), then rat3d_net_update. */
+rat3d_status rat3d_partition_micro_batch(rat3d_net* net, const void* x, const void* dy_upstream,
+                                         int accumulate, void* stream);
+
+/* params -= lr * grads over the whole arena (the network's SGD step). */
+rat3d_status rat3d_net_update(rat3d_net* net, void* stream);
+
+/* Checkpointing of the BN running statistics, which live in the workspace
+ * (the parameter arena is the caller's and is saved by the caller).
+ * rat3d_net_running_count: number of BN channels in the network, R.
+ * rat3d_net_running_save copies [means R][variances R] (float32, device) to
+ * dst; it fails (RAT3D_EINVAL) if no step has run since rat3d_net_bind.
+ * rat3d_net_running_load copies them from src into the workspace and cancels
+ * the reset that rat3d_net_bind scheduled.  Both enqueue device-to-device
+ * copies on `stream`. */
+size_t rat3d_net_running_count(const rat3d_net* net);
+rat3d_status rat3d_net_running_save(const rat3d_net* net, float* dst, void* stream);
+rat3d_status rat3d_net_running_load(rat3d_net* net, const float* src, void* stream);
+
 /* ------------------------------------------------------------------------
  * Measurement (off by default).  While enabled, every launch of a hot kernel
  * is bracketed by two hipEvents recorded on the stream it is launched on, and

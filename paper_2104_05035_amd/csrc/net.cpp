@@ -534,6 +534,24 @@ rat3d_status prepare_call(rat3d_net* n, hipStream_t st) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// One micro-batch of the first-stage partition: forward from x, backward from
+// the gradient received at the partition's output; parameter gradients are
+// written (acc = 0) or added (acc = 1).  The weights must be prepared.
+rat3d_status partition_micro_batch(rat3d_net* net, const void* x, const void* dy, int acc,
+                                   hipStream_t st) {
+    const AMPlan& am = net->ams[0];
+    net->ext_x = x;
+    // the partition's output gradient arrives from the next partition
+    net->ext_dy = dy;
+    Exec e{net, st, acc};
+    RAT3D_TRY(stem_fwd(e, false));
+    RAT3D_TRY(ru_fwd(e, net->rus[0]));
+    RAT3D_TRY(am_fwd(e, am));
+    RAT3D_TRY(am_bwd(e, am));
+    RAT3D_TRY(ru_bwd(e, net->rus[0], false));
+    return stem_bwd(e, false);
+}
+
 }  // namespace
 
 extern "C" {
@@ -787,22 +805,81 @@ rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labe
             }
         }
     } else {
-        const AMPlan& am = net->ams[0];
-        const size_t dy_bytes = (size_t)am.out.s.count() * net->esz;
-        for (int mb = 0; mb < d.micro_batches; ++mb) {
-            net->ext_x = (const char*)x + mb * x_bytes;
-            // the partition's output gradient arrives from the next partition
-            net->ext_dy = (const char*)dy_upstream + mb * dy_bytes;
-            Exec e{net, st, mb > 0 ? 1 : 0};
-            RAT3D_TRY(stem_fwd(e, false));
-            RAT3D_TRY(ru_fwd(e, net->rus[0]));
-            RAT3D_TRY(am_fwd(e, am));
-            RAT3D_TRY(am_bwd(e, am));
-            RAT3D_TRY(ru_bwd(e, net->rus[0], false));
-            RAT3D_TRY(stem_bwd(e, false));
-        }
+        const size_t dy_bytes = (size_t)net->ams[0].out.s.count() * net->esz;
+        for (int mb = 0; mb < d.micro_batches; ++mb)
+            RAT3D_TRY(partition_micro_batch(net, (const char*)x + mb * x_bytes,
+                                            (const char*)dy_upstream + mb * dy_bytes,
+                                            mb > 0 ? 1 : 0, st));
     }
     return sgd_update((int64_t)net->param_count, d.lr, net->P, net->G, st);
+}
+
+rat3d_status rat3d_partition_micro_batch(rat3d_net* net, const void* x, const void* dy_upstream,
+                                         int accumulate, void* stream) {
+    if (!net || net->d.kind != RAT3D_NET_PARTITION1) {
+        set_error("rat3d_partition_micro_batch: needs a PARTITION1 network");
+        return RAT3D_EINVAL;
+    }
+    if (!x || !dy_upstream) {
+        set_error("rat3d_partition_micro_batch: NULL input");
+        return RAT3D_EINVAL;
+    }
+    if (!aligned16(x) || !aligned16(dy_upstream)) {
+        set_error("rat3d_partition_micro_batch: tensors must be 16-byte aligned");
+        return RAT3D_EALIGN;
+    }
+    hipStream_t st = (hipStream_t)stream;
+    RAT3D_TRY(prepare_call(net, st));
+    return partition_micro_batch(net, x, dy_upstream, accumulate ? 1 : 0, st);
+}
+
+rat3d_status rat3d_net_update(rat3d_net* net, void* stream) {
+    if (!net || !net->P || !net->G) {
+        set_error("rat3d_net_update: network missing or not bound");
+        return RAT3D_EINVAL;
+    }
+    return sgd_update((int64_t)net->param_count, net->d.lr, net->P, net->G, (hipStream_t)stream);
+}
+
+size_t rat3d_net_running_count(const rat3d_net* net) { return net ? net->run_count : 0; }
+
+rat3d_status rat3d_net_running_save(const rat3d_net* net, float* dst, void* stream) {
+    if (!net || !net->ws || !dst) {
+        set_error("rat3d_net_running_save: network not bound or NULL destination");
+        return RAT3D_EINVAL;
+    }
+    if (net->reset_running) {
+        set_error("rat3d_net_running_save: no step has run since the buffers were bound");
+        return RAT3D_EINVAL;
+    }
+    hipStream_t st = (hipStream_t)stream;
+    const size_t bytes = net->run_count * sizeof(float);
+    if (hipMemcpyAsync(dst, net->ws + net->run_mean_off, bytes, hipMemcpyDeviceToDevice, st) !=
+            hipSuccess ||
+        hipMemcpyAsync(dst + net->run_count, net->ws + net->run_var_off, bytes,
+                       hipMemcpyDeviceToDevice, st) != hipSuccess) {
+        set_error("rat3d_net_running_save: copy failed");
+        return RAT3D_EHIP;
+    }
+    return RAT3D_OK;
+}
+
+rat3d_status rat3d_net_running_load(rat3d_net* net, const float* src, void* stream) {
+    if (!net || !net->ws || !src) {
+        set_error("rat3d_net_running_load: network not bound or NULL source");
+        return RAT3D_EINVAL;
+    }
+    hipStream_t st = (hipStream_t)stream;
+    const size_t bytes = net->run_count * sizeof(float);
+    if (hipMemcpyAsync(net->ws + net->run_mean_off, src, bytes, hipMemcpyDeviceToDevice, st) !=
+            hipSuccess ||
+        hipMemcpyAsync(net->ws + net->run_var_off, src + net->run_count, bytes,
+                       hipMemcpyDeviceToDevice, st) != hipSuccess) {
+        set_error("rat3d_net_running_load: copy failed");
+        return RAT3D_EHIP;
+    }
+    net->reset_running = false;  // the loaded statistics replace the bind-time reset
+    return RAT3D_OK;
 }
 
 }  // extern "C"

@@ -96,6 +96,11 @@ _SIGS = {
     "rat3d_net_bind": (_I, [_VP, _VP, _VP, _VP, _SZ]),
     "rat3d_block_fwd_bwd": (_I, [_VP] * 6),
     "rat3d_train_step": (_I, [_VP] * 6),
+    "rat3d_partition_micro_batch": (_I, [_VP, _VP, _VP, _I, _VP]),
+    "rat3d_net_update": (_I, [_VP, _VP]),
+    "rat3d_net_running_count": (_SZ, [_VP]),
+    "rat3d_net_running_save": (_I, [_VP, _VP, _VP]),
+    "rat3d_net_running_load": (_I, [_VP, _VP, _VP]),
     "rat3d_profile_enable": (_I, [_I]),
     "rat3d_profile_filter": (_I, [ctypes.c_char_p]),
     "rat3d_profile_reset": (_I, []),
@@ -335,3 +340,20 @@ class Net:
     def rat3d_train_step(self, x, labels, dy_upstream, loss_dev, stream=None):
         _check(lib().rat3d_train_step(self.h, _p(x), _p(labels), _p(dy_upstream), _p(loss_dev),
                                       _stream(stream)))
+
+    def rat3d_partition_micro_batch(self, x, dy_upstream, accumulate, stream=None):
+        _check(lib().rat3d_partition_micro_batch(self.h, _p(x), _p(dy_upstream), int(accumulate),
+                                                 _stream(stream)))
+
+    def rat3d_net_update(self, stream=None):
+        _check(lib().rat3d_net_update(self.h, _stream(stream)))
+
+    @property
+    def running_count(self):
+        return lib().rat3d_net_running_count(self.h)
+
+    def rat3d_net_running_save(self, dst, stream=None):
+        _check(lib().rat3d_net_running_save(self.h, _p(dst), _stream(stream)))
+
+    def rat3d_net_running_load(self, src, stream=None):
+        _check(lib().rat3d_net_running_load(self.h, _p(src), _stream(stream)))

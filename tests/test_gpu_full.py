@@ -8,13 +8,20 @@ The whole step is too large for the float64 oracle, so each kernel family is
 checked on what the step left in the workspace (the last micro-batch's
 activations and gradients): the oracle applies the layer to the GPU's own
 stored inputs and is compared with the GPU's stored output -- convolutions at
-sampled output points (the oracle's point-evaluated loops), batch norm,
-pooling, upsampling (with the fused BN) and the soft-mask fuse over whole
-channels, the weight
-gradient of a 3^3 layer at sampled entries (the C ABI's wgrad on the step's
-tensors), and the SGD update over the whole arena.  Gates as everywhere:
-2e-2 norm-wise for bf16 outputs, 1e-4 for float32 statistics, bit-exact for
-pooling values and argmax."""
+sampled output points (random points plus the first and last depth, row and
+column of the 4x8x16-voxel tiles), batch norm, pooling, upsampling (with the
+fused BN) and the soft-mask fuse over every channel, the weight gradient of a
+3^3 layer at sampled entries (the C ABI's wgrad on the step's tensors), and
+the SGD update over the whole arena.  The gradients accumulated over the 4
+micro-batches are checked for a 3^3 conv, a BN, the stem and both 1^3 convs
+of the mask tail (c2's bias through the soft-mask backward's partial sums),
+summing the oracle's per-micro-batch gradients.  Gates as everywhere
+(tests/gpu_util.check): the stated tolerance norm-wise plus the element-wise
+bound; pooling values and argmax bit-exact.
+
+The step is also run again: bit-identical arenas and workspace
+(determinism), and two steps equal one step, a checkpoint (parameter arena
+and BN running statistics) restored into a new network, and one more step."""
 import numpy as np
 import pytest
 
@@ -29,7 +36,8 @@ pytestmark = pytest.mark.gpu
 N, MB, VOL, C = 16, 4, (96, 112, 96), 64
 EPS = 1e-5
 NPTS = 3000
-CHANNELS = (0, 37)  # channels compared whole
+TILE = (4, 8, 16)  # voxels of a conv output tile (depth, rows, columns)
+CHUNK = 8  # channels per host pass over a full-size tensor
 
 
 class Full:
@@ -59,6 +67,8 @@ class Full:
         U.sync()
         self.G = self.B.grads()
         self.new = self.B.new_params()
+        self.G_dev, self.P_dev = self.B.G.clone(), self.B.P.clone()
+        self.ws0 = self.B.ws.clone()
         # the forward used the bf16 working copy of the parameters before the update
         self.wb = {k: ops.round_bf16(v) for k, v in self.old.items()}
 
@@ -94,30 +104,46 @@ def full():
     return Full()
 
 
-def chk(got, ref, dt, what):
-    r = U.check(got, ref, dt, what)
-    print("   %-32s rel %.3e  (|ref| %.3e, %d values)" % (what, r, np.linalg.norm(ref), np.size(ref)))
+def chk(got, ref, dt, what, **kw):
+    r = U.check(got, ref, dt, what, **kw)
+    st = U.LAST
+    print("   %-34s rel %.3e  >1ulp %d of %d  (|ref| %.3e)" % (
+        what, r, st["above_1ulp"], st["size"], np.linalg.norm(ref)), flush=True)
     assert np.linalg.norm(ref) > 0.0, what + ": reference is all zero"
 
 
 def points(shape, count, seed):
+    """Random output points plus points on tile edges: the first or last
+    depth, row and column of the 4x8x16-voxel tiles (and the map's own last
+    ones, where a tile is ragged)."""
     rng = np.random.default_rng(seed)
-    return np.stack([rng.integers(0, s, count) for s in shape], axis=1).astype(np.int32)
+    rnd = np.stack([rng.integers(0, s, count) for s in shape], axis=1)
+    edge = [rng.integers(0, shape[0], count // 3), rng.integers(0, shape[1], count // 3)]
+    for ax, t in zip(range(2, 5), TILE):
+        L = shape[ax]
+        tiles = rng.integers(0, (L + t - 1) // t, count // 3)
+        last = np.minimum(tiles * t + t - 1, L - 1)
+        edge.append(np.where(rng.integers(0, 2, count // 3) == 1, last, tiles * t))
+    return np.concatenate([rnd, np.stack(edge, axis=1)]).astype(np.int32)
 
 
 def test_full_stem_conv(full):
     """7^3 stride-2 stem conv (stem kernel) at sampled outputs."""
     pts = points(full.B.tinfo["stem.h"][2], NPTS, 1)
     ref = ops.conv3d_fwd_points(full.x_last, full.wb["stem.w"], None, 2, 3, pts)
-    chk(full.at("stem.h", pts), ref, "bf16", "stem conv output")
+    terms = ops.conv3d_fwd_points(np.abs(full.x_last), np.abs(full.wb["stem.w"]), None, 2, 3,
+                                  pts)
+    chk(full.at("stem.h", pts), ops.round_bf16(ref), "bf16", "stem conv output", terms=terms)
 
 
 def test_full_brick_conv_fwd(full):
     """64 -> 64 3^3 conv at 48x56x48 (brick forward kernel, the dominant one)."""
     x = full.host("ru.y")
     pts = points(full.B.tinfo["am.t1.h1"][2], NPTS, 2)
-    ref = ops.conv3d_fwd_points(x, full.wb["am.t1.conv1.w"], None, 1, 1, pts)
-    chk(full.at("am.t1.h1", pts), ref, "bf16", "t1.conv1 output")
+    w = full.wb["am.t1.conv1.w"]
+    ref = ops.conv3d_fwd_points(x, w, None, 1, 1, pts)
+    terms = ops.conv3d_fwd_points(np.abs(x), np.abs(w), None, 1, 1, pts)
+    chk(full.at("am.t1.h1", pts), ops.round_bf16(ref), "bf16", "t1.conv1 output", terms=terms)
 
 
 def test_full_brick_dgrad(full):
@@ -125,8 +151,11 @@ def test_full_brick_dgrad(full):
     dy = full.host("d:am.t1.h2")
     shp = full.B.tinfo["d:am.t1.a1"][2]
     pts = points(shp, NPTS, 3)
-    ref = ops.conv3d_dgrad_points(dy, full.wb["am.t1.conv2.w"], shp, 1, 1, pts)
-    chk(full.at("d:am.t1.a1", pts), ref, "bf16", "t1.conv2 input gradient")
+    w = full.wb["am.t1.conv2.w"]
+    ref = ops.conv3d_dgrad_points(dy, w, shp, 1, 1, pts)
+    terms = ops.conv3d_dgrad_points(np.abs(dy), np.abs(w), shp, 1, 1, pts)
+    chk(full.at("d:am.t1.a1", pts), ops.round_bf16(ref), "bf16", "t1.conv2 input gradient",
+        terms=terms)
 
 
 def test_full_brick_dgrad_accumulating(full):
@@ -136,10 +165,13 @@ def test_full_brick_dgrad_accumulating(full):
     shp = full.B.tinfo["d:am.t1.y"][2]
     pts = points(shp, NPTS, 4)
     dh1 = full.host("d:am.t2.h1")
-    conv = ops.conv3d_dgrad_points(dh1, full.wb["am.t2.conv1.w"], shp, 1, 1, pts)
+    w = full.wb["am.t2.conv1.w"]
+    conv = ops.conv3d_dgrad_points(dh1, w, shp, 1, 1, pts)
+    terms = ops.conv3d_dgrad_points(np.abs(dh1), np.abs(w), shp, 1, 1, pts)
     del dh1
     skip = full.at("d:am.t2.y", pts) * (full.at("am.t2.y", pts) > 0.0)
-    chk(full.at("d:am.t1.y", pts), skip + conv, "bf16", "t2 input gradient")
+    chk(full.at("d:am.t1.y", pts), ops.round_bf16(skip + conv), "bf16", "t2 input gradient",
+        terms=terms + np.abs(skip))
 
 
 def test_full_band_wgrad(full):
@@ -152,103 +184,310 @@ def test_full_band_wgrad(full):
     R.rat3d_conv3d_wgrad(desc, full.dev("am.t1.a1"), full.dev("d:am.t1.h2"), dw, None, 0, ws,
                          ws.numel())
     U.sync()
-    pts = points((C, C, 3, 3, 3), 256, 5)
-    ref = ops.conv3d_wgrad_points(full.host("am.t1.a1"), full.host("d:am.t1.h2"), 3, 1, 1, pts)
+    pts = points((C, C, 3, 3, 3), 256, 5)[:256]
+    a1, dh2 = full.host("am.t1.a1"), full.host("d:am.t1.h2")
+    ref = ops.conv3d_wgrad_points(a1, dh2, 3, 1, 1, pts)
+    terms = ops.conv3d_wgrad_points(np.abs(a1), np.abs(dh2), 3, 1, 1, pts)
     got = U.f64(dw)[tuple(pts.T)]
-    # float32 sums of bf16 products over 2 M voxels: the bf16 gate
-    chk(got, ref, "bf16", "t1.conv2 weight gradient")
+    chk(got, ref, "bf16", "t1.conv2 weight gradient", kind="sum", terms=terms)
 
 
 def test_full_pointwise_convs(full):
     """1^3 convs: the mask tail's second conv (+bias) at 48x56x48 and its first
     conv on the coarse map (streaming pointwise kernel)."""
     pts = points(full.B.tinfo["am.z"][2], NPTS, 6)
-    ref = ops.conv3d_fwd_points(full.host("am.a"), full.wb["am.c2.w"], full.old["am.c2.bias"],
-                                1, 0, pts)
-    chk(full.at("am.z", pts), ref, "bf16", "c2 output")
+    a, w, b = full.host("am.a"), full.wb["am.c2.w"], full.old["am.c2.bias"]
+    ref = ops.conv3d_fwd_points(a, w, b, 1, 0, pts)
+    terms = ops.conv3d_fwd_points(np.abs(a), np.abs(w), np.abs(b), 1, 0, pts)
+    chk(full.at("am.z", pts), ops.round_bf16(ref), "bf16", "c2 output", terms=terms)
+    del a
     pts = points(full.B.tinfo["am.c1out.coarse"][2], NPTS, 7)
-    ref = ops.conv3d_fwd_points(full.host("am.m4.y"), full.wb["am.c1.w"], None, 1, 0, pts)
-    chk(full.at("am.c1out.coarse", pts), ref, "bf16", "c1 output (coarse)")
+    y, w = full.host("am.m4.y"), full.wb["am.c1.w"]
+    ref = ops.conv3d_fwd_points(y, w, None, 1, 0, pts)
+    terms = ops.conv3d_fwd_points(np.abs(y), np.abs(w), None, 1, 0, pts)
+    chk(full.at("am.c1out.coarse", pts), ops.round_bf16(ref), "bf16", "c1 output (coarse)",
+        terms=terms)
+
+
+def _chunks():
+    return [list(range(c, min(c + CHUNK, C))) for c in range(0, C, CHUNK)]
+
+
+def _bn_apply(x, mean, invstd, g, b):
+    """BN + ReLU of x with the given (the GPU's saved) statistics."""
+    bc = lambda v: v[None, :, None, None, None]
+    return np.maximum(bc(g * invstd) * (x - bc(mean)) + bc(b), 0.0)
+
+
+def _bn_terms(x, mean, invstd, g, b, res=None):
+    sc = g * invstd
+    t = np.abs(x) * np.abs(sc)[None, :, None, None, None] + \
+        (np.abs(b) + np.abs(mean * sc))[None, :, None, None, None]
+    return t if res is None else t + np.abs(res)
+
+
+def _bn_bwd_terms(gres, x, mean, invstd, g):
+    bc = lambda v: v[None, :, None, None, None]
+    M = x.shape[0] * x.shape[2] * x.shape[3] * x.shape[4]
+    xh = (x - bc(mean)) * bc(invstd)
+    ag = np.abs(gres)
+    Sg = ag.sum(axis=(0, 2, 3, 4))
+    Sgx = np.abs(gres * xh).sum(axis=(0, 2, 3, 4))
+    return bc(np.abs(g * invstd)) * (ag + bc(Sg / M) + (np.abs(x) + bc(np.abs(mean)))
+                                     * bc(invstd * Sgx / M)), Sg, Sgx
 
 
 def test_full_bn_fwd(full):
-    """BN + ReLU forward over whole channels of a 16 x 64 x 48x56x48 tensor, and
+    """BN + ReLU forward over every channel of a 16 x 64 x 48x56x48 tensor, and
     the saved batch statistics of every channel."""
-    x = full.host("am.t1.h1")
-    mean, var = ops.bn_stats(x)
-    chk(full.host("am.t1.bn1.mean").ravel(), mean, "f32", "bn1 mean")
-    chk(full.host("am.t1.bn1.invstd").ravel(), 1.0 / np.sqrt(var + EPS), "f32",
-            "bn1 invstd")
-    cs = list(CHANNELS)
-    y, _, _, _ = ops.bn_fwd(x[:, cs], full.old["am.t1.bn1.g"][cs], full.old["am.t1.bn1.b"][cs],
-                            EPS, True)
-    chk(full.host("am.t1.a1", cs), y, "bf16", "bn1 + relu output")
+    mean_g = full.host("am.t1.bn1.mean").ravel()
+    inv_g = full.host("am.t1.bn1.invstd").ravel()
+    for cs in _chunks():
+        x = full.host("am.t1.h1", cs)
+        mean, var = ops.bn_stats(x)
+        inv = 1.0 / np.sqrt(var + EPS)
+        chk(mean_g[cs], mean, "f32", "bn1 mean %d-%d" % (cs[0], cs[-1]), kind="sum", norm=False,
+            terms=np.abs(x).mean(axis=(0, 2, 3, 4)))
+        chk(inv_g[cs], inv, "f32", "bn1 invstd %d-%d" % (cs[0], cs[-1]),
+            terms=inv * (x * x).mean(axis=(0, 2, 3, 4)) / (var + EPS))
+        g, b = full.old["am.t1.bn1.g"][cs], full.old["am.t1.bn1.b"][cs]
+        y = _bn_apply(x, mean_g[cs], inv_g[cs], g, b)
+        chk(full.host("am.t1.a1", cs), ops.round_bf16(y), "bf16",
+            "bn1 + relu output %d-%d" % (cs[0], cs[-1]),
+            terms=_bn_terms(x, mean_g[cs], inv_g[cs], g, b))
 
 
 def test_full_bn_bwd_output_mask(full):
     """Backward of the residual unit's output BN (BN + residual + ReLU; the
-    kernels read the forward's y > 0 bits): input gradient and residual
-    gradient over whole channels."""
-    cs = list(CHANNELS)
-    x, y, dy = full.host("am.t2.h2", cs), full.host("am.t2.y", cs), full.host("d:am.t2.y", cs)
-    mean, var = ops.bn_stats(x)
-    dx, dres, _, _ = ops.bn_bwd(dy, x, y, full.old["am.t2.bn2.g"][cs], mean,
-                                1.0 / np.sqrt(var + EPS), True)
-    chk(full.host("d:am.t2.h2", cs), dx, "bf16", "bn2 input gradient")
-    # the residual gradient is the skip part of the unit's input gradient,
-    # checked with the accumulating dgrad; here its mask: zero where y == 0
-    assert np.all(dres[y <= 0.0] == 0.0)
+    kernels read the forward's y > 0 bits): input gradient over every channel,
+    and the residual gradient's mask."""
+    mean_g = full.host("am.t2.bn2.mean").ravel()
+    inv_g = full.host("am.t2.bn2.invstd").ravel()
+    for cs in _chunks():
+        x, y, dy = full.host("am.t2.h2", cs), full.host("am.t2.y", cs), full.host("d:am.t2.y", cs)
+        mean, inv = mean_g[cs], inv_g[cs]
+        g = full.old["am.t2.bn2.g"][cs]
+        dx, dres, _, _ = ops.bn_bwd(dy, x, y, g, mean, inv, True)
+        terms, _, _ = _bn_bwd_terms(dres, x, mean, inv, g)
+        chk(full.host("d:am.t2.h2", cs), ops.round_bf16(dx), "bf16",
+            "bn2 input gradient %d-%d" % (cs[0], cs[-1]), terms=terms)
+        # the residual gradient is the skip part of the unit's input gradient,
+        # checked with the accumulating dgrad; here its mask: zero where y == 0
+        assert np.all(dres[y <= 0.0] == 0.0)
 
 
 def test_full_maxpool(full):
     """3^3 s2 p1 max pooling of 48x56x48 maps: values and first-maximum argmax
-    bit-exact over whole channels; its gradient at the next level likewise
-    within the bf16 gate."""
-    cs = list(CHANNELS)
-    yref, amref = ops.maxpool3d_fwd(full.host("ru.y", cs))
-    assert np.array_equal(full.host("am.p1", cs), yref)
-    assert np.array_equal(full.host("am.p1.argmax", cs), amref)
+    bit-exact over every channel; its gradient at the next level within the
+    bf16 gate."""
     shp = full.B.tinfo["am.m1.y"][2]
-    dref = ops.maxpool3d_bwd(full.host("d:am.p2", cs), full.host("am.p2.argmax", cs),
-                             (shp[0], len(cs)) + tuple(shp[2:]))
-    chk(full.host("d:am.m1.y", cs), dref, "bf16", "pool gradient")
+    for cs in _chunks():
+        yref, amref = ops.maxpool3d_fwd(full.host("ru.y", cs))
+        assert np.array_equal(full.host("am.p1", cs), yref)
+        assert np.array_equal(full.host("am.p1.argmax", cs), amref)
+        dp2, am2 = full.host("d:am.p2", cs), full.host("am.p2.argmax", cs)
+        ins = (shp[0], len(cs)) + tuple(shp[2:])
+        dref = ops.maxpool3d_bwd(dp2, am2, ins)
+        chk(full.host("d:am.m1.y", cs), ops.round_bf16(dref), "bf16",
+            "pool gradient %d-%d" % (cs[0], cs[-1]), terms=ops.maxpool3d_bwd(np.abs(dp2), am2, ins))
 
 
 def test_full_upsample_bn(full):
     """Mask tail: x2 trilinear 24x28x24 -> 48x56x48 of the first 1^3 conv's
     output, whose pass also yields the following BN's statistics, then BN +
     ReLU; backward: the BN's input gradient formed inside the upsampling
-    transpose.  Whole channels, plus every channel's saved statistics."""
-    cs = list(CHANNELS)
-    h = full.host("am.c1out")
-    chk(full.host("am.c1out", cs), ops.trilinear_fwd(full.host("am.c1out.coarse", cs),
-                                                      (48, 56, 48)), "bf16", "upsampled c1 output")
-    mean, var = ops.bn_stats(h)
-    chk(full.host("am.bn.mean").ravel(), mean, "f32", "mask bn mean")
-    chk(full.host("am.bn.invstd").ravel(), 1.0 / np.sqrt(var + EPS), "f32", "mask bn invstd")
-    del h
-    hc = full.host("am.c1out", cs)
-    y, mc, _, ic = ops.bn_fwd(hc, full.old["am.bn.g"][cs], full.old["am.bn.b"][cs], EPS, True)
-    a = full.host("am.a", cs)
-    chk(a, y, "bf16", "mask bn + relu output")
-    dh, _, _, _ = ops.bn_bwd(full.host("d:am.a", cs), hc, a, full.old["am.bn.g"][cs], mc, ic, True)
-    chk(full.host("d:am.c1out.coarse", cs), ops.trilinear_bwd(dh, (24, 28, 24)), "bf16",
-        "mask bn + upsampling gradient")
+    transpose.  Every channel, and every channel's saved statistics."""
+    mean_g = full.host("am.bn.mean").ravel()
+    inv_g = full.host("am.bn.invstd").ravel()
+    for cs in _chunks():
+        tag = " %d-%d" % (cs[0], cs[-1])
+        hc_coarse = full.host("am.c1out.coarse", cs)
+        hc = full.host("am.c1out", cs)
+        chk(hc, ops.round_bf16(ops.trilinear_fwd(hc_coarse, (48, 56, 48))), "bf16",
+            "upsampled c1 output" + tag, terms=ops.trilinear_fwd(np.abs(hc_coarse), (48, 56, 48)))
+        mean, var = ops.bn_stats(hc)
+        inv = 1.0 / np.sqrt(var + EPS)
+        chk(mean_g[cs], mean, "f32", "mask bn mean" + tag, kind="sum", norm=False,
+            terms=np.abs(hc).mean(axis=(0, 2, 3, 4)))
+        chk(inv_g[cs], inv, "f32", "mask bn invstd" + tag,
+            terms=inv * (hc * hc).mean(axis=(0, 2, 3, 4)) / (var + EPS))
+        g, b = full.old["am.bn.g"][cs], full.old["am.bn.b"][cs]
+        mean, inv = mean_g[cs], inv_g[cs]
+        y = _bn_apply(hc, mean, inv, g, b)
+        a = full.host("am.a", cs)
+        chk(a, ops.round_bf16(y), "bf16", "mask bn + relu output" + tag,
+            terms=_bn_terms(hc, mean, inv, g, b))
+        dh, gres, _, _ = ops.bn_bwd(full.host("d:am.a", cs), hc, a, g, mean, inv, True)
+        tdh, _, _ = _bn_bwd_terms(gres, hc, mean, inv, g)
+        dhr = ops.round_bf16(dh)
+        # the BN input gradient is rounded inside the transpose, as its store
+        # would be: one rounding of it is carried as `extra`
+        chk(full.host("d:am.c1out.coarse", cs), ops.round_bf16(ops.trilinear_bwd(dhr, (24, 28, 24))),
+            "bf16", "mask bn + upsampling gradient" + tag,
+            terms=ops.trilinear_bwd(np.abs(dhr), (24, 28, 24)),
+            extra=ops.trilinear_bwd(2.0 * U.ulp(dhr, "bf16") + U.C_OUT * tdh, (24, 28, 24)))
 
 
 def test_full_softmask(full):
-    """(1 + sigmoid(z)) T and its gradients over whole channels; the incoming
+    """(1 + sigmoid(z)) T and its gradients over every channel; the incoming
     gradient is the last micro-batch's upstream tensor."""
-    cs = list(CHANNELS)
-    z, t = full.host("am.z", cs), full.host("am.t2.y", cs)
-    out, m = ops.softmask_fwd(z, t, ops.round_bf16)
-    chk(full.host("am.out", cs), out, "bf16", "attention output")
-    dT, dz = ops.softmask_bwd(full.dy_last[:, cs], t, m)
-    chk(full.host("d:am.z", cs), dz, "bf16", "mask logit gradient")
-    chk(full.host("d:am.t2.y", cs), dT, "bf16", "trunk output gradient")
+    for cs in _chunks():
+        tag = " %d-%d" % (cs[0], cs[-1])
+        z, t = full.host("am.z", cs), full.host("am.t2.y", cs)
+        m = ops.sigmoid(z)
+        out = (1.0 + m) * t
+        chk(full.host("am.out", cs), ops.round_bf16(out), "bf16", "attention output" + tag,
+            terms=np.abs(out))
+        mr = ops.round_bf16(m)
+        um = U.ulp(mr, "bf16")
+        dout = full.dy_last[:, cs]
+        dT, dz = (1.0 + mr) * dout, dout * t * mr * (1.0 - mr)
+        chk(full.host("d:am.z", cs), ops.round_bf16(dz), "bf16", "mask logit gradient" + tag,
+            terms=np.abs(dz), extra=um * (np.abs(1.0 - 2.0 * mr) + um) * np.abs(dout * t))
+        chk(full.host("d:am.t2.y", cs), ops.round_bf16(dT), "bf16", "trunk output gradient" + tag,
+            terms=np.abs(dT), extra=um * np.abs(dout))
 
 
 def test_full_sgd_update(full):
     """Every parameter moved by exactly one float32 rounding of w - lr g."""
     check_sgd(full.old, full.new, full.G, 1e-4)
     assert all(np.all(np.isfinite(g)) for g in full.G.values())
+
+
+def test_full_accumulated_gradients(full):
+    """The gradient arena after 4 micro-batches (float32 sums) against the
+    oracle's per-micro-batch gradients, summed: the 3^3 conv am.t1.conv2
+    (band weight gradient, sampled entries), the BN am.t1.bn1 (every channel),
+    the stem (sampled entries) and the mask tail's 1^3 convs am.c1 / am.c2 with
+    c2's bias (summed by the soft-mask backward in per-block partials), all
+    entries.  The step is rerun micro-batch by micro-batch
+    (rat3d_partition_micro_batch, then rat3d_net_update) and must also give
+    bit-identical arenas to the rat3d_train_step run."""
+    torch = U.torch_mod()
+    B = full.B
+    B.reset_params()
+    wpts = points((C, C, 3, 3, 3), 192, 11)[:192]
+    spts = points((32, 1, 7, 7, 7), 128, 12)[:128]
+    acc = {}
+
+    def add(k, v, t):
+        if k in acc:
+            acc[k] = (acc[k][0] + v, acc[k][1] + t)
+        else:
+            acc[k] = (v, t)
+
+    for m in range(MB):
+        print("micro-batch %d of %d: step and oracle sums" % (m + 1, MB), flush=True)
+        sl = slice(m * N, (m + 1) * N)
+        B.net.rat3d_partition_micro_batch(full.x[sl], full.dy[sl], m > 0)
+        U.sync()
+        a1, dh2 = full.host("am.t1.a1"), full.host("d:am.t1.h2")
+        add("am.t1.conv2.w", ops.conv3d_wgrad_points(a1, dh2, 3, 1, 1, wpts),
+            ops.conv3d_wgrad_points(np.abs(a1), np.abs(dh2), 3, 1, 1, wpts))
+        del a1, dh2
+        dgam, dbet = np.zeros(C), np.zeros(C)
+        tgam, tbet = np.zeros(C), np.zeros(C)
+        mean_g = full.host("am.t1.bn1.mean").ravel()
+        inv_g = full.host("am.t1.bn1.invstd").ravel()
+        for cs in _chunks():
+            h, a, da = full.host("am.t1.h1", cs), full.host("am.t1.a1", cs), \
+                full.host("d:am.t1.a1", cs)
+            mean, inv = mean_g[cs], inv_g[cs]
+            _, gres, dg, db = ops.bn_bwd(da, h, a, full.old["am.t1.bn1.g"][cs], mean, inv, True)
+            _, sg, sgx = _bn_bwd_terms(gres, h, mean, inv, full.old["am.t1.bn1.g"][cs])
+            dgam[cs], dbet[cs], tgam[cs], tbet[cs] = dg, db, sgx, sg
+        add("am.t1.bn1.g", dgam, tgam)
+        add("am.t1.bn1.b", dbet, tbet)
+        # 1^3 convs: a (C, voxels) x (C, voxels)^T product per micro-batch
+        for wname, xname, dname, bname in (("am.c2.w", "am.a", "d:am.z", "am.c2.bias"),
+                                           ("am.c1.w", "am.m4.y", "d:am.c1out.coarse", None)):
+            xv = full.host(xname).transpose(1, 0, 2, 3, 4).reshape(C, -1)
+            dv = full.host(dname).transpose(1, 0, 2, 3, 4).reshape(C, -1)
+            add(wname, (dv @ xv.T).reshape(C, C, 1, 1, 1),
+                (np.abs(dv) @ np.abs(xv).T).reshape(C, C, 1, 1, 1))
+            if bname:
+                add(bname, dv.sum(axis=1), np.abs(dv).sum(axis=1))
+            del xv, dv
+        xs = full.x[sl].to(torch.float64).cpu().numpy()
+        dh0 = full.host("d:stem.h")
+        add("stem.w", ops.conv3d_wgrad_points(xs, dh0, 7, 2, 3, spts),
+            ops.conv3d_wgrad_points(np.abs(xs), np.abs(dh0), 7, 2, 3, spts))
+        del xs, dh0
+    G = B.grads()
+    for k, (ref, terms) in sorted(acc.items()):
+        if k == "am.t1.conv2.w":
+            got = G[k][tuple(wpts.T)]
+        elif k == "stem.w":
+            got = G[k][tuple(spts.T)]
+        else:
+            got = G[k]
+        cancel = k.endswith(".g") or k.endswith(".b") or k.endswith(".bias")
+        chk(got, ref, "bf16", "accumulated grad " + k, kind="sum", norm=not cancel, terms=terms)
+    B.net.rat3d_net_update()
+    U.sync()
+    assert torch.equal(B.G, full.G_dev), "micro-batch calls: gradient arena differs"
+    assert torch.equal(B.P, full.P_dev), "micro-batch calls: parameter arena differs"
+
+
+def test_full_determinism(full):
+    """The same step again from the same parameters (running statistics reset
+    by a new bind): gradient arena, parameter arena and the whole workspace
+    (every saved activation, gradient, mask, argmax map, statistic and scratch
+    region) bit-identical."""
+    torch = U.torch_mod()
+    B = full.B
+    B.reset_params()
+    B.net.rat3d_net_bind(B.P, B.G, B.ws, B.ws.numel())
+    B.net.rat3d_train_step(full.x, None, full.dy, None)
+    U.sync()
+    assert torch.equal(B.G, full.G_dev), "gradient arena differs between two runs"
+    assert torch.equal(B.P, full.P_dev), "parameter arena differs between two runs"
+    if not torch.equal(B.ws, full.ws0):
+        step = 1 << 28
+        for a in range(0, B.ws.numel(), step):
+            if not torch.equal(B.ws[a:a + step], full.ws0[a:a + step]):
+                off = a + int((B.ws[a:a + step] != full.ws0[a:a + step]).nonzero()[0])
+                break
+        names = [k for k, (o, dt, shp) in B.tinfo.items()
+                 if o <= off < o + int(np.prod(shp)) * {R.BF16: 2, R.F32: 4, R.U8: 1}[dt]]
+        raise AssertionError("workspace differs between two runs, first at byte %d (%s)" % (
+            off, names))
+
+
+def test_full_resume(full):
+    """Two steps in a row equal one step, a checkpoint (the parameter arena and
+    the BN running statistics via rat3d_net_running_save), a new network bound
+    to fresh buffers restored from it (rat3d_net_running_load), and one more
+    step: parameters and running statistics bit-identical."""
+    torch = U.torch_mod()
+    B = full.B
+    B.reset_params()
+    B.net.rat3d_net_bind(B.P, B.G, B.ws, B.ws.numel())
+    for _ in range(2):
+        B.net.rat3d_train_step(full.x, None, full.dy, None)
+    run2 = torch.empty(2 * B.net.running_count, dtype=torch.float32, device="cuda:0")
+    B.net.rat3d_net_running_save(run2)
+    U.sync()
+    P2 = B.P.clone()
+    # one step, checkpoint
+    B.reset_params()
+    B.net.rat3d_net_bind(B.P, B.G, B.ws, B.ws.numel())
+    B.net.rat3d_train_step(full.x, None, full.dy, None)
+    run1 = torch.empty_like(run2)
+    B.net.rat3d_net_running_save(run1)
+    P1 = B.P.clone()
+    U.sync()
+    # restore into a new network with its own buffers, one more step
+    net2 = R.Net(R.NET_PARTITION1, N, 1, C, *VOL, R.BF16, micro_batches=MB, lr=1e-4)
+    P = P1.clone()
+    G = torch.zeros_like(P)
+    ws = U.workspace(net2.workspace_size)
+    net2.rat3d_net_bind(P, G, ws, ws.numel())
+    net2.rat3d_net_running_load(run1)
+    net2.rat3d_train_step(full.x, None, full.dy, None)
+    run3 = torch.empty_like(run2)
+    net2.rat3d_net_running_save(run3)
+    U.sync()
+    assert torch.equal(P, P2), "resumed parameters differ"
+    assert torch.equal(run3, run2), "resumed running statistics differ"
+    del ws

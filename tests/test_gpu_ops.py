@@ -80,6 +80,9 @@ def _id(c):
 
 @pytest.mark.parametrize("case", CONV_CASES, ids=_id)
 def test_conv3d(case):
+    """Forward, input gradient (plain and accumulating) and weight gradient
+    (plain and accumulating, with the bias gradient) against the oracle; every
+    output lies between two 4 KiB sentinel bands that must stay untouched."""
     from paper_2104_05035_amd import rat3d as R
     N, Ci, Co, D, H, W, k, s, p, has_bias, dt = case
     rng = np.random.default_rng(zlib.crc32(repr(case).encode()))
@@ -94,31 +97,44 @@ def test_conv3d(case):
     ws = U.workspace(max(R.rat3d_conv3d_workspace_size(desc, i) for i in range(3)))
     nbytes = ws.numel()
     # forward
-    y = U.empty((N, Co, Do, Ho, Wo), dt)
+    y, yb = U.guarded((N, Co, Do, Ho, Wo), dt)
     R.rat3d_conv3d_fwd(desc, x, w, bias, y, ws, nbytes)
     yref = rnd(ops.conv3d_fwd(xr, wr, br, s, p))
     # input gradient, plain and accumulated
     dy, dyr = U.dev_input(rng.standard_normal((N, Co, Do, Ho, Wo)), dt)
-    dx = U.empty((N, Ci, D, H, W), dt)
+    dx, dxb = U.guarded((N, Ci, D, H, W), dt)
     R.rat3d_conv3d_dgrad(desc, dy, w, dx, 0, ws, nbytes)
     dxref = ops.conv3d_dgrad(dyr, wr, xr.shape, s, p)
-    base, baser = U.dev_input(rng.standard_normal((N, Ci, D, H, W)), dt)
+    base0, baser = U.dev_input(rng.standard_normal((N, Ci, D, H, W)), dt)
+    base, baseb = U.guarded((N, Ci, D, H, W), dt)
+    base.copy_(base0)
     R.rat3d_conv3d_dgrad(desc, dy, w, base, 1, ws, nbytes)
     # weight gradient, plain and accumulated
-    dw = U.zeros_f32((Co, Ci, k, k, k))
-    db = U.zeros_f32((Co,)) if has_bias else None
+    torch = U.torch_mod()
+    dw, dwb = U.guarded((Co, Ci, k, k, k), torch.float32)
+    dw.zero_()
+    db, dbb = U.guarded((Co,), torch.float32) if has_bias else (None, None)
     R.rat3d_conv3d_wgrad(desc, x, dy, dw, db, 0, ws, nbytes)
-    dw2 = U.to_dev(U.torch_mod().ones((Co, Ci, k, k, k)))
+    dw2, dw2b = U.guarded((Co, Ci, k, k, k), torch.float32)
+    dw2.fill_(1.0)
     R.rat3d_conv3d_wgrad(desc, x, dy, dw2, None, 1, ws, nbytes)
     U.sync()
+    for buf, nm in ((yb, "y"), (dxb, "dx"), (baseb, "dx accumulate"), (dwb, "dw"),
+                    (dw2b, "dw accumulate"), (dbb, "db")):
+        if buf is not None:
+            U.guard_intact(buf, nm)
     dwref, dbref = ops.conv3d_wgrad(xr, dyr, k, s, p, has_bias)
-    U.check(U.f64(y), yref, dt, "y")
-    U.check(U.f64(dx), rnd(dxref), dt, "dx")
-    U.check(U.f64(base), rnd(baser + dxref), dt, "dx accumulate")
-    U.check(U.f64(dw), dwref, dt, "dw")
-    U.check(U.f64(dw2), dwref + 1.0, dt, "dw accumulate")
+    ax, aw, ady = np.abs(xr), np.abs(wr), np.abs(dyr)
+    ty = ops.conv3d_fwd(ax, aw, None if br is None else np.abs(br), s, p)
+    tdx = ops.conv3d_dgrad(ady, aw, xr.shape, s, p)
+    tdw, tdb = ops.conv3d_wgrad(ax, ady, k, s, p, has_bias)
+    U.check(U.f64(y), yref, dt, "y", terms=ty)
+    U.check(U.f64(dx), rnd(dxref), dt, "dx", terms=tdx)
+    U.check(U.f64(base), rnd(baser + dxref), dt, "dx accumulate", terms=tdx + np.abs(baser))
+    U.check(U.f64(dw), dwref, dt, "dw", kind="sum", terms=tdw)
+    U.check(U.f64(dw2), dwref + 1.0, dt, "dw accumulate", kind="sum", terms=tdw + 1.0)
     if has_bias:
-        U.check(U.f64(db), dbref, dt, "db")
+        U.check(U.f64(db), dbref, dt, "db", kind="sum", norm=False, terms=tdb)
 
 
 BN_CASES = [
@@ -154,22 +170,39 @@ def test_bn(case, relu, resid):
     R.rat3d_bn_relu_bwd(desc, dy, x, y, gamma, mean, invstd, dx, dres, dg, dbt, 0, ws,
                         ws.numel())
     U.sync()
-    yref, mref, vref, isref = ops.bn_fwd(xr, g32.astype(np.float64), b32.astype(np.float64),
-                                         1e-5, relu, rr)
-    yref = rnd(yref)
-    U.check(U.f64(y), yref, dt, "y")
-    U.check(U.f64(mean), mref, "f32", "mean")
-    U.check(U.f64(invstd), isref, "f32", "invstd")
+    g64, b64 = g32.astype(np.float64), b32.astype(np.float64)
+    _, mref, vref, isref = ops.bn_fwd(xr, g64, b64, 1e-5, relu, rr)
+    # the output with the statistics the GPU saved (checked just below)
+    bc = lambda v: v[None, :, None, None, None]
+    mg, ig = U.f64(mean), U.f64(invstd)
+    yref = bc(g64 * ig) * (xr - bc(mg)) + bc(b64) + (0.0 if rr is None else rr)
+    yref = rnd(np.maximum(yref, 0.0) if relu else yref)
+    sc = g64 * ig
+    ty = np.abs(xr) * bc(np.abs(sc)) + bc(np.abs(b64) + np.abs(mg * sc))
+    if resid:
+        ty = ty + np.abs(rr)
+    U.check(U.f64(y), yref, dt, "y", terms=ty)
+    U.check(U.f64(mean), mref, "f32", "mean", kind="sum", norm=False,
+            terms=np.abs(xr).mean(axis=(0, 2, 3, 4)))
+    U.check(U.f64(invstd), isref, "f32", "invstd",
+            terms=isref * (xr * xr).mean(axis=(0, 2, 3, 4)) / (vref + 1e-5))
     cnt = N * D * H * W
     rmr, rvr = ops.bn_running_update(np.zeros(C), np.ones(C), mref, vref, cnt, 0.1)
     U.check(U.f64(rm), rmr, "f32", "running mean")
     U.check(U.f64(rv), rvr, "f32", "running var")
-    dxr, gr, dgr, dbr = ops.bn_bwd(dyr, xr, yref, g32.astype(np.float64), mref, isref, relu)
-    U.check(U.f64(dx), rnd(dxr), dt, "dx")
-    U.check(U.f64(dg), dgr, dt, "dgamma")
-    U.check(U.f64(dbt), dbr, dt, "dbeta")
+    # the ReLU mask is the GPU's stored y > 0 (decision-matched)
+    dxr, gr, dgr, dbr = ops.bn_bwd(dyr, xr, U.f64(y), g64, mg, ig, relu)
+    M = N * D * H * W
+    xh = (xr - bc(mg)) * bc(ig)
+    Sg = np.abs(gr).sum(axis=(0, 2, 3, 4))
+    Sgx = np.abs(gr * xh).sum(axis=(0, 2, 3, 4))
+    tdx = bc(np.abs(sc)) * (np.abs(gr) + bc(Sg / M) + (np.abs(xr) + bc(np.abs(mg)))
+                            * bc(ig * Sgx / M))
+    U.check(U.f64(dx), rnd(dxr), dt, "dx", terms=tdx)
+    U.check(U.f64(dg), dgr, dt, "dgamma", kind="sum", norm=False, terms=Sgx)
+    U.check(U.f64(dbt), dbr, dt, "dbeta", kind="sum", norm=False, terms=Sg)
     if resid:
-        U.check(U.f64(dres), gr, dt, "dresidual")
+        U.check(U.f64(dres), rnd(gr), dt, "dresidual", terms=np.abs(gr))
 
 
 POOL_CASES = [(2, 3, 9, 8, 7, "bf16"), (2, 16, 24, 28, 24, "bf16"), (1, 2, 3, 4, 3, "f32"),
@@ -201,8 +234,9 @@ def test_maxpool(case):
     np.testing.assert_array_equal(U.f64(y), yref)                      # bit-exact
     np.testing.assert_array_equal(am.cpu().numpy().astype(np.int32), amref)
     dxr = ops.maxpool3d_bwd(dyr, amref, xr.shape)
-    U.check(U.f64(dx), rnd(dxr), dt, "dx")
-    U.check(U.f64(base), rnd(baser + dxr), dt, "dx accumulate")
+    tdx = ops.maxpool3d_bwd(np.abs(dyr), amref, xr.shape)
+    U.check(U.f64(dx), rnd(dxr), dt, "dx", terms=tdx)
+    U.check(U.f64(base), rnd(baser + dxr), dt, "dx accumulate", terms=tdx + np.abs(baser))
 
 
 UP_CASES = [((6, 7, 6), (12, 14, 12)), ((3, 4, 3), (6, 7, 6)), ((2, 2, 2), (3, 4, 3)),
@@ -228,8 +262,10 @@ def test_trilinear(sizes, dt):
     dx = U.empty((N, C, Di, Hi, Wi), dt)
     R.rat3d_softmask_up_bwd(desc, dy, dx, 0)
     U.sync()
-    U.check(U.f64(y), rnd(ops.trilinear_fwd(xr, (Do, Ho, Wo))), dt, "y")
-    U.check(U.f64(dx), rnd(ops.trilinear_bwd(dyr, (Di, Hi, Wi))), dt, "dx")
+    U.check(U.f64(y), rnd(ops.trilinear_fwd(xr, (Do, Ho, Wo))), dt, "y",
+            terms=ops.trilinear_fwd(np.abs(xr), (Do, Ho, Wo)))
+    U.check(U.f64(dx), rnd(ops.trilinear_bwd(dyr, (Di, Hi, Wi))), dt, "dx",
+            terms=ops.trilinear_bwd(np.abs(dyr), (Di, Hi, Wi)))
 
 
 @pytest.mark.parametrize("count", [1, 1001, 4096, 131072 + 5])
@@ -250,12 +286,16 @@ def test_softmask_fuse(count, dt):
     R.rat3d_softmask_bwd(count, U.code(dt), dout, t, m, acc, 1, dz2)
     U.sync()
     outr, mr = ops.softmask_fwd(zr, tr, rnd)
-    U.check(U.f64(out), outr, dt, "out")
-    U.check(U.f64(m), mr, dt, "m")
-    dtr, dzr = ops.softmask_bwd(doutr, tr, mr, rnd)
-    U.check(U.f64(dtt), dtr, dt, "dt")
-    U.check(U.f64(dz), dzr, dt, "dz")
-    U.check(U.f64(acc), rnd(accr + (1.0 + mr) * doutr), dt, "dt accumulate")
+    mraw = ops.sigmoid(zr)
+    U.check(U.f64(out), outr, dt, "out", terms=np.abs((1.0 + mraw) * tr))
+    U.check(U.f64(m), mr, dt, "m", terms=mraw)
+    # the backward reads the M the GPU stored
+    mg = U.f64(m)
+    dtr, dzr = ops.softmask_bwd(doutr, tr, mg, rnd)
+    U.check(U.f64(dtt), dtr, dt, "dt", terms=np.abs((1.0 + mg) * doutr))
+    U.check(U.f64(dz), dzr, dt, "dz", terms=np.abs(doutr * tr * mg * (1.0 - mg)))
+    U.check(U.f64(acc), rnd(accr + (1.0 + mg) * doutr), dt, "dt accumulate",
+            terms=np.abs(accr) + np.abs((1.0 + mg) * doutr))
 
 
 @pytest.mark.parametrize("N,C,V,dt", [(8, 256, 252, "bf16"), (3, 5, 7, "f32"), (1, 1, 1, "f32")])
@@ -281,11 +321,15 @@ def test_head(N, C, V, dt):
     lref = ops.fc_fwd(g, w32.astype(np.float64), b32.astype(np.float64))
     lossr, dl = ops.ce_fwd_bwd(lref, lab)
     dg, dwr, dbr = ops.fc_bwd(dl, g, w32.astype(np.float64))
-    U.check(U.f64(logits), lref, "f32", "logits")
+    w64 = w32.astype(np.float64)
+    U.check(U.f64(logits), lref, "f32", "logits",
+            terms=np.abs(g) @ np.abs(w64).T + np.abs(b32.astype(np.float64)))
     assert abs(float(U.f64(loss)[0]) - lossr) <= 1e-4 * max(1.0, abs(lossr))
-    U.check(U.f64(dfw), dwr, "f32", "dfc_w")
-    U.check(U.f64(dfb), dbr, "f32", "dfc_b")
-    U.check(U.f64(dx), rnd(np.repeat(dg[:, :, None] / V, V, axis=2)), dt, "dx")
+    U.check(U.f64(dfw), dwr, "f32", "dfc_w", kind="sum", terms=np.abs(dl).T @ np.abs(g))
+    U.check(U.f64(dfb), dbr, "f32", "dfc_b", kind="sum", norm=False,
+            terms=np.abs(dl).sum(axis=0))
+    tdx = np.repeat((np.abs(dl) @ np.abs(w64))[:, :, None] / V, V, axis=2)
+    U.check(U.f64(dx), rnd(np.repeat(dg[:, :, None] / V, V, axis=2)), dt, "dx", terms=tdx)
 
 
 def test_sgd_update_is_one_rounding():

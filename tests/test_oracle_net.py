@@ -243,3 +243,91 @@ def test_conv_flop_totals():
     assert abs(f3 / 1e9 - 453.7) < 0.1 and abs(a3 / 1e12 - 1.361) < 0.001
     assert abs(f4 / 1e9 - 331.2) < 0.1 and abs(a4 / 1e12 - 0.971) < 0.001
     assert abs(f5 / 1e12 - 2.856) < 0.001 and abs(a5 / 1e12 - 8.522) < 0.001
+
+
+# ------------------------------------------------------- bf16 store points
+def _is_bf16(a):
+    a = np.asarray(a, dtype=np.float64)
+    return np.array_equal(a, ops.round_bf16(a))
+
+
+# for each operation the network calls: the positions (and keywords) of its
+# arguments that are stored tensors -- activations, activation gradients, the
+# bf16 weight copy -- in bf16 mode (None arguments are skipped)
+_STORED_ARGS = {
+    "conv3d_fwd": (0, 1), "conv3d_dgrad": (0, 1), "conv3d_wgrad": (0, 1),
+    "maxpool3d_fwd": (0,), "maxpool3d_bwd": (0,), "trilinear_fwd": (0,),
+    "trilinear_bwd": (0,), "bn_fwd": (0, 5, "residual"), "bn_bwd": (0, 1, 2),
+    "softmask_fwd": (0, 1), "softmask_bwd": (0, 1, 2), "gap_fwd": (0,),
+}
+
+
+def _trace_inputs(monkeypatch):
+    """Wraps the operations so that every call records its stored-tensor
+    arguments and the unrounded float32 quantities they are given: the conv
+    bias, the BN statistics passed to the backward, the pooled features."""
+    seen = {"stored": [], "unrounded": []}
+    for name, pos in _STORED_ARGS.items():
+        f = getattr(ops, name)
+
+        def wrap(*a, _f=f, _name=name, _pos=pos, **kw):
+            for p in _pos:
+                v = kw.get(p) if isinstance(p, str) else (a[p] if p < len(a) else None)
+                if v is not None:
+                    seen["stored"].append(("%s arg %s" % (_name, p), v))
+            if _name == "conv3d_fwd" and len(a) > 2 and a[2] is not None:
+                seen["unrounded"].append(("conv bias", a[2]))
+            if _name == "bn_bwd":
+                seen["unrounded"] += [("bn mean", a[4]), ("bn invstd", a[5])]
+            return _f(*a, **kw)
+        monkeypatch.setattr(ops, name, wrap)
+    fc = ops.fc_fwd
+
+    def fc_wrap(g, w, b):
+        seen["unrounded"].append(("pooled features", g))
+        return fc(g, w, b)
+    monkeypatch.setattr(ops, "fc_fwd", fc_wrap)
+    return seen
+
+
+def test_bf16_store_points_partition(monkeypatch):
+    """In bf16 mode every tensor an operation reads as a stored activation,
+    activation gradient or conv weight is exactly bf16-representable (a missing
+    rounding at a store point fails here), while the weight gradients, BN
+    statistics and conv biases are not rounded (an extra rounding fails)."""
+    seen = _trace_inputs(monkeypatch)
+    P, _ = _params("partition1", 1, 8, 31)
+    P = {k: v.astype(np.float32).astype(np.float64) for k, v in P.items()}
+    rng = np.random.default_rng(32)
+    x = rng.standard_normal((2, 1, 12, 16, 12))
+    dy = rng.standard_normal((2, 8, 6, 8, 6))
+    y, G, _ = net.partition1_fwd_bwd(P, x, dy, bf16=True)
+    assert len(seen["stored"]) > 100
+    for what, v in seen["stored"]:
+        assert _is_bf16(v), what + " is not a bf16 store"
+    assert _is_bf16(y)
+    for what, v in seen["unrounded"]:
+        assert not _is_bf16(v), what + " was rounded to bf16"
+    for k, g in G.items():
+        if g.size >= 4:
+            assert not _is_bf16(g), "gradient of %s was rounded to bf16" % k
+
+
+def test_bf16_store_points_network(monkeypatch):
+    """The same for the full network (stem with pooling, two stages, head):
+    additionally the logits and the loss stay unrounded."""
+    seen = _trace_inputs(monkeypatch)
+    P, _ = _params("resattnet", 1, 8, 33, stages=(8, 16), stem_c=8)
+    P = {k: v.astype(np.float32).astype(np.float64) for k, v in P.items()}
+    rng = np.random.default_rng(34)
+    x = rng.standard_normal((2, 1, 48, 40, 48))
+    labels = np.array([0, 1])
+    loss, logits, G, _ = net.resattnet_fwd_bwd(P, x, labels, bf16=True)
+    for what, v in seen["stored"]:
+        assert _is_bf16(v), what + " is not a bf16 store"
+    for what, v in seen["unrounded"]:
+        assert not _is_bf16(v), what + " was rounded to bf16"
+    assert not _is_bf16(logits) and not _is_bf16(np.array([loss]))
+    for k, g in G.items():
+        if g.size >= 4:
+            assert not _is_bf16(g), "gradient of %s was rounded to bf16" % k
