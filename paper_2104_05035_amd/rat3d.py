@@ -121,6 +121,11 @@ def lib():
     """The loaded library (built first if no build exists)."""
     global _lib
     if _lib is None:
+        # torch supplies the device memory and streams every call uses; it is
+        # imported before the library is loaded so that its HIP runtime is
+        # loaded first (a HIP call through the library before torch was
+        # imported left torch without a visible GPU)
+        import torch  # noqa: F401
         if not os.path.exists(LIB_PATH):
             from . import build as _b
             _b.build()
