@@ -110,6 +110,23 @@ rat3d_status rat3d_conv3d_wgrad(const rat3d_conv3d_desc* desc, const void* x, co
                                 float* dw, float* dbias, int accumulate, void* ws,
                                 size_t ws_bytes, void* stream);
 
+/* rat3d_conv3d_wgrad without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, results and errors as
+ * rat3d_conv3d_wgrad, except: the split partial sums live in a scratch array
+ * built into the library (rat3d_conv3d_wgrad_noalloc_max_bytes() bytes, 32
+ * MiB, held on each GPU the library runs on until the process ends); a shape
+ * whose rat3d_conv3d_workspace_size(desc, 2) exceeds it returns
+ * RAT3D_EWORKSPACE before anything is enqueued.  The call allocates nothing.
+ * All calls on one GPU share that GPU's scratch array: calls that may run at
+ * the same time on one GPU (different streams) race and must be ordered by
+ * the caller.  The first call on a device looks the array's address up (a
+ * HIP symbol query, no allocation). */
+size_t rat3d_conv3d_wgrad_noalloc_max_bytes(void);
+rat3d_status rat3d_conv3d_wgrad_noalloc(const rat3d_conv3d_desc* desc, const void* x,
+                                        const void* dy, float* dw, float* dbias, int accumulate,
+                                        void* stream);
+
 /* ------------------------------------------------------------------------
  * 3D batch normalisation, training mode, fused with the ReLU of the conv
  * block and the residual add of the residual layer (use-case section).

@@ -86,6 +86,13 @@ static rat3d_status check_conv(const rat3d_conv3d_desc* d, ConvGeom* g) {
     return RAT3D_OK;
 }
 
+rat3d_status check_conv_desc(const rat3d_conv3d_desc* d, ConvGeom* g) { return check_conv(d, g); }
+
+rat3d_status check_act(const void* p, const char* name) {
+    RAT3D_ACT(p, name);
+    return RAT3D_OK;
+}
+
 static rat3d_status check_ws(void* ws, size_t ws_bytes, size_t need) {
     if (need == 0) return RAT3D_OK;
     RAT3D_REQUIRE(ws_bytes >= need, RAT3D_EWORKSPACE, "workspace needs %zu bytes, got %zu",

@@ -21,6 +21,13 @@ inline ConvGeom make_geom(int N, int Ci, int Co, int D, int H, int W, int k, int
     return g;
 }
 
+// ---- argument validation shared by the C entry points (api.cpp) --------
+// The descriptor checks of the conv calls (sizes, k/stride/pad, dtype,
+// non-empty output), filling g; and the NULL / 16-byte alignment check of an
+// activation pointer.  Both set the thread's error message on failure.
+rat3d_status check_conv_desc(const rat3d_conv3d_desc* d, ConvGeom* g);
+rat3d_status check_act(const void* p, const char* name);
+
 // ---- convolution: dispatch (conv.cpp) ----------------------------------
 // Workspace bytes of a pass (0 fwd, 1 dgrad, 2 wgrad).
 size_t conv_ws_bytes(const ConvGeom& g, rat3d_dtype dt, int pass);

@@ -69,6 +69,8 @@ _SIGS = {
     "rat3d_conv3d_dgrad": (_I, [ctypes.POINTER(ConvDesc), _VP, _VP, _VP, _I, _VP, _SZ, _VP]),
     "rat3d_conv3d_wgrad": (_I, [ctypes.POINTER(ConvDesc), _VP, _VP, _VP, _VP, _I, _VP, _SZ,
                                 _VP]),
+    "rat3d_conv3d_wgrad_noalloc_max_bytes": (_SZ, []),
+    "rat3d_conv3d_wgrad_noalloc": (_I, [ctypes.POINTER(ConvDesc), _VP, _VP, _VP, _VP, _I, _VP]),
     "rat3d_bn_workspace_size": (_SZ, [ctypes.POINTER(BnDesc)]),
     "rat3d_bn_relu_fwd": (_I, [ctypes.POINTER(BnDesc)] + [_VP] * 9 + [_VP, _SZ, _VP]),
     "rat3d_bn_relu_bwd": (_I, [ctypes.POINTER(BnDesc)] + [_VP] * 10 + [_I, _VP, _SZ, _VP]),
@@ -194,6 +196,15 @@ def rat3d_conv3d_dgrad(desc, dy, w, dx, accumulate, ws, ws_bytes, stream=None):
 def rat3d_conv3d_wgrad(desc, x, dy, dw, dbias, accumulate, ws, ws_bytes, stream=None):
     _check(lib().rat3d_conv3d_wgrad(ctypes.byref(desc), _p(x), _p(dy), _p(dw), _p(dbias),
                                     int(accumulate), _p(ws), ws_bytes, _stream(stream)))
+
+
+def rat3d_conv3d_wgrad_noalloc_max_bytes():
+    return lib().rat3d_conv3d_wgrad_noalloc_max_bytes()
+
+
+def rat3d_conv3d_wgrad_noalloc(desc, x, dy, dw, dbias, accumulate, stream=None):
+    _check(lib().rat3d_conv3d_wgrad_noalloc(ctypes.byref(desc), _p(x), _p(dy), _p(dw),
+                                            _p(dbias), int(accumulate), _stream(stream)))
 
 
 # ---------------------------------------------------------------- batch norm
