@@ -358,6 +358,52 @@ rat3d_status rat3d_net_running_save(const rat3d_net* net, float* dst, void* stre
 rat3d_status rat3d_net_running_load(rat3d_net* net, const float* src, void* stream);
 
 /* ------------------------------------------------------------------------
+ * GABRA: allocation of the partitions of a model-parallel split to GPUs by
+ * a genetic algorithm (model-parallelisation section, "Genetic Algorithm
+ * Based Resource Allocation": eqs. 3-10, Algorithms 1-3).  Host-only: every
+ * pointer here is HOST memory, nothing is enqueued.
+ *   loads[n] (p_i > 0): computation load of each partition;
+ *   capacities[m] (d_j > 0): capacity of each GPU, in the loads' unit;
+ *   profit of running partition i on GPU j: c_ij = p_i / d_j;
+ *   maximise sum of c over the allocation (eq. 7) subject to no GPU's load
+ *   exceeding its capacity (eq. 8) and each partition on exactly one GPU
+ *   (eq. 9); with every_gpu != 0, also every GPU runs a partition (the
+ *   paper's stated assumption).
+ * Chromosome: gene i = GPU of partition i.  Initial population: each
+ * partition in turn to a GPU drawn uniformly among those with room left (a
+ * stuck chromosome is redrawn, at most init_tries times).  Loop: two
+ * roulette-wheel parents (probability fitness / total), midpoint crossover
+ * with probability crossover_p (paper: 0.8; offspring keep genes at their
+ * positions: first half of one parent, second half of the other; one of the
+ * two offspring by a fair draw, else a copy of the first parent), inversion
+ * mutation of a random segment; an offspring equal to a population member or
+ * infeasible is dropped (selection starts over); otherwise it replaces the
+ * worst member and becomes the best if strictly fitter.  Stops after
+ * `generations` accepted offspring or max_attempts offspring in all.
+ * Random numbers: SplitMix64 seeded with `seed` (deterministic for a seed).
+ * Output: assignment[n] (GPU index of each partition, 0-based) and *profit of
+ * the best allocation found; stats (nullable) receives the counters.
+ * RAT3D_EINVAL on invalid arguments or when no feasible initial chromosome
+ * is found (e.g. total capacity below total load). */
+typedef struct {
+    int population;       /* chromosomes, >= 2 */
+    int generations;      /* t_max: offspring accepted into the population */
+    double crossover_p;   /* in [0, 1] */
+    uint64_t seed;        /* SplitMix64 seed */
+    int every_gpu;        /* nonzero: every GPU must run at least one partition */
+    int64_t max_attempts; /* offspring drawn in all; 0 = 50 * generations */
+    int init_tries;       /* redraws of a stuck initial chromosome; 0 = 1000 */
+} rat3d_gabra_params;
+
+typedef struct {
+    int64_t generations, duplicates, infeasible, attempts;
+} rat3d_gabra_stats;
+
+rat3d_status rat3d_gabra(int n, const double* loads, int m, const double* capacities,
+                         const rat3d_gabra_params* params, int32_t* assignment, double* profit,
+                         rat3d_gabra_stats* stats);
+
+/* ------------------------------------------------------------------------
  * Measurement (off by default).  While enabled, every launch of a hot kernel
  * is bracketed by two hipEvents recorded on the stream it is launched on, and
  * the operation's algorithmic work is added to its tag: convolutions count

@@ -54,6 +54,18 @@ class NetDesc(ctypes.Structure):
                 ("bn_momentum", ctypes.c_float), ("dtype", ctypes.c_int)]
 
 
+class GabraParams(ctypes.Structure):
+    _fields_ = [("population", ctypes.c_int), ("generations", ctypes.c_int),
+                ("crossover_p", ctypes.c_double), ("seed", ctypes.c_uint64),
+                ("every_gpu", ctypes.c_int), ("max_attempts", ctypes.c_int64),
+                ("init_tries", ctypes.c_int)]
+
+
+class GabraStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("generations", "duplicates", "infeasible",
+                                              "attempts")]
+
+
 _lib = None
 _VP = ctypes.c_void_p
 _I = ctypes.c_int
@@ -103,6 +115,8 @@ _SIGS = {
     "rat3d_net_running_count": (_SZ, [_VP]),
     "rat3d_net_running_save": (_I, [_VP, _VP, _VP]),
     "rat3d_net_running_load": (_I, [_VP, _VP, _VP]),
+    "rat3d_gabra": (_I, [_I, _VP, _I, _VP, ctypes.POINTER(GabraParams), _VP, _VP,
+                         ctypes.POINTER(GabraStats)]),
     "rat3d_profile_enable": (_I, [_I]),
     "rat3d_profile_filter": (_I, [ctypes.c_char_p]),
     "rat3d_profile_reset": (_I, []),
@@ -273,6 +287,24 @@ def rat3d_head_fwd_bwd(n, c, v, classes, dtype, x, fc_w, fc_b, labels, logits, l
 
 def rat3d_sgd(count, lr, params, grads, stream=None):
     _check(lib().rat3d_sgd(count, lr, _p(params), _p(grads), _stream(stream)))
+
+
+# ---------------------------------------------------------------- GABRA (host)
+def rat3d_gabra(loads, capacities, population=20, generations=200, crossover_p=0.8, seed=0,
+                every_gpu=False, max_attempts=0, init_tries=0):
+    """Host-side GPU allocation; returns (assignment list, profit, stats dict)."""
+    import numpy as np
+    p = np.ascontiguousarray(loads, dtype=np.float64)
+    d = np.ascontiguousarray(capacities, dtype=np.float64)
+    out = np.zeros(len(p), dtype=np.int32)
+    prof = ctypes.c_double()
+    st = GabraStats()
+    prm = GabraParams(population, generations, crossover_p, seed & ((1 << 64) - 1),
+                      int(every_gpu), max_attempts, init_tries)
+    _check(lib().rat3d_gabra(len(p), p.ctypes.data, len(d), d.ctypes.data, ctypes.byref(prm),
+                             out.ctypes.data, ctypes.byref(prof), ctypes.byref(st)))
+    return ([int(v) for v in out], prof.value,
+            {k: getattr(st, k) for k, _ in GabraStats._fields_})
 
 
 # ---------------------------------------------------------------- measurement
