@@ -125,8 +125,13 @@ class Ctx:
     step has ReLU and max-pool decisions, so it is only piecewise smooth).
     """
 
-    def __init__(self, params, bf16, eps=1e-5, momentum=0.1, running=None, jitter=None):
+    def __init__(self, params, bf16, eps=1e-5, momentum=0.1, running=None, jitter=None,
+                 eval_stats=None):
         self.P = params
+        # inference mode: BN applies the given running statistics
+        # {bn name: (mean, var)} and no parameter gradient is formed
+        self.eval_stats = eval_stats
+        self.param_grads = eval_stats is None
         base = ops.round_bf16 if bf16 else ops.identity
         if jitter is None:
             self.rnd = base
@@ -146,6 +151,10 @@ class Ctx:
         return self.rnd(self.P[name])
 
     def bn(self, name, x, relu, residual=None):
+        if self.eval_stats is not None:
+            rm, rv = self.eval_stats[name]
+            return self.rnd(ops.bn_eval_fwd(x, self.P[name + ".g"], self.P[name + ".b"], rm, rv,
+                                            self.eps, relu, residual)), None
         y, mean, var, invstd = ops.bn_fwd(x, self.P[name + ".g"], self.P[name + ".b"],
                                           self.eps, relu, residual)
         cnt = x.shape[0] * x.shape[2] * x.shape[3] * x.shape[4]
@@ -154,6 +163,10 @@ class Ctx:
         return self.rnd(y), (mean, invstd)
 
     def bn_back(self, name, dy, x, y, st, relu):
+        if self.eval_stats is not None:
+            dx, g = ops.bn_eval_bwd(dy, y, self.P[name + ".g"], self.eval_stats[name][1],
+                                    self.eps, relu)
+            return self.rnd(dx), self.rnd(g)
         dx, g, dgam, dbet = ops.bn_bwd(dy, x, y, self.P[name + ".g"], st[0], st[1], relu)
         self.G[name + ".g"] += dgam
         self.G[name + ".b"] += dbet
@@ -190,17 +203,20 @@ def ru_bwd(ctx, pre, c, dy, dx_acc=None):
     x, s = c["x"], c["stride"]
     dh2, dskip = ctx.bn_back(pre + "bn2", dy, c["h2"], c["y"], c["st2"], relu=True)
     da1 = rnd(ops.conv3d_dgrad(dh2, ctx.w(pre + "conv2.w"), c["a1"].shape, 1, 1))
-    G[pre + "conv2.w"] += ops.conv3d_wgrad(c["a1"], dh2, 3, 1, 1, False)[0]
+    if ctx.param_grads:
+        G[pre + "conv2.w"] += ops.conv3d_wgrad(c["a1"], dh2, 3, 1, 1, False)[0]
     dh1, _ = ctx.bn_back(pre + "bn1", da1, c["h1"], c["a1"], c["st1"], relu=True)
     if c["proj"]:
         dhp, _ = ctx.bn_back(pre + "projbn", dskip, c["hp"], c["sp"], c["stp"], relu=False)
         dxs = ops.conv3d_dgrad(dhp, ctx.w(pre + "proj.w"), x.shape, s, 0)
-        G[pre + "proj.w"] += ops.conv3d_wgrad(x, dhp, 1, s, 0, False)[0]
+        if ctx.param_grads:
+            G[pre + "proj.w"] += ops.conv3d_wgrad(x, dhp, 1, s, 0, False)[0]
     else:
         dxs = dskip
     dx = rnd(dxs if dx_acc is None else dx_acc + dxs)
     dx = rnd(dx + ops.conv3d_dgrad(dh1, ctx.w(pre + "conv1.w"), x.shape, s, 1))
-    G[pre + "conv1.w"] += ops.conv3d_wgrad(x, dh1, 3, s, 1, False)[0]
+    if ctx.param_grads:
+        G[pre + "conv1.w"] += ops.conv3d_wgrad(x, dh1, 3, s, 1, False)[0]
     return dx
 
 
@@ -241,12 +257,14 @@ def am_bwd(ctx, pre, c, dout):
     x = c["x"]
     dT, dz = ops.softmask_bwd(dout, c["T"], c["m"], rnd)
     da = rnd(ops.conv3d_dgrad(dz, ctx.w(pre + "c2.w"), c["a"].shape, 1, 0))
-    dw, db = ops.conv3d_wgrad(c["a"], dz, 1, 1, 0, True)
-    G[pre + "c2.w"] += dw
-    G[pre + "c2.bias"] += db
+    if ctx.param_grads:
+        dw, db = ops.conv3d_wgrad(c["a"], dz, 1, 1, 0, True)
+        G[pre + "c2.w"] += dw
+        G[pre + "c2.bias"] += db
     dc1, _ = ctx.bn_back(pre + "bn", da, c["c1"], c["a"], c["stb"], relu=True)
     du2 = rnd(ops.conv3d_dgrad(dc1, ctx.w(pre + "c1.w"), c["u2"].shape, 1, 0))
-    G[pre + "c1.w"] += ops.conv3d_wgrad(c["u2"], dc1, 1, 1, 0, False)[0]
+    if ctx.param_grads:
+        G[pre + "c1.w"] += ops.conv3d_wgrad(c["u2"], dc1, 1, 1, 0, False)[0]
     dr3 = rnd(ops.trilinear_bwd(du2, c["r3"].shape[2:]))
     du1 = ru_bwd(ctx, pre + "m4.", c["cm4"], dr3)
     dr2b = rnd(ops.trilinear_bwd(du1, c["r2b"].shape[2:]))
@@ -279,7 +297,8 @@ def stem_bwd(ctx, c, dy):
     rnd = ctx.rnd
     da0 = rnd(ops.maxpool3d_bwd(dy, c["am0"], c["a0"].shape)) if c["pool"] else dy
     dh0, _ = ctx.bn_back("stem.bn", da0, c["h0"], c["a0"], c["st0"], relu=True)
-    ctx.G["stem.w"] += ops.conv3d_wgrad(c["x"], dh0, 7, 2, 3, False)[0]
+    if ctx.param_grads:
+        ctx.G["stem.w"] += ops.conv3d_wgrad(c["x"], dh0, 7, 2, 3, False)[0]
 
 
 # --------------------------------------------------------------------------
@@ -373,3 +392,48 @@ def train_step(kind, params, lr, bf16, x=None, labels=None, dy=None,
         raise ValueError(kind)
     new = {k: ops.sgd(v, G[k], lr) for k, v in params.items()}
     return new, G, info
+
+
+def gradcam(params, x, classes, running, target, bf16, eps=1e-5):
+    """3D Grad-CAM of the full network (the explainable block of the use-case
+    section; gradient-weighted class activation mapping), in inference mode:
+    BN applies the running statistics `running` = {bn name: (mean, var)}.
+
+      y^k    = logit of class k = classes[n] for volume n (before the softmax);
+      A      = output of the target stage (0: the stem after pooling, s >= 1:
+               stage s's attention module), shape (N, C, D, H, W);
+      alpha  = alpha[n, c] = mean over voxels of d y^k / d A[n, c];
+      cam    = ReLU(sum_c alpha[n, c] A[n, c]), shape (N, D, H, W);
+      up     = cam resampled trilinearly (half-pixel centres) to the input's
+               D, H, W.
+    bf16 mode rounds stored activations and activation gradients as in
+    training; alpha, cam and up stay unrounded.  Returns dict(logits, A, dA,
+    alpha, cam, up)."""
+    ctx = Ctx(params, bf16, eps, eval_stats=running)
+    x = ctx.rnd(np.asarray(x, dtype=np.float64))
+    h, cs = stem_fwd(ctx, x, pool=True)
+    ns = n_stages(params)
+    caches = []
+    acts = [h]
+    for i in range(ns):
+        pre = "s%d." % (i + 1)
+        h, cr = ru_fwd(ctx, pre + "ru.", h, 1 if i == 0 else 2)
+        h, ca = am_fwd(ctx, pre + "am.", h)
+        caches.append((cr, ca))
+        acts.append(h)
+    g = ops.gap_fwd(h)
+    logits = ops.fc_fwd(g, params["fc.w"], params["fc.b"])
+    n = x.shape[0]
+    # d y^k / d(pooled features) = fc.w[k]; the average pool spreads it evenly
+    dg = np.stack([params["fc.w"][int(classes[i])] for i in range(n)])
+    dh = ctx.rnd(ops.gap_bwd(dg, h.shape[2:]))
+    for i in reversed(range(target, ns)):
+        pre = "s%d." % (i + 1)
+        cr, ca = caches[i]
+        dh = am_bwd(ctx, pre + "am.", ca, dh)
+        dh = ru_bwd(ctx, pre + "ru.", cr, dh)
+    A = acts[target]
+    alpha = dh.mean(axis=(2, 3, 4))
+    cam = np.maximum((alpha[:, :, None, None, None] * A).sum(axis=1), 0.0)
+    up = ops.trilinear_fwd(cam[:, None], x.shape[2:])[:, 0]
+    return dict(logits=logits, A=A, dA=dh, alpha=alpha, cam=cam, up=up)

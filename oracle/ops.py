@@ -310,6 +310,25 @@ def bn_bwd(dy, x, y, gamma, mean, invstd, relu):
     return dx, g, dgamma, dbeta
 
 
+def bn_eval_fwd(x, gamma, beta, run_mean, run_var, eps, relu, residual=None):
+    """Inference-mode BN: y = act(gamma * (x - run_mean) / sqrt(run_var + eps)
+    + beta [+ residual]) with the running statistics in place of the batch's."""
+    s = gamma / np.sqrt(run_var + eps)
+    y = _bc(s) * (x - _bc(run_mean)) + _bc(beta)
+    if residual is not None:
+        y = y + residual
+    return np.maximum(y, 0.0) if relu else y
+
+
+def bn_eval_bwd(dy, y, gamma, run_var, eps, relu):
+    """Gradients of bn_eval_fwd with respect to x and the residual: the map is
+    affine per channel, so dx = g * gamma / sqrt(run_var + eps) with
+    g = dy masked by (y > 0) under ReLU; the residual's gradient is g.
+    Returns (dx, g)."""
+    g = dy * (y > 0.0) if relu else dy.copy()
+    return _bc(gamma / np.sqrt(run_var + eps)) * g, g
+
+
 def bn_running_update(run_mean, run_var, mean, var, count, momentum):
     """Running statistics: r <- (1 - m) r + m * batch value, with the unbiased
     variance var * count / (count - 1)."""

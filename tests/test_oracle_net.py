@@ -17,11 +17,17 @@ def _params(kind, c_in, c, seed, **kw):
 
 
 # ------------------------------------------------------- torch re-build
-def _torch_graph():
+def _torch_graph(running=None):
+    """The graph in torch ops; with `running` = {bn name: (mean, var)} the BN
+    layers run in inference mode on those statistics."""
     torch = pytest.importorskip("torch")
     F = torch.nn.functional
 
     def bn(P, name, x):
+        if running is not None:
+            rm, rv = running[name]
+            return F.batch_norm(x, torch.tensor(rm), torch.tensor(rv), P[name + ".g"],
+                                P[name + ".b"], training=False, eps=1e-5)
         return F.batch_norm(x, None, None, P[name + ".g"], P[name + ".b"], training=True,
                             eps=1e-5)
 
@@ -60,7 +66,7 @@ def _torch_graph():
     def partition1(P, x):
         return am(P, "am.", ru(P, "ru.", stem(P, x, False), 1))
 
-    return torch, dict(ru=ru, am=am, resattnet=resattnet, partition1=partition1)
+    return torch, dict(ru=ru, am=am, resattnet=resattnet, partition1=partition1, stem=stem)
 
 
 def _tp(torch, params):
@@ -331,3 +337,66 @@ def test_bf16_store_points_network(monkeypatch):
     for k, g in G.items():
         if g.size >= 4:
             assert not _is_bf16(g), "gradient of %s was rounded to bf16" % k
+
+
+# ------------------------------------------------------- Grad-CAM
+def _running(layout, seed):
+    rng = np.random.default_rng(seed)
+    return {b: (rng.normal(0, 0.3, dict(layout)[b + ".g"]),
+                rng.uniform(0.5, 2.0, dict(layout)[b + ".g"])) for b in net.bn_names(layout)}
+
+
+def test_gradcam_against_autograd():
+    """Inference-mode Grad-CAM of the full network at every target stage
+    against a torch build of the same graph (BN on the running statistics,
+    autograd for d logit_k / d A): logits, target activations and their
+    gradient, alpha, the map and its trilinear upsampling to the input."""
+    torch, g = _torch_graph()
+    P, layout = _params("resattnet", 1, 4, 41, stages=(8, 8, 8), stem_c=4)
+    running = _running(layout, 42)
+    torch, g = _torch_graph(running)
+    F = torch.nn.functional
+    rng = np.random.default_rng(43)
+    x = rng.standard_normal((2, 1, 24, 28, 24))
+    classes = np.array([1, 0])
+    for target in range(4):
+        out = net.gradcam(P, x, classes, running, target, bf16=False)
+        TP = _tp(torch, P)
+        h = g["stem"](TP, torch.tensor(x), True)
+        acts = [h]
+        for i in range(3):
+            h = g["am"](TP, "s%d.am." % (i + 1),
+                        g["ru"](TP, "s%d.ru." % (i + 1), h, 1 if i == 0 else 2))
+            acts.append(h)
+        acts[target].retain_grad()
+        logits = F.linear(h.mean(dim=(2, 3, 4)), TP["fc.w"], TP["fc.b"])
+        logits[torch.arange(2), torch.tensor(classes)].sum().backward()
+        A, dA = acts[target].detach().numpy(), acts[target].grad.numpy()
+        np.testing.assert_allclose(out["logits"], logits.detach().numpy(), rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(out["A"], A, rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(out["dA"], dA, rtol=1e-8, atol=1e-12)
+        alpha = dA.mean(axis=(2, 3, 4))
+        cam = np.maximum((alpha[:, :, None, None, None] * A).sum(axis=1), 0.0)
+        up = F.interpolate(torch.tensor(cam[:, None]), size=x.shape[2:], mode="trilinear",
+                           align_corners=False)[:, 0].numpy()
+        np.testing.assert_allclose(out["alpha"], alpha, rtol=1e-8, atol=1e-14)
+        np.testing.assert_allclose(out["cam"], cam, rtol=1e-8, atol=1e-14)
+        np.testing.assert_allclose(out["up"], up, rtol=1e-8, atol=1e-14)
+        assert out["cam"].max() > 0.0
+
+
+def test_gradcam_last_stage_is_cam():
+    """At the last stage the head is an average pool and a linear layer, so
+    d logit_k / d A[n, c, v] = fc.w[k, c] / V everywhere: alpha is fc.w[k] / V
+    exactly (class activation mapping)."""
+    P, layout = _params("resattnet", 1, 4, 44, stages=(8, 8, 8), stem_c=4)
+    running = _running(layout, 45)
+    rng = np.random.default_rng(46)
+    x = rng.standard_normal((2, 1, 24, 28, 24))
+    out = net.gradcam(P, x, np.array([0, 1]), running, 3, bf16=False)
+    V = np.prod(out["A"].shape[2:])
+    np.testing.assert_allclose(out["alpha"], P["fc.w"][[0, 1]] / V, rtol=1e-14)
+    # the map is invariant to the class-independent bias and scales with fc.w
+    P2 = dict(P, **{"fc.w": 2.0 * P["fc.w"], "fc.b": P["fc.b"] + 5.0})
+    out2 = net.gradcam(P2, x, np.array([0, 1]), running, 3, bf16=False)
+    np.testing.assert_allclose(out2["cam"], 2.0 * out["cam"], rtol=1e-12)
