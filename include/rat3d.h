@@ -329,6 +329,28 @@ rat3d_status rat3d_block_fwd_bwd(rat3d_net* net, const void* x, const void* dy, 
 rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labels,
                               const void* dy_upstream, float* loss_dev, void* stream);
 
+/* RESATTNET: 3D Grad-CAM, the explainable block of the use-case section
+ * (gradient-weighted class activation mapping), in inference mode: every BN
+ * applies the running statistics held in the workspace (mean 0 / var 1 after
+ * rat3d_net_bind, updated by rat3d_train_step or set by
+ * rat3d_net_running_load), no parameter or its gradient is changed.
+ *   x        [n][1][d][h][w] in the network dtype (device);
+ *   classes  int32 [n] (device): the class k whose logit is explained for
+ *            each volume (clamped into [0, 1]);
+ *   target   the explained map A: 0 = the stem's pooled output, s = 1..3 =
+ *            the output of stage s's attention module;
+ *   logits   float32 [n][2] (device, nullable): the inference-mode logits;
+ *   cam      float32 [n][D_t][H_t][W_t] (device): ReLU(sum_c alpha_c A_c),
+ *            alpha_c = mean over voxels of d logit_k / d A_c, at the target's
+ *            resolution (rat3d_gradcam_shape gives C_t, D_t, H_t, W_t);
+ *   cam_up   float32 [n][d][h][w] (device, nullable): cam resampled
+ *            trilinearly (half-pixel centres) to the input's size.
+ * Uses the network's workspace (the saved activations and gradients are
+ * overwritten). */
+rat3d_status rat3d_gradcam_shape(const rat3d_net* net, int target, int shape[4]);
+rat3d_status rat3d_gradcam(rat3d_net* net, const void* x, const int32_t* classes, int target,
+                           float* logits, float* cam, float* cam_up, void* stream);
+
 /* PARTITION1, one micro-batch at a time (model-parallelisation section: a
  * partition processes micro-batches one after another, computing its weight
  * gradients from the gradient received at its output and accumulating them

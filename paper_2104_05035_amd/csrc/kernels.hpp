@@ -196,6 +196,30 @@ rat3d_status bn_relu_bwd_up2(int N, int C, int Di, int Hi, int Wi, const void* d
                              float* dbeta, int accumulate, void* bn_ws, void* dxc,
                              hipStream_t st);
 
+// ---- inference mode and Grad-CAM (gradcam.hip) --------------------------
+// BN with the running statistics: y = act(x * s + t [+ residual]),
+// s = gamma / sqrt(run_var + eps), t = beta - run_mean * s.
+rat3d_status bn_eval_fwd(const BnGeom& g, rat3d_dtype dt, int relu, float eps, const void* x,
+                         const void* residual, const float* gamma, const float* beta,
+                         const float* run_mean, const float* run_var, void* y, hipStream_t st);
+// Its gradients: dx = s * g (dx may be null), dres = g or dres += g (one
+// rounding; dres may be null), g = dy masked by y > 0 under ReLU.
+rat3d_status bn_eval_bwd(const BnGeom& g, rat3d_dtype dt, int relu, float eps, const void* dy,
+                         const void* y, const float* gamma, const float* run_var, void* dx,
+                         void* dres, int dres_acc, hipStream_t st);
+// dtop[n, c, v] = fc_w[classes[n], c] / V (classes clamped into range).
+rat3d_status gradcam_seed(int N, int C, int64_t V, int classes_n, rat3d_dtype dt,
+                          const float* fc_w, const int32_t* classes, void* dtop, hipStream_t st);
+// logits[n, k] = fc_w[k] . mean_v top[n, :, v] + fc_b[k] (classes_n <= 8).
+rat3d_status gradcam_logits(int N, int C, int64_t V, int classes_n, rat3d_dtype dt,
+                            const void* top, const float* fc_w, const float* fc_b,
+                            float* logits, hipStream_t st);
+// alpha[n, c] = voxel mean of dA; cam[n, v] = max(0, sum_c alpha A); cam_up
+// (nullable) = cam resampled trilinearly to D0 x H0 x W0.
+rat3d_status gradcam_maps(int N, int C, int Dt, int Ht, int Wt, rat3d_dtype dt, const void* A,
+                          const void* dA, float* alpha, float* cam, int D0, int H0, int W0,
+                          float* cam_up, hipStream_t st);
+
 // ---- head, update, casts (head.hip) ------------------------------------
 size_t head_ws_bytes(int N, int C, int classes);
 rat3d_status head_fwd_bwd(int N, int C, int64_t V, int classes, rat3d_dtype dt, const void* x,

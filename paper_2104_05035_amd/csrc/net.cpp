@@ -102,6 +102,7 @@ struct rat3d_net {
            bn_scr_bytes = 0, head_scr_off = 0, run_mean_off = 0, run_var_off = 0,
            logits_off = 0, loss_off = 0;
     size_t run_count = 0;
+    size_t gcam_alpha_off = 0;  // Grad-CAM weights alpha [n][256] (RESATTNET)
     // plan
     TRef stem_h, stem_a, stem_p;
     ConvL stem_conv;
@@ -510,6 +511,118 @@ rat3d_status stem_bwd(const Exec& e, bool pool) {
     return e.conv_w(n->stem_conv, n->ext_x, e.g(n->stem_h));
 }
 
+// ------------------------------------------------------------ inference mode
+// The explainable block (Grad-CAM) runs the network in inference mode: every
+// BN applies its running statistics, an affine map per channel, so its
+// gradient needs no batch sums; no parameter gradient is formed.
+rat3d_status bn_eval_f(const Exec& e, const BnL& b, const TRef& x, const void* res, int relu,
+                       void* y) {
+    return bn_eval_fwd(BnGeom{x.s.n, b.c, x.s.vox()}, e.n->dt, relu, e.n->d.bn_eps, e.a(x), res,
+                       e.par(b.g_off), e.par(b.b_off), e.rmean(b), e.rvar(b), y, e.st);
+}
+
+// x: the BN's input (for its shape); y: its stored output (the ReLU mask)
+rat3d_status bn_eval_b(const Exec& e, const BnL& b, const TRef& x, const void* dy, const void* y,
+                       int relu, void* dx, void* dres, int dres_acc) {
+    return bn_eval_bwd(BnGeom{x.s.n, b.c, x.s.vox()}, e.n->dt, relu, e.n->d.bn_eps, dy, y,
+                       e.par(b.g_off), e.rvar(b), dx, dres, dres_acc, e.st);
+}
+
+rat3d_status ru_fwd_eval(const Exec& e, const RUPlan& r) {
+    RAT3D_TRY(e.conv_f(r.c1, e.a(r.x), e.a(r.h1)));
+    RAT3D_TRY(bn_eval_f(e, r.b1, r.h1, nullptr, 1, e.a(r.a1)));
+    RAT3D_TRY(e.conv_f(r.c2, e.a(r.a1), e.a(r.h2)));
+    const void* skip = e.a(r.x);
+    if (r.proj) {
+        RAT3D_TRY(e.conv_f(r.cp, e.a(r.x), e.a(r.hp)));
+        RAT3D_TRY(bn_eval_f(e, r.bp, r.hp, nullptr, 0, e.a(r.sp)));
+        skip = e.a(r.sp);
+    }
+    return bn_eval_f(e, r.b2, r.h2, skip, 1, e.a(r.y));
+}
+
+// Input gradient of a residual unit in inference mode (acc_dx: add onto the
+// partial sum already in x's gradient); the same join order as training.
+rat3d_status ru_bwd_eval(const Exec& e, const RUPlan& r, bool acc_dx) {
+    void* dx = e.g(r.x);
+    void* dskip = e.p(r.dskip);
+    RAT3D_TRY(bn_eval_b(e, r.b2, r.h2, e.g(r.y), e.a(r.y), 1, e.g(r.h2), r.proj ? dskip : dx,
+                        !r.proj && acc_dx ? 1 : 0));
+    RAT3D_TRY(e.conv_d(r.c2, e.g(r.h2), e.g(r.a1), 0));
+    RAT3D_TRY(bn_eval_b(e, r.b1, r.h1, e.g(r.a1), e.a(r.a1), 1, e.g(r.h1), nullptr, 0));
+    if (r.proj) {
+        RAT3D_TRY(bn_eval_b(e, r.bp, r.hp, dskip, nullptr, 0, e.g(r.hp), nullptr, 0));
+        RAT3D_TRY(e.conv_d(r.cp, e.g(r.hp), dx, acc_dx ? 1 : 0));
+    }
+    return e.conv_d(r.c1, e.g(r.h1), dx, 1);
+}
+
+rat3d_status am_fwd_eval(const Exec& e, const AMPlan& m) {
+    const Shape& s = m.x.s;
+    const Shape& s1 = m.p1.s;
+    const Shape& s2 = m.p2.s;
+    const rat3d_dtype dt = e.n->dt;
+    RAT3D_TRY(ru_fwd_eval(e, m.t1));
+    RAT3D_TRY(ru_fwd_eval(e, m.t2));
+    RAT3D_TRY(pool_fwd(s.n, s.c, s.d, s.h, s.w, 3, 2, 1, dt, e.a(m.x), e.a(m.p1),
+                       (uint8_t*)e.p(m.am1), e.st));
+    RAT3D_TRY(ru_fwd_eval(e, m.m1));
+    RAT3D_TRY(pool_fwd(s.n, s.c, s1.d, s1.h, s1.w, 3, 2, 1, dt, e.a(m.m1.y), e.a(m.p2),
+                       (uint8_t*)e.p(m.am2), e.st));
+    RAT3D_TRY(ru_fwd_eval(e, m.m2));
+    RAT3D_TRY(ru_fwd_eval(e, m.m3));
+    RAT3D_TRY(up_fwd(s.n, s.c, s2.d, s2.h, s2.w, s1.d, s1.h, s1.w, dt, e.a(m.m3.y), e.a(m.u1),
+                     e.st));
+    RAT3D_TRY(ru_fwd_eval(e, m.m4));
+    RAT3D_TRY(e.conv_f(m.c1, e.a(m.m4.y), e.a(m.h1c)));
+    RAT3D_TRY(up_fwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.a(m.h1c), e.a(m.h1),
+                     e.st));
+    RAT3D_TRY(bn_eval_f(e, m.bn, m.h1, nullptr, 1, e.a(m.a)));
+    RAT3D_TRY(e.conv_f(m.c2, e.a(m.a), e.a(m.z)));
+    return softmask_fwd(s.count(), dt, e.a(m.z), e.a(m.t2.y), e.a(m.out), nullptr, e.st);
+}
+
+rat3d_status am_bwd_eval(const Exec& e, const AMPlan& m) {
+    const Shape& s = m.x.s;
+    const Shape& s1 = m.p1.s;
+    const Shape& s2 = m.p2.s;
+    const rat3d_dtype dt = e.n->dt;
+    RAT3D_TRY(softmask_bwd(s.count(), dt, e.g(m.out), e.a(m.t2.y), e.a(m.z), e.g(m.t2.y), 0,
+                           e.g(m.z), e.st, 1));
+    RAT3D_TRY(e.conv_d(m.c2, e.g(m.z), e.g(m.a), 0));
+    RAT3D_TRY(bn_eval_b(e, m.bn, m.h1, e.g(m.a), e.a(m.a), 1, e.g(m.h1), nullptr, 0));
+    RAT3D_TRY(up_bwd(s.n, s.c, s1.d, s1.h, s1.w, s.d, s.h, s.w, dt, e.g(m.h1), e.g(m.h1c), 0,
+                     e.st));
+    RAT3D_TRY(e.conv_d(m.c1, e.g(m.h1c), e.g(m.m4.y), 0));
+    RAT3D_TRY(ru_bwd_eval(e, m.m4, false));
+    RAT3D_TRY(up_bwd(s.n, s.c, s2.d, s2.h, s2.w, s1.d, s1.h, s1.w, dt, e.g(m.u1), e.g(m.m3.y), 0,
+                     e.st));
+    RAT3D_TRY(ru_bwd_eval(e, m.m3, false));
+    RAT3D_TRY(ru_bwd_eval(e, m.m2, false));
+    RAT3D_TRY(pool_bwd(s.n, s.c, s1.d, s1.h, s1.w, 3, 2, 1, dt, e.g(m.p2),
+                       (const uint8_t*)e.p(m.am2), e.g(m.m1.y), 0, e.st));
+    RAT3D_TRY(ru_bwd_eval(e, m.m1, false));
+    RAT3D_TRY(pool_bwd(s.n, s.c, s.d, s.h, s.w, 3, 2, 1, dt, e.g(m.p1),
+                       (const uint8_t*)e.p(m.am1), e.g(m.x), 0, e.st));
+    RAT3D_TRY(ru_bwd_eval(e, m.t2, false));
+    return ru_bwd_eval(e, m.t1, true);
+}
+
+rat3d_status stem_fwd_eval(const Exec& e) {
+    rat3d_net* n = e.n;
+    RAT3D_TRY(e.conv_f(n->stem_conv, n->ext_x, e.a(n->stem_h)));
+    RAT3D_TRY(bn_eval_f(e, n->stem_bn, n->stem_h, nullptr, 1, e.a(n->stem_a)));
+    const Shape& s = n->stem_a.s;
+    return pool_fwd(s.n, s.c, s.d, s.h, s.w, 3, 2, 1, n->dt, e.a(n->stem_a), e.a(n->stem_p),
+                    (uint8_t*)e.p(n->stem_am), e.st);
+}
+
+// The map Grad-CAM weights: the stem's pooled output (target 0) or a stage's
+// attention-module output (targets 1-3).
+const TRef& gradcam_target(const rat3d_net* n, int target) {
+    return target == 0 ? n->stem_p : n->ams[target - 1].out;
+}
+
 rat3d_status prepare_call(rat3d_net* n, hipStream_t st) {
     if (!n->P || !n->G || !n->ws) {
         set_error("rat3d_net: buffers not bound (call rat3d_net_bind first)");
@@ -658,6 +771,8 @@ rat3d_status rat3d_net_create(const rat3d_net_desc* desc, rat3d_net** out) {
     n->head_scr_off = b.alloc(head_ws_bytes(d.n, 256, 2));
     n->run_mean_off = b.alloc(n->run_count * sizeof(float));
     n->run_var_off = b.alloc(n->run_count * sizeof(float));
+    if (d.kind == RAT3D_NET_RESATTNET)
+        n->gcam_alpha_off = b.alloc((size_t)d.n * 256 * sizeof(float));
     n->logits_off = b.alloc((size_t)d.n * 2 * sizeof(float));
     n->loss_off = b.alloc(sizeof(float));
     b.record("logits", n->logits_off, RAT3D_F32, Shape{d.n, 2, 1, 1, 1});
@@ -880,6 +995,59 @@ rat3d_status rat3d_net_running_load(rat3d_net* net, const float* src, void* stre
     }
     net->reset_running = false;  // the loaded statistics replace the bind-time reset
     return RAT3D_OK;
+}
+
+rat3d_status rat3d_gradcam_shape(const rat3d_net* net, int target, int shape[4]) {
+    if (!net || net->d.kind != RAT3D_NET_RESATTNET || target < 0 || target > 3 || !shape) {
+        set_error("rat3d_gradcam_shape: needs a RESATTNET network and 0 <= target <= 3");
+        return RAT3D_EINVAL;
+    }
+    const Shape& t = gradcam_target(net, target).s;
+    shape[0] = t.c;
+    shape[1] = t.d;
+    shape[2] = t.h;
+    shape[3] = t.w;
+    return RAT3D_OK;
+}
+
+rat3d_status rat3d_gradcam(rat3d_net* net, const void* x, const int32_t* classes, int target,
+                           float* logits, float* cam, float* cam_up, void* stream) {
+    if (!net || net->d.kind != RAT3D_NET_RESATTNET) {
+        set_error("rat3d_gradcam: needs a RESATTNET network");
+        return RAT3D_EINVAL;
+    }
+    if (!x || !classes || !cam || target < 0 || target > 3) {
+        set_error("rat3d_gradcam: x, classes and cam must be non-NULL and 0 <= target <= 3");
+        return RAT3D_EINVAL;
+    }
+    if (!aligned16(x)) {
+        set_error("rat3d_gradcam: x must be 16-byte aligned");
+        return RAT3D_EALIGN;
+    }
+    hipStream_t st = (hipStream_t)stream;
+    RAT3D_TRY(prepare_call(net, st));
+    const rat3d_net_desc& d = net->d;
+    net->ext_x = x;
+    Exec e{net, st, 0};
+    RAT3D_TRY(stem_fwd_eval(e));
+    for (int i = 0; i < 3; ++i) {
+        RAT3D_TRY(ru_fwd_eval(e, net->rus[i]));
+        RAT3D_TRY(am_fwd_eval(e, net->ams[i]));
+    }
+    const TRef& top = net->ams[2].out;
+    if (logits)
+        RAT3D_TRY(gradcam_logits(d.n, net->fc_c, top.s.vox(), 2, net->dt, e.a(top),
+                                 e.par(net->fc.w_off), e.par(net->fc.b_off), logits, st));
+    // d logit_k / d top: the FC row of class k spread evenly by the average pool
+    RAT3D_TRY(gradcam_seed(d.n, net->fc_c, top.s.vox(), 2, net->dt, e.par(net->fc.w_off), classes,
+                           e.g(top), st));
+    for (int i = 2; i >= target; --i) {
+        RAT3D_TRY(am_bwd_eval(e, net->ams[i]));
+        RAT3D_TRY(ru_bwd_eval(e, net->rus[i], false));
+    }
+    const TRef& A = gradcam_target(net, target);
+    return gradcam_maps(d.n, A.s.c, A.s.d, A.s.h, A.s.w, net->dt, e.a(A), e.g(A),
+                        (float*)(net->ws + net->gcam_alpha_off), cam, d.d, d.h, d.w, cam_up, st);
 }
 
 }  // extern "C"

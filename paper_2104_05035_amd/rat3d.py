@@ -111,6 +111,8 @@ _SIGS = {
     "rat3d_block_fwd_bwd": (_I, [_VP] * 6),
     "rat3d_train_step": (_I, [_VP] * 6),
     "rat3d_partition_micro_batch": (_I, [_VP, _VP, _VP, _I, _VP]),
+    "rat3d_gradcam_shape": (_I, [_VP, _I, ctypes.POINTER(_I * 4)]),
+    "rat3d_gradcam": (_I, [_VP, _VP, _VP, _I, _VP, _VP, _VP, _VP]),
     "rat3d_net_update": (_I, [_VP, _VP]),
     "rat3d_net_running_count": (_SZ, [_VP]),
     "rat3d_net_running_save": (_I, [_VP, _VP, _VP]),
@@ -405,3 +407,13 @@ class Net:
 
     def rat3d_net_running_load(self, src, stream=None):
         _check(lib().rat3d_net_running_load(self.h, _p(src), _stream(stream)))
+
+    def rat3d_gradcam_shape(self, target):
+        """(C, D, H, W) of the map Grad-CAM explains at `target`."""
+        shp = (_I * 4)()
+        _check(lib().rat3d_gradcam_shape(self.h, int(target), ctypes.byref(shp)))
+        return tuple(shp)
+
+    def rat3d_gradcam(self, x, classes, target, logits, cam, cam_up, stream=None):
+        _check(lib().rat3d_gradcam(self.h, _p(x), _p(classes), int(target), _p(logits), _p(cam),
+                                   _p(cam_up), _stream(stream)))

@@ -13,7 +13,8 @@ whose oracle sees the very inputs the GPU saw:
     neighbouring values), S = sum of |terms| of the defining sum (the float32
     accumulation error of K <= 64k terms stays below 2^-16 S: sqrt(K) 2^-24),
     and `extra` is the propagated bound of an intermediate that the GPU
-    overwrites (a chain of two stores);
+    overwrites (a chain of two stores); plus 2^-126, since float32 results
+    below the normal range may be flushed to zero;
   * float32 sums over voxels (kind "sum": weight, bias and BN-parameter
     gradients, BN means): |g - o| <= extra + min(2^-12, tol) S, where S is
     the sum of |terms| (float32 sums of up to 16 M terms: sqrt(K) 2^-24 <=
@@ -87,6 +88,7 @@ def rel(got, ref):
 
 C_OUT = 2.0 ** -16  # float32 accumulation error of a stored output, per unit of sum|terms|
 C_SUM = 2.0 ** -12  # the same for float32 sums over up to 16 M voxels
+FLUSH = 2.0 ** -126  # smallest normal float32: results below it may be flushed to zero
 
 LAST = {}  # statistics of the last check: rel, n_above_1ulp, n_terms_evaluated, worst
 
@@ -116,11 +118,12 @@ def check(got, ref, dt, what="", terms=None, extra=None, kind="out", norm=True):
             "%s: max abs %.3e" % (what, mx)
     d = np.abs(got - ref)
     ex = 0.0 if extra is None else np.broadcast_to(np.asarray(extra, np.float64), ref.shape)
+    # FLUSH: float32 results below the normal range may be flushed to zero
     if kind == "out":
-        lim = 2.0 * ulp(ref, dt) + ex
+        lim = 2.0 * ulp(ref, dt) + ex + FLUSH
         c = C_OUT
     else:
-        lim = np.broadcast_to(np.asarray(ex, np.float64), ref.shape)
+        lim = np.broadcast_to(np.asarray(ex, np.float64), ref.shape) + FLUSH
         c = min(C_SUM, TOL[dt])
     bad = d > lim + c * np.abs(ref)
     nterms = int(bad.sum())

@@ -82,8 +82,11 @@ class Replay:
     """Checks every layer of a step; accumulates the oracle's parameter
     gradients (and their sum|terms|) over micro-batches."""
 
-    def __init__(self, params, dt, eps=1e-5, verbose=True):
+    def __init__(self, params, dt, eps=1e-5, verbose=True, eval_stats=None):
         self.P = params
+        # inference mode (Grad-CAM): BN on the running statistics
+        # {name: (mean, var)}; no parameter gradients
+        self.eval_stats = eval_stats
         self.dt = dt
         self.rnd = ops.round_bf16 if dt == "bf16" else ops.identity
         self.eps = eps
@@ -149,6 +152,8 @@ class Replay:
         return self.S(dname)
 
     def conv_wgrad(self, wname, x, dy, k, s, p, bname=None):
+        if self.eval_stats is not None:
+            return
         dw, db = ops.conv3d_wgrad(x, dy, k, s, p, bname is not None)
         ax, ady = np.abs(x), np.abs(dy)
         self.add_grad(wname, dw, lambda idx: ops.conv3d_wgrad_points(ax, ady, k, s, p, idx))
@@ -172,10 +177,15 @@ class Replay:
         return gm, gi
 
     def bn_value(self, name, h, st, relu, residual=None):
-        """BN (+ residual) (+ ReLU) of h with statistics st; (unrounded value,
-        sum|terms| of the float32 evaluation x * scale + shift [+ r])."""
-        mean, invstd = st
+        """BN (+ residual) (+ ReLU) of h with statistics st (inference mode:
+        the running statistics); (unrounded value, sum|terms| of the float32
+        evaluation x * scale + shift [+ r])."""
         g, b = self.P[name + ".g"], self.P[name + ".b"]
+        if self.eval_stats is not None:
+            rm, rv = self.eval_stats[name]
+            mean, invstd = rm, 1.0 / np.sqrt(rv + self.eps)
+        else:
+            mean, invstd = st
         sc = g * invstd
         y = _bc(sc) * (h - _bc(mean)) + _bc(b)
         terms = np.abs(h) * _bc(np.abs(sc)) + _bc(np.abs(b) + np.abs(mean * sc))
@@ -187,7 +197,7 @@ class Replay:
         return y, terms
 
     def bn_fwd(self, name, h, yname, relu, residual=None, res_extra=None):
-        st = self.bn_stats(name, h)
+        st = self.bn_stats(name, h) if self.eval_stats is None else None
         y, terms = self.bn_value(name, h, st, relu, residual)
         self.chk(yname, self.S(yname), self.rnd(y), terms=terms, extra=res_extra)
         return st
@@ -196,8 +206,16 @@ class Replay:
         """Backward of a BN (+ReLU); the ReLU mask is y > 0 of the GPU's
         stored output.  Returns (rounded dx, gradient of the residual input,
         sum|terms| of dx)."""
-        mean, invstd = st
         gam = self.P[name + ".g"]
+        if self.eval_stats is not None:
+            # inference mode: dx = g * gamma / sqrt(running var + eps)
+            dx, gres = ops.bn_eval_bwd(dy, y, gam, self.eval_stats[name][1], self.eps, relu)
+            terms = np.abs(dx)
+            ref = self.rnd(dx)
+            if dxname is not None:
+                self.chk(dxname, self.S(dxname), ref, terms=terms)
+            return ref, gres, terms
+        mean, invstd = st
         dx, gres, dgam, dbet = ops.bn_bwd(dy, h, y, gam, mean, invstd, relu)
         M = h.shape[0] * h.shape[2] * h.shape[3] * h.shape[4]
         xh = (h - _bc(mean)) * _bc(invstd)
@@ -239,7 +257,14 @@ class Replay:
         c["a1"] = self.S(pre + "a1")
         c["h2"] = self.conv_fwd(pre + "h2", c["a1"], pre + "conv2.w", None, 1, 1)
         extra = None
-        if proj:
+        if proj and self.eval_stats is not None:
+            # inference mode: the projection BN's output is stored
+            c["hp"] = self.conv_fwd(pre + "hp", x, pre + "proj.w", None, stride, 0)
+            c["stp"] = None
+            spv, spt = self.bn_value(pre + "projbn", c["hp"], None, relu=False)
+            self.chk(pre + "sp", self.S(pre + "sp"), self.rnd(spv), terms=spt)
+            skip = self.S(pre + "sp")
+        elif proj:
             c["hp"] = self.conv_fwd(pre + "hp", x, pre + "proj.w", None, stride, 0)
             c["stp"] = self.bn_stats(pre + "projbn", c["hp"])
             spv, spt = self.bn_value(pre + "projbn", c["hp"], c["stp"], relu=False)
@@ -330,9 +355,12 @@ class Replay:
         um = U.ulp(m, self.dt)
         dT = (1.0 + m) * dout
         dz = dout * T * m * (1.0 - m)
-        self.chk("d:" + pre + "t2.y", self.S("d:" + pre + "t2.y"), self.rnd(dT), terms=np.abs(dT),
-                 extra=um * np.abs(dout))
-        self.chk("d:" + pre + "z", self.S("d:" + pre + "z"), self.rnd(dz), terms=np.abs(dz),
+        # sum|terms| of the factors 1 + M and 1 - M is 1 + |M| (1 - M cancels
+        # when M is close to 1)
+        self.chk("d:" + pre + "t2.y", self.S("d:" + pre + "t2.y"), self.rnd(dT),
+                 terms=np.abs(dout) * (1.0 + np.abs(m)), extra=um * np.abs(dout))
+        self.chk("d:" + pre + "z", self.S("d:" + pre + "z"), self.rnd(dz),
+                 terms=np.abs(dout * T * m) * (1.0 + np.abs(m)),
                  extra=um * (np.abs(1.0 - 2.0 * m) + um) * np.abs(dout * T))
         dzg = self.S("d:" + pre + "z")
         self.conv_dgrad("d:" + pre + "a", dzg, pre + "c2.w", c["a"].shape, 1, 0)
@@ -446,6 +474,37 @@ class Replay:
             self.am_bwd(pre + "am.", ca, "d:" + pre + "am.out", "d:" + pre + "ru.y")
             self.ru_bwd(pre + "ru.", cr, "d:" + pre + "ru.y", "d:" + hin)
         self.stem_bwd(cs, pool=True)
+
+    def gradcam(self, S, classes, target, stages=3):
+        """Inference-mode Grad-CAM pass (the forward, the logits, the seed
+        d logit_k / d top, and the backward down to the target map); the map
+        kernels themselves are checked by the caller on the GPU's A and dA."""
+        assert self.eval_stats is not None
+        self.S = S
+        cs = self.stem_fwd(pool=True)
+        h = "stem.p"
+        caches = []
+        for i in range(stages):
+            pre = "s%d." % (i + 1)
+            cr = self.ru_fwd(pre + "ru.", h, 1 if i == 0 else 2)
+            ca = self.am_fwd(pre + "am.", pre + "ru.y", pre + "am.out")
+            caches.append((cr, ca, h))
+            h = pre + "am.out"
+        top = S(h)
+        W, b = self.P["fc.w"], self.P["fc.b"]
+        g = ops.gap_fwd(top)
+        self.chk("logits", S("logits"), ops.fc_fwd(g, W, b), dt="f32",
+                 terms=np.abs(g) @ np.abs(W).T + np.abs(b))
+        V = top.shape[2] * top.shape[3] * top.shape[4]
+        seed = np.stack([W[int(k)] for k in classes])[:, :, None, None, None] / V
+        seed = np.broadcast_to(seed, top.shape)
+        self.chk("d:" + h, S("d:" + h), self.rnd(seed), terms=np.abs(seed))
+        del cs
+        for i in reversed(range(target, stages)):
+            pre = "s%d." % (i + 1)
+            cr, ca, hin = caches[i]
+            self.am_bwd(pre + "am.", ca, "d:" + pre + "am.out", "d:" + pre + "ru.y")
+            self.ru_bwd(pre + "ru.", cr, "d:" + pre + "ru.y", "d:" + hin)
 
     # ------------------------------------------------------------ gradients
     def finish(self, G):

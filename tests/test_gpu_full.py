@@ -343,9 +343,10 @@ def test_full_softmask(full):
         dout = full.dy_last[:, cs]
         dT, dz = (1.0 + mr) * dout, dout * t * mr * (1.0 - mr)
         chk(full.host("d:am.z", cs), ops.round_bf16(dz), "bf16", "mask logit gradient" + tag,
-            terms=np.abs(dz), extra=um * (np.abs(1.0 - 2.0 * mr) + um) * np.abs(dout * t))
+            terms=np.abs(dout * t * mr) * (1.0 + mr),
+            extra=um * (np.abs(1.0 - 2.0 * mr) + um) * np.abs(dout * t))
         chk(full.host("d:am.t2.y", cs), ops.round_bf16(dT), "bf16", "trunk output gradient" + tag,
-            terms=np.abs(dT), extra=um * np.abs(dout))
+            terms=np.abs(dout) * (1.0 + mr), extra=um * np.abs(dout))
 
 
 def test_full_sgd_update(full):

@@ -292,8 +292,8 @@ def test_softmask_fuse(count, dt):
     # the backward reads the M the GPU stored
     mg = U.f64(m)
     dtr, dzr = ops.softmask_bwd(doutr, tr, mg, rnd)
-    U.check(U.f64(dtt), dtr, dt, "dt", terms=np.abs((1.0 + mg) * doutr))
-    U.check(U.f64(dz), dzr, dt, "dz", terms=np.abs(doutr * tr * mg * (1.0 - mg)))
+    U.check(U.f64(dtt), dtr, dt, "dt", terms=np.abs(doutr) * (1.0 + np.abs(mg)))
+    U.check(U.f64(dz), dzr, dt, "dz", terms=np.abs(doutr * tr * mg) * (1.0 + np.abs(mg)))
     U.check(U.f64(acc), rnd(accr + (1.0 + mg) * doutr), dt, "dt accumulate",
             terms=np.abs(accr) + np.abs((1.0 + mg) * doutr))
 
