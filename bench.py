@@ -13,10 +13,15 @@ Prints one JSON line.  value = algorithmic conv3d fwd+dgrad+wgrad TFLOP/s of
 the whole step (conv flops per step / step time); volumes_per_s is the same
 step counted in volumes.  An untimed breakdown pass brackets every tagged
 launch with hipEvents (kernels_ms_per_step, conv_kernels = conv flops over
-the conv kernels' own time, elementwise_hbm) and names the dominant kernel;
-in the timed region only that kernel's launches are bracketed.  The roofline object is for the kernel with the most
-time, timed with hipEvents recorded on its own launch stream by the library
-during the timed region.  cpu_baseline times the oracle on a bounded sample.
+the conv kernels' own time, elementwise_hbm) and names the dominant kernel.
+In the timed region only the dominant kernel's launches of the last step
+carry event pairs (hipEvents recorded by the library on its launch stream):
+they give the roofline's average launch duration.  After the timed region:
+achievable-peak probes (a bf16 MFMA stream and a 16-byte streaming copy),
+whose rates give the `frac_achievable` fields next to the datasheet
+fractions, and the throughput of the full network's train step (8 volumes)
+and of one attention module (4 x 64 x 48^3), each timed without events.
+cpu_baseline times the oracle on a bounded sample.
 """
 import argparse
 import json
@@ -79,20 +84,122 @@ def cpu_baseline(volumes=2):
                       % (volumes, flops / 1e12)}
 
 
-def elementwise_hbm(tags):
+def elementwise_hbm(tags, copy_gbs):
     """Achieved HBM bandwidth of the bandwidth-bound kernels: algorithmic bytes
     (each tensor a kernel must read or write, once) over their hipEvent time,
-    overall and per kernel tag, as a fraction of the 8 TB/s peak."""
+    overall and per kernel tag, as a fraction of the 8 TB/s peak and of the
+    measured streaming-copy rate."""
     ew = [t for t in tags if t[3] == 0 and t[4] > 0]
     tot_b = sum(t[4] for t in ew)
     tot_ms = sum(t[2] for t in ew)
     if tot_ms <= 0:
         return None
     per = sorted(ew, key=lambda t: -t[2])[:10]
-    return {"achieved": round(tot_b / (tot_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
-            "unit": "GB/s", "frac": round(tot_b / (tot_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+    ach = tot_b / (tot_ms * 1e-3) / 1e9
+    return {"achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+            "frac_achievable": round(ach / copy_gbs, 4),
             "by_kernel": {t[0]: round(t[4] / (t[2] * 1e-3) / 1e9 / PEAK_HBM_GBS, 3)
                           for t in per}}
+
+
+def achievable_peaks(torch, R, reps=5):
+    """Measured ceilings (untimed, after the step): a pure bf16 MFMA stream
+    (4 waves per SIMD, independent accumulators) and a 16-byte streaming copy
+    of 1 GiB (four times the Infinity Cache); best of `reps`."""
+    stream = torch.cuda.current_stream()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks, iters = 4 * cus, 20000
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda:0")
+    flops = R.rat3d_probe_mfma_flops(blocks, iters)
+    nb = 1 << 30
+    src = torch.ones(nb // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+
+    def best(fn):
+        fn()
+        t = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            t.append(e0.elapsed_time(e1))
+        return min(t)
+    ms_m = best(lambda: R.rat3d_probe_mfma(blocks, iters, sink))
+    ms_c = best(lambda: R.rat3d_probe_copy(src, dst, nb))
+    del sink, src, dst
+    torch.cuda.empty_cache()
+    return {"mfma_tflops": round(flops / (ms_m * 1e-3) / 1e12, 1),
+            "copy_gbs": round(2.0 * nb / (ms_c * 1e-3) / 1e9, 1),
+            "probes": "bf16 MFMA 16x16x32 stream, %d workgroups x 4 waves x %d x 4 MFMA; "
+                      "16-byte copy of 1 GiB; best of %d" % (blocks, iters, reps)}
+
+
+def other_config(torch, R, synth, kind, steps, warmup):
+    """Throughput of the other two bf16 workloads: the full network's train
+    step (8 volumes 96x112x96, stem, three stages, head, SGD) and one
+    attention module's forward + backward (4 x 64 x 48^3).  Conv flops per step
+    from one profiled step; the timed steps carry no events."""
+    import numpy as np
+    stream = torch.cuda.current_stream()
+    if kind == "resattnet":
+        n, vol = 8, (96, 112, 96)
+        net = R.Net(R.NET_RESATTNET, n, 1, 32, *vol, R.BF16, lr=1e-4)
+    else:
+        n, vol = 4, (48, 48, 48)
+        net = R.Net(R.NET_ATTN, n, 64, 64, *vol, R.BF16)
+    layout = net.params()
+    rng_p, rng_x, rng_l = synth.streams(3 if kind == "resattnet" else 2, 3)
+    P0 = synth.init_params(rng_p, [(nm, shp) for nm, _, shp in layout])
+    arena = np.concatenate([P0[nm].astype(np.float32).ravel() for nm, _, _ in layout])
+    P = torch.from_numpy(arena).to("cuda:0")
+    G = torch.zeros_like(P)
+    ws = torch.empty(net.workspace_size, dtype=torch.uint8, device="cuda:0")
+    net.rat3d_net_bind(P, G, ws, ws.numel())
+    if kind == "resattnet":
+        x = torch.from_numpy(synth.mri_volumes(rng_x, n, vol)).to(torch.bfloat16).to("cuda:0")
+        labels = torch.from_numpy(rng_l.integers(0, 2, n).astype(np.int32)).to("cuda:0")
+        step = lambda: net.rat3d_train_step(x, labels, None, None)
+    else:
+        shp = (n, 64) + vol
+        x = torch.from_numpy(rng_x.standard_normal(shp, dtype=np.float32)).to(torch.bfloat16)
+        x = x.to("cuda:0")
+        dy = torch.from_numpy(rng_l.standard_normal(shp, dtype=np.float32)).to(torch.bfloat16)
+        dy = dy.to("cuda:0")
+        y, dx = torch.empty_like(x), torch.empty_like(x)
+        step = lambda: net.rat3d_block_fwd_bwd(x, dy, y, dx)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    R.rat3d_profile_reset()
+    R.rat3d_profile_enable(1)
+    step()
+    torch.cuda.synchronize()
+    R.rat3d_profile_enable(0)
+    tags = [R.rat3d_profile_read(i) for i in range(R.rat3d_profile_count())]
+    conv_flops = sum(t[3] for t in tags if t[0].startswith("conv"))
+    conv_ms = sum(t[2] for t in tags if t[3] > 0 or t[0] in ("wgrad_reduce", "bias_grad"))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    out = {"workload": ("full network train step: 8 volumes 96x112x96, stem 7^3 s2 -> 32, "
+                        "stages 64/128/256 (RU + attention module), GAP, FC, CE, SGD"
+                        if kind == "resattnet" else
+                        "attention module forward + backward, 4 x 64 x 48^3"),
+           "ms_per_step": round(ms, 3), "volumes_per_s": round(n / (ms * 1e-3), 1),
+           "conv_tflop_per_step": round(conv_flops / 1e12, 4),
+           "conv_tflops": round(conv_flops / (ms * 1e-3) / 1e12, 1),
+           "conv_kernels_tflops": round(conv_flops / (conv_ms * 1e-3) / 1e12, 1),
+           "launches_per_step": int(sum(t[1] for t in tags)), "steps": steps}
+    del net, P, G, ws
+    torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -101,6 +208,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the full-network and attention-module throughput lines")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the timed steps, copy 256 MiB device-to-device once (the "
                          "reference dispatch that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -134,17 +243,19 @@ def main():
     tags = [R.rat3d_profile_read(i) for i in range(R.rat3d_profile_count())]
     dom_tag = max(tags, key=lambda t: t[2])[0]
 
-    # Timed region: only the dominant kernel's launches carry event pairs (an
-    # event pair around each of the ~650 launches of a step would add its own
-    # cost to the step time).
+    # Timed region: K steps.  Only the dominant kernel's launches of the last
+    # step carry event pairs (an event pair costs ~10 us of gap; around each
+    # of the ~650 launches of every step it would add its own cost to the
+    # step time); they give its average launch duration for the roofline.
     R.rat3d_profile_reset()
     R.rat3d_profile_filter(dom_tag)
-    R.rat3d_profile_enable(1)
     torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     ev0.record(stream)
-    for _ in range(args.steps):
+    for i in range(args.steps):
+        if i == args.steps - 1:
+            R.rat3d_profile_enable(1)
         net.rat3d_train_step(x, None, dy, None)
     ev1.record(stream)
     torch.cuda.synchronize()
@@ -170,8 +281,17 @@ def main():
     roof["traffic"] = profsum.lookup(dom[0])
     roof["kernel"] = dom[0]
     roof["avg_launch_us"] = round(per_launch_ms * 1e3, 3)
-    roof["launches_per_step"] = dom[1] // args.steps
-    roof["timed_in"] = "timed region (hipEvents on the launch stream)"
+    roof["launches_per_step"] = dom[1]
+    roof["timed_in"] = "last step of the timed region (hipEvents on the launch stream)"
+    del net, P, G, ws, x, dy
+    torch.cuda.empty_cache()
+    peaks = achievable_peaks(torch, R)
+    if roof["bound"] == "mfma":
+        roof["frac_achievable"] = round(achieved / peaks["mfma_tflops"], 5)
+        roof["achievable_peak"] = peaks["mfma_tflops"]
+    else:
+        roof["frac_achievable"] = round(achieved / peaks["copy_gbs"], 5)
+        roof["achievable_peak"] = peaks["copy_gbs"]
 
     if args.calib_copy:
         src = torch.empty(256 * 1024 * 1024, dtype=torch.uint8, device="cuda:0").fill_(1)
@@ -205,8 +325,12 @@ def main():
         "kernels_ms_per_step": {t[0]: round(t[2] / bsteps, 3) for t in kernels},
         "breakdown_steps": bsteps,
         "roofline": roof,
-        "elementwise_hbm": elementwise_hbm(tags),
+        "elementwise_hbm": elementwise_hbm(tags, peaks["copy_gbs"]),
+        "achievable_peaks": peaks,
     }
+    if not args.no_other_configs:
+        out["full_network"] = other_config(torch, R, synth, "resattnet", args.steps, args.warmup)
+        out["attention_module"] = other_config(torch, R, synth, "attn", args.steps, args.warmup)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out), flush=True)

@@ -445,6 +445,16 @@ int rat3d_profile_count(void);
 rat3d_status rat3d_profile_read(int i, const char** name, int64_t* launches, double* total_ms,
                                 double* alg_flops, double* alg_bytes);
 
+/* Achievable-peak probes (measurement only; they touch no training data).
+ * rat3d_probe_mfma: `blocks` workgroups of 4 waves, each wave issuing `iters`
+ * iterations of 4 independent bf16 MFMAs (16x16x32); sink [blocks * 256]
+ * float32 (device) receives per-lane sums.  rat3d_probe_mfma_flops gives the
+ * flops of such a launch.  rat3d_probe_copy: dst = src over `bytes` (a
+ * multiple of 16; both 16-byte aligned) with 16-byte accesses. */
+double rat3d_probe_mfma_flops(int blocks, int iters);
+rat3d_status rat3d_probe_mfma(int blocks, int iters, float* sink, void* stream);
+rat3d_status rat3d_probe_copy(const void* src, void* dst, size_t bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -214,6 +214,152 @@ __global__ __launch_bounds__(256) void conv_gather_fd(ConvGeom g, const T* __res
             }
 }
 
+// ---------------------------------------------------------------- strided dgrad
+// Input gradient of a strided convolution, decomposed by phase: input voxel
+// i (per axis) receives from tap t only when s divides i + p - t, i.e. when
+// t = (i + p) mod s (mod s).  The voxels of one residue class r = i mod s per
+// axis therefore share one tap set (t0 + s j < k, t0 = (r + p) mod s), and
+// for such a voxel i = r + s m the source position is od = m + (r + p - t)/s.
+// blockIdx.z picks the class (rd, rh, rw); its rows are the class's voxels
+// (n, md, mh, mw) and its K the Co x (its taps) products, so no product is a
+// structural zero (the k^3 taps are split over the s^3 classes).  A class
+// without taps (k < s) stores zeros (or leaves an accumulated dx unchanged).
+template <typename T>
+__global__ __launch_bounds__(256) void conv_gather_dgrad_phase(ConvGeom g,
+                                                               const T* __restrict__ dy,
+                                                               const T* __restrict__ wt,
+                                                               T* __restrict__ dx,
+                                                               int accumulate) {
+    constexpr int KV = MfmaCfg<T>::KV, BK = MfmaCfg<T>::BK;
+    __shared__ __align__(16) unsigned char As[64 * kRow];
+    __shared__ __align__(16) unsigned char Bs[64 * kRow];
+    __shared__ int4 ktab[BK];  // (co or -1, od offset, oh offset, ow offset)
+    __shared__ int ttab[BK];   // flattened tap kd * k^2 + kh * k + kw
+
+    const int s = g.s;
+    const int cls = blockIdx.z;
+    const int rd = cls / (s * s), rh = (cls / s) % s, rw = cls % s;
+    // rows: the class's voxels; taps per axis
+    const int Md = rd < g.D ? (g.D - rd + s - 1) / s : 0;
+    const int Mh = rh < g.H ? (g.H - rh + s - 1) / s : 0;
+    const int Mw = rw < g.W ? (g.W - rw + s - 1) / s : 0;
+    const int t0d = (rd + g.p) % s, t0h = (rh + g.p) % s, t0w = (rw + g.p) % s;
+    const int nd = t0d < g.k ? (g.k - t0d + s - 1) / s : 0;
+    const int nh = t0h < g.k ? (g.k - t0h + s - 1) / s : 0;
+    const int nw = t0w < g.k ? (g.k - t0w + s - 1) / s : 0;
+    const int KTc = nd * nh * nw;
+    const int Kc = g.Co * KTc;
+    const int64_t Vc = (int64_t)Md * Mh * Mw;
+    const int64_t M = (int64_t)g.N * Vc;
+    const int64_t m0 = (int64_t)blockIdx.x * 64;
+    if (m0 >= M) return;  // this class has fewer rows than the grid covers
+    const int c0 = blockIdx.y * 64;
+    const int KT = g.k * g.k * g.k;
+    const int64_t Vsrc = (int64_t)g.Do * g.Ho * g.Wo;
+    const int64_t Vdst = (int64_t)g.D * g.H * g.W;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    const int ar = tid >> 2, aq = tid & 3;
+    const int64_t am = m0 + ar;
+    const bool arow_ok = am < M;
+    int a_d = 0, a_h = 0, a_w = 0;
+    int64_t a_base = 0;
+    if (arow_ok) {
+        const int64_t n = am / Vc;
+        int64_t sp = am - n * Vc;
+        a_d = (int)(sp / ((int64_t)Mh * Mw));
+        sp -= (int64_t)a_d * Mh * Mw;
+        a_h = (int)(sp / Mw);
+        a_w = (int)(sp - (int64_t)a_h * Mw);
+        a_base = n * g.Co * Vsrc;
+    }
+    const int bcol = c0 + (tid >> 2), bq = tid & 3;
+
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int k0 = 0; k0 < Kc; k0 += BK) {
+        if (tid < BK) {
+            const int k = k0 + tid;
+            int4 e = make_int4(-1, 0, 0, 0);
+            int t = 0;
+            if (k < Kc) {
+                const int co = k / KTc;
+                int r = k - co * KTc;
+                const int jd = r / (nh * nw);
+                r -= jd * nh * nw;
+                const int jh = r / nw, jw = r - (r / nw) * nw;
+                const int td = t0d + s * jd, th = t0h + s * jh, tw = t0w + s * jw;
+                e = make_int4(co, (rd + g.p - td) / s, (rh + g.p - th) / s, (rw + g.p - tw) / s);
+                t = (td * g.k + th) * g.k + tw;
+            }
+            ktab[tid] = e;
+            ttab[tid] = t;
+        }
+        __syncthreads();
+        {
+            T v[KV];
+#pragma unroll
+            for (int j = 0; j < KV; ++j) {
+                const int4 e = ktab[aq * KV + j];
+                T val = Elt<T>::to_bits(0.f);
+                if (arow_ok && e.x >= 0) {
+                    const int od = a_d + e.y, oh = a_h + e.z, ow = a_w + e.w;
+                    if ((unsigned)od < (unsigned)g.Do && (unsigned)oh < (unsigned)g.Ho &&
+                        (unsigned)ow < (unsigned)g.Wo)
+                        val = dy[a_base + e.x * Vsrc + ((int64_t)od * g.Ho + oh) * g.Wo + ow];
+                }
+                v[j] = val;
+            }
+            store_frag<T>(As + ar * kRow + aq * 16, v);
+        }
+        {
+            T v[KV];
+#pragma unroll
+            for (int j = 0; j < KV; ++j) {
+                const int kk = bq * KV + j;
+                T val = Elt<T>::to_bits(0.f);
+                const int co = ktab[kk].x;
+                if (bcol < g.Ci && co >= 0)
+                    val = wt[((int64_t)co * g.Ci + bcol) * KT + ttab[kk]];
+                v[j] = val;
+            }
+            store_frag<T>(Bs + (tid >> 2) * kRow + bq * 16, v);
+        }
+        __syncthreads();
+        tile_mma<T>(As, Bs, acc, lane, wm, wn);
+    }
+
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int row = wm * 32 + i * 16 + 4 * (lane >> 4) + e;
+                const int col = wn * 32 + j * 16 + (lane & 15);
+                const int64_t m = m0 + row;
+                const int c = c0 + col;
+                if (m < M && c < g.Ci) {
+                    const int64_t n = m / Vc;
+                    int64_t sp = m - n * Vc;
+                    const int md = (int)(sp / ((int64_t)Mh * Mw));
+                    sp -= (int64_t)md * Mh * Mw;
+                    const int mh = (int)(sp / Mw), mw = (int)(sp - (sp / Mw) * Mw);
+                    const int64_t off = (n * g.Ci + c) * Vdst +
+                                        ((int64_t)(rd + s * md) * g.H + rh + s * mh) * g.W + rw +
+                                        s * mw;
+                    float v = acc[i][j][e];
+                    if (accumulate) v += Elt<T>::ld(dx + off);
+                    Elt<T>::st(dx + off, v);
+                }
+            }
+}
+
 // ---------------------------------------------------------------- wgrad
 template <typename T>
 __global__ __launch_bounds__(256) void conv_gather_wgrad(ConvGeom g, const T* __restrict__ x,
@@ -484,8 +630,26 @@ rat3d_status conv_fwd_gather(const ConvGeom& g, rat3d_dtype dt, const void* x, c
                             : gather_fd<float>(g, false, x, w, bias, y, 0, st);
 }
 
+template <typename T>
+static rat3d_status gather_dgrad_phase(const ConvGeom& g, const void* dy, const void* w, void* dx,
+                                       int accumulate, hipStream_t st) {
+    ProfScope ps("conv_gather_dgrad_s2", st, conv_flops(g), conv_bytes(g, sizeof(T)));
+    // the largest class (residue 0 on every axis) sets the row grid
+    const int64_t rows = (int64_t)g.N * ceil_div(g.D, g.s) * ceil_div(g.H, g.s) *
+                         ceil_div(g.W, g.s);
+    dim3 grid((unsigned)ceil_div(rows, 64), (unsigned)ceil_div(g.Ci, 64),
+              (unsigned)(g.s * g.s * g.s));
+    conv_gather_dgrad_phase<T><<<grid, 256, 0, st>>>(g, (const T*)dy, (const T*)w, (T*)dx,
+                                                     accumulate);
+    RAT3D_LAUNCH_CHECK();
+    return RAT3D_OK;
+}
+
 rat3d_status conv_dgrad_gather(const ConvGeom& g, rat3d_dtype dt, const void* dy, const void* w,
                                void* dx, int accumulate, hipStream_t st) {
+    if (g.s > 1)  // phase-decomposed: no structurally zero products
+        return dt == RAT3D_BF16 ? gather_dgrad_phase<bf16>(g, dy, w, dx, accumulate, st)
+                                : gather_dgrad_phase<float>(g, dy, w, dx, accumulate, st);
     return dt == RAT3D_BF16 ? gather_fd<bf16>(g, true, dy, w, nullptr, dx, accumulate, st)
                             : gather_fd<float>(g, true, dy, w, nullptr, dx, accumulate, st);
 }

@@ -119,6 +119,9 @@ _SIGS = {
     "rat3d_net_running_load": (_I, [_VP, _VP, _VP]),
     "rat3d_gabra": (_I, [_I, _VP, _I, _VP, ctypes.POINTER(GabraParams), _VP, _VP,
                          ctypes.POINTER(GabraStats)]),
+    "rat3d_probe_mfma_flops": (ctypes.c_double, [_I, _I]),
+    "rat3d_probe_mfma": (_I, [_I, _I, _VP, _VP]),
+    "rat3d_probe_copy": (_I, [_VP, _VP, _SZ, _VP]),
     "rat3d_profile_enable": (_I, [_I]),
     "rat3d_profile_filter": (_I, [ctypes.c_char_p]),
     "rat3d_profile_reset": (_I, []),
@@ -310,6 +313,18 @@ def rat3d_gabra(loads, capacities, population=20, generations=200, crossover_p=0
 
 
 # ---------------------------------------------------------------- measurement
+def rat3d_probe_mfma_flops(blocks, iters):
+    return lib().rat3d_probe_mfma_flops(blocks, iters)
+
+
+def rat3d_probe_mfma(blocks, iters, sink, stream=None):
+    _check(lib().rat3d_probe_mfma(blocks, iters, _p(sink), _stream(stream)))
+
+
+def rat3d_probe_copy(src, dst, nbytes, stream=None):
+    _check(lib().rat3d_probe_copy(_p(src), _p(dst), nbytes, _stream(stream)))
+
+
 def rat3d_profile_enable(enable):
     _check(lib().rat3d_profile_enable(int(enable)))
 

@@ -66,6 +66,13 @@ CONV_CASES = [
     (2, 64, 64, 4, 8, 16, 1, 1, 0, True, "bf16"),
     (1, 32, 64, 8, 8, 8, 1, 1, 0, False, "bf16"),
     (3, 80, 48, 4, 4, 8, 1, 1, 0, False, "bf16"),
+    # strided input gradients by phase class: float32, stride 3, even kernels,
+    # classes without taps (1^3 stride 2), ragged class grids
+    (2, 3, 5, 9, 8, 7, 3, 2, 1, False, "f32"),
+    (1, 4, 6, 7, 9, 8, 1, 2, 0, True, "f32"),
+    (1, 2, 3, 8, 8, 8, 2, 2, 0, False, "f32"),
+    (1, 2, 3, 10, 9, 8, 3, 3, 1, False, "bf16"),
+    (3, 70, 65, 5, 6, 7, 3, 2, 1, False, "bf16"),
     # stem kernels (1 -> 32, 7^3, stride 2, pad 3): full and ragged tiles
     (2, 1, 32, 24, 30, 32, 7, 2, 3, False, "bf16"),
     (1, 1, 32, 13, 9, 21, 7, 2, 3, False, "bf16"),
