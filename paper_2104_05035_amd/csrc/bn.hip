@@ -66,21 +66,30 @@ size_t bn_ws_bytes(const BnGeom& g) {
     return ((size_t)g.C * sl.per_channel * 2 + (size_t)g.C) * sizeof(float);
 }
 
-// Block reduction of two floats; result valid in thread 0.
+// Block reduction of two floats; result valid in thread 0.  Each wave sums
+// its lanes with an xor butterfly, then thread 0 adds the four wave sums in
+// order: one barrier instead of a shared-memory tree (a fixed order).
 __device__ __forceinline__ void block_sum2(float& a, float& b) {
-    __shared__ float ra[kBnThreads], rb[kBnThreads];
-    ra[threadIdx.x] = a;
-    rb[threadIdx.x] = b;
-    __syncthreads();
-    for (int w = kBnThreads / 2; w > 0; w >>= 1) {
-        if ((int)threadIdx.x < w) {
-            ra[threadIdx.x] += ra[threadIdx.x + w];
-            rb[threadIdx.x] += rb[threadIdx.x + w];
-        }
-        __syncthreads();
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        a += __shfl_xor(a, m, 64);
+        b += __shfl_xor(b, m, 64);
     }
-    a = ra[0];
-    b = rb[0];
+    __shared__ float ra[kBnThreads / 64], rb[kBnThreads / 64];
+    if ((threadIdx.x & 63) == 0) {
+        ra[threadIdx.x >> 6] = a;
+        rb[threadIdx.x >> 6] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        a = ra[0];
+        b = rb[0];
+#pragma unroll
+        for (int w = 1; w < kBnThreads / 64; ++w) {
+            a += ra[w];
+            b += rb[w];
+        }
+    }
 }
 
 // Block (c, n * SP + seg): segment seg of plane (n, c).

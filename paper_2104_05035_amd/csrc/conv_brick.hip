@@ -91,6 +91,59 @@ __global__ void prep_dgrad_weights(const bf16* __restrict__ w, int Co, int Ci, i
     wt[(((int64_t)(co >> 5) * KT + (KT - 1 - t)) * Ci + ci) * 32 + (co & 31)] = w[i];
 }
 
+// Several convolutions' weight layouts in one launch: job j covers global
+// indices [begin_j, begin_j + Co*Ci*KT) and writes the forward or
+// input-gradient layout above.
+struct PrepBatch {
+    const bf16* w[kPrepJobs];
+    bf16* wt[kPrepJobs];
+    int co[kPrepJobs], ci[kPrepJobs], kt[kPrepJobs], dg[kPrepJobs];
+    int64_t begin[kPrepJobs + 1];
+    int n;
+};
+
+__global__ void prep_weights_batch(PrepBatch b) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= b.begin[b.n]) return;
+    int lo = 0, hi = b.n - 1;  // the job whose range holds i
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (b.begin[mid] <= i) lo = mid;
+        else hi = mid - 1;
+    }
+    const int64_t e = i - b.begin[lo];
+    const int KT = b.kt[lo], Ci = b.ci[lo], Co = b.co[lo];
+    const int t = (int)(e % KT);
+    const int c = (int)((e / KT) % Ci);
+    const int co = (int)(e / ((int64_t)KT * Ci));
+    const bf16 v = b.w[lo][e];
+    if (b.dg[lo])
+        b.wt[lo][(((int64_t)(co >> 5) * KT + (KT - 1 - t)) * Ci + c) * 32 + (co & 31)] = v;
+    else
+        b.wt[lo][(((int64_t)(c >> 5) * KT + t) * Co + co) * 32 + (c & 31)] = v;
+}
+
+rat3d_status brick_prep_weights_batch(const PrepJob* jobs, int n, hipStream_t st) {
+    for (int j0 = 0; j0 < n; j0 += kPrepJobs) {
+        PrepBatch b{};
+        b.n = n - j0 < kPrepJobs ? n - j0 : kPrepJobs;
+        b.begin[0] = 0;
+        for (int j = 0; j < b.n; ++j) {
+            const PrepJob& J = jobs[j0 + j];
+            b.w[j] = (const bf16*)J.w;
+            b.wt[j] = (bf16*)J.wt;
+            b.co[j] = J.g.Co;
+            b.ci[j] = J.g.Ci;
+            b.kt[j] = J.g.k * J.g.k * J.g.k;
+            b.dg[j] = J.dgrad ? 1 : 0;
+            b.begin[j + 1] = b.begin[j] + (int64_t)J.g.Co * J.g.Ci * b.kt[j];
+        }
+        prep_weights_batch<<<(unsigned)ceil_div(b.begin[b.n], 256), 256, 0, st>>>(b);
+        RAT3D_LAUNCH_CHECK();
+    }
+    return RAT3D_OK;
+}
+
 // ---------------------------------------------------------------- fwd / dgrad
 // LDS brick layout: voxel v = (dd * PH + hh) * PW + ww holds 64 bytes, four
 // 16-byte slots of eight channels; channel group cg sits in slot

@@ -88,6 +88,15 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
 // pass (Co * Ci * k^3 bf16 elements) from w [Co][Ci][k^3].
 rat3d_status brick_prep_weights(const ConvGeom& g, bool dgrad, const void* w, void* wt,
                                 hipStream_t st);
+// The same for several convolutions, kPrepJobs per launch.
+constexpr int kPrepJobs = 24;
+struct PrepJob {
+    ConvGeom g;
+    bool dgrad;
+    const void* w;
+    void* wt;
+};
+rat3d_status brick_prep_weights_batch(const PrepJob* jobs, int n, hipStream_t st);
 rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, float* dw,
                               int accumulate, void* ws, hipStream_t st);
 

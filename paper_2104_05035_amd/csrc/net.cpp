@@ -635,14 +635,15 @@ rat3d_status prepare_call(rat3d_net* n, hipStream_t st) {
     }
     if (n->dt == RAT3D_BF16)
         RAT3D_TRY(cast_f32_bf16((int64_t)n->param_count, n->P, (bf16*)(n->ws + n->mirror_off), st));
+    // every conv's prepared weight layouts, a few launches in all
+    std::vector<PrepJob> jobs;
     for (const ConvL& c : n->convs) {
         const void* w = n->dt == RAT3D_BF16 ? (const void*)(n->ws + n->mirror_off + c.w_off * 2)
                                             : (const void*)(n->P + c.w_off);
         for (int pass = 0; pass < 2; ++pass)
-            if (c.wt_off[pass] >= 0)
-                RAT3D_TRY(conv_prepare(c.g, n->dt, pass, w, n->ws + c.wt_off[pass], st));
+            if (c.wt_off[pass] >= 0) jobs.push_back(PrepJob{c.g, pass == 1, w, n->ws + c.wt_off[pass]});
     }
-    return RAT3D_OK;
+    return jobs.empty() ? RAT3D_OK : brick_prep_weights_batch(jobs.data(), (int)jobs.size(), st);
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }

@@ -40,21 +40,24 @@ __global__ __launch_bounds__(kProbeThreads) void probe_mfma_k(int iters, float* 
     sink[(int64_t)blockIdx.x * kProbeThreads + threadIdx.x] = s;
 }
 
+// Each workgroup copies 4 x 256 16-byte vectors: four loads in flight per
+// thread, every load instruction covering 1 KiB contiguous per wave; the grid
+// covers the buffer once (the shape of the fast elementwise passes).
 __global__ __launch_bounds__(kProbeThreads) void probe_copy_k(const uint4* __restrict__ src,
                                                               uint4* __restrict__ dst,
                                                               int64_t n) {
-    // four 16-byte loads in flight per thread before their stores
-    const int64_t stride = (int64_t)gridDim.x * kProbeThreads;
-    int64_t i = (int64_t)blockIdx.x * kProbeThreads + threadIdx.x;
-    for (; i + 3 * stride < n; i += 4 * stride) {
-        const uint4 v0 = src[i], v1 = src[i + stride], v2 = src[i + 2 * stride],
-                    v3 = src[i + 3 * stride];
-        dst[i] = v0;
-        dst[i + stride] = v1;
-        dst[i + 2 * stride] = v2;
-        dst[i + 3 * stride] = v3;
+    const int64_t base = (int64_t)blockIdx.x * kProbeThreads * 4 + threadIdx.x;
+    uint4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int64_t i = base + j * kProbeThreads;
+        if (i < n) v[j] = src[i];
     }
-    for (; i < n; i += stride) dst[i] = src[i];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int64_t i = base + j * kProbeThreads;
+        if (i < n) dst[i] = v[j];
+    }
 }
 
 }  // namespace
@@ -86,9 +89,9 @@ rat3d_status rat3d_probe_copy(const void* src, void* dst, size_t bytes, void* st
         return RAT3D_EINVAL;
     }
     const int64_t n = (int64_t)(bytes / 16);
-    const int blocks = device_cus() * 8;
-    probe_copy_k<<<blocks, kProbeThreads, 0, (hipStream_t)stream>>>((const uint4*)src,
-                                                                     (uint4*)dst, n);
+    const int64_t blocks = ceil_div(n, (int64_t)kProbeThreads * 4);
+    probe_copy_k<<<(unsigned)blocks, kProbeThreads, 0, (hipStream_t)stream>>>(
+        (const uint4*)src, (uint4*)dst, n);
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }

@@ -419,25 +419,35 @@ __global__ __launch_bounds__(kEwThreads) void up_fwd_tab_k(const T* __restrict__
     Elt<T>::st(y + (int64_t)plane * Ho * Wo + t, c0 * (1.f - ld) + c1 * ld);
 }
 
+// Transpose of the trilinear resampling with per-axis tap tables: every
+// block builds the tables of the three axes in LDS (an input index's output
+// positions and weights), then each thread forms one input voxel's gradient.
 template <typename T>
-__global__ __launch_bounds__(kEwThreads) void up_bwd_tab_k(const T* __restrict__ dy, int Di,
-                                                           int Hi, int Wi, int Do, int Ho, int Wo,
-                                                           float sd, float sh, float sw,
+__global__ __launch_bounds__(kEwThreads) void up_bwd_tab_k(const T* __restrict__ dy, int NC,
+                                                           int Di, int Hi, int Wi, int Do, int Ho,
+                                                           int Wo, float sd, float sh, float sw,
                                                            T* __restrict__ dx, int accumulate) {
-    __shared__ AxisTaps hts[kAxisMax], wts[kAxisMax];
-    for (int i = threadIdx.x; i < Hi; i += kEwThreads) axis_taps(i, Hi, Ho, sh, hts[i]);
-    for (int i = threadIdx.x; i < Wi; i += kEwThreads) axis_taps(i, Wi, Wo, sw, wts[i]);
+    extern __shared__ AxisTaps tabs[];  // [Di + Hi + Wi]
+    AxisTaps* dts = tabs;
+    AxisTaps* hts = tabs + Di;
+    AxisTaps* wts = hts + Hi;
+    for (int i = threadIdx.x; i < Di + Hi + Wi; i += kEwThreads) {
+        if (i < Di)
+            axis_taps(i, Di, Do, sd, dts[i]);
+        else if (i < Di + Hi)
+            axis_taps(i - Di, Hi, Ho, sh, hts[i - Di]);
+        else
+            axis_taps(i - Di - Hi, Wi, Wo, sw, wts[i - Di - Hi]);
+    }
     __syncthreads();
-    const int t = blockIdx.x * kEwThreads + threadIdx.x;
-    if (t >= Hi * Wi) return;
-    const int ih = t / Wi, iw = t - ih * Wi;
-    const int plane = blockIdx.y;  // nc * Di + id
-    const int nc = plane / Di, id = plane - nc * Di;
-    AxisTaps td;
-    axis_taps(id, Di, Do, sd, td);
+    const int64_t t = (int64_t)blockIdx.x * kEwThreads + threadIdx.x;
+    if (t >= (int64_t)NC * Di * Hi * Wi) return;
+    const int iw = (int)(t % Wi), ih = (int)((t / Wi) % Hi), id = (int)((t / ((int64_t)Wi * Hi)) % Di);
+    const int64_t nc = t / ((int64_t)Wi * Hi * Di);
+    const AxisTaps& td = dts[id];
     const AxisTaps& th = hts[ih];
     const AxisTaps& tw = wts[iw];
-    const T* g = dy + (int64_t)nc * Do * Ho * Wo;
+    const T* g = dy + nc * Do * Ho * Wo;
     float sum = 0.f;
     for (int a = 0; a < td.n; ++a)
         for (int b = 0; b < th.n; ++b) {
@@ -446,9 +456,8 @@ __global__ __launch_bounds__(kEwThreads) void up_bwd_tab_k(const T* __restrict__
             for (int c = 0; c < tw.n; ++c) r += tw.w[c] * Elt<T>::ld(row + tw.o[c]);
             sum += td.w[a] * th.w[b] * r;
         }
-    const int64_t i = (int64_t)plane * Hi * Wi + t;
-    const float base = accumulate ? Elt<T>::ld(dx + i) : 0.f;
-    Elt<T>::st(dx + i, base + sum);
+    const float base = accumulate ? Elt<T>::ld(dx + t) : 0.f;
+    Elt<T>::st(dx + t, base + sum);
 }
 
 // ---------------------------------------------------------------- exact x2, bf16
@@ -480,7 +489,8 @@ __device__ __forceinline__ float x2_w(int o, int m, int n) {
 // share at most one or two halo planes; the XCD-aware block order keeps
 // them in the same L2.
 
-constexpr int kPlanes = 2;           // destination depth planes per block
+constexpr int kPlanes = 2;           // destination depth planes per block (pool gradient)
+constexpr int kPlanesF = 2;          // output depth planes per block (pool forward)
 constexpr size_t kPlaneLds = 65536;  // dynamic LDS limit of the staged kernels
 
 // 8 consecutive elements p .. p+7 of a plane of n elements (p % 8 == 0);
@@ -501,36 +511,47 @@ __device__ __forceinline__ void ld8(const bf16* __restrict__ plane, int p, int n
     }
 }
 
-// Max pool 3^3, stride 2, pad 1, bf16.  Phase A: per input (h, w), the
-// maximum over the depth taps of each output plane and the first kd that
-// reaches it.  Phase B: the 3 x 3 in-plane window; a later (kh, kw) wins on a
-// larger value, or on an equal value with a smaller kd -- together the first
-// maximum in (kd, kh, kw) order, as in pool_fwd_k.
+// Order-preserving key of a bfloat16 value (upper half) and a window tap:
+// the unsigned maximum of keys is the largest value and, among equal values,
+// the smallest scan index (the low byte holds 255 - index).  Signed zeros
+// map to one key, as they compare equal.
+__device__ __forceinline__ uint32_t pool_key_hi(uint32_t bits) {
+    bits &= 0xffffu;
+    if (bits == 0x8000u) bits = 0u;
+    return ((bits & 0x8000u) ? (~bits & 0xffffu) : (bits | 0x8000u)) << 16;
+}
+__device__ __forceinline__ float pool_key_value(uint32_t key) {
+    const uint32_t o = key >> 16;
+    const uint32_t bits = (o & 0x8000u) ? (o & 0x7fffu) : (~o & 0xffffu);
+    return __uint_as_float(bits << 16);
+}
+
+// Max pool 3^3, stride 2, pad 1, bf16, as maxima of order-preserving keys
+// (value, then the first tap in (kd, kh, kw) scan order, as in pool_fwd_k).
+// Phase A: per input (h, w) and output plane, the maximum key over the depth
+// taps (low byte 255 - 9 kd), kept in LDS.  Phase B: the 3 x 3 in-plane
+// window, each tap's key lowered by kh * 3 + kw; with Wo % 4 == 0 a thread
+// forms four outputs of a row from the 3 x 9 keys their windows share.
 __global__ __launch_bounds__(kEwThreads) void pool332_fwd_pl(const bf16* __restrict__ x, int D,
                                                              int H, int W, int Do, int Ho, int Wo,
                                                              int nblk, bf16* __restrict__ y,
                                                              uint8_t* __restrict__ am) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int HW = H * W, HW8 = (HW + 7) & ~7;
-    bf16* mv = reinterpret_cast<bf16*>(smem);                    // [kPlanes][HW8]
-    uint8_t* mk = smem + (size_t)kPlanes * HW8 * sizeof(bf16);  // [kPlanes][HW8]
+    uint32_t* mk = reinterpret_cast<uint32_t*>(smem);  // [kPlanesF][HW8] keys
     const int L = xcd_remap(blockIdx.x, gridDim.x);
-    const int nc = L / nblk, od0 = (L - nc * nblk) * kPlanes;
+    const int nc = L / nblk, od0 = (L - nc * nblk) * kPlanesF;
     const bool vec = (HW & 7) == 0;
     const bf16* xv = x + (int64_t)nc * D * HW;
     for (int p = threadIdx.x * 8; p < HW; p += kEwThreads * 8) {
-        float best[kPlanes][8];
-        int bkd[kPlanes][8];
+        uint32_t best[kPlanesF][8];
 #pragma unroll
-        for (int j = 0; j < kPlanes; ++j)
+        for (int j = 0; j < kPlanesF; ++j)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                best[j][e] = 0.f;
-                bkd[j][e] = -1;
-            }
+            for (int e = 0; e < 8; ++e) best[j][e] = 0u;
         // all source planes are requested before any is used (clamped plane
         // index, so no load waits behind a branch)
-        constexpr int NQ = 2 * kPlanes + 1;
+        constexpr int NQ = 2 * kPlanesF + 1;
         uint4 raw[NQ];
         if (vec) {
 #pragma unroll
@@ -543,51 +564,82 @@ __global__ __launch_bounds__(kEwThreads) void pool332_fwd_pl(const bf16* __restr
         for (int q = 0; q < NQ; ++q) {
             const int id = 2 * od0 - 1 + q;
             if (id < 0 || id >= D) continue;
-            float v[8];
+            uint32_t kv[8];
             if (vec) {
                 const uint32_t w[4] = {raw[q].x, raw[q].y, raw[q].z, raw[q].w};
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    v[2 * i] = __uint_as_float(w[i] << 16);
-                    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+                    kv[2 * i] = pool_key_hi(w[i]);
+                    kv[2 * i + 1] = pool_key_hi(w[i] >> 16);
                 }
             } else {
-                ld8(xv + (int64_t)id * HW, p, HW, false, v);
+                const bf16* pl = xv + (int64_t)id * HW;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) kv[e] = p + e < HW ? pool_key_hi(pl[p + e]) : 0u;
             }
 #pragma unroll
-            for (int j = 0; j < kPlanes; ++j) {
+            for (int j = 0; j < kPlanesF; ++j) {
                 const int kd = q - 2 * j;
                 if (kd < 0 || kd > 2) continue;
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    if (bkd[j][e] < 0 || v[e] > best[j][e]) {
-                        best[j][e] = v[e];
-                        bkd[j][e] = kd;
-                    }
+                    best[j][e] = max(best[j][e], kv[e] | (uint32_t)(255 - 9 * kd));
             }
         }
 #pragma unroll
-        for (int j = 0; j < kPlanes; ++j) {
-            uint32_t w4[4], k2[2] = {0u, 0u};
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                w4[i] = (__float_as_uint(best[j][2 * i]) >> 16) |
-                        (__float_as_uint(best[j][2 * i + 1]) & 0xffff0000u);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) k2[e >> 2] |= (uint32_t)(bkd[j][e] & 0xff) << (8 * (e & 3));
-            *reinterpret_cast<uint4*>(mv + j * HW8 + p) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
-            *reinterpret_cast<uint2*>(mk + j * HW8 + p) = make_uint2(k2[0], k2[1]);
+        for (int j = 0; j < kPlanesF; ++j) {
+            uint4* dst = reinterpret_cast<uint4*>(mk + j * HW8 + p);
+            dst[0] = make_uint4(best[j][0], best[j][1], best[j][2], best[j][3]);
+            dst[1] = make_uint4(best[j][4], best[j][5], best[j][6], best[j][7]);
         }
     }
     __syncthreads();
     const int HWo = Ho * Wo;
-    for (int it = threadIdx.x; it < kPlanes * HWo; it += kEwThreads) {
+    if ((Wo & 3) == 0) {
+        const int Q = Wo >> 2, HQ = Ho * Q;
+        for (int it = threadIdx.x; it < kPlanesF * HQ; it += kEwThreads) {
+            const int j = it / HQ, r = it - j * HQ;
+            const int od = od0 + j;
+            if (od >= Do) break;
+            const int oh = r / Q, ow0 = (r - oh * Q) * 4;
+            uint32_t b[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int kh = 0; kh < 3; ++kh) {
+                const int ih = 2 * oh - 1 + kh;
+                if ((unsigned)ih >= (unsigned)H) continue;
+                // columns 2 * ow0 - 1 .. 2 * ow0 + 7: tap kw of output e is c = 2e + kw;
+                // a padding column keeps key 0, below every value
+                const uint32_t* row = mk + j * HW8 + ih * W;
+                uint32_t cw[9];
+#pragma unroll
+                for (int c = 0; c < 9; ++c) {
+                    const int iw = 2 * ow0 - 1 + c;
+                    cw[c] = (unsigned)iw < (unsigned)W ? row[iw] : 0u;
+                }
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int kw = 0; kw < 3; ++kw) {
+                        const uint32_t k = cw[2 * e + kw];
+                        b[e] = max(b[e], k ? k - (uint32_t)(kh * 3 + kw) : 0u);
+                    }
+            }
+            const int64_t o = ((int64_t)nc * Do + od) * HWo + oh * Wo + ow0;
+            *reinterpret_cast<uint2*>(y + o) = make_uint2(
+                pack_bf16x2(pool_key_value(b[0]), pool_key_value(b[1])),
+                pack_bf16x2(pool_key_value(b[2]), pool_key_value(b[3])));
+            *reinterpret_cast<uint32_t*>(am + o) =
+                (255u - (b[0] & 0xffu)) | (255u - (b[1] & 0xffu)) << 8 |
+                (255u - (b[2] & 0xffu)) << 16 | (255u - (b[3] & 0xffu)) << 24;
+        }
+        return;
+    }
+    for (int it = threadIdx.x; it < kPlanesF * HWo; it += kEwThreads) {
         const int j = it / HWo, r = it - j * HWo;
         const int od = od0 + j;
         if (od >= Do) break;
         const int oh = r / Wo, ow = r - oh * Wo;
-        float best = 0.f;
-        int bk = 3, arg = -1;
+        uint32_t b = 0u;
 #pragma unroll
         for (int kh = 0; kh < 3; ++kh) {
             const int ih = 2 * oh - 1 + kh;
@@ -596,19 +648,12 @@ __global__ __launch_bounds__(kEwThreads) void pool332_fwd_pl(const bf16* __restr
             for (int kw = 0; kw < 3; ++kw) {
                 const int iw = 2 * ow - 1 + kw;
                 if ((unsigned)iw >= (unsigned)W) continue;
-                const int s = j * HW8 + ih * W + iw;
-                const float v = bf2f(mv[s]);
-                const int kd = mk[s];
-                if (arg < 0 || v > best || (v == best && kd < bk)) {
-                    best = v;
-                    bk = kd;
-                    arg = kh * 3 + kw;
-                }
+                b = max(b, mk[j * HW8 + ih * W + iw] - (uint32_t)(kh * 3 + kw));
             }
         }
         const int64_t o = ((int64_t)nc * Do + od) * HWo + r;
-        y[o] = f2bf(best);
-        am[o] = (uint8_t)(bk * 9 + arg);
+        y[o] = f2bf(pool_key_value(b));
+        am[o] = (uint8_t)(255u - (b & 0xffu));
     }
 }
 
@@ -1056,9 +1101,9 @@ rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, ra
     const double es = dt == RAT3D_BF16 ? 2.0 : 4.0;
     ProfScope ps("pool_fwd", st, 0.0, es * ((double)N * C * D * H * W + total) + total);
     const int HW8 = (H * W + 7) & ~7;
-    const size_t lds_f = (size_t)kPlanes * HW8 * 3;
+    const size_t lds_f = (size_t)kPlanesF * HW8 * 4;
     if (k == 3 && s == 2 && p == 1 && dt == RAT3D_BF16 && lds_f <= kPlaneLds) {
-        const int nblk = (int)ceil_div(Do, kPlanes);
+        const int nblk = (int)ceil_div(Do, kPlanesF);
         pool332_fwd_pl<<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_f, st>>>(
             (const bf16*)x, D, H, W, Do, Ho, Wo, nblk, (bf16*)y, argmax);
         RAT3D_LAUNCH_CHECK();
@@ -1181,15 +1226,16 @@ rat3d_status up_bwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
         RAT3D_LAUNCH_CHECK();
         return RAT3D_OK;
     }
-    if (Hi <= kAxisMax && Wi <= kAxisMax && (int64_t)N * C * Di < 65536) {
-        const dim3 grid((unsigned)ceil_div((int64_t)Hi * Wi, kEwThreads), N * C * Di);
+    if (Di <= kAxisMax && Hi <= kAxisMax && Wi <= kAxisMax) {
+        const size_t lds = (size_t)(Di + Hi + Wi) * sizeof(AxisTaps);
         if (dt == RAT3D_BF16)
-            up_bwd_tab_k<bf16><<<grid, kEwThreads, 0, st>>>((const bf16*)dy, Di, Hi, Wi, Do, Ho, Wo,
-                                                            sd, sh, sw, (bf16*)dx, accumulate);
+            up_bwd_tab_k<bf16><<<blocks, kEwThreads, lds, st>>>((const bf16*)dy, N * C, Di, Hi, Wi,
+                                                                Do, Ho, Wo, sd, sh, sw, (bf16*)dx,
+                                                                accumulate);
         else
-            up_bwd_tab_k<float><<<grid, kEwThreads, 0, st>>>((const float*)dy, Di, Hi, Wi, Do, Ho,
-                                                             Wo, sd, sh, sw, (float*)dx,
-                                                             accumulate);
+            up_bwd_tab_k<float><<<blocks, kEwThreads, lds, st>>>((const float*)dy, N * C, Di, Hi,
+                                                                 Wi, Do, Ho, Wo, sd, sh, sw,
+                                                                 (float*)dx, accumulate);
         RAT3D_LAUNCH_CHECK();
         return RAT3D_OK;
     }
