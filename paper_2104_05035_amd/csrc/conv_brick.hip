@@ -430,11 +430,39 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     // stages into the buffer again, so no producer overwrites a unit another
     // has not drained, and the global stores (and any wait for them) stay off
     // the consumer waves.
+    auto dst_rsrc = [&](const Tile& T) {
+        return buf_rsrc_u(a.dst + (int64_t)T.n * a.Ct * V, (uint32_t)a.Ct * Vb);
+    };
     constexpr int kRowsMain = PD * PH * 8;  // rows in columns 1 .. 16
     static_assert(KS != 3 || (PW == 18 && kRowsMain + PD * PH / 2 + 2 >= 16 * kBD * kBH),
                   "staged outputs fit the brick");
-    const bool staged_epi = !ACC && (a.W & 7) == 0;
-    auto write_outputs = [&](int k, unsigned char* buf) {
+    // Accumulating 3^3 outputs take the same path: the consumer lanes load
+    // the old values of the results they hold (all loads of a tile in flight
+    // together, after the tile's last MFMA has freed the operand registers)
+    // and add them before the single rounding; the producers' stores stay
+    // plain bf16 stores.
+    const bool staged_epi = (!ACC || KS == 3) && (a.W & 7) == 0;
+    using OldV = uint2[ACC ? NR : 1][ACC ? CT : 1];
+    auto load_old = [&](int k, OldV& o) {
+        const Tile T = tile_of(k);
+        const __amdgpu_buffer_rsrc_t dst_r = dst_rsrc(T);
+        const int w = T.w0 + 4 * kg;
+        // lanes past the width read zeros (offset past the buffer end); the
+        // producers never store those units
+        const uint32_t lo =
+            w < a.W ? (uint32_t)(((T.co0 + wc * CT * 16 + li) * V + w) * 2) : 0x80000000u;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            const int d = T.d0 + wd * RD + r / kBH, h = T.h0 + r % kBH;  // wave-uniform
+            const bool ok = d < a.D && h < a.H;
+            const uint32_t so = ok ? (uint32_t)((d * HW + h * a.W) * 2) : 0u;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct)
+                o[r][ct] = ok ? buf_ld8(dst_r, lo + (uint32_t)(ct * 16 * V * 2), so)
+                              : make_uint2(0u, 0u);
+        }
+    };
+    auto write_outputs = [&](int k, unsigned char* buf, const OldV& old) {
         const Tile T = tile_of(k);
         float bv[CT];
 #pragma unroll
@@ -479,10 +507,19 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             unsigned char* base = buf + (uint32_t)(row * PW + col) * 64u + (kg & 1) * 8;
             const int sk = brick_swizzle(col);
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-                *reinterpret_cast<uint2*>(base + (((wc * CT + ct) ^ sk) << 4)) = make_uint2(
-                    pack_bf16x2(acc[r][ct][0] + bv[ct], acc[r][ct][1] + bv[ct]),
-                    pack_bf16x2(acc[r][ct][2] + bv[ct], acc[r][ct][3] + bv[ct]));
+            for (int ct = 0; ct < CT; ++ct) {
+                float v0 = acc[r][ct][0] + bv[ct], v1 = acc[r][ct][1] + bv[ct];
+                float v2 = acc[r][ct][2] + bv[ct], v3 = acc[r][ct][3] + bv[ct];
+                if constexpr (ACC) {
+                    const uint2 o = old[r][ct];
+                    v0 += __uint_as_float(o.x << 16);
+                    v1 += __uint_as_float(o.x & 0xffff0000u);
+                    v2 += __uint_as_float(o.y << 16);
+                    v3 += __uint_as_float(o.y & 0xffff0000u);
+                }
+                *reinterpret_cast<uint2*>(base + (((wc * CT + ct) ^ sk) << 4)) =
+                    make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+            }
             __builtin_amdgcn_sched_barrier(0);  // one row at a time (register pressure)
         }
     };
@@ -519,9 +556,6 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             v[e] = *reinterpret_cast<const uint4*>(buf + lo);
         }
     };
-    auto dst_rsrc = [&](const Tile& T) {
-        return buf_rsrc_u(a.dst + (int64_t)T.n * a.Ct * V, (uint32_t)a.Ct * Vb);
-    };
     auto unit_store = [&](__amdgpu_buffer_rsrc_t dst_r, const uint4 (&v)[8], const uint32_t (&go)[8]) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
@@ -555,90 +589,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         }
         drain_items(T, buf, 0, NRND);
     };
-    // Accumulating outputs (dst += conv), staged in float32 so that each output
-    // is rounded once: the 32 channels of consumer column group wc (CT = 2)
-    // are written as 16-byte units of four w, i = ((co % 8) * 4 + d) * 32 + h * 4
-    // + w / 4 in brick row i / PW, column i % PW, channel slot (co % 32) / 8,
-    // and drained (old value added, then rounded) by the producer that owns
-    // the slot.  The groups are written one after the other; the last one is
-    // drained in the next step, the others before the next group is written.
-    const bool staged_acc = ACC && KS == 3 && CT == 2 && (a.W & 7) == 0;
-    auto write_fp32 = [&](int k, unsigned char* buf) {
-        const Tile T = tile_of(k);
-        float bv[CT];
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-            bv[ct] = !DG && a.bias ? a.bias[T.co0 + (wc * CT + ct) * 16 + li] : 0.f;
-        int ib = ((li & 7) * kBD + wd * RD) * kBH * 4 + kg;
-        asm volatile("" : "+v"(ib));
-#pragma unroll
-        for (int r = 0; r < NR; ++r) {
-            const int i = ib + r * 4;
-            const int row = i / PW, ww = i - row * PW;
-            unsigned char* base = buf + (uint32_t)(row * PW) * 64u;
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-                *reinterpret_cast<float4*>(base + brick_slot_off<KS>(ww, ct * 2 + (li >> 3))) =
-                    make_float4(acc[r][ct][0] + bv[ct], acc[r][ct][1] + bv[ct],
-                                acc[r][ct][2] + bv[ct], acc[r][ct][3] + bv[ct]);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    };
-    auto drain_fp32 = [&](int k, int hf, const unsigned char* buf) {
-        const Tile T = tile_of(k);
-        // every owned unit's old value is requested at once (one round trip);
-        // units outside the tensor or the group use an offset past the buffer
-        // end, which reads zeros and is never stored
-        const __amdgpu_buffer_rsrc_t dst_r =
-            buf_rsrc_u(a.dst + (int64_t)T.n * a.Ct * V, (uint32_t)a.Ct * Vb);
-        constexpr int RB = 2;  // items per batch (16 old values in flight)
-#pragma unroll
-        for (int r0 = 0; r0 < NRND; r0 += RB) {
-            uint32_t off[RB][8];
-            uint2 old[RB][8];
-#pragma unroll
-            for (int ri = 0; ri < RB; ++ri) {
-                int pair, q;
-                const bool live = r0 + ri < NRND && item_of(r0 + ri, pair, q);
-                const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int ww = 8 * (q + Q0) + e + P;
-                    const int i = row * PW + ww;
-                    const int q4 = i & 3, h = (i >> 2) & (kBH - 1), d = (i >> 5) & (kBD - 1);
-                    const int co = T.co0 + hf * 32 + cg * 8 + (i >> 7);
-                    const int dd = T.d0 + d, hh = T.h0 + h, w = T.w0 + 4 * q4;
-                    const bool ok = live && ww >= 0 && ww < PW && i < 32 * kBD * kBH &&
-                                    dd < a.D && hh < a.H && w < a.W;
-                    off[ri][e] =
-                        ok ? (uint32_t)((co * V + dd * HW + hh * a.W + w) * 2) : 0x80000000u;
-                    old[ri][e] = buf_ld8(dst_r, off[ri][e], 0u);
-                }
-            }
-#pragma unroll
-            for (int ri = 0; ri < RB; ++ri) {
-                int pair, q;
-                if (!(r0 + ri < NRND && item_of(r0 + ri, pair, q))) continue;
-                const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    if (off[ri][e] == 0x80000000u) continue;
-                    const int ww = 8 * (q + Q0) + e + P;
-                    const float4 v = *reinterpret_cast<const float4*>(
-                        buf + (uint32_t)(row * PW) * 64u + brick_slot_off<KS>(ww, cg));
-                    const uint2 o = old[ri][e];
-                    buf_st8(dst_r,
-                            make_uint2(pack_bf16x2(v.x + __uint_as_float(o.x << 16),
-                                                   v.y + __uint_as_float(o.x & 0xffff0000u)),
-                                       pack_bf16x2(v.z + __uint_as_float(o.y << 16),
-                                                   v.w + __uint_as_float(o.y & 0xffff0000u))),
-                            off[ri][e], 0u);
-                }
-            }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    };
-    // direct epilogue (accumulating outputs, widths not a multiple of 8, 1^3):
+    // direct epilogue (widths not a multiple of 8, accumulating 1^3):
     // lane holds 4 consecutive w of one output channel per tile row
     auto direct_outputs = [&](int k) {
         const Tile T = tile_of(k);
@@ -692,24 +643,10 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             unsigned char* buf = lds + (k & 1) * BB;
             compute(k, buf);
             if (tile_end(k) && staged_epi) {
+                OldV old;
+                if constexpr (ACC) load_old(k, old);
                 lds_barrier();  // every consumer is done reading buf
-                write_outputs(k, buf);
-                lds_barrier();
-            } else if (tile_end(k) && staged_acc) {
-                lds_barrier();  // every consumer is done reading buf
-                // column group wc is written after the groups before it were
-                // written and drained (two barriers each), then waits out the
-                // later ones: one write_fp32 call site, so the accumulators
-                // stay where the step loop keeps them
-                for (int hf = 0; hf < wc; ++hf) {
-                    lds_barrier();
-                    lds_barrier();
-                }
-                write_fp32(k, buf);
-                for (int hf = wc; hf + 1 < WC; ++hf) {
-                    lds_barrier();
-                    lds_barrier();
-                }
+                write_outputs(k, buf, old);
                 lds_barrier();
             } else {
                 if (tile_end(k)) direct_outputs(k);
@@ -764,23 +701,12 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
                     drain_split(k - 1, lds + ((k - 1) & 1) * BB);
                 } else if (staged_epi) {
                     drain(k - 1, lds + ((k - 1) & 1) * BB);
-                } else if (staged_acc) {
-                    drain_fp32(k - 1, WC - 1, lds + ((k - 1) & 1) * BB);
                 }
             }
             if (more) stage_all(k + 1, lds + ((k + 1) & 1) * BB);
             if (tile_end(k) && staged_epi) {
                 lds_barrier();
                 lds_barrier();
-            } else if (tile_end(k) && staged_acc) {
-                lds_barrier();
-                for (int hf = 0; hf < WC; ++hf) {
-                    lds_barrier();
-                    if (hf + 1 < WC) {
-                        drain_fp32(k, hf, lds + (k & 1) * BB);
-                        lds_barrier();
-                    }
-                }
             } else {
                 lds_barrier();
             }
@@ -789,8 +715,6 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             if (split) late_store();
             if (staged_epi) {
                 drain(S - 1, lds + ((S - 1) & 1) * BB);
-            } else if (staged_acc) {
-                drain_fp32(S - 1, WC - 1, lds + ((S - 1) & 1) * BB);
             }
         }
     }

@@ -38,6 +38,9 @@ CONV_CASES = [
     (2, 64, 64, 5, 9, 24, 1, 1, 0, True, "bf16"),
     (1, 32, 64, 3, 3, 8, 1, 1, 0, False, "bf16"),
     (1, 96, 64, 9, 17, 48, 3, 1, 1, False, "bf16"),
+    # 64-channel output tiles (128 spatial tiles or more), ragged in d and h:
+    # the input gradient's accumulating drain in two column groups
+    (4, 64, 64, 14, 30, 32, 3, 1, 1, False, "bf16"),
     # weight gradient over row bands (W a multiple of 8, at most 56): the widest
     # band, one-row-per-group widths, a single plane, ragged last bands
     (1, 32, 64, 4, 5, 56, 3, 1, 1, False, "bf16"),
