@@ -183,10 +183,18 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     constexpr int PD = kBD + KS - 1, PH = kBH + KS - 1, PW = kBW + KS - 1;
     constexpr int NV = PD * PH * PW;
     constexpr int KT = KS * KS * KS;
-    constexpr uint32_t BB = NV * 64;            // bytes per brick buffer
+    // Brick row stride, padded to an odd multiple of 32 bytes.  Measured on
+    // gfx950 with 16-byte LDS accesses whose 16-lane groups step through rows
+    // of stride S: S = 32 or 96 (mod 128) is conflict-free, S = 16, 48, 80 or
+    // 112 (mod 128) costs two passes, S = 0 (mod 128) four or more.  A bare row
+    // of 18 or 16 voxels x 64 bytes is a multiple of 128 bytes, so without the
+    // padding the lanes of one staging store (the same column of different
+    // rows) would all hit the same banks.
+    constexpr uint32_t RS = PW * 64 + 32;
+    constexpr uint32_t BB = PD * PH * RS;       // bytes per brick buffer
     // 1^3: the output tile does not fit a brick buffer and gets its own region
-    // (co stride padded by 16 bytes so that 16 channels hit distinct banks)
-    constexpr uint32_t OCS = kBD * kBH * kBW * 2 + 16;
+    // (co stride padded to an odd multiple of 32 bytes, as the row stride)
+    constexpr uint32_t OCS = kBD * kBH * kBW * 2 + 32;
     constexpr uint32_t OB = KS == 1 ? NT * 16 * OCS : 0;
     __shared__ __align__(16) unsigned char lds[2 * BB + OB];
 
@@ -283,7 +291,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             int pair, q;
             if (!(i0 + ii < NRND && item_of(i0 + ii, pair, q))) continue;
             const int cg = pair / (PD * PH), row = pair - cg * (PD * PH);
-            unsigned char* rb = buf + (uint32_t)(row * PW) * 64u;
+            unsigned char* rb = buf + (uint32_t)row * RS;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int ww = 8 * (q + Q0) + e + P;  // brick column
@@ -330,7 +338,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
                     pk.z = u[4] | (u[5] << 16);
                     pk.w = u[6] | (u[7] << 16);
                 }
-                *reinterpret_cast<uint4*>(buf + (uint32_t)(rr * PW) * 64u +
+                *reinterpret_cast<uint4*>(buf + (uint32_t)rr * RS +
                                           brick_slot_off<KS>(ww, cg)) = pk;
             }
         }
@@ -346,13 +354,13 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     uint32_t sw[KS];
 #pragma unroll
     for (int kw = 0; kw < KS; ++kw)
-        sw[kw] = (uint32_t)(wd * RD * PH * PW) * 64u + brick_slot_off<KS>(li + kw, kg);
+        sw[kw] = (uint32_t)(wd * RD * PH) * RS + brick_slot_off<KS>(li + kw, kg);
     const uint32_t wlane = (uint32_t)(li * 64 + kg * 16);
     const __amdgpu_buffer_rsrc_t wt_r =
         buf_rsrc(a.wt, (uint32_t)(a.Cs / 32) * KT * (uint32_t)a.Ct * 64u);
     f32x4 acc[NR][CT];
     // brick offset of the wave's row r (depth slice r / 8, tile row r % 8)
-    auto row_off = [](int r) { return ((r / kBH) * PH + (r % kBH)) * PW * 64; };
+    auto row_off = [](int r) { return ((r / kBH) * PH + (r % kBH)) * (int)RS; };
 
     auto compute = [&](int k, const unsigned char* buf) {
         const Tile T = tile_of(k);
@@ -376,7 +384,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         auto a_ptr = [&](int g) {
             const int tap = g / NR, r = g % NR;
             const int kd = tap / (KS * KS), kh = (tap / KS) % KS, kw = tap % KS;
-            return buf + sw[kw] + ((kd * PH + kh) * PW) * 64 + row_off(r);
+            return buf + sw[kw] + (kd * PH + kh) * (int)RS + row_off(r);
         };
         auto load_b = [&](int tap, F16B (&bv)[CT]) {
 #pragma unroll
@@ -504,7 +512,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
                 row = (c0 ? 2 * j : 2 * (j - PD * PH / 2)) + half;
                 col = c0 ? 0 : PW - 1;
             }
-            unsigned char* base = buf + (uint32_t)(row * PW + col) * 64u + (kg & 1) * 8;
+            unsigned char* base = buf + (uint32_t)row * RS + (uint32_t)col * 64u + (kg & 1) * 8;
             const int sk = brick_swizzle(col);
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct) {
@@ -552,7 +560,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
                             !(col == PW - 1 && row >= 4) && dd < a.D && hh < a.H && w < a.W;
             go[e] = ok ? (uint32_t)(((T.co0 + cg * 16 + li_o) * V + dd * HW + hh * a.W + w) * 2)
                        : 0x80000000u;
-            const uint32_t lo = ok ? (uint32_t)(row * PW) * 64u + brick_slot_off<KS>(col, cg) : 0u;
+            const uint32_t lo = ok ? (uint32_t)row * RS + brick_slot_off<KS>(col, cg) : 0u;
             v[e] = *reinterpret_cast<const uint4*>(buf + lo);
         }
     };
@@ -1041,10 +1049,11 @@ struct WbArgs {
 };
 constexpr int kBandK = 192;                                  // voxels per step, at most
 constexpr int kBandSlotVox = 288;                            // bound on (hb + 2) * W
-constexpr int kBandCisMax = 4 * kBandSlotVox * 2 + 16;       // 2320
+constexpr int kBandCisMax = 4 * kBandSlotVox * 2 + 32;       // 2336
 constexpr int kBandDys = kBandK * 2 + 16;                    // bytes per output channel
 constexpr int kBandXBytes = 3 * 16 * kBandCisMax;            // three kw copies
-constexpr int kBandLds = kBandXBytes + 2 * 64 * kBandDys;    // 162560
+constexpr int kBandLds = kBandXBytes + 2 * 64 * kBandDys;    // 163328
+static_assert(kBandLds <= 160 * 1024, "band LDS");
 }  // namespace
 
 template <int NK, bool PART>
@@ -1614,7 +1623,14 @@ rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, 
         a.cigs = cigs;
         a.cogs = cogs;
         a.sls = (hb + 2) * bc.Wp * 2;
-        a.cis = ((4 * a.sls + 127) & ~127) + 16;  // 16 input channels on distinct banks
+        // input-channel stride an odd multiple of 32 bytes: the 16 channels of
+        // one operand read (one per lane of a 16-lane group) then take one LDS
+        // pass (a stride of 16 mod 128 measured two)
+        a.cis = ((4 * a.sls + 127) & ~127) + 32;
+        if (a.cis > kBandCisMax) {  // band_cfg keeps (hb + 2) * Wp <= kBandSlotVox
+            set_error("conv3d wgrad: band slot of %d bytes exceeds the LDS layout", a.cis);
+            return RAT3D_EINVAL;
+        }
         const int XG = (hb + 2) * bc.Wp / 8, YG = hb * bc.Wp / 8;
         auto magic = [](int d) { return (uint32_t)(((1u << 20) + d - 1) / d); };
         a.mWp = magic(bc.Wp);
