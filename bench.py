@@ -210,6 +210,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-other-configs", action="store_true",
                     help="skip the full-network and attention-module throughput lines")
+    ap.add_argument("--workload", default="partition1",
+                    choices=("partition1", "full_network", "attention_module"),
+                    help="partition1 (default): the contract line; the others time only that "
+                         "configuration (as the fields of the same name) and print its JSON, "
+                         "e.g. for a profiler run of that workload alone")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the timed steps, copy 256 MiB device-to-device once (the "
                          "reference dispatch that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -222,6 +227,12 @@ def main():
     import torch
     from paper_2104_05035_amd import rat3d as R, synth
     R.lib()
+    if args.workload != "partition1":
+        kind = "resattnet" if args.workload == "full_network" else "attn"
+        print(json.dumps({"workload_name": args.workload,
+                          **other_config(torch, R, synth, kind, args.steps, args.warmup)}),
+              flush=True)
+        return
     n, mb, vol, c = 16, 4, (96, 112, 96), 64
     net, P, G, ws, x, dy = build_inputs(torch, R, synth, n, mb, vol, c)
     stream = torch.cuda.current_stream()
