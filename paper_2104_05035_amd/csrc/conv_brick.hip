@@ -67,33 +67,14 @@ struct FdArgs {
 }  // namespace
 
 // ---------------------------------------------------------------- weight prep
-// fwd:   wt[((c/32)*KT + t)*Co + co]*32 + c%32] = w[co][c][t]
-__global__ void prep_fwd_weights(const bf16* __restrict__ w, int Co, int Ci, int KT,
-                                 bf16* __restrict__ wt) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int64_t total = (int64_t)Co * Ci * KT;
-    if (i >= total) return;
-    const int t = (int)(i % KT);
-    const int c = (int)((i / KT) % Ci);
-    const int co = (int)(i / ((int64_t)KT * Ci));
-    wt[(((int64_t)(c >> 5) * KT + t) * Co + co) * 32 + (c & 31)] = w[i];
-}
-
-// dgrad: wt[((co/32)*KT + t)*Ci + ci]*32 + co%32] = w[co][ci][KT - 1 - t]
-__global__ void prep_dgrad_weights(const bf16* __restrict__ w, int Co, int Ci, int KT,
-                                   bf16* __restrict__ wt) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int64_t total = (int64_t)Co * Ci * KT;
-    if (i >= total) return;
-    const int t = (int)(i % KT);
-    const int ci = (int)((i / KT) % Ci);
-    const int co = (int)(i / ((int64_t)KT * Ci));
-    wt[(((int64_t)(co >> 5) * KT + (KT - 1 - t)) * Ci + ci) * 32 + (co & 31)] = w[i];
-}
-
-// Several convolutions' weight layouts in one launch: job j covers global
-// indices [begin_j, begin_j + Co*Ci*KT) and writes the forward or
-// input-gradient layout above.
+// Prepared layouts (source channels innermost, in chunks of 32; Cs is a
+// multiple of 32 on every path that reads them):
+//   fwd:   wt[((c/32)*KT + t)*Co + co]*32 + c%32] = w[co][c][t]
+//   dgrad: wt[((co/32)*KT + t)*Ci + ci]*32 + co%32] = w[co][ci][KT - 1 - t]
+// Several convolutions' layouts in one launch: job j covers 16-byte
+// destination units [begin_j, begin_j + Co*Ci*KT/8).  One thread per unit
+// (eight consecutive source channels): eight gathered 2-byte reads (cached)
+// and one 16-byte store, so the writes are whole, contiguous lines.
 struct PrepBatch {
     const bf16* w[kPrepJobs];
     bf16* wt[kPrepJobs];
@@ -103,27 +84,47 @@ struct PrepBatch {
 };
 
 __global__ void prep_weights_batch(PrepBatch b) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= b.begin[b.n]) return;
-    int lo = 0, hi = b.n - 1;  // the job whose range holds i
+    const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (u >= b.begin[b.n]) return;
+    int lo = 0, hi = b.n - 1;  // the job whose range holds u
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (b.begin[mid] <= i) lo = mid;
+        if (b.begin[mid] <= u) lo = mid;
         else hi = mid - 1;
     }
-    const int64_t e = i - b.begin[lo];
+    const int64_t e = u - b.begin[lo];
     const int KT = b.kt[lo], Ci = b.ci[lo], Co = b.co[lo];
-    const int t = (int)(e % KT);
-    const int c = (int)((e / KT) % Ci);
-    const int co = (int)(e / ((int64_t)KT * Ci));
-    const bf16 v = b.w[lo][e];
-    if (b.dg[lo])
-        b.wt[lo][(((int64_t)(co >> 5) * KT + (KT - 1 - t)) * Ci + c) * 32 + (co & 31)] = v;
-    else
-        b.wt[lo][(((int64_t)(c >> 5) * KT + t) * Co + co) * 32 + (c & 31)] = v;
+    const bool dg = b.dg[lo] != 0;
+    const int Ct = dg ? Ci : Co;  // target channels (the row index of the layout)
+    // e = ((cb * KT + t) * Ct + tc) * 4 + s8: unit s8 of the 32 source channels of chunk cb
+    const int s8 = (int)(e & 3);
+    const int64_t r = e >> 2;
+    const int tc = (int)(r % Ct);
+    const int64_t r2 = r / Ct;
+    const int t = (int)(r2 % KT), cb = (int)(r2 / KT);
+    const int s0 = cb * 32 + s8 * 8;
+    const bf16* w = b.w[lo];
+    // fwd: w[tc][s][t]; dgrad: w[s][tc][KT - 1 - t]
+    const int64_t base = dg ? ((int64_t)s0 * Ci + tc) * KT + (KT - 1 - t)
+                            : ((int64_t)tc * Ci + s0) * KT + t;
+    const int64_t step = dg ? (int64_t)Ci * KT : KT;
+    uint32_t v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = w[base + j * step];
+    *reinterpret_cast<uint4*>(b.wt[lo] + e * 8) =
+        make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16),
+                   v[6] | (v[7] << 16));
 }
 
 rat3d_status brick_prep_weights_batch(const PrepJob* jobs, int n, hipStream_t st) {
+    for (int j = 0; j < n; ++j) {
+        const int cs = jobs[j].dgrad ? jobs[j].g.Co : jobs[j].g.Ci;
+        if (cs % 32 != 0 || ((uintptr_t)jobs[j].wt & 15u)) {
+            set_error("weight layout: source channels (%d) must be a multiple of 32 and the "
+                      "prepared buffer 16-byte aligned", cs);
+            return RAT3D_EINVAL;
+        }
+    }
     for (int j0 = 0; j0 < n; j0 += kPrepJobs) {
         PrepBatch b{};
         b.n = n - j0 < kPrepJobs ? n - j0 : kPrepJobs;
@@ -136,7 +137,7 @@ rat3d_status brick_prep_weights_batch(const PrepJob* jobs, int n, hipStream_t st
             b.ci[j] = J.g.Ci;
             b.kt[j] = J.g.k * J.g.k * J.g.k;
             b.dg[j] = J.dgrad ? 1 : 0;
-            b.begin[j + 1] = b.begin[j] + (int64_t)J.g.Co * J.g.Ci * b.kt[j];
+            b.begin[j + 1] = b.begin[j] + (int64_t)J.g.Co * J.g.Ci * b.kt[j] / 8;
         }
         prep_weights_batch<<<(unsigned)ceil_div(b.begin[b.n], 256), 256, 0, st>>>(b);
         RAT3D_LAUNCH_CHECK();
@@ -1514,16 +1515,8 @@ size_t brick_wgrad_ws(const ConvGeom& g) {
 
 rat3d_status brick_prep_weights(const ConvGeom& g, bool dgrad, const void* w, void* wt,
                                 hipStream_t st) {
-    const int KT = g.k * g.k * g.k;
-    const int64_t wn = (int64_t)g.Co * g.Ci * KT;
-    if (dgrad)
-        prep_dgrad_weights<<<(unsigned)ceil_div(wn, 256), 256, 0, st>>>((const bf16*)w, g.Co,
-                                                                        g.Ci, KT, (bf16*)wt);
-    else
-        prep_fwd_weights<<<(unsigned)ceil_div(wn, 256), 256, 0, st>>>((const bf16*)w, g.Co, g.Ci,
-                                                                      KT, (bf16*)wt);
-    RAT3D_LAUNCH_CHECK();
-    return RAT3D_OK;
+    const PrepJob job{g, dgrad, w, wt};
+    return brick_prep_weights_batch(&job, 1, st);
 }
 
 rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const void* w,
