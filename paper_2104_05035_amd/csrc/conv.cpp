@@ -17,9 +17,9 @@ static size_t wgrad_ws(const ConvGeom& g, rat3d_dtype dt) {
 size_t conv_ws_bytes(const ConvGeom& g, rat3d_dtype dt, int pass) {
     if (pass == 0) {
         if (stem_ok(g, dt)) return stem_fwd_ws();
-        return brick_fd_ok(g, dt, false) ? brick_fd_ws(g) : 0;
+        return brick_fd_ok(g, dt, false) ? brick_fd_ws(g, false) : 0;
     }
-    if (pass == 1) return brick_fd_ok(g, dt, true) ? brick_fd_ws(g) : 0;
+    if (pass == 1) return brick_fd_ok(g, dt, true) ? brick_fd_ws(g, true) : 0;
     // weight-gradient partials, then the bias-gradient slice sums
     const size_t wb = wgrad_ws(g, dt);
     return ((wb + 255) & ~(size_t)255) + bias_grad_ws(g);

@@ -60,8 +60,13 @@ struct FdArgs {
     int N, Cs, Ct, D, H, W;
     int td, th, tw;    // tiles per axis
     int cogs;          // output-channel groups of NT * 16
-    int ntiles;        // N * td * th * tw * cogs
+    int ntiles;        // work items: N * td * th * tw * cogs * nsplit
     int accumulate;
+    // split over the source channels (maps too small to occupy every CU):
+    // item = (tile, split) sums chunks [split * cps, (split + 1) * cps) and
+    // stores fp32 partials, part[split][n][co][v], summed by brick_split_reduce
+    int nsplit, cps;
+    float* part;
 };
 
 }  // namespace
@@ -203,7 +208,6 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     // then stay in scalar registers instead of forcing per-lane loops
     const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const bool consumer = wave < 4;
-    const int nchunk = a.Cs >> 5;
     const int HW = a.H * a.W, V = HW * a.D;
     const uint32_t Vb = (uint32_t)V * 2u;
 
@@ -221,14 +225,16 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
             t_end = a.ntiles;
         }
     }
-    const int S = (t_first < t_end ? (t_end - t_first + t_stride - 1) / t_stride : 0) * nchunk;
+    const int S = (t_first < t_end ? (t_end - t_first + t_stride - 1) / t_stride : 0) * a.cps;
 
     struct Tile {
-        int n, d0, h0, w0, co0;
+        int n, d0, h0, w0, co0, split;
     };
     auto tile_of = [&](int k) {
-        int r = t_first + (k / nchunk) * t_stride;
+        int r = t_first + (k / a.cps) * t_stride;
         Tile T;
+        T.split = r % a.nsplit;
+        r /= a.nsplit;
         T.co0 = (r % a.cogs) * NT * 16;
         r /= a.cogs;
         T.w0 = (r % a.tw) * kBW;
@@ -264,10 +270,12 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     // buffer.  The producer stages in blocks of two items after it has
     // drained the previous tile's outputs (issuing all loads before the drain
     // measured slower).
+    // first source channel of step k's 32-channel chunk
+    auto chunk_c0 = [&](const Tile& T, int k) { return (T.split * a.cps + k % a.cps) * 32; };
     auto stage_load = [&](int k, auto& v, int i0) {
         constexpr int NB = sizeof(v) / sizeof(v[0]);
         const Tile T = tile_of(k);
-        const int c0 = (k % nchunk) * 32;
+        const int c0 = chunk_c0(T, k);
         const __amdgpu_buffer_rsrc_t src_r =
             buf_rsrc_u(a.src + (int64_t)T.n * a.Cs * V, (uint32_t)a.Cs * Vb);
 #pragma unroll
@@ -318,7 +326,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     // voxel), voxel fastest, loaded and written in one pass.
     auto stage_generic = [&](int k, unsigned char* buf) {
         const Tile T = tile_of(k);
-        const int c0 = (k % nchunk) * 32;
+        const int c0 = chunk_c0(T, k);
         {
             // item = (channel group, brick voxel), voxel fastest
             for (int it = ptid; it < NV * 4; it += 256) {
@@ -365,8 +373,8 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
 
     auto compute = [&](int k, const unsigned char* buf) {
         const Tile T = tile_of(k);
-        const int c0 = (k % nchunk) * 32;
-        if (c0 == 0) {
+        const int c0 = chunk_c0(T, k);
+        if (k % a.cps == 0) {
 #pragma unroll
             for (int i = 0; i < NR; ++i)
 #pragma unroll
@@ -450,7 +458,8 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     // together, after the tile's last MFMA has freed the operand registers)
     // and add them before the single rounding; the producers' stores stay
     // plain bf16 stores.
-    const bool staged_epi = (!ACC || KS == 3) && (a.W & 7) == 0;
+    const bool split_out = a.nsplit > 1;
+    const bool staged_epi = !split_out && (!ACC || KS == 3) && (a.W & 7) == 0;
     using OldV = uint2[ACC ? NR : 1][ACC ? CT : 1];
     auto load_old = [&](int k, OldV& o) {
         const Tile T = tile_of(k);
@@ -598,6 +607,33 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
         }
         drain_items(T, buf, 0, NRND);
     };
+    // split items: fp32 partial sums straight from the accumulators (bias and
+    // old values are added by the reduction)
+    auto split_outputs = [&](int k) {
+        const Tile T = tile_of(k);
+        float* pb = a.part + ((int64_t)T.split * a.N + T.n) * a.Ct * (int64_t)V;
+        const int w = T.w0 + 4 * kg;
+        const bool vec = (a.W & 3) == 0 && w + 4 <= a.W;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            const int d = T.d0 + wd * RD + r / kBH, h = T.h0 + r % kBH;
+            if (d >= a.D || h >= a.H) continue;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                const int co = T.co0 + (wc * CT + ct) * 16 + li;
+                float* q = pb + (int64_t)co * V + (int64_t)d * HW + (int64_t)h * a.W + w;
+                if (vec) {
+                    *reinterpret_cast<float4*>(q) =
+                        make_float4(acc[r][ct][0], acc[r][ct][1], acc[r][ct][2], acc[r][ct][3]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (w + e < a.W) q[e] = acc[r][ct][e];
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
     // direct epilogue (widths not a multiple of 8, accumulating 1^3):
     // lane holds 4 consecutive w of one output channel per tile row
     auto direct_outputs = [&](int k) {
@@ -645,7 +681,7 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
     // step with the staged epilogue); the roles are wave-uniform, and the two
     // loops keep the consumers' accumulators out of the producers' live range.
     // The barriers order LDS only: global stores are never waited for.
-    auto tile_end = [&](int k) { return (k % nchunk) == nchunk - 1; };
+    auto tile_end = [&](int k) { return (k % a.cps) == a.cps - 1; };
     if (consumer) {
         lds_barrier();
         for (int k = 0; k < S; ++k) {
@@ -658,7 +694,10 @@ __global__ __launch_bounds__(512, 1) void conv_brick_fd(FdArgs a) {
                 write_outputs(k, buf, old);
                 lds_barrier();
             } else {
-                if (tile_end(k)) direct_outputs(k);
+                if (tile_end(k)) {
+                    if (split_out) split_outputs(k);
+                    else direct_outputs(k);
+                }
                 lds_barrier();
             }
         }
@@ -1443,6 +1482,21 @@ __global__ __launch_bounds__(256) void wgrad_brick_reduce(const float* __restric
     *o = accumulate ? *o + s : s;
 }
 
+// dst[i] = round((sum over splits, in split order, of part[split][i]) + bias[co]
+// (+ dst[i] when accumulating)): one rounding, as the unsplit epilogue.
+__global__ __launch_bounds__(256) void brick_split_reduce(const float* __restrict__ part,
+                                                          int nsplit, int64_t count, int Ct,
+                                                          int64_t V, const float* __restrict__ bias,
+                                                          bf16* __restrict__ dst, int accumulate) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= count) return;
+    float s = part[i];
+    for (int z = 1; z < nsplit; ++z) s += part[(int64_t)z * count + i];
+    if (bias) s += bias[(int)((i / V) % Ct)];
+    if (accumulate) s += bf2f(dst[i]);
+    dst[i] = f2bf(s);
+}
+
 // ---------------------------------------------------------------- dispatch
 bool brick_fd_ok(const ConvGeom& g, rat3d_dtype dt, bool dgrad) {
     if (dt != RAT3D_BF16 || g.s != 1) return false;
@@ -1490,7 +1544,50 @@ bool brick_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) {
            g.Co % 64 == 0 && (g.W % 8 == 0 || band_cfg(g).hb > 0);
 }
 
-size_t brick_fd_ws(const ConvGeom& g) { return (size_t)g.Co * g.Ci * g.k * g.k * g.k * 2; }
+// Tile plan of a brick pass: 64-channel tiles unless that leaves most CUs
+// idle (small volumes: then 32-channel tiles double the workgroups), and a
+// split over the 32-channel source chunks when the tiles are fewer than the
+// CUs and splitting at least halves the busiest CU's step count (a smaller
+// gain does not pay for writing and summing the fp32 partials).
+struct BrickPlan {
+    int nt, cogs, ntiles, nsplit;  // ntiles: spatial tiles x channel groups
+};
+static BrickPlan brick_plan(const ConvGeom& g, bool dgrad) {
+    const int cs = dgrad ? g.Co : g.Ci, ct = dgrad ? g.Ci : g.Co;
+    const int64_t sp_tiles =
+        (int64_t)g.N * ceil_div(g.D, kBD) * ceil_div(g.H, kBH) * ceil_div(g.W, kBW);
+    const int cus = device_cus();
+    BrickPlan p;
+    p.nt = (ct % 64 == 0 && sp_tiles * (ct / 64) >= cus / 2) ? 4 : 2;
+    p.cogs = ct / (p.nt * 16);
+    p.ntiles = (int)(sp_tiles * p.cogs);
+    p.nsplit = 1;
+    if (g.k == 3 && p.ntiles < cus) {
+        const int nchunk = cs / 32;
+        auto steps = [&](int ns) { return ceil_div((int64_t)p.ntiles * ns, cus) * (nchunk / ns); };
+        int64_t best = steps(1);
+        for (int ns = 2; ns <= nchunk && nchunk % ns == 0; ns *= 2) {
+            const int64_t st = steps(ns);
+            if (st * 2 <= steps(1) && st < best) {
+                best = st;
+                p.nsplit = ns;
+            }
+        }
+    }
+    return p;
+}
+
+static size_t brick_prepared_bytes(const ConvGeom& g) {
+    return ((size_t)g.Co * g.Ci * g.k * g.k * g.k * 2 + 255) & ~(size_t)255;
+}
+
+size_t brick_fd_ws(const ConvGeom& g, bool dgrad) {
+    const BrickPlan p = brick_plan(g, dgrad);
+    const size_t part = p.nsplit > 1 ? (size_t)p.nsplit * g.N * (dgrad ? g.Ci : g.Co) *
+                                           ((size_t)g.D * g.H * g.W) * sizeof(float)
+                                     : 0;
+    return brick_prepared_bytes(g) + part;
+}
 
 static int64_t wgrad_steps(const ConvGeom& g) {
     const int hb = band_cfg(g).hb;
@@ -1545,13 +1642,14 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
     a.th = (int)ceil_div(g.H, kBH);
     a.tw = (int)ceil_div(g.W, kBW);
     a.accumulate = accumulate;
-    // 64-channel tiles, unless that leaves most CUs idle (small volumes): then
-    // 32-channel tiles double the workgroups
-    const int64_t sp_tiles = (int64_t)g.N * a.td * a.th * a.tw;
-    const int nt = (a.Ct % 64 == 0 && sp_tiles * (a.Ct / 64) >= device_cus() / 2) ? 4 : 2;
-    a.cogs = a.Ct / (nt * 16);
-    a.ntiles = (int)((int64_t)g.N * a.td * a.th * a.tw * a.cogs);
-    // one persistent workgroup per CU (fewer when there are fewer tiles)
+    const BrickPlan plan = brick_plan(g, dgrad);
+    const int nt = plan.nt;
+    a.cogs = plan.cogs;
+    a.nsplit = plan.nsplit;
+    a.cps = (a.Cs / 32) / plan.nsplit;
+    a.ntiles = plan.ntiles * plan.nsplit;
+    a.part = (float*)((char*)ws + brick_prepared_bytes(g));
+    // one persistent workgroup per CU (fewer when there are fewer items)
     const int grid = a.ntiles < device_cus() ? a.ntiles : device_cus();
     // one tag (and one kernel symbol) per variant, so that live timings and
     // profiler counters describe the same launches
@@ -1560,9 +1658,10 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
                                         : "conv_brick3_fwd")
                                : (dgrad ? (acc ? "conv_brick1_dgrad_acc" : "conv_brick1_dgrad")
                                         : "conv_brick1_fwd");
-    char tagbuf[40];
-    if (nt == 2) {
-        snprintf(tagbuf, sizeof tagbuf, "%s_c32", tag);
+    char tagbuf[48];
+    if (nt == 2 || plan.nsplit > 1) {
+        snprintf(tagbuf, sizeof tagbuf, "%s%s%s", tag, nt == 2 ? "_c32" : "",
+                 plan.nsplit > 1 ? "_split" : "");
         tag = tagbuf;
     }
     ProfScope ps(tag, st, conv_flops(g), conv_bytes(g, 2));
@@ -1585,6 +1684,12 @@ rat3d_status conv_fd_brick(const ConvGeom& g, bool dgrad, const void* src, const
     }
 #undef RAT3D_FD
     RAT3D_LAUNCH_CHECK();
+    if (plan.nsplit > 1) {
+        const int64_t V = (int64_t)g.D * g.H * g.W, count = (int64_t)g.N * a.Ct * V;
+        brick_split_reduce<<<(unsigned)ceil_div(count, 256), 256, 0, st>>>(
+            a.part, plan.nsplit, count, a.Ct, V, dgrad ? nullptr : bias, (bf16*)dst, accumulate);
+        RAT3D_LAUNCH_CHECK();
+    }
     return RAT3D_OK;
 }
 

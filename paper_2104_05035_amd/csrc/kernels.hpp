@@ -77,7 +77,7 @@ rat3d_status wgrad_reduce_launch(const float* part, int splits, int64_t count, f
 // ---- LDS-brick kernels for bf16, stride 1, k in {1, 3} (conv_brick.hip) ---
 bool brick_fd_ok(const ConvGeom& g, rat3d_dtype dt, bool dgrad);
 bool brick_wgrad_ok(const ConvGeom& g, rat3d_dtype dt);
-size_t brick_fd_ws(const ConvGeom& g);
+size_t brick_fd_ws(const ConvGeom& g, bool dgrad);  // prepared weights (+ split partials)
 size_t brick_wgrad_ws(const ConvGeom& g);
 // w_prepared: w already holds the layout brick_prep_weights writes for this
 // pass (the workspace is then unused); otherwise it is prepared into ws.

@@ -147,6 +147,36 @@ def test_conv3d(case):
         U.check(U.f64(db), dbref, dt, "db", kind="sum", norm=False, terms=tdb)
 
 
+# Maps with fewer brick tiles than CUs split the 32-channel source chunks
+# over workgroups (fp32 partials summed in order, then bias, old value and one
+# rounding): a bias case, eight splits over 256 source channels, and an odd
+# width (element-wise partial stores).
+SPLIT_CASES = [
+    (2, 64, 64, 12, 14, 12, 3, 1, 1, True, "bf16"),
+    (1, 256, 64, 6, 7, 6, 3, 1, 1, False, "bf16"),
+    (1, 64, 64, 5, 6, 7, 3, 1, 1, False, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", SPLIT_CASES, ids=_id)
+def test_conv3d_source_split(case):
+    """The split forward and input-gradient passes run (their measurement tags
+    appear) and match the oracle like every other conv pass."""
+    from paper_2104_05035_amd import rat3d as R
+    R.rat3d_profile_reset()
+    R.rat3d_profile_filter(None)
+    R.rat3d_profile_enable(1)
+    try:
+        test_conv3d(case)
+        U.sync()
+    finally:
+        R.rat3d_profile_enable(0)
+    tags = {R.rat3d_profile_read(i)[0] for i in range(R.rat3d_profile_count())}
+    for t in ("conv_brick3_fwd_c32_split", "conv_brick3_dgrad_c32_split",
+              "conv_brick3_dgrad_acc_c32_split"):
+        assert t in tags, "%s not launched (tags: %s)" % (t, sorted(tags))
+
+
 BN_CASES = [
     (2, 3, 5, 6, 7, "f32"), (4, 16, 12, 14, 12, "bf16"), (2, 8, 6, 7, 6, "bf16"),
     (1, 2, 1, 1, 3, "f32"), (3, 4, 3, 4, 3, "bf16"),
