@@ -1096,8 +1096,11 @@ constexpr int kBandLds = kBandXBytes + 2 * 64 * kBandDys;    // 163328
 static_assert(kBandLds <= 160 * 1024, "band LDS");
 }  // namespace
 
-template <int NK, bool PART>
+// MODE: 0 W % 8 = 0 (16-byte loads), 1 W % 8 = 4 (the last group of a row
+// holds four voxels: an 8-byte load), 2 any other width (element loads).
+template <int NK, int MODE>
 __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
+    constexpr bool PART = MODE == 1, ELEM = MODE == 2;
     constexpr int KT = 27, NTAP = kWgNtap;
     static_assert(NK * 32 <= kBandK, "K steps per band");
     constexpr int DYB = 64 * kBandDys;
@@ -1167,7 +1170,14 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
             const bool ok = live && (unsigned)z < (unsigned)a.D && (unsigned)h < (unsigned)a.H;
             const uint32_t o = ok ? (uint32_t)((ci0 + ci) * (uint32_t)V + z * HW + h * a.W + col) * 2u
                                   : 0x80000000u;
-            if constexpr (PART) {
+            if constexpr (ELEM) {
+                uint32_t e[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    e[j] = buf_ld2(xr, ok && col + j < a.W ? o + 2u * j : 0x80000000u, 0);
+                m[1] = e[0] | (e[1] << 16); m[2] = e[2] | (e[3] << 16);
+                m[3] = e[4] | (e[5] << 16); m[4] = e[6] | (e[7] << 16);
+            } else if constexpr (PART) {
                 const bool full = col + 8 <= a.W;
                 const uint4 v = buf_ld16(xr, full ? o : 0x80000000u, 0);
                 const uint2 w = buf_ld8(xr, full ? 0x80000000u : o, 0);
@@ -1201,6 +1211,14 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
                 live && h < a.H
                     ? (uint32_t)((co0 + co) * (uint32_t)V + t.d * HW + h * a.W + col) * 2u
                     : 0x80000000u;
+            if constexpr (ELEM) {
+                uint32_t e[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    e[j] = buf_ld2(yr, o != 0x80000000u && col + j < a.W ? o + 2u * j : 0x80000000u, 0);
+                return make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
+                                  e[6] | (e[7] << 16));
+            }
             if constexpr (PART) {
                 const bool full = col + 8 <= a.W;
                 uint4 v = buf_ld16(yr, full ? o : 0x80000000u, 0);
@@ -1235,8 +1253,10 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
                 const int u = 8 * gi, rr = qdiv(u, a.mWp), col = u - rr * a.Wp;
                 xo[q] = (uint32_t)(ci0 + ci) * (uint32_t)V + (uint32_t)(rr * a.W + col);
                 xl[q] = (uint32_t)(ci * a.cis + gi * 16);
+                const int nv = a.W - col < 8 ? (a.W - col > 0 ? a.W - col : 0) : 8;
                 xf[q] = (uint32_t)rr | (live ? 1u << 16 : 0u) | (col > 0 ? 1u << 17 : 0u) |
-                        (col + 8 < a.W ? 1u << 18 : 0u) | (col + 8 <= a.W ? 1u << 19 : 0u);
+                        (col + 8 < a.W ? 1u << 18 : 0u) | (col + 8 <= a.W ? 1u << 19 : 0u) |
+                        ((uint32_t)nv << 20);
             }
 #pragma unroll
             for (int q = 0; q < NDY; ++q) {
@@ -1246,7 +1266,9 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
                 const int u = 8 * gi, rr = qdiv(u, a.mWp), col = u - rr * a.Wp;
                 yo[q] = (uint32_t)(co0 + co) * (uint32_t)V + (uint32_t)(rr * a.W + col);
                 yl[q] = (uint32_t)(co * kBandDys + gi * 16);
-                yf[q] = (uint32_t)rr | (live ? 1u << 16 : 0u) | (col + 8 <= a.W ? 1u << 19 : 0u);
+                const int nv = a.W - col < 8 ? (a.W - col > 0 ? a.W - col : 0) : 8;
+                yf[q] = (uint32_t)rr | (live ? 1u << 16 : 0u) | (col + 8 <= a.W ? 1u << 19 : 0u) |
+                        ((uint32_t)nv << 20);
             }
         }
         // one new plane (d + 1 of step t) and the dy of step t, into registers
@@ -1270,7 +1292,15 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
                 const bool ok = (f & (1u << 16)) && zok && (unsigned)(rr - 1 + t.h0) < (unsigned)a.H;
                 const uint32_t o = ok ? (xo[q] + xb) * 2u : 0x80000000u;
                 uint32_t* m = R.m[q];
-                if constexpr (PART) {
+                if constexpr (ELEM) {
+                    const int nv = (int)((f >> 20) & 15u);
+                    uint32_t e[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        e[j] = buf_ld2(xr, ok && j < nv ? o + 2u * j : 0x80000000u, 0);
+                    m[1] = e[0] | (e[1] << 16); m[2] = e[2] | (e[3] << 16);
+                    m[3] = e[4] | (e[5] << 16); m[4] = e[6] | (e[7] << 16);
+                } else if constexpr (PART) {
                     const bool full = f & (1u << 19);
                     const uint4 v = buf_ld16(xr, full ? o : 0x80000000u, 0);
                     const uint2 w = buf_ld8(xr, full ? 0x80000000u : o, 0);
@@ -1288,7 +1318,15 @@ __global__ __launch_bounds__(512, 1) void conv_band_wgrad(WbArgs a) {
                 const int rr = (int)(f & 0xffffu);
                 const bool ok = (f & (1u << 16)) && rr < hy;
                 const uint32_t o = ok ? (yo[q] + yb) * 2u : 0x80000000u;
-                if constexpr (PART) {
+                if constexpr (ELEM) {
+                    const int nv = (int)((f >> 20) & 15u);
+                    uint32_t e[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        e[j] = buf_ld2(yr, ok && j < nv ? o + 2u * j : 0x80000000u, 0);
+                    R.dy[q] = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16),
+                                         e[4] | (e[5] << 16), e[6] | (e[7] << 16));
+                } else if constexpr (PART) {
                     const bool full = f & (1u << 19);
                     uint4 v = buf_ld16(yr, full ? o : 0x80000000u, 0);
                     const uint2 w = buf_ld8(yr, full ? 0x80000000u : o, 0);
@@ -1520,15 +1558,24 @@ static BandCfg band_cfg(const ConvGeom& g) {
     const int Wp = (g.W + 7) & ~7;
     // staging addresses one sample's tensor with 32-bit byte offsets
     const int64_t v2 = (int64_t)g.D * g.H * g.W * 2;
-    if (g.W % 4 != 0 || Wp > 56 || (int64_t)g.Ci * v2 >= ((int64_t)1 << 31) ||
+    if (Wp > 56 || (int64_t)g.Ci * v2 >= ((int64_t)1 << 31) ||
         (int64_t)g.Co * v2 >= ((int64_t)1 << 31))
         return c;
+    // element-loaded widths (W % 4 != 0) only on maps of 128 voxels or more:
+    // below that the kernel's fixed costs (prologue, one partial block per
+    // workgroup) exceed the gather kernel's time (3x4x3: 47 vs 39 us at 256
+    // channels, measured; 6x7x6: 69 vs 128 us)
+    if (g.W % 4 != 0 && (int64_t)g.D * g.H * g.W < 128) return c;
     int64_t best = -1;
-    for (int nk : {6, 4}) {
+    // least work per plane: each band costs its nk K steps plus a fixed
+    // overhead of about two (barrier, staging of hb + 2 rows); two or one K
+    // step of 32 voxels serve the smallest planes (a 6 x 7 plane at pitch 8
+    // fills 56 of 64 slots)
+    for (int nk : {6, 4, 2, 1}) {
         const int a = nk * 32 / Wp, b = kBandSlotVox / Wp - 2;
         const int hb = a < b ? a : b;
         if (hb < 1) continue;
-        const int64_t cost = ceil_div(g.H, hb) * nk;
+        const int64_t cost = ceil_div(g.H, hb) * (nk + 2);
         if (best < 0 || cost < best) {
             best = cost;
             c.hb = hb;
@@ -1735,18 +1782,26 @@ rat3d_status conv_wgrad_brick(const ConvGeom& g, const void* x, const void* dy, 
         a.mXG = magic(XG);
         a.m3XG = magic(3 * XG);
         a.mYG = magic(YG);
-        const bool part = (g.W & 7) != 0;
-        const char* tag = bc.nk == 6 ? (part ? "conv_band3_wgrad_w4" : "conv_band3_wgrad")
-                                     : (part ? "conv_band3_wgrad_k128_w4" : "conv_band3_wgrad_k128");
+        // staging mode: whole 8-voxel groups, a half-filled last group, or
+        // element loads (widths that are not a multiple of 4)
+        const int mode = (g.W & 7) == 0 ? 0 : ((g.W & 3) == 0 ? 1 : 2);
+        char tag[48];
+        snprintf(tag, sizeof tag, "conv_band3_wgrad%s%s",
+                 bc.nk == 6 ? "" : bc.nk == 4 ? "_k128" : bc.nk == 2 ? "_k64" : "_k32",
+                 mode == 1 ? "_w4" : mode == 2 ? "_elem" : "");
         ProfScope ps(tag, st, conv_flops(g), conv_bytes(g, 2));
         const unsigned grid = (unsigned)((int64_t)Rreal * cigs * cogs);
-        if (bc.nk == 6) {
-            if (part) conv_band_wgrad<6, true><<<grid, 512, 0, st>>>(a);
-            else conv_band_wgrad<6, false><<<grid, 512, 0, st>>>(a);
-        } else {
-            if (part) conv_band_wgrad<4, true><<<grid, 512, 0, st>>>(a);
-            else conv_band_wgrad<4, false><<<grid, 512, 0, st>>>(a);
-        }
+#define RAT3D_BAND(NK)                                                           \
+    do {                                                                         \
+        if (mode == 0) conv_band_wgrad<NK, 0><<<grid, 512, 0, st>>>(a);          \
+        else if (mode == 1) conv_band_wgrad<NK, 1><<<grid, 512, 0, st>>>(a);     \
+        else conv_band_wgrad<NK, 2><<<grid, 512, 0, st>>>(a);                    \
+    } while (0)
+        if (bc.nk == 6) RAT3D_BAND(6);
+        else if (bc.nk == 4) RAT3D_BAND(4);
+        else if (bc.nk == 2) RAT3D_BAND(2);
+        else RAT3D_BAND(1);
+#undef RAT3D_BAND
         RAT3D_LAUNCH_CHECK();
     } else {
         WgArgs a;

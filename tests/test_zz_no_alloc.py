@@ -69,7 +69,8 @@ def test_noalloc_rejects_oversize():
     """A shape whose partials exceed the built-in scratch is refused before
     anything is enqueued."""
     from paper_2104_05035_amd import rat3d as R
-    desc = R.conv_desc(64, 256, 256, 6, 7, 6, 3, 1, 1, False, R.BF16)
+    # a stride-2 conv (split-K gather partials: 3 x 512 x 256 x 27 floats)
+    desc = R.conv_desc(8, 256, 512, 12, 14, 12, 3, 2, 1, False, R.BF16)
     assert R.rat3d_conv3d_workspace_size(desc, 2) > R.rat3d_conv3d_wgrad_noalloc_max_bytes()
     fake = 0x10000
     with pytest.raises(R.Rat3dError) as e:
