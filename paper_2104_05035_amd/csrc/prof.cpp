@@ -31,8 +31,11 @@ hipEvent_t get_event() {
         g_free.pop_back();
         return e;
     }
+    // timing only: no system-scope fence on record (no cache writeback and
+    // invalidation around every bracketed launch; the host reads only the
+    // timestamps)
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     return e;
 }
 
