@@ -657,6 +657,136 @@ __global__ __launch_bounds__(kEwThreads) void pool332_fwd_pl(const bf16* __restr
     }
 }
 
+// Order-preserving 16-bit codes of the two bfloat16 halves of a word: a
+// value with the sign bit clear maps to v ^ 0x8000, one with it set to
+// (v ^ 0xffff) + 1.  Codes order like the values, -0 and +0 share 0x8000
+// (they compare equal) and every code is at least 1.  Packed 16-bit integer
+// operations: the sign mask by an arithmetic shift, one xor, one subtract.
+typedef __attribute__((ext_vector_type(2))) short pool_s16x2;
+typedef __attribute__((ext_vector_type(2))) unsigned short pool_u16x2;
+__device__ __forceinline__ uint32_t pool_codes2(uint32_t w) {
+    const uint32_t m = __builtin_bit_cast(uint32_t, __builtin_bit_cast(pool_s16x2, w) >> 15);
+    const uint32_t x = w ^ (m | 0x80008000u);
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(pool_u16x2, x) -
+                                            __builtin_bit_cast(pool_u16x2, m));
+}
+// bf16 bits of a code (low 16 bits of c)
+__device__ __forceinline__ uint32_t pool_code_bits(uint32_t c) {
+    return (c & 0x8000u) ? (c & 0x7fffu) : (0x8000u | (0x8000u - c));
+}
+// Key of a padding column: below every value's key (those are at least
+// 1 << 16) and still non-negative after the largest tap offset is taken off.
+constexpr uint32_t kPoolPadKey = 8u;
+
+// Max pool 3^3, stride 2, pad 1, bf16, W % 8 == 0 (so every 8-element group
+// lies in one row and Wo % 4 == 0).  Keys as in pool332_fwd_pl: the 16-bit
+// code of the value above 255 - (9 kd + 3 kh + kw), so the unsigned maximum
+// is the first maximum in scan order together with its index.  The LDS key
+// rows are padded: column iw at 4 + iw, a padding key at 3, so phase B reads
+// the nine columns 2 ow0 - 1 .. 2 ow0 + 7 of four outputs with two aligned
+// 16-byte reads and one 4-byte read, without bounds checks.  Phase B reduces
+// each row over kw first (max3), then over kh.
+__global__ __launch_bounds__(kEwThreads) void pool332_fwd_rows(const bf16* __restrict__ x, int D,
+                                                               int H, int W, int Do, int Ho,
+                                                               int Wo, int nblk,
+                                                               bf16* __restrict__ y,
+                                                               uint8_t* __restrict__ am) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int HW = H * W, RP = W + 4, PP = H * RP;
+    uint32_t* mk = reinterpret_cast<uint32_t*>(smem);  // [kPlanesF][H][RP] keys
+    const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int nc = L / nblk, od0 = (L - nc * nblk) * kPlanesF;
+    const bf16* xv = x + (int64_t)nc * D * HW;
+    constexpr int NQ = 2 * kPlanesF + 1;
+    auto process = [&](int p, const uint4 (&raw)[NQ]) {
+        const int ih = p / W, iw0 = p - ih * W;
+        uint32_t best[kPlanesF][8];
+#pragma unroll
+        for (int j = 0; j < kPlanesF; ++j)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) best[j][e] = 0u;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int id = 2 * od0 - 1 + q;
+            if (id < 0 || id >= D) continue;
+            const uint32_t c[4] = {pool_codes2(raw[q].x), pool_codes2(raw[q].y),
+                                   pool_codes2(raw[q].z), pool_codes2(raw[q].w)};
+#pragma unroll
+            for (int j = 0; j < kPlanesF; ++j) {
+                const int kd = q - 2 * j;
+                if (kd < 0 || kd > 2) continue;
+                const uint32_t tb = 255u - 9u * (uint32_t)kd;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    best[j][2 * i] = max(best[j][2 * i], (c[i] << 16) | tb);
+                    best[j][2 * i + 1] = max(best[j][2 * i + 1], (c[i] & 0xffff0000u) | tb);
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kPlanesF; ++j) {
+            uint32_t* row = mk + j * PP + ih * RP;
+            uint4* dst = reinterpret_cast<uint4*>(row + 4 + iw0);
+            dst[0] = make_uint4(best[j][0], best[j][1], best[j][2], best[j][3]);
+            dst[1] = make_uint4(best[j][4], best[j][5], best[j][6], best[j][7]);
+            if (iw0 == 0) row[3] = kPoolPadKey;
+        }
+    };
+    auto fetch = [&](int p, uint4 (&raw)[NQ]) {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int id = min(max(2 * od0 - 1 + q, 0), D - 1);
+            raw[q] = *reinterpret_cast<const uint4*>(xv + (int64_t)id * HW + p);
+        }
+    };
+    // both 8-element groups of a thread (a 48 x 56 plane has 336) are
+    // requested before either is reduced
+    {
+        const int p0 = threadIdx.x * 8, p1 = p0 + kEwThreads * 8;
+        uint4 r0[NQ], r1[NQ];
+        if (p0 < HW) fetch(p0, r0);
+        if (p1 < HW) fetch(p1, r1);
+        if (p0 < HW) process(p0, r0);
+        if (p1 < HW) process(p1, r1);
+        for (int p = p1 + kEwThreads * 8; p < HW; p += kEwThreads * 8) {
+            fetch(p, r0);
+            process(p, r0);
+        }
+    }
+    __syncthreads();
+    const int Q = Wo >> 2, HQ = Ho * Q;
+    for (int it = threadIdx.x; it < kPlanesF * HQ; it += kEwThreads) {
+        const int j = it / HQ, r = it - j * HQ;
+        const int od = od0 + j;
+        if (od >= Do) break;
+        const int oh = r / Q, ow0 = (r - oh * Q) * 4;
+        uint32_t b[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int kh = 0; kh < 3; ++kh) {
+            const int ih = 2 * oh - 1 + kh;
+            if ((unsigned)ih >= (unsigned)H) continue;
+            // columns 2 ow0 - 1 .. 2 ow0 + 7: tap kw of output e is column 2e + kw
+            const uint32_t* row = mk + j * PP + ih * RP + 3 + 2 * ow0;
+            const uint4 lo = *reinterpret_cast<const uint4*>(row + 1);
+            const uint4 hi = *reinterpret_cast<const uint4*>(row + 5);
+            const uint32_t cw[9] = {row[0], lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+            const uint32_t toff = 3u * (uint32_t)kh;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t m = max(max(cw[2 * e], cw[2 * e + 1] - 1u), cw[2 * e + 2] - 2u);
+                b[e] = max(b[e], m - toff);
+            }
+        }
+        const int64_t o = ((int64_t)nc * Do + od) * (int64_t)(Ho * Wo) + oh * Wo + ow0;
+        *reinterpret_cast<uint2*>(y + o) =
+            make_uint2(pool_code_bits(b[0] >> 16) | pool_code_bits(b[1] >> 16) << 16,
+                       pool_code_bits(b[2] >> 16) | pool_code_bits(b[3] >> 16) << 16);
+        *reinterpret_cast<uint32_t*>(am + o) =
+            (255u - (b[0] & 0xffu)) | (255u - (b[1] & 0xffu)) << 8 |
+            (255u - (b[2] & 0xffu)) << 16 | (255u - (b[3] & 0xffu)) << 24;
+    }
+}
+
 // Max-pool gradient (3^3, stride 2, pad 1), bf16, W % 8 == 0.  A block owns
 // input planes 2*j0 .. 2*j0 + 2*kPlanes - 1, whose windows lie in output
 // planes j0 .. j0 + kPlanes; their dy and argmax are staged in LDS, then
@@ -776,6 +906,128 @@ __global__ __launch_bounds__(kEwThreads) void pool332_bwd_pl(const bf16* __restr
     }
 }
 
+// Max-pool gradient (3^3, stride 2, pad 1), bf16, W % 8 == 0, in scatter
+// form through a float32 LDS tile.  A block owns input planes
+// [2 j0, 2 j0 + 2 kp) of one (n, c) volume and reads the windows of output
+// planes j0 .. j0 + kp (the last one only reaches the block's planes through
+// its kd = 0 taps).  An item is a 2 x 2 group of windows of one output plane
+// (rows 2i, 2i + 1, columns 2k, 2k + 1); each window adds its dy to the input
+// voxel its argmax names, if the block owns it.  Windows whose (od, oh, ow)
+// parities agree never overlap, so their targets are distinct: the block
+// deposits the eight parity classes in eight steps separated by barriers,
+// each a plain LDS read-add-write (a fixed order per voxel: deterministic).
+// Then each thread rounds 8 consecutive voxels (after adding the old value
+// when accumulating) and stores them with one 16-byte store.
+constexpr int kScItems = 2;  // items per thread
+__global__ __launch_bounds__(kEwThreads) void pool332_bwd_sc(const bf16* __restrict__ dy,
+                                                             const uint8_t* __restrict__ am,
+                                                             int D, int H, int W, int Do, int Ho,
+                                                             int Wo, int kp, int nblk,
+                                                             bf16* __restrict__ dx,
+                                                             int accumulate) {
+    extern __shared__ __align__(16) float tile[];  // [2 kp][H][W]
+    const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int nc = L / nblk, j0 = (L - nc * nblk) * kp;
+    const int np = min(2 * kp, D - 2 * j0);  // owned input planes
+    const int HW = H * W;
+    const int HI = (Ho + 1) >> 1, WK = Wo >> 1, per = HI * WK;
+    const int nitems = min(kp + 1, Do - j0) * per;
+    // every item's dy and argmax pairs requested first (Wo is even, so a pair
+    // of columns 2k, 2k + 1 is one aligned 4-byte dy load and 2-byte argmax load)
+    uint32_t dv[kScItems][2], av[kScItems][2];
+    int odr[kScItems], ii[kScItems], kk[kScItems];
+#pragma unroll
+    for (int m = 0; m < kScItems; ++m) {
+        const int it = threadIdx.x + m * kEwThreads;
+        dv[m][0] = dv[m][1] = 0u;
+        av[m][0] = av[m][1] = 0xffffu;  // no window: arguments past 26 deposit nothing
+        odr[m] = -1;
+        ii[m] = kk[m] = 0;
+        if (it < nitems) {
+            const int o = it / per, r = it - o * per;
+            const int i = r / WK, k = r - i * WK;
+            odr[m] = o;
+            ii[m] = i;
+            kk[m] = k;
+            const int64_t b = (((int64_t)nc * Do + j0 + o) * Ho + 2 * i) * Wo + 2 * k;
+            dv[m][0] = *reinterpret_cast<const uint32_t*>(dy + b);
+            av[m][0] = *reinterpret_cast<const uint16_t*>(am + b);
+            if (2 * i + 1 < Ho) {
+                dv[m][1] = *reinterpret_cast<const uint32_t*>(dy + b + Wo);
+                av[m][1] = *reinterpret_cast<const uint16_t*>(am + b + Wo);
+            }
+        }
+    }
+    for (int e = threadIdx.x * 4; e < np * HW; e += kEwThreads * 4)
+        *reinterpret_cast<float4*>(tile + e) = make_float4(0.f, 0.f, 0.f, 0.f);
+    // target of each window in the tile (-1: none, or outside the block's planes)
+    int tg[kScItems][2][2];
+#pragma unroll
+    for (int m = 0; m < kScItems; ++m)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const uint32_t arg = (av[m][b] >> (8 * c)) & 0xffu;
+                // arg = 9 kd + 3 kh + kw, arg < 27
+                const uint32_t kd = (arg * 57u) >> 9, r = arg - 9u * kd;
+                const uint32_t kh = (r * 11u) >> 5, kw = r - 3u * kh;
+                const int tp = 2 * odr[m] - 1 + (int)kd;  // plane, relative to 2 j0
+                const int ih = 2 * (2 * ii[m] + b) - 1 + (int)kh;
+                const int iw = 2 * (2 * kk[m] + c) - 1 + (int)kw;
+                const bool ok = arg < 27u && (unsigned)tp < (unsigned)np &&
+                                (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W;
+                tg[m][b][c] = ok ? (tp * H + ih) * W + iw : -1;
+            }
+#pragma unroll
+    for (int pd = 0; pd < 2; ++pd)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                __syncthreads();
+#pragma unroll
+                for (int m = 0; m < kScItems; ++m) {
+                    const int t = tg[m][b][c];
+                    if (t >= 0 && ((j0 + odr[m]) & 1) == pd) {
+                        const uint32_t h = dv[m][b];
+                        tile[t] += __uint_as_float(c ? (h & 0xffff0000u) : (h << 16));
+                    }
+                }
+            }
+    __syncthreads();
+    bf16* out = dx + ((int64_t)nc * D + 2 * j0) * HW;
+    for (int e = threadIdx.x * 8; e < np * HW; e += kEwThreads * 8) {
+        const float4 s0 = *reinterpret_cast<const float4*>(tile + e);
+        const float4 s1 = *reinterpret_cast<const float4*>(tile + e + 4);
+        float acc[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        uint4* q4 = reinterpret_cast<uint4*>(out + e);
+        if (accumulate) {
+            const uint4 o = *q4;
+            const uint32_t ws[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                acc[2 * i] += __uint_as_float(ws[i] << 16);
+                acc[2 * i + 1] += __uint_as_float(ws[i] & 0xffff0000u);
+            }
+        }
+        *q4 = make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
+                         pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7]));
+    }
+}
+
+// Output planes per block of the scatter-form pool gradient (0: not taken):
+// the largest kp whose tile fits 24 KB and whose items fit the block.
+static int pool_sc_kp(int D, int H, int W, int Do, int Ho, int Wo) {
+    if (W % 8 != 0 || Wo % 2 != 0) return 0;
+    const int64_t per = (int64_t)((Ho + 1) / 2) * (Wo / 2);
+    int kp = (int)(24576 / ((int64_t)2 * H * W * 4));
+    kp = min(kp, Do);
+    while (kp >= 1 && (kp + 1) * per > (int64_t)kScItems * kEwThreads) --kp;
+    (void)D;
+    return kp < 1 ? 0 : kp;
+}
+
 // Exact x2 trilinear, bf16, Wi % 4 == 0.  A block owns fine planes
 // 2*m0 .. 2*m0 + 2*kPlanes - 1.  Phase A blends coarse planes m0-1 .. m0+kPlanes
 // along depth into LDS (float32); phase B blends rows and columns and writes
@@ -853,60 +1105,71 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
         }
     }
     __syncthreads();
-    const int G = Wo >> 3;
-    for (int it = threadIdx.x; it < NF * Ho * G; it += kEwThreads) {
-        const int l = it / (Ho * G), r = it - l * (Ho * G);
+    // an item is two fine rows 2 mh, 2 mh + 1 by 8 fine columns 8g .. 8g + 7:
+    // they blend coarse rows mh - 1, mh, mh + 1 at coarse columns 4g - 1 ..
+    // 4g + 4 (one 16-byte and two 4-byte LDS reads per row).  A border takes
+    // its one existing neighbour with weight 1: its missing row or column is
+    // read clamped and weighted 0.
+    const int G = Wi >> 2;
+    for (int it = threadIdx.x; it < NF * Hi * G; it += kEwThreads) {
+        const int l = it / (Hi * G), r = it - l * (Hi * G);
         const int od = 2 * m0 + l;
         if (od >= Do) break;
-        const int oh = r / G, g = r - oh * G;
-        const int m0w = 4 * g;  // fine 8g .. 8g+7 read coarse m0w-1 .. m0w+4
-        // row blend: fine oh = 2m reads m-1 (1/4) and m (3/4), oh = 2m+1 reads
-        // m (3/4) and m+1 (1/4); at the first / last coarse row the one
-        // existing neighbour takes weight 1
-        const int mh = oh >> 1;
-        int ha, hb;
-        float wa, wb;
-        if ((oh & 1) == 0) {
-            ha = mh - 1; hb = mh; wa = 0.25f; wb = 0.75f;
-            if (mh == 0) { ha = 0; wa = 0.f; wb = 1.f; }
-        } else {
-            ha = mh; hb = mh + 1; wa = 0.75f; wb = 0.25f;
-            if (mh == Hi - 1) { hb = mh; wa = 1.f; wb = 0.f; }
-        }
-        const float* sa = t + l * HW8 + ha * Wi;
-        const float* sb = t + l * HW8 + hb * Wi;
-        float row[6];
+        const int mh = r / G, g = r - mh * G;
+        const float* tl = t + l * HW8;
+        const int ra = max(mh - 1, 0), rd = min(mh + 1, Hi - 1);
+        const int cl = max(4 * g - 1, 0), cr = min(4 * g + 4, Wi - 1);
+        float A[6], B[6], Dn[6];
+        auto rd6 = [&](int row, float (&v)[6]) {
+            const float* q = tl + row * Wi;
+            const float4 m = *reinterpret_cast<const float4*>(q + 4 * g);
+            v[0] = q[cl];
+            v[1] = m.x;
+            v[2] = m.y;
+            v[3] = m.z;
+            v[4] = m.w;
+            v[5] = q[cr];
+        };
+        rd6(ra, A);
+        rd6(mh, B);
+        rd6(rd, Dn);
+        // fine row 2 mh: 1/4 row mh-1 + 3/4 row mh; 2 mh + 1: 3/4 row mh + 1/4 row mh+1
+        const float wea = mh == 0 ? 0.f : 0.25f, web = mh == 0 ? 1.f : 0.75f;
+        const float wob = mh == Hi - 1 ? 1.f : 0.75f, wod = mh == Hi - 1 ? 0.f : 0.25f;
+        // columns: fine 8g + 2k reads coarse 4g + k - 1, 4g + k (row[k], row[k + 1]);
+        // fine 8g + 2k + 1 reads 4g + k, 4g + k + 1 (row[k + 1], row[k + 2])
+        const float c0l = g == 0 ? 0.f : 0.25f, c0r = g == 0 ? 1.f : 0.75f;
+        const float c7l = g == G - 1 ? 1.f : 0.75f, c7r = g == G - 1 ? 0.f : 0.25f;
 #pragma unroll
-        for (int c = 0; c < 6; ++c) {
-            const int m = min(max(m0w - 1 + c, 0), Wi - 1);
-            row[c] = wa * sa[m];
-            row[c] += wb * sb[m];
-        }
-        // column blend, same weights: fine 8g + 2k reads coarse 4g+k-1, 4g+k
-        // (row[k], row[k+1]); fine 8g + 2k + 1 reads 4g+k, 4g+k+1 (row[k+1],
-        // row[k+2]); the borders clamp as above
-        float out[8];
+        for (int half = 0; half < 2; ++half) {
+            float row[6];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int m = m0w + k;
-            out[2 * k] = m == 0 ? row[k + 1] : 0.25f * row[k] + 0.75f * row[k + 1];
-            out[2 * k + 1] = m == Wi - 1 ? row[k + 1] : 0.75f * row[k + 1] + 0.25f * row[k + 2];
-        }
-        uint32_t w4[4];
+            for (int c = 0; c < 6; ++c)
+                row[c] = half == 0 ? fmaf(web, B[c], wea * A[c]) : fmaf(wod, Dn[c], wob * B[c]);
+            float out[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            w4[i] = pack_bf16x2(out[2 * i], out[2 * i + 1]);
-        *reinterpret_cast<uint4*>(y + (((int64_t)nc * Do + od) * Ho + oh) * Wo + 8 * g) =
-            make_uint4(w4[0], w4[1], w4[2], w4[3]);
-        if constexpr (STATS) {
+            for (int k = 0; k < 4; ++k) {
+                out[2 * k] = k == 0 ? fmaf(c0r, row[1], c0l * row[0])
+                                    : fmaf(0.75f, row[k + 1], 0.25f * row[k]);
+                out[2 * k + 1] = k == 3 ? fmaf(c7r, row[5], c7l * row[4])
+                                        : fmaf(0.25f, row[k + 2], 0.75f * row[k + 1]);
+            }
+            uint32_t w4[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float lo = __uint_as_float(w4[i] << 16) - shift;
-                const float hi = __uint_as_float(w4[i] & 0xffff0000u) - shift;
-                s1 += lo;
-                s2 += lo * lo;
-                s1 += hi;
-                s2 += hi * hi;
+            for (int i = 0; i < 4; ++i) w4[i] = pack_bf16x2(out[2 * i], out[2 * i + 1]);
+            const int oh = 2 * mh + half;
+            *reinterpret_cast<uint4*>(y + (((int64_t)nc * Do + od) * Ho + oh) * Wo + 8 * g) =
+                make_uint4(w4[0], w4[1], w4[2], w4[3]);
+            if constexpr (STATS) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float lo = __uint_as_float(w4[i] << 16) - shift;
+                    const float hi = __uint_as_float(w4[i] & 0xffff0000u) - shift;
+                    s1 += lo;
+                    s2 += lo * lo;
+                    s1 += hi;
+                    s2 += hi * hi;
+                }
             }
         }
     }
@@ -1102,6 +1365,14 @@ rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, ra
     ProfScope ps("pool_fwd", st, 0.0, es * ((double)N * C * D * H * W + total) + total);
     const int HW8 = (H * W + 7) & ~7;
     const size_t lds_f = (size_t)kPlanesF * HW8 * 4;
+    const size_t lds_r = (size_t)kPlanesF * H * (W + 4) * 4;
+    if (k == 3 && s == 2 && p == 1 && dt == RAT3D_BF16 && W % 8 == 0 && lds_r <= kPlaneLds) {
+        const int nblk = (int)ceil_div(Do, kPlanesF);
+        pool332_fwd_rows<<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_r, st>>>(
+            (const bf16*)x, D, H, W, Do, Ho, Wo, nblk, (bf16*)y, argmax);
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
     if (k == 3 && s == 2 && p == 1 && dt == RAT3D_BF16 && lds_f <= kPlaneLds) {
         const int nblk = (int)ceil_div(Do, kPlanesF);
         pool332_fwd_pl<<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_f, st>>>(
@@ -1140,6 +1411,16 @@ rat3d_status pool_bwd(int N, int C, int D, int H, int W, int k, int s, int p, ra
     const double small = (double)N * C * Do * Ho * Wo;
     ProfScope ps("pool_bwd", st, 0.0, es * (small + total * (1 + accumulate)) + small);
     const size_t lds_b = (size_t)(kPlanes + 1) * Ho * Wo * 3;
+    const int kp = k == 3 && s == 2 && p == 1 && dt == RAT3D_BF16 ? pool_sc_kp(D, H, W, Do, Ho, Wo)
+                                                                  : 0;
+    if (kp > 0) {
+        const int nblk = (int)ceil_div(D, 2 * kp);
+        pool332_bwd_sc<<<(unsigned)((int64_t)N * C * nblk), kEwThreads,
+                         (size_t)2 * kp * H * W * sizeof(float), st>>>(
+            (const bf16*)dy, argmax, D, H, W, Do, Ho, Wo, kp, nblk, (bf16*)dx, accumulate);
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
     if (k == 3 && s == 2 && p == 1 && dt == RAT3D_BF16 && W % 8 == 0 && lds_b <= kPlaneLds) {
         const int nblk = (int)ceil_div(D, 2 * kPlanes);
         pool332_bwd_pl<<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_b, st>>>(

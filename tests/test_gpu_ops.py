@@ -279,7 +279,30 @@ def test_maxpool(case):
     U.check(U.f64(base), rnd(baser + dxr), dt, "dx accumulate", terms=tdx + np.abs(baser))
 
 
-UP_CASES = [((6, 7, 6), (12, 14, 12)), ((3, 4, 3), (6, 7, 6)), ((2, 2, 2), (3, 4, 3)),
+# values from a five-element set: most windows hold ties, all-negative windows
+# and both signed zeros, so the first-maximum rule decides most argmax bytes
+TIE_CASES = [(2, 3, 10, 12, 16), (1, 2, 9, 7, 24), (2, 2, 6, 5, 6), (1, 4, 48, 56, 48)]
+
+
+@pytest.mark.parametrize("case", TIE_CASES, ids=lambda c: "%dx%dx%dx%dx%d" % c)
+def test_maxpool_ties(case):
+    from paper_2104_05035_amd import rat3d as R
+    torch = U.torch_mod()
+    N, C, D, H, W = case
+    rng = np.random.default_rng(7 * D + W)
+    vals = np.array([-1.0, -0.0, 0.0, 0.5, -0.5])
+    x, xr = U.dev_input(vals[rng.integers(0, len(vals), (N, C, D, H, W))], "bf16")
+    yref, amref = ops.maxpool3d_fwd(xr)
+    desc = R.PoolDesc(N, C, D, H, W, 3, 2, 1, U.code("bf16"))
+    y = U.empty(yref.shape, "bf16")
+    am = torch.empty(yref.shape, dtype=torch.uint8, device="cuda:0")
+    R.rat3d_softmask_down_fwd(desc, x, y, am)
+    U.sync()
+    np.testing.assert_array_equal(U.f64(y), yref)  # -0 and +0 compare equal
+    np.testing.assert_array_equal(am.cpu().numpy().astype(np.int32), amref)
+
+
+UP_CASES =[((6, 7, 6), (12, 14, 12)), ((3, 4, 3), (6, 7, 6)), ((2, 2, 2), (3, 4, 3)),
             ((12, 12, 12), (24, 24, 24)), ((5, 3, 4), (5, 9, 7)), ((1, 1, 1), (2, 3, 1)),
             ((24, 28, 24), (48, 56, 48)), ((2, 130, 3), (4, 260, 5)),
             # exact x2 with a plane size that is not a multiple of 8, odd depth
