@@ -1355,6 +1355,183 @@ __global__ __launch_bounds__(kEwThreads) void up2_bwd_pl(const bf16* __restrict_
     }
 }
 
+// Transpose of up2_fwd_pl walking a chunk of coarse planes [m0, m1) of one
+// (n, c) volume (bf16, Wi % 4 == 0, a fine plane of at most 2 * 256 groups
+// of 8).  Each fine plane the chunk reaches is read, and with BN transformed
+// as in up2_bwd_pl, exactly once, in increasing order; its depth weights add
+// it to the two coarse planes it reaches (register sums, the order of
+// up2_bwd_pl).  A completed coarse plane's depth sums go to one of two LDS
+// buffers and, after one barrier, are finished in-plane as in up2_bwd_pl,
+// while the next two fine planes are already requested.
+constexpr int kUpChunk = 24;  // coarse planes per block (a 24-plane volume: one block)
+constexpr int kUpItems = 2;  // fine 8-element groups per thread
+
+template <bool BN>
+__global__ __launch_bounds__(kEwThreads) void up2_bwd_roll(const bf16* __restrict__ dy, int Di,
+                                                           int Hi, int Wi, int nchunk,
+                                                           bf16* __restrict__ dx, int accumulate,
+                                                           UpBn ub) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int Do = 2 * Di, Ho = 2 * Hi, Wo = 2 * Wi;
+    const int HWo = Ho * Wo, NG = HWo >> 3;
+    float* t = reinterpret_cast<float*>(smem);  // [2][HWo]
+    const int L = xcd_remap(blockIdx.x, gridDim.x);
+    const int nc = L / nchunk, ch = L - nc * nchunk;
+    const int m0 = ch * kUpChunk, m1 = min(m0 + kUpChunk, Di);
+    const bf16* gv = dy + (int64_t)nc * Do * HWo;
+    [[maybe_unused]] float bk = 0.f, ba = 0.f, bb = 0.f, bmean = 0.f, fsc = 0.f, fsh = 0.f;
+    [[maybe_unused]] const bf16* hv = nullptr;
+    if constexpr (BN) {
+        // every lane is active here, as the coefficient reduction needs
+        const int c = nc % ub.C;
+        bn_bwd_coefs(ub.N, (int64_t)Do * HWo, c, ub.st, nc < ub.C && ch == 0 && threadIdx.x == 0,
+                     bk, ba, bb);
+        bmean = ub.mean[c];
+        fsc = ub.fcoef[c];
+        fsh = ub.fcoef[ub.C + c];
+        hv = ub.h + (int64_t)nc * Do * HWo;
+    }
+    bool live[kUpItems];
+#pragma unroll
+    for (int j = 0; j < kUpItems; ++j) live[j] = threadIdx.x + j * kEwThreads < NG;
+    // two fine planes in flight: raw dy (and h) per item
+    uint4 rg[2][kUpItems];
+    [[maybe_unused]] uint4 rh[2][kUpItems];
+    auto issue = [&](int s, int od) {
+        if (od < 0 || od >= Do) return;
+#pragma unroll
+        for (int j = 0; j < kUpItems; ++j) {
+            if (!live[j]) continue;
+            const int64_t o = (int64_t)od * HWo + (threadIdx.x + j * kEwThreads) * 8;
+            rg[s][j] = *reinterpret_cast<const uint4*>(gv + o);
+            if constexpr (BN) rh[s][j] = *reinterpret_cast<const uint4*>(hv + o);
+        }
+    };
+    float cur[kUpItems][8], nxt[kUpItems][8];
+#pragma unroll
+    for (int j = 0; j < kUpItems; ++j)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cur[j][e] = nxt[j][e] = 0.f;
+    // fine plane od (loaded in slot s) added to coarse planes ma (into cur)
+    // and mb (into nxt, when mb >= 0)
+    auto consume = [&](int s, int od, int ma, int mb) {
+        if (od < 0 || od >= Do) return;
+        const float wa = x2_w(od, ma, Di), wb = mb >= 0 ? x2_w(od, mb, Di) : 0.f;
+#pragma unroll
+        for (int j = 0; j < kUpItems; ++j) {
+            if (!live[j]) continue;
+            float v[8];
+            const uint32_t w[4] = {rg[s][j].x, rg[s][j].y, rg[s][j].z, rg[s][j].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                v[2 * i] = __uint_as_float(w[i] << 16);
+                v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+            }
+            if constexpr (BN) {
+                const uint32_t hw[4] = {rh[s][j].x, rh[s][j].y, rh[s][j].z, rh[s][j].w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float h0 = __uint_as_float(hw[i] << 16);
+                    const float h1 = __uint_as_float(hw[i] & 0xffff0000u);
+                    const float g0 = fmaf(h0, fsc, fsh) > 0.f ? v[2 * i] : 0.f;
+                    const float g1 = fmaf(h1, fsc, fsh) > 0.f ? v[2 * i + 1] : 0.f;
+                    v[2 * i] = Elt<bf16>::round(bk * (g0 - ba - (h0 - bmean) * bb));
+                    v[2 * i + 1] = Elt<bf16>::round(bk * (g1 - ba - (h1 - bmean) * bb));
+                }
+            }
+            if (wa != 0.f)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) cur[j][e] += wa * v[e];
+            if (wb != 0.f)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) nxt[j][e] += wb * v[e];
+        }
+    };
+    // coarse m0 starts with fine planes 2 m0 - 1 and 2 m0 (they reach m0 - 1 and m0)
+    issue(0, 2 * m0 - 1);
+    issue(1, 2 * m0);
+    consume(0, 2 * m0 - 1, m0, -1);
+    consume(1, 2 * m0, m0, -1);
+    issue(0, 2 * m0 + 1);
+    issue(1, 2 * m0 + 2);
+    const int G = Wi >> 2;
+    for (int m = m0; m < m1; ++m) {
+        // fine planes 2m + 1 and 2m + 2 complete coarse m and start m + 1
+        const int mb = m + 1 < m1 ? m + 1 : -1;
+        consume(0, 2 * m + 1, m, mb);
+        consume(1, 2 * m + 2, m, mb);
+        if (mb >= 0) {
+            issue(0, 2 * m + 3);
+            issue(1, 2 * m + 4);
+        }
+        float* tb = t + (m & 1) * HWo;
+#pragma unroll
+        for (int j = 0; j < kUpItems; ++j) {
+            if (!live[j]) continue;
+            float4* d4 = reinterpret_cast<float4*>(tb + (threadIdx.x + j * kEwThreads) * 8);
+            d4[0] = make_float4(cur[j][0], cur[j][1], cur[j][2], cur[j][3]);
+            d4[1] = make_float4(cur[j][4], cur[j][5], cur[j][6], cur[j][7]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                cur[j][e] = nxt[j][e];
+                nxt[j][e] = 0.f;
+            }
+        }
+        __syncthreads();
+        for (int it = threadIdx.x; it < Hi * G; it += kEwThreads) {
+            const int ih = it / G, g = it - ih * G;
+            float rowacc[10];  // fine columns 8g-1 .. 8g+8 blended over the fine rows
+#pragma unroll
+            for (int j = 0; j < 10; ++j) rowacc[j] = 0.f;
+#pragma unroll
+            for (int hh = 0; hh < 4; ++hh) {
+                const int oh = 2 * ih - 1 + hh;
+                if (oh < 0 || oh >= Ho) continue;
+                const float wh = (hh == 0 || hh == 3)
+                                     ? 0.25f
+                                     : (hh == 1 ? (ih == 0 ? 1.f : 0.75f)
+                                                : (ih == Hi - 1 ? 1.f : 0.75f));
+                const float* src = tb + oh * Wo;
+                const float4 a = *reinterpret_cast<const float4*>(src + 8 * g);
+                const float4 b = *reinterpret_cast<const float4*>(src + 8 * g + 4);
+                rowacc[1] += wh * a.x; rowacc[2] += wh * a.y; rowacc[3] += wh * a.z;
+                rowacc[4] += wh * a.w; rowacc[5] += wh * b.x; rowacc[6] += wh * b.y;
+                rowacc[7] += wh * b.z; rowacc[8] += wh * b.w;
+                if (g > 0) rowacc[0] += wh * src[8 * g - 1];
+                if (8 * g + 8 < Wo) rowacc[9] += wh * src[8 * g + 8];
+            }
+            float out[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int mw = 4 * g + k;
+                float v = 0.f;
+                v += 0.25f * rowacc[2 * k];
+                v += (mw == 0 ? 1.f : 0.75f) * rowacc[2 * k + 1];
+                v += (mw == Wi - 1 ? 1.f : 0.75f) * rowacc[2 * k + 2];
+                v += 0.25f * rowacc[2 * k + 3];
+                out[k] = v;
+            }
+            uint2* q2 =
+                reinterpret_cast<uint2*>(dx + (((int64_t)nc * Di + m) * Hi + ih) * Wi + 4 * g);
+            if (accumulate) {
+                const uint2 o = *q2;
+                out[0] += __uint_as_float(o.x << 16);
+                out[1] += __uint_as_float(o.x & 0xffff0000u);
+                out[2] += __uint_as_float(o.y << 16);
+                out[3] += __uint_as_float(o.y & 0xffff0000u);
+            }
+            *q2 = make_uint2(pack_bf16x2(out[0], out[1]), pack_bf16x2(out[2], out[3]));
+        }
+    }
+}
+
+// taken where every thread has a fine group (smaller planes leave most lanes
+// idle through the per-plane steps; there the plane-pair blocks are faster)
+static bool up2_roll_ok(int Hi, int Wi) {
+    const int64_t ng = (int64_t)4 * Hi * Wi / 8;
+    return Wi % 4 == 0 && ng >= kEwThreads && ng <= (int64_t)kUpItems * kEwThreads;
+}
+
 // ---------------------------------------------------------------- launchers
 rat3d_status pool_fwd(int N, int C, int D, int H, int W, int k, int s, int p, rat3d_dtype dt,
                       const void* x, void* y, uint8_t* argmax, hipStream_t st) {
@@ -1500,6 +1677,15 @@ rat3d_status up_bwd(int N, int C, int Di, int Hi, int Wi, int Do, int Ho, int Wo
                      ((double)N * C * Do * Ho * Wo + total * (1 + accumulate)));
     const bool x2 = Do == 2 * Di && Ho == 2 * Hi && Wo == 2 * Wi;
     const size_t lds_b = (size_t)kPlanes * Ho * Wo * sizeof(float);
+    if (x2 && dt == RAT3D_BF16 && up2_roll_ok(Hi, Wi) &&
+        (size_t)2 * Ho * Wo * sizeof(float) <= kPlaneLds) {
+        const int nchunk = (int)ceil_div(Di, kUpChunk);
+        up2_bwd_roll<false><<<(unsigned)((int64_t)N * C * nchunk), kEwThreads,
+                              (size_t)2 * Ho * Wo * sizeof(float), st>>>(
+            (const bf16*)dy, Di, Hi, Wi, nchunk, (bf16*)dx, accumulate, UpBn{});
+        RAT3D_LAUNCH_CHECK();
+        return RAT3D_OK;
+    }
     if (x2 && dt == RAT3D_BF16 && Wi % 4 == 0 && lds_b <= kPlaneLds) {
         const int nblk = (int)ceil_div(Di, kPlanes);
         up2_bwd_pl<false><<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_b, st>>>(
@@ -1677,8 +1863,15 @@ rat3d_status bn_relu_bwd_up2(int N, int C, int Di, int Hi, int Wi, const void* d
     const size_t lds_b = (size_t)kPlanes * 4 * Hi * Wi * sizeof(float);
     ProfScope ps("bn_bwd_apply_up", st, 0.0,
                  2.0 * (2.0 * N * C * g.V + (double)N * C * Di * Hi * Wi));
-    up2_bwd_pl<true><<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_b, st>>>(
-        (const bf16*)dy, Di, Hi, Wi, nblk, (bf16*)dxc, 0, ub);
+    if (up2_roll_ok(Hi, Wi)) {
+        const int nchunk = (int)ceil_div(Di, kUpChunk);
+        up2_bwd_roll<true><<<(unsigned)((int64_t)N * C * nchunk), kEwThreads,
+                             (size_t)2 * 4 * Hi * Wi * sizeof(float), st>>>(
+            (const bf16*)dy, Di, Hi, Wi, nchunk, (bf16*)dxc, 0, ub);
+    } else {
+        up2_bwd_pl<true><<<(unsigned)((int64_t)N * C * nblk), kEwThreads, lds_b, st>>>(
+            (const bf16*)dy, Di, Hi, Wi, nblk, (bf16*)dxc, 0, ub);
+    }
     RAT3D_LAUNCH_CHECK();
     return RAT3D_OK;
 }
