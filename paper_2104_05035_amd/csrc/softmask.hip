@@ -754,19 +754,28 @@ __global__ __launch_bounds__(kEwThreads) void pool332_fwd_rows(const bf16* __res
         }
     }
     __syncthreads();
+    // items it = tid, tid + 256, ... of the flattened (j, oh, q) range, the
+    // indices stepped incrementally (no per-item division), 32-bit offsets
     const int Q = Wo >> 2, HQ = Ho * Q;
-    for (int it = threadIdx.x; it < kPlanesF * HQ; it += kEwThreads) {
-        const int j = it / HQ, r = it - j * HQ;
-        const int od = od0 + j;
-        if (od >= Do) break;
-        const int oh = r / Q, ow0 = (r - oh * Q) * 4;
+    const int jmax = min(kPlanesF, Do - od0);
+    const int dq = kEwThreads / Q, dr = kEwThreads - dq * Q;
+    int j = (int)threadIdx.x / HQ, oh, q;
+    {
+        const int r0 = (int)threadIdx.x - j * HQ;
+        oh = r0 / Q;
+        q = r0 - oh * Q;
+    }
+    bf16* yb = y + ((int64_t)nc * Do + od0) * (int64_t)(Ho * Wo);
+    uint8_t* ab = am + ((int64_t)nc * Do + od0) * (int64_t)(Ho * Wo);
+    for (; j < jmax;) {
+        const int ow0 = 4 * q;
         uint32_t b[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int kh = 0; kh < 3; ++kh) {
             const int ih = 2 * oh - 1 + kh;
             if ((unsigned)ih >= (unsigned)H) continue;
             // columns 2 ow0 - 1 .. 2 ow0 + 7: tap kw of output e is column 2e + kw
-            const uint32_t* row = mk + j * PP + ih * RP + 3 + 2 * ow0;
+            const uint32_t* row = mk + __mul24(j, PP) + __mul24(ih, RP) + 3 + 2 * ow0;
             const uint4 lo = *reinterpret_cast<const uint4*>(row + 1);
             const uint4 hi = *reinterpret_cast<const uint4*>(row + 5);
             const uint32_t cw[9] = {row[0], lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
@@ -777,13 +786,23 @@ __global__ __launch_bounds__(kEwThreads) void pool332_fwd_rows(const bf16* __res
                 b[e] = max(b[e], m - toff);
             }
         }
-        const int64_t o = ((int64_t)nc * Do + od) * (int64_t)(Ho * Wo) + oh * Wo + ow0;
-        *reinterpret_cast<uint2*>(y + o) =
+        const int o = __mul24(j, Ho * Wo) + __mul24(oh, Wo) + ow0;
+        *reinterpret_cast<uint2*>(yb + o) =
             make_uint2(pool_code_bits(b[0] >> 16) | pool_code_bits(b[1] >> 16) << 16,
                        pool_code_bits(b[2] >> 16) | pool_code_bits(b[3] >> 16) << 16);
-        *reinterpret_cast<uint32_t*>(am + o) =
+        *reinterpret_cast<uint32_t*>(ab + o) =
             (255u - (b[0] & 0xffu)) | (255u - (b[1] & 0xffu)) << 8 |
             (255u - (b[2] & 0xffu)) << 16 | (255u - (b[3] & 0xffu)) << 24;
+        oh += dq;
+        q += dr;
+        if (q >= Q) {
+            q -= Q;
+            ++oh;
+        }
+        while (oh >= Ho) {
+            oh -= Ho;
+            ++j;
+        }
     }
 }
 
@@ -936,6 +955,8 @@ __global__ __launch_bounds__(kEwThreads) void pool332_bwd_sc(const bf16* __restr
     // of columns 2k, 2k + 1 is one aligned 4-byte dy load and 2-byte argmax load)
     uint32_t dv[kScItems][2], av[kScItems][2];
     int odr[kScItems], ii[kScItems], kk[kScItems];
+    const bf16* dyb = dy + ((int64_t)nc * Do + j0) * (int64_t)(Ho * Wo);
+    const uint8_t* amb = am + ((int64_t)nc * Do + j0) * (int64_t)(Ho * Wo);
 #pragma unroll
     for (int m = 0; m < kScItems; ++m) {
         const int it = threadIdx.x + m * kEwThreads;
@@ -949,12 +970,12 @@ __global__ __launch_bounds__(kEwThreads) void pool332_bwd_sc(const bf16* __restr
             odr[m] = o;
             ii[m] = i;
             kk[m] = k;
-            const int64_t b = (((int64_t)nc * Do + j0 + o) * Ho + 2 * i) * Wo + 2 * k;
-            dv[m][0] = *reinterpret_cast<const uint32_t*>(dy + b);
-            av[m][0] = *reinterpret_cast<const uint16_t*>(am + b);
+            const int b = __mul24(o, Ho * Wo) + __mul24(2 * i, Wo) + 2 * k;
+            dv[m][0] = *reinterpret_cast<const uint32_t*>(dyb + b);
+            av[m][0] = *reinterpret_cast<const uint16_t*>(amb + b);
             if (2 * i + 1 < Ho) {
-                dv[m][1] = *reinterpret_cast<const uint32_t*>(dy + b + Wo);
-                av[m][1] = *reinterpret_cast<const uint16_t*>(am + b + Wo);
+                dv[m][1] = *reinterpret_cast<const uint32_t*>(dyb + b + Wo);
+                av[m][1] = *reinterpret_cast<const uint16_t*>(amb + b + Wo);
             }
         }
     }
@@ -970,14 +991,14 @@ __global__ __launch_bounds__(kEwThreads) void pool332_bwd_sc(const bf16* __restr
             for (int c = 0; c < 2; ++c) {
                 const uint32_t arg = (av[m][b] >> (8 * c)) & 0xffu;
                 // arg = 9 kd + 3 kh + kw, arg < 27
-                const uint32_t kd = (arg * 57u) >> 9, r = arg - 9u * kd;
-                const uint32_t kh = (r * 11u) >> 5, kw = r - 3u * kh;
+                const uint32_t kd = __umul24(arg, 57u) >> 9, r = arg - __umul24(9u, kd);
+                const uint32_t kh = __umul24(r, 11u) >> 5, kw = r - __umul24(3u, kh);
                 const int tp = 2 * odr[m] - 1 + (int)kd;  // plane, relative to 2 j0
                 const int ih = 2 * (2 * ii[m] + b) - 1 + (int)kh;
                 const int iw = 2 * (2 * kk[m] + c) - 1 + (int)kw;
                 const bool ok = arg < 27u && (unsigned)tp < (unsigned)np &&
                                 (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W;
-                tg[m][b][c] = ok ? (tp * H + ih) * W + iw : -1;
+                tg[m][b][c] = ok ? __mul24(tp, H * W) + __mul24(ih, W) + iw : -1;
             }
 #pragma unroll
     for (int pd = 0; pd < 2; ++pd)
@@ -1110,18 +1131,27 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
     // 4g + 4 (one 16-byte and two 4-byte LDS reads per row).  A border takes
     // its one existing neighbour with weight 1: its missing row or column is
     // read clamped and weighted 0.
-    const int G = Wi >> 2;
-    for (int it = threadIdx.x; it < NF * Hi * G; it += kEwThreads) {
-        const int l = it / (Hi * G), r = it - l * (Hi * G);
-        const int od = 2 * m0 + l;
-        if (od >= Do) break;
-        const int mh = r / G, g = r - mh * G;
+    // Items it = tid, tid + 256, ... of the flattened (l, mh, g) range; the
+    // indices step incrementally (no per-item division) and the offsets are
+    // 32-bit products of small values (full-rate 24-bit multiplies).
+    const int G = Wi >> 2, HG = Hi * G;
+    const int lmax = min(NF, Do - 2 * m0);
+    const int dq = kEwThreads / G, dr = kEwThreads - dq * G;
+    int l = (int)threadIdx.x / HG, mh, g;
+    {
+        const int r0 = (int)threadIdx.x - l * HG;
+        mh = r0 / G;
+        g = r0 - mh * G;
+    }
+    bf16* yb = y + ((int64_t)nc * Do + 2 * m0) * Ho * Wo;
+    for (; l < lmax;) {
         const float* tl = t + l * HW8;
-        const int ra = max(mh - 1, 0), rd = min(mh + 1, Hi - 1);
+        const int mhW = __mul24(mh, Wi);
+        const int roff[3] = {mh > 0 ? mhW - Wi : mhW, mhW, mh < Hi - 1 ? mhW + Wi : mhW};
         const int cl = max(4 * g - 1, 0), cr = min(4 * g + 4, Wi - 1);
         float A[6], B[6], Dn[6];
-        auto rd6 = [&](int row, float (&v)[6]) {
-            const float* q = tl + row * Wi;
+        auto rd6 = [&](int ro, float (&v)[6]) {
+            const float* q = tl + ro;
             const float4 m = *reinterpret_cast<const float4*>(q + 4 * g);
             v[0] = q[cl];
             v[1] = m.x;
@@ -1130,9 +1160,9 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
             v[4] = m.w;
             v[5] = q[cr];
         };
-        rd6(ra, A);
-        rd6(mh, B);
-        rd6(rd, Dn);
+        rd6(roff[0], A);
+        rd6(roff[1], B);
+        rd6(roff[2], Dn);
         // fine row 2 mh: 1/4 row mh-1 + 3/4 row mh; 2 mh + 1: 3/4 row mh + 1/4 row mh+1
         const float wea = mh == 0 ? 0.f : 0.25f, web = mh == 0 ? 1.f : 0.75f;
         const float wob = mh == Hi - 1 ? 1.f : 0.75f, wod = mh == Hi - 1 ? 0.f : 0.25f;
@@ -1157,8 +1187,8 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
             uint32_t w4[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) w4[i] = pack_bf16x2(out[2 * i], out[2 * i + 1]);
-            const int oh = 2 * mh + half;
-            *reinterpret_cast<uint4*>(y + (((int64_t)nc * Do + od) * Ho + oh) * Wo + 8 * g) =
+            // fine row 2 mh + half of plane l: (l Ho + 2 mh + half) Wo, Wo = 2 Wi
+            *reinterpret_cast<uint4*>(yb + __mul24(l, Ho * Wo) + 4 * mhW + half * Wo + 8 * g) =
                 make_uint4(w4[0], w4[1], w4[2], w4[3]);
             if constexpr (STATS) {
 #pragma unroll
@@ -1171,6 +1201,16 @@ __global__ __launch_bounds__(kEwThreads) void up2_fwd_pl(const bf16* __restrict_
                     s2 += hi * hi;
                 }
             }
+        }
+        mh += dq;
+        g += dr;
+        if (g >= G) {
+            g -= G;
+            ++mh;
+        }
+        while (mh >= Hi) {
+            mh -= Hi;
+            ++l;
         }
     }
     if constexpr (STATS) {
