@@ -249,7 +249,9 @@ POOL_CASES = [(2, 3, 9, 8, 7, "bf16"), (2, 16, 24, 28, 24, "bf16"), (1, 2, 3, 4,
               (1, 1, 2, 2, 2, "bf16"), (2, 4, 6, 7, 6, "bf16"), (1, 1, 1, 1, 1, "f32"),
               (1, 2, 48, 56, 48, "bf16"), (1, 1, 5, 300, 7, "f32"),
               # plane-staged bf16 paths: odd depth/height, W a multiple of 8
-              (1, 3, 7, 5, 16, "bf16"), (2, 2, 5, 3, 8, "bf16")]
+              (1, 3, 7, 5, 16, "bf16"), (2, 2, 5, 3, 8, "bf16"),
+              # the smallest maps of the W % 8 = 0 paths: one plane, one row
+              (1, 2, 1, 1, 8, "bf16"), (1, 1, 2, 3, 8, "bf16"), (2, 2, 3, 2, 16, "bf16")]
 
 
 @pytest.mark.parametrize("case", POOL_CASES, ids=lambda c: "%dx%dx%dx%dx%d_%s" % c)
@@ -306,7 +308,10 @@ UP_CASES =[((6, 7, 6), (12, 14, 12)), ((3, 4, 3), (6, 7, 6)), ((2, 2, 2), (3, 4,
             ((12, 12, 12), (24, 24, 24)), ((5, 3, 4), (5, 9, 7)), ((1, 1, 1), (2, 3, 1)),
             ((24, 28, 24), (48, 56, 48)), ((2, 130, 3), (4, 260, 5)),
             # exact x2 with a plane size that is not a multiple of 8, odd depth
-            ((3, 5, 4), (6, 10, 8)), ((5, 3, 8), (10, 6, 16))]
+            ((3, 5, 4), (6, 10, 8)), ((5, 3, 8), (10, 6, 16)),
+            # fine planes of 256-512 groups of 8 (the whole-volume transpose):
+            # one coarse plane, and an odd count
+            ((1, 16, 32), (2, 32, 64)), ((3, 16, 32), (6, 32, 64))]
 
 
 @pytest.mark.parametrize("sizes", UP_CASES, ids=lambda s: "%s_to_%s" % s)
