@@ -329,11 +329,15 @@ def test_trilinear(sizes, dt):
     dy, dyr = U.dev_input(rng.standard_normal((N, C, Do, Ho, Wo)), dt)
     dx = U.empty((N, C, Di, Hi, Wi), dt)
     R.rat3d_softmask_up_bwd(desc, dy, dx, 0)
+    base, baser = U.dev_input(rng.standard_normal((N, C, Di, Hi, Wi)), dt)
+    R.rat3d_softmask_up_bwd(desc, dy, base, 1)
     U.sync()
     U.check(U.f64(y), rnd(ops.trilinear_fwd(xr, (Do, Ho, Wo))), dt, "y",
             terms=ops.trilinear_fwd(np.abs(xr), (Do, Ho, Wo)))
-    U.check(U.f64(dx), rnd(ops.trilinear_bwd(dyr, (Di, Hi, Wi))), dt, "dx",
-            terms=ops.trilinear_bwd(np.abs(dyr), (Di, Hi, Wi)))
+    dxr = ops.trilinear_bwd(dyr, (Di, Hi, Wi))
+    tdx = ops.trilinear_bwd(np.abs(dyr), (Di, Hi, Wi))
+    U.check(U.f64(dx), rnd(dxr), dt, "dx", terms=tdx)
+    U.check(U.f64(base), rnd(baser + dxr), dt, "dx accumulate", terms=tdx + np.abs(baser))
 
 
 @pytest.mark.parametrize("count", [1, 1001, 4096, 131072 + 5])
