@@ -6,17 +6,21 @@
 // channels.  K is ordered (kd, kh, kw) with kw padded from 7 to 8, so the
 // eight K values of one MFMA operand row are eight consecutive input columns
 // of one (kd, kh) row: columns 2i .. 2i+7 of the input brick for output
-// column i.  The brick is stored twice, the second copy shifted by two
-// columns, so that the row starts on an 8-byte boundary in one of the copies
-// and the operand is two aligned 8-byte LDS reads.  Padding taps (kw = 7,
-// and (kd, kh) rows 49..51 of the last K step) have zero weights.
+// column i, four 4-byte LDS reads.  Padding taps (kw = 7, and (kd, kh) rows
+// 49..51 of the last K step) have zero weights.  The weights are re-laid in
+// MFMA lane order once per launch and copied into LDS with the brick: every
+// staging load of a workgroup is issued before the first LDS store, so a
+// workgroup waits for one global round trip, and three workgroups share a
+// CU.
 //
 // Weight gradient: rows = output channels, columns = padded taps, K = output
-// voxels.  The A operand is dy (8 consecutive output voxels of one channel:
-// one 16-byte global load); the B operand needs input columns 2w - 3 + kw at
-// stride 2, so the input brick is stored split by column parity, each parity
-// plane twice (shifted by one element) so that the 8 values start on a
-// 4-byte boundary and load as four aligned 4-byte LDS reads.
+// voxels.  The A operand is dy (8 consecutive output voxels of one channel),
+// staged in LDS in MFMA lane order; the B operand needs input columns
+// 2w - 3 + kw at stride 2, so the input brick is stored split by column
+// parity, each parity plane twice (shifted by one element) so that the 8
+// values start on a 4-byte boundary and load as four aligned 4-byte LDS
+// reads.  Each brick's dy and input loads are all issued before the barrier
+// that frees the LDS, and three workgroups share a CU.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "prof.hpp"
@@ -43,23 +47,35 @@ constexpr int kFBH = (kFH - 1) * kSS + kSK;       // 21
 constexpr int kFBW = 40;                          // >= (16-1)*2 + 8 = 38 columns, 80-byte rows
 }  // namespace
 
-// wp[co][r][8] = w[co][0][kd][kh][kw] (r = kd*7 + kh, kw < 7), zero elsewhere
+// wp[ks][ct][lane][8], the B operands in MFMA lane order: lane = kg * 16 + li
+// holds w[co][0][kd][kh][kw] for co = ct * 16 + li, row r = kd * 7 + kh =
+// 4 ks + kg and kw = 0 .. 7; zero for kw = 7 and rows past 48
+constexpr int kSKSteps = kSRowsPad / 4;           // 13 K steps
+constexpr int kSWUnits = kSKSteps * 2 * 64;       // 16-byte units of wp
 __global__ void stem_prep_weights(const bf16* __restrict__ w, bf16* __restrict__ wp) {
     const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= kSCo * kSRowsPad * 8) return;
-    const int kw = i & 7, r = (i >> 3) % kSRowsPad, co = i / (8 * kSRowsPad);
+    if (i >= kSWUnits * 8) return;
+    const int kw = i & 7, lane = (i >> 3) & 63, ct = (i >> 9) & 1, ks = i >> 10;
+    const int co = ct * 16 + (lane & 15), r = ks * 4 + (lane >> 4);
     bf16 v = 0;
     if (kw < kSK && r < kSRows) v = w[(co * kSRows + r) * kSK + kw];
     wp[i] = v;
 }
 
-__global__ __launch_bounds__(256, 2) void stem_fwd_k(const bf16* __restrict__ x,
+__global__ __launch_bounds__(256, 3) void stem_fwd_k(const bf16* __restrict__ x,
                                                      const bf16* __restrict__ wp,
                                                      bf16* __restrict__ y, int N, int D, int H,
                                                      int W, int Do, int Ho, int Wo, int td,
                                                      int th, int tw) {
-    __shared__ __align__(16) bf16 brick[2][kFBD * kFBH * kFBW];
+    constexpr int NWU = (kSWUnits + 255) / 256;       // weight units per thread
+    constexpr int NCH = kFBW / 8;                     // 16-byte chunks per brick row (5)
+    constexpr int NIT = kFBD * kFBH * NCH;            // staging items (1365)
+    constexpr int NI = (NIT + 255) / 256;             // items per thread
+    // rows past kFBD * kFBH take the stores of items past NIT and are never read
+    __shared__ __align__(16) bf16 brick[(NI * 256 + NCH - 1) / NCH * kFBW];
+    __shared__ __align__(16) uint4 wl[NWU * 256];     // units past kSWUnits: unused
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __builtin_assume(tid < 256);
     const int li = lane & 15, kg = lane >> 4;
     int L = blockIdx.x;
     const int twi = L % tw;
@@ -75,48 +91,59 @@ __global__ __launch_bounds__(256, 2) void stem_fwd_k(const bf16* __restrict__ x,
 
     // Staging (W % 8 == 0): brick column c is input column bw + c with
     // bw = 2 w0 - 3 = a0 + 5, a0 a multiple of 8.  A brick row is five
-    // 16-byte chunks; chunk k of copy 0 holds input dwords G[4k + 2 ..] moved
-    // by one bf16 (G = the row's dwords from a0), chunk k of copy 1 the same
-    // one dword further.  Each item loads the two aligned 16-byte groups that
-    // cover it (unconditionally: rows or groups outside the volume load from
-    // a clamped address and are zeroed) and writes both copies.
+    // 16-byte chunks; chunk k holds input dwords G[4k + 2 ..] moved by one
+    // bf16 (G = the row's dwords from a0).  Each item loads the two aligned
+    // 16-byte groups that cover it (rows or groups outside the volume load
+    // from a clamped address and are zeroed).  The weight units and all items
+    // of a thread are loaded before anything is stored.
     {
         const int a0 = bw - 5;
-        constexpr int NCH = kFBW / 8;                     // 5 chunks per row
-        constexpr int NIT = kFBD * kFBH * NCH;            // 1365 items
         const int64_t plane = (int64_t)D * HW;
-#pragma unroll 2
-        for (int it = tid; it < NIT; it += 256) {
+        uint4 wv[NWU];
+#pragma unroll
+        for (int i = 0; i < NWU; ++i) {
+            const int u = tid + 256 * i;
+            wv[i] = reinterpret_cast<const uint4*>(wp)[u < kSWUnits ? u : 0];
+        }
+        uint4 gv[NI][2];
+        uint32_t okm = 0;
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int it = tid + 256 * j;
             const int k = it % NCH, r = it / NCH;
             const int hh = r % kFBH, dd = r / kFBH;
             const int d = bd + dd, h = bh + hh;
-            const bool rok = (unsigned)d < (unsigned)D && (unsigned)h < (unsigned)H;
-            uint32_t g[8];
+            const bool rok = it < NIT && (unsigned)d < (unsigned)D && (unsigned)h < (unsigned)H;
 #pragma unroll
             for (int q = 0; q < 2; ++q) {
                 const int c0 = a0 + 8 * (k + q);
                 const bool ok = rok && c0 >= 0 && c0 < W;
                 const int64_t off = ok ? (int64_t)d * HW + (int64_t)h * W + c0 : 0;
-                const uint4 u = *reinterpret_cast<const uint4*>(xp + (off < plane ? off : 0));
-                g[4 * q + 0] = ok ? u.x : 0u;
-                g[4 * q + 1] = ok ? u.y : 0u;
-                g[4 * q + 2] = ok ? u.z : 0u;
-                g[4 * q + 3] = ok ? u.w : 0u;
+                gv[j][q] = *reinterpret_cast<const uint4*>(xp + (off < plane ? off : 0));
+                okm |= (ok ? 1u : 0u) << (2 * j + q);
             }
-            // brick dword j (columns 2j, 2j + 1) = high half of G[j + 2], low half of G[j + 3]
-            uint32_t o0[4], o1[4];
+        }
+        __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any is used
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                o0[j] = __builtin_amdgcn_alignbit(g[j + 3], g[j + 2], 16);
-                o1[j] = __builtin_amdgcn_alignbit(g[j + 4], g[j + 3], 16);
+        for (int i = 0; i < NWU; ++i) wl[tid + 256 * i] = wv[i];
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int it = tid + 256 * j;
+            const int k = it % NCH, r = it / NCH;
+            uint32_t g[8];
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const bool ok = (okm >> (2 * j + q)) & 1u;
+                g[4 * q + 0] = ok ? gv[j][q].x : 0u;
+                g[4 * q + 1] = ok ? gv[j][q].y : 0u;
+                g[4 * q + 2] = ok ? gv[j][q].z : 0u;
+                g[4 * q + 3] = ok ? gv[j][q].w : 0u;
             }
-            // the last chunk's copy 1 would read past the loaded groups: its
-            // final dword (columns 38, 39 of copy 0 + 2) lies outside the brick
-            if (k == NCH - 1) o1[3] = 0u;
-            bf16* row0 = &brick[0][r * kFBW + 8 * k];
-            bf16* row1 = &brick[1][r * kFBW + 8 * k];
-            *reinterpret_cast<uint4*>(row0) = make_uint4(o0[0], o0[1], o0[2], o0[3]);
-            *reinterpret_cast<uint4*>(row1) = make_uint4(o1[0], o1[1], o1[2], o1[3]);
+            // brick dword m (columns 2m, 2m + 1) = high half of G[m + 2], low half of G[m + 3]
+            uint32_t o[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) o[m] = __builtin_amdgcn_alignbit(g[m + 3], g[m + 2], 16);
+            *reinterpret_cast<uint4*>(&brick[r * kFBW + 8 * k]) = make_uint4(o[0], o[1], o[2], o[3]);
         }
     }
     __syncthreads();
@@ -127,26 +154,24 @@ __global__ __launch_bounds__(256, 2) void stem_fwd_k(const bf16* __restrict__ x,
         acc[i][0] = f32x4{0.f, 0.f, 0.f, 0.f};
         acc[i][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    // operand column start 2*li: copy 0 when li is even (8-byte aligned),
-    // else copy 1 at column 2*li - 2
-    const int copy = li & 1;
-    const int col = 2 * li - 2 * copy;
-#pragma unroll 1
-    for (int ks = 0; ks < kSRowsPad / 4; ++ks) {
+    // operand of output column li: brick columns 2 li .. 2 li + 7, which start
+    // on a 4-byte boundary (rows are 80 bytes)
+#pragma unroll
+    for (int ks = 0; ks < kSKSteps; ++ks) {
         const int r = ks * 4 + kg;
         F16B b[2];
 #pragma unroll
-        for (int ct = 0; ct < 2; ++ct)
-            b[ct].u = *reinterpret_cast<const uint4*>(wp + ((ct * 16 + li) * kSRowsPad + r) * 8);
+        for (int ct = 0; ct < 2; ++ct) b[ct].u = wl[(ks * 2 + ct) * 64 + lane];
         const int rr = r < kSRows ? r : kSRows - 1;  // padding rows: any valid row, zero weights
         const int kd = rr / kSK, kh = rr - kd * kSK;
 #pragma unroll
         for (int rw = 0; rw < 8; ++rw) {
             const int dd = wave * kSS + kd, hh = rw * kSS + kh;
-            const bf16* src = &brick[copy][(dd * kFBH + hh) * kFBW + col];
+            const uint32_t* src =
+                reinterpret_cast<const uint32_t*>(&brick[(dd * kFBH + hh) * kFBW + 2 * li]);
             F16B a;
-            a.h[0] = *reinterpret_cast<const uint2*>(src);
-            a.h[1] = *reinterpret_cast<const uint2*>(src + 4);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) a.w[q] = src[q];
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct)
                 acc[rw][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.b, b[ct].b, acc[rw][ct],
@@ -200,11 +225,17 @@ struct StemWg {
 };
 }  // namespace
 
-__global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
+__global__ __launch_bounds__(256, 3) void stem_wgrad_k(StemWg a) {
     // xs[parity][shift][row][col]: parity plane p holds brick columns 2c + p;
-    // shift 1 is the same plane moved left by one column
+    // shift 1 is the same plane moved left by one column.  dys[ct][step][lane]:
+    // the A operand of each step in MFMA lane order, lane = kg * 16 + li holding
+    // the 8 voxels (d0 + dl, h0 + 2 (step % 4) + (kg >> 1), w0 + 8 (kg & 1) ..)
+    // of channel ct * 16 + li (dl = step / 4)
+    constexpr int kSteps = kGD * kGH / 2;
     __shared__ __align__(16) bf16 xs[2][2][kGBD * kGBH][kGHalf];
+    __shared__ __align__(16) uint4 dys[2 * kSteps * 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __builtin_assume(tid < 256);
     const int li = lane & 15, kg = lane >> 4;
     const int hl_l = kg >> 1, wl = (kg & 1) * 8;
     const int64_t b_beg = (int64_t)blockIdx.x * a.bpr;
@@ -228,72 +259,102 @@ __global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
         const int d0 = tdi * kGD, h0 = thi * kGH, w0 = twi * kGW;
         const int bd = d0 * kSS - kSP, bh = h0 * kSS - kSP, bw = w0 * kSS - kSP;
         const bf16* xp = a.x + (int64_t)n * a.D * HW;
-        // The dy fragments of the brick's steps are requested before the
-        // staging, so their round trip overlaps it and the MFMA loop below
-        // waits for no global load (outside the volume: the plane's first
-        // voxels, zeroed at their use).
-        constexpr int kSteps = kGD * kGH / 2;
-        uint4 dyr[kSteps][2];
-        bool dok[kSteps];
+        // Every load of the brick is issued before the barrier that ends the
+        // previous brick's MFMAs, so the round trip overlaps them.
+        // dy: 32 channels x 2 depths x 8 rows x two 8-voxel halves, unit
+        // u = ((co * 2 + dl) * 8 + hl) * 2 + half; outside the map: zero (the
+        // load reads the plane's first voxels)
+        constexpr int NDU = kSCo * kGD * kGH * 2 / 256;   // dy units per thread (4)
+        uint4 dv[NDU];
+        uint32_t dokm = 0;
 #pragma unroll
-        for (int s = 0; s < kSteps; ++s) {
-            const int dl = s / (kGH / 2);
-            const int hl = (s % (kGH / 2)) * 2 + hl_l;
-            const int d = d0 + dl, h = h0 + hl, w = w0 + wl;
-            dok[s] = d < a.Do && h < a.Ho && w + 8 <= a.Wo;
-            const int64_t vo = dok[s] ? ((int64_t)d * a.Ho + h) * a.Wo + w : 0;
-#pragma unroll
-            for (int ct = 0; ct < 2; ++ct)
-                dyr[s][ct] = *reinterpret_cast<const uint4*>(
-                    a.dy + ((int64_t)n * kSCo + ct * 16 + li) * Vo + vo);
+        for (int i = 0; i < NDU; ++i) {
+            const int u = tid + 256 * i;
+            const int half = u & 1, hl = (u >> 1) & 7, dl = (u >> 4) & 1, co = u >> 5;
+            const int d = d0 + dl, h = h0 + hl, w = w0 + 8 * half;
+            const bool ok = d < a.Do && h < a.Ho && w + 8 <= a.Wo;
+            const int64_t vo = ok ? ((int64_t)d * a.Ho + h) * a.Wo + w : 0;
+            dv[i] = *reinterpret_cast<const uint4*>(a.dy + ((int64_t)n * kSCo + co) * Vo + vo);
+            dokm |= (ok ? 1u : 0u) << i;
         }
-        __syncthreads();
-        // Staging (W % 8 == 0): brick column c is input column a0 + 5 + c
+        // Input staging (W % 8 == 0): brick column c is input column a0 + 5 + c
         // (a0 = bw - 5, a multiple of 8).  With G the row's dwords from a0,
         // plane 0 column cc = high half of G[cc + 2], plane 1 column cc = low
         // half of G[cc + 3]; the shifted copies start one column later.  An
         // item (row, k) builds dwords 4k .. 4k + 3 of the four plane copies
-        // from the three aligned 16-byte groups G[8k .. 8k + 11], loaded
-        // unconditionally (rows or groups outside the volume: clamped address,
-        // zeroed).
-        {
-            const int a0 = bw - 5;
-            constexpr int NIT = kGBD * kGBH * 3;
-            const int64_t plane = (int64_t)a.D * HW;
-#pragma unroll 2
-            for (int it = tid; it < NIT; it += 256) {
-                const int k = it % 3, row = it / 3;
-                const int hh = row % kGBH, dd = row / kGBH;
-                const int d = bd + dd, h = bh + hh;
-                const bool rok = (unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H;
-                uint32_t g[12];
+        // from the three aligned 16-byte groups G[8k .. 8k + 11] (rows or
+        // groups outside the volume: clamped address, zeroed).
+        const int a0 = bw - 5;
+        constexpr int NIT = kGBD * kGBH * 3;
+        constexpr int NI = (NIT + 255) / 256;             // items per thread, at most
+        const int64_t plane = (int64_t)a.D * HW;
+        // G[8k], G[8k + 1] are not used: the first group loads its upper 8 bytes
+        uint2 gv0[NI];
+        uint4 gv[NI][2];
+        uint32_t okm = 0;
 #pragma unroll
-                for (int q = 0; q < 3; ++q) {
-                    const int c0 = a0 + 8 * (2 * k + q);
-                    const bool ok = rok && c0 >= 0 && c0 < a.W;
-                    const int64_t off = ok ? (int64_t)d * HW + (int64_t)h * a.W + c0 : 0;
-                    const uint4 u = *reinterpret_cast<const uint4*>(xp + (off < plane ? off : 0));
-                    g[4 * q + 0] = ok ? u.x : 0u;
-                    g[4 * q + 1] = ok ? u.y : 0u;
-                    g[4 * q + 2] = ok ? u.z : 0u;
-                    g[4 * q + 3] = ok ? u.w : 0u;
-                }
-                // plane dword m = 4k + j uses G[2m + 2 .. 2m + 5] = g[2j + 2 .. 2j + 5]
-                uint32_t p0[4], p1[4], s0[4], s1[4];
+        for (int j = 0; j < NI; ++j) {
+            const int it = tid + 256 * j;
+            const int k = it % 3, row = it / 3;
+            const int hh = row % kGBH, dd = row / kGBH;
+            const int d = bd + dd, h = bh + hh;
+            const bool rok = it < NIT && (unsigned)d < (unsigned)a.D && (unsigned)h < (unsigned)a.H;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const uint32_t a2 = g[2 * j + 2], a3 = g[2 * j + 3], a4 = g[2 * j + 4],
-                                   a5 = g[2 * j + 5];
-                    p0[j] = __builtin_amdgcn_perm(a3, a2, 0x07060302u);  // hi(a2) | hi(a3) << 16
-                    p1[j] = __builtin_amdgcn_perm(a4, a3, 0x05040100u);  // lo(a3) | lo(a4) << 16
-                    s0[j] = __builtin_amdgcn_perm(a4, a3, 0x07060302u);  // hi(a3) | hi(a4) << 16
-                    s1[j] = __builtin_amdgcn_perm(a5, a4, 0x05040100u);  // lo(a4) | lo(a5) << 16
-                }
-                *reinterpret_cast<uint4*>(&xs[0][0][row][8 * k]) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
-                *reinterpret_cast<uint4*>(&xs[1][0][row][8 * k]) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
-                *reinterpret_cast<uint4*>(&xs[0][1][row][8 * k]) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
-                *reinterpret_cast<uint4*>(&xs[1][1][row][8 * k]) = make_uint4(s1[0], s1[1], s1[2], s1[3]);
+            for (int q = 0; q < 3; ++q) {
+                const int c0 = a0 + 8 * (2 * k + q);
+                const bool ok = rok && c0 >= 0 && c0 < a.W;
+                const int64_t off = ok ? (int64_t)d * HW + (int64_t)h * a.W + c0 : 0;
+                const bf16* src = xp + (off < plane ? off : 0);
+                if (q == 0) gv0[j] = reinterpret_cast<const uint2*>(src)[1];
+                else gv[j][q - 1] = *reinterpret_cast<const uint4*>(src);
+                okm |= (ok ? 1u : 0u) << (3 * j + q);
             }
+        }
+        __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any is used
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < NDU; ++i) {
+            const int u = tid + 256 * i;
+            const int half = u & 1, hl = (u >> 1) & 7, dl = (u >> 4) & 1, co = u >> 5;
+            const int step = dl * 4 + (hl >> 1), ul = ((hl & 1) * 2 + half) * 16 + (co & 15);
+            dys[((co >> 4) * kSteps + step) * 64 + ul] =
+                (dokm >> i) & 1u ? dv[i] : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int it = tid + 256 * j;
+            if (it >= NIT) continue;
+            const int k = it % 3, row = it / 3;
+            uint32_t g[12];
+            {
+                const bool ok = okm >> (3 * j) & 1u;
+                g[0] = g[1] = 0u;
+                g[2] = ok ? gv0[j].x : 0u;
+                g[3] = ok ? gv0[j].y : 0u;
+            }
+#pragma unroll
+            for (int q = 1; q < 3; ++q) {
+                const bool ok = (okm >> (3 * j + q)) & 1u;
+                g[4 * q + 0] = ok ? gv[j][q - 1].x : 0u;
+                g[4 * q + 1] = ok ? gv[j][q - 1].y : 0u;
+                g[4 * q + 2] = ok ? gv[j][q - 1].z : 0u;
+                g[4 * q + 3] = ok ? gv[j][q - 1].w : 0u;
+            }
+            // plane dword m = 4k + j uses G[2m + 2 .. 2m + 5] = g[2j + 2 .. 2j + 5]
+            uint32_t p0[4], p1[4], s0[4], s1[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const uint32_t a2 = g[2 * m + 2], a3 = g[2 * m + 3], a4 = g[2 * m + 4],
+                               a5 = g[2 * m + 5];
+                p0[m] = __builtin_amdgcn_perm(a3, a2, 0x07060302u);  // hi(a2) | hi(a3) << 16
+                p1[m] = __builtin_amdgcn_perm(a4, a3, 0x05040100u);  // lo(a3) | lo(a4) << 16
+                s0[m] = __builtin_amdgcn_perm(a4, a3, 0x07060302u);  // hi(a3) | hi(a4) << 16
+                s1[m] = __builtin_amdgcn_perm(a5, a4, 0x05040100u);  // lo(a4) | lo(a5) << 16
+            }
+            *reinterpret_cast<uint4*>(&xs[0][0][row][8 * k]) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
+            *reinterpret_cast<uint4*>(&xs[1][0][row][8 * k]) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
+            *reinterpret_cast<uint4*>(&xs[0][1][row][8 * k]) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
+            *reinterpret_cast<uint4*>(&xs[1][1][row][8 * k]) = make_uint4(s1[0], s1[1], s1[2], s1[3]);
         }
         __syncthreads();
 #pragma unroll
@@ -302,7 +363,7 @@ __global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
             const int hl = (s % (kGH / 2)) * 2 + hl_l;
             F16B av[2];
 #pragma unroll
-            for (int ct = 0; ct < 2; ++ct) av[ct].u = dok[s] ? dyr[s][ct] : make_uint4(0u, 0u, 0u, 0u);
+            for (int ct = 0; ct < 2; ++ct) av[ct].u = dys[(ct * kSteps + s) * 64 + lane];
 #pragma unroll
             for (int j = 0; j < kTilesPerWave; ++j) {
                 const int tile = wave + 4 * j;
@@ -387,7 +448,7 @@ bool stem_ok(const ConvGeom& g, rat3d_dtype dt) {
 size_t stem_fwd_ws() { return (size_t)kSCo * kSRowsPad * 8 * 2; }
 
 static int stem_ranges(int64_t nbricks) {
-    int64_t r = 512;
+    int64_t r = 768;  // three workgroups per CU
     if (r > nbricks) r = nbricks;
     return (int)(r < 1 ? 1 : r);
 }
