@@ -19,8 +19,8 @@
 // 2w - 3 + kw at stride 2, so the input brick is stored split by column
 // parity, each parity plane twice (shifted by one element) so that the 8
 // values start on a 4-byte boundary and load as four aligned 4-byte LDS
-// reads.  Each brick's dy and input loads are all issued before the barrier
-// that frees the LDS, and three workgroups share a CU.
+// reads.  A workgroup walks a range of bricks with the next brick's dy and
+// input loads in flight while the current one is multiplied.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "prof.hpp"
@@ -220,78 +220,77 @@ struct StemWg {
     float* part;  // [ranges][32][kSRows * 8]
     int N, D, H, W, Do, Ho, Wo;
     int td, th, tw;
-    int64_t nbricks;
+    int nbricks;
     int bpr;
 };
 }  // namespace
 
-__global__ __launch_bounds__(256, 3) void stem_wgrad_k(StemWg a) {
-    // xs[parity][shift][row][col]: parity plane p holds brick columns 2c + p;
+__global__ __launch_bounds__(256, 2) void stem_wgrad_k(StemWg a) {
+    // xs: parity plane p holds brick columns 2c + p, rows of kGHalf columns;
     // shift 1 is the same plane moved left by one column.  dys[ct][step][lane]:
     // the A operand of each step in MFMA lane order, lane = kg * 16 + li holding
     // the 8 voxels (d0 + dl, h0 + 2 (step % 4) + (kg >> 1), w0 + 8 (kg & 1) ..)
     // of channel ct * 16 + li (dl = step / 4)
     constexpr int kSteps = kGD * kGH / 2;
-    __shared__ __align__(16) bf16 xs[2][2][kGBD * kGBH][kGHalf];
+    // plane (parity p, shift s) starts at (2 p + s) * kGPlane elements: the
+    // 112-byte pad spreads the B reads of one instruction, whose lanes hit
+    // all four planes, over the LDS banks
+    constexpr int kGPlane = kGBD * kGBH * kGHalf + 56;
+    __shared__ __align__(16) bf16 xs[4 * kGPlane];
     __shared__ __align__(16) uint4 dys[2 * kSteps * 64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar branches
     __builtin_assume(tid < 256);
     const int li = lane & 15, kg = lane >> 4;
     const int hl_l = kg >> 1, wl = (kg & 1) * 8;
-    const int64_t b_beg = (int64_t)blockIdx.x * a.bpr;
-    const int64_t b_end = b_beg + a.bpr < a.nbricks ? b_beg + a.bpr : a.nbricks;
+    const int b_beg = blockIdx.x * a.bpr;
+    const int b_end = b_beg + a.bpr < a.nbricks ? b_beg + a.bpr : a.nbricks;
     const int64_t HW = (int64_t)a.H * a.W, Vo = (int64_t)a.Do * a.Ho * a.Wo;
 
-    f32x4 acc[kTilesPerWave][2];
-#pragma unroll
-    for (int j = 0; j < kTilesPerWave; ++j) {
-        acc[j][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-        acc[j][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-
-    for (int64_t b = b_beg; b < b_end; ++b) {
-        const int twi = (int)(b % a.tw);
-        int64_t r = b / a.tw;
-        const int thi = (int)(r % a.th);
+    // One brick's staging registers: its dy units (thread tid fills the dys
+    // slots tid + 256 i: consecutive lanes, consecutive 16-byte slots) and
+    // its input items.  Input staging (W % 8 == 0): brick column c is input
+    // column a0 + 5 + c (a0 = bw - 5, a multiple of 8).  With G the row's
+    // dwords from a0, plane 0 column cc = high half of G[cc + 2], plane 1
+    // column cc = low half of G[cc + 3]; the shifted copies start one column
+    // later.  An item (row, k) builds dwords 4k .. 4k + 3 of the four plane
+    // copies from the three aligned 16-byte groups G[8k .. 8k + 11], of which
+    // G[8k] and G[8k + 1] are not used.
+    constexpr int NDU = kSCo * kGD * kGH * 2 / 256;   // dy units per thread (4)
+    constexpr int NIT = kGBD * kGBH * 3;
+    constexpr int NI = (NIT + 255) / 256;             // items per thread, at most
+    struct Stage {
+        uint4 dv[NDU];
+        uint2 gv0[NI];
+        uint4 gv[NI][2];
+    };
+    // Buffer loads of the sample's dy and input volumes: an offset past the
+    // end (voxels outside the map, padding) reads zeros.
+    auto issue = [&](int b, Stage& S) {
+        const int twi = b % a.tw;
+        int r = b / a.tw;
+        const int thi = r % a.th;
         r /= a.th;
-        const int tdi = (int)(r % a.td);
-        const int n = (int)(r / a.td);
+        const int tdi = r % a.td;
+        const int n = r / a.td;
         const int d0 = tdi * kGD, h0 = thi * kGH, w0 = twi * kGW;
         const int bd = d0 * kSS - kSP, bh = h0 * kSS - kSP, bw = w0 * kSS - kSP;
-        const bf16* xp = a.x + (int64_t)n * a.D * HW;
-        // Every load of the brick is issued before the barrier that ends the
-        // previous brick's MFMAs, so the round trip overlaps them.
-        // dy: 32 channels x 2 depths x 8 rows x two 8-voxel halves, unit
-        // u = ((co * 2 + dl) * 8 + hl) * 2 + half; outside the map: zero (the
-        // load reads the plane's first voxels)
-        constexpr int NDU = kSCo * kGD * kGH * 2 / 256;   // dy units per thread (4)
-        uint4 dv[NDU];
-        uint32_t dokm = 0;
+        const __amdgpu_buffer_rsrc_t dyr =
+            buf_rsrc_u(a.dy + (int64_t)n * kSCo * Vo, (uint32_t)(kSCo * Vo * 2));
+        const __amdgpu_buffer_rsrc_t xr =
+            buf_rsrc_u(a.x + (int64_t)n * a.D * HW, (uint32_t)(a.D * HW * 2));
 #pragma unroll
         for (int i = 0; i < NDU; ++i) {
             const int u = tid + 256 * i;
-            const int half = u & 1, hl = (u >> 1) & 7, dl = (u >> 4) & 1, co = u >> 5;
-            const int d = d0 + dl, h = h0 + hl, w = w0 + 8 * half;
+            const int ul = u & 63, step = (u >> 6) & 7, co = (u >> 9) * 16 + (ul & 15);
+            const int ukg = ul >> 4, dl = step >> 2, hl = (step & 3) * 2 + (ukg >> 1);
+            const int d = d0 + dl, h = h0 + hl, w = w0 + 8 * (ukg & 1);
             const bool ok = d < a.Do && h < a.Ho && w + 8 <= a.Wo;
-            const int64_t vo = ok ? ((int64_t)d * a.Ho + h) * a.Wo + w : 0;
-            dv[i] = *reinterpret_cast<const uint4*>(a.dy + ((int64_t)n * kSCo + co) * Vo + vo);
-            dokm |= (ok ? 1u : 0u) << i;
+            const uint32_t vo =
+                ok ? (uint32_t)((co * Vo + ((int64_t)d * a.Ho + h) * a.Wo + w) * 2) : 0x80000000u;
+            S.dv[i] = buf_ld16(dyr, vo, 0);
         }
-        // Input staging (W % 8 == 0): brick column c is input column a0 + 5 + c
-        // (a0 = bw - 5, a multiple of 8).  With G the row's dwords from a0,
-        // plane 0 column cc = high half of G[cc + 2], plane 1 column cc = low
-        // half of G[cc + 3]; the shifted copies start one column later.  An
-        // item (row, k) builds dwords 4k .. 4k + 3 of the four plane copies
-        // from the three aligned 16-byte groups G[8k .. 8k + 11] (rows or
-        // groups outside the volume: clamped address, zeroed).
         const int a0 = bw - 5;
-        constexpr int NIT = kGBD * kGBH * 3;
-        constexpr int NI = (NIT + 255) / 256;             // items per thread, at most
-        const int64_t plane = (int64_t)a.D * HW;
-        // G[8k], G[8k + 1] are not used: the first group loads its upper 8 bytes
-        uint2 gv0[NI];
-        uint4 gv[NI][2];
-        uint32_t okm = 0;
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int it = tid + 256 * j;
@@ -303,43 +302,24 @@ __global__ __launch_bounds__(256, 3) void stem_wgrad_k(StemWg a) {
             for (int q = 0; q < 3; ++q) {
                 const int c0 = a0 + 8 * (2 * k + q);
                 const bool ok = rok && c0 >= 0 && c0 < a.W;
-                const int64_t off = ok ? (int64_t)d * HW + (int64_t)h * a.W + c0 : 0;
-                const bf16* src = xp + (off < plane ? off : 0);
-                if (q == 0) gv0[j] = reinterpret_cast<const uint2*>(src)[1];
-                else gv[j][q - 1] = *reinterpret_cast<const uint4*>(src);
-                okm |= (ok ? 1u : 0u) << (3 * j + q);
+                const uint32_t xo = ok ? (uint32_t)((d * HW + h * a.W + c0) * 2) : 0x80000000u;
+                if (q == 0) S.gv0[j] = buf_ld8(xr, xo, 8);
+                else S.gv[j][q - 1] = buf_ld16(xr, xo, 0);
             }
         }
-        __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any is used
-        __syncthreads();
+    };
+    // The staged brick into LDS (no brick coordinates needed).
+    auto commit = [&](const Stage& S) {
 #pragma unroll
-        for (int i = 0; i < NDU; ++i) {
-            const int u = tid + 256 * i;
-            const int half = u & 1, hl = (u >> 1) & 7, dl = (u >> 4) & 1, co = u >> 5;
-            const int step = dl * 4 + (hl >> 1), ul = ((hl & 1) * 2 + half) * 16 + (co & 15);
-            dys[((co >> 4) * kSteps + step) * 64 + ul] =
-                (dokm >> i) & 1u ? dv[i] : make_uint4(0u, 0u, 0u, 0u);
-        }
+        for (int i = 0; i < NDU; ++i) dys[tid + 256 * i] = S.dv[i];
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
             const int it = tid + 256 * j;
             if (it >= NIT) continue;
             const int k = it % 3, row = it / 3;
-            uint32_t g[12];
-            {
-                const bool ok = okm >> (3 * j) & 1u;
-                g[0] = g[1] = 0u;
-                g[2] = ok ? gv0[j].x : 0u;
-                g[3] = ok ? gv0[j].y : 0u;
-            }
-#pragma unroll
-            for (int q = 1; q < 3; ++q) {
-                const bool ok = (okm >> (3 * j + q)) & 1u;
-                g[4 * q + 0] = ok ? gv[j][q - 1].x : 0u;
-                g[4 * q + 1] = ok ? gv[j][q - 1].y : 0u;
-                g[4 * q + 2] = ok ? gv[j][q - 1].z : 0u;
-                g[4 * q + 3] = ok ? gv[j][q - 1].w : 0u;
-            }
+            const uint32_t g[12] = {0u, 0u, S.gv0[j].x, S.gv0[j].y,
+                                    S.gv[j][0].x, S.gv[j][0].y, S.gv[j][0].z, S.gv[j][0].w,
+                                    S.gv[j][1].x, S.gv[j][1].y, S.gv[j][1].z, S.gv[j][1].w};
             // plane dword m = 4k + j uses G[2m + 2 .. 2m + 5] = g[2j + 2 .. 2j + 5]
             uint32_t p0[4], p1[4], s0[4], s1[4];
 #pragma unroll
@@ -351,12 +331,22 @@ __global__ __launch_bounds__(256, 3) void stem_wgrad_k(StemWg a) {
                 s0[m] = __builtin_amdgcn_perm(a4, a3, 0x07060302u);  // hi(a3) | hi(a4) << 16
                 s1[m] = __builtin_amdgcn_perm(a5, a4, 0x05040100u);  // lo(a4) | lo(a5) << 16
             }
-            *reinterpret_cast<uint4*>(&xs[0][0][row][8 * k]) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
-            *reinterpret_cast<uint4*>(&xs[1][0][row][8 * k]) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
-            *reinterpret_cast<uint4*>(&xs[0][1][row][8 * k]) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
-            *reinterpret_cast<uint4*>(&xs[1][1][row][8 * k]) = make_uint4(s1[0], s1[1], s1[2], s1[3]);
+            bf16* const xr = &xs[row * kGHalf + 8 * k];
+            *reinterpret_cast<uint4*>(xr) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
+            *reinterpret_cast<uint4*>(xr + 2 * kGPlane) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
+            *reinterpret_cast<uint4*>(xr + kGPlane) = make_uint4(s0[0], s0[1], s0[2], s0[3]);
+            *reinterpret_cast<uint4*>(xr + 3 * kGPlane) = make_uint4(s1[0], s1[1], s1[2], s1[3]);
         }
-        __syncthreads();
+    };
+
+    f32x4 acc[kTilesPerWave][2];
+#pragma unroll
+    for (int j = 0; j < kTilesPerWave; ++j) {
+        acc[j][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+        acc[j][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    auto compute = [&]() {
 #pragma unroll
         for (int s = 0; s < kSteps; ++s) {
             const int dl = s / (kGH / 2);
@@ -364,10 +354,14 @@ __global__ __launch_bounds__(256, 3) void stem_wgrad_k(StemWg a) {
             F16B av[2];
 #pragma unroll
             for (int ct = 0; ct < 2; ++ct) av[ct].u = dys[(ct * kSteps + s) * 64 + lane];
+            // tiles wave + 4 j: all exist for j < kTilesPerWave - 1, the last
+            // only for the waves below kTapTiles % 4 (one wave-uniform branch)
+            const int nj = wave + 4 * (kTilesPerWave - 1) < kTapTiles ? kTilesPerWave
+                                                                     : kTilesPerWave - 1;
 #pragma unroll
             for (int j = 0; j < kTilesPerWave; ++j) {
+                if (j == kTilesPerWave - 1 && j >= nj) break;
                 const int tile = wave + 4 * j;
-                if (tile >= kTapTiles) continue;
                 // this lane's B column: padded tap t = tile*16 + li
                 const int t = tile * 16 + li;
                 const int rrow = t >> 3, kw = t & 7;
@@ -382,8 +376,9 @@ __global__ __launch_bounds__(256, 3) void stem_wgrad_k(StemWg a) {
                     // = parity kw & 1, plane column wl + i + (kw >> 1)
                     const int start = wl + (kwc >> 1);
                     const int sh = start & 1;
-                    const bf16* src =
-                        &xs[kwc & 1][sh][(dl * kSS + kd) * kGBH + hl * kSS + kh][start - sh];
+                    const bf16* src = &xs[((kwc & 1) * 2 + sh) * kGPlane +
+                                          ((dl * kSS + kd) * kGBH + hl * kSS + kh) * kGHalf +
+                                          start - sh];
 #pragma unroll
                     for (int q = 0; q < 4; ++q) bv.w[q] = reinterpret_cast<const uint32_t*>(src)[q];
                 }
@@ -393,6 +388,18 @@ __global__ __launch_bounds__(256, 3) void stem_wgrad_k(StemWg a) {
                                                                         acc[j][ct], 0, 0, 0);
             }
         }
+    };
+
+    // Software pipeline: brick b + 1's loads are issued right after brick b
+    // is written to LDS, so their round trip overlaps brick b's MFMAs.
+    Stage S;
+    if (b_beg < b_end) issue(b_beg, S);
+    for (int b = b_beg; b < b_end; ++b) {
+        __syncthreads();  // every wave is done reading the previous brick
+        commit(S);
+        if (b + 1 < b_end) issue(b + 1, S);
+        __syncthreads();
+        compute();
     }
 
     float* out = a.part + (int64_t)blockIdx.x * kSCo * kSRows * 8;
@@ -448,7 +455,7 @@ bool stem_ok(const ConvGeom& g, rat3d_dtype dt) {
 size_t stem_fwd_ws() { return (size_t)kSCo * kSRowsPad * 8 * 2; }
 
 static int stem_ranges(int64_t nbricks) {
-    int64_t r = 768;  // three workgroups per CU
+    int64_t r = 512;  // two workgroups per CU
     if (r > nbricks) r = nbricks;
     return (int)(r < 1 ? 1 : r);
 }
@@ -457,7 +464,12 @@ static int64_t stem_bricks(const ConvGeom& g) {
     return (int64_t)g.N * ceil_div(g.Do, kGD) * ceil_div(g.Ho, kGH) * ceil_div(g.Wo, kGW);
 }
 
-bool stem_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) { return stem_ok(g, dt) && g.Wo % 8 == 0; }
+bool stem_wgrad_ok(const ConvGeom& g, rat3d_dtype dt) {
+    // one sample's dy and input volumes are addressed with 32-bit byte offsets
+    return stem_ok(g, dt) && g.Wo % 8 == 0 &&
+           (int64_t)kSCo * g.Do * g.Ho * g.Wo * 2 < (1LL << 31) &&
+           (int64_t)g.D * g.H * g.W * 2 < (1LL << 31) && stem_bricks(g) < (1LL << 31);
+}
 
 size_t stem_wgrad_ws(const ConvGeom& g) {
     return (size_t)stem_ranges(stem_bricks(g)) * kSCo * kSRows * 8 * sizeof(float);
