@@ -294,7 +294,8 @@ void rat3d_net_destroy(rat3d_net* net);
 size_t rat3d_net_param_count(const rat3d_net* net);
 
 /* Bytes of workspace: saved activations, activation gradients, bf16 weight
- * copies, BN statistics and scratch. */
+ * copies, BN statistics and scratch (PARTITION1 with several micro-batches:
+ * two copies of the per-micro-batch part, see rat3d_train_step). */
 size_t rat3d_net_workspace_size(const rat3d_net* net);
 
 /* Number of parameter tensors, and the i-th one's name, arena offset
@@ -312,9 +313,16 @@ rat3d_status rat3d_net_tensor_info(const rat3d_net* net, int i, const char** nam
 /* Binds the caller's device buffers: params and grads (float32 arenas) and
  * the workspace.  Also resets BN running statistics (mean 0, var 1) when the
  * kernels next run: the reset is enqueued by the next call that takes a
- * stream. */
+ * stream.  PARTITION1 with several micro-batches: the first bind also creates
+ * the network's forward stream (default priority) and five events, released
+ * by rat3d_net_destroy; RAT3D_EHIP if the runtime refuses them. */
 rat3d_status rat3d_net_bind(rat3d_net* net, float* params, float* grads, void* ws,
                             size_t ws_bytes);
+
+/* PARTITION1: whether rat3d_train_step overlaps micro-batches (enable != 0,
+ * the default) or runs every kernel on the caller's stream in order
+ * (enable == 0, for per-kernel timing).  Both give bit-identical results. */
+rat3d_status rat3d_net_set_overlap(rat3d_net* net, int enable);
 
 /* RESUNIT / ATTN: forward on x (input shape), backward from dy (output
  * shape); writes y, dx and the gradient arena (overwritten).  No update. */
@@ -324,8 +332,14 @@ rat3d_status rat3d_block_fwd_bwd(rat3d_net* net, const void* x, const void* dy, 
 /* RESATTNET: x [n][1][d][h][w], labels int32 [n]; dy_upstream unused.
  * PARTITION1: x [micro_batches*n][1][d][h][w], dy_upstream [micro_batches*n]
  * [c][d/2][h/2][w/2]; labels unused.
- * One training step: gradients (overwritten, then summed over micro-batches)
- * and params -= lr * grads.  loss_dev (nullable, RESATTNET) receives the loss. */
+ * One training step: gradients (overwritten, then summed over micro-batches
+ * in order) and params -= lr * grads.  loss_dev (nullable, RESATTNET)
+ * receives the loss.  PARTITION1 with overlap on: micro-batch k + 1's forward
+ * runs on the network's own stream while micro-batch k's backward runs on
+ * `stream`, in two alternating copies of the saved activations (the last
+ * micro-batch in the copy rat3d_net_tensor_info describes); the caller's
+ * stream waits for all of it, so work enqueued after the call sees the
+ * update. */
 rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labels,
                               const void* dy_upstream, float* loss_dev, void* stream);
 
@@ -359,8 +373,8 @@ rat3d_status rat3d_gradcam(rat3d_net* net, const void* x, const int32_t* classes
  * micro-batch; the gradient arena is overwritten (accumulate == 0) or added
  * to (accumulate != 0).  No update: rat3d_net_update applies it.  The saved
  * activations and gradients in the workspace are those of this micro-batch.
- * rat3d_train_step runs exactly these calls (accumulate = 0 for the first
- * micro-batch, 1 after), then rat3d_net_update. */
+ * rat3d_train_step computes exactly these calls (accumulate = 0 for the
+ * first micro-batch, 1 after), then rat3d_net_update. */
 rat3d_status rat3d_partition_micro_batch(rat3d_net* net, const void* x, const void* dy_upstream,
                                          int accumulate, void* stream);
 

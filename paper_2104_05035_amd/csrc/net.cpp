@@ -1,6 +1,10 @@
 // Composite blocks and the training step: a host-side plan (parameter arena
 // and workspace layout) plus an executor that enqueues the kernels of the
-// forward pass, the backward pass and the SGD update on one stream.
+// forward pass, the backward pass and the SGD update on the caller's stream.
+// The partition's training step over several micro-batches also uses a
+// stream of its own: micro-batch k + 1's forward runs there while
+// micro-batch k's backward runs on the caller's stream, each micro-batch in
+// one of two copies of the activation region (see train_partition).
 //
 // Graph readings (the paper names conv blocks, residual layers and a
 // self-attention layer but leaves their wiring open):
@@ -123,6 +127,19 @@ struct rat3d_net {
     void* ext_y = nullptr;
     void* ext_dx = nullptr;
     const void* ext_dy = nullptr;
+    // PARTITION1 with several micro-batches: a second activation context (the
+    // graph region [0, graph_bytes) again at graph_bytes, with its own
+    // scratch), the forward stream and the events that order the two
+    size_t graph_bytes = 0;
+    size_t conv_scr_off1 = 0, bn_scr_off1 = 0, bn_scr2_off1 = 0;
+    bool overlap = true;
+    hipStream_t fwd_stream = nullptr;
+    hipEvent_t ev_prep = nullptr, ev_fwd[2] = {nullptr, nullptr}, ev_bwd[2] = {nullptr, nullptr};
+    ~rat3d_net() {
+        if (fwd_stream) hipStreamDestroy(fwd_stream);
+        for (hipEvent_t e : {ev_prep, ev_fwd[0], ev_fwd[1], ev_bwd[0], ev_bwd[1]})
+            if (e) hipEventDestroy(e);
+    }
 };
 
 namespace {
@@ -281,14 +298,21 @@ struct Exec {
     rat3d_net* n;
     hipStream_t st;
     int acc;  // accumulate parameter gradients (micro-batches after the first)
+    // activation context: 0, or 1 for the second copy of the graph region
+    // (per-micro-batch tensors, BN statistics, masks and scratch)
+    int ctx = 0;
+    // the call's input and output gradient (null: the net's)
+    const void* x_in = nullptr;
+    const void* dy_in = nullptr;
 
+    int64_t shift() const { return ctx ? (int64_t)n->graph_bytes : 0; }
     void* p(int64_t off) const {
         switch (off) {
-            case kExtX: return const_cast<void*>(n->ext_x);
+            case kExtX: return const_cast<void*>(x_in ? x_in : n->ext_x);
             case kExtY: return n->ext_y;
             case kExtDx: return n->ext_dx;
-            case kExtDy: return const_cast<void*>(n->ext_dy);
-            default: return n->ws + off;
+            case kExtDy: return const_cast<void*>(dy_in ? dy_in : n->ext_dy);
+            default: return n->ws + off + shift();
         }
     }
     void* a(const TRef& t) const { return p(t.off); }
@@ -299,12 +323,12 @@ struct Exec {
     }
     float* par(size_t off) const { return n->P + off; }
     float* grd(size_t off) const { return n->G + off; }
-    void* conv_scr() const { return n->ws + n->conv_scr_off; }
-    void* bn_scr() const { return n->ws + n->bn_scr_off; }
-    void* bn_scr2() const { return n->ws + n->bn_scr2_off; }
-    float* mean(const BnL& b) const { return (float*)(n->ws + b.stat_off); }
-    float* invstd(const BnL& b) const { return (float*)(n->ws + b.stat_off) + b.c; }
-    float* fcoef(const BnL& b) const { return (float*)(n->ws + b.stat_off) + 2 * b.c; }
+    void* conv_scr() const { return n->ws + (ctx ? n->conv_scr_off1 : n->conv_scr_off); }
+    void* bn_scr() const { return n->ws + (ctx ? n->bn_scr_off1 : n->bn_scr_off); }
+    void* bn_scr2() const { return n->ws + (ctx ? n->bn_scr2_off1 : n->bn_scr2_off); }
+    float* mean(const BnL& b) const { return (float*)(n->ws + b.stat_off + shift()); }
+    float* invstd(const BnL& b) const { return mean(b) + b.c; }
+    float* fcoef(const BnL& b) const { return mean(b) + 2 * b.c; }
     float* rmean(const BnL& b) const { return (float*)(n->ws + n->run_mean_off) + b.run_idx; }
     float* rvar(const BnL& b) const { return (float*)(n->ws + n->run_var_off) + b.run_idx; }
 
@@ -346,7 +370,9 @@ struct Exec {
                       par(b.g_off), mean(b), invstd(b), fcoef(b), dx, nullptr, 0, grd(b.g_off),
                       grd(b.b_off), acc, bn_scr(), st);
     }
-    uint8_t* bits(int64_t off) const { return off >= 0 ? (uint8_t*)(n->ws + off) : nullptr; }
+    uint8_t* bits(int64_t off) const {
+        return off >= 0 ? (uint8_t*)(n->ws + off + shift()) : nullptr;
+    }
 };
 
 #define RAT3D_TRY(expr)                       \
@@ -492,7 +518,7 @@ rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
 
 rat3d_status stem_fwd(const Exec& e, bool pool) {
     rat3d_net* n = e.n;
-    RAT3D_TRY(e.conv_f(n->stem_conv, n->ext_x, e.a(n->stem_h)));
+    RAT3D_TRY(e.conv_f(n->stem_conv, e.p(kExtX), e.a(n->stem_h)));
     RAT3D_TRY(e.bn_f(n->stem_bn, n->stem_h, nullptr, 1, e.a(n->stem_a)));
     if (!pool) return RAT3D_OK;
     const Shape& s = n->stem_a.s;
@@ -508,7 +534,7 @@ rat3d_status stem_bwd(const Exec& e, bool pool) {
                            (const uint8_t*)e.p(n->stem_am), e.g(n->stem_a), 0, e.st));
     }
     RAT3D_TRY(e.bn_bwd_x(n->stem_bn, e.g(n->stem_a), n->stem_h, e.g(n->stem_h)));
-    return e.conv_w(n->stem_conv, n->ext_x, e.g(n->stem_h));
+    return e.conv_w(n->stem_conv, e.p(kExtX), e.g(n->stem_h));
 }
 
 // ------------------------------------------------------------ inference mode
@@ -649,21 +675,81 @@ rat3d_status prepare_call(rat3d_net* n, hipStream_t st) {
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 // One micro-batch of the first-stage partition: forward from x, backward from
-// the gradient received at the partition's output; parameter gradients are
-// written (acc = 0) or added (acc = 1).  The weights must be prepared.
-rat3d_status partition_micro_batch(rat3d_net* net, const void* x, const void* dy, int acc,
-                                   hipStream_t st) {
-    const AMPlan& am = net->ams[0];
-    net->ext_x = x;
-    // the partition's output gradient arrives from the next partition
-    net->ext_dy = dy;
-    Exec e{net, st, acc};
+// the gradient received at the partition's output (it arrives from the next
+// partition); parameter gradients are written (acc = 0) or added (acc = 1).
+// The weights must be prepared.
+rat3d_status partition_fwd(const Exec& e) {
+    rat3d_net* net = e.n;
     RAT3D_TRY(stem_fwd(e, false));
     RAT3D_TRY(ru_fwd(e, net->rus[0]));
-    RAT3D_TRY(am_fwd(e, am));
-    RAT3D_TRY(am_bwd(e, am));
+    return am_fwd(e, net->ams[0]);
+}
+rat3d_status partition_bwd(const Exec& e) {
+    rat3d_net* net = e.n;
+    RAT3D_TRY(am_bwd(e, net->ams[0]));
     RAT3D_TRY(ru_bwd(e, net->rus[0], false));
     return stem_bwd(e, false);
+}
+rat3d_status partition_micro_batch(rat3d_net* net, const void* x, const void* dy, int acc,
+                                   hipStream_t st) {
+    Exec e{net, st, acc};
+    e.x_in = x;
+    e.dy_in = dy;
+    RAT3D_TRY(partition_fwd(e));
+    return partition_bwd(e);
+}
+
+bool hip_ok(hipError_t r, const char* what) {
+    if (r == hipSuccess) return true;
+    set_error("rat3d_train_step: %s failed (%s)", what, hipGetErrorString(r));
+    return false;
+}
+
+// The partition's step over M micro-batches.  Micro-batch k runs in context
+// (M - 1 - k) % 2 (the last one in context 0, whose tensors
+// rat3d_net_tensor_info describes); its forward is enqueued on the net's
+// forward stream and its backward on the caller's stream st:
+//   forward k      waits for the weight preparation (k = 0) and for the
+//                  backward of micro-batch k - 2 (the same context);
+//   backward k     waits for forward k and follows backward k - 1 on st.
+// So micro-batch k + 1's forward runs while micro-batch k's backward does.
+// The two share only read-only data (weights, the prepared layouts) and the
+// BN running statistics, which only the forwards update, in order; parameter
+// gradients are formed by the backwards alone, in order.  Every forward is
+// done before the last backward starts, so the caller's stream covers the
+// whole step.
+rat3d_status train_partition(rat3d_net* net, const char* x, const char* dy, size_t x_bytes,
+                             size_t dy_bytes, hipStream_t st) {
+    const int M = net->d.micro_batches;
+    if (!net->fwd_stream || !net->overlap || M < 2) {
+        for (int k = 0; k < M; ++k)
+            RAT3D_TRY(partition_micro_batch(net, x + k * x_bytes, dy + k * dy_bytes, k > 0 ? 1 : 0,
+                                            st));
+        return RAT3D_OK;
+    }
+    hipStream_t fs = net->fwd_stream;
+    if (!hip_ok(hipEventRecord(net->ev_prep, st), "event record") ||
+        !hip_ok(hipStreamWaitEvent(fs, net->ev_prep, 0), "stream wait"))
+        return RAT3D_EHIP;
+    for (int k = 0; k < M; ++k) {
+        const int c = (M - 1 - k) % 2;
+        Exec f{net, fs, 0};
+        f.ctx = c;
+        f.x_in = x + k * x_bytes;
+        if (k >= 2 && !hip_ok(hipStreamWaitEvent(fs, net->ev_bwd[c], 0), "stream wait"))
+            return RAT3D_EHIP;
+        RAT3D_TRY(partition_fwd(f));
+        if (!hip_ok(hipEventRecord(net->ev_fwd[c], fs), "event record") ||
+            !hip_ok(hipStreamWaitEvent(st, net->ev_fwd[c], 0), "stream wait"))
+            return RAT3D_EHIP;
+        Exec b{net, st, k > 0 ? 1 : 0};
+        b.ctx = c;
+        b.x_in = f.x_in;
+        b.dy_in = dy + k * dy_bytes;
+        RAT3D_TRY(partition_bwd(b));
+        if (!hip_ok(hipEventRecord(net->ev_bwd[c], st), "event record")) return RAT3D_EHIP;
+    }
+    return RAT3D_OK;
 }
 
 }  // namespace
@@ -764,11 +850,20 @@ rat3d_status rat3d_net_create(const rat3d_net_desc* desc, rat3d_net** out) {
         set_error("rat3d_net_create: invalid kind or channel counts");
         return RAT3D_EINVAL;
     }
+    // the partition's second activation context: the graph region again
+    n->graph_bytes = (b.top + 255) & ~(size_t)255;
+    const bool two_ctx = d.kind == RAT3D_NET_PARTITION1 && mb > 1;
+    if (two_ctx) b.top = 2 * n->graph_bytes;
     // fixed regions
     if (n->dt == RAT3D_BF16) n->mirror_off = b.alloc(n->param_count * 2);
     n->conv_scr_off = b.alloc(n->conv_scr_bytes);
     n->bn_scr_off = b.alloc(n->bn_scr_bytes);
     n->bn_scr2_off = b.alloc(n->bn_scr_bytes);  // a second BN's partials (projection skip)
+    if (two_ctx) {
+        n->conv_scr_off1 = b.alloc(n->conv_scr_bytes);
+        n->bn_scr_off1 = b.alloc(n->bn_scr_bytes);
+        n->bn_scr2_off1 = b.alloc(n->bn_scr_bytes);
+    }
     n->head_scr_off = b.alloc(head_ws_bytes(d.n, 256, 2));
     n->run_mean_off = b.alloc(n->run_count * sizeof(float));
     n->run_var_off = b.alloc(n->run_count * sizeof(float));
@@ -839,10 +934,31 @@ rat3d_status rat3d_net_bind(rat3d_net* net, float* params, float* grads, void* w
         set_error("rat3d_net_bind: arenas must be 16-byte and the workspace 256-byte aligned");
         return RAT3D_EALIGN;
     }
+    if (net->conv_scr_off1 && !net->fwd_stream) {
+        // the partition's forward stream (default priority) and its events
+        hipError_t r = hipStreamCreateWithFlags(&net->fwd_stream, hipStreamNonBlocking);
+        for (hipEvent_t* e : {&net->ev_prep, &net->ev_fwd[0], &net->ev_fwd[1], &net->ev_bwd[0],
+                              &net->ev_bwd[1]})
+            if (r == hipSuccess) r = hipEventCreateWithFlags(e, hipEventDisableTiming);
+        if (r != hipSuccess) {
+            set_error("rat3d_net_bind: stream or event creation failed (%s)",
+                      hipGetErrorString(r));
+            return RAT3D_EHIP;
+        }
+    }
     net->P = params;
     net->G = grads;
     net->ws = (char*)ws;
     net->reset_running = true;
+    return RAT3D_OK;
+}
+
+rat3d_status rat3d_net_set_overlap(rat3d_net* net, int enable) {
+    if (!net) {
+        set_error("rat3d_net_set_overlap: NULL network");
+        return RAT3D_EINVAL;
+    }
+    net->overlap = enable != 0;
     return RAT3D_OK;
 }
 
@@ -922,10 +1038,8 @@ rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labe
         }
     } else {
         const size_t dy_bytes = (size_t)net->ams[0].out.s.count() * net->esz;
-        for (int mb = 0; mb < d.micro_batches; ++mb)
-            RAT3D_TRY(partition_micro_batch(net, (const char*)x + mb * x_bytes,
-                                            (const char*)dy_upstream + mb * dy_bytes,
-                                            mb > 0 ? 1 : 0, st));
+        RAT3D_TRY(train_partition(net, (const char*)x, (const char*)dy_upstream, x_bytes,
+                                  dy_bytes, st));
     }
     return sgd_update((int64_t)net->param_count, d.lr, net->P, net->G, st);
 }

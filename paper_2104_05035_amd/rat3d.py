@@ -108,6 +108,7 @@ _SIGS = {
                                    ctypes.POINTER(_SZ), ctypes.POINTER(_I),
                                    ctypes.POINTER(_I * 5)]),
     "rat3d_net_bind": (_I, [_VP, _VP, _VP, _VP, _SZ]),
+    "rat3d_net_set_overlap": (_I, [_VP, _I]),
     "rat3d_block_fwd_bwd": (_I, [_VP] * 6),
     "rat3d_train_step": (_I, [_VP] * 6),
     "rat3d_partition_micro_batch": (_I, [_VP, _VP, _VP, _I, _VP]),
@@ -398,6 +399,9 @@ class Net:
 
     def rat3d_net_bind(self, params, grads, ws, ws_bytes):
         _check(lib().rat3d_net_bind(self.h, _p(params), _p(grads), _p(ws), ws_bytes))
+
+    def rat3d_net_set_overlap(self, enable):
+        _check(lib().rat3d_net_set_overlap(self.h, int(enable)))
 
     def rat3d_block_fwd_bwd(self, x, dy, y, dx, stream=None):
         _check(lib().rat3d_block_fwd_bwd(self.h, _p(x), _p(dy), _p(y), _p(dx), _stream(stream)))

@@ -115,13 +115,21 @@ def partition_replayed(n, mb, d, h, w, c, seed, verbose=True):
     U.sync()
     new = B.new_params()
     check_sgd(old, new, G, 1e-4)
-    # the same step through rat3d_train_step: bit-identical results
+    # the same step through rat3d_train_step: bit-identical results, with
+    # micro-batches overlapped (the default) and with every kernel on one
+    # stream; the last micro-batch's tensors are where rat3d_net_tensor_info
+    # says they are
     G1, P1 = B.G.clone(), B.P.clone()
-    B.reset_params()
-    B.net.rat3d_train_step(x, None, dy, None)
-    U.sync()
-    assert torch.equal(B.G, G1) and torch.equal(B.P, P1), \
-        "rat3d_train_step differs from its micro-batch calls"
+    for overlap in (1, 0):
+        B.net.rat3d_net_set_overlap(overlap)
+        B.reset_params()
+        B.net.rat3d_train_step(x, None, dy, None)
+        U.sync()
+        assert torch.equal(B.G, G1) and torch.equal(B.P, P1), \
+            "rat3d_train_step (overlap %d) differs from its micro-batch calls" % overlap
+        assert np.array_equal(B.tensor("am.out"), out_last), \
+            "rat3d_train_step (overlap %d): last micro-batch output not in place" % overlap
+    B.net.rat3d_net_set_overlap(1)
     _, Gref, info = onet.train_step("partition1", old, 1e-4, True, x=xr, dy=dyr,
                                     micro_batches=mb)
     r = U.rel(out_last, info["y"][-1])
