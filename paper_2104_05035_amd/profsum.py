@@ -43,9 +43,14 @@ def stats(csv_path, bench_log, out, title, cmd):
              "Workload: %s; bf16 storage, fp32 accumulation." % work, "",
              "Command (repository root, one MI355X):", "", "    " + cmd, ""]
     if "roofline" in b:
-        lines += ["Calls cover 1 warm-up, 3 breakdown and 3 timed steps.  Dominant kernel per "
-                  "bench.py's live hipEvents: `%s`, %.1f us/launch (rocprofv3 average in the "
-                  "table)." % (b["roofline"]["kernel"], b["roofline"]["avg_launch_us"]), ""]
+        wu, bk, ts = b.get("warmup", 1), b.get("breakdown_steps", 3), b.get("steps", 3)
+        sched = ("all of them with micro-batches not overlapped, like the step whose launches "
+                 "the live timing brackets" if wu == 0 and ts == 1 else
+                 "the warm-up and all timed steps but the last overlap micro-batches")
+        lines += ["Calls cover %d warm-up, %d breakdown and %d timed steps, %s.  Dominant kernel "
+                  "per bench.py's live hipEvents: `%s`, %.1f us/launch (rocprofv3 average in the "
+                  "table)." % (wu, bk, ts, sched, b["roofline"]["kernel"],
+                               b["roofline"]["avg_launch_us"]), ""]
     else:
         lines += ["Calls cover 1 warm-up, 1 profiled (tagged) and 3 timed steps.", ""]
     lines += ["| kernel | calls | total ms | avg us | % |", "|---|---|---|---|---|"]
