@@ -132,13 +132,22 @@ struct rat3d_net {
     // scratch), the forward stream and the events that order the two
     size_t graph_bytes = 0;
     size_t conv_scr_off1 = 0, bn_scr_off1 = 0, bn_scr2_off1 = 0;
+    // scratch of the attention modules' mask branches, per context, when
+    // they run on a stream of their own (see am_fwd)
+    size_t mask_conv_scr[2] = {0, 0}, mask_bn_scr[2] = {0, 0}, mask_bn_scr2[2] = {0, 0};
     bool overlap = true;
     hipStream_t fwd_stream = nullptr;
+    // mask-branch streams of the forward and of the backward, with the
+    // events that fork and join them
+    hipStream_t mask_stream[2] = {nullptr, nullptr};
     hipEvent_t ev_prep = nullptr, ev_fwd[2] = {nullptr, nullptr}, ev_bwd[2] = {nullptr, nullptr};
+    hipEvent_t ev_fork[2] = {nullptr, nullptr}, ev_join[2] = {nullptr, nullptr};
     ~rat3d_net() {
-        if (fwd_stream) hipStreamDestroy(fwd_stream);
-        for (hipEvent_t e : {ev_prep, ev_fwd[0], ev_fwd[1], ev_bwd[0], ev_bwd[1]})
-            if (e) hipEventDestroy(e);
+        for (hipStream_t s : {fwd_stream, mask_stream[0], mask_stream[1]})
+            if (s) (void)hipStreamDestroy(s);
+        for (hipEvent_t e : {ev_prep, ev_fwd[0], ev_fwd[1], ev_bwd[0], ev_bwd[1], ev_fork[0],
+                             ev_fork[1], ev_join[0], ev_join[1]})
+            if (e) (void)hipEventDestroy(e);
     }
 };
 
@@ -304,6 +313,11 @@ struct Exec {
     // the call's input and output gradient (null: the net's)
     const void* x_in = nullptr;
     const void* dy_in = nullptr;
+    // side >= 0: the attention modules' mask branches run on
+    // n->mask_stream[side] (0 forward, 1 backward; see am_fwd); mask: this
+    // Exec is such a branch (its own scratch)
+    int side = -1;
+    bool mask = false;
 
     int64_t shift() const { return ctx ? (int64_t)n->graph_bytes : 0; }
     void* p(int64_t off) const {
@@ -323,9 +337,38 @@ struct Exec {
     }
     float* par(size_t off) const { return n->P + off; }
     float* grd(size_t off) const { return n->G + off; }
-    void* conv_scr() const { return n->ws + (ctx ? n->conv_scr_off1 : n->conv_scr_off); }
-    void* bn_scr() const { return n->ws + (ctx ? n->bn_scr_off1 : n->bn_scr_off); }
-    void* bn_scr2() const { return n->ws + (ctx ? n->bn_scr2_off1 : n->bn_scr2_off); }
+    void* conv_scr() const {
+        return n->ws + (mask ? n->mask_conv_scr[ctx] : ctx ? n->conv_scr_off1 : n->conv_scr_off);
+    }
+    void* bn_scr() const {
+        return n->ws + (mask ? n->mask_bn_scr[ctx] : ctx ? n->bn_scr_off1 : n->bn_scr_off);
+    }
+    void* bn_scr2() const {
+        return n->ws + (mask ? n->mask_bn_scr2[ctx] : ctx ? n->bn_scr2_off1 : n->bn_scr2_off);
+    }
+    // The Exec of a mask branch forked off this one's stream: everything
+    // enqueued on st so far happens before the branch's first kernel.
+    rat3d_status fork(Exec& m) const {
+        m = *this;
+        m.side = -1;
+        m.mask = true;
+        m.st = n->mask_stream[side];
+        if (hipEventRecord(n->ev_fork[side], st) != hipSuccess ||
+            hipStreamWaitEvent(m.st, n->ev_fork[side], 0) != hipSuccess) {
+            set_error("rat3d_net: mask-branch stream fork failed");
+            return RAT3D_EHIP;
+        }
+        return RAT3D_OK;
+    }
+    // st waits for the branch m's kernels.
+    rat3d_status join(const Exec& m) const {
+        if (hipEventRecord(n->ev_join[side], m.st) != hipSuccess ||
+            hipStreamWaitEvent(st, n->ev_join[side], 0) != hipSuccess) {
+            set_error("rat3d_net: mask-branch stream join failed");
+            return RAT3D_EHIP;
+        }
+        return RAT3D_OK;
+    }
     float* mean(const BnL& b) const { return (float*)(n->ws + b.stat_off + shift()); }
     float* invstd(const BnL& b) const { return mean(b) + b.c; }
     float* fcoef(const BnL& b) const { return mean(b) + 2 * b.c; }
@@ -435,11 +478,10 @@ static bool fuse_up_bn(const AMPlan& m, rat3d_dtype dt) {
            up2_bn_ok(s.n, s.c, s1.d, s1.h, s1.w, dt);
 }
 
-rat3d_status am_fwd(const Exec& e, const AMPlan& m) {
+// The mask branch of the forward: x -> z (the soft mask before its sigmoid).
+static rat3d_status am_mask_fwd(const Exec& e, const AMPlan& m) {
     const Shape& s = m.x.s;
     const rat3d_dtype dt = e.n->dt;
-    RAT3D_TRY(ru_fwd(e, m.t1));
-    RAT3D_TRY(ru_fwd(e, m.t2));
     RAT3D_TRY(pool_fwd(s.n, s.c, s.d, s.h, s.w, 3, 2, 1, dt, e.a(m.x), e.a(m.p1),
                        (uint8_t*)e.p(m.am1), e.st));
     RAT3D_TRY(ru_fwd(e, m.m1));
@@ -464,19 +506,30 @@ rat3d_status am_fwd(const Exec& e, const AMPlan& m) {
                          e.st));
         RAT3D_TRY(e.bn_f(m.bn, m.h1, nullptr, 1, e.a(m.a)));
     }
-    RAT3D_TRY(e.conv_f(m.c2, e.a(m.a), e.a(m.z)));
-    // m is not stored: the backward recomputes it from z (same bits)
-    return softmask_fwd(s.count(), dt, e.a(m.z), e.a(m.t2.y), e.a(m.out), nullptr, e.st);
+    return e.conv_f(m.c2, e.a(m.a), e.a(m.z));
 }
 
-rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
+// The trunk (t1, t2) and the mask branch read only the module input, touch
+// disjoint tensors, parameters and running statistics, and meet in the
+// soft-mask fuse; with e.side set the mask branch runs on a stream of its own.
+rat3d_status am_fwd(const Exec& e, const AMPlan& m) {
+    Exec k = e;
+    if (e.side >= 0) RAT3D_TRY(e.fork(k));
+    RAT3D_TRY(ru_fwd(e, m.t1));
+    RAT3D_TRY(ru_fwd(e, m.t2));
+    RAT3D_TRY(am_mask_fwd(k, m));
+    if (e.side >= 0) RAT3D_TRY(e.join(k));
+    // m is not stored: the backward recomputes it from z (same bits)
+    return softmask_fwd(m.x.s.count(), e.n->dt, e.a(m.z), e.a(m.t2.y), e.a(m.out), nullptr, e.st);
+}
+
+// The mask branch of the backward, from z's gradient (and its per-block sums)
+// to x's gradient (stored, not added: the trunk's is added onto it).
+static rat3d_status am_mask_bwd(const Exec& e, const AMPlan& m, float* zsum, bool need_dx) {
     const Shape& s = m.x.s;
     const Shape& s1 = m.p1.s;
     const Shape& s2 = m.p2.s;
     const rat3d_dtype dt = e.n->dt;
-    float* zsum = m.zsum >= 0 ? (float*)e.p(m.zsum) : nullptr;
-    RAT3D_TRY(softmask_bwd(s.count(), dt, e.g(m.out), e.a(m.t2.y), e.a(m.z), e.g(m.t2.y), 0,
-                           e.g(m.z), e.st, 1, zsum, s.n, s.c, s.vox()));
     RAT3D_TRY(e.conv_d(m.c2, e.g(m.z), e.g(m.a), 0));
     if (zsum) {
         // c2's bias gradient from the soft-mask backward's dz sums
@@ -512,7 +565,22 @@ rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
     if (need_dx)
         RAT3D_TRY(pool_bwd(s.n, s.c, s.d, s.h, s.w, 3, 2, 1, dt, e.g(m.p1),
                            (const uint8_t*)e.p(m.am1), e.g(m.x), 0, e.st));
+    return RAT3D_OK;
+}
+
+// After the soft-mask backward the mask branch and the trunk's second unit
+// are independent (with e.side set the mask branch runs on its own stream);
+// the first unit adds its input gradient onto the mask branch's.
+rat3d_status am_bwd(const Exec& e, const AMPlan& m, bool need_dx = true) {
+    const Shape& s = m.x.s;
+    float* zsum = m.zsum >= 0 ? (float*)e.p(m.zsum) : nullptr;
+    RAT3D_TRY(softmask_bwd(s.count(), e.n->dt, e.g(m.out), e.a(m.t2.y), e.a(m.z), e.g(m.t2.y), 0,
+                           e.g(m.z), e.st, 1, zsum, s.n, s.c, s.vox()));
+    Exec k = e;
+    if (e.side >= 0) RAT3D_TRY(e.fork(k));
+    RAT3D_TRY(am_mask_bwd(k, m, zsum, need_dx));
     RAT3D_TRY(ru_bwd(e, m.t2, false));
+    if (e.side >= 0) RAT3D_TRY(e.join(k));
     return ru_bwd(e, m.t1, true, need_dx);
 }
 
@@ -713,6 +781,8 @@ bool hip_ok(hipError_t r, const char* what) {
 //                  backward of micro-batch k - 2 (the same context);
 //   backward k     waits for forward k and follows backward k - 1 on st.
 // So micro-batch k + 1's forward runs while micro-batch k's backward does.
+// Each of the two also runs its attention module's mask branch on a stream of
+// its own (am_fwd, am_bwd).
 // The two share only read-only data (weights, the prepared layouts) and the
 // BN running statistics, which only the forwards update, in order; parameter
 // gradients are formed by the backwards alone, in order.  Every forward is
@@ -735,6 +805,7 @@ rat3d_status train_partition(rat3d_net* net, const char* x, const char* dy, size
         const int c = (M - 1 - k) % 2;
         Exec f{net, fs, 0};
         f.ctx = c;
+        f.side = 0;
         f.x_in = x + k * x_bytes;
         if (k >= 2 && !hip_ok(hipStreamWaitEvent(fs, net->ev_bwd[c], 0), "stream wait"))
             return RAT3D_EHIP;
@@ -744,6 +815,7 @@ rat3d_status train_partition(rat3d_net* net, const char* x, const char* dy, size
             return RAT3D_EHIP;
         Exec b{net, st, k > 0 ? 1 : 0};
         b.ctx = c;
+        b.side = 1;
         b.x_in = f.x_in;
         b.dy_in = dy + k * dy_bytes;
         RAT3D_TRY(partition_bwd(b));
@@ -864,6 +936,13 @@ rat3d_status rat3d_net_create(const rat3d_net_desc* desc, rat3d_net** out) {
         n->bn_scr_off1 = b.alloc(n->bn_scr_bytes);
         n->bn_scr2_off1 = b.alloc(n->bn_scr_bytes);
     }
+    // mask-branch scratch: the partition's two contexts, the full network's one
+    const int mask_ctx = two_ctx ? 2 : d.kind == RAT3D_NET_RESATTNET ? 1 : 0;
+    for (int c = 0; c < mask_ctx; ++c) {
+        n->mask_conv_scr[c] = b.alloc(n->conv_scr_bytes);
+        n->mask_bn_scr[c] = b.alloc(n->bn_scr_bytes);
+        n->mask_bn_scr2[c] = b.alloc(n->bn_scr_bytes);
+    }
     n->head_scr_off = b.alloc(head_ws_bytes(d.n, 256, 2));
     n->run_mean_off = b.alloc(n->run_count * sizeof(float));
     n->run_var_off = b.alloc(n->run_count * sizeof(float));
@@ -934,11 +1013,16 @@ rat3d_status rat3d_net_bind(rat3d_net* net, float* params, float* grads, void* w
         set_error("rat3d_net_bind: arenas must be 16-byte and the workspace 256-byte aligned");
         return RAT3D_EALIGN;
     }
-    if (net->conv_scr_off1 && !net->fwd_stream) {
-        // the partition's forward stream (default priority) and its events
-        hipError_t r = hipStreamCreateWithFlags(&net->fwd_stream, hipStreamNonBlocking);
+    if (net->mask_conv_scr[0] && !net->mask_stream[0]) {
+        // the partition's forward stream, the mask-branch streams (default
+        // priority) and their events
+        hipError_t r = hipSuccess;
+        if (net->conv_scr_off1) r = hipStreamCreateWithFlags(&net->fwd_stream, hipStreamNonBlocking);
+        for (hipStream_t* s : {&net->mask_stream[0], &net->mask_stream[1]})
+            if (r == hipSuccess) r = hipStreamCreateWithFlags(s, hipStreamNonBlocking);
         for (hipEvent_t* e : {&net->ev_prep, &net->ev_fwd[0], &net->ev_fwd[1], &net->ev_bwd[0],
-                              &net->ev_bwd[1]})
+                              &net->ev_bwd[1], &net->ev_fork[0], &net->ev_fork[1],
+                              &net->ev_join[0], &net->ev_join[1]})
             if (r == hipSuccess) r = hipEventCreateWithFlags(e, hipEventDisableTiming);
         if (r != hipSuccess) {
             set_error("rat3d_net_bind: stream or event creation failed (%s)",
@@ -1013,6 +1097,8 @@ rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labe
     if (full) {
         net->ext_x = x;
         Exec e{net, st, 0};
+        // the attention modules' mask branches on a stream of their own
+        if (net->overlap && net->mask_stream[0]) e.side = 0;
         RAT3D_TRY(stem_fwd(e, true));
         for (int i = 0; i < 3; ++i) {
             RAT3D_TRY(ru_fwd(e, net->rus[i]));

@@ -133,6 +133,16 @@ def _resattnet(n, d, h, w, seed, dt="bf16"):
         U.rel(B.tensor("logits").reshape(n, 2), info["logits"]), float(U.f64(loss)[0]),
         info["loss"]))
     end_to_end(G, Gref)
+    # the same step with every kernel on one stream (no mask-branch stream):
+    # bit-identical gradients and parameters
+    G1, P1 = B.G.clone(), B.P.clone()
+    B.net.rat3d_net_set_overlap(0)
+    B.reset_params()
+    B.net.rat3d_train_step(x, labels, None, loss)
+    U.sync()
+    B.net.rat3d_net_set_overlap(1)
+    assert torch.equal(B.G, G1) and torch.equal(B.P, P1), \
+        "serial full-network step differs from the one with mask-branch streams"
 
 
 def test_resattnet_reduced_f32():
