@@ -175,15 +175,13 @@ def other_config(torch, R, synth, kind, steps, warmup):
     torch.cuda.synchronize()
     # the profiled step runs every kernel on one stream (events of concurrent
     # kernels would each count the shared time); the timed steps do not
-    if kind == "resattnet":
-        net.rat3d_net_set_overlap(0)
+    net.rat3d_net_set_overlap(0)
     R.rat3d_profile_reset()
     R.rat3d_profile_enable(1)
     step()
     torch.cuda.synchronize()
     R.rat3d_profile_enable(0)
-    if kind == "resattnet":
-        net.rat3d_net_set_overlap(1)
+    net.rat3d_net_set_overlap(1)
     tags = [R.rat3d_profile_read(i) for i in range(R.rat3d_profile_count())]
     conv_flops = sum(t[3] for t in tags if t[0].startswith("conv"))
     conv_ms = sum(t[2] for t in tags if t[3] > 0 or t[0] in ("wgrad_reduce", "bias_grad"))

@@ -313,17 +313,19 @@ rat3d_status rat3d_net_tensor_info(const rat3d_net* net, int i, const char** nam
 /* Binds the caller's device buffers: params and grads (float32 arenas) and
  * the workspace.  Also resets BN running statistics (mean 0, var 1) when the
  * kernels next run: the reset is enqueued by the next call that takes a
- * stream.  PARTITION1 with several micro-batches and RESATTNET: the first
- * bind also creates the network's streams (default priority) and events,
- * released by rat3d_net_destroy; RAT3D_EHIP if the runtime refuses them. */
+ * stream.  PARTITION1 with several micro-batches, RESATTNET and ATTN: the
+ * first bind also creates the network's streams (default priority) and
+ * events, released by rat3d_net_destroy; RAT3D_EHIP if the runtime refuses
+ * them. */
 rat3d_status rat3d_net_bind(rat3d_net* net, float* params, float* grads, void* ws,
                             size_t ws_bytes);
 
-/* Whether rat3d_train_step runs independent work concurrently (enable != 0,
- * the default) or every kernel on the caller's stream in order (enable == 0,
- * for per-kernel timing).  Concurrent: PARTITION1 overlaps micro-batches and
- * RESATTNET runs each attention module's mask branch on a stream of the
- * network's own next to its trunk.  Both give bit-identical results. */
+/* Whether rat3d_train_step and rat3d_block_fwd_bwd run independent work
+ * concurrently (enable != 0, the default) or every kernel on the caller's
+ * stream in order (enable == 0, for per-kernel timing).  Concurrent:
+ * PARTITION1 overlaps micro-batches, and every attention module runs its mask
+ * branch on a stream of the network's own next to its trunk.  Both give
+ * bit-identical results. */
 rat3d_status rat3d_net_set_overlap(rat3d_net* net, int enable);
 
 /* RESUNIT / ATTN: forward on x (input shape), backward from dy (output

@@ -937,7 +937,8 @@ rat3d_status rat3d_net_create(const rat3d_net_desc* desc, rat3d_net** out) {
         n->bn_scr2_off1 = b.alloc(n->bn_scr_bytes);
     }
     // mask-branch scratch: the partition's two contexts, the full network's one
-    const int mask_ctx = two_ctx ? 2 : d.kind == RAT3D_NET_RESATTNET ? 1 : 0;
+    const int mask_ctx =
+        two_ctx ? 2 : d.kind == RAT3D_NET_RESATTNET || d.kind == RAT3D_NET_ATTN ? 1 : 0;
     for (int c = 0; c < mask_ctx; ++c) {
         n->mask_conv_scr[c] = b.alloc(n->conv_scr_bytes);
         n->mask_bn_scr[c] = b.alloc(n->bn_scr_bytes);
@@ -1071,6 +1072,8 @@ rat3d_status rat3d_block_fwd_bwd(rat3d_net* net, const void* x, const void* dy, 
         RAT3D_TRY(ru_fwd(e, net->rus[0]));
         return ru_bwd(e, net->rus[0], false);
     }
+    // the mask branch on a stream of its own
+    if (net->overlap && net->mask_stream[0]) e.side = 0;
     RAT3D_TRY(am_fwd(e, net->ams[0]));
     return am_bwd(e, net->ams[0]);
 }

@@ -81,6 +81,17 @@ def _block(kind, code, n, c, d, h, w, dt, seed, perturb_bn=0.0):
         r, U.rel(U.f64(dx), dxref)))
     assert r <= U.TOL[dt], "block output: relative error %.3e" % r
     end_to_end(B.grads(), Gref)
+    # the same call with every kernel on one stream: bit-identical outputs
+    # and gradients (an attention module's mask branch otherwise runs on a
+    # stream of its own)
+    torch = U.torch_mod()
+    y1, dx1, G1 = y.clone(), dx.clone(), B.G.clone()
+    B.net.rat3d_net_set_overlap(0)
+    B.net.rat3d_block_fwd_bwd(x, dy, y, dx)
+    U.sync()
+    B.net.rat3d_net_set_overlap(1)
+    assert torch.equal(y, y1) and torch.equal(dx, dx1) and torch.equal(B.G, G1), \
+        "serial block call differs from the concurrent one"
 
 
 def test_resunit_workload():
