@@ -323,9 +323,10 @@ rat3d_status rat3d_net_bind(rat3d_net* net, float* params, float* grads, void* w
 /* Whether rat3d_train_step and rat3d_block_fwd_bwd run independent work
  * concurrently (enable != 0, the default) or every kernel on the caller's
  * stream in order (enable == 0, for per-kernel timing).  Concurrent:
- * PARTITION1 overlaps micro-batches, and every attention module runs its mask
- * branch on a stream of the network's own next to its trunk.  Both give
- * bit-identical results. */
+ * PARTITION1 overlaps micro-batches, every attention module runs its mask
+ * branch on a stream of the network's own next to its trunk, and RESATTNET
+ * and ATTN run their weight gradients on another.  Both give bit-identical
+ * results. */
 rat3d_status rat3d_net_set_overlap(rat3d_net* net, int enable);
 
 /* RESUNIT / ATTN: forward on x (input shape), backward from dy (output

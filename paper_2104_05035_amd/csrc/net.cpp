@@ -135,18 +135,21 @@ struct rat3d_net {
     // scratch of the attention modules' mask branches, per context, when
     // they run on a stream of their own (see am_fwd)
     size_t mask_conv_scr[2] = {0, 0}, mask_bn_scr[2] = {0, 0}, mask_bn_scr2[2] = {0, 0};
+    size_t wgrad_conv_scr = 0;  // the weight-gradient stream's (RESATTNET, ATTN)
     bool overlap = true;
     hipStream_t fwd_stream = nullptr;
     // mask-branch streams of the forward and of the backward, with the
     // events that fork and join them
     hipStream_t mask_stream[2] = {nullptr, nullptr};
+    hipStream_t wgrad_stream = nullptr;
     hipEvent_t ev_prep = nullptr, ev_fwd[2] = {nullptr, nullptr}, ev_bwd[2] = {nullptr, nullptr};
     hipEvent_t ev_fork[2] = {nullptr, nullptr}, ev_join[2] = {nullptr, nullptr};
+    hipEvent_t ev_w_in = nullptr, ev_w_done = nullptr;
     ~rat3d_net() {
-        for (hipStream_t s : {fwd_stream, mask_stream[0], mask_stream[1]})
+        for (hipStream_t s : {fwd_stream, mask_stream[0], mask_stream[1], wgrad_stream})
             if (s) (void)hipStreamDestroy(s);
         for (hipEvent_t e : {ev_prep, ev_fwd[0], ev_fwd[1], ev_bwd[0], ev_bwd[1], ev_fork[0],
-                             ev_fork[1], ev_join[0], ev_join[1]})
+                             ev_fork[1], ev_join[0], ev_join[1], ev_w_in, ev_w_done})
             if (e) (void)hipEventDestroy(e);
     }
 };
@@ -318,6 +321,8 @@ struct Exec {
     // Exec is such a branch (its own scratch)
     int side = -1;
     bool mask = false;
+    // non-null: weight gradients run on this stream (see conv_w)
+    hipStream_t wst = nullptr;
 
     int64_t shift() const { return ctx ? (int64_t)n->graph_bytes : 0; }
     void* p(int64_t off) const {
@@ -386,9 +391,32 @@ struct Exec {
         return conv_dgrad_prepared(c.g, n->dt, dy, w(c), wt(c, 1), dx, accumulate, conv_scr(),
                                    n->conv_scr_bytes, st);
     }
+    // With wst set, a weight gradient runs on wst once everything enqueued on
+    // st so far (which produced dy) is done: it reads only x, an activation,
+    // and dy, which no later kernel of the backward writes, and writes only
+    // its own parameter gradients, so it overlaps the rest of the backward;
+    // the caller joins wst (join_wgrad) before anything reads the gradients.
     rat3d_status conv_w(const ConvL& c, const void* x, const void* dy) const {
-        return conv_wgrad(c.g, n->dt, x, dy, grd(c.w_off), c.bias ? grd(c.b_off) : nullptr, acc,
-                          conv_scr(), n->conv_scr_bytes, st);
+        float* db = c.bias ? grd(c.b_off) : nullptr;
+        if (!wst)
+            return conv_wgrad(c.g, n->dt, x, dy, grd(c.w_off), db, acc, conv_scr(),
+                              n->conv_scr_bytes, st);
+        if (hipEventRecord(n->ev_w_in, st) != hipSuccess ||
+            hipStreamWaitEvent(wst, n->ev_w_in, 0) != hipSuccess) {
+            set_error("rat3d_net: weight-gradient stream hand-off failed");
+            return RAT3D_EHIP;
+        }
+        return conv_wgrad(c.g, n->dt, x, dy, grd(c.w_off), db, acc, n->ws + n->wgrad_conv_scr,
+                          n->conv_scr_bytes, wst);
+    }
+    // st waits for every weight gradient handed to wst.
+    rat3d_status join_wgrad() const {
+        if (wst && (hipEventRecord(n->ev_w_done, wst) != hipSuccess ||
+                    hipStreamWaitEvent(st, n->ev_w_done, 0) != hipSuccess)) {
+            set_error("rat3d_net: weight-gradient stream join failed");
+            return RAT3D_EHIP;
+        }
+        return RAT3D_OK;
     }
     // The forward keeps the apply's scale and shift; a BN + ReLU without a
     // residual recomputes its backward mask from x with them (bn_bwd_x).
@@ -944,6 +972,7 @@ rat3d_status rat3d_net_create(const rat3d_net_desc* desc, rat3d_net** out) {
         n->mask_bn_scr[c] = b.alloc(n->bn_scr_bytes);
         n->mask_bn_scr2[c] = b.alloc(n->bn_scr_bytes);
     }
+    if (!two_ctx && mask_ctx) n->wgrad_conv_scr = b.alloc(n->conv_scr_bytes);
     n->head_scr_off = b.alloc(head_ws_bytes(d.n, 256, 2));
     n->run_mean_off = b.alloc(n->run_count * sizeof(float));
     n->run_var_off = b.alloc(n->run_count * sizeof(float));
@@ -1021,9 +1050,11 @@ rat3d_status rat3d_net_bind(rat3d_net* net, float* params, float* grads, void* w
         if (net->conv_scr_off1) r = hipStreamCreateWithFlags(&net->fwd_stream, hipStreamNonBlocking);
         for (hipStream_t* s : {&net->mask_stream[0], &net->mask_stream[1]})
             if (r == hipSuccess) r = hipStreamCreateWithFlags(s, hipStreamNonBlocking);
+        if (r == hipSuccess && net->wgrad_conv_scr)
+            r = hipStreamCreateWithFlags(&net->wgrad_stream, hipStreamNonBlocking);
         for (hipEvent_t* e : {&net->ev_prep, &net->ev_fwd[0], &net->ev_fwd[1], &net->ev_bwd[0],
                               &net->ev_bwd[1], &net->ev_fork[0], &net->ev_fork[1],
-                              &net->ev_join[0], &net->ev_join[1]})
+                              &net->ev_join[0], &net->ev_join[1], &net->ev_w_in, &net->ev_w_done})
             if (r == hipSuccess) r = hipEventCreateWithFlags(e, hipEventDisableTiming);
         if (r != hipSuccess) {
             set_error("rat3d_net_bind: stream or event creation failed (%s)",
@@ -1072,10 +1103,14 @@ rat3d_status rat3d_block_fwd_bwd(rat3d_net* net, const void* x, const void* dy, 
         RAT3D_TRY(ru_fwd(e, net->rus[0]));
         return ru_bwd(e, net->rus[0], false);
     }
-    // the mask branch on a stream of its own
-    if (net->overlap && net->mask_stream[0]) e.side = 0;
+    // the mask branch and the weight gradients on streams of their own
+    if (net->overlap && net->mask_stream[0]) {
+        e.side = 0;
+        e.wst = net->wgrad_stream;
+    }
     RAT3D_TRY(am_fwd(e, net->ams[0]));
-    return am_bwd(e, net->ams[0]);
+    RAT3D_TRY(am_bwd(e, net->ams[0]));
+    return e.join_wgrad();
 }
 
 rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labels,
@@ -1100,8 +1135,12 @@ rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labe
     if (full) {
         net->ext_x = x;
         Exec e{net, st, 0};
-        // the attention modules' mask branches on a stream of their own
-        if (net->overlap && net->mask_stream[0]) e.side = 0;
+        // the attention modules' mask branches and the weight gradients on
+        // streams of their own
+        if (net->overlap && net->mask_stream[0]) {
+            e.side = 0;
+            e.wst = net->wgrad_stream;
+        }
         RAT3D_TRY(stem_fwd(e, true));
         for (int i = 0; i < 3; ++i) {
             RAT3D_TRY(ru_fwd(e, net->rus[i]));
@@ -1118,6 +1157,7 @@ rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labe
             RAT3D_TRY(ru_bwd(e, net->rus[i], false));
         }
         RAT3D_TRY(stem_bwd(e, true));
+        RAT3D_TRY(e.join_wgrad());
         if (loss_dev) {
             if (hipMemcpyAsync(loss_dev, net->ws + net->loss_off, sizeof(float),
                                hipMemcpyDeviceToDevice, st) != hipSuccess) {
