@@ -317,8 +317,9 @@ struct Exec {
     const void* x_in = nullptr;
     const void* dy_in = nullptr;
     // side >= 0: the attention modules' mask branches run on
-    // n->mask_stream[side] (0 forward, 1 backward; see am_fwd); mask: this
-    // Exec is such a branch (its own scratch)
+    // n->mask_stream[side] (see am_fwd): the partition's forwards use 0 and
+    // its backwards 1, which run at the same time; the full network and the
+    // block call use 0.  mask: this Exec is such a branch (its own scratch)
     int side = -1;
     bool mask = false;
     // non-null: weight gradients run on this stream (see conv_w)
