@@ -110,3 +110,22 @@ def test_net_create_rejects_bad_desc():
         R.Net(R.NET_RESATTNET, 2, 2, 32, 96, 112, 96, R.BF16)  # two input channels
     with pytest.raises(R.Rat3dError):
         R.Net(R.NET_RESUNIT, 2, 4, 4, 8, 8, 8, R.BF16, micro_batches=2)
+
+
+def test_partition_workspace_holds_two_activation_contexts():
+    """With several micro-batches the partition's training step keeps two
+    copies of everything a micro-batch stores (the overlapped schedule runs
+    micro-batch k + 1's forward during micro-batch k's backward): the
+    workspace grows by at least the extent of the per-micro-batch tensors the
+    single-micro-batch plan lays out, and the tensors described (the copy the
+    last micro-batch uses) are the same in both plans."""
+    shape = (2, 1, 64, 48, 56, 48)
+    one = R.Net(R.NET_PARTITION1, *shape, R.BF16, micro_batches=1)
+    four = R.Net(R.NET_PARTITION1, *shape, R.BF16, micro_batches=4)
+    es = {R.BF16: 2, R.F32: 4, R.U8: 1}
+    shared = ("running_", "logits", "loss")  # after the per-micro-batch region: they move
+    t1 = {k: v for k, v in one.tensors().items() if not k.startswith(shared)}
+    t4 = {k: v for k, v in four.tensors().items() if not k.startswith(shared)}
+    extent = max(off + int(np.prod(shp)) * es[dt] for off, dt, shp in t1.values())
+    assert t4 == t1
+    assert four.workspace_size >= one.workspace_size + extent
