@@ -453,13 +453,22 @@ struct Exec {
         if (s_ != RAT3D_OK) return s_;        \
     } while (0)
 
+// With e.side set, a projection skip's 1^3 conv runs on the branch stream
+// (it reads only x) while conv1 -> BN -> conv2 run on e.st.
 rat3d_status ru_fwd(const Exec& e, const RUPlan& r) {
+    Exec k = e;
+    const bool fork = r.proj && e.side >= 0;
+    if (fork) {
+        RAT3D_TRY(e.fork(k));
+        RAT3D_TRY(k.conv_f(r.cp, k.a(r.x), k.a(r.hp)));
+    }
     RAT3D_TRY(e.conv_f(r.c1, e.a(r.x), e.a(r.h1)));
     RAT3D_TRY(e.bn_f(r.b1, r.h1, nullptr, 1, e.a(r.a1)));
     RAT3D_TRY(e.conv_f(r.c2, e.a(r.a1), e.a(r.h2)));
     const void* skip = e.a(r.x);
     if (r.proj) {
-        RAT3D_TRY(e.conv_f(r.cp, e.a(r.x), e.a(r.hp)));
+        if (fork) RAT3D_TRY(e.join(k));
+        else RAT3D_TRY(e.conv_f(r.cp, e.a(r.x), e.a(r.hp)));
         const BnGeom g{r.h2.s.n, r.b2.c, r.h2.s.vox()};
         if (e.n->dt == RAT3D_BF16 && g.V % 8 == 0) {
             // the projection's BN is applied inside the output BN's apply
@@ -477,7 +486,10 @@ rat3d_status ru_fwd(const Exec& e, const RUPlan& r) {
 }
 
 // Backward of a residual unit from y's gradient to x's gradient.  acc_dx: the
-// input gradient already holds a partial sum to add to.
+// input gradient already holds a partial sum to add to.  With e.side set, a
+// projection skip's backward (it needs only the skip gradient) runs on the
+// branch stream beside conv2's backward and BN1's; conv1's input gradient,
+// added onto the projection's, waits for it.
 rat3d_status ru_bwd(const Exec& e, const RUPlan& r, bool acc_dx, bool need_dx = true) {
     void* dskip = e.p(r.dskip);
     void* dx = need_dx ? e.g(r.x) : nullptr;
@@ -486,14 +498,22 @@ rat3d_status ru_bwd(const Exec& e, const RUPlan& r, bool acc_dx, bool need_dx = 
     const bool skip_direct = !r.proj && need_dx;
     RAT3D_TRY(e.bn_b(r.b2, e.g(r.y), r.h2, e.a(r.y), 1, e.g(r.h2), skip_direct ? dx : dskip,
                      skip_direct && acc_dx ? 1 : 0, e.bits(r.ybits)));
+    auto proj_bwd = [&](const Exec& x) -> rat3d_status {
+        RAT3D_TRY(x.bn_b(r.bp, dskip, r.hp, nullptr, 0, x.g(r.hp), nullptr));
+        if (need_dx) RAT3D_TRY(x.conv_d(r.cp, x.g(r.hp), dx, acc_dx ? 1 : 0));
+        return x.conv_w(r.cp, x.a(r.x), x.g(r.hp));
+    };
+    Exec k = e;
+    const bool fork = r.proj && e.side >= 0;
+    if (fork) {
+        RAT3D_TRY(e.fork(k));
+        RAT3D_TRY(proj_bwd(k));
+    }
     RAT3D_TRY(e.conv_d(r.c2, e.g(r.h2), e.g(r.a1), 0));
     RAT3D_TRY(e.conv_w(r.c2, e.a(r.a1), e.g(r.h2)));
     RAT3D_TRY(e.bn_bwd_x(r.b1, e.g(r.a1), r.h1, e.g(r.h1)));
-    if (r.proj) {
-        RAT3D_TRY(e.bn_b(r.bp, dskip, r.hp, nullptr, 0, e.g(r.hp), nullptr));
-        if (need_dx) RAT3D_TRY(e.conv_d(r.cp, e.g(r.hp), dx, acc_dx ? 1 : 0));
-        RAT3D_TRY(e.conv_w(r.cp, e.a(r.x), e.g(r.hp)));
-    }
+    if (fork) RAT3D_TRY(e.join(k));
+    else if (r.proj) RAT3D_TRY(proj_bwd(e));
     if (need_dx) RAT3D_TRY(e.conv_d(r.c1, e.g(r.h1), dx, 1));
     return e.conv_w(r.c1, e.a(r.x), e.g(r.h1));
 }
