@@ -78,6 +78,12 @@ def test_other_validation():
         R.rat3d_head_fwd_bwd(200, 256, 8, 2, R.BF16, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                              FAKE, FAKE, 0, FAKE, 1 << 20, stream=0)
     assert e.value.status == R.EUNSUPPORTED
+    assert R.lib().rat3d_net_set_overlap(None, 1) == R.EINVAL
+    # the schedule switch needs no buffers and no GPU: it only selects how
+    # the next training step is enqueued
+    net = R.Net(R.NET_PARTITION1, 2, 1, 64, 48, 56, 48, R.BF16, micro_batches=2)
+    net.rat3d_net_set_overlap(0)
+    net.rat3d_net_set_overlap(1)
 
 
 KINDS = [
