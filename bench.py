@@ -224,7 +224,7 @@ def main():
                          "reference dispatch that scales rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build runs the per-device training step "
+        print("bench.py measures one GPU only: the library runs the per-device training step "
               "on a single MI355X and uses no collectives; run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
