@@ -45,8 +45,8 @@ def stats(csv_path, bench_log, out, title, cmd):
     if "roofline" in b:
         wu, bk, ts = b.get("warmup", 1), b.get("breakdown_steps", 3), b.get("steps", 3)
         sched = ("all of them with micro-batches not overlapped, like the step whose launches "
-                 "the live timing brackets" if wu == 0 and ts == 1 else
-                 "the warm-up and all timed steps but the last overlap micro-batches")
+                 "the live timing brackets" if ts == 1 else
+                 "all timed steps but the last with micro-batches overlapped")
         lines += ["Calls cover %d warm-up, %d breakdown and %d timed steps, %s.  Dominant kernel "
                   "per bench.py's live hipEvents: `%s`, %.1f us/launch (rocprofv3 average in the "
                   "table)." % (wu, bk, ts, sched, b["roofline"]["kernel"],
