@@ -16,6 +16,8 @@
 // innermost, so that every lane fetches its MFMA operand with one 16-byte
 // LDS read: bf16 uses v_mfma_f32_16x16x32_bf16 (8 K values per lane),
 // float32 uses four v_mfma_f32_16x16x4_f32 (4 K values per lane).
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "vec.hpp"
@@ -210,6 +212,126 @@ __global__ __launch_bounds__(256) void conv_gather_fd(ConvGeom g, const T* __res
                     if (bias) v += bias[c];
                     if (accumulate) v += Elt<T>::ld(dst + off);
                     Elt<T>::st(dst + off, v);
+                }
+            }
+}
+
+// Forward, bfloat16, source channels a multiple of 32 (every K step of 32
+// is whole): the same 64 x 64 tiles, pipelined.  The next K step's operands
+// are loaded into registers (unconditionally: taps outside the volume read
+// element 0 and are zeroed) while the current step multiplies from one of
+// two LDS buffers, so a step costs one barrier and no exposed load latency.
+// A thread's 8 K values are consecutive taps of one or two channels: the
+// channel and tap of the first come from one division, the rest by stepping
+// the tap with a wrap; a tap's (kd, kh, kw) come from a table in LDS.
+constexpr int kGatherMaxTaps = 343;
+__global__ __launch_bounds__(256) void conv_gather_fwd_pipe(ConvGeom g, const bf16* __restrict__ src,
+                                                            const bf16* __restrict__ wt,
+                                                            const float* __restrict__ bias,
+                                                            bf16* __restrict__ dst) {
+    constexpr int KV = 8, BK = 32;
+    __shared__ __align__(16) unsigned char As[2][64 * kRow];
+    __shared__ __align__(16) unsigned char Bs[2][64 * kRow];
+    __shared__ int taps[kGatherMaxTaps];  // kd | kh << 8 | kw << 16
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    const int KT = g.k * g.k * g.k, K = g.Ci * KT;
+    const int64_t Vrow = (int64_t)g.Do * g.Ho * g.Wo, M = (int64_t)g.N * Vrow;
+    const int64_t Vsrc = (int64_t)g.D * g.H * g.W;
+    const int64_t m0 = (int64_t)blockIdx.x * 64;
+    const int c0 = blockIdx.y * 64;
+    for (int t = tid; t < KT; t += 256) {
+        const int kd = t / (g.k * g.k), r = t - kd * g.k * g.k, kh = r / g.k;
+        taps[t] = kd | kh << 8 | (r - kh * g.k) << 16;
+    }
+
+    // this thread's A row (an output voxel) and B row (an output channel)
+    const int ar = tid >> 2, aq = tid & 3;
+    const int64_t am = m0 + ar;
+    const bool arow_ok = am < M;
+    int id0 = 0, ih0 = 0, iw0 = 0;
+    int64_t a_base = 0;
+    {
+        const int64_t mm = arow_ok ? am : 0;
+        const int64_t n = mm / Vrow;
+        int64_t sp = mm - n * Vrow;
+        const int od = (int)(sp / ((int64_t)g.Ho * g.Wo));
+        sp -= (int64_t)od * g.Ho * g.Wo;
+        const int oh = (int)(sp / g.Wo), ow = (int)(sp - (int64_t)oh * g.Wo);
+        id0 = od * g.s - g.p;
+        ih0 = oh * g.s - g.p;
+        iw0 = ow * g.s - g.p;
+        a_base = n * g.Ci * Vsrc;
+    }
+    const int bcol = c0 + (tid >> 2);
+    const bool bcol_ok = bcol < g.Co;
+    const bf16* wrow = wt + (int64_t)(bcol_ok ? bcol : 0) * K;
+
+    uint32_t av[KV / 2];
+    uint4 bv;
+    auto load = [&](int k0) {
+        const int kf = k0 + aq * KV;
+        int c = kf / KT, t = kf - c * KT;
+        bf16 v[KV];
+#pragma unroll
+        for (int j = 0; j < KV; ++j) {
+            const int e = taps[t];
+            const int id = id0 + (e & 0xff), ih = ih0 + ((e >> 8) & 0xff), iw = iw0 + (e >> 16);
+            const bool ok = arow_ok && (unsigned)id < (unsigned)g.D &&
+                            (unsigned)ih < (unsigned)g.H && (unsigned)iw < (unsigned)g.W;
+            const int64_t off = ok ? a_base + c * Vsrc + ((int64_t)id * g.H + ih) * g.W + iw : 0;
+            const bf16 x = src[off];
+            v[j] = ok ? x : (bf16)0;
+            if (++t == KT) {
+                t = 0;
+                ++c;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < KV / 2; ++j) av[j] = (uint32_t)v[2 * j] | (uint32_t)v[2 * j + 1] << 16;
+        const uint4 w4 = *reinterpret_cast<const uint4*>(wrow + k0 + aq * KV);
+        bv = bcol_ok ? w4 : make_uint4(0u, 0u, 0u, 0u);
+    };
+    auto stage = [&](int buf) {
+        *reinterpret_cast<uint4*>(As[buf] + ar * kRow + aq * 16) = make_uint4(av[0], av[1], av[2], av[3]);
+        *reinterpret_cast<uint4*>(Bs[buf] + (tid >> 2) * kRow + aq * 16) = bv;
+    };
+
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    __syncthreads();  // the tap table
+    const int S = K / BK;
+    load(0);
+    stage(0);
+    __syncthreads();
+    for (int st = 0; st < S; ++st) {
+        const bool more = st + 1 < S;
+        if (more) load((st + 1) * BK);
+        tile_mma<bf16>(As[st & 1], Bs[st & 1], acc, lane, wm, wn);
+        if (more) stage((st + 1) & 1);
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int row = wm * 32 + i * 16 + 4 * (lane >> 4) + e;
+                const int col = wn * 32 + j * 16 + (lane & 15);
+                const int64_t m = m0 + row;
+                const int c = c0 + col;
+                if (m < M && c < g.Co) {
+                    const int64_t n = m / Vrow, sp = m - n * Vrow;
+                    float v = acc[i][j][e];
+                    if (bias) v += bias[c];
+                    dst[(n * g.Co + c) * Vrow + sp] = f2bf(v);
                 }
             }
 }
@@ -614,6 +736,16 @@ static rat3d_status gather_fd(const ConvGeom& g, bool dgrad, const void* src, co
                                                : (int64_t)g.Do * g.Ho * g.Wo);
     const int cols = dgrad ? g.Ci : g.Co;
     dim3 grid((unsigned)ceil_div(rows, 64), (unsigned)ceil_div(cols, 64));
+    if constexpr (std::is_same<T, bf16>::value) {
+        // (16-byte weight loads: K = Ci k^3 is a multiple of 8, the base must be aligned)
+        if (!dgrad && !accumulate && g.Ci % 32 == 0 && g.k * g.k * g.k <= kGatherMaxTaps &&
+            ((uintptr_t)w & 15u) == 0) {
+            conv_gather_fwd_pipe<<<grid, 256, 0, st>>>(g, (const bf16*)src, (const bf16*)w, bias,
+                                                       (bf16*)dst);
+            RAT3D_LAUNCH_CHECK();
+            return RAT3D_OK;
+        }
+    }
     if (dgrad)
         conv_gather_fd<T, true><<<grid, 256, 0, st>>>(g, (const T*)src, (const T*)w, nullptr,
                                                       (T*)dst, accumulate);
