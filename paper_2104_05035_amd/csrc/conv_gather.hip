@@ -482,6 +482,152 @@ __global__ __launch_bounds__(256) void conv_gather_dgrad_phase(ConvGeom g,
             }
 }
 
+// The strided input gradient in bf16 with C_out (the channels its K runs
+// over) a multiple of 32, pipelined like conv_gather_fwd_pipe: the
+// class's taps (at most (k / s + 1)^3) in an LDS table built once, each
+// thread's 8 consecutive K values (co, tap) stepped through it, the next K
+// step's loads issued unconditionally before the current step's MFMAs into
+// the other of two LDS buffers.
+constexpr int kPhaseMaxTaps = 64;
+__global__ __launch_bounds__(256) void conv_gather_dgrad_phase_pipe(ConvGeom g,
+                                                                    const bf16* __restrict__ dy,
+                                                                    const bf16* __restrict__ wt,
+                                                                    bf16* __restrict__ dx,
+                                                                    int accumulate) {
+    constexpr int KV = 8, BK = 32;
+    __shared__ __align__(16) unsigned char As[2][64 * kRow];
+    __shared__ __align__(16) unsigned char Bs[2][64 * kRow];
+    __shared__ int toff[kPhaseMaxTaps];  // od | oh << 8 | ow << 16 offsets (each + 128)
+    __shared__ int tflat[kPhaseMaxTaps]; // flattened tap kd * k^2 + kh * k + kw
+
+    const int s = g.s;
+    const int cls = blockIdx.z;
+    const int rd = cls / (s * s), rh = (cls / s) % s, rw = cls % s;
+    const int Md = rd < g.D ? (g.D - rd + s - 1) / s : 0;
+    const int Mh = rh < g.H ? (g.H - rh + s - 1) / s : 0;
+    const int Mw = rw < g.W ? (g.W - rw + s - 1) / s : 0;
+    const int t0d = (rd + g.p) % s, t0h = (rh + g.p) % s, t0w = (rw + g.p) % s;
+    const int nd = t0d < g.k ? (g.k - t0d + s - 1) / s : 0;
+    const int nh = t0h < g.k ? (g.k - t0h + s - 1) / s : 0;
+    const int nw = t0w < g.k ? (g.k - t0w + s - 1) / s : 0;
+    const int KTc = nd * nh * nw;
+    const int Kc = g.Co * KTc;
+    const int64_t Vc = (int64_t)Md * Mh * Mw;
+    const int64_t M = (int64_t)g.N * Vc;
+    const int64_t m0 = (int64_t)blockIdx.x * 64;
+    if (m0 >= M) return;  // this class has fewer rows than the grid covers
+    const int c0 = blockIdx.y * 64;
+    const int KT = g.k * g.k * g.k;
+    const int64_t Vsrc = (int64_t)g.Do * g.Ho * g.Wo;
+    const int64_t Vdst = (int64_t)g.D * g.H * g.W;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave & 1, wn = wave >> 1;
+    for (int j = tid; j < KTc; j += 256) {
+        const int jd = j / (nh * nw), r = j - jd * nh * nw, jh = r / nw, jw = r - jh * nw;
+        const int td = t0d + s * jd, th = t0h + s * jh, tw = t0w + s * jw;
+        toff[j] = ((rd + g.p - td) / s + 128) | ((rh + g.p - th) / s + 128) << 8 |
+                  ((rw + g.p - tw) / s + 128) << 16;
+        tflat[j] = (td * g.k + th) * g.k + tw;
+    }
+    const int ar = tid >> 2, aq = tid & 3;
+    const int64_t am = m0 + ar;
+    const bool arow_ok = am < M;
+    int a_d = 0, a_h = 0, a_w = 0;
+    int64_t a_base = 0;
+    if (arow_ok) {
+        const int64_t n = am / Vc;
+        int64_t sp = am - n * Vc;
+        a_d = (int)(sp / ((int64_t)Mh * Mw));
+        sp -= (int64_t)a_d * Mh * Mw;
+        a_h = (int)(sp / Mw);
+        a_w = (int)(sp - (int64_t)a_h * Mw);
+        a_base = n * g.Co * Vsrc;
+    }
+    const int bcol = c0 + (tid >> 2);
+    const bool bcol_ok = bcol < g.Ci;
+    const int bc = bcol_ok ? bcol : 0;
+
+    uint32_t av[KV / 2], bv[KV / 2];
+    auto load = [&](int k0) {
+        const int kf = k0 + aq * KV;
+        int co = kf / KTc, j = kf - co * KTc;
+        bf16 a[KV], b[KV];
+#pragma unroll
+        for (int q = 0; q < KV; ++q) {
+            const int e = toff[j];
+            const int od = a_d + (e & 0xff) - 128, oh = a_h + ((e >> 8) & 0xff) - 128,
+                      ow = a_w + (e >> 16) - 128;
+            const bool ok = arow_ok && (unsigned)od < (unsigned)g.Do &&
+                            (unsigned)oh < (unsigned)g.Ho && (unsigned)ow < (unsigned)g.Wo;
+            const int64_t off = ok ? a_base + co * Vsrc + ((int64_t)od * g.Ho + oh) * g.Wo + ow : 0;
+            const bf16 xa = dy[off];
+            a[q] = ok ? xa : (bf16)0;
+            const bf16 xb = wt[((int64_t)co * g.Ci + bc) * KT + tflat[j]];
+            b[q] = bcol_ok ? xb : (bf16)0;
+            if (++j == KTc) {
+                j = 0;
+                ++co;
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < KV / 2; ++q) {
+            av[q] = (uint32_t)a[2 * q] | (uint32_t)a[2 * q + 1] << 16;
+            bv[q] = (uint32_t)b[2 * q] | (uint32_t)b[2 * q + 1] << 16;
+        }
+    };
+    auto stage = [&](int buf) {
+        *reinterpret_cast<uint4*>(As[buf] + ar * kRow + aq * 16) = make_uint4(av[0], av[1], av[2], av[3]);
+        *reinterpret_cast<uint4*>(Bs[buf] + (tid >> 2) * kRow + aq * 16) = make_uint4(bv[0], bv[1], bv[2], bv[3]);
+    };
+
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    __syncthreads();  // the tap tables
+    const int S = Kc / BK;
+    if (S > 0) {
+        load(0);
+        stage(0);
+    }
+    __syncthreads();
+    for (int st = 0; st < S; ++st) {
+        const bool more = st + 1 < S;
+        if (more) load((st + 1) * BK);
+        tile_mma<bf16>(As[st & 1], Bs[st & 1], acc, lane, wm, wn);
+        if (more) stage((st + 1) & 1);
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int row = wm * 32 + i * 16 + 4 * (lane >> 4) + e;
+                const int col = wn * 32 + j * 16 + (lane & 15);
+                const int64_t m = m0 + row;
+                const int c = c0 + col;
+                if (m < M && c < g.Ci) {
+                    const int64_t n = m / Vc;
+                    int64_t sp = m - n * Vc;
+                    const int md = (int)(sp / ((int64_t)Mh * Mw));
+                    sp -= (int64_t)md * Mh * Mw;
+                    const int mh = (int)(sp / Mw), mw = (int)(sp - (sp / Mw) * Mw);
+                    const int64_t off = (n * g.Ci + c) * Vdst +
+                                        ((int64_t)(rd + s * md) * g.H + rh + s * mh) * g.W + rw +
+                                        s * mw;
+                    float v = acc[i][j][e];
+                    if (accumulate) v += bf2f(dx[off]);
+                    dx[off] = f2bf(v);
+                }
+            }
+}
+
 // ---------------------------------------------------------------- wgrad
 template <typename T>
 __global__ __launch_bounds__(256) void conv_gather_wgrad(ConvGeom g, const T* __restrict__ x,
@@ -771,6 +917,16 @@ static rat3d_status gather_dgrad_phase(const ConvGeom& g, const void* dy, const 
                          ceil_div(g.W, g.s);
     dim3 grid((unsigned)ceil_div(rows, 64), (unsigned)ceil_div(g.Ci, 64),
               (unsigned)(g.s * g.s * g.s));
+    if constexpr (std::is_same<T, bf16>::value) {
+        // class tap sets of at most (k / s + 1)^3 taps, offsets within +-127
+        const int tps = g.k / g.s + 1;
+        if (g.Co % 32 == 0 && tps * tps * tps <= kPhaseMaxTaps && g.k <= 127) {
+            conv_gather_dgrad_phase_pipe<<<grid, 256, 0, st>>>(g, (const bf16*)dy, (const bf16*)w,
+                                                               (bf16*)dx, accumulate);
+            RAT3D_LAUNCH_CHECK();
+            return RAT3D_OK;
+        }
+    }
     conv_gather_dgrad_phase<T><<<grid, 256, 0, st>>>(g, (const T*)dy, (const T*)w, (T*)dx,
                                                      accumulate);
     RAT3D_LAUNCH_CHECK();

@@ -26,6 +26,8 @@ CONV_CASES = [
     (2, 64, 128, 12, 14, 12, 1, 2, 0, False, "bf16"),
     # pipelined strided forward: ragged rows and output channels, bias
     (3, 32, 40, 9, 11, 7, 3, 2, 1, True, "bf16"),
+    # pipelined strided input gradient: ragged rows and input channels
+    (2, 40, 64, 9, 11, 7, 3, 2, 1, False, "bf16"),
     (2, 64, 64, 6, 7, 6, 1, 1, 0, True, "bf16"),
     (1, 1, 1, 1, 1, 1, 1, 1, 0, True, "f32"),
     (1, 2, 3, 2, 2, 2, 3, 1, 1, False, "bf16"),
