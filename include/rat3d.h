@@ -344,7 +344,13 @@ rat3d_status rat3d_block_fwd_bwd(rat3d_net* net, const void* x, const void* dy, 
  * `stream`, in two alternating copies of the saved activations (the last
  * micro-batch in the copy rat3d_net_tensor_info describes); the caller's
  * stream waits for all of it, so work enqueued after the call sees the
- * update. */
+ * update.  The call enqueues kernels, stream-ordered copies and event
+ * waits only, and every stream it forks joins `stream` again before it
+ * returns, so a caller may capture it into a HIP graph from `stream` and
+ * replay that graph (the buffers bound at rat3d_net_bind stay fixed).  While
+ * `stream` is capturing, PARTITION1 enqueues its micro-batches one after
+ * another (the two-stream overlap is not captured); the mask-branch and
+ * weight-gradient streams are captured as forked work. */
 rat3d_status rat3d_train_step(rat3d_net* net, const void* x, const int32_t* labels,
                               const void* dy_upstream, float* loss_dev, void* stream);
 

@@ -840,7 +840,12 @@ bool hip_ok(hipError_t r, const char* what) {
 rat3d_status train_partition(rat3d_net* net, const char* x, const char* dy, size_t x_bytes,
                              size_t dy_bytes, hipStream_t st) {
     const int M = net->d.micro_batches;
-    if (!net->fwd_stream || !net->overlap || M < 2) {
+    // under stream capture the micro-batches are enqueued one after another:
+    // capturing the two-stream form ended in a crash inside the runtime's end
+    // of capture, with every fork joined back within this call
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (!hip_ok(hipStreamIsCapturing(st, &cap), "capture query")) return RAT3D_EHIP;
+    if (!net->fwd_stream || !net->overlap || M < 2 || cap != hipStreamCaptureStatusNone) {
         for (int k = 0; k < M; ++k)
             RAT3D_TRY(partition_micro_batch(net, x + k * x_bytes, dy + k * dy_bytes, k > 0 ? 1 : 0,
                                             st));
